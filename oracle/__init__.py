@@ -1,0 +1,46 @@
+"""CPU oracle for the ES parameter path (test infrastructure, not product code).
+
+This package is a plain, slow, obviously-correct NumPy implementation of what
+the GPU library computes: the counter-based noise (Philox4x32-10 words, the
+uniform map, the Box-Muller transform), in-place perturb/restore of bf16
+parameters, the population z-score of rewards, the reward-weighted update, and
+the cosine schedule of the perturbation radius.  Floating point work is done in
+fp64 and rounded to bf16 exactly once, round-to-nearest-even.
+
+Only the test suite, the smoke check and the CPU-baseline leg of the benchmark
+may import it.  It shares no code with the HIP library and imports nothing from
+it; the two meet only through the seeded input generators, which hold none of
+the method's arithmetic.
+
+Paper sections followed (arXiv 2608.17310, "Agentic ESOpt"):
+  * Section 3 (Methodology): Gaussian-smoothed objective, population z-score,
+    the implemented update theta += (alpha/G) sum_i zhat_i eps_i, seed-only
+    noise with in-place addition and subtraction.
+  * Section 3.1: cosine decay of sigma.
+  * Appendix C.1: canonical estimator with the explicit 1/(G sigma) factor.
+  * Appendix D.6 (hyperparameter summary): perturb, evaluate, revert,
+    regenerate the direction from its integer seed at update time.
+The paper names no generator and no transform; Philox4x32-10 is the published
+generator of Salmon, Moraes, Dror and Shaw (SC'11) and Box-Muller the textbook
+transform of Box and Muller (1958).
+
+Pin status of every function is listed in the module docstrings; all functions
+are pinned (none is "parity unpinned").
+"""
+
+from .philox import philox4x32_10, philox4x32_10_bigint, MASK32
+from .noise import (key_words, counter_words, uniform_from_word, box_muller,
+                    noise_words, normals)
+from .bf16 import bf16_to_f64, f64_to_bf16_rne, bf16_ulp
+from .es import (perturb, restore, zscore, update_coefficient, member_weights,
+                 update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
+                 ES_REWARDS_ARE_WEIGHTS)
+
+__all__ = [
+    "philox4x32_10", "philox4x32_10_bigint", "MASK32",
+    "key_words", "counter_words", "uniform_from_word", "box_muller",
+    "noise_words", "normals",
+    "bf16_to_f64", "f64_to_bf16_rne", "bf16_ulp",
+    "perturb", "restore", "zscore", "update_coefficient", "member_weights",
+    "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
+]

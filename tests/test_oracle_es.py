@@ -1,0 +1,236 @@
+"""Pins of the oracle's perturb / restore / z-score / update / schedule against
+closed forms, library routines, special cases and the paper's own printed
+update-magnitude distribution."""
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle
+from oracle import (bf16_to_f64, f64_to_bf16_rne, normals, perturb, restore,
+                    zscore, update, update_coefficient, member_weights,
+                    sigma_cosine, ES_UPDATE_DIV_SIGMA, ES_REWARDS_ARE_WEIGHTS)
+from paper_2608_17310_amd.workloads import random_bf16_bits
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+EPS32 = float(np.float32(1e-8))
+
+
+# ---------------------------------------------------------------- perturb --
+
+def test_exact_restore_of_unrounded_accumulation():
+    # Seed replay: theta + s sigma eps - s sigma eps, accumulated without an
+    # intermediate bf16 rounding, rounds back to theta exactly.
+    theta = random_bf16_bits(1 << 16, 1)
+    x = bf16_to_f64(theta)
+    for sigma, sign in [(1e-3, 1), (1.5e-3, -1), (1e-4, 1)]:
+        s32 = float(np.float32(sigma))
+        e = normals(11, 2, np.arange(x.size, dtype=np.uint64))
+        acc = (x + sign * s32 * e) - sign * s32 * e
+        np.testing.assert_array_equal(f64_to_bf16_rne(acc), theta)
+        # binary32 accumulation too: theta is bf16, so the error stays below
+        # half a bf16 ulp
+        acc32 = (x.astype(np.float32) + np.float32(sign * s32) * e.astype(np.float32)) \
+            - np.float32(sign * s32) * e.astype(np.float32)
+        np.testing.assert_array_equal(f64_to_bf16_rne(acc32.astype(np.float64)), theta)
+
+
+def test_zero_theta_round_trip_leaves_rounding_residue():
+    # In place, theta = 0 is perturbed to RNE(sigma eps) and restored to the
+    # rounding error of that step, |RNE(sigma eps) - sigma eps| <= 2^-8 |sigma eps|;
+    # only the unrounded accumulation restores exactly.
+    theta = np.zeros(4096, dtype=np.uint16)
+    s32 = float(np.float32(1e-3))
+    e = normals(5, 0, np.arange(4096, dtype=np.uint64))
+    back = bf16_to_f64(restore(perturb(theta, 5, 0, 1, 1e-3), 5, 0, 1, 1e-3))
+    assert np.all(np.abs(back) <= 2.0 ** -8 * s32 * np.abs(e))
+    assert np.mean(back != 0) > 0.9
+    np.testing.assert_array_equal(f64_to_bf16_rne((0.0 + s32 * e) - s32 * e), theta)
+
+
+def test_inplace_bf16_round_trip_drift_is_small():
+    theta = random_bf16_bits(1 << 16, 2)
+    p = perturb(theta, 9, 1, 1, 1e-3)
+    back = restore(p, 9, 1, 1, 1e-3)
+    drift = np.mean(back != theta)
+    assert 0.01 < drift < 0.10          # a few percent of elements move
+    # the drift is at most the two rounding errors: half an ulp of the
+    # perturbed value plus half an ulp of the restored one
+    d = np.abs(bf16_to_f64(back) - bf16_to_f64(theta))
+    bound = 0.5 * oracle.bf16_ulp(bf16_to_f64(p)) + 0.5 * oracle.bf16_ulp(bf16_to_f64(back))
+    assert np.all(d <= bound)
+
+
+def test_sigma_zero_identity_and_sign():
+    theta = random_bf16_bits(4096, 3)
+    theta[:3] = [0x8000, 0x0000, 0x0001]
+    np.testing.assert_array_equal(perturb(theta, 1, 0, 1, 0.0), theta)
+    up = bf16_to_f64(perturb(theta, 1, 0, 1, 1e-2)) - bf16_to_f64(theta)
+    dn = bf16_to_f64(perturb(theta, 1, 0, -1, 1e-2)) - bf16_to_f64(theta)
+    e = normals(1, 0, np.arange(4096, dtype=np.uint64))
+    assert np.corrcoef(up, e)[0, 1] > 0.95
+    assert np.corrcoef(dn, e)[0, 1] < -0.95
+    with pytest.raises(ValueError):
+        perturb(theta, 1, 0, 0, 1e-3)
+
+
+def test_perturbation_is_sigma_times_standard_normal():
+    # on theta = 0 the bf16 result is sigma*eps to 2^-8 relative
+    theta = np.zeros(1 << 18, dtype=np.uint16)
+    p = bf16_to_f64(perturb(theta, 77, 4, 1, 1e-3)) / float(np.float32(1e-3))
+    assert abs(p.std() - 1.0) < 0.01
+    assert stats.kstest(p, "norm").pvalue > 1e-4
+
+
+def test_sampled_elements_equal_dense():
+    theta = random_bf16_bits(10000, 4)
+    dense = perturb(theta, 3, 7, -1, 1e-3)
+    pick = np.array([9999, 0, 1, 2, 3, 5000, 4097], dtype=np.uint64)
+    np.testing.assert_array_equal(
+        perturb(theta[pick.astype(np.int64)], 3, 7, -1, 1e-3, elems=pick),
+        dense[pick.astype(np.int64)])
+
+
+# ---------------------------------------------------------------- z-score --
+
+def test_zscore_matches_scipy():
+    rng = np.random.default_rng(0)
+    for g in [2, 3, 8, 32, 257, 1024]:
+        r = rng.random(g).astype(np.float32)
+        z, st = zscore(r)
+        assert st == 0
+        r64 = r.astype(np.float64)
+        s = r64.std()
+        np.testing.assert_allclose(z * (s + EPS32) / s, stats.zscore(r64), rtol=1e-12, atol=1e-12)
+
+
+def test_zscore_closed_forms():
+    rng = np.random.default_rng(1)
+    r = (rng.standard_normal(64) * 3 + 10).astype(np.float32)
+    z, _ = zscore(r)
+    s = r.astype(np.float64).std()
+    assert abs(z.sum()) < 1e-12
+    assert abs(np.mean(z ** 2) - (s / (s + EPS32)) ** 2) < 1e-12
+    z, _ = zscore(np.array([0.0, 1.0], dtype=np.float32))
+    k = 0.5 / (0.5 + EPS32)
+    np.testing.assert_array_equal(z, [-k, k])
+    z, _ = zscore(np.array([2.0, 5.0], dtype=np.float32))
+    k = 1.5 / (1.5 + EPS32)
+    np.testing.assert_allclose(z, [-k, k], rtol=0, atol=1e-15)
+
+
+def test_zscore_degenerate_cases():
+    z, st = zscore(np.full(7, 0.1, dtype=np.float32))
+    assert st == 0 and np.all(z == 0)
+    z, st = zscore(np.array([3.0], dtype=np.float32))
+    assert st == 0 and np.all(z == 0)
+    for bad in [np.nan, np.inf, -np.inf]:
+        z, st = zscore(np.array([0.0, bad, 1.0], dtype=np.float32))
+        assert st == 1 and np.all(z == 0)
+
+
+# ----------------------------------------------------------------- update --
+
+def test_update_coefficient_modes():
+    assert update_coefficient(5e-4, 1e-3, 8) == float(np.float32(5e-4)) / 8
+    assert update_coefficient(5e-4, 1e-3, 8, ES_UPDATE_DIV_SIGMA) == \
+        float(np.float32(5e-4)) / 8 / float(np.float32(1e-3))
+
+
+def test_member_weights_merge_antithetic_pairs():
+    seeds, w = member_weights([4, 4, 9, 9, 2], [1, -1, 1, -1, 1],
+                              [0.5, 0.5, 1.0, -1.0, 0.25], 2.0)
+    assert seeds == [4, 9, 2]
+    np.testing.assert_array_equal(w, [0.0, 4.0, 0.5])
+
+
+def test_single_member_update_equals_perturb():
+    theta = random_bf16_bits(1 << 14, 5)
+    sigma = 1e-3
+    got, st = update(theta, 3, [21], [1], np.array([1.0], np.float32),
+                     alpha=sigma, sigma=0.5, flags=ES_REWARDS_ARE_WEIGHTS)
+    assert st == 0
+    np.testing.assert_array_equal(got, perturb(theta, 21, 3, 1, sigma))
+
+
+def test_update_identities():
+    theta = random_bf16_bits(4096, 6)
+    theta[:2] = [0x8000, 0x0000]
+    r = np.array([0.3, 0.9, 0.1, 0.5], dtype=np.float32)
+    # alpha = 0
+    got, st = update(theta, 0, [0, 1, 2, 3], [1, 1, 1, 1], r, alpha=0.0, sigma=1e-3)
+    np.testing.assert_array_equal(got, theta)
+    # all-equal rewards
+    got, st = update(theta, 0, [0, 1, 2, 3], [1] * 4, np.full(4, 0.7, np.float32), 5e-4, 1e-3)
+    np.testing.assert_array_equal(got, theta)
+    # antithetic pairs with equal rewards inside each pair
+    got, st = update(theta, 0, [0, 0, 1, 1], [1, -1, 1, -1],
+                     np.array([1.0, 1.0, 0.0, 0.0], np.float32), 5e-4, 1e-3)
+    np.testing.assert_array_equal(got, theta)
+    # non-finite reward: no-op with status
+    got, st = update(theta, 0, [0, 1], [1, 1], np.array([np.nan, 1.0], np.float32), 5e-4, 1e-3)
+    assert st == 1
+    np.testing.assert_array_equal(got, theta)
+
+
+def test_update_direction_and_antithetic_equivalence():
+    n = 1 << 15
+    theta = np.zeros(n, dtype=np.uint16)
+    el = np.arange(n, dtype=np.uint64)
+    got, _ = update(theta, 1, [10, 11], [1, 1], np.array([1.0, 0.0], np.float32),
+                    alpha=1e-2, sigma=1e-3)
+    d = bf16_to_f64(got)
+    assert np.corrcoef(d, normals(10, 1, el))[0, 1] > 0.6
+    assert np.corrcoef(d, normals(11, 1, el))[0, 1] < -0.6
+    # an antithetic pair rewarded (1, 0) moves theta along +eps with twice the
+    # per-member weight of a one-sided member
+    got_pair, _ = update(theta, 1, [10, 10], [1, -1], np.array([1.0, 0.0], np.float32),
+                         alpha=1e-2, sigma=1e-3)
+    w = float(np.float32(1e-2)) / 2 * 2 * (0.5 / (0.5 + EPS32))
+    np.testing.assert_array_equal(got_pair, f64_to_bf16_rne(w * normals(10, 1, el)))
+
+
+def test_update_magnitude_matches_paper_table():
+    """70 updates, G = 8, alpha = 2.5e-4, z-scored random rewards, starting
+    from theta = 0 in bf16: the fractions of |delta theta| under each
+    threshold match the paper's printed table (Appendix A.1) and the
+    closed form N(0, T alpha^2 / G)."""
+    lines = [l.split() for l in open(os.path.join(GOLDEN, "update_magnitude.txt"))
+             if l.strip() and not l.startswith("#")]
+    meta = {k: float(v) for k, v in lines[:4]}
+    rows = [(float(a), float(b)) for a, b in lines[4:]]
+    T, G, alpha = int(meta["updates"]), int(meta["population"]), meta["alpha"]
+    n = 1 << 15
+    theta = np.zeros(n, dtype=np.uint16)
+    rng = np.random.default_rng(2024)
+    for t in range(T):
+        r = rng.random(G).astype(np.float32)
+        theta, st = update(theta, 0, [1000 * t + i for i in range(G)], [1] * G, r,
+                           alpha, meta["sigma"])
+        assert st == 0
+    d = np.abs(bf16_to_f64(theta))
+    std = math.sqrt(T / G) * float(np.float32(alpha))
+    for thr, paper_frac in rows:
+        frac = np.mean(d <= thr)
+        closed = math.erf(thr / (std * math.sqrt(2)))
+        se = math.sqrt(closed * (1 - closed) / n)
+        assert abs(frac - closed) < 5 * se + 2e-3, (thr, frac, closed)
+        assert abs(frac - paper_frac) < 0.025, (thr, frac, paper_frac)
+
+
+# --------------------------------------------------------------- schedule --
+
+def test_sigma_cosine_closed_forms():
+    assert sigma_cosine(1e-3, 1e-4, 0, 100) == 1e-3
+    assert abs(sigma_cosine(1e-3, 1e-4, 100, 100) - 1e-4) < 1e-19
+    assert abs(sigma_cosine(1e-3, 1e-4, 50, 100) - 5.5e-4) < 1e-18
+    assert abs(sigma_cosine(1e-3, 1e-4, 25, 100) - (1e-4 + 9e-4 * (1 + math.sqrt(0.5)) / 2)) < 1e-18
+    assert abs(sigma_cosine(1e-3, 1e-4, 75, 100) - (1e-4 + 9e-4 * (1 - math.sqrt(0.5)) / 2)) < 1e-18
+    vals = [sigma_cosine(1e-3, 0.0, t, 50) for t in range(51)]
+    assert all(a > b for a, b in zip(vals, vals[1:]))
+    assert vals[-1] == 0.0
+    assert sigma_cosine(1.5e-3, 1.5e-3, 37, 70) == 1.5e-3    # constant schedule
+    with pytest.raises(ValueError):
+        sigma_cosine(1e-3, 1e-4, 101, 100)
