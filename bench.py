@@ -1,0 +1,263 @@
+"""Benchmark of the ES parameter path on one MI355X.
+
+One step is one ES generation's parameter-space work (arXiv 2608.17310,
+Section 3; Appendix D.6): for each of the N members, es_perturb (theta +=
+s sigma_t eps_i) and es_restore (theta -= s sigma_t eps_i) over the whole
+parameter set, then one fused es_update (z-score of the N rewards, merged
+member weights, theta += sum_d w_d eps_d) over the whole set.  Model
+evaluation between perturb and restore is outside this path and not run.
+
+Inputs are synthetic and resident in HBM before timing: a transformer-shaped
+bf16 parameter set with N(0, 0.02) values and a precomputed reward vector per
+step.  Throughput `value` counts parameter passes: each step makes 2N
+perturb/restore passes and one N-member update pass over P parameters, so
+value = (2N + 1) P / step time.  Per-kernel figures come from HIP events
+recorded on the launch stream around every launch inside the timed region.
+
+    python bench.py [--steps K] [--warmup W] [--workload dense-27b]
+"""
+import argparse
+import json
+import math
+import multiprocessing as mp
+import os
+import sys
+import time
+
+import numpy as np
+
+REPO = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, REPO)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, public spec
+VALU_PEAK_TINST = 256 * 64 * 2.4e9 / 1e12   # 39.3 T lane-instructions/s (256 CU x 64 lanes x 2.4 GHz)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="dense-27b")
+    ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target CPU time of the oracle baseline sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="run one perturb, one update and a calibration copy, for rocprofv3")
+    ap.add_argument("--traffic-json", default=os.path.join(REPO, "profiles", "traffic.json"),
+                    help="per-launch HBM bytes measured with rocprofv3 counters")
+    return ap.parse_args()
+
+
+def step_seeds(W, t, n_members):
+    """Seeds of generation t: a fresh seed per distinct member seed."""
+    base = W.seeds if n_members is None else tuple(range(n_members))
+    return [int(s) + 1_000_003 * (t + 1) for s in base]
+
+
+def sigma_at(W, t):
+    if W.sigma0 == W.sigma_T:
+        return W.sigma0
+    return W.sigma_T + (W.sigma0 - W.sigma_T) * (1 + math.cos(math.pi * (t % W.T) / W.T)) / 2
+
+
+# ---------------------------------------------------------------- CPU leg --
+
+def _oracle_chunk(args):
+    """The oracle's work of one step on a sample of one tensor's elements."""
+    import oracle
+    theta, tid, elems, seeds, signs, rewards, alpha, sigma = args
+    t0 = time.perf_counter()
+    for s, sg in zip(seeds, signs):
+        p = oracle.perturb(theta, s, tid, sg, sigma, elems=elems)
+        theta = oracle.restore(p, s, tid, sg, sigma, elems=elems)
+    theta, _ = oracle.update(theta, tid, seeds, signs, rewards, alpha, sigma, elems=elems)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(W, seeds, signs, rewards, sigma, theta_samples, workers, budget_s):
+    """Time the oracle (as it stands) on a bounded element sample; returns the
+    rate in parameter passes per second and a description of the sample."""
+    n = len(seeds)
+    # calibrate: one small chunk on one core
+    t_small = _oracle_chunk((theta_samples[0][1][:4096], theta_samples[0][0],
+                             theta_samples[0][2][:4096], seeds, signs, rewards, W.alpha, sigma))
+    per_elem = t_small / 4096
+    total = sum(len(x[1]) for x in theta_samples)
+    target = int(budget_s * workers / per_elem)
+    frac = min(1.0, target / total)
+    jobs = []
+    for tid, theta, elems in theta_samples:
+        k = max(1, int(len(elems) * frac))
+        jobs.append((theta[:k], tid, elems[:k], seeds, signs, rewards, W.alpha, sigma))
+    n_elems = sum(len(j[2]) for j in jobs)
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(workers) as pool:
+        pool.map(_oracle_chunk, jobs, chunksize=1)
+    wall = time.perf_counter() - t0
+    rate = (2 * n + 1) * n_elems / wall
+    return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            "sample": f"{n_elems} elements sampled across {len(jobs)} tensors of {W.name}, "
+                      f"one full step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 "
+                      f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
+
+
+def host_samples(W, per_tensor=1 << 14):
+    """A bounded element sample of every tensor of W: random element indices
+    and N(0, 0.02) bf16 values drawn on the host (the oracle's cost does not
+    depend on the values)."""
+    from paper_2608_17310_amd import workloads as wl
+    rng = np.random.default_rng(0)
+    out = []
+    for tid, n in enumerate(W.numels):
+        idx = np.unique(rng.integers(0, n, size=min(n, per_tensor))).astype(np.uint64)
+        out.append((tid, wl.random_bf16_bits(idx.size, 1000 + tid), idx))
+    return out
+
+
+# ---------------------------------------------------------------- GPU leg --
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs the ES parameter path on one GPU; "
+                                   "--gpus above 1 is not supported (see the sharding design)"}))
+        sys.exit(2)
+    import torch
+    from paper_2608_17310_amd import esopt, workloads as wl
+
+    W = wl.WORKLOADS[args.workload]
+    n_members = args.members
+    signs = list(W.signs) if n_members is None else [1] * n_members
+    N = len(signs)
+    cpu = None
+    if not args.no_cpu_baseline and not args.profile_pass:
+        # before the GPU is touched: worker processes fork from a clean parent
+        cpu = cpu_baseline(W, step_seeds(W, args.warmup, n_members), signs,
+                           wl.rewards(W, args.warmup, n=N), sigma_at(W, args.warmup),
+                           host_samples(W), min(16, os.cpu_count() or 1), args.cpu_seconds)
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU"}))
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    flat, views = wl.device_params(W)
+    plan = esopt.Plan(views)
+    P = plan.numel
+    stream = torch.cuda.current_stream()
+    total_steps = args.warmup + args.steps
+    rewards_all = torch.from_numpy(np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])).cuda()
+    torch.cuda.synchronize()
+
+    if args.profile_pass:
+        seeds = step_seeds(W, 0, n_members)
+        plan.perturb(seeds[0], signs[0], W.sigma0)
+        plan.restore(seeds[0], signs[0], W.sigma0)
+        plan.update(seeds, signs, rewards_all[0], W.alpha, sigma=W.sigma0)
+        calib = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")     # 1 GiB copy
+        calib2 = torch.empty_like(calib)
+        calib2.copy_(calib)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": W.name, "params": P, "members": N,
+                          "calibration_copy_bytes": 1 << 30}))
+        return
+
+    ev = []   # (kind, start, end) event pairs inside the timed region
+
+    def run_step(t, record):
+        seeds = step_seeds(W, t, n_members)
+        sigma = sigma_at(W, t)
+        for s, sg in zip(seeds, signs):
+            for kind, fn in (("es_perturb", plan.perturb), ("es_restore", plan.restore)):
+                if record:
+                    a = torch.cuda.Event(enable_timing=True)
+                    b = torch.cuda.Event(enable_timing=True)
+                    a.record(stream)
+                    fn(s, sg, sigma)
+                    b.record(stream)
+                    ev.append((kind, a, b))
+                else:
+                    fn(s, sg, sigma)
+        if record:
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+        plan.update(seeds, signs, rewards_all[t], W.alpha, sigma=sigma)
+        if record:
+            b.record(stream)
+            ev.append(("es_update", a, b))
+
+    for t in range(args.warmup):
+        run_step(t, record=False)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for t in range(args.warmup, total_steps):
+        run_step(t, record=True)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    per = {}
+    for kind, a, b in ev:
+        per.setdefault(kind, []).append(a.elapsed_time(b))
+    t_pert = float(np.mean(per["es_perturb"] + per["es_restore"])) / 1e3
+    t_upd = float(np.mean(per["es_update"])) / 1e3
+    value = (2 * N + 1) * P / (ms_step / 1e3)
+    n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
+
+    traffic = None
+    if os.path.exists(args.traffic_json):
+        tj = json.load(open(args.traffic_json))
+        rec = tj.get(W.name, {}).get("es_perturb")
+        if rec and rec.get("source_hash") == _kernel_source_hash():
+            traffic = rec["bytes_per_launch"]
+    perturb_gbs = 4 * P / t_pert / 1e9
+    roofline = {"bound": "hbm", "achieved": round(perturb_gbs, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(perturb_gbs / HBM_PEAK_GBS, 4),
+                "traffic": traffic, "kernel": "es_tiles_kernel<perturb> (es_perturb/es_restore)",
+                "algorithmic_bytes_per_launch": 4 * P}
+    update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
+              "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
+              "normals_per_s": n_distinct * P / t_upd, "distinct_seeds": n_distinct}
+    out = {
+        "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
+        "value": value,
+        "unit": "params/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "param_dtype": "bf16", "data": "synthetic",
+        "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
+                   "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
+                   "counting": "value = (2N+1) P / step time: 2N perturb/restore passes "
+                               "and one fused N-member update pass per step"},
+        "roofline": roofline,
+        "per_kernel": {
+            "es_perturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
+                           "GBps_algorithmic": round(perturb_gbs, 1),
+                           "frac_hbm_peak": round(perturb_gbs / HBM_PEAK_GBS, 4)},
+            "es_update": update,
+        },
+        "wall_s_timed": round(wall, 3),
+    }
+    if cpu is not None:
+        out["cpu_baseline"] = cpu
+    plan.close()
+    print(json.dumps(out))
+
+
+def _kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("es_noise.hpp", "esopt.hip"):
+        h.update(open(os.path.join(REPO, "paper_2608_17310_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,182 @@
+/*
+ * esopt.h -- C ABI of the MI355X (gfx950) ES parameter-path library.
+ *
+ * What it computes (arXiv 2608.17310, "Agentic ESOpt"):
+ *   Section 3 samples G full-parameter Gaussian directions eps_i around the
+ *   current parameters theta, evaluates each perturbed model theta + sigma
+ *   eps_i, z-scores the rewards within the population and applies
+ *   theta <- theta + (alpha / G) sum_i zhat_i eps_i.  Only the integer seed
+ *   of each direction is stored; the perturbation is applied and reverted in
+ *   place, and the direction is regenerated from its seed for the update
+ *   (Section 3; Appendix D.6).  Section 3.1 decays sigma on a cosine
+ *   schedule.  Appendix C.1 gives the canonical estimator with 1/(G sigma).
+ *
+ * Noise definition (the paper names no generator; this is the library's):
+ *   eps_j of element j of the tensor with noise identity `tensor_id`, for a
+ *   64-bit seed, comes from Philox4x32-10 (Salmon et al., SC'11) with
+ *     key     = (seed & 0xffffffff, seed >> 32)
+ *     counter = (q & 0xffffffff, q >> 32, tensor_id, 0),  q = j >> 2
+ *   Word pair (w0,w1) serves elements 4q, 4q+1 and (w2,w3) serves 4q+2,
+ *   4q+3.  u(w) = ((w >> 9) + 0.5) * 2^-23; Box-Muller (1958):
+ *   r = sqrt(-2 ln u(wa)), phi = 2 pi u(wb); first element r cos(phi),
+ *   second r sin(phi).  The GPU evaluates this in binary32.
+ *
+ * Parameters are bf16 (the paper states no dtype; its memory figures imply
+ * 16-bit weights).  Each result is computed in binary32 and rounded to bf16
+ * round-to-nearest-even, with exactly one read and one write per element.
+ *
+ * Conventions for every call:
+ *   - Device pointers are HIP device memory of the device current at the
+ *     call; the caller owns every buffer it passes.  A plan keeps the
+ *     tensors' addresses, so they must stay allocated and unmoved while the
+ *     plan exists; calls on one plan must be ordered (one stream, or
+ *     externally synchronised) because they share the plan's small scratch.
+ *   - `stream` is a hipStream_t (NULL: the default stream).  Every call is
+ *     stream-ordered and returns without synchronising the host; launch
+ *     errors are reported by the return code.
+ *   - Return value: ES_OK (0) or a negative ES_ERR_* code; es_strerror()
+ *     names a code, es_last_error() gives the detail of the last failure on
+ *     the calling thread.  A call that fails validation launches nothing and
+ *     leaves every buffer untouched.
+ */
+#ifndef ESOPT_H
+#define ESOPT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ES_OK                0
+#define ES_ERR_INVALID_ARG  -1   /* null pointer, bad size, sign, sigma, flags */
+#define ES_ERR_ALIGN        -2   /* data not 2-byte aligned */
+#define ES_ERR_HIP          -3   /* a HIP runtime call or launch failed */
+#define ES_ERR_DEVICE       -4   /* current device differs from the plan's */
+#define ES_ERR_NOMEM        -5   /* device or host allocation failed */
+
+#define ES_MAX_MEMBERS      1024u   /* population size limit of es_update */
+#define ES_MAX_TENSORS      (1u << 20)
+
+/* es_update flags */
+#define ES_UPDATE_DIV_SIGMA     1u  /* c = alpha / (G sigma) (Appendix C.1)
+                                       instead of the paper's alpha / G */
+#define ES_REWARDS_ARE_WEIGHTS  2u  /* use rewards as zhat directly (no z-score) */
+
+typedef void* es_stream_t;          /* hipStream_t */
+
+/* One parameter tensor: `numel` contiguous bf16 values at device address
+ * `data` (2-byte aligned; 16-byte alignment takes the vector path).
+ * `tensor_id` is the tensor's noise identity (counter word 2) and must be
+ * unique within a plan and stable across calls; the list index is the usual
+ * choice.  `reserved` must be 0.  numel may be 0 (the tensor is skipped). */
+typedef struct es_tensor {
+    void*    data;
+    uint64_t numel;
+    uint32_t tensor_id;
+    uint32_t reserved;
+} es_tensor_t;
+
+/* Opaque plan: the tensor list laid out as tiles for one launch per pass,
+ * plus O(ES_MAX_MEMBERS) device scratch for the update's member table. */
+typedef struct es_plan es_plan_t;
+
+/* Build a plan over `n_tensors` tensors (1 .. ES_MAX_TENSORS) on the current
+ * device.  Copies the list; does not touch the tensors' values.  Errors:
+ * INVALID_ARG for a null pointer, n_tensors out of range, duplicate
+ * tensor_id, nonzero reserved field, null data with numel > 0, or tensors
+ * whose byte ranges overlap; ALIGN for odd addresses; NOMEM / HIP for
+ * allocation failures.  On success *out owns a device table of
+ * 32 * (n_tensors + 1) bytes and ~42 KB of scratch, freed by es_plan_destroy. */
+int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out);
+
+/* Free a plan (NULL is a no-op).  Synchronises the device first so that no
+ * queued launch still reads the plan's tables. */
+int es_plan_destroy(es_plan_t* plan);
+
+/* Total number of bf16 elements and number of tiles of a plan. */
+uint64_t es_plan_numel(const es_plan_t* plan);
+uint64_t es_plan_tiles(const es_plan_t* plan);
+
+/* Perturb in place (Section 3; Appendix D.6):
+ *   theta_j <- RNE_bf16(theta_j + sign * sigma * eps_j(seed))
+ * for every element of every tensor of the plan, one kernel launch.
+ * sign is +1 or -1 (antithetic member); sigma is finite and >= 0; sigma == 0
+ * leaves theta bit-for-bit unchanged and launches nothing. */
+int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+
+/* Revert a perturbation (Section 3; Appendix D.6): es_perturb with -sign,
+ *   theta_j <- RNE_bf16(theta_j - sign * sigma * eps_j(seed)).
+ * Because each step rounds to bf16, the round trip returns theta except for
+ * rounding residues (about 5% of N(0,0.02) elements move by one ulp at
+ * sigma = 1e-3). */
+int es_restore(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+
+/* Population z-score (Section 3): mu = mean(R), s = sqrt(mean((R - mu)^2)),
+ *   z_i = (R_i - mu) / (s + eps),
+ * computed in fp64 by one wavefront and written as binary32 to z_dev[n].
+ * All rewards equal (including n == 1) gives z = 0 exactly.  If any reward is
+ * not finite, z = 0 and *status_dev = 1, else *status_dev = 0 (status_dev may
+ * be NULL).  rewards_dev and z_dev: device arrays of n floats, 1 <= n <=
+ * ES_MAX_MEMBERS; they may alias.  eps must be finite and >= 0. */
+int es_zscore(const float* rewards_dev, uint32_t n, float eps, float* z_dev,
+              int32_t* status_dev, es_stream_t stream);
+
+typedef struct es_update_opts {
+    float    alpha;       /* step size, finite */
+    float    sigma;       /* sigma_t of this generation; read only with
+                             ES_UPDATE_DIV_SIGMA (then finite and > 0) */
+    float    zscore_eps;  /* epsilon of the z-score denominator, >= 0 (1e-8) */
+    uint32_t flags;       /* ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS */
+} es_update_opts_t;
+
+/* Fused reward-weighted update (Section 3; Appendix C.1 with
+ * ES_UPDATE_DIV_SIGMA):
+ *   zhat = zscore(rewards) (or rewards as given with ES_REWARDS_ARE_WEIGHTS)
+ *   c    = alpha / G  (or alpha / (G sigma)),  G = n_members
+ *   w_d  = sum over members i with seed d of c * sign_i * zhat_i   (fp64)
+ *   theta_j <- RNE_bf16(theta_j + sum_d w_d eps_j(seed_d))
+ * Members sharing a seed (antithetic pairs) are merged into one weight, so
+ * the noise of each distinct seed is generated once per element; the sum is
+ * accumulated in binary32 registers and theta is read and written once.
+ * Seeds with a zero merged weight are skipped, and when no weight is nonzero
+ * theta is not written at all.  A non-finite reward leaves theta unchanged
+ * and sets the status word to 1.
+ *   seeds, signs : host arrays of n_members entries (signs +1 or -1)
+ *   rewards_dev  : device array of n_members binary32 rewards
+ *   n_members    : 1 .. ES_MAX_MEMBERS
+ *   z_out_dev    : optional device array of n_members floats receiving zhat
+ *   status_out_dev: optional device int32 receiving the status word
+ * The host arrays are read before the call returns. */
+int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
+              const float* rewards_dev, uint32_t n_members,
+              const es_update_opts_t* opts, float* z_out_dev,
+              int32_t* status_out_dev, es_stream_t stream);
+
+/* Cosine schedule of the perturbation radius (Section 3.1):
+ *   sigma_t = sigma_T + (sigma_0 - sigma_T) (1 + cos(pi t / T)) / 2,
+ * 0 <= t <= T, T >= 1; returns NaN for arguments out of range.  Update t
+ * (0-based) uses sigma_t. Host-only helper. */
+double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T);
+
+/* Test hooks exposing the device noise functions the kernels use.
+ * es_philox_words: out_dev[4 i + k] = word k of the Philox call at counter
+ *   (q & 0xffffffff, q >> 32, tensor_id, domain), q = quad0 + i,
+ *   key from seed, for i < n_quads (n_quads <= 2^28).
+ * es_normals: out_dev[i] = eps_j(seed) of element j = elem0 + i of tensor
+ *   `tensor_id`, binary32, for i < n (n <= 2^30). */
+int es_philox_words(uint64_t seed, uint32_t tensor_id, uint32_t domain,
+                    uint64_t quad0, uint64_t n_quads, uint32_t* out_dev,
+                    es_stream_t stream);
+int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n,
+               float* out_dev, es_stream_t stream);
+
+/* Static name of an error code; detail of the calling thread's last error. */
+const char* es_strerror(int code);
+const char* es_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ESOPT_H */

@@ -1,0 +1,696 @@
+// ES parameter path for MI355X (gfx950): perturb / restore / fused N-member
+// update / reward z-score over a list of bf16 tensors, behind the C ABI of
+// include/esopt.h.
+//
+// Method (arXiv 2608.17310): Section 3 (perturb theta + sigma eps_i, revert
+// by subtraction, z-score rewards, theta += (alpha/G) sum zhat_i eps_i, noise
+// regenerated from seeds), Section 3.1 (cosine sigma schedule), Appendix C.1
+// (1/(G sigma) estimator), Appendix D.6 (order of apply / evaluate / revert /
+// regenerate).
+//
+// Layout and launch shape:
+//   * A plan cuts every tensor into tiles of kTileElems = 4096 elements
+//     (256 lanes x 2 groups x 8 bf16) and numbers the tiles of all tensors
+//     consecutively.  One launch covers the whole parameter list: a grid of
+//     (CUs x WGs-per-CU) workgroups strides over the tiles.  Each workgroup
+//     keeps the index of its current tensor in a scalar register and
+//     advances it through a small tensor table read with scalar loads, so a
+//     tile's tensor, address and noise identity are wave-uniform.
+//   * Within a tile, lane l of group slot u owns elements
+//     8 (u * 256 + l) .. +7: one 16-byte load and one 16-byte store, 64
+//     lanes covering 1 KB contiguous per instruction.  Its two Philox calls
+//     are the quads 2 g and 2 g + 1 of that group; since tiles start at
+//     multiples of 4096 elements, the counter's high word is uniform per
+//     tile.
+//   * Perturb/restore read and write each parameter once (4 bytes of HBM
+//     traffic per parameter).  The update regenerates the noise of all
+//     distinct member seeds for the same 8 elements in registers,
+//     accumulates sum_d w_d eps_d in binary32, and then does the single
+//     read-modify-write, so its HBM traffic does not depend on N.
+//   * Tiles that are partial (tensor tails) or belong to a tensor whose
+//     address is not 16-byte aligned take a bounds-checked 2-byte path with
+//     identical arithmetic.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <unordered_map>
+#include <vector>
+#include <algorithm>
+
+#include "../../include/esopt.h"
+#include "es_noise.hpp"
+
+namespace {
+
+constexpr int kBlock = 256;                 // lanes per workgroup (4 waves)
+constexpr int kGroupsPerLane = 2;           // 8-element groups per lane per tile
+constexpr int kGroupElems = 8;
+constexpr uint64_t kTileElems = uint64_t(kBlock) * kGroupsPerLane * kGroupElems;  // 4096
+constexpr uint32_t kFlagAligned = 1u;       // tensor base is 16-byte aligned
+constexpr int kDefaultWgPerCu = 8;
+
+struct DevTensor {                          // 32 bytes, device tensor table entry
+    uint16_t* data;
+    uint64_t numel;
+    uint64_t first_tile;                    // global index of the tensor's tile 0
+    uint32_t tensor_id;
+    uint32_t flags;
+};
+static_assert(sizeof(DevTensor) == 32, "tensor table entry layout");
+
+struct MemberIn {                           // one population member, CSR order
+    uint32_t reward_index;
+    int32_t sign;
+};
+struct DistinctIn {                         // one distinct seed and its members
+    uint32_t k0, k1;
+    uint32_t first;
+    uint32_t count;
+};
+struct Member {                             // merged weight of one distinct seed
+    uint32_t k0, k1;
+    float w;
+    uint32_t pad;
+};
+struct UpdateHeader {
+    uint32_t n_distinct;
+    uint32_t n_live;                        // distinct seeds with w != 0
+    int32_t status;                         // 1: non-finite reward, update skipped
+    uint32_t pad;
+};
+
+// Plan scratch layout (bytes).
+constexpr size_t kOffMembersIn = 0;
+constexpr size_t kOffDistinctIn = kOffMembersIn + sizeof(MemberIn) * ES_MAX_MEMBERS;
+constexpr size_t kOffMembers = kOffDistinctIn + sizeof(DistinctIn) * ES_MAX_MEMBERS;
+constexpr size_t kOffHeader = kOffMembers + sizeof(Member) * ES_MAX_MEMBERS;
+constexpr size_t kScratchBytes = kOffHeader + 256;
+
+constexpr int kStageWords = 256;            // 1 KB of kernel arguments per launch
+struct StageChunk {
+    uint32_t words[kStageWords];
+};
+
+thread_local std::string g_last_error;
+
+int fail(int code, const std::string& msg) {
+    g_last_error = msg;
+    return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+    return fail(ES_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------------------
+// Device code
+// ------------------------------------------------------------------------
+
+// Load the 8 bf16 of one group (packed in 4 words).  Fast path: one 16-byte
+// load.  Checked path: element-wise 2-byte loads with bounds.
+template <bool kFast>
+__device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint64_t e,
+                                           uint64_t numel, uint32_t raw[4]) {
+    if constexpr (kFast) {
+        const uint4 v = *reinterpret_cast<const uint4*>(p + e);
+        raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const uint32_t lo = (e + 2 * k < numel) ? p[e + 2 * k] : 0u;
+            const uint32_t hi = (e + 2 * k + 1 < numel) ? p[e + 2 * k + 1] : 0u;
+            raw[k] = lo | (hi << 16);
+        }
+    }
+}
+
+template <bool kFast>
+__device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e, uint64_t numel,
+                                            const uint32_t out[4]) {
+    if constexpr (kFast) {
+        *reinterpret_cast<uint4*>(p + e) = make_uint4(out[0], out[1], out[2], out[3]);
+    } else {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            if (e + 2 * k < numel) p[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
+            if (e + 2 * k + 1 < numel) p[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
+        }
+    }
+}
+
+// Normals of the 8 elements of a group starting at element 8 g (quads 2 g,
+// 2 g + 1; q_lo is even so q_lo + 1 does not carry into q_hi).
+__device__ __forceinline__ void group_normals(uint32_t q_lo, uint32_t q_hi, uint32_t tensor_id,
+                                              uint32_t k0, uint32_t k1, float e[8]) {
+    es::quad_normals(q_lo, q_hi, tensor_id, k0, k1, e);
+    es::quad_normals(q_lo + 1u, q_hi, tensor_id, k0, k1, e + 4);
+}
+
+// One tile of perturb: theta <- RNE(fma(coef, eps, theta)), coef = sign * sigma.
+template <bool kFast>
+__device__ __forceinline__ void perturb_tile(uint16_t* __restrict__ data, uint64_t numel,
+                                             uint64_t elem0, uint32_t tensor_id,
+                                             uint32_t k0, uint32_t k1, float coef) {
+    const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
+    uint32_t raw[kGroupsPerLane][4];
+#pragma unroll
+    for (int u = 0; u < kGroupsPerLane; ++u) {
+        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
+        load_group<kFast>(data, e, numel, raw[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kGroupsPerLane; ++u) {
+        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
+        float eps[8];
+        group_normals(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, k0, k1, eps);
+        uint32_t out[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float lo = __builtin_fmaf(coef, eps[2 * k], es::bf16_lo(raw[u][k]));
+            const float hi = __builtin_fmaf(coef, eps[2 * k + 1], es::bf16_hi(raw[u][k]));
+            out[k] = es::pack_bf16x2(lo, hi);
+        }
+        store_group<kFast>(data, e, numel, out);
+    }
+}
+
+// One tile of the fused update: acc = sum_d w_d eps_d (binary32, members in
+// table order, zero weights skipped), theta <- RNE(theta + acc).
+template <bool kFast>
+__device__ __forceinline__ void update_tile(uint16_t* __restrict__ data, uint64_t numel,
+                                            uint64_t elem0, uint32_t tensor_id,
+                                            const Member* __restrict__ members,
+                                            uint32_t n_distinct) {
+    const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
+    uint32_t raw[kGroupsPerLane][4];
+    float acc[kGroupsPerLane][8];
+#pragma unroll
+    for (int u = 0; u < kGroupsPerLane; ++u) {
+        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
+        load_group<kFast>(data, e, numel, raw[u]);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) acc[u][k] = 0.0f;
+    }
+    const uint32_t q_lo0 = static_cast<uint32_t>((elem0 >> 2) + uint64_t(threadIdx.x) * 2u);
+    for (uint32_t d = 0; d < n_distinct; ++d) {
+        const Member m = members[d];
+        if (m.w == 0.0f) continue;
+#pragma unroll
+        for (int u = 0; u < kGroupsPerLane; ++u) {
+            float eps[8];
+            group_normals(q_lo0 + uint32_t(u * kBlock * 2), q_hi, tensor_id, m.k0, m.k1, eps);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) acc[u][k] = __builtin_fmaf(m.w, eps[k], acc[u][k]);
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kGroupsPerLane; ++u) {
+        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
+        uint32_t out[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const float lo = es::bf16_lo(raw[u][k]) + acc[u][2 * k];
+            const float hi = es::bf16_hi(raw[u][k]) + acc[u][2 * k + 1];
+            out[k] = es::pack_bf16x2(lo, hi);
+        }
+        store_group<kFast>(data, e, numel, out);
+    }
+}
+
+// Whole-parameter-list launch.  kUpdate selects the fused update (member
+// table + header written by es_prepare_kernel) over perturb (one key, coef).
+template <bool kUpdate>
+__global__ __launch_bounds__(kBlock) void es_tiles_kernel(const DevTensor* __restrict__ tab,
+                                                          uint64_t n_tiles, uint32_t k0,
+                                                          uint32_t k1, float coef,
+                                                          const Member* __restrict__ members,
+                                                          const UpdateHeader* __restrict__ hdr) {
+    uint32_t n_distinct = 0;
+    if constexpr (kUpdate) {
+        if (hdr->n_live == 0u) return;      // nothing to add: theta is not written
+        n_distinct = hdr->n_distinct;
+    }
+    uint32_t t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+        while (tile >= tab[t + 1].first_tile) ++t;      // sentinel ends the table
+        uint16_t* const data = tab[t].data;
+        const uint64_t numel = tab[t].numel;
+        const uint32_t tensor_id = tab[t].tensor_id;
+        const uint64_t elem0 = (tile - tab[t].first_tile) * kTileElems;
+        const bool fast = (tab[t].flags & kFlagAligned) && (elem0 + kTileElems <= numel);
+        if constexpr (kUpdate) {
+            if (fast) update_tile<true>(data, numel, elem0, tensor_id, members, n_distinct);
+            else      update_tile<false>(data, numel, elem0, tensor_id, members, n_distinct);
+        } else {
+            if (fast) perturb_tile<true>(data, numel, elem0, tensor_id, k0, k1, coef);
+            else      perturb_tile<false>(data, numel, elem0, tensor_id, k0, k1, coef);
+        }
+    }
+}
+
+// Copy up to 1 KB of host-packed words (passed as kernel arguments) into
+// device scratch: how es_update hands its member tables to the device
+// without a host-side staging buffer or synchronisation.
+__global__ __launch_bounds__(kBlock) void es_stage_kernel(uint32_t* __restrict__ dst,
+                                                          uint32_t n_words, StageChunk chunk) {
+    for (uint32_t i = threadIdx.x; i < n_words; i += blockDim.x) dst[i] = chunk.words[i];
+}
+
+// Wave-wide reductions (one wavefront of 64 lanes).
+__device__ __forceinline__ double wave_sum(double x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+__device__ __forceinline__ float wave_min(float x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x = fminf(x, __shfl_xor(x, off, 64));
+    return x;
+}
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x = fmaxf(x, __shfl_xor(x, off, 64));
+    return x;
+}
+
+// Population z-score of n rewards by one wavefront, fp64, into LDS z[].
+// Returns the status (1 if any reward is not finite; then z = 0).  All
+// rewards equal gives z = 0 exactly.
+__device__ int wave_zscore(const float* __restrict__ r, uint32_t n, double eps, double* z) {
+    const uint32_t lane = threadIdx.x;
+    double s = 0.0;
+    float lo = INFINITY, hi = -INFINITY;
+    int bad = 0;
+    for (uint32_t i = lane; i < n; i += 64) {
+        const float x = r[i];
+        bad |= !isfinite(x);
+        s += static_cast<double>(x);
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
+    }
+    bad = __any(bad);
+    if (bad) {
+        for (uint32_t i = lane; i < n; i += 64) z[i] = 0.0;
+        return 1;
+    }
+    lo = wave_min(lo);
+    hi = wave_max(hi);
+    if (lo == hi) {
+        for (uint32_t i = lane; i < n; i += 64) z[i] = 0.0;
+        return 0;
+    }
+    const double mu = wave_sum(s) / static_cast<double>(n);
+    double q = 0.0;
+    for (uint32_t i = lane; i < n; i += 64) {
+        const double d = static_cast<double>(r[i]) - mu;
+        q += d * d;
+    }
+    const double sd = sqrt(wave_sum(q) / static_cast<double>(n));
+    for (uint32_t i = lane; i < n; i += 64) z[i] = (static_cast<double>(r[i]) - mu) / (sd + eps);
+    return 0;
+}
+
+__global__ __launch_bounds__(64) void es_zscore_kernel(const float* __restrict__ r, uint32_t n,
+                                                       double eps, float* __restrict__ z_out,
+                                                       int32_t* __restrict__ status_out) {
+    __shared__ double z[ES_MAX_MEMBERS];
+    const int status = wave_zscore(r, n, eps, z);
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < n; i += 64) z_out[i] = static_cast<float>(z[i]);
+    if (status_out != nullptr && threadIdx.x == 0) *status_out = status;
+}
+
+// z-score (or rewards as weights), then one merged weight per distinct seed:
+// w_d = sum over its members (in member order) of c * sign * zhat, fp64,
+// stored as binary32 with the seed's key for es_tiles_kernel<true>.
+__global__ __launch_bounds__(64) void es_prepare_kernel(
+    const float* __restrict__ r, uint32_t n, double eps, uint32_t flags, double c,
+    const MemberIn* __restrict__ min, const DistinctIn* __restrict__ din, uint32_t n_distinct,
+    Member* __restrict__ out, UpdateHeader* __restrict__ hdr, float* __restrict__ z_out,
+    int32_t* __restrict__ status_out) {
+    __shared__ double z[ES_MAX_MEMBERS];
+    const uint32_t lane = threadIdx.x;
+    int status;
+    if (flags & ES_REWARDS_ARE_WEIGHTS) {
+        int bad = 0;
+        for (uint32_t i = lane; i < n; i += 64) {
+            const float x = r[i];
+            bad |= !isfinite(x);
+            z[i] = static_cast<double>(x);
+        }
+        status = __any(bad) ? 1 : 0;
+    } else {
+        status = wave_zscore(r, n, eps, z);
+    }
+    __syncthreads();
+    if (z_out != nullptr)
+        for (uint32_t i = lane; i < n; i += 64) z_out[i] = static_cast<float>(status ? 0.0 : z[i]);
+    uint32_t live = 0;
+    for (uint32_t d = lane; d < n_distinct; d += 64) {
+        const DistinctIn di = din[d];
+        double w = 0.0;
+        for (uint32_t m = di.first; m < di.first + di.count; ++m)
+            w += c * static_cast<double>(min[m].sign) * z[min[m].reward_index];
+        const float wf = status ? 0.0f : static_cast<float>(w);
+        out[d] = Member{di.k0, di.k1, wf, 0u};
+        live += (wf != 0.0f) ? 1u : 0u;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) live += __shfl_xor(live, off, 64);
+    if (lane == 0) {
+        *hdr = UpdateHeader{n_distinct, live, status, 0u};
+        if (status_out != nullptr) *status_out = status;
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void es_philox_words_kernel(uint32_t k0, uint32_t k1,
+                                                                 uint32_t tensor_id, uint32_t domain,
+                                                                 uint64_t quad0, uint64_t n_quads,
+                                                                 uint4* __restrict__ out) {
+    const uint64_t i = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= n_quads) return;
+    const uint64_t q = quad0 + i;
+    const es::Words w = es::philox4x32_10(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32),
+                                          tensor_id, domain, k0, k1);
+    out[i] = make_uint4(w.w0, w.w1, w.w2, w.w3);
+}
+
+__global__ __launch_bounds__(kBlock) void es_normals_kernel(uint32_t k0, uint32_t k1,
+                                                            uint32_t tensor_id, uint64_t elem0,
+                                                            uint64_t n, float* __restrict__ out) {
+    const uint64_t q = (elem0 >> 2) + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (4 * q >= elem0 + n) return;
+    float e[4];
+    es::quad_normals(static_cast<uint32_t>(q), static_cast<uint32_t>(q >> 32), tensor_id, k0, k1, e);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint64_t j = 4 * q + k;
+        if (j >= elem0 && j < elem0 + n) out[j - elem0] = e[k];
+    }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------------------
+// Host side
+// ------------------------------------------------------------------------
+
+struct es_plan {
+    int device = -1;
+    uint32_t n_tensors = 0;
+    uint64_t numel = 0;
+    uint64_t n_tiles = 0;
+    uint32_t grid = 0;
+    DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
+    uint8_t* d_scratch = nullptr;   // kScratchBytes
+};
+
+namespace {
+
+int check_device(const es_plan_t* p) {
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != p->device)
+        return fail(ES_ERR_DEVICE, "current device " + std::to_string(dev) +
+                                       " differs from the plan's device " +
+                                       std::to_string(p->device));
+    return ES_OK;
+}
+
+int launch_perturb(es_plan_t* p, uint64_t seed, float coef, hipStream_t s) {
+    if (p->n_tiles == 0) return ES_OK;
+    hipLaunchKernelGGL(es_tiles_kernel<false>, dim3(p->grid), dim3(kBlock), 0, s, p->d_tab,
+                       p->n_tiles, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                       coef, nullptr, nullptr);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<perturb> launch");
+    return ES_OK;
+}
+
+int perturb_impl(es_plan_t* p, uint64_t seed, int32_t sign, float sigma, es_stream_t stream,
+                 const char* name) {
+    if (p == nullptr) return fail(ES_ERR_INVALID_ARG, std::string(name) + ": null plan");
+    if (sign != 1 && sign != -1)
+        return fail(ES_ERR_INVALID_ARG, std::string(name) + ": sign must be +1 or -1");
+    if (!std::isfinite(sigma) || sigma < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, std::string(name) + ": sigma must be finite and >= 0");
+    if (sigma == 0.0f) return ES_OK;
+    const int rc = check_device(p);
+    if (rc != ES_OK) return rc;
+    return launch_perturb(p, seed, sign > 0 ? sigma : -sigma, static_cast<hipStream_t>(stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out) {
+    if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null output pointer");
+    *out = nullptr;
+    if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null tensor list");
+    if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
+        return fail(ES_ERR_INVALID_ARG, "es_plan_create: n_tensors out of range");
+    std::vector<DevTensor> tab(n_tensors + 1);
+    std::unordered_map<uint32_t, uint32_t> ids;
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    uint64_t tiles = 0, numel = 0;
+    for (uint32_t i = 0; i < n_tensors; ++i) {
+        const es_tensor_t& t = tensors[i];
+        const std::string where = "es_plan_create: tensor " + std::to_string(i);
+        if (t.reserved != 0) return fail(ES_ERR_INVALID_ARG, where + ": reserved field must be 0");
+        if (!ids.emplace(t.tensor_id, i).second)
+            return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
+        if (t.numel > 0 && t.data == nullptr) return fail(ES_ERR_INVALID_ARG, where + ": null data");
+        if (t.numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, where + ": numel too large");
+        const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
+        if (t.numel > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
+        const uint64_t nt = (t.numel + kTileElems - 1) / kTileElems;
+        tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, tiles, t.tensor_id,
+                           (a % 16 == 0) ? kFlagAligned : 0u};
+        if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
+        tiles += nt;
+        numel += t.numel;
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+        if (ranges[i].first < ranges[i - 1].second)
+            return fail(ES_ERR_INVALID_ARG, "es_plan_create: tensors overlap in memory");
+    tab[n_tensors] = DevTensor{nullptr, 0, tiles, 0xFFFFFFFFu, 0u};   // sentinel
+
+    es_plan_t* p = new (std::nothrow) es_plan_t;
+    if (p == nullptr) return fail(ES_ERR_NOMEM, "es_plan_create: host allocation");
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
+    int wg_per_cu = kDefaultWgPerCu;
+    if (const char* env = std::getenv("ESOPT_WG_PER_CU")) {
+        const int v = std::atoi(env);
+        if (v >= 1 && v <= 64) wg_per_cu = v;
+    }
+    p->n_tensors = n_tensors;
+    p->numel = numel;
+    p->n_tiles = tiles;
+    p->grid = static_cast<uint32_t>(std::min<uint64_t>(tiles, uint64_t(cus) * wg_per_cu));
+    if (p->grid == 0) p->grid = 1;
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(DevTensor) * tab.size());
+    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        delete p;
+        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    e = hipMemcpy(p->d_tab, tab.data(), sizeof(DevTensor) * tab.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        (void)hipFree(p->d_scratch);
+        delete p;
+        return hip_fail(e, "es_plan_create: table upload");
+    }
+    *out = p;
+    return ES_OK;
+}
+
+int es_plan_destroy(es_plan_t* plan) {
+    if (plan == nullptr) return ES_OK;
+    int rc = ES_OK;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) rc = hip_fail(e, "es_plan_destroy: hipDeviceSynchronize");
+    e = hipFree(plan->d_tab);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_plan_destroy: hipFree");
+    e = hipFree(plan->d_scratch);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_plan_destroy: hipFree");
+    delete plan;
+    return rc;
+}
+
+uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
+uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_tiles : 0; }
+
+int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
+    return perturb_impl(plan, seed, sign, sigma, stream, "es_perturb");
+}
+
+int es_restore(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
+    if (sign != 1 && sign != -1)
+        return fail(ES_ERR_INVALID_ARG, "es_restore: sign must be +1 or -1");
+    return perturb_impl(plan, seed, -sign, sigma, stream, "es_restore");
+}
+
+int es_zscore(const float* rewards_dev, uint32_t n, float eps, float* z_dev, int32_t* status_dev,
+              es_stream_t stream) {
+    if (rewards_dev == nullptr || z_dev == nullptr)
+        return fail(ES_ERR_INVALID_ARG, "es_zscore: null pointer");
+    if (n == 0 || n > ES_MAX_MEMBERS) return fail(ES_ERR_INVALID_ARG, "es_zscore: n out of range");
+    if (!std::isfinite(eps) || eps < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, "es_zscore: eps must be finite and >= 0");
+    hipLaunchKernelGGL(es_zscore_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream),
+                       rewards_dev, n, static_cast<double>(eps), z_dev, status_dev);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_zscore_kernel launch");
+    return ES_OK;
+}
+
+int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
+              const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+              float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) {
+    if (plan == nullptr || seeds == nullptr || signs == nullptr || rewards_dev == nullptr ||
+        opts == nullptr)
+        return fail(ES_ERR_INVALID_ARG, "es_update: null pointer");
+    if (n_members == 0 || n_members > ES_MAX_MEMBERS)
+        return fail(ES_ERR_INVALID_ARG, "es_update: n_members out of range");
+    if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS)) != 0)
+        return fail(ES_ERR_INVALID_ARG, "es_update: unknown flags");
+    if (!std::isfinite(opts->alpha)) return fail(ES_ERR_INVALID_ARG, "es_update: alpha not finite");
+    if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
+        return fail(ES_ERR_INVALID_ARG, "es_update: sigma must be finite and > 0 with ES_UPDATE_DIV_SIGMA");
+    if (!std::isfinite(opts->zscore_eps) || opts->zscore_eps < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, "es_update: zscore_eps must be finite and >= 0");
+    for (uint32_t i = 0; i < n_members; ++i)
+        if (signs[i] != 1 && signs[i] != -1)
+            return fail(ES_ERR_INVALID_ARG, "es_update: signs must be +1 or -1");
+    int rc = check_device(plan);
+    if (rc != ES_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+
+    // Distinct seeds in order of first appearance; members grouped by seed
+    // (CSR), in member order within a seed.
+    std::unordered_map<uint64_t, uint32_t> index;
+    std::vector<uint64_t> distinct;
+    std::vector<uint32_t> of(n_members);
+    for (uint32_t i = 0; i < n_members; ++i) {
+        auto it = index.emplace(seeds[i], static_cast<uint32_t>(distinct.size()));
+        if (it.second) distinct.push_back(seeds[i]);
+        of[i] = it.first->second;
+    }
+    const uint32_t nd = static_cast<uint32_t>(distinct.size());
+    std::vector<uint32_t> count(nd, 0), first(nd, 0);
+    for (uint32_t i = 0; i < n_members; ++i) ++count[of[i]];
+    for (uint32_t d = 1; d < nd; ++d) first[d] = first[d - 1] + count[d - 1];
+    std::vector<MemberIn> min(n_members);
+    std::vector<uint32_t> fill(first);
+    for (uint32_t i = 0; i < n_members; ++i) min[fill[of[i]]++] = MemberIn{i, signs[i]};
+    std::vector<DistinctIn> din(nd);
+    for (uint32_t d = 0; d < nd; ++d)
+        din[d] = DistinctIn{static_cast<uint32_t>(distinct[d]),
+                            static_cast<uint32_t>(distinct[d] >> 32), first[d], count[d]};
+
+    // Stage both tables through kernel arguments, 1 KB per launch.
+    auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
+        const uint32_t* words = static_cast<const uint32_t*>(src);
+        const size_t n_words = bytes / 4;
+        for (size_t w0 = 0; w0 < n_words; w0 += kStageWords) {
+            StageChunk chunk;
+            const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
+            std::memcpy(chunk.words, words + w0, nw * 4);
+            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kBlock), 0, s,
+                               reinterpret_cast<uint32_t*>(plan->d_scratch + dst_off) + w0, nw, chunk);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
+        }
+        return ES_OK;
+    };
+    rc = stage(kOffMembersIn, min.data(), sizeof(MemberIn) * n_members);
+    if (rc == ES_OK) rc = stage(kOffDistinctIn, din.data(), sizeof(DistinctIn) * nd);
+    if (rc != ES_OK) return rc;
+
+    double c = static_cast<double>(opts->alpha) / static_cast<double>(n_members);
+    if (opts->flags & ES_UPDATE_DIV_SIGMA) c /= static_cast<double>(opts->sigma);
+    auto* members = reinterpret_cast<Member*>(plan->d_scratch + kOffMembers);
+    auto* hdr = reinterpret_cast<UpdateHeader*>(plan->d_scratch + kOffHeader);
+    hipLaunchKernelGGL(es_prepare_kernel, dim3(1), dim3(64), 0, s, rewards_dev, n_members,
+                       static_cast<double>(opts->zscore_eps), opts->flags, c,
+                       reinterpret_cast<const MemberIn*>(plan->d_scratch + kOffMembersIn),
+                       reinterpret_cast<const DistinctIn*>(plan->d_scratch + kOffDistinctIn), nd,
+                       members, hdr, z_out_dev, status_out_dev);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
+    if (plan->n_tiles == 0) return ES_OK;
+    hipLaunchKernelGGL(es_tiles_kernel<true>, dim3(plan->grid), dim3(kBlock), 0, s, plan->d_tab,
+                       plan->n_tiles, 0u, 0u, 0.0f, members, hdr);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<update> launch");
+    return ES_OK;
+}
+
+double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T) {
+    if (T == 0 || t > T) return NAN;
+    return sigma_T + (sigma0 - sigma_T) * (1.0 + std::cos(M_PI * double(t) / double(T))) / 2.0;
+}
+
+int es_philox_words(uint64_t seed, uint32_t tensor_id, uint32_t domain, uint64_t quad0,
+                    uint64_t n_quads, uint32_t* out_dev, es_stream_t stream) {
+    if (out_dev == nullptr) return fail(ES_ERR_INVALID_ARG, "es_philox_words: null output");
+    if (n_quads > (uint64_t(1) << 28)) return fail(ES_ERR_INVALID_ARG, "es_philox_words: n_quads too large");
+    if (reinterpret_cast<uintptr_t>(out_dev) % 16 != 0)
+        return fail(ES_ERR_ALIGN, "es_philox_words: output not 16-byte aligned");
+    if (n_quads == 0) return ES_OK;
+    const uint32_t blocks = static_cast<uint32_t>((n_quads + kBlock - 1) / kBlock);
+    hipLaunchKernelGGL(es_philox_words_kernel, dim3(blocks), dim3(kBlock), 0,
+                       static_cast<hipStream_t>(stream), static_cast<uint32_t>(seed),
+                       static_cast<uint32_t>(seed >> 32), tensor_id, domain, quad0, n_quads,
+                       reinterpret_cast<uint4*>(out_dev));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_philox_words_kernel launch");
+    return ES_OK;
+}
+
+int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, float* out_dev,
+               es_stream_t stream) {
+    if (out_dev == nullptr) return fail(ES_ERR_INVALID_ARG, "es_normals: null output");
+    if (n > (uint64_t(1) << 30)) return fail(ES_ERR_INVALID_ARG, "es_normals: n too large");
+    if (elem0 > (uint64_t(1) << 62) - n) return fail(ES_ERR_INVALID_ARG, "es_normals: element range beyond 2^62");
+    if (n == 0) return ES_OK;
+    const uint64_t quads = ((elem0 + n - 1) >> 2) - (elem0 >> 2) + 1;
+    const uint32_t blocks = static_cast<uint32_t>((quads + kBlock - 1) / kBlock);
+    hipLaunchKernelGGL(es_normals_kernel, dim3(blocks), dim3(kBlock), 0,
+                       static_cast<hipStream_t>(stream), static_cast<uint32_t>(seed),
+                       static_cast<uint32_t>(seed >> 32), tensor_id, elem0, n, out_dev);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_normals_kernel launch");
+    return ES_OK;
+}
+
+const char* es_strerror(int code) {
+    switch (code) {
+        case ES_OK: return "ES_OK";
+        case ES_ERR_INVALID_ARG: return "ES_ERR_INVALID_ARG";
+        case ES_ERR_ALIGN: return "ES_ERR_ALIGN";
+        case ES_ERR_HIP: return "ES_ERR_HIP";
+        case ES_ERR_DEVICE: return "ES_ERR_DEVICE";
+        case ES_ERR_NOMEM: return "ES_ERR_NOMEM";
+        default: return "ES_ERR_UNKNOWN";
+    }
+}
+
+const char* es_last_error(void) { return g_last_error.c_str(); }
+
+}  // extern "C"

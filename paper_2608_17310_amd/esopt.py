@@ -1,0 +1,234 @@
+"""ctypes binding of libesopt.so (the C ABI in include/esopt.h).
+
+Argument marshalling only: every step of the ES parameter path runs in the HIP
+kernels of the library.  PyTorch supplies device memory and the current HIP
+stream.  The library is loaded on first use; if it has not been built the
+call raises (there is no fallback).
+
+    plan = Plan([w0, w1, ...])           # bf16, contiguous, on the current device
+    plan.perturb(seed, sign, sigma)      # theta += sign sigma eps(seed)
+    plan.restore(seed, sign, sigma)      # theta -= sign sigma eps(seed)
+    plan.update(seeds, signs, rewards, alpha)   # fused z-score + N-member update
+"""
+
+import ctypes
+import os
+
+import torch
+
+LIB_NAME = "libesopt.so"
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), LIB_NAME)
+
+ES_OK = 0
+ES_ERR_INVALID_ARG = -1
+ES_ERR_ALIGN = -2
+ES_ERR_HIP = -3
+ES_ERR_DEVICE = -4
+ES_ERR_NOMEM = -5
+ES_MAX_MEMBERS = 1024
+ES_UPDATE_DIV_SIGMA = 1
+ES_REWARDS_ARE_WEIGHTS = 2
+
+# Every symbol the header declares, with (restype, argtypes).
+_u32, _u64, _i32, _f32, _f64 = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32,
+                                ctypes.c_float, ctypes.c_double)
+_vp = ctypes.c_void_p
+
+
+class EsTensor(ctypes.Structure):
+    _fields_ = [("data", _vp), ("numel", _u64), ("tensor_id", _u32), ("reserved", _u32)]
+
+
+class EsUpdateOpts(ctypes.Structure):
+    _fields_ = [("alpha", _f32), ("sigma", _f32), ("zscore_eps", _f32), ("flags", _u32)]
+
+
+SIGNATURES = {
+    "es_plan_create": (ctypes.c_int, [ctypes.POINTER(EsTensor), _u32, ctypes.POINTER(_vp)]),
+    "es_plan_destroy": (ctypes.c_int, [_vp]),
+    "es_plan_numel": (_u64, [_vp]),
+    "es_plan_tiles": (_u64, [_vp]),
+    "es_perturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
+    "es_restore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
+    "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
+    "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
+                                 ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
+    "es_sigma_cosine": (_f64, [_f64, _f64, _u32, _u32]),
+    "es_philox_words": (ctypes.c_int, [_u64, _u32, _u32, _u64, _u64, _vp, _vp]),
+    "es_normals": (ctypes.c_int, [_u64, _u32, _u64, _u64, _vp, _vp]),
+    "es_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "es_last_error": (ctypes.c_char_p, []),
+}
+
+_lib = None
+
+
+class EsError(RuntimeError):
+    def __init__(self, code, what, detail):
+        super().__init__(f"{what}: {name_of(code)}: {detail}")
+        self.code = code
+
+
+def load():
+    """Load libesopt.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; "
+                f"g.build()'` (hipcc, gfx950); there is no CPU fallback")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+def name_of(code):
+    return load().es_strerror(code).decode()
+
+
+def last_error():
+    return load().es_last_error().decode()
+
+
+def _check(rc, what):
+    if rc != ES_OK:
+        raise EsError(rc, what, last_error())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dev_ptr(t, dtype, what):
+    if t is None:
+        return None
+    if not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous {dtype} tensor on the GPU")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+class Plan:
+    """A list of bf16 parameter tensors prepared for single-launch passes.
+
+    tensor_ids defaults to the list index.  The plan holds references to the
+    tensors so their storage stays alive and in place while it exists.
+    """
+
+    def __init__(self, tensors, tensor_ids=None):
+        tensors = list(tensors)
+        if not tensors:
+            raise ValueError("empty tensor list")
+        ids = list(range(len(tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
+        if len(ids) != len(tensors):
+            raise ValueError("tensor_ids must match tensors")
+        arr = (EsTensor * len(tensors))()
+        for i, (t, tid) in enumerate(zip(tensors, ids)):
+            if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"tensor {i} must be a contiguous bf16 CUDA tensor")
+            arr[i] = EsTensor(t.data_ptr() if t.numel() else None, t.numel(), tid, 0)
+        self._tensors = tensors
+        self.tensor_ids = ids
+        self.device = tensors[0].device
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(load().es_plan_create(arr, len(tensors), ctypes.byref(handle)), "es_plan_create")
+        self._h = handle
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise RuntimeError("plan is closed")
+        return self._h
+
+    @property
+    def numel(self):
+        return int(load().es_plan_numel(self.handle))
+
+    @property
+    def tiles(self):
+        return int(load().es_plan_tiles(self.handle))
+
+    @property
+    def tensors(self):
+        return list(self._tensors)
+
+    def perturb(self, seed, sign, sigma, stream=None):
+        _check(load().es_perturb(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
+               "es_perturb")
+
+    def restore(self, seed, sign, sigma, stream=None):
+        _check(load().es_restore(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
+               "es_restore")
+
+    def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
+               z_out=None, status_out=None, stream=None):
+        """Fused update; rewards is a float32 CUDA tensor of len(seeds)."""
+        n = len(seeds)
+        if len(signs) != n:
+            raise ValueError("seeds and signs differ in length")
+        if rewards.numel() != n:
+            raise ValueError("rewards must have one entry per member")
+        c_seeds = (_u64 * max(n, 1))(*[int(s) for s in seeds])
+        c_signs = (_i32 * max(n, 1))(*[int(s) for s in signs])
+        opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags))
+        _check(load().es_update(self.handle, c_seeds, c_signs,
+                                _dev_ptr(rewards, torch.float32, "rewards"), n, ctypes.byref(opts),
+                                _dev_ptr(z_out, torch.float32, "z_out"),
+                                _dev_ptr(status_out, torch.int32, "status_out"), _stream(stream)),
+               "es_update")
+
+    def close(self):
+        if self._h is not None:
+            _check(load().es_plan_destroy(self._h), "es_plan_destroy")
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def zscore(rewards, eps=1e-8, out=None, status=None, stream=None):
+    """Population z-score of a float32 CUDA tensor (one wavefront, fp64)."""
+    out = torch.empty_like(rewards) if out is None else out
+    _check(load().es_zscore(_dev_ptr(rewards, torch.float32, "rewards"), rewards.numel(),
+                            float(eps), _dev_ptr(out, torch.float32, "out"),
+                            _dev_ptr(status, torch.int32, "status"), _stream(stream)), "es_zscore")
+    return out
+
+
+def sigma_cosine(sigma0, sigma_T, t, T):
+    return float(load().es_sigma_cosine(float(sigma0), float(sigma_T), int(t), int(T)))
+
+
+def philox_words(seed, tensor_id, quad0, n_quads, domain=0, device="cuda", stream=None):
+    """Raw Philox words as an int32 CUDA tensor of shape (n_quads, 4)
+    (reinterpret as uint32)."""
+    out = torch.empty((n_quads, 4), dtype=torch.int32, device=device)
+    _check(load().es_philox_words(int(seed), int(tensor_id), int(domain), int(quad0),
+                                  int(n_quads), ctypes.c_void_p(out.data_ptr()), _stream(stream)),
+           "es_philox_words")
+    return out
+
+
+def normals(seed, tensor_id, elem0, n, device="cuda", stream=None):
+    """eps_j for j = elem0 .. elem0 + n - 1 of one tensor, float32 CUDA tensor."""
+    out = torch.empty(n, dtype=torch.float32, device=device)
+    _check(load().es_normals(int(seed), int(tensor_id), int(elem0), int(n),
+                             ctypes.c_void_p(out.data_ptr()), _stream(stream)), "es_normals")
+    return out

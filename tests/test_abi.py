@@ -1,0 +1,122 @@
+"""The C ABI library loads, exports every symbol include/esopt.h declares,
+and rejects invalid arguments before touching the GPU (CPU-only checks)."""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2608_17310_amd import esopt
+import oracle
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
+                      "include", "esopt.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(es_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(esopt.LIB_PATH):
+        pytest.fail("libesopt.so is not built (run __graft_entry__.build())")
+    return esopt.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = _declared()
+    assert "es_update" in names and "es_perturb" in names
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(esopt.SIGNATURES) == names
+
+
+def test_error_names(lib):
+    for code, name in [(0, "ES_OK"), (-1, "ES_ERR_INVALID_ARG"), (-2, "ES_ERR_ALIGN"),
+                       (-3, "ES_ERR_HIP"), (-4, "ES_ERR_DEVICE"), (-5, "ES_ERR_NOMEM"),
+                       (-99, "ES_ERR_UNKNOWN")]:
+        assert esopt.name_of(code) == name
+
+
+def _create(lib, specs):
+    arr = (esopt.EsTensor * max(len(specs), 1))(*[esopt.EsTensor(*s) for s in specs])
+    h = ctypes.c_void_p()
+    return lib.es_plan_create(arr, len(specs), ctypes.byref(h)), esopt.last_error()
+
+
+def test_plan_create_validation(lib):
+    h = ctypes.c_void_p()
+    assert lib.es_plan_create(None, 1, ctypes.byref(h)) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_plan_create((esopt.EsTensor * 1)(), 1, None) == esopt.ES_ERR_INVALID_ARG
+    rc, msg = _create(lib, [])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "n_tensors" in msg
+    rc, msg = _create(lib, [(0x1000, 10, 0, 0), (0x2000, 10, 0, 0)])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "duplicate" in msg
+    rc, msg = _create(lib, [(0x1000, 10, 0, 7)])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "reserved" in msg
+    rc, msg = _create(lib, [(None, 10, 0, 0)])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "null data" in msg
+    rc, msg = _create(lib, [(0x1001, 10, 0, 0)])
+    assert rc == esopt.ES_ERR_ALIGN
+    rc, msg = _create(lib, [(0x1000, 100, 0, 0), (0x1000 + 2 * 99, 10, 1, 0)])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "overlap" in msg
+
+
+def test_call_validation_without_device(lib):
+    assert lib.es_perturb(None, 1, 1, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_restore(None, 1, 1, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.es_perturb(fake, 1, 0, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_perturb(fake, 1, 1, float("nan"), None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_perturb(fake, 1, 1, -1e-3, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_restore(fake, 1, 2, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_zscore(None, 4, 1e-8, fake, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_zscore(fake, 0, 1e-8, fake, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_zscore(fake, 1025, 1e-8, fake, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_zscore(fake, 4, -1.0, fake, None, None) == esopt.ES_ERR_INVALID_ARG
+    seeds = (ctypes.c_uint64 * 2)(1, 2)
+    signs = (ctypes.c_int32 * 2)(1, 1)
+    bad_signs = (ctypes.c_int32 * 2)(1, 0)
+    opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0)
+    U = lib.es_update
+    assert U(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert U(fake, seeds, signs, fake, 0, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert U(fake, seeds, signs, fake, 1025, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert U(fake, seeds, bad_signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    for o in [esopt.EsUpdateOpts(float("inf"), 1e-3, 1e-8, 0),
+              esopt.EsUpdateOpts(5e-4, 0.0, 1e-8, esopt.ES_UPDATE_DIV_SIGMA),
+              esopt.EsUpdateOpts(5e-4, 1e-3, -1.0, 0),
+              esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8)]:
+        assert U(fake, seeds, signs, fake, 2, ctypes.byref(o), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_philox_words(1, 0, 0, 0, 4, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_philox_words(1, 0, 0, 0, 4, ctypes.c_void_p(0x1004), None) == esopt.ES_ERR_ALIGN
+    assert lib.es_philox_words(1, 0, 0, 0, 1 << 29, fake, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_normals(1, 0, 0, 4, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_normals(1, 0, (1 << 62) - 2, 4, fake, None) == esopt.ES_ERR_INVALID_ARG
+    # zero-length requests are valid no-ops
+    assert lib.es_philox_words(1, 0, 0, 0, 0, fake, None) == esopt.ES_OK
+    assert lib.es_normals(1, 0, 0, 0, fake, None) == esopt.ES_OK
+    assert lib.es_plan_destroy(None) == esopt.ES_OK
+    assert lib.es_plan_numel(None) == 0
+
+
+def test_sigma_cosine_helper_matches_oracle(lib):
+    for s0, sT, T in [(1e-3, 1e-4, 100), (1e-3, 0.0, 50), (1.5e-3, 1.5e-3, 70), (7e-4, 5e-4, 100)]:
+        for t in range(T + 1):
+            a = lib.es_sigma_cosine(s0, sT, t, T)
+            b = oracle.sigma_cosine(s0, sT, t, T)
+            assert abs(a - b) <= 1e-18 + 1e-15 * abs(b)
+    assert math.isnan(lib.es_sigma_cosine(1e-3, 1e-4, 101, 100))
+    assert math.isnan(lib.es_sigma_cosine(1e-3, 1e-4, 0, 0))
+
+
+def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
+    monkeypatch.setattr(esopt, "_lib", None)
+    monkeypatch.setattr(esopt, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="no CPU fallback"):
+        esopt.load()

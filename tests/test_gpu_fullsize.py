@@ -1,0 +1,98 @@
+"""Full-size parameter sets (0.5B, 4B, 27B-shaped; and the 4B set with a
+256-member update) in the launch configuration the benchmark times: one
+plan over every tensor, one launch per pass.  Outputs are checked on sampled
+elements that the oracle recomputes one by one (every element of a
+counter-based, elementwise method can be checked in isolation): random
+elements of every tensor plus each tensor's first and last elements and
+elements on both sides of tile boundaries."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_17310_amd import esopt, workloads as wl
+from parity import to_host, report, assert_parity, perturb_delta, update_delta
+
+pytestmark = pytest.mark.gpu
+
+TILE = 4096
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _samples(numel, rng, k=256):
+    fixed = [0, 1, 2, 3, 4, 7, 8, TILE - 1, TILE, TILE + 1, numel // 2, numel - 8, numel - 2,
+             numel - 1]
+    idx = np.concatenate([np.array([i for i in fixed if 0 <= i < numel], dtype=np.int64),
+                          rng.integers(0, numel, size=min(k, numel))])
+    return np.unique(idx)
+
+
+def _gather(views, idx_dev):
+    return [to_host(v.view(-1).index_select(0, i)) for v, i in zip(views, idx_dev)]
+
+
+def _run(W, n_members=None, samples_per_tensor=256):
+    seeds = W.seeds if n_members is None else tuple(range(n_members))
+    signs = W.signs if n_members is None else (1,) * n_members
+    rng = np.random.default_rng(7)
+    flat, views = wl.device_params(W)
+    plan = esopt.Plan(views)
+    assert plan.numel == W.n_params
+    idx = [_samples(v.numel(), rng, samples_per_tensor) for v in views]
+    idx_dev = [torch.from_numpy(i).cuda() for i in idx]
+    sigma = W.sigma0
+    theta0 = _gather(views, idx_dev)
+    seed, sign = seeds[-1], signs[-1]
+    plan.perturb(seed, sign, sigma)
+    torch.cuda.synchronize()
+    pert = _gather(views, idx_dev)
+    plan.restore(seed, sign, sigma)
+    torch.cuda.synchronize()
+    rest = _gather(views, idx_dev)
+    r = wl.rewards(W, n=len(seeds))
+    status = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    plan.update(seeds, signs, torch.from_numpy(r).cuda(), W.alpha, sigma=sigma, status_out=status)
+    torch.cuda.synchronize()
+    upd = _gather(views, idx_dev)
+    assert int(status.item()) == 0
+    plan.close()
+    del flat, views
+    torch.cuda.empty_cache()
+
+    reps = {"perturb": [], "restore": [], "update": []}
+    for t, el_i in enumerate(idx):
+        el = el_i.astype(np.uint64)
+        exp = oracle.perturb(theta0[t], seed, t, sign, sigma, elems=el)
+        reps["perturb"].append(report(pert[t], exp, theta0[t], perturb_delta(seed, t, sign, sigma, el)))
+        exp = oracle.restore(pert[t], seed, t, sign, sigma, elems=el)
+        reps["restore"].append(report(rest[t], exp, pert[t], perturb_delta(seed, t, -sign, sigma, el)))
+        exp, st = oracle.update(rest[t], t, seeds, signs, r, W.alpha, sigma, elems=el)
+        reps["update"].append(report(upd[t], exp, rest[t],
+                                     update_delta(t, seeds, signs, r, W.alpha, sigma, 0, el)))
+    for k, rs in reps.items():
+        n = sum(x["n"] for x in rs)
+        agg = {
+            "n": n,
+            "exact": sum(x["exact"] * x["n"] for x in rs) / n,
+            "le1": sum(x["le1"] * x["n"] for x in rs) / n,
+            "max_ulp": max(x["max_ulp"] for x in rs),
+            "plain_max_ulp": max(x["plain_max_ulp"] for x in rs),
+            "n_gt1": sum(x["n_gt1"] for x in rs),
+        }
+        print(W.name, k, agg)
+        assert_parity(agg, f"{W.name} {k}")
+
+
+@pytest.mark.parametrize("name", ["dense-0.5b", "dense-4b", "dense-27b"])
+def test_full_size_sampled_parity(name):
+    _run(wl.WORKLOADS[name])
+
+
+def test_large_population_sweep_n256_on_4b_set():
+    _run(wl.sweep_workload(256), samples_per_tensor=64)

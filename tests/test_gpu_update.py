@@ -1,0 +1,158 @@
+"""Fused es_update and es_zscore on the GPU against the oracle: the tiny set
+(N=4), antithetic pairs, both coefficient modes, rewards-as-weights, large
+N, identities (alpha = 0, equal rewards, cancelling pairs), non-finite
+rewards, determinism and the z-score itself."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_17310_amd import esopt, workloads as wl
+from parity import to_device, to_host, report, assert_parity, update_delta, perturb_delta
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _rewards_dev(r):
+    return torch.from_numpy(np.asarray(r, dtype=np.float32)).cuda()
+
+
+def _run_update(bits_list, seeds, signs, rewards, alpha, sigma=1e-3, flags=0, ids=None):
+    ts = [to_device(b) for b in bits_list]
+    plan = esopt.Plan(ts, tensor_ids=ids)
+    status = torch.full((1,), -7, dtype=torch.int32, device="cuda")
+    z = torch.zeros(len(seeds), dtype=torch.float32, device="cuda")
+    plan.update(seeds, signs, _rewards_dev(rewards), alpha, sigma=sigma, flags=flags,
+                z_out=z, status_out=status)
+    torch.cuda.synchronize()
+    out = [to_host(t) for t in ts]
+    plan.close()
+    return out, int(status.item()), z.cpu().numpy()
+
+
+def _check(bits_list, out, seeds, signs, rewards, alpha, sigma, flags, ids, what):
+    for i, b in enumerate(bits_list):
+        tid = ids[i] if ids else i
+        el = np.arange(b.size, dtype=np.uint64)
+        exp, st = oracle.update(b, tid, seeds, signs, rewards, alpha, sigma, flags=flags)
+        rep = report(out[i], exp, b, update_delta(tid, seeds, signs, rewards, alpha, sigma, flags, el))
+        print(what, i, rep)
+        assert_parity(rep, f"{what} tensor {i}")
+
+
+def test_tiny_config_update():
+    W = wl.TINY
+    host = wl.host_params(W)
+    r = wl.rewards(W)
+    out, st, z = _run_update(host, W.seeds, W.signs, r, W.alpha)
+    assert st == 0
+    ez, _ = oracle.zscore(r)
+    np.testing.assert_allclose(z, ez, rtol=1e-6, atol=1e-7)
+    _check(host, out, W.seeds, W.signs, r, W.alpha, W.sigma0, 0, None, "tiny update")
+
+
+@pytest.mark.parametrize("flags", [0, esopt.ES_UPDATE_DIV_SIGMA])
+def test_antithetic_pairs_and_modes(flags):
+    sizes = [5000, 4096 * 3 + 1, 77]
+    bits = [wl.random_bf16_bits(n, 30 + i) for i, n in enumerate(sizes)]
+    seeds = [11, 11, 12, 12, 13, 13, 14, 14]
+    signs = [1, -1] * 4
+    r = (np.random.default_rng(3).random(8) < 0.4).astype(np.float32)
+    r[0] = 1.0; r[1] = 0.0
+    out, st, _ = _run_update(bits, seeds, signs, r, 5e-4, sigma=1e-3, flags=flags)
+    assert st == 0
+    _check(bits, out, seeds, signs, r, 5e-4, 1e-3, flags, None, f"antithetic flags={flags}")
+
+
+def test_rewards_as_weights_and_single_member_vs_perturb():
+    bits = [wl.random_bf16_bits(1 << 16, 40)]
+    out, st, z = _run_update(bits, [77], [1], [1.0], alpha=1e-3,
+                             flags=esopt.ES_REWARDS_ARE_WEIGHTS)
+    assert st == 0 and z[0] == 1.0
+    _check(bits, out, [77], [1], [1.0], 1e-3, 1e-3, esopt.ES_REWARDS_ARE_WEIGHTS, None, "weights")
+    # the same step through es_perturb: equal up to binary32 rounding ties
+    t = to_device(bits[0])
+    plan = esopt.Plan([t])
+    plan.perturb(77, 1, 1e-3)
+    torch.cuda.synchronize()
+    p = to_host(t)
+    plan.close()
+    rep = report(out[0], p, bits[0], perturb_delta(77, 0, 1, 1e-3, np.arange(1 << 16, dtype=np.uint64)))
+    assert rep["max_ulp"] <= 1.0 and rep["exact"] >= 0.9999, rep
+
+
+@pytest.mark.parametrize("n_members", [32, 256, 1024])
+def test_large_population(n_members):
+    bits = [wl.random_bf16_bits(4096 * 2 + 8, 50)]
+    seeds = list(range(1000, 1000 + n_members))
+    r = np.random.default_rng(n_members).standard_normal(n_members).astype(np.float32)
+    out, st, _ = _run_update(bits, seeds, [1] * n_members, r, 5e-4)
+    assert st == 0
+    _check(bits, out, seeds, [1] * n_members, r, 5e-4, 1e-3, 0, None, f"N={n_members}")
+
+
+def test_update_identities_leave_theta_bit_identical():
+    bits = [wl.random_bf16_bits(20000, 60)]
+    bits[0][:4] = [0x8000, 0x0000, 0x8000, 0x0001]
+    cases = [
+        ([1, 2, 3, 4], [1] * 4, [0.3, 0.9, 0.1, 0.5], 0.0),             # alpha = 0
+        ([1, 2, 3, 4], [1] * 4, [0.7] * 4, 5e-4),                       # equal rewards
+        ([5], [1], [0.2], 5e-4),                                        # N = 1
+        ([1, 1, 2, 2], [1, -1, 1, -1], [1.0, 1.0, 0.0, 0.0], 5e-4),     # cancelling pairs
+    ]
+    for seeds, signs, r, alpha in cases:
+        out, st, _ = _run_update(bits, seeds, signs, r, alpha)
+        assert st == 0
+        np.testing.assert_array_equal(out[0], bits[0])
+
+
+def test_non_finite_reward_is_a_no_op_with_status():
+    bits = [wl.random_bf16_bits(9000, 61)]
+    for bad in [np.nan, np.inf, -np.inf]:
+        out, st, z = _run_update(bits, [1, 2, 3], [1, 1, 1], [0.5, bad, 0.1], 5e-4)
+        assert st == 1
+        assert np.all(z == 0)
+        np.testing.assert_array_equal(out[0], bits[0])
+    out, st, _ = _run_update(bits, [1, 2], [1, 1], [np.nan, 1.0], 5e-4,
+                             flags=esopt.ES_REWARDS_ARE_WEIGHTS)
+    assert st == 1
+    np.testing.assert_array_equal(out[0], bits[0])
+
+
+def test_update_deterministic():
+    bits = [wl.random_bf16_bits(1 << 17, 62)]
+    r = np.random.default_rng(5).random(16).astype(np.float32)
+    a, _, _ = _run_update(bits, list(range(16)), [1] * 16, r, 5e-4)
+    b, _, _ = _run_update(bits, list(range(16)), [1] * 16, r, 5e-4)
+    np.testing.assert_array_equal(a[0], b[0])
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 63, 64, 65, 1000, 1024])
+def test_zscore_kernel(n):
+    rng = np.random.default_rng(n)
+    r = (rng.standard_normal(n) * 2 + 5).astype(np.float32)
+    st = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    z = esopt.zscore(_rewards_dev(r), status=st).cpu().numpy().astype(np.float64)
+    ez, est = oracle.zscore(r)
+    assert int(st.item()) == est == 0
+    assert np.all(np.abs(z - ez) <= 1e-6 * np.maximum(1, np.abs(ez)))
+    if n == 1:
+        assert np.all(z == 0)
+
+
+def test_zscore_kernel_edge_cases():
+    st = torch.full((1,), -1, dtype=torch.int32, device="cuda")
+    z = esopt.zscore(_rewards_dev([0.1] * 37), status=st).cpu().numpy()
+    assert int(st.item()) == 0 and np.all(z == 0)
+    z = esopt.zscore(_rewards_dev([0.0, 1.0]), status=st).cpu().numpy()
+    k = 0.5 / (0.5 + float(np.float32(1e-8)))
+    np.testing.assert_array_equal(z, np.float32([-k, k]))
+    z = esopt.zscore(_rewards_dev([1.0, np.nan, 2.0]), status=st).cpu().numpy()
+    assert int(st.item()) == 1 and np.all(z == 0)
