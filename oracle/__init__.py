@@ -29,8 +29,8 @@ are pinned (none is "parity unpinned").
 """
 
 from .philox import philox4x32_10, philox4x32_10_bigint, MASK32
-from .noise import (key_words, counter_words, uniform_from_word, box_muller,
-                    noise_words, normals)
+from .noise import (key_words, counter_words, uniform_from_word, angle_from_word,
+                    box_muller, noise_words, normals)
 from .bf16 import bf16_to_f64, f64_to_bf16_rne, bf16_ulp
 from .es import (perturb, restore, zscore, update_coefficient, member_weights,
                  update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
@@ -38,7 +38,7 @@ from .es import (perturb, restore, zscore, update_coefficient, member_weights,
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
-    "key_words", "counter_words", "uniform_from_word", "box_muller",
+    "key_words", "counter_words", "uniform_from_word", "angle_from_word", "box_muller",
     "noise_words", "normals",
     "bf16_to_f64", "f64_to_bf16_rne", "bf16_ulp",
     "perturb", "restore", "zscore", "update_coefficient", "member_weights",

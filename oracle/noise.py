@@ -13,11 +13,13 @@ element of any tensor can be regenerated in isolation:
   counter q when j mod 4 is 0 or 1, and the pair (w2, w3) when it is 2 or 3.
   domain is 0 for the perturbation noise (other values are reserved).
 
-  uniform u(w) = (floor(w / 2^9) + 1/2) * 2^-23, in [2^-24, 1 - 2^-24]; the
-  value is exact in binary32 as well as binary64, so log(0) cannot occur.
+  m(w) = w mod 2^23 (the low 23 bits of a word)
+  radius uniform u(w) = (m(w) + 1/2) * 2^-23, in [2^-24, 1 - 2^-24]
+  angle (in turns)  v(w) = m(w) * 2^-23,     in [0, 1)
+  Both are exact in binary32 as well as binary64, and log(0) cannot occur.
 
   Box-Muller (G. E. P. Box, M. E. Muller, 1958) on a word pair (wa, wb):
-      r   = sqrt(-2 ln u(wa)),  phi = 2 pi u(wb)
+      r   = sqrt(-2 ln u(wa)),  phi = 2 pi v(wb)
       first  element of the pair: r cos(phi)
       second element of the pair: r sin(phi)
 
@@ -58,16 +60,25 @@ def noise_words(seed, tensor_id, quads, domain=DOMAIN_NOISE):
                          key_words(seed))
 
 
+def low23(w):
+    """m(w) = w mod 2^23."""
+    return np.asarray(w, dtype=np.uint64) & np.uint64((1 << 23) - 1)
+
+
 def uniform_from_word(w):
-    """u(w) = (floor(w / 2^9) + 1/2) * 2^-23, computed exactly in fp64."""
-    w = np.asarray(w, dtype=np.uint64)
-    return ((w >> np.uint64(9)).astype(np.float64) + 0.5) * 2.0 ** -23
+    """Radius uniform u(w) = (m(w) + 1/2) * 2^-23, exact in fp64."""
+    return (low23(w).astype(np.float64) + 0.5) * 2.0 ** -23
+
+
+def angle_from_word(w):
+    """Angle in turns v(w) = m(w) * 2^-23, exact in fp64."""
+    return low23(w).astype(np.float64) * 2.0 ** -23
 
 
 def box_muller(wa, wb):
     """Box-Muller on word pairs; returns (r cos phi, r sin phi) in fp64."""
     r = np.sqrt(-2.0 * np.log(uniform_from_word(wa)))
-    phi = 2.0 * np.pi * uniform_from_word(wb)
+    phi = 2.0 * np.pi * angle_from_word(wb)
     return r * np.cos(phi), r * np.sin(phi)
 
 

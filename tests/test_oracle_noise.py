@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 from scipy import stats
 
-from oracle import uniform_from_word, box_muller, normals, noise_words
+from oracle import uniform_from_word, angle_from_word, box_muller, normals, noise_words
 
 BM_BOUND = math.sqrt(48.0 * math.log(2.0))     # sqrt(-2 ln 2^-24)
 
@@ -44,33 +44,44 @@ def test_assignment_matches_engine_counter_api(kat_harness, engine):
 
 def test_uniform_map_closed_forms():
     assert uniform_from_word(0) == 2.0 ** -24
+    assert uniform_from_word(0x7FFFFF) == 1.0 - 2.0 ** -24
     assert uniform_from_word(0xFFFFFFFF) == 1.0 - 2.0 ** -24
-    assert uniform_from_word(1 << 31) == 0.5 + 2.0 ** -24
-    assert uniform_from_word(511) == 2.0 ** -24          # low 9 bits are dropped
+    assert uniform_from_word(1 << 22) == 0.5 + 2.0 ** -24
+    assert uniform_from_word(0xFF800000) == 2.0 ** -24     # high 9 bits are dropped
+    assert angle_from_word(0) == 0.0
+    assert angle_from_word(1 << 22) == 0.5
+    assert angle_from_word(1 << 21) == 0.25
+    assert angle_from_word(0x7FFFFF) == 1.0 - 2.0 ** -23
+    assert angle_from_word(0xFF800000 | 5) == 5 * 2.0 ** -23
     w = np.random.default_rng(0).integers(0, 1 << 32, size=100000, dtype=np.uint64)
-    u = uniform_from_word(w)
-    assert np.all(u.astype(np.float32).astype(np.float64) == u)   # exact in binary32
-    assert np.all((u > 0) & (u < 1))
-    grid = uniform_from_word(np.arange(0, 1 << 14, dtype=np.uint64) << np.uint64(9))
-    assert np.all(np.diff(grid) == 2.0 ** -23)
+    for f in (uniform_from_word, angle_from_word):
+        u = f(w)
+        assert np.all(u.astype(np.float32).astype(np.float64) == u)   # exact in binary32
+        assert np.all((u >= 0) & (u < 1))
+        grid = f(np.arange(0, 1 << 14, dtype=np.uint64))
+        assert np.all(np.diff(grid) == 2.0 ** -23)
+    assert np.all(uniform_from_word(w) > 0)
 
 
 def test_box_muller_hand_values():
-    half = np.uint64(1 << 31)            # u = 1/2 + 2^-24
-    zero = np.uint64(0)                  # u = 2^-24
-    quarter = np.uint64(1 << 30)         # u = 1/4 + 2^-24
+    half = np.uint64(1 << 22)            # u = 1/2 + 2^-24, or half a turn
+    zero = np.uint64(0)                  # u = 2^-24, or angle 0
+    quarter = np.uint64(1 << 21)         # a quarter turn
     r_half = math.sqrt(2.0 * math.log(2.0))          # Rayleigh median, 1.17741...
-    c, s = box_muller(half, zero)
+    c, s = box_muller(half, zero)        # phi = 0: (r, 0) exactly
     assert abs(float(c) - r_half) < 1e-6
-    assert abs(float(s) - r_half * 2 * math.pi * 2.0 ** -24) < 1e-12
-    c, s = box_muller(half, quarter)     # phi just past pi/2
+    assert float(s) == 0.0
+    c, s = box_muller(half, quarter)     # phi = pi/2
     assert abs(float(s) - r_half) < 1e-6
-    assert -1e-6 < float(c) < 0
-    c, s = box_muller(zero, half)        # largest radius, phi just past pi
-    assert abs(float(c) + BM_BOUND) < 1e-5
-    assert abs(float(s)) < 1e-5
-    c, s = box_muller(np.uint64(0xFFFFFFFF), half)   # smallest radius
-    assert abs(float(c)) < 1e-3 and abs(float(s)) < 1e-3
+    assert abs(float(c)) < 1e-15
+    c, s = box_muller(zero, half)        # largest radius, phi = pi
+    assert abs(float(c) + BM_BOUND) < 1e-12
+    assert abs(float(s)) < 1e-14
+    c, s = box_muller(np.uint64(0x7FFFFF), half)   # smallest radius
+    assert abs(abs(float(c)) - math.sqrt(2.0 ** -23)) < 1e-9
+    # the high bits of the words play no part
+    c2, s2 = box_muller(np.uint64(0xABC00000 | (1 << 22)), np.uint64(0x12800000 | (1 << 21)))
+    assert (float(c2), float(s2)) == tuple(float(x) for x in box_muller(half, quarter))
 
 
 def test_normal_moments_and_ks():
