@@ -1,6 +1,6 @@
 // Device-side noise and bf16 helpers for gfx950.
 //
-// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), the uniform map and
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11), the uniform maps and
 // the Box-Muller transform, evaluated in binary32 registers.  The paper
 // (arXiv 2608.17310, Section 3 and Appendix D.6) only requires that each
 // direction be regenerated from an integer seed; the generator, the
@@ -10,16 +10,23 @@
 //   counter = (q lo, q hi, tensor_id, domain),  q = element >> 2
 //   element 4q+0, 4q+1 <- Box-Muller(w0, w1) = (r cos phi, r sin phi)
 //   element 4q+2, 4q+3 <- Box-Muller(w2, w3)
-//   u(w) = ((w >> 9) + 1/2) 2^-23,  r = sqrt(-2 ln u(wa)),  phi = 2 pi u(wb)
+//   m(w) = w & (2^23 - 1),  u = (m(wa) + 1/2) 2^-23,  v = m(wb) 2^-23
+//   r = sqrt(-2 ln u),  phi = 2 pi v
 //
 // Instruction choices (CDNA4 VALU):
-//   * the 32x32->64 products are written as 64-bit multiplies of zero-
-//     extended words, which select v_mad_u64_u32 (one instruction for both
-//     halves); products and XORs whose operands are wave-uniform (the
-//     counter's high words, tensor id, key) are left to the scalar unit;
-//   * ln u is taken as ln 2 * log2 u with the hardware v_log_f32, the root
-//     with v_sqrt_f32, and the angle goes to v_sin_f32 / v_cos_f32, which
-//     take their argument in revolutions, so 2 pi u needs no multiply;
+//   * the 32x32->64 products are 64-bit multiplies of zero-extended words,
+//     which select v_mad_u64_u32 (both halves in one instruction);
+//   * the two three-way XORs of a round are single v_bitop3_b32 (truth table
+//     0x96) from the third round on; the first two rounds keep plain XORs,
+//     where the counter's high words, the tensor id and the key are
+//     wave-uniform and the compiler moves those parts to the scalar unit;
+//   * OR-ing the low 23 bits of a word into the exponent of 1.0 (one
+//     v_and_or_b32) gives f = 1 + m 2^-23 in [1, 2); u = f - (1 - 2^-24) is
+//     exact, and v_sin_f32 / v_cos_f32 take turns and are periodic, so f
+//     itself is the angle with no further instruction;
+//   * r = sqrt(2 ln 2) sqrt(-log2 u) with the hardware v_log_f32 (log2) and
+//     v_sqrt_f32; the constant sqrt(2 ln 2) is folded into the caller's
+//     per-pair scale, so applying a scaled normal is one FMA per element;
 //   * bf16 results use the gfx950 packed convert (round to nearest even).
 #pragma once
 
@@ -38,49 +45,69 @@ struct Words {
     uint32_t w0, w1, w2, w3;
 };
 
-// One Philox4x32-10 call: ten rounds of two 32x32->64 products and two
-// three-way XORs, the key advanced by the Weyl increments between rounds.
+constexpr float kSqrt2Ln2 = 1.17741002251547466f;       // sqrt(2 ln 2)
+
+// One Philox round: two 32x32->64 products, two three-way XORs.
+template <bool kBitop3>
+__device__ __forceinline__ void philox_round(uint32_t& c0, uint32_t& c1, uint32_t& c2,
+                                             uint32_t& c3, uint32_t k0, uint32_t k1) {
+    const uint64_t p0 = static_cast<uint64_t>(kPhiloxM0) * c0;
+    const uint64_t p1 = static_cast<uint64_t>(kPhiloxM1) * c2;
+    uint32_t n0, n2;
+    if constexpr (kBitop3) {
+        n0 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(p1 >> 32), c1, k0, 0x96);
+        n2 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(p0 >> 32), c3, k1, 0x96);
+    } else {
+        n0 = static_cast<uint32_t>(p1 >> 32) ^ c1 ^ k0;
+        n2 = static_cast<uint32_t>(p0 >> 32) ^ c3 ^ k1;
+    }
+    c1 = static_cast<uint32_t>(p1);
+    c3 = static_cast<uint32_t>(p0);
+    c0 = n0;
+    c2 = n2;
+}
+
+// One Philox4x32-10 call: ten rounds, the key advanced by the Weyl
+// increments between rounds.
 __device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
                                                uint32_t c3, uint32_t k0, uint32_t k1) {
+    philox_round<false>(c0, c1, c2, c3, k0, k1);
+    philox_round<false>(c0, c1, c2, c3, k0 + kWeyl0, k1 + kWeyl1);
 #pragma unroll
-    for (int round = 0; round < 10; ++round) {
-        const uint64_t p0 = static_cast<uint64_t>(kPhiloxM0) * c0;
-        const uint64_t p1 = static_cast<uint64_t>(kPhiloxM1) * c2;
-        const uint32_t n0 = static_cast<uint32_t>(p1 >> 32) ^ c1 ^ k0;
-        const uint32_t n2 = static_cast<uint32_t>(p0 >> 32) ^ c3 ^ k1;
-        c1 = static_cast<uint32_t>(p1);
-        c3 = static_cast<uint32_t>(p0);
-        c0 = n0;
-        c2 = n2;
-        k0 += kWeyl0;
-        k1 += kWeyl1;
-    }
+    for (uint32_t round = 2; round < 10; ++round)
+        philox_round<true>(c0, c1, c2, c3, k0 + round * kWeyl0, k1 + round * kWeyl1);
     return Words{c0, c1, c2, c3};
 }
 
-// u(w) = ((w >> 9) + 1/2) * 2^-23: the conversion of a 23-bit integer and
-// the fused multiply-add are both exact, so u is bit-identical to its fp64
-// value.
-__device__ __forceinline__ float uniform_open(uint32_t w) {
-    return __builtin_fmaf(static_cast<float>(w >> 9), 0x1p-23f, 0x1p-24f);
+// f = 1 + m(w) 2^-23 in [1, 2): the low 23 bits under the exponent of 1.0.
+__device__ __forceinline__ float unit_interval_plus_one(uint32_t w) {
+    return __uint_as_float((w & 0x007FFFFFu) | 0x3F800000u);
 }
 
-// Box-Muller on one word pair: (r cos phi, r sin phi).
-__device__ __forceinline__ void box_muller(uint32_t wa, uint32_t wb, float& e_cos, float& e_sin) {
-    const float ua = uniform_open(wa);
-    const float ub = uniform_open(wb);                    // revolutions
-    // -2 ln u = (-2 ln 2) log2 u
-    const float r = __builtin_amdgcn_sqrtf(-1.38629436111989061883f * __builtin_amdgcn_logf(ua));
-    e_cos = r * __builtin_amdgcn_cosf(ub);
-    e_sin = r * __builtin_amdgcn_sinf(ub);
+// Box-Muller on one word pair, scaled: the pair's two normals times `scale`
+// are t * c and t * s.  t = scale sqrt(2 ln 2) sqrt(-log2 u) is returned
+// separately so the caller applies each normal with one FMA.
+// scale_k must be scale * kSqrt2Ln2.
+__device__ __forceinline__ void scaled_pair(uint32_t wa, uint32_t wb, float scale_k, float& t,
+                                            float& c, float& s) {
+    const float u = unit_interval_plus_one(wa) - 0x1.fffffep-1f;   // (m + 1/2) 2^-23, exact
+    const float turns = unit_interval_plus_one(wb);                // 1 + v: same sin / cos as v
+    t = scale_k * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u));
+    c = __builtin_amdgcn_cosf(turns);
+    s = __builtin_amdgcn_sinf(turns);
 }
 
 // The four normals of one Philox call, in element order 4q .. 4q+3.
 __device__ __forceinline__ void quad_normals(uint32_t q_lo, uint32_t q_hi, uint32_t tensor_id,
                                              uint32_t k0, uint32_t k1, float e[4]) {
     const Words w = philox4x32_10(q_lo, q_hi, tensor_id, kDomainNoise, k0, k1);
-    box_muller(w.w0, w.w1, e[0], e[1]);
-    box_muller(w.w2, w.w3, e[2], e[3]);
+    float t, c, s;
+    scaled_pair(w.w0, w.w1, kSqrt2Ln2, t, c, s);
+    e[0] = t * c;
+    e[1] = t * s;
+    scaled_pair(w.w2, w.w3, kSqrt2Ln2, t, c, s);
+    e[2] = t * c;
+    e[3] = t * s;
 }
 
 // bf16 <-> binary32.  A bf16 value is the high half of a binary32.

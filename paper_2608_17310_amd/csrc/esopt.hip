@@ -9,19 +9,25 @@
 // regenerate).
 //
 // Layout and launch shape:
-//   * A plan cuts every tensor into tiles of kTileElems = 4096 elements
-//     (256 lanes x 2 groups x 8 bf16) and numbers the tiles of all tensors
+//   * A plan cuts every tensor into tiles of T x U x 8 elements (T lanes per
+//     workgroup, U 8-element groups per lane; by default 256 x 8 x 8 =
+//     16384 elements, 32 KB) and numbers the tiles of all tensors
 //     consecutively.  One launch covers the whole parameter list: a grid of
 //     (CUs x WGs-per-CU) workgroups strides over the tiles.  Each workgroup
 //     keeps the index of its current tensor in a scalar register and
 //     advances it through a small tensor table read with scalar loads, so a
 //     tile's tensor, address and noise identity are wave-uniform.
 //   * Within a tile, lane l of group slot u owns elements
-//     8 (u * 256 + l) .. +7: one 16-byte load and one 16-byte store, 64
-//     lanes covering 1 KB contiguous per instruction.  Its two Philox calls
-//     are the quads 2 g and 2 g + 1 of that group; since tiles start at
-//     multiples of 4096 elements, the counter's high word is uniform per
-//     tile.
+//     8 (u * T + l) .. +7: one 16-byte load and one 16-byte store, 64 lanes
+//     covering 1 KB contiguous per instruction.  Its two Philox calls are
+//     the quads 2 g and 2 g + 1 of that group; since tiles start at
+//     multiples of a power-of-two tile size, the counter's high word is
+//     uniform per tile.
+//   * Perturb is HBM-bound: each lane issues all eight of its 16-byte loads
+//     before any arithmetic, and one workgroup per CU streams 32 KB tiles.
+//     The update is VALU-bound (N noise streams per element): 16 workgroups
+//     per CU keep every wave slot busy, one 8-element group per lane at a
+//     time.  Both shapes were chosen by sweeping on MI355X.
 //   * Perturb/restore read and write each parameter once (4 bytes of HBM
 //     traffic per parameter).  The update regenerates the noise of all
 //     distinct member seeds for the same 8 elements in registers,
@@ -41,17 +47,26 @@
 #include <vector>
 #include <algorithm>
 
+#ifndef ESOPT_SERIAL_GROUPS
+#define ESOPT_SERIAL_GROUPS 1
+#endif
 #include "../../include/esopt.h"
 #include "es_noise.hpp"
 
 namespace {
 
-constexpr int kBlock = 256;                 // lanes per workgroup (4 waves)
-constexpr int kGroupsPerLane = 2;           // 8-element groups per lane per tile
-constexpr int kGroupElems = 8;
-constexpr uint64_t kTileElems = uint64_t(kBlock) * kGroupsPerLane * kGroupElems;  // 4096
+constexpr int kAuxBlock = 256;              // lanes per workgroup of the small kernels
+constexpr int kGroupElems = 8;              // bf16 per lane-group (one 16-byte access)
 constexpr uint32_t kFlagAligned = 1u;       // tensor base is 16-byte aligned
-constexpr int kDefaultWgPerCu = 8;
+// Default tile shape and grids (measured on MI355X; see the launch-shape
+// notes above).  The update is VALU-bound and wants every wave slot filled;
+// perturb is HBM-bound and wants large contiguous per-CU streams.
+constexpr int kDefaultThreads = 256;
+constexpr int kDefaultGroups = 8;
+constexpr int kDefaultPerturbWgPerCu = 1;
+constexpr int kDefaultUpdateWgPerCu = 16;
+constexpr bool kSerialGroups = ESOPT_SERIAL_GROUPS;
+constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
 struct DevTensor {                          // 32 bytes, device tensor table entry
     uint16_t* data;
@@ -73,7 +88,7 @@ struct DistinctIn {                         // one distinct seed and its members
 };
 struct Member {                             // merged weight of one distinct seed
     uint32_t k0, k1;
-    float w;
+    float w_k;                              // weight times sqrt(2 ln 2)
     uint32_t pad;
 };
 struct UpdateHeader {
@@ -110,123 +125,176 @@ int hip_fail(hipError_t e, const char* what) {
 // Device code
 // ------------------------------------------------------------------------
 
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+// The tensor table holds generic pointers; every parameter lives in global
+// memory, and saying so lets the compiler use global_load / global_store
+// (vector-memory counters only) instead of flat accesses.
+#define ES_GLOBAL __attribute__((address_space(1)))
+
 // Load the 8 bf16 of one group (packed in 4 words).  Fast path: one 16-byte
-// load.  Checked path: element-wise 2-byte loads with bounds.
-template <bool kFast>
+// load (nontemporal when kNT: the parameters are streamed once per pass).
+// Checked path: element-wise 2-byte loads with bounds.
+template <bool kFast, bool kNT>
 __device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint64_t e,
                                            uint64_t numel, uint32_t raw[4]) {
     if constexpr (kFast) {
-        const uint4 v = *reinterpret_cast<const uint4*>(p + e);
+        const ES_GLOBAL u32x4_t* a = (const ES_GLOBAL u32x4_t*)(p + e);
+        const u32x4_t v = kNT ? __builtin_nontemporal_load(a) : *a;
         raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
     } else {
+        const ES_GLOBAL uint16_t* g = (const ES_GLOBAL uint16_t*)p;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const uint32_t lo = (e + 2 * k < numel) ? p[e + 2 * k] : 0u;
-            const uint32_t hi = (e + 2 * k + 1 < numel) ? p[e + 2 * k + 1] : 0u;
+            const uint32_t lo = (e + 2 * k < numel) ? g[e + 2 * k] : 0u;
+            const uint32_t hi = (e + 2 * k + 1 < numel) ? g[e + 2 * k + 1] : 0u;
             raw[k] = lo | (hi << 16);
         }
     }
 }
 
-template <bool kFast>
+template <bool kFast, bool kNT>
 __device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e, uint64_t numel,
                                             const uint32_t out[4]) {
     if constexpr (kFast) {
-        *reinterpret_cast<uint4*>(p + e) = make_uint4(out[0], out[1], out[2], out[3]);
+        ES_GLOBAL u32x4_t* a = (ES_GLOBAL u32x4_t*)(p + e);
+        const u32x4_t v = {out[0], out[1], out[2], out[3]};
+        if constexpr (kNT) __builtin_nontemporal_store(v, a);
+        else *a = v;
     } else {
+        ES_GLOBAL uint16_t* g = (ES_GLOBAL uint16_t*)p;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            if (e + 2 * k < numel) p[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
-            if (e + 2 * k + 1 < numel) p[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
+            if (e + 2 * k < numel) g[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
+            if (e + 2 * k + 1 < numel) g[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
         }
     }
 }
 
-// Normals of the 8 elements of a group starting at element 8 g (quads 2 g,
-// 2 g + 1; q_lo is even so q_lo + 1 does not carry into q_hi).
-__device__ __forceinline__ void group_normals(uint32_t q_lo, uint32_t q_hi, uint32_t tensor_id,
-                                              uint32_t k0, uint32_t k1, float e[8]) {
-    es::quad_normals(q_lo, q_hi, tensor_id, k0, k1, e);
-    es::quad_normals(q_lo + 1u, q_hi, tensor_id, k0, k1, e + 4);
+// The Philox words of the 8 elements of the group starting at element 8 g:
+// quads 2 g and 2 g + 1 (q_lo is even, so q_lo + 1 does not carry into q_hi).
+__device__ __forceinline__ void group_words(uint32_t q_lo, uint32_t q_hi, uint32_t tensor_id,
+                                            uint32_t k0, uint32_t k1, uint32_t w[8]) {
+    const es::Words a = es::philox4x32_10(q_lo, q_hi, tensor_id, es::kDomainNoise, k0, k1);
+    const es::Words b = es::philox4x32_10(q_lo + 1u, q_hi, tensor_id, es::kDomainNoise, k0, k1);
+    w[0] = a.w0; w[1] = a.w1; w[2] = a.w2; w[3] = a.w3;
+    w[4] = b.w0; w[5] = b.w1; w[6] = b.w2; w[7] = b.w3;
 }
 
-// One tile of perturb: theta <- RNE(fma(coef, eps, theta)), coef = sign * sigma.
-template <bool kFast>
+// x[k] += scale * eps_k for the 8 elements of a group, in binary32: each
+// Box-Muller pair (words 2p, 2p+1) feeds elements 2p (cos) and 2p+1 (sin);
+// scale_k = scale * sqrt(2 ln 2).
+__device__ __forceinline__ void group_axpy(const uint32_t w[8], float scale_k, float x[8]) {
+#pragma unroll
+    for (int p = 0; p < 4; ++p) {
+        float t, c, sn;
+        es::scaled_pair(w[2 * p], w[2 * p + 1], scale_k, t, c, sn);
+        x[2 * p] = __builtin_fmaf(t, c, x[2 * p]);
+        x[2 * p + 1] = __builtin_fmaf(t, sn, x[2 * p + 1]);
+    }
+}
+
+// Perturb one 8-element group in registers: x = theta + coef * eps, packed
+// back to bf16.
+__device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e, uint32_t q_hi,
+                                              uint32_t tensor_id, uint32_t k0, uint32_t k1,
+                                              float coef_k, uint32_t out[4]) {
+    uint32_t w[8];
+    group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, k0, k1, w);
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        x[2 * k] = es::bf16_lo(raw[k]);
+        x[2 * k + 1] = es::bf16_hi(raw[k]);
+    }
+    group_axpy(w, coef_k, x);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
+}
+
+// One tile of perturb: theta <- RNE(theta + coef * eps), coef = sign sigma,
+// one binary32 FMA per element.  Full aligned tiles issue all of the lane's
+// 16-byte loads first and then work group by group; partial or unaligned
+// tiles (tensor tails) go group by group with bounds-checked 2-byte accesses.
+template <int kThreads, int kU, bool kFast, bool kNT>
 __device__ __forceinline__ void perturb_tile(uint16_t* __restrict__ data, uint64_t numel,
                                              uint64_t elem0, uint32_t tensor_id,
-                                             uint32_t k0, uint32_t k1, float coef) {
+                                             uint32_t k0, uint32_t k1, float coef_k) {
     const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
-    uint32_t raw[kGroupsPerLane][4];
+    if constexpr (kFast) {
+        uint32_t raw[kU][4];
 #pragma unroll
-    for (int u = 0; u < kGroupsPerLane; ++u) {
-        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
-        load_group<kFast>(data, e, numel, raw[u]);
-    }
-#pragma unroll
-    for (int u = 0; u < kGroupsPerLane; ++u) {
-        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
-        float eps[8];
-        group_normals(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, k0, k1, eps);
-        uint32_t out[4];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float lo = __builtin_fmaf(coef, eps[2 * k], es::bf16_lo(raw[u][k]));
-            const float hi = __builtin_fmaf(coef, eps[2 * k + 1], es::bf16_hi(raw[u][k]));
-            out[k] = es::pack_bf16x2(lo, hi);
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            load_group<true, kNT>(data, e, numel, raw[u]);
         }
-        store_group<kFast>(data, e, numel, out);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            uint32_t out[4];
+            perturb_group(raw[u], e, q_hi, tensor_id, k0, k1, coef_k, out);
+            store_group<true, kNT>(data, e, numel, out);
+            // keep the groups' Philox chains from being interleaved: one
+            // group's registers at a time leaves room for more resident waves
+            if constexpr (kSerialGroups) __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            if (e >= numel) break;
+            uint32_t raw[4], out[4];
+            load_group<false, kNT>(data, e, numel, raw);
+            perturb_group(raw, e, q_hi, tensor_id, k0, k1, coef_k, out);
+            store_group<false, kNT>(data, e, numel, out);
+        }
     }
 }
 
-// One tile of the fused update: acc = sum_d w_d eps_d (binary32, members in
-// table order, zero weights skipped), theta <- RNE(theta + acc).
-template <bool kFast>
+// One tile of the fused update: for each of the lane's groups in turn,
+// load it, acc = sum_d w_d eps_d (binary32, members in table order, zero
+// weights skipped), theta <- RNE(theta + acc), store it.  The kernel is
+// VALU-bound, so one group's registers are live at a time and the wave count
+// (two 1024-lane workgroups per CU) hides the memory latency.
+template <int kThreads, int kU, bool kFast, bool kNT>
 __device__ __forceinline__ void update_tile(uint16_t* __restrict__ data, uint64_t numel,
                                             uint64_t elem0, uint32_t tensor_id,
                                             const Member* __restrict__ members,
                                             uint32_t n_distinct) {
     const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
-    uint32_t raw[kGroupsPerLane][4];
-    float acc[kGroupsPerLane][8];
+#pragma unroll 1
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        uint32_t raw[4];
+        load_group<kFast, kNT>(data, e, numel, raw);
+        const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
+        float acc[8];
 #pragma unroll
-    for (int u = 0; u < kGroupsPerLane; ++u) {
-        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
-        load_group<kFast>(data, e, numel, raw[u]);
-#pragma unroll
-        for (int k = 0; k < 8; ++k) acc[u][k] = 0.0f;
-    }
-    const uint32_t q_lo0 = static_cast<uint32_t>((elem0 >> 2) + uint64_t(threadIdx.x) * 2u);
-    for (uint32_t d = 0; d < n_distinct; ++d) {
-        const Member m = members[d];
-        if (m.w == 0.0f) continue;
-#pragma unroll
-        for (int u = 0; u < kGroupsPerLane; ++u) {
-            float eps[8];
-            group_normals(q_lo0 + uint32_t(u * kBlock * 2), q_hi, tensor_id, m.k0, m.k1, eps);
-#pragma unroll
-            for (int k = 0; k < 8; ++k) acc[u][k] = __builtin_fmaf(m.w, eps[k], acc[u][k]);
+        for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
+        for (uint32_t d = 0; d < n_distinct; ++d) {
+            const Member m = members[d];
+            if (m.w_k == 0.0f) continue;
+            uint32_t w[8];
+            group_words(q_lo, q_hi, tensor_id, m.k0, m.k1, w);
+            group_axpy(w, m.w_k, acc);
         }
-    }
-#pragma unroll
-    for (int u = 0; u < kGroupsPerLane; ++u) {
-        const uint64_t e = elem0 + uint64_t(u * kBlock + threadIdx.x) * kGroupElems;
         uint32_t out[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const float lo = es::bf16_lo(raw[u][k]) + acc[u][2 * k];
-            const float hi = es::bf16_hi(raw[u][k]) + acc[u][2 * k + 1];
+            const float lo = es::bf16_lo(raw[k]) + acc[2 * k];
+            const float hi = es::bf16_hi(raw[k]) + acc[2 * k + 1];
             out[k] = es::pack_bf16x2(lo, hi);
         }
-        store_group<kFast>(data, e, numel, out);
+        store_group<kFast, kNT>(data, e, numel, out);
     }
 }
 
 // Whole-parameter-list launch.  kUpdate selects the fused update (member
-// table + header written by es_prepare_kernel) over perturb (one key, coef).
-template <bool kUpdate>
-__global__ __launch_bounds__(kBlock) void es_tiles_kernel(const DevTensor* __restrict__ tab,
+// table + header written by es_prepare_kernel) over perturb (one key,
+// coef_k = sign sigma sqrt(2 ln 2)).
+template <int kThreads, int kU, bool kUpdate, bool kNT>
+__global__ __launch_bounds__(kThreads) void es_tiles_kernel(const DevTensor* __restrict__ tab,
                                                           uint64_t n_tiles, uint32_t k0,
-                                                          uint32_t k1, float coef,
+                                                          uint32_t k1, float coef_k,
                                                           const Member* __restrict__ members,
                                                           const UpdateHeader* __restrict__ hdr) {
     uint32_t n_distinct = 0;
@@ -240,14 +308,15 @@ __global__ __launch_bounds__(kBlock) void es_tiles_kernel(const DevTensor* __res
         uint16_t* const data = tab[t].data;
         const uint64_t numel = tab[t].numel;
         const uint32_t tensor_id = tab[t].tensor_id;
+        constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
         const uint64_t elem0 = (tile - tab[t].first_tile) * kTileElems;
         const bool fast = (tab[t].flags & kFlagAligned) && (elem0 + kTileElems <= numel);
         if constexpr (kUpdate) {
-            if (fast) update_tile<true>(data, numel, elem0, tensor_id, members, n_distinct);
-            else      update_tile<false>(data, numel, elem0, tensor_id, members, n_distinct);
+            if (fast) update_tile<kThreads, kU, true, kNT>(data, numel, elem0, tensor_id, members, n_distinct);
+            else      update_tile<kThreads, kU, false, kNT>(data, numel, elem0, tensor_id, members, n_distinct);
         } else {
-            if (fast) perturb_tile<true>(data, numel, elem0, tensor_id, k0, k1, coef);
-            else      perturb_tile<false>(data, numel, elem0, tensor_id, k0, k1, coef);
+            if (fast) perturb_tile<kThreads, kU, true, kNT>(data, numel, elem0, tensor_id, k0, k1, coef_k);
+            else      perturb_tile<kThreads, kU, false, kNT>(data, numel, elem0, tensor_id, k0, k1, coef_k);
         }
     }
 }
@@ -255,7 +324,7 @@ __global__ __launch_bounds__(kBlock) void es_tiles_kernel(const DevTensor* __res
 // Copy up to 1 KB of host-packed words (passed as kernel arguments) into
 // device scratch: how es_update hands its member tables to the device
 // without a host-side staging buffer or synchronisation.
-__global__ __launch_bounds__(kBlock) void es_stage_kernel(uint32_t* __restrict__ dst,
+__global__ __launch_bounds__(kAuxBlock) void es_stage_kernel(uint32_t* __restrict__ dst,
                                                           uint32_t n_words, StageChunk chunk) {
     for (uint32_t i = threadIdx.x; i < n_words; i += blockDim.x) dst[i] = chunk.words[i];
 }
@@ -355,7 +424,7 @@ __global__ __launch_bounds__(64) void es_prepare_kernel(
         double w = 0.0;
         for (uint32_t m = di.first; m < di.first + di.count; ++m)
             w += c * static_cast<double>(min[m].sign) * z[min[m].reward_index];
-        const float wf = status ? 0.0f : static_cast<float>(w);
+        const float wf = status ? 0.0f : static_cast<float>(w * kSqrt2Ln2Double);
         out[d] = Member{di.k0, di.k1, wf, 0u};
         live += (wf != 0.0f) ? 1u : 0u;
     }
@@ -367,7 +436,7 @@ __global__ __launch_bounds__(64) void es_prepare_kernel(
     }
 }
 
-__global__ __launch_bounds__(kBlock) void es_philox_words_kernel(uint32_t k0, uint32_t k1,
+__global__ __launch_bounds__(kAuxBlock) void es_philox_words_kernel(uint32_t k0, uint32_t k1,
                                                                  uint32_t tensor_id, uint32_t domain,
                                                                  uint64_t quad0, uint64_t n_quads,
                                                                  uint4* __restrict__ out) {
@@ -379,7 +448,7 @@ __global__ __launch_bounds__(kBlock) void es_philox_words_kernel(uint32_t k0, ui
     out[i] = make_uint4(w.w0, w.w1, w.w2, w.w3);
 }
 
-__global__ __launch_bounds__(kBlock) void es_normals_kernel(uint32_t k0, uint32_t k1,
+__global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint32_t k1,
                                                             uint32_t tensor_id, uint64_t elem0,
                                                             uint64_t n, float* __restrict__ out) {
     const uint64_t q = (elem0 >> 2) + uint64_t(blockIdx.x) * blockDim.x + threadIdx.x;
@@ -393,6 +462,33 @@ __global__ __launch_bounds__(kBlock) void es_normals_kernel(uint32_t k0, uint32_
     }
 }
 
+using TilesKernel = void (*)(const DevTensor*, uint64_t, uint32_t, uint32_t, float, const Member*,
+                             const UpdateHeader*);
+
+// Tile shapes instantiated: T lanes per workgroup x U groups per lane.
+template <bool kUpdate, bool kNT>
+TilesKernel tiles_kernel_for(int threads, int groups) {
+    switch (threads * 16 + groups) {
+        case 256 * 16 + 2: return es_tiles_kernel<256, 2, kUpdate, kNT>;
+        case 256 * 16 + 4: return es_tiles_kernel<256, 4, kUpdate, kNT>;
+        case 512 * 16 + 2: return es_tiles_kernel<512, 2, kUpdate, kNT>;
+        case 512 * 16 + 4: return es_tiles_kernel<512, 4, kUpdate, kNT>;
+        case 1024 * 16 + 2: return es_tiles_kernel<1024, 2, kUpdate, kNT>;
+        case 1024 * 16 + 4: return es_tiles_kernel<1024, 4, kUpdate, kNT>;
+        case 256 * 16 + 8: return es_tiles_kernel<256, 8, kUpdate, kNT>;
+        case 512 * 16 + 8: return es_tiles_kernel<512, 8, kUpdate, kNT>;
+        case 1024 * 16 + 8: return es_tiles_kernel<1024, 8, kUpdate, kNT>;
+        default: return nullptr;
+    }
+}
+
+TilesKernel tiles_kernel(bool update, bool nt, int threads, int groups) {
+    if (update) return nt ? tiles_kernel_for<true, true>(threads, groups)
+                          : tiles_kernel_for<true, false>(threads, groups);
+    return nt ? tiles_kernel_for<false, true>(threads, groups)
+              : tiles_kernel_for<false, false>(threads, groups);
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------------
@@ -404,12 +500,25 @@ struct es_plan {
     uint32_t n_tensors = 0;
     uint64_t numel = 0;
     uint64_t n_tiles = 0;
-    uint32_t grid = 0;
+    uint32_t grid_perturb = 0;      // workgroups of the perturb / restore launch
+    uint32_t grid_update = 0;       // workgroups of the update launch
+    int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
+    int groups = kDefaultGroups;    // 8-element groups per lane per tile
+    uint64_t tile_elems = 0;        // threads * groups * 8
+    bool nontemporal = true;        // streaming (nontemporal) 16-byte loads and stores
     DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
 
 namespace {
+
+// Integer from the environment within [lo, hi], else the default.
+int env_int(const char* name, int dflt, int lo, int hi) {
+    const char* v = std::getenv(name);
+    if (v == nullptr) return dflt;
+    const int x = std::atoi(v);
+    return (x >= lo && x <= hi) ? x : dflt;
+}
 
 int check_device(const es_plan_t* p) {
     int dev = -1;
@@ -422,11 +531,13 @@ int check_device(const es_plan_t* p) {
     return ES_OK;
 }
 
-int launch_perturb(es_plan_t* p, uint64_t seed, float coef, hipStream_t s) {
+int launch_perturb(es_plan_t* p, uint64_t seed, double coef, hipStream_t s) {
     if (p->n_tiles == 0) return ES_OK;
-    hipLaunchKernelGGL(es_tiles_kernel<false>, dim3(p->grid), dim3(kBlock), 0, s, p->d_tab,
-                       p->n_tiles, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
-                       coef, nullptr, nullptr);
+    const float coef_k = static_cast<float>(coef * kSqrt2Ln2Double);
+    TilesKernel kernel = tiles_kernel(false, p->nontemporal, p->threads, p->groups);
+    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_tiles,
+                       static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), coef_k,
+                       nullptr, nullptr);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<perturb> launch");
     return ES_OK;
@@ -442,7 +553,8 @@ int perturb_impl(es_plan_t* p, uint64_t seed, int32_t sign, float sigma, es_stre
     if (sigma == 0.0f) return ES_OK;
     const int rc = check_device(p);
     if (rc != ES_OK) return rc;
-    return launch_perturb(p, seed, sign > 0 ? sigma : -sigma, static_cast<hipStream_t>(stream));
+    return launch_perturb(p, seed, sign > 0 ? double(sigma) : -double(sigma),
+                          static_cast<hipStream_t>(stream));
 }
 
 }  // namespace
@@ -455,6 +567,14 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null tensor list");
     if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
         return fail(ES_ERR_INVALID_ARG, "es_plan_create: n_tensors out of range");
+    // Launch shape: the defaults, or overrides for launch-shape sweeps.
+    int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
+    int groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
+    if (tiles_kernel(false, true, threads, groups) == nullptr) {
+        threads = kDefaultThreads;
+        groups = kDefaultGroups;
+    }
+    const uint64_t tile_elems = uint64_t(threads) * groups * kGroupElems;
     std::vector<DevTensor> tab(n_tensors + 1);
     std::unordered_map<uint32_t, uint32_t> ids;
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
@@ -469,7 +589,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         if (t.numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, where + ": numel too large");
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
         if (t.numel > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
-        const uint64_t nt = (t.numel + kTileElems - 1) / kTileElems;
+        const uint64_t nt = (t.numel + tile_elems - 1) / tile_elems;
         tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, tiles, t.tensor_id,
                            (a % 16 == 0) ? kFlagAligned : 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
@@ -489,16 +609,18 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     int cus = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
-    int wg_per_cu = kDefaultWgPerCu;
-    if (const char* env = std::getenv("ESOPT_WG_PER_CU")) {
-        const int v = std::atoi(env);
-        if (v >= 1 && v <= 64) wg_per_cu = v;
-    }
+    const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
+    const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
+    p->nontemporal = env_int("ESOPT_NONTEMPORAL", 1, 0, 1) != 0;
+    p->threads = threads;
+    p->groups = groups;
+    p->tile_elems = tile_elems;
     p->n_tensors = n_tensors;
     p->numel = numel;
     p->n_tiles = tiles;
-    p->grid = static_cast<uint32_t>(std::min<uint64_t>(tiles, uint64_t(cus) * wg_per_cu));
-    if (p->grid == 0) p->grid = 1;
+    const uint64_t cap = std::max<uint64_t>(tiles, 1);
+    p->grid_perturb = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_perturb));
+    p->grid_update = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_update));
     e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(DevTensor) * tab.size());
     if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
     e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
@@ -611,7 +733,7 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
             StageChunk chunk;
             const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
             std::memcpy(chunk.words, words + w0, nw * 4);
-            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kBlock), 0, s,
+            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s,
                                reinterpret_cast<uint32_t*>(plan->d_scratch + dst_off) + w0, nw, chunk);
             const hipError_t e = hipGetLastError();
             if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
@@ -634,8 +756,10 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
     if (plan->n_tiles == 0) return ES_OK;
-    hipLaunchKernelGGL(es_tiles_kernel<true>, dim3(plan->grid), dim3(kBlock), 0, s, plan->d_tab,
-                       plan->n_tiles, 0u, 0u, 0.0f, members, hdr);
+    TilesKernel kernel = tiles_kernel(true, plan->nontemporal, plan->threads, plan->groups);
+    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
+                       plan->n_tiles,
+                       0u, 0u, 0.0f, members, hdr);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<update> launch");
     return ES_OK;
@@ -653,8 +777,8 @@ int es_philox_words(uint64_t seed, uint32_t tensor_id, uint32_t domain, uint64_t
     if (reinterpret_cast<uintptr_t>(out_dev) % 16 != 0)
         return fail(ES_ERR_ALIGN, "es_philox_words: output not 16-byte aligned");
     if (n_quads == 0) return ES_OK;
-    const uint32_t blocks = static_cast<uint32_t>((n_quads + kBlock - 1) / kBlock);
-    hipLaunchKernelGGL(es_philox_words_kernel, dim3(blocks), dim3(kBlock), 0,
+    const uint32_t blocks = static_cast<uint32_t>((n_quads + kAuxBlock - 1) / kAuxBlock);
+    hipLaunchKernelGGL(es_philox_words_kernel, dim3(blocks), dim3(kAuxBlock), 0,
                        static_cast<hipStream_t>(stream), static_cast<uint32_t>(seed),
                        static_cast<uint32_t>(seed >> 32), tensor_id, domain, quad0, n_quads,
                        reinterpret_cast<uint4*>(out_dev));
@@ -670,8 +794,8 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, fl
     if (elem0 > (uint64_t(1) << 62) - n) return fail(ES_ERR_INVALID_ARG, "es_normals: element range beyond 2^62");
     if (n == 0) return ES_OK;
     const uint64_t quads = ((elem0 + n - 1) >> 2) - (elem0 >> 2) + 1;
-    const uint32_t blocks = static_cast<uint32_t>((quads + kBlock - 1) / kBlock);
-    hipLaunchKernelGGL(es_normals_kernel, dim3(blocks), dim3(kBlock), 0,
+    const uint32_t blocks = static_cast<uint32_t>((quads + kAuxBlock - 1) / kAuxBlock);
+    hipLaunchKernelGGL(es_normals_kernel, dim3(blocks), dim3(kAuxBlock), 0,
                        static_cast<hipStream_t>(stream), static_cast<uint32_t>(seed),
                        static_cast<uint32_t>(seed >> 32), tensor_id, elem0, n, out_dev);
     const hipError_t e = hipGetLastError();
