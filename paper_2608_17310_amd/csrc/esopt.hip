@@ -10,10 +10,11 @@
 //
 // Layout and launch shape:
 //   * A plan cuts every tensor into tiles of T x U x 8 elements (T lanes per
-//     workgroup, U 8-element groups per lane; by default 256 x 8 x 8 =
-//     16384 elements, 32 KB) and numbers the tiles of all tensors
-//     consecutively.  One launch covers the whole parameter list: a grid of
-//     (CUs x WGs-per-CU) workgroups strides over the tiles.  Each workgroup
+//     workgroup, U 8-element groups per lane; by default 1024 x 8 x 8 =
+//     65536 elements, 128 KB) and numbers the full tiles of all tensors
+//     consecutively, then the tail tiles (partial or unaligned).  One launch
+//     covers the whole parameter list: a grid of (CUs x WGs-per-CU)
+//     workgroups strides over the full tiles, then the tails.  Each workgroup
 //     keeps the index of its current tensor in a scalar register and
 //     advances it through a small tensor table read with scalar loads, so a
 //     tile's tensor, address and noise identity are wave-uniform.
@@ -23,11 +24,13 @@
 //     the quads 2 g and 2 g + 1 of that group; since tiles start at
 //     multiples of a power-of-two tile size, the counter's high word is
 //     uniform per tile.
-//   * Perturb is HBM-bound: each lane issues all eight of its 16-byte loads
-//     before any arithmetic, and one workgroup per CU streams 32 KB tiles.
-//     The update is VALU-bound (N noise streams per element): 16 workgroups
-//     per CU keep every wave slot busy, one 8-element group per lane at a
-//     time.  Both shapes were chosen by sweeping on MI355X.
+//   * Perturb is HBM-bound: one 1024-lane workgroup per CU streams 128 KB
+//     tiles; the loads of its next tile are issued before the current tile's
+//     arithmetic (software pipelining), and each tile's stores leave in one
+//     burst after all its arithmetic.  The update is VALU-bound (N noise
+//     streams per element): four workgroups per CU keep every wave slot busy,
+//     one 8-element group per lane at a time.  Both shapes were chosen by
+//     sweeping on MI355X.
 //   * Perturb/restore read and write each parameter once (4 bytes of HBM
 //     traffic per parameter).  The update regenerates the noise of all
 //     distinct member seeds for the same 8 elements in registers,
@@ -47,9 +50,6 @@
 #include <vector>
 #include <algorithm>
 
-#ifndef ESOPT_SERIAL_GROUPS
-#define ESOPT_SERIAL_GROUPS 1
-#endif
 #include "../../include/esopt.h"
 #include "es_noise.hpp"
 
@@ -57,25 +57,29 @@ namespace {
 
 constexpr int kAuxBlock = 256;              // lanes per workgroup of the small kernels
 constexpr int kGroupElems = 8;              // bf16 per lane-group (one 16-byte access)
-constexpr uint32_t kFlagAligned = 1u;       // tensor base is 16-byte aligned
 // Default tile shape and grids (measured on MI355X; see the launch-shape
 // notes above).  The update is VALU-bound and wants every wave slot filled;
 // perturb is HBM-bound and wants large contiguous per-CU streams.
-constexpr int kDefaultThreads = 256;
+constexpr int kDefaultThreads = 1024;
 constexpr int kDefaultGroups = 8;
 constexpr int kDefaultPerturbWgPerCu = 1;
-constexpr int kDefaultUpdateWgPerCu = 16;
-constexpr bool kSerialGroups = ESOPT_SERIAL_GROUPS;
+constexpr int kDefaultUpdateWgPerCu = 4;
 constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
-struct DevTensor {                          // 32 bytes, device tensor table entry
+// Device tensor table entry.  Tiles are numbered in two sequences: full
+// tiles (16-byte aligned, entirely inside the tensor) and tail tiles (the
+// partial last tile, or every tile of a tensor whose base is not 16-byte
+// aligned).  A sentinel entry closes both sequences.
+struct DevTensor {
     uint16_t* data;
     uint64_t numel;
-    uint64_t first_tile;                    // global index of the tensor's tile 0
+    uint64_t first_full;                    // global index of the tensor's first full tile
+    uint64_t first_tail;                    // global index of its first tail tile
     uint32_t tensor_id;
-    uint32_t flags;
+    uint32_t pad0;
+    uint64_t pad1;
 };
-static_assert(sizeof(DevTensor) == 32, "tensor table entry layout");
+static_assert(sizeof(DevTensor) == 48, "tensor table entry layout");
 
 struct MemberIn {                           // one population member, CSR order
     uint32_t reward_index;
@@ -211,61 +215,169 @@ __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e,
     for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
 }
 
-// One tile of perturb: theta <- RNE(theta + coef * eps), coef = sign sigma,
-// one binary32 FMA per element.  Full aligned tiles issue all of the lane's
-// 16-byte loads first and then work group by group; partial or unaligned
-// tiles (tensor tails) go group by group with bounds-checked 2-byte accesses.
-template <int kThreads, int kU, bool kFast, bool kNT>
-__device__ __forceinline__ void perturb_tile(uint16_t* __restrict__ data, uint64_t numel,
-                                             uint64_t elem0, uint32_t tensor_id,
-                                             uint32_t k0, uint32_t k1, float coef_k) {
-    const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
-    if constexpr (kFast) {
-        uint32_t raw[kU][4];
+// A tile: kThreads * kU * 8 consecutive elements of one tensor.
+struct TileRef {
+    uint16_t* data;
+    uint64_t numel;
+    uint64_t elem0;
+    uint32_t tensor_id;
+};
+
+// Tile lookup.  A workgroup's tiles increase monotonically, so its table
+// index t only moves forward; t, the table entries and the tile are
+// wave-uniform (scalar registers and scalar loads).
+template <uint64_t kTileElems>
+__device__ __forceinline__ TileRef locate_full(const DevTensor* __restrict__ tab, uint32_t& t,
+                                               uint64_t tile) {
+    while (tile >= tab[t + 1].first_full) ++t;
+    return TileRef{tab[t].data, tab[t].numel, (tile - tab[t].first_full) * kTileElems,
+                   tab[t].tensor_id};
+}
+
+template <uint64_t kTileElems>
+__device__ __forceinline__ TileRef locate_tail(const DevTensor* __restrict__ tab, uint32_t& t,
+                                               uint64_t tile) {
+    while (tile >= tab[t + 1].first_tail) ++t;
+    const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
+    return TileRef{tab[t].data, tab[t].numel, (n_full + tile - tab[t].first_tail) * kTileElems,
+                   tab[t].tensor_id};
+}
+
+template <int kThreads, int kU, bool kNT>
+__device__ __forceinline__ void load_tile(const TileRef& r, uint32_t raw[kU][4]) {
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        load_group<true, kNT>(r.data, e, r.numel, raw[u]);
+    }
+}
+
+// Perturb a full tile whose groups are already in registers.  With kBurst
+// every group is computed first and the tile's stores then leave as one
+// burst: on MI355X an in-place stream whose writes come in per-tile bursts
+// sustains ~6.2 TB/s, against ~5.5 TB/s when each group's store is
+// interleaved with the next group's arithmetic.
+template <int kThreads, int kU, bool kNT, bool kBurst>
+__device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU][4],
+                                               uint32_t k0, uint32_t k1, float coef_k) {
+    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    if constexpr (kBurst) {
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            load_group<true, kNT>(data, e, numel, raw[u]);
-        }
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
             uint32_t out[4];
-            perturb_group(raw[u], e, q_hi, tensor_id, k0, k1, coef_k, out);
-            store_group<true, kNT>(data, e, numel, out);
-            // keep the groups' Philox chains from being interleaved: one
-            // group's registers at a time leaves room for more resident waves
-            if constexpr (kSerialGroups) __builtin_amdgcn_sched_barrier(0);
+            perturb_group(raw[u], e, q_hi, r.tensor_id, k0, k1, coef_k, out);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) raw[u][k] = out[k];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            store_group<true, kNT>(r.data, e, r.numel, raw[u]);
         }
     } else {
-#pragma unroll 1
+#pragma unroll
         for (int u = 0; u < kU; ++u) {
-            const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            if (e >= numel) break;
-            uint32_t raw[4], out[4];
-            load_group<false, kNT>(data, e, numel, raw);
-            perturb_group(raw, e, q_hi, tensor_id, k0, k1, coef_k, out);
-            store_group<false, kNT>(data, e, numel, out);
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            uint32_t out[4];
+            perturb_group(raw[u], e, q_hi, r.tensor_id, k0, k1, coef_k, out);
+            store_group<true, kNT>(r.data, e, r.numel, out);
         }
     }
+}
+
+// Perturb a tail tile group by group with bounds-checked 2-byte accesses.
+template <int kThreads, int kU, bool kNT>
+__device__ __forceinline__ void perturb_tail(const TileRef& r, uint32_t k0, uint32_t k1,
+                                             float coef_k) {
+    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+#pragma unroll 1
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        if (e >= r.numel) break;
+        uint32_t raw[4], out[4];
+        load_group<false, kNT>(r.data, e, r.numel, raw);
+        perturb_group(raw, e, q_hi, r.tensor_id, k0, k1, coef_k, out);
+        store_group<false, kNT>(r.data, e, r.numel, out);
+    }
+}
+
+// One software-pipeline step over full tiles: issue the 16-byte loads of the
+// workgroup's next tile into `next_buf`, then perturb the current tile from
+// `cur_buf`, so the memory pipe does not idle through the Philox /
+// Box-Muller arithmetic.  Returns true when the workgroup has no next tile.
+template <int kThreads, int kU, bool kNT, bool kBurst>
+__device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, uint32_t& t,
+                                             uint64_t& tile, uint64_t n_full, TileRef& cur,
+                                             uint32_t cur_buf[kU][4], uint32_t next_buf[kU][4],
+                                             uint32_t k0, uint32_t k1, float coef_k) {
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
+    const uint64_t next = tile + gridDim.x;
+    const bool more = next < n_full;
+    TileRef nxt = cur;
+    if (more) {
+        nxt = locate_full<kTileElems>(tab, t, next);
+        load_tile<kThreads, kU, kNT>(nxt, next_buf);
+    }
+    perturb_loaded<kThreads, kU, kNT, kBurst>(cur, cur_buf, k0, k1, coef_k);
+    if (!more) return true;
+    tile = next;
+    cur = nxt;
+    return false;
+}
+
+// Perturb over the whole parameter list: full tiles first (16-byte accesses,
+// software-pipelined when kPipelined; two register buffers alternate, the
+// loop unrolled twice), then tail tiles.  coef_k = sign sigma sqrt(2 ln 2).
+template <int kThreads, int kU, bool kPipelined, bool kBurst>
+__global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* __restrict__ tab,
+                                                              uint64_t n_full, uint64_t n_tail,
+                                                              uint32_t k0, uint32_t k1,
+                                                              float coef_k) {
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
+    constexpr bool kNT = true;
+    if constexpr (kPipelined) {
+        uint64_t tile = blockIdx.x;
+        if (tile < n_full) {
+            uint32_t t = 0;
+            TileRef cur = locate_full<kTileElems>(tab, t, tile);
+            uint32_t a[kU][4], b[kU][4];
+            load_tile<kThreads, kU, kNT>(cur, a);
+            for (;;) {
+                if (perturb_step<kThreads, kU, kNT, kBurst>(tab, t, tile, n_full, cur, a, b, k0, k1, coef_k)) break;
+                if (perturb_step<kThreads, kU, kNT, kBurst>(tab, t, tile, n_full, cur, b, a, k0, k1, coef_k)) break;
+            }
+        }
+    } else {
+        uint32_t t = 0;
+        for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
+            const TileRef r = locate_full<kTileElems>(tab, t, tile);
+            uint32_t raw[kU][4];
+            load_tile<kThreads, kU, kNT>(r, raw);
+            perturb_loaded<kThreads, kU, kNT, kBurst>(r, raw, k0, k1, coef_k);
+        }
+    }
+    uint32_t t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
+        perturb_tail<kThreads, kU, kNT>(locate_tail<kTileElems>(tab, t, tile), k0, k1, coef_k);
 }
 
 // One tile of the fused update: for each of the lane's groups in turn,
 // load it, acc = sum_d w_d eps_d (binary32, members in table order, zero
 // weights skipped), theta <- RNE(theta + acc), store it.  The kernel is
-// VALU-bound, so one group's registers are live at a time and the wave count
-// (two 1024-lane workgroups per CU) hides the memory latency.
+// VALU-bound, so one group's registers are live at a time and the number of
+// resident waves hides the memory latency.
 template <int kThreads, int kU, bool kFast, bool kNT>
-__device__ __forceinline__ void update_tile(uint16_t* __restrict__ data, uint64_t numel,
-                                            uint64_t elem0, uint32_t tensor_id,
-                                            const Member* __restrict__ members,
+__device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct) {
-    const uint32_t q_hi = static_cast<uint32_t>(elem0 >> 34);
+    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
-        const uint64_t e = elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        if (!kFast && e >= r.numel) break;
         uint32_t raw[4];
-        load_group<kFast, kNT>(data, e, numel, raw);
+        load_group<kFast, kNT>(r.data, e, r.numel, raw);
         const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
         float acc[8];
 #pragma unroll
@@ -274,7 +386,7 @@ __device__ __forceinline__ void update_tile(uint16_t* __restrict__ data, uint64_
             const Member m = members[d];
             if (m.w_k == 0.0f) continue;
             uint32_t w[8];
-            group_words(q_lo, q_hi, tensor_id, m.k0, m.k1, w);
+            group_words(q_lo, q_hi, r.tensor_id, m.k0, m.k1, w);
             group_axpy(w, m.w_k, acc);
         }
         uint32_t out[4];
@@ -284,41 +396,26 @@ __device__ __forceinline__ void update_tile(uint16_t* __restrict__ data, uint64_
             const float hi = es::bf16_hi(raw[k]) + acc[2 * k + 1];
             out[k] = es::pack_bf16x2(lo, hi);
         }
-        store_group<kFast, kNT>(data, e, numel, out);
+        store_group<kFast, kNT>(r.data, e, r.numel, out);
     }
 }
 
-// Whole-parameter-list launch.  kUpdate selects the fused update (member
-// table + header written by es_prepare_kernel) over perturb (one key,
-// coef_k = sign sigma sqrt(2 ln 2)).
-template <int kThreads, int kU, bool kUpdate, bool kNT>
-__global__ __launch_bounds__(kThreads) void es_tiles_kernel(const DevTensor* __restrict__ tab,
-                                                          uint64_t n_tiles, uint32_t k0,
-                                                          uint32_t k1, float coef_k,
-                                                          const Member* __restrict__ members,
-                                                          const UpdateHeader* __restrict__ hdr) {
-    uint32_t n_distinct = 0;
-    if constexpr (kUpdate) {
-        if (hdr->n_live == 0u) return;      // nothing to add: theta is not written
-        n_distinct = hdr->n_distinct;
-    }
+// Fused update over the whole parameter list (member table and header
+// written by es_prepare_kernel): full tiles, then tail tiles.
+template <int kThreads, int kU, bool kNT>
+__global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTensor* __restrict__ tab,
+                                                             uint64_t n_full, uint64_t n_tail,
+                                                             const Member* __restrict__ members,
+                                                             const UpdateHeader* __restrict__ hdr) {
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
+    if (hdr->n_live == 0u) return;          // nothing to add: theta is not written
+    const uint32_t n_distinct = hdr->n_distinct;
     uint32_t t = 0;
-    for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
-        while (tile >= tab[t + 1].first_tile) ++t;      // sentinel ends the table
-        uint16_t* const data = tab[t].data;
-        const uint64_t numel = tab[t].numel;
-        const uint32_t tensor_id = tab[t].tensor_id;
-        constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
-        const uint64_t elem0 = (tile - tab[t].first_tile) * kTileElems;
-        const bool fast = (tab[t].flags & kFlagAligned) && (elem0 + kTileElems <= numel);
-        if constexpr (kUpdate) {
-            if (fast) update_tile<kThreads, kU, true, kNT>(data, numel, elem0, tensor_id, members, n_distinct);
-            else      update_tile<kThreads, kU, false, kNT>(data, numel, elem0, tensor_id, members, n_distinct);
-        } else {
-            if (fast) perturb_tile<kThreads, kU, true, kNT>(data, numel, elem0, tensor_id, k0, k1, coef_k);
-            else      perturb_tile<kThreads, kU, false, kNT>(data, numel, elem0, tensor_id, k0, k1, coef_k);
-        }
-    }
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
+        update_tile<kThreads, kU, true, kNT>(locate_full<kTileElems>(tab, t, tile), members, n_distinct);
+    t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
+        update_tile<kThreads, kU, false, kNT>(locate_tail<kTileElems>(tab, t, tile), members, n_distinct);
 }
 
 // Copy up to 1 KB of host-packed words (passed as kernel arguments) into
@@ -395,7 +492,7 @@ __global__ __launch_bounds__(64) void es_zscore_kernel(const float* __restrict__
 
 // z-score (or rewards as weights), then one merged weight per distinct seed:
 // w_d = sum over its members (in member order) of c * sign * zhat, fp64,
-// stored as binary32 with the seed's key for es_tiles_kernel<true>.
+// stored as binary32 with the seed's key for es_update_kernel.
 __global__ __launch_bounds__(64) void es_prepare_kernel(
     const float* __restrict__ r, uint32_t n, double eps, uint32_t flags, double c,
     const MemberIn* __restrict__ min, const DistinctIn* __restrict__ din, uint32_t n_distinct,
@@ -462,31 +559,34 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
     }
 }
 
-using TilesKernel = void (*)(const DevTensor*, uint64_t, uint32_t, uint32_t, float, const Member*,
-                             const UpdateHeader*);
+using PerturbKernel = void (*)(const DevTensor*, uint64_t, uint64_t, uint32_t, uint32_t, float);
+using UpdateKernel = void (*)(const DevTensor*, uint64_t, uint64_t, const Member*,
+                              const UpdateHeader*);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
-template <bool kUpdate, bool kNT>
-TilesKernel tiles_kernel_for(int threads, int groups) {
-    switch (threads * 16 + groups) {
-        case 256 * 16 + 2: return es_tiles_kernel<256, 2, kUpdate, kNT>;
-        case 256 * 16 + 4: return es_tiles_kernel<256, 4, kUpdate, kNT>;
-        case 512 * 16 + 2: return es_tiles_kernel<512, 2, kUpdate, kNT>;
-        case 512 * 16 + 4: return es_tiles_kernel<512, 4, kUpdate, kNT>;
-        case 1024 * 16 + 2: return es_tiles_kernel<1024, 2, kUpdate, kNT>;
-        case 1024 * 16 + 4: return es_tiles_kernel<1024, 4, kUpdate, kNT>;
-        case 256 * 16 + 8: return es_tiles_kernel<256, 8, kUpdate, kNT>;
-        case 512 * 16 + 8: return es_tiles_kernel<512, 8, kUpdate, kNT>;
-        case 1024 * 16 + 8: return es_tiles_kernel<1024, 8, kUpdate, kNT>;
-        default: return nullptr;
-    }
+#define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
+
+template <bool kPipelined, bool kBurst>
+PerturbKernel perturb_kernel_for(int threads, int groups) {
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_perturb_kernel<T, U, kPipelined, kBurst>;
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
 }
 
-TilesKernel tiles_kernel(bool update, bool nt, int threads, int groups) {
-    if (update) return nt ? tiles_kernel_for<true, true>(threads, groups)
-                          : tiles_kernel_for<true, false>(threads, groups);
-    return nt ? tiles_kernel_for<false, true>(threads, groups)
-              : tiles_kernel_for<false, false>(threads, groups);
+PerturbKernel perturb_kernel(bool pipelined, bool burst, int threads, int groups) {
+    if (burst) return pipelined ? perturb_kernel_for<true, true>(threads, groups)
+                                : perturb_kernel_for<false, true>(threads, groups);
+    return pipelined ? perturb_kernel_for<true, false>(threads, groups)
+                     : perturb_kernel_for<false, false>(threads, groups);
+}
+
+UpdateKernel update_kernel(int threads, int groups) {
+#define ES_CASE(T, U) \
+    if (threads == T && groups == U) return es_update_kernel<T, U, true>;
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
 }
 
 }  // namespace
@@ -499,13 +599,15 @@ struct es_plan {
     int device = -1;
     uint32_t n_tensors = 0;
     uint64_t numel = 0;
-    uint64_t n_tiles = 0;
+    uint64_t n_full = 0;            // full tiles (16-byte path)
+    uint64_t n_tail = 0;            // tail tiles (bounds-checked path)
     uint32_t grid_perturb = 0;      // workgroups of the perturb / restore launch
     uint32_t grid_update = 0;       // workgroups of the update launch
     int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
     int groups = kDefaultGroups;    // 8-element groups per lane per tile
     uint64_t tile_elems = 0;        // threads * groups * 8
-    bool nontemporal = true;        // streaming (nontemporal) 16-byte loads and stores
+    bool pipelined = true;          // perturb prefetches the next full tile
+    bool burst = true;              // perturb stores each tile in one burst
     DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
@@ -532,14 +634,14 @@ int check_device(const es_plan_t* p) {
 }
 
 int launch_perturb(es_plan_t* p, uint64_t seed, double coef, hipStream_t s) {
-    if (p->n_tiles == 0) return ES_OK;
+    if (p->n_full + p->n_tail == 0) return ES_OK;
     const float coef_k = static_cast<float>(coef * kSqrt2Ln2Double);
-    TilesKernel kernel = tiles_kernel(false, p->nontemporal, p->threads, p->groups);
-    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_tiles,
-                       static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32), coef_k,
-                       nullptr, nullptr);
+    const PerturbKernel kernel = perturb_kernel(p->pipelined, p->burst, p->threads, p->groups);
+    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_full,
+                       p->n_tail, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                       coef_k);
     const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<perturb> launch");
+    if (e != hipSuccess) return hip_fail(e, "es_perturb_kernel launch");
     return ES_OK;
 }
 
@@ -570,7 +672,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     // Launch shape: the defaults, or overrides for launch-shape sweeps.
     int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
     int groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
-    if (tiles_kernel(false, true, threads, groups) == nullptr) {
+    if (update_kernel(threads, groups) == nullptr) {
         threads = kDefaultThreads;
         groups = kDefaultGroups;
     }
@@ -578,7 +680,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     std::vector<DevTensor> tab(n_tensors + 1);
     std::unordered_map<uint32_t, uint32_t> ids;
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
-    uint64_t tiles = 0, numel = 0;
+    uint64_t n_full = 0, n_tail = 0, numel = 0;
     for (uint32_t i = 0; i < n_tensors; ++i) {
         const es_tensor_t& t = tensors[i];
         const std::string where = "es_plan_create: tensor " + std::to_string(i);
@@ -589,18 +691,21 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         if (t.numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, where + ": numel too large");
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
         if (t.numel > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
-        const uint64_t nt = (t.numel + tile_elems - 1) / tile_elems;
-        tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, tiles, t.tensor_id,
-                           (a % 16 == 0) ? kFlagAligned : 0u};
+        // full tiles need a 16-byte aligned base; the rest are tail tiles
+        const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
+        const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
+        tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, n_full, n_tail, t.tensor_id,
+                           0u, 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
-        tiles += nt;
+        n_full += full;
+        n_tail += tail;
         numel += t.numel;
     }
     std::sort(ranges.begin(), ranges.end());
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_plan_create: tensors overlap in memory");
-    tab[n_tensors] = DevTensor{nullptr, 0, tiles, 0xFFFFFFFFu, 0u};   // sentinel
+    tab[n_tensors] = DevTensor{nullptr, 0, n_full, n_tail, 0xFFFFFFFFu, 0u, 0u};   // sentinel
 
     es_plan_t* p = new (std::nothrow) es_plan_t;
     if (p == nullptr) return fail(ES_ERR_NOMEM, "es_plan_create: host allocation");
@@ -611,14 +716,16 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
     const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
     const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
-    p->nontemporal = env_int("ESOPT_NONTEMPORAL", 1, 0, 1) != 0;
+    p->pipelined = env_int("ESOPT_PIPELINE", 1, 0, 1) != 0;
+    p->burst = env_int("ESOPT_BURST", 1, 0, 1) != 0;
     p->threads = threads;
     p->groups = groups;
     p->tile_elems = tile_elems;
     p->n_tensors = n_tensors;
     p->numel = numel;
-    p->n_tiles = tiles;
-    const uint64_t cap = std::max<uint64_t>(tiles, 1);
+    p->n_full = n_full;
+    p->n_tail = n_tail;
+    const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
     p->grid_perturb = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_perturb));
     p->grid_update = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_update));
     e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(DevTensor) * tab.size());
@@ -655,7 +762,7 @@ int es_plan_destroy(es_plan_t* plan) {
 }
 
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
-uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_tiles : 0; }
+uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_full + plan->n_tail : 0; }
 
 int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
     return perturb_impl(plan, seed, sign, sigma, stream, "es_perturb");
@@ -755,13 +862,12 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
                        members, hdr, z_out_dev, status_out_dev);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
-    if (plan->n_tiles == 0) return ES_OK;
-    TilesKernel kernel = tiles_kernel(true, plan->nontemporal, plan->threads, plan->groups);
+    if (plan->n_full + plan->n_tail == 0) return ES_OK;
+    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups);
     hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
-                       plan->n_tiles,
-                       0u, 0u, 0.0f, members, hdr);
+                       plan->n_full, plan->n_tail, members, hdr);
     e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_tiles_kernel<update> launch");
+    if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
     return ES_OK;
 }
 
