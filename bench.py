@@ -45,8 +45,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-pass", action="store_true",
                     help="run one perturb, one update and a calibration copy, for rocprofv3")
-    ap.add_argument("--traffic-json", default=os.path.join(REPO, "profiles", "traffic.json"),
-                    help="per-launch HBM bytes measured with rocprofv3 counters")
+    ap.add_argument("--counters-json", default=os.path.join(REPO, "profiles", "counters.json"),
+                    help="per-launch counter values measured with rocprofv3 (see --summarize)")
+    ap.add_argument("--summarize", nargs=4, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR", "VALU_DIR"),
+                    help="turn rocprofv3 CSV output of the profiling runs into profiles/")
     return ap.parse_args()
 
 
@@ -120,6 +122,9 @@ def host_samples(W, per_tensor=1 << 14):
 
 def main():
     args = parse()
+    if args.summarize:
+        summarize(*args.summarize, workload=args.workload)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs the ES parameter path on one GPU; "
                                    "--gpus above 1 is not supported (see the sharding design)"}))
@@ -210,20 +215,30 @@ def main():
     value = (2 * N + 1) * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
 
-    traffic = None
-    if os.path.exists(args.traffic_json):
-        tj = json.load(open(args.traffic_json))
-        rec = tj.get(W.name, {}).get("es_perturb")
-        if rec and rec.get("source_hash") == _kernel_source_hash():
-            traffic = rec["bytes_per_launch"]
+    counters = None
+    if os.path.exists(args.counters_json):
+        cj = json.load(open(args.counters_json))
+        if cj.get("source_hash") == _kernel_source_hash() and cj.get("workload") == W.name:
+            counters = cj
+    traffic = counters["es_perturb"]["bytes_per_launch"] if counters else None
     perturb_gbs = 4 * P / t_pert / 1e9
     roofline = {"bound": "hbm", "achieved": round(perturb_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(perturb_gbs / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": "es_tiles_kernel<perturb> (es_perturb/es_restore)",
+                "traffic": traffic, "kernel": "es_perturb_kernel (es_perturb / es_restore)",
                 "algorithmic_bytes_per_launch": 4 * P}
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
               "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
               "normals_per_s": n_distinct * P / t_upd, "distinct_seeds": n_distinct}
+    # The update is VALU-bound: its roofline is the VALU issue rate.  The
+    # instruction count per launch is a counter measurement (SQ_INSTS_VALU,
+    # same workload and kernel sources); the duration is live.
+    roofline_update = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
+                       "achieved": None, "frac": None,
+                       "kernel": "es_update_kernel (fused N-member update)",
+                       "traffic": counters["es_update"]["bytes_per_launch"] if counters else None}
+    if counters and N == len(W.seeds) and n_members is None:
+        ach = counters["es_update"]["valu_insts_per_launch"] * 64 / t_upd / 1e12
+        roofline_update.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
     out = {
         "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
         "value": value,
@@ -237,6 +252,7 @@ def main():
                    "counting": "value = (2N+1) P / step time: 2N perturb/restore passes "
                                "and one fused N-member update pass per step"},
         "roofline": roofline,
+        "roofline_update": roofline_update,
         "per_kernel": {
             "es_perturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
                            "GBps_algorithmic": round(perturb_gbs, 1),
@@ -249,6 +265,108 @@ def main():
         out["cpu_baseline"] = cpu
     plan.close()
     print(json.dumps(out))
+
+
+# ------------------------------------------------------------ profiling --
+
+PROFILE_COMMANDS = {
+    "trace": "rocprofv3 --kernel-trace --stats -f csv rocpd -d <out>/trace -o trace -- "
+             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
+    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv rocpd -d <out>/fetch -o fetch -- "
+             "python3 bench.py --profile-pass",
+    "write": "rocprofv3 --pmc WRITE_SIZE -f csv rocpd -d <out>/write -o write -- "
+             "python3 bench.py --profile-pass",
+    "valu": "rocprofv3 --pmc SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_VALU_TRANS_F32 SQ_WAVES "
+            "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE -f csv rocpd -d <out>/valu -o valu -- "
+            "python3 bench.py --profile-pass",
+}
+
+
+def _kind(name):
+    if "es_perturb_kernel" in name:
+        return "es_perturb"
+    if "es_update_kernel" in name:
+        return "es_update"
+    if "copyBuffer" in name:
+        return "copy"
+    return None
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    f = glob.glob(os.path.join(d, "*counter_collection.csv"))[0]
+    out = {}
+    for r in csv.DictReader(open(f)):
+        k = _kind(r["Kernel_Name"])
+        if k:
+            out.setdefault((k, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    return out
+
+
+def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload):
+    """Write profiles/<kernel>_<workload>.md and profiles/counters.json from
+    the CSV output of the four rocprofv3 runs in PROFILE_COMMANDS."""
+    import csv
+    import glob
+    stats = list(csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0])))
+    fetch, write, valu = _counter_rows(fetch_dir), _counter_rows(write_dir), _counter_rows(valu_dir)
+    # calibration: the largest copyBuffer dispatch of the profile pass is the 1 GiB device copy
+    copy_bytes = 1 << 30
+    f_copy = max(fetch[("copy", "FETCH_SIZE")]) * 1024
+    w_copy = max(write[("copy", "WRITE_SIZE")]) * 1024
+    f_scale, w_scale = copy_bytes / f_copy, copy_bytes / w_copy
+    from paper_2608_17310_amd import workloads as wl
+    P = wl.WORKLOADS[workload].n_params
+    counters = {"source_hash": _kernel_source_hash(), "workload": workload, "params": P,
+                "calibration": {"copy_bytes": copy_bytes, "fetch_scale": f_scale, "write_scale": w_scale}}
+    for kind in ("es_perturb", "es_update"):
+        st = [r for r in stats if _kind(r["Name"]) == kind][0]
+        fb = float(np.mean(fetch[(kind, "FETCH_SIZE")])) * 1024 * f_scale
+        wb = float(np.mean(write[(kind, "WRITE_SIZE")])) * 1024 * w_scale
+        v = {c: float(np.mean(valu[(kind, c)])) for c in
+             ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_WAVES",
+              "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")}
+        counters[kind] = {"bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
+                          "valu_insts_per_launch": v["SQ_INSTS_VALU"], "counters": v,
+                          "avg_ns": float(st["AverageNs"]), "calls": int(st["Calls"])}
+        lines = [
+            f"# {kind} on {workload} ({P:,} bf16 parameters)",
+            "",
+            "Commands (run from the repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first; "
+            "`<out>` is an output directory):",
+            "",
+        ] + [f"* `{c}`" for c in PROFILE_COMMANDS.values()] + [
+            "",
+            f"Kernel-sources hash: `{counters['source_hash']}`",
+            "",
+            "## Kernel trace (--stats)",
+            "",
+            "| kernel | calls | average ns | min ns | max ns |",
+            "|---|---|---|---|---|",
+            f"| `{st['Name'][:90]}` | {st['Calls']} | {float(st['AverageNs']):.0f} | {st['MinNs']} | {st['MaxNs']} |",
+            "",
+            "## HBM traffic per launch (FETCH_SIZE / WRITE_SIZE, KiB counters scaled by a 1 GiB copy)",
+            "",
+            f"* calibration copy of {copy_bytes} B read {f_copy:.0f} B by FETCH_SIZE and {w_copy:.0f} B by "
+            f"WRITE_SIZE: scale factors {f_scale:.3f} and {w_scale:.3f}",
+            f"* fetched {fb:.4e} B, written {wb:.4e} B, total {fb + wb:.4e} B = {(fb + wb) / P:.3f} B per "
+            f"parameter (algorithmic: 4)",
+            "",
+            "## VALU counters per launch",
+            "",
+        ] + [f"* {k}: {val:.4e}" for k, val in v.items()] + [
+            f"* VALU instructions per parameter: {v['SQ_INSTS_VALU'] * 64 / P:.2f} (wave instructions x 64 lanes / P)",
+            f"* of which transcendental: {v['SQ_INSTS_VALU_TRANS_F32'] * 64 / P:.2f}",
+            f"* VALU lane-instruction rate: {v['SQ_INSTS_VALU'] * 64 / (float(st['AverageNs']) * 1e-9) / 1e12:.2f} "
+            f"T/s of {VALU_PEAK_TINST:.1f} T/s peak",
+            "",
+        ]
+        with open(os.path.join(REPO, "profiles", f"{kind}_{workload}.md"), "w") as fh:
+            fh.write("\n".join(lines))
+    with open(os.path.join(REPO, "profiles", "counters.json"), "w") as fh:
+        json.dump(counters, fh, indent=1)
+    print(json.dumps({k: counters[k]["bytes_per_launch"] for k in ("es_perturb", "es_update")}))
 
 
 def _kernel_source_hash():
