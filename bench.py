@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="dense-27b")
     ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
+    ap.add_argument("--swap", action="store_true",
+                    help="move between members with the fused es_swap (N+1 passes per step)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -170,20 +172,30 @@ def main():
 
     ev = []   # (kind, start, end) event pairs inside the timed region
 
+    def timed_call(kind, record, fn, *a):
+        if record:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(*a)
+            e1.record(stream)
+            ev.append((kind, e0, e1))
+        else:
+            fn(*a)
+
     def run_step(t, record):
         seeds = step_seeds(W, t, n_members)
         sigma = sigma_at(W, t)
-        for s, sg in zip(seeds, signs):
-            for kind, fn in (("es_perturb", plan.perturb), ("es_restore", plan.restore)):
-                if record:
-                    a = torch.cuda.Event(enable_timing=True)
-                    b = torch.cuda.Event(enable_timing=True)
-                    a.record(stream)
-                    fn(s, sg, sigma)
-                    b.record(stream)
-                    ev.append((kind, a, b))
-                else:
-                    fn(s, sg, sigma)
+        if args.swap:
+            timed_call("es_perturb", record, plan.perturb, seeds[0], signs[0], sigma)
+            for i in range(N - 1):
+                timed_call("es_swap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
+                           signs[i + 1], sigma)
+            timed_call("es_restore", record, plan.restore, seeds[-1], signs[-1], sigma)
+        else:
+            for s, sg in zip(seeds, signs):
+                timed_call("es_perturb", record, plan.perturb, s, sg, sigma)
+                timed_call("es_restore", record, plan.restore, s, sg, sigma)
         if record:
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
@@ -212,7 +224,8 @@ def main():
         per.setdefault(kind, []).append(a.elapsed_time(b))
     t_pert = float(np.mean(per["es_perturb"] + per["es_restore"])) / 1e3
     t_upd = float(np.mean(per["es_update"])) / 1e3
-    value = (2 * N + 1) * P / (ms_step / 1e3)
+    passes = (N + 2) if args.swap else (2 * N + 1)
+    value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
 
     counters = None
@@ -249,8 +262,11 @@ def main():
         "dtype": "f32", "param_dtype": "bf16", "data": "synthetic",
         "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
-                   "counting": "value = (2N+1) P / step time: 2N perturb/restore passes "
-                               "and one fused N-member update pass per step"},
+                   "member_moves": "es_swap" if args.swap else "es_perturb/es_restore",
+                   "counting": ("value = (N+2) P / step time: perturb, N-1 fused swaps, restore "
+                                "and one fused N-member update pass per step") if args.swap else
+                               ("value = (2N+1) P / step time: 2N perturb/restore passes "
+                                "and one fused N-member update pass per step")},
         "roofline": roofline,
         "roofline_update": roofline_update,
         "per_kernel": {
@@ -258,6 +274,10 @@ def main():
                            "GBps_algorithmic": round(perturb_gbs, 1),
                            "frac_hbm_peak": round(perturb_gbs / HBM_PEAK_GBS, 4)},
             "es_update": update,
+            **({"es_swap": {"ms": round(float(np.mean(per["es_swap"])), 3),
+                            "params_per_s": P / (float(np.mean(per["es_swap"])) / 1e3),
+                            "GBps_algorithmic": round(4 * P / (float(np.mean(per["es_swap"])) / 1e3) / 1e9, 1)}}
+               if "es_swap" in per else {}),
         },
         "wall_s_timed": round(wall, 3),
     }

@@ -17,9 +17,10 @@
  *     key     = (seed & 0xffffffff, seed >> 32)
  *     counter = (q & 0xffffffff, q >> 32, tensor_id, 0),  q = j >> 2
  *   Word pair (w0,w1) serves elements 4q, 4q+1 and (w2,w3) serves 4q+2,
- *   4q+3.  u(w) = ((w >> 9) + 0.5) * 2^-23; Box-Muller (1958):
- *   r = sqrt(-2 ln u(wa)), phi = 2 pi u(wb); first element r cos(phi),
- *   second r sin(phi).  The GPU evaluates this in binary32.
+ *   4q+3.  With m(w) = w & (2^23 - 1): radius uniform u = (m(wa) + 0.5)
+ *   * 2^-23, angle v = m(wb) * 2^-23 turns; Box-Muller (1958):
+ *   r = sqrt(-2 ln u), phi = 2 pi v; first element r cos(phi), second
+ *   r sin(phi).  The GPU evaluates this in binary32.
  *
  * Parameters are bf16 (the paper states no dtype; its memory figures imply
  * 16-bit weights).  Each result is computed in binary32 and rounded to bf16
@@ -87,7 +88,7 @@ typedef struct es_plan es_plan_t;
  * tensor_id, nonzero reserved field, null data with numel > 0, or tensors
  * whose byte ranges overlap; ALIGN for odd addresses; NOMEM / HIP for
  * allocation failures.  On success *out owns a device table of
- * 32 * (n_tensors + 1) bytes and ~42 KB of scratch, freed by es_plan_destroy. */
+ * 48 * (n_tensors + 1) bytes and ~42 KB of scratch, freed by es_plan_destroy. */
 int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out);
 
 /* Free a plan (NULL is a no-op).  Synchronises the device first so that no
@@ -111,6 +112,18 @@ int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_str
  * rounding residues (about 5% of N(0,0.02) elements move by one ulp at
  * sigma = 1e-3). */
 int es_restore(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+
+/* Move the perturbation from one member to the next in one pass (Section 3;
+ * Appendix D.6 -- revert member a after its evaluation, apply member b):
+ *   theta_j <- RNE_bf16(theta_j - sign_from sigma_from eps_j(seed_from)
+ *                               + sign_to   sigma_to   eps_j(seed_to))
+ * one read and one write per element, both noise streams generated in
+ * registers and summed in binary32.  Equivalent to es_restore(from) then
+ * es_perturb(to) but with one bf16 rounding instead of two.  Equal seeds
+ * merge; when the net weight is zero theta is left unchanged and nothing is
+ * launched.  Signs +1 or -1; sigmas finite and >= 0. */
+int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
+            uint64_t seed_to, int32_t sign_to, float sigma_to, es_stream_t stream);
 
 /* Population z-score (Section 3): mu = mean(R), s = sqrt(mean((R - mu)^2)),
  *   z_i = (R_i - mu) / (s + eps),

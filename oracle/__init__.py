@@ -32,7 +32,7 @@ from .philox import philox4x32_10, philox4x32_10_bigint, MASK32
 from .noise import (key_words, counter_words, uniform_from_word, angle_from_word,
                     box_muller, noise_words, normals)
 from .bf16 import bf16_to_f64, f64_to_bf16_rne, bf16_ulp
-from .es import (perturb, restore, zscore, update_coefficient, member_weights,
+from .es import (perturb, restore, swap, zscore, update_coefficient, member_weights,
                  update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
                  ES_REWARDS_ARE_WEIGHTS)
 
@@ -41,6 +41,6 @@ __all__ = [
     "key_words", "counter_words", "uniform_from_word", "angle_from_word", "box_muller",
     "noise_words", "normals",
     "bf16_to_f64", "f64_to_bf16_rne", "bf16_ulp",
-    "perturb", "restore", "zscore", "update_coefficient", "member_weights",
+    "perturb", "restore", "swap", "zscore", "update_coefficient", "member_weights",
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
 ]

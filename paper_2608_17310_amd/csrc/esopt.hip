@@ -44,6 +44,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstdlib>
+#include <cstddef>
 #include <cstring>
 #include <string>
 #include <unordered_map>
@@ -107,7 +108,8 @@ constexpr size_t kOffMembersIn = 0;
 constexpr size_t kOffDistinctIn = kOffMembersIn + sizeof(MemberIn) * ES_MAX_MEMBERS;
 constexpr size_t kOffMembers = kOffDistinctIn + sizeof(DistinctIn) * ES_MAX_MEMBERS;
 constexpr size_t kOffHeader = kOffMembers + sizeof(Member) * ES_MAX_MEMBERS;
-constexpr size_t kScratchBytes = kOffHeader + 256;
+constexpr size_t kOffSwap = kOffHeader + 256;       // es_swap: 2 members + header
+constexpr size_t kScratchBytes = kOffSwap + 256;
 
 constexpr int kStageWords = 256;            // 1 KB of kernel arguments per launch
 struct StageChunk {
@@ -197,20 +199,31 @@ __device__ __forceinline__ void group_axpy(const uint32_t w[8], float scale_k, f
     }
 }
 
-// Perturb one 8-element group in registers: x = theta + coef * eps, packed
-// back to bf16.
+// Noise streams applied by one perturb-style pass: theta + sum_m c_m eps_m
+// for m < M (M = 1: perturb / restore; M = 2: swap).  coef_k = c sqrt(2 ln 2).
+struct Streams {
+    uint32_t k0[2], k1[2];
+    float coef_k[2];
+};
+
+// Apply the streams to one 8-element group in registers and pack to bf16.
+// The binary32 value accumulates each stream with one FMA per element.
+template <int kM>
 __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e, uint32_t q_hi,
-                                              uint32_t tensor_id, uint32_t k0, uint32_t k1,
-                                              float coef_k, uint32_t out[4]) {
-    uint32_t w[8];
-    group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, k0, k1, w);
+                                              uint32_t tensor_id, const Streams& st,
+                                              uint32_t out[4]) {
     float x[8];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         x[2 * k] = es::bf16_lo(raw[k]);
         x[2 * k + 1] = es::bf16_hi(raw[k]);
     }
-    group_axpy(w, coef_k, x);
+#pragma unroll
+    for (int m = 0; m < kM; ++m) {
+        uint32_t w[8];
+        group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, st.k0[m], st.k1[m], w);
+        group_axpy(w, st.coef_k[m], x);
+    }
 #pragma unroll
     for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
 }
@@ -243,63 +256,52 @@ __device__ __forceinline__ TileRef locate_tail(const DevTensor* __restrict__ tab
                    tab[t].tensor_id};
 }
 
-template <int kThreads, int kU, bool kNT>
+template <int kThreads, int kU>
 __device__ __forceinline__ void load_tile(const TileRef& r, uint32_t raw[kU][4]) {
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-        load_group<true, kNT>(r.data, e, r.numel, raw[u]);
+        load_group<true, true>(r.data, e, r.numel, raw[u]);
     }
 }
 
-// Perturb a full tile whose groups are already in registers.  With kBurst
-// every group is computed first and the tile's stores then leave as one
-// burst: on MI355X an in-place stream whose writes come in per-tile bursts
-// sustains ~6.2 TB/s, against ~5.5 TB/s when each group's store is
-// interleaved with the next group's arithmetic.
-template <int kThreads, int kU, bool kNT, bool kBurst>
+// Perturb a full tile whose groups are already in registers: every group is
+// computed first and the tile's stores then leave in one burst.  On MI355X
+// an in-place stream whose writes come in per-tile bursts sustains ~6.2 TB/s,
+// against ~5.5 TB/s when each group's store is interleaved with the next
+// group's arithmetic.
+template <int kThreads, int kU, int kM>
 __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU][4],
-                                               uint32_t k0, uint32_t k1, float coef_k) {
+                                               const Streams& st) {
     const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
-    if constexpr (kBurst) {
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            uint32_t out[4];
-            perturb_group(raw[u], e, q_hi, r.tensor_id, k0, k1, coef_k, out);
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        uint32_t out[4];
+        perturb_group<kM>(raw[u], e, q_hi, r.tensor_id, st, out);
 #pragma unroll
-            for (int k = 0; k < 4; ++k) raw[u][k] = out[k];
-        }
-        __builtin_amdgcn_sched_barrier(0);
+        for (int k = 0; k < 4; ++k) raw[u][k] = out[k];
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            store_group<true, kNT>(r.data, e, r.numel, raw[u]);
-        }
-    } else {
-#pragma unroll
-        for (int u = 0; u < kU; ++u) {
-            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            uint32_t out[4];
-            perturb_group(raw[u], e, q_hi, r.tensor_id, k0, k1, coef_k, out);
-            store_group<true, kNT>(r.data, e, r.numel, out);
-        }
+    for (int u = 0; u < kU; ++u) {
+        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        store_group<true, true>(r.data, e, r.numel, raw[u]);
     }
 }
 
 // Perturb a tail tile group by group with bounds-checked 2-byte accesses.
-template <int kThreads, int kU, bool kNT>
-__device__ __forceinline__ void perturb_tail(const TileRef& r, uint32_t k0, uint32_t k1,
-                                             float coef_k) {
+template <int kThreads, int kU, int kM>
+__device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st) {
     const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
         if (e >= r.numel) break;
         uint32_t raw[4], out[4];
-        load_group<false, kNT>(r.data, e, r.numel, raw);
-        perturb_group(raw, e, q_hi, r.tensor_id, k0, k1, coef_k, out);
-        store_group<false, kNT>(r.data, e, r.numel, out);
+        load_group<false, true>(r.data, e, r.numel, raw);
+        perturb_group<kM>(raw, e, q_hi, r.tensor_id, st, out);
+        store_group<false, true>(r.data, e, r.numel, out);
     }
 }
 
@@ -307,60 +309,48 @@ __device__ __forceinline__ void perturb_tail(const TileRef& r, uint32_t k0, uint
 // workgroup's next tile into `next_buf`, then perturb the current tile from
 // `cur_buf`, so the memory pipe does not idle through the Philox /
 // Box-Muller arithmetic.  Returns true when the workgroup has no next tile.
-template <int kThreads, int kU, bool kNT, bool kBurst>
+template <int kThreads, int kU, int kM>
 __device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, uint32_t& t,
                                              uint64_t& tile, uint64_t n_full, TileRef& cur,
                                              uint32_t cur_buf[kU][4], uint32_t next_buf[kU][4],
-                                             uint32_t k0, uint32_t k1, float coef_k) {
+                                             const Streams& st) {
     constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
     const uint64_t next = tile + gridDim.x;
     const bool more = next < n_full;
     TileRef nxt = cur;
     if (more) {
         nxt = locate_full<kTileElems>(tab, t, next);
-        load_tile<kThreads, kU, kNT>(nxt, next_buf);
+        load_tile<kThreads, kU>(nxt, next_buf);
     }
-    perturb_loaded<kThreads, kU, kNT, kBurst>(cur, cur_buf, k0, k1, coef_k);
+    perturb_loaded<kThreads, kU, kM>(cur, cur_buf, st);
     if (!more) return true;
     tile = next;
     cur = nxt;
     return false;
 }
 
-// Perturb over the whole parameter list: full tiles first (16-byte accesses,
-// software-pipelined when kPipelined; two register buffers alternate, the
-// loop unrolled twice), then tail tiles.  coef_k = sign sigma sqrt(2 ln 2).
-template <int kThreads, int kU, bool kPipelined, bool kBurst>
+// One pass over the whole parameter list applying kM noise streams: full
+// tiles first (16-byte nontemporal accesses, software-pipelined: two register
+// buffers alternate, the loop unrolled twice), then tail tiles.
+template <int kThreads, int kU, int kM>
 __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* __restrict__ tab,
                                                               uint64_t n_full, uint64_t n_tail,
-                                                              uint32_t k0, uint32_t k1,
-                                                              float coef_k) {
+                                                              Streams st) {
     constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
-    constexpr bool kNT = true;
-    if constexpr (kPipelined) {
-        uint64_t tile = blockIdx.x;
-        if (tile < n_full) {
-            uint32_t t = 0;
-            TileRef cur = locate_full<kTileElems>(tab, t, tile);
-            uint32_t a[kU][4], b[kU][4];
-            load_tile<kThreads, kU, kNT>(cur, a);
-            for (;;) {
-                if (perturb_step<kThreads, kU, kNT, kBurst>(tab, t, tile, n_full, cur, a, b, k0, k1, coef_k)) break;
-                if (perturb_step<kThreads, kU, kNT, kBurst>(tab, t, tile, n_full, cur, b, a, k0, k1, coef_k)) break;
-            }
-        }
-    } else {
+    uint64_t tile = blockIdx.x;
+    if (tile < n_full) {
         uint32_t t = 0;
-        for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
-            const TileRef r = locate_full<kTileElems>(tab, t, tile);
-            uint32_t raw[kU][4];
-            load_tile<kThreads, kU, kNT>(r, raw);
-            perturb_loaded<kThreads, kU, kNT, kBurst>(r, raw, k0, k1, coef_k);
+        TileRef cur = locate_full<kTileElems>(tab, t, tile);
+        uint32_t a[kU][4], b[kU][4];
+        load_tile<kThreads, kU>(cur, a);
+        for (;;) {
+            if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) break;
+            if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, b, a, st)) break;
         }
     }
     uint32_t t = 0;
-    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        perturb_tail<kThreads, kU, kNT>(locate_tail<kTileElems>(tab, t, tile), k0, k1, coef_k);
+    for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x)
+        perturb_tail<kThreads, kU, kM>(locate_tail<kTileElems>(tab, t, tl), st);
 }
 
 // One tile of the fused update: for each of the lane's groups in turn,
@@ -559,26 +549,24 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
     }
 }
 
-using PerturbKernel = void (*)(const DevTensor*, uint64_t, uint64_t, uint32_t, uint32_t, float);
+using PerturbKernel = void (*)(const DevTensor*, uint64_t, uint64_t, Streams);
 using UpdateKernel = void (*)(const DevTensor*, uint64_t, uint64_t, const Member*,
                               const UpdateHeader*);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
 #define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
 
-template <bool kPipelined, bool kBurst>
+template <int kM>
 PerturbKernel perturb_kernel_for(int threads, int groups) {
-#define ES_CASE(T, U) if (threads == T && groups == U) return es_perturb_kernel<T, U, kPipelined, kBurst>;
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_perturb_kernel<T, U, kM>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
 }
 
-PerturbKernel perturb_kernel(bool pipelined, bool burst, int threads, int groups) {
-    if (burst) return pipelined ? perturb_kernel_for<true, true>(threads, groups)
-                                : perturb_kernel_for<false, true>(threads, groups);
-    return pipelined ? perturb_kernel_for<true, false>(threads, groups)
-                     : perturb_kernel_for<false, false>(threads, groups);
+PerturbKernel perturb_kernel(int members, int threads, int groups) {
+    return members == 1 ? perturb_kernel_for<1>(threads, groups)
+                        : perturb_kernel_for<2>(threads, groups);
 }
 
 UpdateKernel update_kernel(int threads, int groups) {
@@ -606,8 +594,7 @@ struct es_plan {
     int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
     int groups = kDefaultGroups;    // 8-element groups per lane per tile
     uint64_t tile_elems = 0;        // threads * groups * 8
-    bool pipelined = true;          // perturb prefetches the next full tile
-    bool burst = true;              // perturb stores each tile in one burst
+    bool swap_streams = true;       // es_swap runs the two-stream perturb kernel
     DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
@@ -633,13 +620,20 @@ int check_device(const es_plan_t* p) {
     return ES_OK;
 }
 
-int launch_perturb(es_plan_t* p, uint64_t seed, double coef, hipStream_t s) {
+// One perturb-style pass applying `members` (1 or 2) noise streams with
+// coefficients coef[m] (sign sigma), nothing skipped.
+int launch_streams(es_plan_t* p, int members, const uint64_t* seed, const double* coef,
+                   hipStream_t s) {
     if (p->n_full + p->n_tail == 0) return ES_OK;
-    const float coef_k = static_cast<float>(coef * kSqrt2Ln2Double);
-    const PerturbKernel kernel = perturb_kernel(p->pipelined, p->burst, p->threads, p->groups);
+    Streams st = {};
+    for (int m = 0; m < members; ++m) {
+        st.k0[m] = static_cast<uint32_t>(seed[m]);
+        st.k1[m] = static_cast<uint32_t>(seed[m] >> 32);
+        st.coef_k[m] = static_cast<float>(coef[m] * kSqrt2Ln2Double);
+    }
+    const PerturbKernel kernel = perturb_kernel(members, p->threads, p->groups);
     hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_full,
-                       p->n_tail, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
-                       coef_k);
+                       p->n_tail, st);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_perturb_kernel launch");
     return ES_OK;
@@ -655,8 +649,8 @@ int perturb_impl(es_plan_t* p, uint64_t seed, int32_t sign, float sigma, es_stre
     if (sigma == 0.0f) return ES_OK;
     const int rc = check_device(p);
     if (rc != ES_OK) return rc;
-    return launch_perturb(p, seed, sign > 0 ? double(sigma) : -double(sigma),
-                          static_cast<hipStream_t>(stream));
+    const double coef = sign > 0 ? double(sigma) : -double(sigma);
+    return launch_streams(p, 1, &seed, &coef, static_cast<hipStream_t>(stream));
 }
 
 }  // namespace
@@ -716,8 +710,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
     const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
     const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
-    p->pipelined = env_int("ESOPT_PIPELINE", 1, 0, 1) != 0;
-    p->burst = env_int("ESOPT_BURST", 1, 0, 1) != 0;
+    p->swap_streams = env_int("ESOPT_SWAP_STREAMS", 1, 0, 1) != 0;
     p->threads = threads;
     p->groups = groups;
     p->tile_elems = tile_elems;
@@ -868,6 +861,68 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
                        plan->n_full, plan->n_tail, members, hdr);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
+    return ES_OK;
+}
+
+int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
+            uint64_t seed_to, int32_t sign_to, float sigma_to, es_stream_t stream) {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_swap: null plan");
+    if ((sign_from != 1 && sign_from != -1) || (sign_to != 1 && sign_to != -1))
+        return fail(ES_ERR_INVALID_ARG, "es_swap: signs must be +1 or -1");
+    if (!std::isfinite(sigma_from) || sigma_from < 0.0f || !std::isfinite(sigma_to) ||
+        sigma_to < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, "es_swap: sigmas must be finite and >= 0");
+    // Two weighted noise terms, merged when the seeds coincide.
+    uint64_t seeds[2] = {seed_from, seed_to};
+    double w[2] = {-double(sign_from) * double(sigma_from), double(sign_to) * double(sigma_to)};
+    uint32_t nd = 2;
+    if (seed_from == seed_to) {
+        w[0] += w[1];
+        nd = 1;
+    }
+    struct {
+        Member m[2];
+        UpdateHeader h;
+    } table = {};
+    uint32_t live = 0;
+    for (uint32_t d = 0; d < nd; ++d) {
+        const float wk = static_cast<float>(w[d] * kSqrt2Ln2Double);
+        table.m[d] = Member{static_cast<uint32_t>(seeds[d]), static_cast<uint32_t>(seeds[d] >> 32), wk, 0u};
+        live += (wk != 0.0f) ? 1u : 0u;
+    }
+    if (live == 0 || plan->n_full + plan->n_tail == 0) return ES_OK;   // theta unchanged
+    table.h = UpdateHeader{nd, live, 0, 0u};
+    int rc = check_device(plan);
+    if (rc != ES_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (plan->swap_streams) {
+        // the memory-streaming kernel with one or two noise streams
+        uint64_t sd[2];
+        double cf[2];
+        int m = 0;
+        for (uint32_t d = 0; d < nd; ++d)
+            if (table.m[d].w_k != 0.0f) {
+                sd[m] = seeds[d];
+                cf[m] = w[d];
+                ++m;
+            }
+        return launch_streams(plan, m, sd, cf, s);
+    }
+    static_assert(sizeof(table) % 4 == 0 && sizeof(table) <= 4 * kStageWords, "swap table size");
+    StageChunk chunk;
+    std::memcpy(chunk.words, &table, sizeof(table));
+    auto* dst = reinterpret_cast<uint32_t*>(plan->d_scratch + kOffSwap);
+    hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s, dst,
+                       static_cast<uint32_t>(sizeof(table) / 4), chunk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
+    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups);
+    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
+                       plan->n_full, plan->n_tail, reinterpret_cast<const Member*>(dst),
+                       reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffSwap +
+                                                             offsetof(decltype(table), h)));
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_update_kernel (swap) launch");
     return ES_OK;
 }
 

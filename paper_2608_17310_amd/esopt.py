@@ -8,6 +8,7 @@ call raises (there is no fallback).
     plan = Plan([w0, w1, ...])           # bf16, contiguous, on the current device
     plan.perturb(seed, sign, sigma)      # theta += sign sigma eps(seed)
     plan.restore(seed, sign, sigma)      # theta -= sign sigma eps(seed)
+    plan.swap(seed_a, sign_a, seed_b, sign_b, sigma)   # restore a + perturb b, one pass
     plan.update(seeds, signs, rewards, alpha)   # fused z-score + N-member update
 """
 
@@ -50,6 +51,7 @@ SIGNATURES = {
     "es_plan_tiles": (_u64, [_vp]),
     "es_perturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_restore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
+    "es_swap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
@@ -167,6 +169,13 @@ class Plan:
     def restore(self, seed, sign, sigma, stream=None):
         _check(load().es_restore(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
                "es_restore")
+
+    def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
+        """Revert member `from` and apply member `to` in one pass."""
+        sigma_to = sigma if sigma_to is None else sigma_to
+        _check(load().es_swap(self.handle, int(seed_from), int(sign_from), float(sigma),
+                              int(seed_to), int(sign_to), float(sigma_to), _stream(stream)),
+               "es_swap")
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                z_out=None, status_out=None, stream=None):

@@ -1,0 +1,95 @@
+"""One ES generation over a plan, and its deterministic replay.
+
+Host orchestration of the library calls (every step runs in the HIP kernels):
+Section 3 and Appendix D.6 of arXiv 2608.17310 apply theta + sigma_t eps_i
+for candidate i, evaluate it, revert the perturbation, and after the whole
+population apply the z-scored, reward-weighted update with each eps_i
+regenerated from its seed; Section 3.1 sets sigma_t on a cosine schedule.
+
+With fused_swap the revert of member i and the apply of member i+1 are one
+pass (es_swap), so a generation of N members makes N + 1 passes over the
+parameters instead of 2N, plus the update.
+
+Only seeds, signs, rewards and scalars are recorded; because every kernel is
+deterministic, replaying the records from the same starting parameters
+rebuilds the parameters bit for bit (the paper reconstructs its final models
+from the recorded update sequence the same way, Appendix D.2 and D.4).
+"""
+
+from dataclasses import dataclass, field
+from typing import Callable, List
+
+import torch
+
+from . import esopt
+
+
+@dataclass
+class GenerationRecord:
+    seeds: List[int]
+    signs: List[int]
+    rewards: List[float]            # binary32 values, as passed to es_update
+    sigma: float
+    alpha: float
+    flags: int = 0
+    zscore_eps: float = 1e-8
+    fused_swap: bool = True
+
+
+def sigma_schedule(sigma0, sigma_T, T):
+    """sigma_t for the T updates t = 0 .. T-1 (Section 3.1; es_sigma_cosine)."""
+    return [esopt.sigma_cosine(sigma0, sigma_T, t, T) for t in range(T)]
+
+
+def antithetic_seeds(base_seed, n_pairs):
+    """Seeds and signs of n_pairs antithetic pairs: (s, +1), (s, -1), ..."""
+    seeds = [int(base_seed) + p for p in range(n_pairs) for _ in (0, 1)]
+    signs = [sg for _ in range(n_pairs) for sg in (1, -1)]
+    return seeds, signs
+
+
+def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
+    """Apply member 0, visit it, move to member 1, ... and revert the last."""
+    n = len(seeds)
+    plan.perturb(seeds[0], signs[0], sigma, stream=stream)
+    for i in range(n):
+        visit(i)
+        if i + 1 < n and fused_swap:
+            plan.swap(seeds[i], signs[i], seeds[i + 1], signs[i + 1], sigma, stream=stream)
+        else:
+            plan.restore(seeds[i], signs[i], sigma, stream=stream)
+            if i + 1 < n:
+                plan.perturb(seeds[i + 1], signs[i + 1], sigma, stream=stream)
+
+
+def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], float],
+                   flags=0, zscore_eps=1e-8, fused_swap=True, stream=None):
+    """Run one generation; evaluate(i) scores the parameters while member i is
+    applied and returns a float.  Returns the GenerationRecord."""
+    if len(seeds) != len(signs) or not seeds:
+        raise ValueError("seeds and signs must be non-empty and of equal length")
+    rewards = []
+    _walk(plan, seeds, signs, sigma, fused_swap, lambda i: rewards.append(float(evaluate(i))),
+          stream)
+    rec = GenerationRecord(list(map(int, seeds)), list(map(int, signs)),
+                           [float(torch.tensor(r, dtype=torch.float32)) for r in rewards],
+                           float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap)
+    apply_update(plan, rec, stream)
+    return rec
+
+
+def apply_update(plan, rec: GenerationRecord, stream=None):
+    r = torch.tensor(rec.rewards, dtype=torch.float32, device=plan.device)
+    plan.update(rec.seeds, rec.signs, r, rec.alpha, sigma=rec.sigma, zscore_eps=rec.zscore_eps,
+                flags=rec.flags, stream=stream)
+
+
+def replay(plan, records, with_perturbations=True, stream=None):
+    """Re-apply recorded generations.  With with_perturbations (default) the
+    perturb / swap / restore passes are replayed too, which reproduces the
+    live run bit for bit (their bf16 rounding residues included); without,
+    only the updates are applied."""
+    for rec in records:
+        if with_perturbations:
+            _walk(plan, rec.seeds, rec.signs, rec.sigma, rec.fused_swap, lambda i: None, stream)
+        apply_update(plan, rec, stream)

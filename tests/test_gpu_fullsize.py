@@ -52,7 +52,11 @@ def _run(W, n_members=None, samples_per_tensor=256):
     plan.perturb(seed, sign, sigma)
     torch.cuda.synchronize()
     pert = _gather(views, idx_dev)
-    plan.restore(seed, sign, sigma)
+    seed_b, sign_b = seeds[0], signs[0]
+    plan.swap(seed, sign, seed_b, sign_b, sigma)
+    torch.cuda.synchronize()
+    swp = _gather(views, idx_dev)
+    plan.restore(seed_b, sign_b, sigma)
     torch.cuda.synchronize()
     rest = _gather(views, idx_dev)
     r = wl.rewards(W, n=len(seeds))
@@ -65,13 +69,17 @@ def _run(W, n_members=None, samples_per_tensor=256):
     del flat, views
     torch.cuda.empty_cache()
 
-    reps = {"perturb": [], "restore": [], "update": []}
+    reps = {"perturb": [], "swap": [], "restore": [], "update": []}
     for t, el_i in enumerate(idx):
         el = el_i.astype(np.uint64)
         exp = oracle.perturb(theta0[t], seed, t, sign, sigma, elems=el)
         reps["perturb"].append(report(pert[t], exp, theta0[t], perturb_delta(seed, t, sign, sigma, el)))
-        exp = oracle.restore(pert[t], seed, t, sign, sigma, elems=el)
-        reps["restore"].append(report(rest[t], exp, pert[t], perturb_delta(seed, t, -sign, sigma, el)))
+        exp = oracle.swap(pert[t], t, seed, sign, sigma, seed_b, sign_b, sigma, elems=el)
+        dsw = perturb_delta(seed, t, -sign, sigma, el) + perturb_delta(seed_b, t, sign_b, sigma, el) \
+            if seed != seed_b else perturb_delta(seed, t, sign_b - sign, sigma, el)
+        reps["swap"].append(report(swp[t], exp, pert[t], dsw))
+        exp = oracle.restore(swp[t], seed_b, t, sign_b, sigma, elems=el)
+        reps["restore"].append(report(rest[t], exp, swp[t], perturb_delta(seed_b, t, -sign_b, sigma, el)))
         exp, st = oracle.update(rest[t], t, seeds, signs, r, W.alpha, sigma, elems=el)
         reps["update"].append(report(upd[t], exp, rest[t],
                                      update_delta(t, seeds, signs, r, W.alpha, sigma, 0, el)))

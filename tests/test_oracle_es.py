@@ -234,3 +234,43 @@ def test_sigma_cosine_closed_forms():
     assert sigma_cosine(1.5e-3, 1.5e-3, 37, 70) == 1.5e-3    # constant schedule
     with pytest.raises(ValueError):
         sigma_cosine(1e-3, 1e-4, 101, 100)
+
+
+# ------------------------------------------------------------------- swap --
+
+def test_swap_identities_and_update_equivalence():
+    from oracle import swap
+    theta = random_bf16_bits(1 << 14, 70)
+    theta[:2] = [0x8000, 0x0000]
+    np.testing.assert_array_equal(swap(theta, 0, 5, 1, 1e-3, 5, 1, 1e-3), theta)
+    np.testing.assert_array_equal(swap(theta, 0, 5, 1, 0.0, 6, 1, 0.0), theta)
+    # revert a, apply b == one update with weights (-sigma, +sigma): c = alpha/G = 1
+    s32 = np.float32(1e-3)
+    got = swap(theta, 3, 11, 1, 1e-3, 12, -1, 1e-3)
+    upd, st = update(theta, 3, [11, 12], [-1, -1], np.array([s32, s32], np.float32),
+                     alpha=2.0, sigma=1.0, flags=ES_REWARDS_ARE_WEIGHTS)
+    np.testing.assert_array_equal(got, upd)
+
+
+def test_swap_on_zero_is_difference_of_two_normals():
+    from oracle import swap
+    theta = np.zeros(1 << 17, dtype=np.uint16)
+    d = bf16_to_f64(swap(theta, 2, 21, 1, 1e-3, 22, 1, 1e-3)) / float(np.float32(1e-3))
+    assert abs(d.std() - math.sqrt(2.0)) < 0.02
+    e = normals(22, 2, np.arange(1 << 17, dtype=np.uint64)) - normals(21, 2, np.arange(1 << 17, dtype=np.uint64))
+    assert np.corrcoef(d, e)[0, 1] > 0.999
+
+
+def test_swap_close_to_restore_then_perturb():
+    from oracle import swap
+    theta = random_bf16_bits(1 << 16, 71)
+    p = perturb(theta, 5, 0, 1, 1e-3)
+    one = bf16_to_f64(swap(p, 0, 5, 1, 1e-3, 6, -1, 1e-3))
+    mid = restore(p, 5, 0, 1, 1e-3)
+    two = bf16_to_f64(perturb(mid, 6, 0, -1, 1e-3))
+    # the two-pass path rounds the intermediate too: the results differ by at
+    # most the three rounding errors (half an ulp each of the intermediate
+    # and of both results)
+    bound = 0.5 * (oracle.bf16_ulp(bf16_to_f64(mid)) + oracle.bf16_ulp(one) + oracle.bf16_ulp(two))
+    assert np.all(np.abs(one - two) <= bound)
+    assert np.mean(one == two) > 0.5
