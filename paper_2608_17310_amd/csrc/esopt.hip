@@ -64,7 +64,7 @@ constexpr int kGroupElems = 8;              // bf16 per lane-group (one 16-byte 
 constexpr int kDefaultThreads = 1024;
 constexpr int kDefaultGroups = 8;
 constexpr int kDefaultPerturbWgPerCu = 1;
-constexpr int kDefaultUpdateWgPerCu = 4;
+constexpr int kDefaultUpdateWgPerCu = 8;
 constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
 // Device tensor table entry.  Tiles are numbered in two sequences: full
@@ -354,20 +354,31 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
 }
 
 // One tile of the fused update: for each of the lane's groups in turn,
-// load it, acc = sum_d w_d eps_d (binary32, members in table order, zero
-// weights skipped), theta <- RNE(theta + acc), store it.  The kernel is
-// VALU-bound, so one group's registers are live at a time and the number of
-// resident waves hides the memory latency.
+// acc = sum_d w_d eps_d (binary32, members in table order, zero weights
+// skipped), theta <- RNE(theta + acc), store it.  The kernel is VALU-bound,
+// so one group's registers are live at a time and the number of resident
+// waves hides memory latency; full tiles also prefetch the next group while
+// the current one is computed, which matters when N is small (the two-member
+// swap).
 template <int kThreads, int kU, bool kFast, bool kNT>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct) {
     const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
+    uint32_t next[4];
+    if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.numel, next);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
-        const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        const uint64_t e = e0 + uint64_t(u) * kThreads * kGroupElems;
         if (!kFast && e >= r.numel) break;
         uint32_t raw[4];
-        load_group<kFast, kNT>(r.data, e, r.numel, raw);
+        if constexpr (kFast) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) raw[k] = next[k];
+            if (u + 1 < kU) load_group<true, kNT>(r.data, e + uint64_t(kThreads) * kGroupElems, r.numel, next);
+        } else {
+            load_group<false, kNT>(r.data, e, r.numel, raw);
+        }
         const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
         float acc[8];
 #pragma unroll
