@@ -5,7 +5,8 @@ the GPU library computes: the counter-based noise (Philox4x32-10 words, the
 uniform map, the Box-Muller transform), in-place perturb/restore of bf16
 parameters, the population z-score of rewards, the reward-weighted update, and
 the cosine schedule of the perturbation radius.  Floating point work is done in
-fp64 and rounded to bf16 exactly once, round-to-nearest-even.
+fp64 and rounded to bf16 exactly once, round-to-nearest-even (the update can
+instead round stochastically, from binary32, with counter-based draws).
 
 Only the test suite, the smoke check and the CPU-baseline leg of the benchmark
 may import it.  It shares no code with the HIP library and imports nothing from
@@ -30,17 +31,18 @@ are pinned (none is "parity unpinned").
 
 from .philox import philox4x32_10, philox4x32_10_bigint, MASK32
 from .noise import (key_words, counter_words, uniform_from_word, angle_from_word,
-                    box_muller, noise_words, normals)
-from .bf16 import bf16_to_f64, f64_to_bf16_rne, bf16_ulp
+                    box_muller, noise_words, normals, rounding_draws)
+from .bf16 import bf16_to_f64, f64_to_bf16_rne, f64_to_bf16_sr, bf16_ulp
 from .es import (perturb, restore, swap, zscore, update_coefficient, member_weights,
                  update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
-                 ES_REWARDS_ARE_WEIGHTS)
+                 ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND)
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
     "key_words", "counter_words", "uniform_from_word", "angle_from_word", "box_muller",
-    "noise_words", "normals",
-    "bf16_to_f64", "f64_to_bf16_rne", "bf16_ulp",
+    "noise_words", "normals", "rounding_draws",
+    "bf16_to_f64", "f64_to_bf16_rne", "f64_to_bf16_sr", "bf16_ulp",
     "perturb", "restore", "swap", "zscore", "update_coefficient", "member_weights",
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
+    "ES_UPDATE_STOCHASTIC_ROUND",
 ]

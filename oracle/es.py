@@ -18,7 +18,10 @@ Readings where the paper is silent (each also listed in the design notes):
   * Scalars cross the library boundary as binary32 (sigma, alpha, the z-score
     epsilon, rewards); the oracle takes those binary32 values and does all
     arithmetic on them in fp64.
-  * Every result is rounded to bf16 once, round-to-nearest-even.
+  * Every result is rounded to bf16 once, round-to-nearest-even.  The update
+    optionally rounds stochastically instead (ES_UPDATE_STOCHASTIC_ROUND,
+    with a 64-bit rounding seed; the draws and the rounding are defined in
+    the noise and bf16 modules).
   * sigma = 0 leaves the parameters bit-for-bit unchanged (no -0.0 -> +0.0).
   * A per-member sign s_i in {+1, -1} multiplies eps_i (antithetic pairs);
     s_i = +1 for every member is the paper's one-sided sampling.
@@ -47,11 +50,12 @@ WebArena (Appendix A.1, Limitations).
 
 import numpy as np
 
-from .bf16 import bf16_to_f64, f64_to_bf16_rne
-from .noise import normals
+from .bf16 import bf16_to_f64, f64_to_bf16_rne, f64_to_bf16_sr
+from .noise import normals, rounding_draws
 
 ES_UPDATE_DIV_SIGMA = 1
 ES_REWARDS_ARE_WEIGHTS = 2
+ES_UPDATE_STOCHASTIC_ROUND = 4
 
 
 def _f32(x):
@@ -157,11 +161,13 @@ def member_weights(seeds, signs, z, c):
 
 
 def update(theta_bits, tensor_id, seeds, signs, rewards, alpha, sigma,
-           flags=0, zscore_eps=1e-8, elems=None):
+           flags=0, zscore_eps=1e-8, elems=None, round_seed=0):
     """theta' = RNE_bf16(theta + sum_d w_d eps_d) over distinct seeds d.
 
     rewards are z-scored first unless ES_REWARDS_ARE_WEIGHTS is set, in which
-    case they are used as zhat directly.  Returns (bits, status).
+    case they are used as zhat directly.  With ES_UPDATE_STOCHASTIC_ROUND the
+    sum is rounded stochastically with the draws of round_seed instead.
+    Returns (bits, status).
     """
     seeds = [int(s) for s in seeds]
     signs = [int(s) for s in signs]
@@ -186,7 +192,10 @@ def update(theta_bits, tensor_id, seeds, signs, rewards, alpha, sigma,
     delta = np.zeros(el.size, dtype=np.float64)
     for sd, wd in live:
         delta += wd * normals(sd, tensor_id, el)
-    return f64_to_bf16_rne(bf16_to_f64(theta_bits) + delta), 0
+    x = bf16_to_f64(theta_bits) + delta
+    if flags & ES_UPDATE_STOCHASTIC_ROUND:
+        return f64_to_bf16_sr(x, rounding_draws(round_seed, tensor_id, el)), 0
+    return f64_to_bf16_rne(x), 0
 
 
 def sigma_cosine(sigma0, sigma_T, t, T):

@@ -11,7 +11,8 @@ element of any tensor can be regenerated in isolation:
   counter = (q mod 2^32, q div 2^32, tensor_id, domain)    q = j div 4
   element j of tensor `tensor_id` uses the pair (w0, w1) of the call at
   counter q when j mod 4 is 0 or 1, and the pair (w2, w3) when it is 2 or 3.
-  domain is 0 for the perturbation noise (other values are reserved).
+  domain is 0 for the perturbation noise and 1 for the draws of the update's
+  stochastic rounding (other values are reserved).
 
   m(w) = w mod 2^23 (the low 23 bits of a word)
   radius uniform u(w) = (m(w) + 1/2) * 2^-23, in [2^-24, 1 - 2^-24]
@@ -23,11 +24,17 @@ element of any tensor can be regenerated in isolation:
       first  element of the pair: r cos(phi)
       second element of the pair: r sin(phi)
 
-Pins (tests/test_oracle_noise.py): the word-to-element assignment against the
+Stochastic-rounding draws (domain 1, key from the update's rounding seed):
+one Philox call at counter (g mod 2^32, g div 2^32, tensor_id, 1), g = j div 8,
+serves elements 8g .. 8g+7; element j takes word (j mod 8) div 2, its low 16
+bits when j is even and its high 16 bits when j is odd.
+
+Pins (tests/test_oracle_noise.py, tests/test_oracle_rounding.py): the word-to-element assignment against the
 counter/offset API of PyTorch's and rocRAND's Philox engines; the uniform map's
 closed-form endpoints; hand-worked Box-Muller values; the moments, the
 Kolmogorov-Smirnov distance to N(0,1), the closed-form bound
-|eps| <= sqrt(48 ln 2) and the pair correlation of the generated normals.
+|eps| <= sqrt(48 ln 2) and the pair correlation of the generated normals; the
+rounding draws against the big-integer Philox and their uniformity.
 """
 
 import numpy as np
@@ -35,6 +42,7 @@ import numpy as np
 from .philox import philox4x32_10, MASK32
 
 DOMAIN_NOISE = 0
+DOMAIN_ROUNDING = 1
 
 
 def key_words(seed):
@@ -97,3 +105,15 @@ def normals(seed, tensor_id, elems):
     wb = np.where(first_pair, w[1], w[3])
     e_cos, e_sin = box_muller(wa, wb)
     return np.where(lane % 2 == 0, e_cos, e_sin)
+
+
+def rounding_draws(round_seed, tensor_id, elems):
+    """The 16-bit stochastic-rounding draw of each element index j of one
+    tensor (domain 1): an int64 array with values in [0, 65535]."""
+    elems = np.atleast_1d(np.asarray(elems, dtype=np.uint64))
+    g = elems >> np.uint64(3)
+    w = noise_words(round_seed, tensor_id, g, DOMAIN_ROUNDING)
+    word = (elems >> np.uint64(1)) & np.uint64(3)
+    picked = np.choose(word.astype(np.int64), [w[0], w[1], w[2], w[3]])
+    shift = (elems & np.uint64(1)) * np.uint64(16)
+    return ((picked >> shift) & np.uint64(0xFFFF)).astype(np.int64)
