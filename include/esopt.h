@@ -63,6 +63,7 @@ extern "C" {
 #define ES_UPDATE_DIV_SIGMA     1u  /* c = alpha / (G sigma) (Appendix C.1)
                                        instead of the paper's alpha / G */
 #define ES_REWARDS_ARE_WEIGHTS  2u  /* use rewards as zhat directly (no z-score) */
+#define ES_UPDATE_STOCHASTIC_ROUND 4u /* round the update stochastically (round_seed) */
 
 typedef void* es_stream_t;          /* hipStream_t */
 
@@ -140,7 +141,10 @@ typedef struct es_update_opts {
     float    sigma;       /* sigma_t of this generation; read only with
                              ES_UPDATE_DIV_SIGMA (then finite and > 0) */
     float    zscore_eps;  /* epsilon of the z-score denominator, >= 0 (1e-8) */
-    uint32_t flags;       /* ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS */
+    uint32_t flags;       /* ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
+                             ES_UPDATE_STOCHASTIC_ROUND */
+    uint64_t round_seed;  /* key of the stochastic-rounding draws; read only
+                             with ES_UPDATE_STOCHASTIC_ROUND */
 } es_update_opts_t;
 
 /* Fused reward-weighted update (Section 3; Appendix C.1 with
@@ -153,7 +157,16 @@ typedef struct es_update_opts {
  * the noise of each distinct seed is generated once per element; the sum is
  * accumulated in binary32 registers and theta is read and written once.
  * Seeds with a zero merged weight are skipped, and when no weight is nonzero
- * theta is not written at all.  A non-finite reward leaves theta unchanged
+ * theta is not written at all.
+ * The paper does not state how updates are rounded.  With
+ * ES_UPDATE_STOCHASTIC_ROUND, instead of RNE: x = theta_j + sum (binary32),
+ * and x moves from its truncation toward zero on the bf16 grid one step away
+ * from zero when r_j >= 2^16 - (low 16 bits of x), r_j a 16-bit draw; so the
+ * expected result is x.  Draws: key = (round_seed lo, hi), one Philox4x32-10
+ * call at counter (g lo, g hi, tensor_id, 1), g = j >> 3, serves elements
+ * 8g..8g+7; element j takes word (j & 7) >> 1, low half for even j, high
+ * half for odd j.  Overflow past the largest finite bf16 gives infinity; NaN
+ * gives 0x7FC0.  A non-finite reward leaves theta unchanged
  * and sets the status word to 1.
  *   seeds, signs : host arrays of n_members entries (signs +1 or -1)
  *   rewards_dev  : device array of n_members binary32 rewards

@@ -40,6 +40,7 @@ constexpr uint32_t kPhiloxM1 = 0xCD9E8D57u;
 constexpr uint32_t kWeyl0 = 0x9E3779B9u;
 constexpr uint32_t kWeyl1 = 0xBB67AE85u;
 constexpr uint32_t kDomainNoise = 0u;
+constexpr uint32_t kDomainRounding = 1u;     // draws of the update's stochastic rounding
 
 struct Words {
     uint32_t w0, w1, w2, w3;
@@ -125,6 +126,21 @@ typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
     const f32x2_t v = {lo, hi};
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
+// Two binary32 values rounded to bf16 stochastically, packed low/high, with
+// the 16-bit draws r_lo = draws mod 2^16 and r_hi = draws div 2^16.  Adding
+// r to the binary32 pattern carries into the bf16 part exactly when
+// r >= 2^16 - (low 16 bits), i.e. with probability (low 16 bits) / 2^16:
+// the fraction of a bf16 step by which |x| exceeds its truncation.  The
+// carry out of the largest finite value gives infinity; infinities keep
+// their pattern; NaN becomes the quiet NaN 0x7FC0.
+__device__ __forceinline__ uint32_t pack_bf16x2_sr(float lo, float hi, uint32_t draws) {
+    uint32_t a = __builtin_bit_cast(uint32_t, lo) + (draws & 0xFFFFu);
+    uint32_t b = __builtin_bit_cast(uint32_t, hi) + (draws >> 16);
+    a = (lo != lo) ? 0x7FC00000u : a;
+    b = (hi != hi) ? 0x7FC00000u : b;
+    return (b & 0xFFFF0000u) | (a >> 16);
 }
 
 __device__ __forceinline__ uint16_t to_bf16(float x) {

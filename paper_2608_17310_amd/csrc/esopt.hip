@@ -355,15 +355,21 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
 
 // One tile of the fused update: for each of the lane's groups in turn,
 // acc = sum_d w_d eps_d (binary32, members in table order, zero weights
-// skipped), theta <- RNE(theta + acc), store it.  The kernel is VALU-bound,
-// so one group's registers are live at a time and the number of resident
-// waves hides memory latency; full tiles also prefetch the next group while
-// the current one is computed, which matters when N is small (the two-member
-// swap).
-template <int kThreads, int kU, bool kFast, bool kNT>
+// skipped), theta <- round(theta + acc), store it.  Rounding is to nearest
+// even, or stochastic (kSR) with the draws of one domain-1 Philox call per
+// group under the rounding key.  The kernel is VALU-bound, so one group's
+// registers are live at a time and the number of resident waves hides memory
+// latency; full tiles also prefetch the next group while the current one is
+// computed, which matters when N is small (the two-member swap).
+struct RoundKey {
+    uint32_t k0, k1;
+};
+
+template <int kThreads, int kU, bool kFast, bool kNT, bool kSR>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
-                                            uint32_t n_distinct) {
+                                            uint32_t n_distinct, RoundKey rk) {
     const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t g_hi = static_cast<uint32_t>(r.elem0 >> 35);
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
     uint32_t next[4];
     if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.numel, next);
@@ -391,11 +397,19 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
             group_axpy(w, m.w_k, acc);
         }
         uint32_t out[4];
+        if constexpr (kSR) {
+            const es::Words d = es::philox4x32_10(static_cast<uint32_t>(e >> 3), g_hi, r.tensor_id,
+                                                  es::kDomainRounding, rk.k0, rk.k1);
+            const uint32_t draws[4] = {d.w0, d.w1, d.w2, d.w3};
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const float lo = es::bf16_lo(raw[k]) + acc[2 * k];
-            const float hi = es::bf16_hi(raw[k]) + acc[2 * k + 1];
-            out[k] = es::pack_bf16x2(lo, hi);
+            for (int k = 0; k < 4; ++k)
+                out[k] = es::pack_bf16x2_sr(es::bf16_lo(raw[k]) + acc[2 * k],
+                                            es::bf16_hi(raw[k]) + acc[2 * k + 1], draws[k]);
+        } else {
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                out[k] = es::pack_bf16x2(es::bf16_lo(raw[k]) + acc[2 * k],
+                                         es::bf16_hi(raw[k]) + acc[2 * k + 1]);
         }
         store_group<kFast, kNT>(r.data, e, r.numel, out);
     }
@@ -403,20 +417,23 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
 
 // Fused update over the whole parameter list (member table and header
 // written by es_prepare_kernel): full tiles, then tail tiles.
-template <int kThreads, int kU, bool kNT>
+template <int kThreads, int kU, bool kNT, bool kSR>
 __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTensor* __restrict__ tab,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              const Member* __restrict__ members,
-                                                             const UpdateHeader* __restrict__ hdr) {
+                                                             const UpdateHeader* __restrict__ hdr,
+                                                             RoundKey rk) {
     constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
     if (hdr->n_live == 0u) return;          // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
     uint32_t t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        update_tile<kThreads, kU, true, kNT>(locate_full<kTileElems>(tab, t, tile), members, n_distinct);
+        update_tile<kThreads, kU, true, kNT, kSR>(locate_full<kTileElems>(tab, t, tile), members,
+                                                  n_distinct, rk);
     t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        update_tile<kThreads, kU, false, kNT>(locate_tail<kTileElems>(tab, t, tile), members, n_distinct);
+        update_tile<kThreads, kU, false, kNT, kSR>(locate_tail<kTileElems>(tab, t, tile), members,
+                                                   n_distinct, rk);
 }
 
 // Copy up to 1 KB of host-packed words (passed as kernel arguments) into
@@ -562,7 +579,7 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
 
 using PerturbKernel = void (*)(const DevTensor*, uint64_t, uint64_t, Streams);
 using UpdateKernel = void (*)(const DevTensor*, uint64_t, uint64_t, const Member*,
-                              const UpdateHeader*);
+                              const UpdateHeader*, RoundKey);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
 #define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
@@ -580,9 +597,10 @@ PerturbKernel perturb_kernel(int members, int threads, int groups) {
                         : perturb_kernel_for<2>(threads, groups);
 }
 
-UpdateKernel update_kernel(int threads, int groups) {
-#define ES_CASE(T, U) \
-    if (threads == T && groups == U) return es_update_kernel<T, U, true>;
+UpdateKernel update_kernel(int threads, int groups, bool stochastic) {
+#define ES_CASE(T, U)                                                                     \
+    if (threads == T && groups == U)                                                      \
+        return stochastic ? es_update_kernel<T, U, true, true> : es_update_kernel<T, U, true, false>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -677,7 +695,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     // Launch shape: the defaults, or overrides for launch-shape sweeps.
     int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
     int groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
-    if (update_kernel(threads, groups) == nullptr) {
+    if (update_kernel(threads, groups, false) == nullptr) {
         threads = kDefaultThreads;
         groups = kDefaultGroups;
     }
@@ -800,7 +818,8 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
         return fail(ES_ERR_INVALID_ARG, "es_update: null pointer");
     if (n_members == 0 || n_members > ES_MAX_MEMBERS)
         return fail(ES_ERR_INVALID_ARG, "es_update: n_members out of range");
-    if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS)) != 0)
+    if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
+                         ES_UPDATE_STOCHASTIC_ROUND)) != 0)
         return fail(ES_ERR_INVALID_ARG, "es_update: unknown flags");
     if (!std::isfinite(opts->alpha)) return fail(ES_ERR_INVALID_ARG, "es_update: alpha not finite");
     if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
@@ -867,9 +886,12 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
     if (plan->n_full + plan->n_tail == 0) return ES_OK;
-    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups);
+    const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
+    const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
+                      static_cast<uint32_t>(opts->round_seed >> 32)};
+    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
     hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
-                       plan->n_full, plan->n_tail, members, hdr);
+                       plan->n_full, plan->n_tail, members, hdr, rk);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
     return ES_OK;
@@ -927,11 +949,12 @@ int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_
                        static_cast<uint32_t>(sizeof(table) / 4), chunk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
-    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups);
+    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, false);
     hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
                        plan->n_full, plan->n_tail, reinterpret_cast<const Member*>(dst),
                        reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffSwap +
-                                                             offsetof(decltype(table), h)));
+                                                             offsetof(decltype(table), h)),
+                       RoundKey{0u, 0u});
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_update_kernel (swap) launch");
     return ES_OK;

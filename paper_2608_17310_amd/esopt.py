@@ -29,6 +29,7 @@ ES_ERR_NOMEM = -5
 ES_MAX_MEMBERS = 1024
 ES_UPDATE_DIV_SIGMA = 1
 ES_REWARDS_ARE_WEIGHTS = 2
+ES_UPDATE_STOCHASTIC_ROUND = 4
 
 # Every symbol the header declares, with (restype, argtypes).
 _u32, _u64, _i32, _f32, _f64 = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32,
@@ -41,7 +42,8 @@ class EsTensor(ctypes.Structure):
 
 
 class EsUpdateOpts(ctypes.Structure):
-    _fields_ = [("alpha", _f32), ("sigma", _f32), ("zscore_eps", _f32), ("flags", _u32)]
+    _fields_ = [("alpha", _f32), ("sigma", _f32), ("zscore_eps", _f32), ("flags", _u32),
+                ("round_seed", _u64)]
 
 
 SIGNATURES = {
@@ -178,8 +180,9 @@ class Plan:
                "es_swap")
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
-               z_out=None, status_out=None, stream=None):
-        """Fused update; rewards is a float32 CUDA tensor of len(seeds)."""
+               z_out=None, status_out=None, stream=None, round_seed=0):
+        """Fused update; rewards is a float32 CUDA tensor of len(seeds).
+        round_seed keys the draws of ES_UPDATE_STOCHASTIC_ROUND."""
         n = len(seeds)
         if len(signs) != n:
             raise ValueError("seeds and signs differ in length")
@@ -187,7 +190,10 @@ class Plan:
             raise ValueError("rewards must have one entry per member")
         c_seeds = (_u64 * max(n, 1))(*[int(s) for s in seeds])
         c_signs = (_i32 * max(n, 1))(*[int(s) for s in signs])
-        opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags))
+        if not 0 <= int(round_seed) < (1 << 64):
+            raise ValueError("round_seed must be in [0, 2^64)")
+        opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags),
+                            int(round_seed))
         _check(load().es_update(self.handle, c_seeds, c_signs,
                                 _dev_ptr(rewards, torch.float32, "rewards"), n, ctypes.byref(opts),
                                 _dev_ptr(z_out, torch.float32, "z_out"),

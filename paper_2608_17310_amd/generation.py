@@ -10,7 +10,8 @@ With fused_swap the revert of member i and the apply of member i+1 are one
 pass (es_swap), so a generation of N members makes N + 1 passes over the
 parameters instead of 2N, plus the update.
 
-Only seeds, signs, rewards and scalars are recorded; because every kernel is
+Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
+recorded; because every kernel is
 deterministic, replaying the records from the same starting parameters
 rebuilds the parameters bit for bit (the paper reconstructs its final models
 from the recorded update sequence the same way, Appendix D.2 and D.4).
@@ -34,6 +35,7 @@ class GenerationRecord:
     flags: int = 0
     zscore_eps: float = 1e-8
     fused_swap: bool = True
+    round_seed: int = 0             # key of the update's stochastic rounding
 
 
 def sigma_schedule(sigma0, sigma_T, T):
@@ -63,9 +65,11 @@ def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
 
 
 def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], float],
-                   flags=0, zscore_eps=1e-8, fused_swap=True, stream=None):
+                   flags=0, zscore_eps=1e-8, fused_swap=True, stream=None, round_seed=0):
     """Run one generation; evaluate(i) scores the parameters while member i is
-    applied and returns a float.  Returns the GenerationRecord."""
+    applied and returns a float.  With ES_UPDATE_STOCHASTIC_ROUND in flags the
+    update is rounded with the draws of round_seed (use a new one per
+    generation).  Returns the GenerationRecord."""
     if len(seeds) != len(signs) or not seeds:
         raise ValueError("seeds and signs must be non-empty and of equal length")
     rewards = []
@@ -73,7 +77,8 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
           stream)
     rec = GenerationRecord(list(map(int, seeds)), list(map(int, signs)),
                            [float(torch.tensor(r, dtype=torch.float32)) for r in rewards],
-                           float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap)
+                           float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap,
+                           int(round_seed))
     apply_update(plan, rec, stream)
     return rec
 
@@ -81,7 +86,7 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
 def apply_update(plan, rec: GenerationRecord, stream=None):
     r = torch.tensor(rec.rewards, dtype=torch.float32, device=plan.device)
     plan.update(rec.seeds, rec.signs, r, rec.alpha, sigma=rec.sigma, zscore_eps=rec.zscore_eps,
-                flags=rec.flags, stream=stream)
+                flags=rec.flags, stream=stream, round_seed=rec.round_seed)
 
 
 def replay(plan, records, with_perturbations=True, stream=None):

@@ -1,0 +1,27 @@
+/* A plain C99 consumer of the library's public header: it must compile with
+ * a C compiler (no HIP or C++ types), link against the shared library, and
+ * report the layout of every public struct so the Python binding can be
+ * checked against it.  It makes only calls that fail argument validation
+ * before touching a device, so it runs without a GPU. */
+#include <stddef.h>
+#include <stdio.h>
+
+#include "esopt.h"
+
+int main(void) {
+    printf("es_tensor_t %zu data %zu numel %zu tensor_id %zu reserved %zu\n", sizeof(es_tensor_t),
+           offsetof(es_tensor_t, data), offsetof(es_tensor_t, numel),
+           offsetof(es_tensor_t, tensor_id), offsetof(es_tensor_t, reserved));
+    printf("es_update_opts_t %zu alpha %zu sigma %zu zscore_eps %zu flags %zu round_seed %zu\n",
+           sizeof(es_update_opts_t), offsetof(es_update_opts_t, alpha),
+           offsetof(es_update_opts_t, sigma), offsetof(es_update_opts_t, zscore_eps),
+           offsetof(es_update_opts_t, flags), offsetof(es_update_opts_t, round_seed));
+    printf("flags %u %u %u max_members %u\n", ES_UPDATE_DIV_SIGMA, ES_REWARDS_ARE_WEIGHTS,
+           ES_UPDATE_STOCHASTIC_ROUND, ES_MAX_MEMBERS);
+    es_plan_t* plan = NULL;
+    printf("plan_create_null %d\n", es_plan_create(NULL, 1, &plan));
+    printf("perturb_null %d\n", es_perturb(NULL, 1, 1, 1e-3f, NULL));
+    printf("strerror %s\n", es_strerror(ES_ERR_INVALID_ARG));
+    printf("sigma_cosine %.17g\n", es_sigma_cosine(1e-3, 1e-4, 50, 100));
+    return 0;
+}

@@ -4,6 +4,8 @@ import ctypes
 import math
 import os
 import re
+import shutil
+import subprocess
 
 import numpy as np
 import pytest
@@ -120,3 +122,30 @@ def test_binding_fails_loudly_without_library(tmp_path, monkeypatch):
     monkeypatch.setattr(esopt, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="no CPU fallback"):
         esopt.load()
+
+
+def test_plain_c_consumer_of_header(lib, tmp_path):
+    """The public header compiles as C99, links against the library, and its
+    struct layouts and flag values match the Python binding's."""
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    exe = str(tmp_path / "abi_consumer")
+    src = os.path.join(os.path.dirname(__file__), "harness", "abi_consumer.c")
+    libdir = os.path.dirname(esopt.LIB_PATH)
+    subprocess.run([gcc, "-std=c99", "-Wall", "-Werror", "-I", os.path.dirname(HEADER),
+                    src, "-L", libdir, "-l:" + os.path.basename(esopt.LIB_PATH),
+                    "-Wl,-rpath," + libdir, "-o", exe], check=True)
+    out = subprocess.run([exe], capture_output=True, text=True, check=True).stdout
+    rows = {l.split()[0]: l.split()[1:] for l in out.splitlines()}
+
+    def layout(cls):
+        return [str(ctypes.sizeof(cls))] + [x for f, _ in cls._fields_
+                                           for x in (f, str(getattr(cls, f).offset))]
+    assert rows["es_tensor_t"] == layout(esopt.EsTensor)
+    assert rows["es_update_opts_t"] == layout(esopt.EsUpdateOpts)
+    assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
+                             str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
+    assert rows["plan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
+    assert rows["perturb_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
+    assert float(rows["sigma_cosine"][0]) == lib.es_sigma_cosine(1e-3, 1e-4, 50, 100)

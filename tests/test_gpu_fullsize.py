@@ -65,11 +65,16 @@ def _run(W, n_members=None, samples_per_tensor=256):
     torch.cuda.synchronize()
     upd = _gather(views, idx_dev)
     assert int(status.item()) == 0
+    sr_flags, round_seed = esopt.ES_UPDATE_STOCHASTIC_ROUND, 0x5EED
+    plan.update(seeds, signs, torch.from_numpy(r).cuda(), W.alpha, sigma=sigma, flags=sr_flags,
+                round_seed=round_seed)
+    torch.cuda.synchronize()
+    upd_sr = _gather(views, idx_dev)
     plan.close()
     del flat, views
     torch.cuda.empty_cache()
 
-    reps = {"perturb": [], "swap": [], "restore": [], "update": []}
+    reps = {"perturb": [], "swap": [], "restore": [], "update": [], "update_sr": []}
     for t, el_i in enumerate(idx):
         el = el_i.astype(np.uint64)
         exp = oracle.perturb(theta0[t], seed, t, sign, sigma, elems=el)
@@ -83,6 +88,10 @@ def _run(W, n_members=None, samples_per_tensor=256):
         exp, st = oracle.update(rest[t], t, seeds, signs, r, W.alpha, sigma, elems=el)
         reps["update"].append(report(upd[t], exp, rest[t],
                                      update_delta(t, seeds, signs, r, W.alpha, sigma, 0, el)))
+        exp, st = oracle.update(upd[t], t, seeds, signs, r, W.alpha, sigma, flags=sr_flags,
+                                elems=el, round_seed=round_seed)
+        reps["update_sr"].append(report(upd_sr[t], exp, upd[t],
+                                        update_delta(t, seeds, signs, r, W.alpha, sigma, 0, el)))
     for k, rs in reps.items():
         n = sum(x["n"] for x in rs)
         agg = {

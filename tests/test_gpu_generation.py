@@ -67,8 +67,9 @@ def _fresh(W, stream_seed=0):
     return host, [to_device(b, s) for b, s in zip(host, W.shapes)]
 
 
-@pytest.mark.parametrize("fused", [True, False])
-def test_generation_replay_is_bit_exact(fused):
+@pytest.mark.parametrize("fused,flags", [(True, 0), (False, 0),
+                                         (True, esopt.ES_UPDATE_STOCHASTIC_ROUND)])
+def test_generation_replay_is_bit_exact(fused, flags):
     W = wl.TINY
     host, live = _fresh(W)
     plan = esopt.Plan(live)
@@ -78,7 +79,8 @@ def test_generation_replay_is_bit_exact(fused):
     for t in range(4):
         seeds, signs = antithetic_seeds(100 * t, 3)
         rec = run_generation(plan, seeds, signs, sig[t], 5e-4,
-                             evaluate=lambda i: rng.random(), fused_swap=fused)
+                             evaluate=lambda i: rng.random(), fused_swap=fused, flags=flags,
+                             round_seed=1000 + t)
         records.append(rec)
     torch.cuda.synchronize()
     live_bits = [to_host(t) for t in live]
@@ -99,7 +101,8 @@ def test_generation_replay_is_bit_exact(fused):
         x = b0
         for rec in records:
             x, st = oracle.update(x, tid, rec.seeds, rec.signs,
-                                  np.array(rec.rewards, np.float32), rec.alpha, rec.sigma)
+                                  np.array(rec.rewards, np.float32), rec.alpha, rec.sigma,
+                                  flags=rec.flags, round_seed=rec.round_seed)
         got = to_host(dev)
         ex = oracle.bf16_to_f64(x)
         floor = np.abs(oracle.bf16_to_f64(b0)) / 256

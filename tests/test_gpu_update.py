@@ -24,24 +24,26 @@ def _rewards_dev(r):
     return torch.from_numpy(np.asarray(r, dtype=np.float32)).cuda()
 
 
-def _run_update(bits_list, seeds, signs, rewards, alpha, sigma=1e-3, flags=0, ids=None):
+def _run_update(bits_list, seeds, signs, rewards, alpha, sigma=1e-3, flags=0, ids=None,
+                round_seed=0):
     ts = [to_device(b) for b in bits_list]
     plan = esopt.Plan(ts, tensor_ids=ids)
     status = torch.full((1,), -7, dtype=torch.int32, device="cuda")
     z = torch.zeros(len(seeds), dtype=torch.float32, device="cuda")
     plan.update(seeds, signs, _rewards_dev(rewards), alpha, sigma=sigma, flags=flags,
-                z_out=z, status_out=status)
+                z_out=z, status_out=status, round_seed=round_seed)
     torch.cuda.synchronize()
     out = [to_host(t) for t in ts]
     plan.close()
     return out, int(status.item()), z.cpu().numpy()
 
 
-def _check(bits_list, out, seeds, signs, rewards, alpha, sigma, flags, ids, what):
+def _check(bits_list, out, seeds, signs, rewards, alpha, sigma, flags, ids, what, round_seed=0):
     for i, b in enumerate(bits_list):
         tid = ids[i] if ids else i
         el = np.arange(b.size, dtype=np.uint64)
-        exp, st = oracle.update(b, tid, seeds, signs, rewards, alpha, sigma, flags=flags)
+        exp, st = oracle.update(b, tid, seeds, signs, rewards, alpha, sigma, flags=flags,
+                                round_seed=round_seed)
         rep = report(out[i], exp, b, update_delta(tid, seeds, signs, rewards, alpha, sigma, flags, el))
         print(what, i, rep)
         assert_parity(rep, f"{what} tensor {i}")
@@ -156,3 +158,63 @@ def test_zscore_kernel_edge_cases():
     np.testing.assert_array_equal(z, np.float32([-k, k]))
     z = esopt.zscore(_rewards_dev([1.0, np.nan, 2.0]), status=st).cpu().numpy()
     assert int(st.item()) == 1 and np.all(z == 0)
+
+
+# ------------------------------------------------------- stochastic rounding --
+
+SR = esopt.ES_UPDATE_STOCHASTIC_ROUND
+
+
+@pytest.mark.parametrize("flags", [SR, SR | esopt.ES_UPDATE_DIV_SIGMA, SR | esopt.ES_REWARDS_ARE_WEIGHTS])
+def test_stochastic_rounding_matches_oracle(flags):
+    """Ragged tensors spanning several tiles, large tensor ids, a 64-bit
+    rounding seed; both sides decide on the binary32 sum, so results agree
+    except where the two binary32 sums differ across a draw's threshold."""
+    sizes = [1 << 17, 4096 * 5 + 3, 9, 70001]
+    ids = [0, 3, 1000, (1 << 32) - 1]
+    bits = [wl.random_bf16_bits(n, 60 + i) for i, n in enumerate(sizes)]
+    seeds = [21, 21, 22, 22, 23, 24, 25, 26]
+    signs = [1, -1, 1, -1, 1, 1, 1, 1]
+    r = np.random.default_rng(4).random(8).astype(np.float32)
+    rs = 0xDEADBEEF12345678
+    out, st, _ = _run_update(bits, seeds, signs, r, 5e-4, sigma=1e-3, flags=flags, ids=ids,
+                             round_seed=rs)
+    assert st == 0
+    _check(bits, out, seeds, signs, r, 5e-4, 1e-3, flags, ids, f"sr flags={flags}", round_seed=rs)
+    # the rounding actually differs from round-to-nearest on many elements
+    rne, _, _ = _run_update(bits, seeds, signs, r, 5e-4, sigma=1e-3, flags=flags & ~SR, ids=ids)
+    assert np.mean(out[0] != rne[0]) > 0.05
+
+
+def test_stochastic_rounding_unaligned_view_and_seed_dependence():
+    bits = wl.random_bf16_bits(50001, 70)
+    seeds, signs = [5, 6, 7], [1, 1, 1]
+    r = np.array([0.2, 0.9, 0.4], np.float32)
+    outs = {}
+    for rs in (1, 2, 1):
+        buf = to_device(bits)
+        view = buf[5:]
+        plan = esopt.Plan([view])
+        plan.update(seeds, signs, _rewards_dev(r), 5e-4, flags=SR, round_seed=rs)
+        torch.cuda.synchronize()
+        got = to_host(view)
+        assert to_host(buf[:5]).tolist() == bits[:5].tolist()
+        plan.close()
+        if rs in outs:
+            np.testing.assert_array_equal(got, outs[rs])        # deterministic
+        outs[rs] = got
+        b = bits[5:]
+        el = np.arange(b.size, dtype=np.uint64)
+        exp, _ = oracle.update(b, 0, seeds, signs, r, 5e-4, 0.0, flags=SR, round_seed=rs)
+        rep = report(got, exp, b, update_delta(0, seeds, signs, r, 5e-4, 0.0, 0, el))
+        assert_parity(rep, f"sr unaligned round_seed={rs}")
+    assert np.mean(outs[1] != outs[2]) > 0.05
+
+
+def test_stochastic_rounding_identities():
+    bits = wl.random_bf16_bits(20000, 71)
+    # equal rewards: zero weights, theta untouched; alpha = 0 likewise
+    out, st, _ = _run_update([bits], [1, 2], [1, 1], [0.5, 0.5], 5e-4, flags=SR, round_seed=3)
+    np.testing.assert_array_equal(out[0], bits)
+    out, st, _ = _run_update([bits], [1, 2], [1, 1], [0.1, 0.5], 0.0, flags=SR, round_seed=3)
+    np.testing.assert_array_equal(out[0], bits)
