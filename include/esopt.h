@@ -116,13 +116,18 @@ int es_restore(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_str
 
 /* Move the perturbation from one member to the next in one pass (Section 3;
  * Appendix D.6 -- revert member a after its evaluation, apply member b):
- *   theta_j <- RNE_bf16(theta_j - sign_from sigma_from eps_j(seed_from)
- *                               + sign_to   sigma_to   eps_j(seed_to))
- * one read and one write per element, both noise streams generated in
- * registers and summed in binary32.  Equivalent to es_restore(from) then
- * es_perturb(to) but with one bf16 rounding instead of two.  Equal seeds
- * merge; when the net weight is zero theta is left unchanged and nothing is
- * launched.  Signs +1 or -1; sigmas finite and >= 0. */
+ *   mid_j   = RNE_bf16(theta_j - sign_from sigma_from eps_j(seed_from))
+ *   theta_j <- RNE_bf16(mid_j + sign_to sigma_to eps_j(seed_to))
+ * with one read and one write per element, both noise streams generated in
+ * registers and the intermediate rounded in registers: the result is bit for
+ * bit that of es_restore(from) followed by es_perturb(to), at half the
+ * memory traffic.  Rounding the intermediate keeps a walk over many members
+ * anchored to the starting parameters (a revert that stays in the value's
+ * binade lands exactly on it), where a single rounding of
+ * theta - a + b would accumulate each member's rounding error.  The same
+ * seed on both sides (an antithetic partner) generates its noise once.  A
+ * zero sigma makes its half the identity; both zero launches nothing.
+ * Signs +1 or -1; sigmas finite and >= 0. */
 int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
             uint64_t seed_to, int32_t sign_to, float sigma_to, es_stream_t stream);
 

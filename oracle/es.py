@@ -89,30 +89,19 @@ def restore(theta_bits, seed, tensor_id, sign, sigma, elems=None):
 
 def swap(theta_bits, tensor_id, seed_from, sign_from, sigma_from, seed_to, sign_to,
          sigma_to, elems=None):
-    """Move the perturbation from one member to the next in one step:
-    theta' = RNE_bf16(theta - s_a sigma_a eps_a + s_b sigma_b eps_b).
+    """Move the perturbation from member a to member b: the revert of a
+    followed by the apply of b (Section 3; Appendix D.6), each rounded to
+    bf16 as the separate calls would be,
+    theta' = RNE_bf16(RNE_bf16(theta - s_a sigma_a eps_a) + s_b sigma_b eps_b).
 
-    This is the revert of member a followed by the apply of member b
-    (Section 3; Appendix D.6) with one rounding instead of two.  Equal seeds
-    merge into one weight; a zero merged weight contributes nothing, and when
-    nothing is left theta is returned unchanged.
+    Rounding the intermediate is what lets a walk over many members come
+    back to its starting parameters: where a perturbation stays in the
+    parameter's binade, the revert lands exactly on the starting bf16 value,
+    so rounding errors do not accumulate from member to member (a single
+    rounding of theta - a + b would carry each member's error into the next).
     """
-    for sg in (sign_from, sign_to):
-        if sg not in (1, -1):
-            raise ValueError("sign must be +1 or -1")
-    theta_bits = np.asarray(theta_bits, dtype=np.uint16).ravel()
-    terms = {}
-    for seed, w in ((int(seed_from), -sign_from * _f32(sigma_from)),
-                    (int(seed_to), sign_to * _f32(sigma_to))):
-        terms[seed] = terms.get(seed, 0.0) + w
-    live = [(sd, w) for sd, w in terms.items() if w != 0.0]
-    if not live:
-        return theta_bits.copy()
-    el = _elems(theta_bits, elems)
-    delta = np.zeros(el.size, dtype=np.float64)
-    for sd, w in live:
-        delta += w * normals(sd, tensor_id, el)
-    return f64_to_bf16_rne(bf16_to_f64(theta_bits) + delta)
+    mid = restore(theta_bits, seed_from, tensor_id, sign_from, sigma_from, elems=elems)
+    return perturb(mid, seed_to, tensor_id, sign_to, sigma_to, elems=elems)
 
 
 def zscore(rewards, eps=1e-8):

@@ -85,17 +85,27 @@ __device__ __forceinline__ float unit_interval_plus_one(uint32_t w) {
     return __uint_as_float((w & 0x007FFFFFu) | 0x3F800000u);
 }
 
+// Box-Muller on one word pair, in two parts: the radius factor
+// sqrt(-log2 u) (the radius divided by sqrt(2 ln 2)) from the first word,
+// and cos / sin of the angle from the second.
+__device__ __forceinline__ float pair_radius(uint32_t wa) {
+    const float u = unit_interval_plus_one(wa) - 0x1.fffffep-1f;   // (m + 1/2) 2^-23, exact
+    return __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u));
+}
+__device__ __forceinline__ void pair_angle(uint32_t wb, float& c, float& s) {
+    const float turns = unit_interval_plus_one(wb);                // 1 + v: same sin / cos as v
+    c = __builtin_amdgcn_cosf(turns);
+    s = __builtin_amdgcn_sinf(turns);
+}
+
 // Box-Muller on one word pair, scaled: the pair's two normals times `scale`
 // are t * c and t * s.  t = scale sqrt(2 ln 2) sqrt(-log2 u) is returned
 // separately so the caller applies each normal with one FMA.
 // scale_k must be scale * kSqrt2Ln2.
 __device__ __forceinline__ void scaled_pair(uint32_t wa, uint32_t wb, float scale_k, float& t,
                                             float& c, float& s) {
-    const float u = unit_interval_plus_one(wa) - 0x1.fffffep-1f;   // (m + 1/2) 2^-23, exact
-    const float turns = unit_interval_plus_one(wb);                // 1 + v: same sin / cos as v
-    t = scale_k * __builtin_amdgcn_sqrtf(-__builtin_amdgcn_logf(u));
-    c = __builtin_amdgcn_cosf(turns);
-    s = __builtin_amdgcn_sinf(turns);
+    t = scale_k * pair_radius(wa);
+    pair_angle(wb, c, s);
 }
 
 // The four normals of one Philox call, in element order 4q .. 4q+3.

@@ -108,8 +108,7 @@ constexpr size_t kOffMembersIn = 0;
 constexpr size_t kOffDistinctIn = kOffMembersIn + sizeof(MemberIn) * ES_MAX_MEMBERS;
 constexpr size_t kOffMembers = kOffDistinctIn + sizeof(DistinctIn) * ES_MAX_MEMBERS;
 constexpr size_t kOffHeader = kOffMembers + sizeof(Member) * ES_MAX_MEMBERS;
-constexpr size_t kOffSwap = kOffHeader + 256;       // es_swap: 2 members + header
-constexpr size_t kScratchBytes = kOffSwap + 256;
+constexpr size_t kScratchBytes = kOffHeader + 256;
 
 constexpr int kStageWords = 256;            // 1 KB of kernel arguments per launch
 struct StageChunk {
@@ -199,15 +198,29 @@ __device__ __forceinline__ void group_axpy(const uint32_t w[8], float scale_k, f
     }
 }
 
-// Noise streams applied by one perturb-style pass: theta + sum_m c_m eps_m
-// for m < M (M = 1: perturb / restore; M = 2: swap).  coef_k = c sqrt(2 ln 2).
+// Noise streams applied by one perturb-style pass.  kM = 1: one stream,
+// theta <- RNE(theta + c_0 eps_0) (perturb / restore).  kM = 2: two streams
+// applied in turn with a bf16 rounding in between,
+// theta <- RNE(RNE(theta + c_0 eps_0) + c_1 eps_1), which is es_restore of
+// one member followed by es_perturb of the next, bit for bit, in one pass
+// (swap).  kM = 3: the same with both streams on one key (an antithetic
+// partner), whose noise is generated once.  coef_k = c sqrt(2 ln 2).
 struct Streams {
     uint32_t k0[2], k1[2];
     float coef_k[2];
 };
 
+__device__ __forceinline__ void round_to_bf16(float x[8]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t b = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
+        x[2 * k] = es::bf16_lo(b);
+        x[2 * k + 1] = es::bf16_hi(b);
+    }
+}
+
 // Apply the streams to one 8-element group in registers and pack to bf16.
-// The binary32 value accumulates each stream with one FMA per element.
+// Each stream adds one FMA per element to the binary32 value.
 template <int kM>
 __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e, uint32_t q_hi,
                                               uint32_t tensor_id, const Streams& st,
@@ -218,11 +231,33 @@ __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e,
         x[2 * k] = es::bf16_lo(raw[k]);
         x[2 * k + 1] = es::bf16_hi(raw[k]);
     }
-#pragma unroll
-    for (int m = 0; m < kM; ++m) {
+    if constexpr (kM == 3) {
         uint32_t w[8];
-        group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, st.k0[m], st.k1[m], w);
-        group_axpy(w, st.coef_k[m], x);
+        group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, st.k0[0], st.k1[0], w);
+        float r[4], c[4], sn[4];
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+            r[p] = es::pair_radius(w[2 * p]);
+            es::pair_angle(w[2 * p + 1], c[p], sn[p]);
+        }
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            if (m == 1) round_to_bf16(x);
+#pragma unroll
+            for (int p = 0; p < 4; ++p) {
+                const float t = st.coef_k[m] * r[p];
+                x[2 * p] = __builtin_fmaf(t, c[p], x[2 * p]);
+                x[2 * p + 1] = __builtin_fmaf(t, sn[p], x[2 * p + 1]);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < kM; ++m) {
+            if (m > 0) round_to_bf16(x);
+            uint32_t w[8];
+            group_words(static_cast<uint32_t>(e >> 2), q_hi, tensor_id, st.k0[m], st.k1[m], w);
+            group_axpy(w, st.coef_k[m], x);
+        }
     }
 #pragma unroll
     for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
@@ -360,7 +395,7 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
 // group under the rounding key.  The kernel is VALU-bound, so one group's
 // registers are live at a time and the number of resident waves hides memory
 // latency; full tiles also prefetch the next group while the current one is
-// computed, which matters when N is small (the two-member swap).
+// computed, which matters when N is small.
 struct RoundKey {
     uint32_t k0, k1;
 };
@@ -592,9 +627,14 @@ PerturbKernel perturb_kernel_for(int threads, int groups) {
     return nullptr;
 }
 
-PerturbKernel perturb_kernel(int members, int threads, int groups) {
-    return members == 1 ? perturb_kernel_for<1>(threads, groups)
-                        : perturb_kernel_for<2>(threads, groups);
+// streams: 1 (perturb / restore), 2 (swap, two keys), 3 (swap, one key)
+PerturbKernel perturb_kernel(int streams, int threads, int groups) {
+    switch (streams) {
+        case 1: return perturb_kernel_for<1>(threads, groups);
+        case 2: return perturb_kernel_for<2>(threads, groups);
+        case 3: return perturb_kernel_for<3>(threads, groups);
+        default: return nullptr;
+    }
 }
 
 UpdateKernel update_kernel(int threads, int groups, bool stochastic) {
@@ -623,7 +663,6 @@ struct es_plan {
     int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
     int groups = kDefaultGroups;    // 8-element groups per lane per tile
     uint64_t tile_elems = 0;        // threads * groups * 8
-    bool swap_streams = true;       // es_swap runs the two-stream perturb kernel
     DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
@@ -651,16 +690,20 @@ int check_device(const es_plan_t* p) {
 
 // One perturb-style pass applying `members` (1 or 2) noise streams with
 // coefficients coef[m] (sign sigma), nothing skipped.
-int launch_streams(es_plan_t* p, int members, const uint64_t* seed, const double* coef,
+// One pass of the perturb kernel: streams = 1 (seed[0], coef[0]), 2 (two
+// keys) or 3 (both coefficients on seed[0]).
+int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double* coef,
                    hipStream_t s) {
     if (p->n_full + p->n_tail == 0) return ES_OK;
     Streams st = {};
-    for (int m = 0; m < members; ++m) {
-        st.k0[m] = static_cast<uint32_t>(seed[m]);
-        st.k1[m] = static_cast<uint32_t>(seed[m] >> 32);
+    const int terms = streams == 1 ? 1 : 2;
+    for (int m = 0; m < terms; ++m) {
+        const uint64_t sd = streams == 3 ? seed[0] : seed[m];
+        st.k0[m] = static_cast<uint32_t>(sd);
+        st.k1[m] = static_cast<uint32_t>(sd >> 32);
         st.coef_k[m] = static_cast<float>(coef[m] * kSqrt2Ln2Double);
     }
-    const PerturbKernel kernel = perturb_kernel(members, p->threads, p->groups);
+    const PerturbKernel kernel = perturb_kernel(streams, p->threads, p->groups);
     hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_full,
                        p->n_tail, st);
     const hipError_t e = hipGetLastError();
@@ -739,7 +782,6 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
     const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
     const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
-    p->swap_streams = env_int("ESOPT_SWAP_STREAMS", 1, 0, 1) != 0;
     p->threads = threads;
     p->groups = groups;
     p->tile_elems = tile_elems;
@@ -905,59 +947,26 @@ int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_
     if (!std::isfinite(sigma_from) || sigma_from < 0.0f || !std::isfinite(sigma_to) ||
         sigma_to < 0.0f)
         return fail(ES_ERR_INVALID_ARG, "es_swap: sigmas must be finite and >= 0");
-    // Two weighted noise terms, merged when the seeds coincide.
-    uint64_t seeds[2] = {seed_from, seed_to};
-    double w[2] = {-double(sign_from) * double(sigma_from), double(sign_to) * double(sigma_to)};
-    uint32_t nd = 2;
-    if (seed_from == seed_to) {
-        w[0] += w[1];
-        nd = 1;
+    // es_restore(from) then es_perturb(to); a zero sigma makes its half the
+    // identity, as in those calls, and its stream is dropped.
+    uint64_t sd[2];
+    double cf[2];
+    int m = 0;
+    if (sigma_from != 0.0f) {
+        sd[m] = seed_from;
+        cf[m] = sign_from > 0 ? -double(sigma_from) : double(sigma_from);
+        ++m;
     }
-    struct {
-        Member m[2];
-        UpdateHeader h;
-    } table = {};
-    uint32_t live = 0;
-    for (uint32_t d = 0; d < nd; ++d) {
-        const float wk = static_cast<float>(w[d] * kSqrt2Ln2Double);
-        table.m[d] = Member{static_cast<uint32_t>(seeds[d]), static_cast<uint32_t>(seeds[d] >> 32), wk, 0u};
-        live += (wk != 0.0f) ? 1u : 0u;
+    if (sigma_to != 0.0f) {
+        sd[m] = seed_to;
+        cf[m] = sign_to > 0 ? double(sigma_to) : -double(sigma_to);
+        ++m;
     }
-    if (live == 0 || plan->n_full + plan->n_tail == 0) return ES_OK;   // theta unchanged
-    table.h = UpdateHeader{nd, live, 0, 0u};
-    int rc = check_device(plan);
+    if (m == 0) return ES_OK;
+    const int rc = check_device(plan);
     if (rc != ES_OK) return rc;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    if (plan->swap_streams) {
-        // the memory-streaming kernel with one or two noise streams
-        uint64_t sd[2];
-        double cf[2];
-        int m = 0;
-        for (uint32_t d = 0; d < nd; ++d)
-            if (table.m[d].w_k != 0.0f) {
-                sd[m] = seeds[d];
-                cf[m] = w[d];
-                ++m;
-            }
-        return launch_streams(plan, m, sd, cf, s);
-    }
-    static_assert(sizeof(table) % 4 == 0 && sizeof(table) <= 4 * kStageWords, "swap table size");
-    StageChunk chunk;
-    std::memcpy(chunk.words, &table, sizeof(table));
-    auto* dst = reinterpret_cast<uint32_t*>(plan->d_scratch + kOffSwap);
-    hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s, dst,
-                       static_cast<uint32_t>(sizeof(table) / 4), chunk);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
-    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, false);
-    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
-                       plan->n_full, plan->n_tail, reinterpret_cast<const Member*>(dst),
-                       reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffSwap +
-                                                             offsetof(decltype(table), h)),
-                       RoundKey{0u, 0u});
-    e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_update_kernel (swap) launch");
-    return ES_OK;
+    const int streams = (m == 2 && sd[0] == sd[1]) ? 3 : m;
+    return launch_streams(plan, streams, sd, cf, static_cast<hipStream_t>(stream));
 }
 
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T) {

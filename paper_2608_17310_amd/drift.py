@@ -1,0 +1,111 @@
+"""How far in-place bf16 perturb/restore walks move the parameters.
+
+Section 3 and Appendix D.6 of arXiv 2608.17310 apply theta + sigma eps_i in
+place, evaluate, and revert by subtracting the regenerated perturbation.  With
+bf16 storage the revert cannot be exact: round-to-nearest is many-to-one, so
+some elements come back one bf16 step away from where they started.  This
+tool measures that drift on a parameter set with no update at all: each
+generation walks N members (perturb, revert; or perturb, N-1 fused swaps,
+revert), and after selected generations it reports, against the starting
+parameters, the fraction of elements changed, the RMS drift in units of
+sigma and of the starting value's bf16 spacing, the largest drift in
+spacings, and whether magnitudes shrink or grow on average (spacings are
+those of the larger of the start and end values, so a start of exactly 0 is
+measured on the grid where it ended).  For scale it
+also prints the RMS of one update step, alpha / sqrt(G) for z-scored rewards.
+
+    python -m paper_2608_17310_amd.drift --workload dense-4b --generations 70 --members 8
+
+Every pass runs in the library's kernels; the statistics are PyTorch
+reductions on the device.  One JSON line per (walk, checkpoint).
+"""
+
+import argparse
+import json
+import math
+import sys
+
+import torch
+
+from . import esopt, workloads as wl
+from .generation import _walk
+
+CHECKPOINTS = (1, 2, 5, 10, 20, 35, 50, 70, 100, 200)
+
+
+def _bf16_spacing(x):
+    """bf16 spacing at |x| (float32 tensor): 2^(e-7) for |x| in [2^e, 2^(e+1)),
+    floored at the subnormal spacing 2^-133."""
+    _, e = torch.frexp(x.abs())
+    lead = torch.clamp(e.to(torch.int32) - 1, min=-126)
+    lead = torch.where(x == 0, torch.full_like(lead, -126), lead)
+    return torch.ldexp(torch.ones_like(x), (lead - 7).to(torch.float32))
+
+
+def drift_stats(views, start, sigma):
+    n = 0
+    changed = 0
+    sq = 0.0
+    ulps_sum = 0.0
+    ulps_max = 0.0
+    over_one = 0
+    mag = 0.0
+    for v, s in zip(views, start):
+        a = v.reshape(-1).float()
+        b = s.reshape(-1).float()
+        d = a - b
+        n += a.numel()
+        changed += int((v.reshape(-1).view(torch.int16) != s.reshape(-1).view(torch.int16)).sum())
+        sq += float((d.double() ** 2).sum())
+        u = d.abs() / _bf16_spacing(torch.maximum(a.abs(), b.abs()))
+        ulps_sum += float(u.double().sum())
+        ulps_max = max(ulps_max, float(u.max()))
+        over_one += int((u > 1.0).sum())
+        mag += float((a.abs() - b.abs()).double().sum())
+    return {
+        "changed": changed / n,
+        "rms_over_sigma": math.sqrt(sq / n) / sigma,
+        "mean_spacings": ulps_sum / n,
+        "max_spacings": ulps_max,
+        "beyond_one_spacing": over_one / n,
+        "mean_magnitude_change_over_sigma": mag / n / sigma,
+    }
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--workload", default="dense-4b", choices=sorted(wl.WORKLOADS))
+    ap.add_argument("--generations", type=int, default=70)
+    ap.add_argument("--members", type=int, default=8)
+    ap.add_argument("--sigma", type=float, default=1e-3)
+    ap.add_argument("--alpha", type=float, default=5e-4)
+    ap.add_argument("--walks", default="restore,swap")
+    args = ap.parse_args(argv)
+    W = wl.WORKLOADS[args.workload]
+    torch.cuda.set_device(0)
+    flat, views = wl.device_params(W)
+    start_flat = flat.clone()
+    offs, _ = wl.flat_layout(W.numels)
+    start = [start_flat[o:o + n] for o, n in zip(offs, W.numels)]
+    print(json.dumps({"workload": W.name, "params": W.n_params, "members": args.members,
+                      "sigma": args.sigma, "update_step_rms": args.alpha / math.sqrt(args.members)}),
+          flush=True)
+    for walk in args.walks.split(","):
+        flat.copy_(start_flat)
+        plan = esopt.Plan(views)
+        for g in range(1, args.generations + 1):
+            seeds = [1_000_003 * g + i for i in range(args.members)]
+            _walk(plan, seeds, [1] * args.members, args.sigma, walk == "swap",
+                  lambda i: None, None)
+            if g in CHECKPOINTS or g == args.generations:
+                torch.cuda.synchronize()
+                row = {"walk": walk, "generation": g,
+                       "roundings": g * (2 * args.members if walk == "restore" else args.members + 1)}
+                row.update(drift_stats(views, start, args.sigma))
+                print(json.dumps(row), flush=True)
+        plan.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

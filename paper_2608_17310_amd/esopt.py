@@ -173,7 +173,8 @@ class Plan:
                "es_restore")
 
     def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
-        """Revert member `from` and apply member `to` in one pass."""
+        """Revert member `from` and apply member `to` in one pass: the same
+        bits as restore(from) followed by perturb(to)."""
         sigma_to = sigma if sigma_to is None else sigma_to
         _check(load().es_swap(self.handle, int(seed_from), int(sign_from), float(sigma),
                               int(seed_to), int(sign_to), float(sigma_to), _stream(stream)),

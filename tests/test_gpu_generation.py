@@ -1,5 +1,7 @@
 """es_swap against the oracle, and the generation driver / replay: a live run
 over several generations is rebuilt bit for bit from its records."""
+import json
+
 import numpy as np
 import pytest
 import torch
@@ -22,8 +24,6 @@ def _gpu():
 
 def _swap_delta(tid, a, sa, b, sb, sigma, el):
     s32 = float(np.float32(sigma))
-    if a == b:
-        return (sb - sa) * s32 * oracle.normals(a, tid, el)
     return -sa * s32 * oracle.normals(a, tid, el) + sb * s32 * oracle.normals(b, tid, el)
 
 
@@ -43,23 +43,37 @@ def test_swap_matches_oracle(sizes):
     plan.close()
 
 
-def test_swap_unaligned_and_identity():
-    bits = wl.random_bf16_bits(30001, 90)
-    buf = to_device(bits)
-    view = buf[3:]
-    plan = esopt.Plan([view])
-    plan.swap(7, 1, 7, 1, 1e-3)                  # same member: nothing to do
+@pytest.mark.parametrize("case", [
+    (31, 1, 1e-3, 32, -1, 1e-3),        # two keys
+    (7, 1, 1e-3, 7, -1, 1e-3),          # antithetic partner: one key, noise generated once
+    (7, 1, 1e-3, 7, 1, 1e-3),           # the same member: restore then perturb again
+    (9, -1, 2e-3, 10, 1, 5e-4),         # different sigmas
+    (9, 1, 0.0, 10, 1, 1e-3),           # zero sigma halves
+    (9, 1, 1e-3, 10, 1, 0.0),
+])
+def test_swap_is_restore_then_perturb_bit_for_bit(case):
+    a, sa, siga, b, sb, sigb = case
+    bits = [wl.random_bf16_bits(n, 85 + i) for i, n in enumerate([1 << 18, 4097, 30001])]
+    one = [to_device(x) for x in bits]
+    two = [to_device(x) for x in bits]
+    views1 = [one[0], one[1], one[2][3:]]
+    views2 = [two[0], two[1], two[2][3:]]
+    p1, p2 = esopt.Plan(views1), esopt.Plan(views2)
+    p1.swap(a, sa, b, sb, siga, sigma_to=sigb)
+    p2.restore(a, sa, siga)
+    p2.perturb(b, sb, sigb)
     torch.cuda.synchronize()
-    np.testing.assert_array_equal(to_host(buf), bits)
-    plan.swap(7, 1, 7, -1, 2e-3)                 # antithetic partner: weight -2 sigma
-    torch.cuda.synchronize()
-    b = bits[3:]
-    el = np.arange(b.size, dtype=np.uint64)
-    exp = oracle.swap(b, 0, 7, 1, 2e-3, 7, -1, 2e-3)
-    rep = report(to_host(view), exp, b, -2 * float(np.float32(2e-3)) * oracle.normals(7, 0, el))
-    assert_parity(rep, "antithetic swap")
-    assert to_host(buf[:3]).tolist() == bits[:3].tolist()
-    plan.close()
+    for i, (x, y) in enumerate(zip(one, two)):
+        np.testing.assert_array_equal(to_host(x), to_host(y))
+        el = np.arange(bits[i].size - (3 if i == 2 else 0), dtype=np.uint64)
+        src = bits[i][3:] if i == 2 else bits[i]
+        got = to_host(x)[3:] if i == 2 else to_host(x)
+        exp = oracle.swap(src, i, a, sa, siga, b, sb, sigb)
+        rep = report(got, exp, src, _swap_delta(i, a, sa, b, sb, max(siga, sigb), el))
+        assert_parity(rep, f"swap {case} tensor {i}")
+    assert to_host(one[2][:3]).tolist() == bits[2][:3].tolist()
+    p1.close()
+    p2.close()
 
 
 def _fresh(W, stream_seed=0):
@@ -144,3 +158,31 @@ def test_generation_matches_oracle_sequence():
                                oracle.bf16_to_f64(got)[bad[:5]], scale[bad[:5]])
     assert rec.rewards == [float(r) for r in rewards]
     plan.close()
+
+
+def test_drift_study_matches_oracle_walk(capsys):
+    """The drift tool's first restore-walk checkpoint on the tiny set: its
+    changed-element fraction agrees with the oracle's perturb/restore chain
+    over the same members."""
+    from paper_2608_17310_amd import drift
+    assert drift.main(["--workload", "tiny-1m", "--generations", "2", "--members", "4"]) == 0
+    rows = [json.loads(l) for l in capsys.readouterr().out.splitlines() if l.startswith("{")]
+    first = [r for r in rows if r.get("walk") == "restore" and r["generation"] == 1][0]
+    W = wl.TINY
+    flat, views = wl.device_params(W)          # the tool's starting parameters
+    start = [to_host(v) for v in views]
+    del flat, views
+    changed = 0
+    for tid, b in enumerate(start):
+        x = b
+        for i in range(4):
+            x = oracle.perturb(x, 1_000_003 + i, tid, 1, 1e-3)
+            x = oracle.restore(x, 1_000_003 + i, tid, 1, 1e-3)
+        changed += int(np.sum(x != b))
+    frac = changed / W.n_params
+    print("drift gen 1: gpu", first["changed"], "oracle", frac)
+    assert abs(first["changed"] - frac) < 2e-4
+    assert 0.0 < frac < 0.5
+    swap = [r for r in rows if r.get("walk") == "swap" and r["generation"] == 2][0]
+    rest = [r for r in rows if r.get("walk") == "restore" and r["generation"] == 2][0]
+    assert swap["roundings"] == 10 and rest["roundings"] == 16
