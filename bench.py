@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
     ap.add_argument("--swap", action="store_true",
                     help="move between members with the fused es_swap (N+1 passes per step)")
+    ap.add_argument("--stochastic-round", action="store_true",
+                    help="round the update stochastically (ES_UPDATE_STOCHASTIC_ROUND)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -171,6 +173,7 @@ def main():
         return
 
     ev = []   # (kind, start, end) event pairs inside the timed region
+    update_flags = esopt.ES_UPDATE_STOCHASTIC_ROUND if args.stochastic_round else 0
 
     def timed_call(kind, record, fn, *a):
         if record:
@@ -200,7 +203,8 @@ def main():
             a = torch.cuda.Event(enable_timing=True)
             b = torch.cuda.Event(enable_timing=True)
             a.record(stream)
-        plan.update(seeds, signs, rewards_all[t], W.alpha, sigma=sigma)
+        plan.update(seeds, signs, rewards_all[t], W.alpha, sigma=sigma, flags=update_flags,
+                    round_seed=1000 + t)
         if record:
             b.record(stream)
             ev.append(("es_update", a, b))
@@ -263,6 +267,7 @@ def main():
         "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
                    "member_moves": "es_swap" if args.swap else "es_perturb/es_restore",
+                   "update_rounding": "stochastic" if args.stochastic_round else "nearest-even",
                    "counting": ("value = (N+2) P / step time: perturb, N-1 fused swaps, restore "
                                 "and one fused N-member update pass per step") if args.swap else
                                ("value = (2N+1) P / step time: 2N perturb/restore passes "

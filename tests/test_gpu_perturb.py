@@ -149,3 +149,40 @@ def test_invalid_arguments_raise():
     with pytest.raises(esopt.EsError):
         plan.perturb(1, 1, float("nan"))
     plan.close()
+
+
+@pytest.mark.parametrize("shape", [(256, 4, 1, 1), (512, 8, 2, 3), (1024, 4, 1, 8), (256, 8, 4, 2)])
+def test_results_do_not_depend_on_launch_shape(shape, monkeypatch):
+    """Noise is a function of (seed, tensor, element) only, so the tile shape
+    and grid (environment overrides read at plan creation) change no bit of
+    perturb, swap, restore or update (both roundings)."""
+    threads, groups, wg_p, wg_u = shape
+    sizes = [300001, 1 << 16, 4097, 9]
+    bits = [wl.random_bf16_bits(n, 90 + i) for i, n in enumerate(sizes)]
+    r = torch.tensor([0.3, 0.9, 0.1, 0.5], dtype=torch.float32, device="cuda")
+
+    def run():
+        ts = [to_device(b) for b in bits]
+        views = [ts[0][1:], ts[1], ts[2], ts[3]]
+        plan = esopt.Plan(views)
+        out = []
+        plan.perturb(3, 1, 1e-3)
+        plan.swap(3, 1, 4, -1, 1e-3)
+        plan.restore(4, -1, 1e-3)
+        out.append([to_host(t) for t in ts])
+        plan.update([1, 2, 2, 5], [1, 1, -1, 1], r, 5e-4)
+        plan.update([1, 2, 2, 5], [1, 1, -1, 1], r, 5e-4, flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+                    round_seed=77)
+        torch.cuda.synchronize()
+        out.append([to_host(t) for t in ts])
+        plan.close()
+        return out
+
+    ref = run()
+    for k, v in (("ESOPT_THREADS", threads), ("ESOPT_GROUPS", groups),
+                 ("ESOPT_PERTURB_WG_PER_CU", wg_p), ("ESOPT_UPDATE_WG_PER_CU", wg_u)):
+        monkeypatch.setenv(k, str(v))
+    got = run()
+    for a, b in zip(ref, got):
+        for x, y in zip(a, b):
+            np.testing.assert_array_equal(x, y)
