@@ -25,6 +25,10 @@ The paper names no generator and no transform; Philox4x32-10 is the published
 generator of Salmon, Moraes, Dror and Shaw (SC'11) and Box-Muller the textbook
 transform of Box and Muller (1958).
 
+The int8 path (quant.py) perturbs and updates symmetric int8 codes with
+per-row scales in units of the quantum, rounding offsets stochastically; the
+paper lists quantized ES as future work (Appendix A.2).
+
 Pin status of every function is listed in the module docstrings; all functions
 are pinned (none is "parity unpinned").
 """
@@ -36,6 +40,8 @@ from .bf16 import bf16_to_f64, f64_to_bf16_rne, f64_to_bf16_sr, bf16_ulp
 from .es import (perturb, restore, swap, zscore, update_coefficient, member_weights,
                  update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
                  ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND)
+from .quant import (QMAX, row_scales, round_offset, offset_values, qperturb, qrestore,
+                    update_values, qupdate)
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
@@ -45,4 +51,5 @@ __all__ = [
     "perturb", "restore", "swap", "zscore", "update_coefficient", "member_weights",
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
     "ES_UPDATE_STOCHASTIC_ROUND",
+    "QMAX", "row_scales", "round_offset", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
 ]

@@ -11,8 +11,9 @@ element of any tensor can be regenerated in isolation:
   counter = (q mod 2^32, q div 2^32, tensor_id, domain)    q = j div 4
   element j of tensor `tensor_id` uses the pair (w0, w1) of the call at
   counter q when j mod 4 is 0 or 1, and the pair (w2, w3) when it is 2 or 3.
-  domain is 0 for the perturbation noise and 1 for the draws of the update's
-  stochastic rounding (other values are reserved).
+  domain is 0 for the perturbation noise, 1 for the draws of the update's
+  stochastic rounding and 2 for the draws that round the perturbation offsets
+  of quantized parameters (other values are reserved).
 
   m(w) = w mod 2^23 (the low 23 bits of a word)
   radius uniform u(w) = (m(w) + 1/2) * 2^-23, in [2^-24, 1 - 2^-24]
@@ -43,6 +44,7 @@ from .philox import philox4x32_10, MASK32
 
 DOMAIN_NOISE = 0
 DOMAIN_ROUNDING = 1
+DOMAIN_QUANT_OFFSET = 2
 
 
 def key_words(seed):
@@ -107,12 +109,12 @@ def normals(seed, tensor_id, elems):
     return np.where(lane % 2 == 0, e_cos, e_sin)
 
 
-def rounding_draws(round_seed, tensor_id, elems):
+def rounding_draws(round_seed, tensor_id, elems, domain=DOMAIN_ROUNDING):
     """The 16-bit stochastic-rounding draw of each element index j of one
-    tensor (domain 1): an int64 array with values in [0, 65535]."""
+    tensor (domain 1 by default): an int64 array with values in [0, 65535]."""
     elems = np.atleast_1d(np.asarray(elems, dtype=np.uint64))
     g = elems >> np.uint64(3)
-    w = noise_words(round_seed, tensor_id, g, DOMAIN_ROUNDING)
+    w = noise_words(round_seed, tensor_id, g, domain)
     word = (elems >> np.uint64(1)) & np.uint64(3)
     picked = np.choose(word.astype(np.int64), [w[0], w[1], w[2], w[3]])
     shift = (elems & np.uint64(1)) * np.uint64(16)
