@@ -184,6 +184,55 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const es_update_opts_t* opts, float* z_out_dev,
               int32_t* status_out_dev, es_stream_t stream);
 
+/* ---- int8 parameters (quantized ES; the paper lists it as future work,
+ * Appendix A.2: scale-aware noise, stable updates, seed replay) ----
+ *
+ * A quantized tensor holds symmetric int8 codes q_j in [-127, 127] with
+ * binary32 scales: theta_j = s_r q_j, r = j / row (row == 0: one scale for
+ * the tensor).  Every pass moves codes by integer offsets in units of the
+ * quantum:  k_j = floor(d_j + r_j 2^-16),  q_j <- clamp(q_j +- k_j, -127, 127),
+ * where d_j is the step in quanta and r_j a 16-bit draw, so E[k_j] = d_j.
+ * Elements whose scale is not a normal positive finite binary32 value are
+ * left unchanged.  Draws: Philox4x32-10 at counter (g lo, g hi, tensor_id,
+ * domain), g = j >> 3, one call per 8 codes; code j takes word (j & 7) >> 1,
+ * low half for even j, high half for odd j. */
+typedef struct es_qtensor {
+    void*        data;       /* device int8 codes, contiguous; any alignment
+                                (16-byte aligned data takes the vector path) */
+    const float* scales;     /* device binary32 scales, ceil(numel / row)
+                                entries (1 when row == 0), 4-byte aligned */
+    uint64_t     numel;      /* < 2^31 */
+    uint32_t     row;        /* codes per scale: a multiple of 8, or 0 */
+    uint32_t     tensor_id;  /* noise identity, unique within a plan */
+} es_qtensor_t;
+
+typedef struct es_qplan es_qplan_t;
+
+/* Plan over int8 tensors (same ownership, device and launch-shape rules as
+ * es_plan_create; overlapping code ranges and duplicate ids are rejected;
+ * scales may be shared). */
+int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out);
+int es_qplan_destroy(es_qplan_t* plan);
+uint64_t es_qplan_numel(const es_qplan_t* plan);
+
+/* Perturb (Section 3, in quanta): d_j = sign sigma eps_j(seed) / s_r with the
+ * bf16 path's noise, draws of domain 2 under the same seed;
+ * q_j <- clamp(q_j + k_j).  es_qrestore regenerates the same k_j and
+ * subtracts it, so perturb then restore returns every code whose perturbed
+ * value was not clamped exactly.  sigma finite and >= 0 (0: nothing runs). */
+int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+
+/* Update (Section 3 / Appendix C.1, in quanta): the z-score, coefficient and
+ * merged weights of es_update, d_j = sum_d w_d eps_j(seed_d) / s_r, draws of
+ * domain 1 under opts->round_seed; q_j <- clamp(q_j + k_j).  The rounding is
+ * always stochastic (steps are usually a fraction of a quantum, which
+ * rounding to nearest would drop); ES_UPDATE_STOCHASTIC_ROUND is accepted
+ * and changes nothing.  Other arguments, status and z_out as es_update. */
+int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
+               const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+               float* z_out_dev, int32_t* status_out_dev, es_stream_t stream);
+
 /* Cosine schedule of the perturbation radius (Section 3.1):
  *   sigma_t = sigma_T + (sigma_0 - sigma_T) (1 + cos(pi t / T)) / 2,
  * 0 <= t <= T, T >= 1; returns NaN for arguments out of range.  Update t

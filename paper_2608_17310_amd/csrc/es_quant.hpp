@@ -1,0 +1,165 @@
+// Device code of the int8 path: ES on symmetric int8 codes with per-row
+// binary32 scales, theta_j = s_r(j) q_j, q_j in [-127, 127].  The paper lists
+// quantized ES as future work (Appendix A.2): noise must respect the
+// quantization scale, updates must stay numerically stable, and
+// perturbations must remain replayable from a seed.  Here a perturbation or
+// update step d_j (in units of the row's quantum s) becomes the integer offset
+//   k_j = floor(d_j + r_j 2^-16),   E[k_j] = d_j,
+// with a 16-bit draw r_j, and q_j <- clamp(q_j + k_j, -127, 127).
+//   * perturb / restore: d_j = sign sigma eps_j / s, eps_j the bf16 path's
+//     noise (domain 0) under the member seed, r_j from domain 2 under the same
+//     seed; restore subtracts the very same k_j, so it is exact wherever the
+//     perturbation did not clamp.
+//   * update: d_j = sum_d w_d eps_j(seed_d) / s, r_j from domain 1 under the
+//     update's rounding seed.
+// Draw assignment (both domains): one Philox call at counter
+// (g lo, g hi, tensor_id, domain), g = j >> 3, serves elements 8g .. 8g+7;
+// element j takes word (j & 7) >> 1, low half for even j, high half for odd.
+// Elements whose scale is not a normal positive finite binary32 value are
+// left unchanged.
+//
+// Layout: a lane owns 16 consecutive codes (one 16-byte access); a tile is
+// T lanes x U groups x 16 codes.  Both passes are VALU-bound (16 normals per
+// 16 bytes), so they run one group per lane at a time at full occupancy.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "es_noise.hpp"
+
+namespace esq {
+
+constexpr int kQGroup = 16;                     // int8 codes per lane-group
+constexpr uint32_t kDomainQuantOffset = 2u;
+
+// Quantized tensor table entry.  Tiles are numbered as in the bf16 path:
+// full tiles (16-byte aligned base, in bounds) across all tensors, then tail
+// tiles.  numel < 2^31, so element indices within a tensor (and the end of
+// its last tile) fit 32 bits.
+struct DevQTensor {
+    int8_t* data;
+    const float* scales;
+    uint64_t numel;
+    uint64_t first_full;
+    uint64_t first_tail;
+    uint32_t row;                               // codes per scale; 0: one scale
+    uint32_t tensor_id;
+};
+static_assert(sizeof(DevQTensor) == 48, "quantized tensor table entry layout");
+
+struct QTileRef {
+    int8_t* data;
+    const float* scales;
+    uint32_t numel;
+    uint32_t elem0;
+    uint32_t row;
+    uint32_t tensor_id;
+};
+
+template <uint32_t kTileElems>
+__device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ tab, uint32_t& t,
+                                                 uint64_t tile) {
+    while (tile >= tab[t + 1].first_full) ++t;
+    return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
+                    static_cast<uint32_t>((tile - tab[t].first_full) * kTileElems), tab[t].row,
+                    tab[t].tensor_id};
+}
+
+template <uint32_t kTileElems>
+__device__ __forceinline__ QTileRef qlocate_tail(const DevQTensor* __restrict__ tab, uint32_t& t,
+                                                 uint64_t tile) {
+    while (tile >= tab[t + 1].first_tail) ++t;
+    const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
+    return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
+                    static_cast<uint32_t>((n_full + tile - tab[t].first_tail) * kTileElems),
+                    tab[t].row, tab[t].tensor_id};
+}
+
+typedef uint32_t q32x4_t __attribute__((ext_vector_type(4)));
+#define ESQ_GLOBAL __attribute__((address_space(1)))
+
+// 16 codes of one group in 4 words (byte i of word k is code 4k + i).
+template <bool kFast>
+__device__ __forceinline__ void qload(const int8_t* __restrict__ p, uint32_t e, uint32_t numel,
+                                      uint32_t raw[4]) {
+    if constexpr (kFast) {
+        const q32x4_t v = __builtin_nontemporal_load((const ESQ_GLOBAL q32x4_t*)(p + e));
+        raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
+    } else {
+        const ESQ_GLOBAL uint8_t* g = (const ESQ_GLOBAL uint8_t*)p;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint32_t w = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t j = e + 4 * k + i;
+                if (j < numel) w |= uint32_t(g[j]) << (8 * i);
+            }
+            raw[k] = w;
+        }
+    }
+}
+
+template <bool kFast>
+__device__ __forceinline__ void qstore(int8_t* __restrict__ p, uint32_t e, uint32_t numel,
+                                       const uint32_t out[4]) {
+    if constexpr (kFast) {
+        const q32x4_t v = {out[0], out[1], out[2], out[3]};
+        __builtin_nontemporal_store(v, (ESQ_GLOBAL q32x4_t*)(p + e));
+    } else {
+        ESQ_GLOBAL uint8_t* g = (ESQ_GLOBAL uint8_t*)p;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const uint32_t j = e + 4 * k + i;
+                if (j < numel) g[j] = static_cast<uint8_t>(out[k] >> (8 * i));
+            }
+    }
+}
+
+// The reciprocal of the scale of the 8 codes starting at element j (j is a
+// multiple of 8 and the row length a multiple of 8, so the 8 codes share
+// one scale), or 0 when the scale is not a normal positive finite value.
+__device__ __forceinline__ float inv_scale(const QTileRef& r, uint32_t j) {
+    if (j >= r.numel) return 0.0f;
+    const ESQ_GLOBAL float* s = (const ESQ_GLOBAL float*)r.scales;
+    const float v = r.row == 0u ? s[0] : s[j / r.row];
+    const bool ok = v >= 0x1p-126f && v <= 0x1.fffffep127f;
+    return ok ? 1.0f / v : 0.0f;
+}
+
+// One noise stream's scaled normals for the 16 codes of a group:
+// acc[i] += w_k * (normal of element e + i), w_k = weight * sqrt(2 ln 2).
+__device__ __forceinline__ void qgroup_axpy(uint32_t e, uint32_t tensor_id, uint32_t k0,
+                                            uint32_t k1, float w_k, float acc[16]) {
+    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, k0, k1);
+        float t, cs, sn;
+        es::scaled_pair(w.w0, w.w1, w_k, t, cs, sn);
+        acc[4 * c] = __builtin_fmaf(t, cs, acc[4 * c]);
+        acc[4 * c + 1] = __builtin_fmaf(t, sn, acc[4 * c + 1]);
+        es::scaled_pair(w.w2, w.w3, w_k, t, cs, sn);
+        acc[4 * c + 2] = __builtin_fmaf(t, cs, acc[4 * c + 2]);
+        acc[4 * c + 3] = __builtin_fmaf(t, sn, acc[4 * c + 3]);
+    }
+}
+
+// New code: clamp(q + s * floor(d + r 2^-16), -127, 127) with s = -1 when
+// kNegate (a restore subtracts the offset its perturb added).  1 + r 2^-16 is
+// formed exactly from the draw's bits, so floor(d + r 2^-16) =
+// floor(d + (1 + r 2^-16)) - 1.  |d| is capped at 2^30 quanta, far beyond
+// what any code can absorb, so the integer arithmetic cannot overflow.
+template <bool kNegate>
+__device__ __forceinline__ int32_t qstep(int32_t q, float d, uint32_t draw16) {
+    const float one_plus = __uint_as_float((draw16 << 7) | 0x3F800000u);
+    const float dc = __builtin_fminf(__builtin_fmaxf(d, -0x1p30f), 0x1p30f);
+    const int32_t k = static_cast<int32_t>(__builtin_floorf(dc + one_plus)) - 1;
+    const int32_t v = kNegate ? q - k : q + k;
+    return min(max(v, -127), 127);
+}
+
+}  // namespace esq

@@ -53,6 +53,7 @@
 
 #include "../../include/esopt.h"
 #include "es_noise.hpp"
+#include "es_quant.hpp"
 
 namespace {
 
@@ -65,6 +66,7 @@ constexpr int kDefaultThreads = 1024;
 constexpr int kDefaultGroups = 8;
 constexpr int kDefaultPerturbWgPerCu = 1;
 constexpr int kDefaultUpdateWgPerCu = 8;
+constexpr int kDefaultQGroups = 4;          // int8 tiles: 1024 x 4 x 16 codes (64 KB)
 constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
 // Device tensor table entry.  Tiles are numbered in two sequences: full
@@ -646,6 +648,112 @@ UpdateKernel update_kernel(int threads, int groups, bool stochastic) {
     return nullptr;
 }
 
+// ---- int8 path (device code of the passes; helpers in es_quant.hpp) ----
+
+// Kernel arguments of one int8 pass: the key and domain of the rounding
+// draws, and for perturb / restore the single member inline.
+struct QPass {
+    uint32_t dk0, dk1;
+    uint32_t domain;
+    uint32_t pad;
+    Member m;
+};
+
+// One tile of an int8 pass: for each of the lane's 16-code groups in turn,
+// d = (sum over members of w eps) / s in binary32, then the stochastically
+// rounded integer offset and the clamped code.
+template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate>
+__device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
+                                      uint32_t n_members, const QPass& ps) {
+    const uint32_t e0 = r.elem0 + threadIdx.x * esq::kQGroup;
+#pragma unroll 1
+    for (int u = 0; u < kU; ++u) {
+        const uint32_t e = e0 + uint32_t(u) * kThreads * esq::kQGroup;
+        if (!kFast && e >= r.numel) break;
+        uint32_t raw[4];
+        esq::qload<kFast>(r.data, e, r.numel, raw);
+        const float inv0 = esq::inv_scale(r, e);
+        const float inv1 = esq::inv_scale(r, e + 8);
+        float acc[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
+        if constexpr (kTable) {
+            for (uint32_t d = 0; d < n_members; ++d) {
+                const Member m = members[d];
+                if (m.w_k == 0.0f) continue;
+                esq::qgroup_axpy(e, r.tensor_id, m.k0, m.k1, m.w_k, acc);
+            }
+        } else {
+            esq::qgroup_axpy(e, r.tensor_id, ps.m.k0, ps.m.k1, ps.m.w_k, acc);
+        }
+        const es::Words da = es::philox4x32_10(e >> 3, 0u, r.tensor_id, ps.domain, ps.dk0, ps.dk1);
+        const es::Words db = es::philox4x32_10((e >> 3) + 1u, 0u, r.tensor_id, ps.domain, ps.dk0,
+                                               ps.dk1);
+        const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
+        uint32_t out[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            uint32_t w = 0;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int c = 4 * k + i;
+                const float inv = c < 8 ? inv0 : inv1;
+                const int32_t q = static_cast<int8_t>(raw[k] >> (8 * i));
+                const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
+                const int32_t v = inv != 0.0f ? esq::qstep<kNegate>(q, acc[c] * inv, draw) : q;
+                w |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+            }
+            out[k] = w;
+        }
+        esq::qstore<kFast>(r.data, e, r.numel, out);
+    }
+}
+
+// An int8 pass over the whole quantized parameter list: perturb / restore
+// (one inline member, draws of domain 2 under its seed) or the update
+// (member table and header written by es_prepare_kernel, draws of domain 1
+// under the rounding seed).
+template <int kThreads, int kU, bool kTable, bool kNegate>
+__global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTensor* __restrict__ tab,
+                                                            uint64_t n_full, uint64_t n_tail,
+                                                            const Member* __restrict__ members,
+                                                            const UpdateHeader* __restrict__ hdr,
+                                                            QPass ps) {
+    constexpr uint32_t kTileElems = uint32_t(kThreads) * kU * esq::kQGroup;
+    uint32_t n_members = 1;
+    if constexpr (kTable) {
+        if (hdr->n_live == 0u) return;      // nothing to add: codes are not written
+        n_members = hdr->n_distinct;
+    }
+    uint32_t t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
+        qtile<kThreads, kU, true, kTable, kNegate>(esq::qlocate_full<kTileElems>(tab, t, tile),
+                                                   members, n_members, ps);
+    t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
+        qtile<kThreads, kU, false, kTable, kNegate>(esq::qlocate_tail<kTileElems>(tab, t, tile),
+                                                    members, n_members, ps);
+}
+
+using QPassKernel = void (*)(const esq::DevQTensor*, uint64_t, uint64_t, const Member*,
+                             const UpdateHeader*, QPass);
+
+enum class QKind { kPerturb, kRestore, kUpdate };
+
+QPassKernel qpass_kernel(int threads, int groups, QKind kind) {
+#define ES_CASE(T, U)                                                            \
+    if (threads == T && groups == U) {                                           \
+        switch (kind) {                                                          \
+            case QKind::kPerturb: return es_qpass_kernel<T, U, false, false>;    \
+            case QKind::kRestore: return es_qpass_kernel<T, U, false, true>;     \
+            case QKind::kUpdate: return es_qpass_kernel<T, U, true, false>;      \
+        }                                                                        \
+    }
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------------
@@ -665,6 +773,19 @@ struct es_plan {
     uint64_t tile_elems = 0;        // threads * groups * 8
     DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
     uint8_t* d_scratch = nullptr;   // kScratchBytes
+};
+
+struct es_qplan {
+    int device = -1;
+    uint32_t n_tensors = 0;
+    uint64_t numel = 0;
+    uint64_t n_full = 0;
+    uint64_t n_tail = 0;
+    uint32_t grid = 0;              // workgroups of every int8 pass
+    int threads = kDefaultThreads;
+    int groups = kDefaultQGroups;   // 16-code groups per lane per tile
+    esq::DevQTensor* d_tab = nullptr;
+    uint8_t* d_scratch = nullptr;   // kScratchBytes, as the bf16 plan's
 };
 
 namespace {
@@ -723,6 +844,130 @@ int perturb_impl(es_plan_t* p, uint64_t seed, int32_t sign, float sigma, es_stre
     if (rc != ES_OK) return rc;
     const double coef = sign > 0 ? double(sigma) : -double(sigma);
     return launch_streams(p, 1, &seed, &coef, static_cast<hipStream_t>(stream));
+}
+
+int check_qdevice(const es_qplan_t* p) {
+    int dev = -1;
+    const hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev != p->device)
+        return fail(ES_ERR_DEVICE, "current device " + std::to_string(dev) +
+                                       " differs from the plan's device " +
+                                       std::to_string(p->device));
+    return ES_OK;
+}
+
+int launch_qpass(es_qplan_t* p, QKind kind, const QPass& ps, hipStream_t s) {
+    if (p->n_full + p->n_tail == 0) return ES_OK;
+    const QPassKernel kernel = qpass_kernel(p->threads, p->groups, kind);
+    hipLaunchKernelGGL(kernel, dim3(p->grid), dim3(p->threads), 0, s, p->d_tab, p->n_full,
+                       p->n_tail, reinterpret_cast<const Member*>(p->d_scratch + kOffMembers),
+                       reinterpret_cast<const UpdateHeader*>(p->d_scratch + kOffHeader), ps);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_qpass_kernel launch");
+    return ES_OK;
+}
+
+int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_stream_t stream,
+                  QKind kind, const char* name) {
+    if (p == nullptr) return fail(ES_ERR_INVALID_ARG, std::string(name) + ": null plan");
+    if (sign != 1 && sign != -1)
+        return fail(ES_ERR_INVALID_ARG, std::string(name) + ": sign must be +1 or -1");
+    if (!std::isfinite(sigma) || sigma < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, std::string(name) + ": sigma must be finite and >= 0");
+    if (sigma == 0.0f) return ES_OK;
+    const int rc = check_qdevice(p);
+    if (rc != ES_OK) return rc;
+    const double coef = sign > 0 ? double(sigma) : -double(sigma);
+    QPass ps = {};
+    ps.dk0 = static_cast<uint32_t>(seed);
+    ps.dk1 = static_cast<uint32_t>(seed >> 32);
+    ps.domain = esq::kDomainQuantOffset;
+    ps.m = Member{ps.dk0, ps.dk1, static_cast<float>(coef * kSqrt2Ln2Double), 0u};
+    return launch_qpass(p, kind, ps, static_cast<hipStream_t>(stream));
+}
+
+// Argument checks shared by es_update and es_qupdate.
+int validate_update(const char* name, const uint64_t* seeds, const int32_t* signs,
+                    const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts) {
+    const std::string nm(name);
+    if (seeds == nullptr || signs == nullptr || rewards_dev == nullptr || opts == nullptr)
+        return fail(ES_ERR_INVALID_ARG, nm + ": null pointer");
+    if (n_members == 0 || n_members > ES_MAX_MEMBERS)
+        return fail(ES_ERR_INVALID_ARG, nm + ": n_members out of range");
+    if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
+                         ES_UPDATE_STOCHASTIC_ROUND)) != 0)
+        return fail(ES_ERR_INVALID_ARG, nm + ": unknown flags");
+    if (!std::isfinite(opts->alpha)) return fail(ES_ERR_INVALID_ARG, nm + ": alpha not finite");
+    if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
+        return fail(ES_ERR_INVALID_ARG, nm + ": sigma must be finite and > 0 with ES_UPDATE_DIV_SIGMA");
+    if (!std::isfinite(opts->zscore_eps) || opts->zscore_eps < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, nm + ": zscore_eps must be finite and >= 0");
+    for (uint32_t i = 0; i < n_members; ++i)
+        if (signs[i] != 1 && signs[i] != -1)
+            return fail(ES_ERR_INVALID_ARG, nm + ": signs must be +1 or -1");
+    return ES_OK;
+}
+
+// Hand the population to the device: distinct seeds in order of first
+// appearance with their members grouped by seed (CSR, member order within a
+// seed) are staged into the scratch through kernel arguments, then one wave
+// z-scores the rewards and merges the weights per distinct seed, leaving the
+// weighted member table and its header in the scratch.
+int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* signs,
+                   const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+                   float* z_out_dev, int32_t* status_out_dev, hipStream_t s) {
+    std::unordered_map<uint64_t, uint32_t> index;
+    std::vector<uint64_t> distinct;
+    std::vector<uint32_t> of(n_members);
+    for (uint32_t i = 0; i < n_members; ++i) {
+        auto it = index.emplace(seeds[i], static_cast<uint32_t>(distinct.size()));
+        if (it.second) distinct.push_back(seeds[i]);
+        of[i] = it.first->second;
+    }
+    const uint32_t nd = static_cast<uint32_t>(distinct.size());
+    std::vector<uint32_t> count(nd, 0), first(nd, 0);
+    for (uint32_t i = 0; i < n_members; ++i) ++count[of[i]];
+    for (uint32_t d = 1; d < nd; ++d) first[d] = first[d - 1] + count[d - 1];
+    std::vector<MemberIn> min(n_members);
+    std::vector<uint32_t> fill(first);
+    for (uint32_t i = 0; i < n_members; ++i) min[fill[of[i]]++] = MemberIn{i, signs[i]};
+    std::vector<DistinctIn> din(nd);
+    for (uint32_t d = 0; d < nd; ++d)
+        din[d] = DistinctIn{static_cast<uint32_t>(distinct[d]),
+                            static_cast<uint32_t>(distinct[d] >> 32), first[d], count[d]};
+
+    // 1 KB of kernel arguments per staging launch
+    auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
+        const uint32_t* words = static_cast<const uint32_t*>(src);
+        const size_t n_words = bytes / 4;
+        for (size_t w0 = 0; w0 < n_words; w0 += kStageWords) {
+            StageChunk chunk;
+            const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
+            std::memcpy(chunk.words, words + w0, nw * 4);
+            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s,
+                               reinterpret_cast<uint32_t*>(d_scratch + dst_off) + w0, nw, chunk);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
+        }
+        return ES_OK;
+    };
+    int rc = stage(kOffMembersIn, min.data(), sizeof(MemberIn) * n_members);
+    if (rc == ES_OK) rc = stage(kOffDistinctIn, din.data(), sizeof(DistinctIn) * nd);
+    if (rc != ES_OK) return rc;
+
+    double c = static_cast<double>(opts->alpha) / static_cast<double>(n_members);
+    if (opts->flags & ES_UPDATE_DIV_SIGMA) c /= static_cast<double>(opts->sigma);
+    hipLaunchKernelGGL(es_prepare_kernel, dim3(1), dim3(64), 0, s, rewards_dev, n_members,
+                       static_cast<double>(opts->zscore_eps), opts->flags, c,
+                       reinterpret_cast<const MemberIn*>(d_scratch + kOffMembersIn),
+                       reinterpret_cast<const DistinctIn*>(d_scratch + kOffDistinctIn), nd,
+                       reinterpret_cast<Member*>(d_scratch + kOffMembers),
+                       reinterpret_cast<UpdateHeader*>(d_scratch + kOffHeader), z_out_dev,
+                       status_out_dev);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
+    return ES_OK;
 }
 
 }  // namespace
@@ -855,86 +1100,25 @@ int es_zscore(const float* rewards_dev, uint32_t n, float eps, float* z_dev, int
 int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
               float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) {
-    if (plan == nullptr || seeds == nullptr || signs == nullptr || rewards_dev == nullptr ||
-        opts == nullptr)
-        return fail(ES_ERR_INVALID_ARG, "es_update: null pointer");
-    if (n_members == 0 || n_members > ES_MAX_MEMBERS)
-        return fail(ES_ERR_INVALID_ARG, "es_update: n_members out of range");
-    if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
-                         ES_UPDATE_STOCHASTIC_ROUND)) != 0)
-        return fail(ES_ERR_INVALID_ARG, "es_update: unknown flags");
-    if (!std::isfinite(opts->alpha)) return fail(ES_ERR_INVALID_ARG, "es_update: alpha not finite");
-    if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
-        return fail(ES_ERR_INVALID_ARG, "es_update: sigma must be finite and > 0 with ES_UPDATE_DIV_SIGMA");
-    if (!std::isfinite(opts->zscore_eps) || opts->zscore_eps < 0.0f)
-        return fail(ES_ERR_INVALID_ARG, "es_update: zscore_eps must be finite and >= 0");
-    for (uint32_t i = 0; i < n_members; ++i)
-        if (signs[i] != 1 && signs[i] != -1)
-            return fail(ES_ERR_INVALID_ARG, "es_update: signs must be +1 or -1");
-    int rc = check_device(plan);
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_update: null plan");
+    int rc = validate_update("es_update", seeds, signs, rewards_dev, n_members, opts);
+    if (rc != ES_OK) return rc;
+    rc = check_device(plan);
     if (rc != ES_OK) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-
-    // Distinct seeds in order of first appearance; members grouped by seed
-    // (CSR), in member order within a seed.
-    std::unordered_map<uint64_t, uint32_t> index;
-    std::vector<uint64_t> distinct;
-    std::vector<uint32_t> of(n_members);
-    for (uint32_t i = 0; i < n_members; ++i) {
-        auto it = index.emplace(seeds[i], static_cast<uint32_t>(distinct.size()));
-        if (it.second) distinct.push_back(seeds[i]);
-        of[i] = it.first->second;
-    }
-    const uint32_t nd = static_cast<uint32_t>(distinct.size());
-    std::vector<uint32_t> count(nd, 0), first(nd, 0);
-    for (uint32_t i = 0; i < n_members; ++i) ++count[of[i]];
-    for (uint32_t d = 1; d < nd; ++d) first[d] = first[d - 1] + count[d - 1];
-    std::vector<MemberIn> min(n_members);
-    std::vector<uint32_t> fill(first);
-    for (uint32_t i = 0; i < n_members; ++i) min[fill[of[i]]++] = MemberIn{i, signs[i]};
-    std::vector<DistinctIn> din(nd);
-    for (uint32_t d = 0; d < nd; ++d)
-        din[d] = DistinctIn{static_cast<uint32_t>(distinct[d]),
-                            static_cast<uint32_t>(distinct[d] >> 32), first[d], count[d]};
-
-    // Stage both tables through kernel arguments, 1 KB per launch.
-    auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
-        const uint32_t* words = static_cast<const uint32_t*>(src);
-        const size_t n_words = bytes / 4;
-        for (size_t w0 = 0; w0 < n_words; w0 += kStageWords) {
-            StageChunk chunk;
-            const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
-            std::memcpy(chunk.words, words + w0, nw * 4);
-            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s,
-                               reinterpret_cast<uint32_t*>(plan->d_scratch + dst_off) + w0, nw, chunk);
-            const hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
-        }
-        return ES_OK;
-    };
-    rc = stage(kOffMembersIn, min.data(), sizeof(MemberIn) * n_members);
-    if (rc == ES_OK) rc = stage(kOffDistinctIn, din.data(), sizeof(DistinctIn) * nd);
+    rc = prepare_update(plan->d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
+                        status_out_dev, s);
     if (rc != ES_OK) return rc;
-
-    double c = static_cast<double>(opts->alpha) / static_cast<double>(n_members);
-    if (opts->flags & ES_UPDATE_DIV_SIGMA) c /= static_cast<double>(opts->sigma);
-    auto* members = reinterpret_cast<Member*>(plan->d_scratch + kOffMembers);
-    auto* hdr = reinterpret_cast<UpdateHeader*>(plan->d_scratch + kOffHeader);
-    hipLaunchKernelGGL(es_prepare_kernel, dim3(1), dim3(64), 0, s, rewards_dev, n_members,
-                       static_cast<double>(opts->zscore_eps), opts->flags, c,
-                       reinterpret_cast<const MemberIn*>(plan->d_scratch + kOffMembersIn),
-                       reinterpret_cast<const DistinctIn*>(plan->d_scratch + kOffDistinctIn), nd,
-                       members, hdr, z_out_dev, status_out_dev);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
     if (plan->n_full + plan->n_tail == 0) return ES_OK;
     const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
     const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
                       static_cast<uint32_t>(opts->round_seed >> 32)};
     const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
     hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
-                       plan->n_full, plan->n_tail, members, hdr, rk);
-    e = hipGetLastError();
+                       plan->n_full, plan->n_tail,
+                       reinterpret_cast<const Member*>(plan->d_scratch + kOffMembers),
+                       reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffHeader), rk);
+    const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
     return ES_OK;
 }
@@ -967,6 +1151,131 @@ int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_
     if (rc != ES_OK) return rc;
     const int streams = (m == 2 && sd[0] == sd[1]) ? 3 : m;
     return launch_streams(plan, streams, sd, cf, static_cast<hipStream_t>(stream));
+}
+
+int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out) {
+    if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null output pointer");
+    *out = nullptr;
+    if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null tensor list");
+    if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
+        return fail(ES_ERR_INVALID_ARG, "es_qplan_create: n_tensors out of range");
+    int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
+    int groups = env_int("ESOPT_QGROUPS", kDefaultQGroups, 2, 8);
+    if (qpass_kernel(threads, groups, QKind::kUpdate) == nullptr) {
+        threads = kDefaultThreads;
+        groups = kDefaultQGroups;
+    }
+    const uint64_t tile_elems = uint64_t(threads) * groups * esq::kQGroup;
+    std::vector<esq::DevQTensor> tab(n_tensors + 1);
+    std::unordered_map<uint32_t, uint32_t> ids;
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    uint64_t n_full = 0, n_tail = 0, numel = 0;
+    for (uint32_t i = 0; i < n_tensors; ++i) {
+        const es_qtensor_t& t = tensors[i];
+        const std::string where = "es_qplan_create: tensor " + std::to_string(i);
+        if (!ids.emplace(t.tensor_id, i).second)
+            return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
+        // element indices, and the end of the last tile, stay below 2^32
+        if (t.numel >= (uint64_t(1) << 31))
+            return fail(ES_ERR_INVALID_ARG, where + ": numel must be below 2^31");
+        if (t.numel > 0 && (t.data == nullptr || t.scales == nullptr))
+            return fail(ES_ERR_INVALID_ARG, where + ": null data or scales");
+        if (t.row % 8 != 0)
+            return fail(ES_ERR_INVALID_ARG, where + ": row must be a multiple of 8 (or 0)");
+        if (t.numel > 0 && (reinterpret_cast<uintptr_t>(t.scales) & 3u))
+            return fail(ES_ERR_ALIGN, where + ": scales not 4-byte aligned");
+        const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
+        const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
+        const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
+        tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales, t.numel, n_full, n_tail,
+                                 t.row, t.tensor_id};
+        if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
+        n_full += full;
+        n_tail += tail;
+        numel += t.numel;
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+        if (ranges[i].first < ranges[i - 1].second)
+            return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
+    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu};
+
+    es_qplan_t* p = new (std::nothrow) es_qplan_t;
+    if (p == nullptr) return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation");
+    hipError_t e = hipGetDevice(&p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
+    const int wg = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
+    p->threads = threads;
+    p->groups = groups;
+    p->n_tensors = n_tensors;
+    p->numel = numel;
+    p->n_full = n_full;
+    p->n_tail = n_tail;
+    const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
+    p->grid = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg));
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(esq::DevQTensor) * tab.size());
+    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        delete p;
+        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    e = hipMemcpy(p->d_tab, tab.data(), sizeof(esq::DevQTensor) * tab.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        (void)hipFree(p->d_scratch);
+        delete p;
+        return hip_fail(e, "es_qplan_create: table upload");
+    }
+    *out = p;
+    return ES_OK;
+}
+
+int es_qplan_destroy(es_qplan_t* plan) {
+    if (plan == nullptr) return ES_OK;
+    int rc = ES_OK;
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) rc = hip_fail(e, "es_qplan_destroy: hipDeviceSynchronize");
+    e = hipFree(plan->d_tab);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_qplan_destroy: hipFree");
+    e = hipFree(plan->d_scratch);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_qplan_destroy: hipFree");
+    delete plan;
+    return rc;
+}
+
+uint64_t es_qplan_numel(const es_qplan_t* plan) { return plan ? plan->numel : 0; }
+
+int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
+    return qperturb_impl(plan, seed, sign, sigma, stream, QKind::kPerturb, "es_qperturb");
+}
+
+int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
+    return qperturb_impl(plan, seed, sign, sigma, stream, QKind::kRestore, "es_qrestore");
+}
+
+int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
+               const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+               float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qupdate: null plan");
+    int rc = validate_update("es_qupdate", seeds, signs, rewards_dev, n_members, opts);
+    if (rc != ES_OK) return rc;
+    rc = check_qdevice(plan);
+    if (rc != ES_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    rc = prepare_update(plan->d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
+                        status_out_dev, s);
+    if (rc != ES_OK) return rc;
+    QPass ps = {};
+    ps.dk0 = static_cast<uint32_t>(opts->round_seed);
+    ps.dk1 = static_cast<uint32_t>(opts->round_seed >> 32);
+    ps.domain = es::kDomainRounding;
+    return launch_qpass(plan, QKind::kUpdate, ps, s);
 }
 
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T) {

@@ -41,6 +41,11 @@ class EsTensor(ctypes.Structure):
     _fields_ = [("data", _vp), ("numel", _u64), ("tensor_id", _u32), ("reserved", _u32)]
 
 
+class EsQTensor(ctypes.Structure):
+    _fields_ = [("data", _vp), ("scales", _vp), ("numel", _u64), ("row", _u32),
+                ("tensor_id", _u32)]
+
+
 class EsUpdateOpts(ctypes.Structure):
     _fields_ = [("alpha", _f32), ("sigma", _f32), ("zscore_eps", _f32), ("flags", _u32),
                 ("round_seed", _u64)]
@@ -57,6 +62,13 @@ SIGNATURES = {
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
+    "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
+    "es_qplan_destroy": (ctypes.c_int, [_vp]),
+    "es_qplan_numel": (_u64, [_vp]),
+    "es_qperturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
+    "es_qrestore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
+    "es_qupdate": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
+                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
     "es_sigma_cosine": (_f64, [_f64, _f64, _u32, _u32]),
     "es_philox_words": (ctypes.c_int, [_u64, _u32, _u32, _u64, _u64, _vp, _vp]),
     "es_normals": (ctypes.c_int, [_u64, _u32, _u64, _u64, _vp, _vp]),
@@ -184,26 +196,105 @@ class Plan:
                z_out=None, status_out=None, stream=None, round_seed=0):
         """Fused update; rewards is a float32 CUDA tensor of len(seeds).
         round_seed keys the draws of ES_UPDATE_STOCHASTIC_ROUND."""
-        n = len(seeds)
-        if len(signs) != n:
-            raise ValueError("seeds and signs differ in length")
-        if rewards.numel() != n:
-            raise ValueError("rewards must have one entry per member")
-        c_seeds = (_u64 * max(n, 1))(*[int(s) for s in seeds])
-        c_signs = (_i32 * max(n, 1))(*[int(s) for s in signs])
-        if not 0 <= int(round_seed) < (1 << 64):
-            raise ValueError("round_seed must be in [0, 2^64)")
-        opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags),
-                            int(round_seed))
-        _check(load().es_update(self.handle, c_seeds, c_signs,
-                                _dev_ptr(rewards, torch.float32, "rewards"), n, ctypes.byref(opts),
-                                _dev_ptr(z_out, torch.float32, "z_out"),
-                                _dev_ptr(status_out, torch.int32, "status_out"), _stream(stream)),
-               "es_update")
+        _call_update(load().es_update, "es_update", self.handle, seeds, signs, rewards, alpha,
+                     sigma, zscore_eps, flags, z_out, status_out, stream, round_seed)
 
     def close(self):
         if self._h is not None:
             _check(load().es_plan_destroy(self._h), "es_plan_destroy")
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+
+def _call_update(fn, what, handle, seeds, signs, rewards, alpha, sigma, zscore_eps, flags,
+                 z_out, status_out, stream, round_seed):
+    n = len(seeds)
+    if len(signs) != n:
+        raise ValueError("seeds and signs differ in length")
+    if rewards.numel() != n:
+        raise ValueError("rewards must have one entry per member")
+    c_seeds = (_u64 * max(n, 1))(*[int(s) for s in seeds])
+    c_signs = (_i32 * max(n, 1))(*[int(s) for s in signs])
+    if not 0 <= int(round_seed) < (1 << 64):
+        raise ValueError("round_seed must be in [0, 2^64)")
+    opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags), int(round_seed))
+    _check(fn(handle, c_seeds, c_signs, _dev_ptr(rewards, torch.float32, "rewards"), n,
+              ctypes.byref(opts), _dev_ptr(z_out, torch.float32, "z_out"),
+              _dev_ptr(status_out, torch.int32, "status_out"), _stream(stream)), what)
+
+
+class QPlan:
+    """A list of int8 parameter tensors with binary32 scales (theta = s q,
+    one scale per `row` consecutive codes, row a multiple of 8, 0 for one
+    scale per tensor), prepared for single-launch passes.  The plan keeps
+    references to the codes and scales."""
+
+    def __init__(self, codes, scales, rows, tensor_ids=None):
+        codes, scales, rows = list(codes), list(scales), [int(r) for r in rows]
+        if not codes or len(scales) != len(codes) or len(rows) != len(codes):
+            raise ValueError("codes, scales and rows must be non-empty and of equal length")
+        ids = list(range(len(codes))) if tensor_ids is None else [int(i) for i in tensor_ids]
+        if len(ids) != len(codes):
+            raise ValueError("tensor_ids must match tensors")
+        arr = (EsQTensor * len(codes))()
+        for i, (q, sc, row, tid) in enumerate(zip(codes, scales, rows, ids)):
+            if q.dtype != torch.int8 or not q.is_cuda or not q.is_contiguous():
+                raise ValueError(f"codes {i} must be a contiguous int8 CUDA tensor")
+            if sc.dtype != torch.float32 or not sc.is_cuda or not sc.is_contiguous():
+                raise ValueError(f"scales {i} must be a contiguous float32 CUDA tensor")
+            need = 1 if row == 0 else -(-q.numel() // row)
+            if q.numel() and sc.numel() < need:
+                raise ValueError(f"scales {i} has {sc.numel()} entries, needs {need}")
+            arr[i] = EsQTensor(q.data_ptr() if q.numel() else None,
+                               sc.data_ptr() if q.numel() else None, q.numel(), row, tid)
+        self._keep = (codes, scales)
+        self.tensor_ids = ids
+        self.device = codes[0].device
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(load().es_qplan_create(arr, len(codes), ctypes.byref(handle)),
+                   "es_qplan_create")
+        self._h = handle
+
+    @property
+    def handle(self):
+        if self._h is None:
+            raise RuntimeError("plan is closed")
+        return self._h
+
+    @property
+    def numel(self):
+        return int(load().es_qplan_numel(self.handle))
+
+    def perturb(self, seed, sign, sigma, stream=None):
+        _check(load().es_qperturb(self.handle, int(seed), int(sign), float(sigma),
+                                  _stream(stream)), "es_qperturb")
+
+    def restore(self, seed, sign, sigma, stream=None):
+        _check(load().es_qrestore(self.handle, int(seed), int(sign), float(sigma),
+                                  _stream(stream)), "es_qrestore")
+
+    def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
+               z_out=None, status_out=None, stream=None, round_seed=0):
+        """Update in quanta, always stochastically rounded with the draws of
+        round_seed; rewards is a float32 CUDA tensor of len(seeds)."""
+        _call_update(load().es_qupdate, "es_qupdate", self.handle, seeds, signs, rewards, alpha,
+                     sigma, zscore_eps, flags, z_out, status_out, stream, round_seed)
+
+    def close(self):
+        if self._h is not None:
+            _check(load().es_qplan_destroy(self._h), "es_qplan_destroy")
             self._h = None
 
     def __del__(self):

@@ -211,3 +211,61 @@ def device_params(wl, device="cuda", seed=1234):
         v.normal_(0.0, WEIGHT_STD, generator=gen)
         views.append(v.view(shape))
     return flat, views
+
+
+# ------------------------------------------------------------------ int8 sets --
+# The int8 path's inputs: the same synthetic weights, N(0, 0.02), quantized
+# symmetrically to int8 codes with one binary32 scale per row of the last
+# dimension (absmax / 127; per output channel for a [out, in] matrix) and one
+# scale per tensor for vectors.  This prepares inputs only.
+
+def quantize_rows(w, row):
+    """(codes int8, scales float32) of a float32 array quantized per `row`
+    consecutive values (row == 0: one scale), symmetric absmax / 127; an
+    all-zero row gets scale 1.  Works on numpy arrays and torch tensors."""
+    import torch
+    t = torch.as_tensor(w, dtype=torch.float32).reshape(-1)
+    g = t.reshape(1, -1) if row == 0 else t.reshape(-1, row)
+    amax = g.abs().amax(dim=1)
+    s = torch.where(amax > 0, amax / 127.0, torch.ones_like(amax))
+    q = torch.clamp(torch.round(g / s[:, None]), -127, 127).to(torch.int8).reshape(-1)
+    return q, s.contiguous()
+
+
+def row_of(shape):
+    """Scale grouping used for a tensor of this shape: its last dimension for
+    matrices (a multiple of 8 in every workload here), one scale for vectors."""
+    return int(shape[-1]) if len(shape) >= 2 else 0
+
+
+def host_qparams(wl, stream=0):
+    """Host int8 codes, scales and rows of a workload (numpy)."""
+    out = []
+    for i, s in enumerate(wl.shapes):
+        q, sc = quantize_rows(host_tensor_values(s, i, stream), row_of(s))
+        out.append((q.numpy(), sc.numpy(), row_of(s)))
+    return out
+
+
+def device_qparams(wl, device="cuda", seed=1234):
+    """The workload's weights drawn on the device (as device_params) and
+    quantized per row into one flat int8 buffer (tensors 256-byte aligned).
+    Returns (flat_codes, [code views], [scales], [rows])."""
+    import torch
+    offs, total = flat_layout(wl.numels, align=256)
+    flat = torch.empty(total, dtype=torch.int8, device=device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    views, scales, rows = [], [], []
+    for off, n, shape in zip(offs, wl.numels, wl.shapes):
+        w = torch.empty(n, dtype=torch.float32, device=device)
+        w.normal_(0.0, WEIGHT_STD, generator=gen)
+        row = row_of(shape)
+        q, s = quantize_rows(w, row)
+        del w
+        v = flat[off:off + n]
+        v.copy_(q)
+        views.append(v)
+        scales.append(s)
+        rows.append(row)
+    return flat, views, scales, rows

@@ -12,6 +12,10 @@ int main(void) {
     printf("es_tensor_t %zu data %zu numel %zu tensor_id %zu reserved %zu\n", sizeof(es_tensor_t),
            offsetof(es_tensor_t, data), offsetof(es_tensor_t, numel),
            offsetof(es_tensor_t, tensor_id), offsetof(es_tensor_t, reserved));
+    printf("es_qtensor_t %zu data %zu scales %zu numel %zu row %zu tensor_id %zu\n",
+           sizeof(es_qtensor_t), offsetof(es_qtensor_t, data), offsetof(es_qtensor_t, scales),
+           offsetof(es_qtensor_t, numel), offsetof(es_qtensor_t, row),
+           offsetof(es_qtensor_t, tensor_id));
     printf("es_update_opts_t %zu alpha %zu sigma %zu zscore_eps %zu flags %zu round_seed %zu\n",
            sizeof(es_update_opts_t), offsetof(es_update_opts_t, alpha),
            offsetof(es_update_opts_t, sigma), offsetof(es_update_opts_t, zscore_eps),
@@ -21,6 +25,8 @@ int main(void) {
     es_plan_t* plan = NULL;
     printf("plan_create_null %d\n", es_plan_create(NULL, 1, &plan));
     printf("perturb_null %d\n", es_perturb(NULL, 1, 1, 1e-3f, NULL));
+    es_qplan_t* qplan = NULL;
+    printf("qplan_create_null %d\n", es_qplan_create(NULL, 1, &qplan));
     printf("strerror %s\n", es_strerror(ES_ERR_INVALID_ARG));
     printf("sigma_cosine %.17g\n", es_sigma_cosine(1e-3, 1e-4, 50, 100));
     return 0;

@@ -80,3 +80,46 @@ def update_delta(tensor_id, seeds, signs, rewards, alpha, sigma, flags, elems, z
         if wd != 0.0:
             d += wd * oracle.normals(s, tensor_id, elems)
     return d
+
+
+# ------------------------------------------------------------------ int8 path --
+# The int8 passes turn a binary32 step d (in quanta) and a 16-bit draw r into
+# the integer floor(d + r 2^-16).  The GPU's d differs from the oracle's fp64
+# d by the noise error (|d eps| <= 4e-6 + 2e-6 |eps| per unit weight) and a
+# few binary32 roundings, so where d + r 2^-16 lies within that bound of an
+# integer both floor values are correct; everywhere else the code is unique.
+
+F32_EPS = 2.0 ** -23
+
+
+def q_tolerance(abs_weight_sum, noise_abs_sum, d):
+    """Bound on |d_gpu - d_oracle| in quanta: abs_weight_sum = sum_d |w_d| / s,
+    noise_abs_sum = sum_d |w_d eps_d| / s (fp64 arrays)."""
+    return (abs_weight_sum * 4e-6 + noise_abs_sum * (2e-6 + 8 * F32_EPS)
+            + 4 * F32_EPS * (np.abs(d) + 2.0))
+
+
+def qreport(got, q_in, d, r, tol, ok, negate=False):
+    """Compare GPU codes with the oracle's rule code = clamp(q +- floor(d +
+    r 2^-16)); near-integer cases (within tol) accept either floor."""
+    got = np.asarray(got, dtype=np.int8).astype(np.int64)
+    q = np.asarray(q_in, dtype=np.int8).astype(np.int64)
+    v = d + np.asarray(r, dtype=np.int64) * 2.0 ** -16
+    k = np.floor(v).astype(np.int64)
+    near = np.abs(v - np.round(v)) <= tol
+    alt = np.where(v - np.round(v) < 0, k + 1, k - 1)     # the other side of the integer
+    sgn = -1 if negate else 1
+
+    def code(kk):
+        return np.where(ok, np.clip(q + sgn * kk, -127, 127), q)
+    exp, exp_alt = code(k), code(alt)
+    good = (got == exp) | (near & (got == exp_alt))
+    n = got.size
+    return {"n": n, "exact": float(np.mean(got == exp)) if n else 1.0,
+            "near": int(near.sum()), "bad": int((~good).sum()),
+            "first_bad": np.flatnonzero(~good)[:5].tolist()}
+
+
+def assert_qparity(rep, what=""):
+    assert rep["bad"] == 0, (what, rep)
+    assert rep["exact"] >= 0.9999, (what, rep)

@@ -144,8 +144,43 @@ def test_plain_c_consumer_of_header(lib, tmp_path):
                                            for x in (f, str(getattr(cls, f).offset))]
     assert rows["es_tensor_t"] == layout(esopt.EsTensor)
     assert rows["es_update_opts_t"] == layout(esopt.EsUpdateOpts)
+    assert rows["es_qtensor_t"] == layout(esopt.EsQTensor)
+    assert rows["qplan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
                              str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
     assert rows["plan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["perturb_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert float(rows["sigma_cosine"][0]) == lib.es_sigma_cosine(1e-3, 1e-4, 50, 100)
+
+
+def test_quantized_plan_validation_without_gpu(lib):
+    """es_qplan_create and the int8 passes reject bad arguments before any
+    device call."""
+    fake = ctypes.c_void_p(0x10000)
+    out = ctypes.c_void_p()
+    T = esopt.EsQTensor
+
+    def create(*ts):
+        arr = (T * len(ts))(*ts)
+        return lib.es_qplan_create(arr, len(ts), ctypes.byref(out))
+    E = esopt.ES_ERR_INVALID_ARG
+    assert create(T(fake, fake, 100, 12, 0)) == E                  # row not a multiple of 8
+    assert create(T(fake, fake, 1 << 31, 0, 0)) == E               # numel too large
+    assert create(T(None, fake, 100, 8, 0)) == E                   # null codes
+    assert create(T(fake, None, 100, 8, 0)) == E                   # null scales
+    assert create(T(fake, ctypes.c_void_p(0x10002), 100, 8, 0)) == esopt.ES_ERR_ALIGN
+    assert create(T(fake, fake, 100, 8, 3), T(ctypes.c_void_p(0x20000), fake, 10, 8, 3)) == E
+    assert create(T(fake, fake, 100, 8, 0), T(ctypes.c_void_p(0x10010), fake, 10, 8, 1)) == E
+    assert lib.es_qplan_create(None, 1, ctypes.byref(out)) == E
+    assert lib.es_qperturb(None, 1, 1, 1e-3, None) == E
+    assert lib.es_qrestore(None, 1, 1, 1e-3, None) == E
+    assert lib.es_qperturb(fake, 1, 0, 1e-3, None) == E
+    assert lib.es_qperturb(fake, 1, 1, float("nan"), None) == E
+    seeds = (ctypes.c_uint64 * 2)(1, 2)
+    signs = (ctypes.c_int32 * 2)(1, 1)
+    opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0, 0)
+    assert lib.es_qupdate(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == E
+    bad = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8, 0)
+    assert lib.es_qupdate(fake, seeds, signs, fake, 2, ctypes.byref(bad), None, None, None) == E
+    assert lib.es_qplan_destroy(None) == esopt.ES_OK
+    assert lib.es_qplan_numel(None) == 0
