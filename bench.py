@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
     ap.add_argument("--swap", action="store_true",
                     help="move between members with the fused es_swap (N+1 passes per step)")
+    ap.add_argument("--int8", action="store_true",
+                    help="the int8 path: codes with per-row scales, es_qperturb / es_qrestore / "
+                         "es_qupdate")
     ap.add_argument("--stochastic-round", action="store_true",
                     help="round the update stochastically (ES_UPDATE_STOCHASTIC_ROUND)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -122,17 +125,187 @@ def host_samples(W, per_tensor=1 << 14):
     return out
 
 
+def _oracle_qchunk(args):
+    """The oracle's work of one int8 step on a sample of one tensor's codes."""
+    import oracle
+    q, scales, row, tid, elems, seeds, signs, rewards, alpha, sigma = args
+    t0 = time.perf_counter()
+    for s, sg in zip(seeds, signs):
+        p = oracle.qperturb(q, scales, row, s, tid, sg, sigma, elems=elems)
+        q = oracle.qrestore(p, scales, row, s, tid, sg, sigma, elems=elems)
+    q, _ = oracle.qupdate(q, scales, row, tid, seeds, signs, rewards, alpha, sigma, elems=elems,
+                          round_seed=1)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_tensor=1 << 12):
+    """The oracle's int8 step on a bounded sample: random codes and indices,
+    per-row scales of the workload's shapes (values do not change the cost)."""
+    from paper_2608_17310_amd import workloads as wl
+    rng = np.random.default_rng(0)
+    samples = []
+    for tid, (n, shape) in enumerate(zip(W.numels, W.shapes)):
+        row = wl.row_of(shape)
+        idx = np.unique(rng.integers(0, n, size=min(n, per_tensor))).astype(np.uint64)
+        scales = rng.uniform(3e-4, 1e-3, 1 if row == 0 else n // row).astype(np.float32)
+        codes = rng.integers(-127, 128, size=idx.size).astype(np.int8)
+        samples.append((codes, scales, row, tid, idx))
+    n = len(seeds)
+    c0 = samples[0]
+    t_small = _oracle_qchunk((c0[0][:1024], c0[1], c0[2], c0[3], c0[4][:1024], seeds, signs,
+                              rewards, W.alpha, sigma))
+    per_elem = t_small / 1024
+    total = sum(x[4].size for x in samples)
+    frac = min(1.0, int(budget_s * workers / per_elem) / total)
+    jobs = []
+    for codes, scales, row, tid, idx in samples:
+        k = max(1, int(idx.size * frac))
+        jobs.append((codes[:k], scales, row, tid, idx[:k], seeds, signs, rewards, W.alpha, sigma))
+    n_elems = sum(j[4].size for j in jobs)
+    t0 = time.perf_counter()
+    with mp.get_context("fork").Pool(workers) as pool:
+        pool.map(_oracle_qchunk, jobs, chunksize=1)
+    wall = time.perf_counter() - t0
+    return {"value": (2 * n + 1) * n_elems / wall, "unit": "params/s", "cores": workers,
+            "kind": "oracle",
+            "sample": f"{n_elems} int8 codes sampled across {len(jobs)} tensors of {W.name}, one "
+                      f"full int8 step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 NumPy "
+                      f"over {workers} worker processes, {wall:.1f} s wall"}
+
+
 # ---------------------------------------------------------------- GPU leg --
+
+def run_int8(args):
+    """The int8 step on the workload's shapes: N x (es_qperturb + es_qrestore)
+    + es_qupdate over codes with per-row scales, inputs resident in HBM."""
+    import torch
+    from paper_2608_17310_amd import esopt, workloads as wl
+    W = wl.WORKLOADS[args.workload]
+    n_members = args.members
+    signs = list(W.signs) if n_members is None else [1] * n_members
+    N = len(signs)
+    cpu = None
+    if not args.no_cpu_baseline and not args.profile_pass:
+        cpu = cpu_baseline_int8(W, step_seeds(W, args.warmup, n_members), signs,
+                                wl.rewards(W, args.warmup, n=N), sigma_at(W, args.warmup),
+                                min(16, os.cpu_count() or 1), args.cpu_seconds)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU"}))
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    flat, views, scales, rows = wl.device_qparams(W)
+    plan = esopt.QPlan(views, scales, rows)
+    P = plan.numel
+    stream = torch.cuda.current_stream()
+    total_steps = args.warmup + args.steps
+    rewards_all = torch.from_numpy(np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])).cuda()
+    torch.cuda.synchronize()
+    if args.profile_pass:
+        seeds = step_seeds(W, 0, n_members)
+        plan.perturb(seeds[0], signs[0], W.sigma0)
+        plan.restore(seeds[0], signs[0], W.sigma0)
+        plan.update(seeds, signs, rewards_all[0], W.alpha, sigma=W.sigma0, round_seed=1)
+        calib = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")     # 1 GiB copy
+        torch.empty_like(calib).copy_(calib)
+        torch.cuda.synchronize()
+        print(json.dumps({"profile_pass": W.name + "-int8", "params": P, "members": N,
+                          "calibration_copy_bytes": 1 << 30}))
+        return
+    ev = []
+
+    def timed(kind, record, fn, *a, **kw):
+        if record:
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn(*a, **kw)
+            e1.record(stream)
+            ev.append((kind, e0, e1))
+        else:
+            fn(*a, **kw)
+
+    def run_step(t, record):
+        seeds = step_seeds(W, t, n_members)
+        sigma = sigma_at(W, t)
+        for sd, sg in zip(seeds, signs):
+            timed("es_qperturb", record, plan.perturb, sd, sg, sigma)
+            timed("es_qrestore", record, plan.restore, sd, sg, sigma)
+        timed("es_qupdate", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
+              sigma=sigma, round_seed=1000 + t)
+
+    for t in range(args.warmup):
+        run_step(t, record=False)
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for t in range(args.warmup, total_steps):
+        run_step(t, record=True)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    ms_step = start.elapsed_time(end) / args.steps
+    per = {}
+    for kind, a, b in ev:
+        per.setdefault(kind, []).append(a.elapsed_time(b))
+    t_pert = float(np.mean(per["es_qperturb"] + per["es_qrestore"])) / 1e3
+    t_upd = float(np.mean(per["es_qupdate"])) / 1e3
+    value = (2 * N + 1) * P / (ms_step / 1e3)
+    n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
+    label = W.name + "-int8"
+    c_pert = _counters_for(args.counters_json, "es_qperturb", label)
+    c_upd = _counters_for(args.counters_json, "es_qupdate", label)
+
+    def alu_roofline(c, t, kernel, extra):
+        r = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
+             "achieved": None, "frac": None, "kernel": kernel,
+             "traffic": c["bytes_per_launch"] if c else None,
+             "algorithmic_bytes_per_launch": 2 * P,
+             "achieved_GBps_algorithmic": round(2 * P / t / 1e9, 1)}
+        if c and extra:
+            ach = c["valu_insts_per_launch"] * 64 / t / 1e12
+            r.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
+        return r
+    same_config = N == len(W.seeds) and n_members is None
+    out = {
+        "metric": "params/s of the int8 ES step (es_qperturb/es_qrestore and fused es_qupdate, "
+                  "N members)",
+        "value": value, "unit": "params/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "param_dtype": "int8",
+        "data": "synthetic",
+        "config": {"workload": label, "params": P, "tensors": len(views), "members": N,
+                   "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
+                   "scales": "one binary32 scale per row of the last dimension, one per vector",
+                   "counting": "value = (2N+1) P / step time: 2N perturb/restore passes and one "
+                               "fused N-member update pass per step"},
+        "roofline": alu_roofline(c_pert, t_pert, "es_qpass_kernel (es_qperturb / es_qrestore)", True),
+        "roofline_update": alu_roofline(c_upd, t_upd, "es_qpass_kernel (es_qupdate)", same_config),
+        "per_kernel": {
+            "es_qperturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
+                            "GBps_algorithmic": round(2 * P / t_pert / 1e9, 1)},
+            "es_qupdate": {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
+                           "normals_per_s": n_distinct * P / t_upd,
+                           "distinct_seeds": n_distinct}},
+        "wall_s_timed": round(wall, 3),
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out))
+    plan.close()
+
 
 def main():
     args = parse()
     if args.summarize:
-        summarize(*args.summarize, workload=args.workload)
+        summarize(*args.summarize, workload=args.workload, int8=args.int8)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs the ES parameter path on one GPU; "
                                    "--gpus above 1 is not supported (see the sharding design)"}))
         sys.exit(2)
+    if args.int8:
+        return run_int8(args)
     import torch
     from paper_2608_17310_amd import esopt, workloads as wl
 
@@ -232,12 +405,9 @@ def main():
     value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
 
-    counters = None
-    if os.path.exists(args.counters_json):
-        cj = json.load(open(args.counters_json))
-        if cj.get("source_hash") == _kernel_source_hash() and cj.get("workload") == W.name:
-            counters = cj
-    traffic = counters["es_perturb"]["bytes_per_launch"] if counters else None
+    c_pert = _counters_for(args.counters_json, "es_perturb", W.name)
+    c_upd = _counters_for(args.counters_json, "es_update", W.name)
+    traffic = c_pert["bytes_per_launch"] if c_pert else None
     perturb_gbs = 4 * P / t_pert / 1e9
     roofline = {"bound": "hbm", "achieved": round(perturb_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(perturb_gbs / HBM_PEAK_GBS, 4),
@@ -252,9 +422,9 @@ def main():
     roofline_update = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
                        "achieved": None, "frac": None,
                        "kernel": "es_update_kernel (fused N-member update)",
-                       "traffic": counters["es_update"]["bytes_per_launch"] if counters else None}
-    if counters and N == len(W.seeds) and n_members is None:
-        ach = counters["es_update"]["valu_insts_per_launch"] * 64 / t_upd / 1e12
+                       "traffic": c_upd["bytes_per_launch"] if c_upd else None}
+    if c_upd and N == len(W.seeds) and n_members is None and not args.stochastic_round:
+        ach = c_upd["valu_insts_per_launch"] * 64 / t_upd / 1e12
         roofline_update.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
     out = {
         "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
@@ -295,19 +465,25 @@ def main():
 # ------------------------------------------------------------ profiling --
 
 PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats -f csv rocpd -d <out>/trace -o trace -- "
+    "trace": "rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o trace -- "
              "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv rocpd -d <out>/fetch -o fetch -- "
+    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/fetch -o fetch -- "
              "python3 bench.py --profile-pass",
-    "write": "rocprofv3 --pmc WRITE_SIZE -f csv rocpd -d <out>/write -o write -- "
+    "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/write -o write -- "
              "python3 bench.py --profile-pass",
     "valu": "rocprofv3 --pmc SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_VALU_TRANS_F32 SQ_WAVES "
-            "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE -f csv rocpd -d <out>/valu -o valu -- "
+            "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE -f csv -d <out>/valu -o valu -- "
             "python3 bench.py --profile-pass",
 }
 
 
 def _kind(name):
+    if "es_qpass_kernel" in name:
+        if "true, false>" in name:
+            return "es_qupdate"
+        if "false, true>" in name:
+            return "es_qrestore"
+        return "es_qperturb"
     if "es_perturb_kernel" in name:
         return "es_perturb"
     if "es_update_kernel" in name:
@@ -329,9 +505,10 @@ def _counter_rows(d):
     return out
 
 
-def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload):
-    """Write profiles/<kernel>_<workload>.md and profiles/counters.json from
-    the CSV output of the four rocprofv3 runs in PROFILE_COMMANDS."""
+def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload, int8=False):
+    """Write profiles/<kernel>_<workload>.md and merge the kernels' entries
+    into profiles/counters.json from the CSV output of the four rocprofv3 runs
+    in PROFILE_COMMANDS (with --int8 added for the int8 path)."""
     import csv
     import glob
     stats = list(csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0])))
@@ -343,27 +520,36 @@ def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload):
     f_scale, w_scale = copy_bytes / f_copy, copy_bytes / w_copy
     from paper_2608_17310_amd import workloads as wl
     P = wl.WORKLOADS[workload].n_params
-    counters = {"source_hash": _kernel_source_hash(), "workload": workload, "params": P,
-                "calibration": {"copy_bytes": copy_bytes, "fetch_scale": f_scale, "write_scale": w_scale}}
-    for kind in ("es_perturb", "es_update"):
+    label = workload + ("-int8" if int8 else "")
+    bytes_per_param = 2 if int8 else 4
+    dtype = "int8" if int8 else "bf16"
+    path = os.path.join(REPO, "profiles", "counters.json")
+    counters = json.load(open(path)) if os.path.exists(path) else {}
+    counters = {k: v for k, v in counters.items() if isinstance(v, dict) and "source_hash" in v}
+    suffix = " --int8" if int8 else ""
+    commands = [c.replace("bench.py --", "bench.py" + suffix + " --") for c in PROFILE_COMMANDS.values()]
+    for kind in (("es_qperturb", "es_qupdate") if int8 else ("es_perturb", "es_update")):
         st = [r for r in stats if _kind(r["Name"]) == kind][0]
         fb = float(np.mean(fetch[(kind, "FETCH_SIZE")])) * 1024 * f_scale
         wb = float(np.mean(write[(kind, "WRITE_SIZE")])) * 1024 * w_scale
         v = {c: float(np.mean(valu[(kind, c)])) for c in
              ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_WAVES",
               "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")}
-        counters[kind] = {"bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
+        counters[kind] = {"source_hash": _kernel_source_hash(), "workload": label, "params": P,
+                          "calibration": {"copy_bytes": copy_bytes, "fetch_scale": f_scale,
+                                          "write_scale": w_scale},
+                          "bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
                           "valu_insts_per_launch": v["SQ_INSTS_VALU"], "counters": v,
                           "avg_ns": float(st["AverageNs"]), "calls": int(st["Calls"])}
         lines = [
-            f"# {kind} on {workload} ({P:,} bf16 parameters)",
+            f"# {kind} on {label} ({P:,} {dtype} parameters)",
             "",
             "Commands (run from the repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first; "
             "`<out>` is an output directory):",
             "",
-        ] + [f"* `{c}`" for c in PROFILE_COMMANDS.values()] + [
+        ] + [f"* `{c}`" for c in commands] + [
             "",
-            f"Kernel-sources hash: `{counters['source_hash']}`",
+            f"Kernel-sources hash: `{_kernel_source_hash()}`",
             "",
             "## Kernel trace (--stats)",
             "",
@@ -376,7 +562,7 @@ def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload):
             f"* calibration copy of {copy_bytes} B read {f_copy:.0f} B by FETCH_SIZE and {w_copy:.0f} B by "
             f"WRITE_SIZE: scale factors {f_scale:.3f} and {w_scale:.3f}",
             f"* fetched {fb:.4e} B, written {wb:.4e} B, total {fb + wb:.4e} B = {(fb + wb) / P:.3f} B per "
-            f"parameter (algorithmic: 4)",
+            f"parameter (algorithmic: {bytes_per_param})",
             "",
             "## VALU counters per launch",
             "",
@@ -387,17 +573,28 @@ def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload):
             f"T/s of {VALU_PEAK_TINST:.1f} T/s peak",
             "",
         ]
-        with open(os.path.join(REPO, "profiles", f"{kind}_{workload}.md"), "w") as fh:
+        with open(os.path.join(REPO, "profiles", f"{kind}_{label}.md"), "w") as fh:
             fh.write("\n".join(lines))
-    with open(os.path.join(REPO, "profiles", "counters.json"), "w") as fh:
+    with open(path, "w") as fh:
         json.dump(counters, fh, indent=1)
-    print(json.dumps({k: counters[k]["bytes_per_launch"] for k in ("es_perturb", "es_update")}))
+    print(json.dumps({k: v["bytes_per_launch"] for k, v in counters.items()}))
+
+
+def _counters_for(path, kind, label):
+    """The counter entry of a kernel if it was taken on these kernel sources
+    and this workload, else None."""
+    if not os.path.exists(path):
+        return None
+    e = json.load(open(path)).get(kind)
+    if isinstance(e, dict) and e.get("source_hash") == _kernel_source_hash() and e.get("workload") == label:
+        return e
+    return None
 
 
 def _kernel_source_hash():
     import hashlib
     h = hashlib.sha256()
-    for f in ("es_noise.hpp", "esopt.hip"):
+    for f in ("es_noise.hpp", "es_quant.hpp", "esopt.hip"):
         h.update(open(os.path.join(REPO, "paper_2608_17310_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
