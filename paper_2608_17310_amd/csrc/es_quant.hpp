@@ -36,7 +36,10 @@ constexpr uint32_t kDomainQuantOffset = 2u;
 // Quantized tensor table entry.  Tiles are numbered as in the bf16 path:
 // full tiles (16-byte aligned base, in bounds) across all tensors, then tail
 // tiles.  numel < 2^31, so element indices within a tensor (and the end of
-// its last tile) fit 32 bits.
+// its last tile) fit 32 bits.  The row index j / row is computed as
+// mulhi(j, magic) >> shift, exact for every j < 2^31 (Granlund and
+// Montgomery, 1994: magic = ceil(2^(31 + l) / row), l = ceil(log2 row),
+// shift = l - 1).
 struct DevQTensor {
     int8_t* data;
     const float* scales;
@@ -45,8 +48,11 @@ struct DevQTensor {
     uint64_t first_tail;
     uint32_t row;                               // codes per scale; 0: one scale
     uint32_t tensor_id;
+    uint32_t magic;
+    uint32_t shift;
+    uint64_t pad;
 };
-static_assert(sizeof(DevQTensor) == 48, "quantized tensor table entry layout");
+static_assert(sizeof(DevQTensor) == 64, "quantized tensor table entry layout");
 
 struct QTileRef {
     int8_t* data;
@@ -55,6 +61,8 @@ struct QTileRef {
     uint32_t elem0;
     uint32_t row;
     uint32_t tensor_id;
+    uint32_t magic;
+    uint32_t shift;
 };
 
 template <uint32_t kTileElems>
@@ -63,7 +71,7 @@ __device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ 
     while (tile >= tab[t + 1].first_full) ++t;
     return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
                     static_cast<uint32_t>((tile - tab[t].first_full) * kTileElems), tab[t].row,
-                    tab[t].tensor_id};
+                    tab[t].tensor_id, tab[t].magic, tab[t].shift};
 }
 
 template <uint32_t kTileElems>
@@ -73,7 +81,7 @@ __device__ __forceinline__ QTileRef qlocate_tail(const DevQTensor* __restrict__ 
     const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
     return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
                     static_cast<uint32_t>((n_full + tile - tab[t].first_tail) * kTileElems),
-                    tab[t].row, tab[t].tensor_id};
+                    tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift};
 }
 
 typedef uint32_t q32x4_t __attribute__((ext_vector_type(4)));
@@ -122,12 +130,22 @@ __device__ __forceinline__ void qstore(int8_t* __restrict__ p, uint32_t e, uint3
 // The reciprocal of the scale of the 8 codes starting at element j (j is a
 // multiple of 8 and the row length a multiple of 8, so the 8 codes share
 // one scale), or 0 when the scale is not a normal positive finite value.
+// The hardware reciprocal (1 ulp) is well inside the offsets' tolerance.
 __device__ __forceinline__ float inv_scale(const QTileRef& r, uint32_t j) {
     if (j >= r.numel) return 0.0f;
     const ESQ_GLOBAL float* s = (const ESQ_GLOBAL float*)r.scales;
-    const float v = r.row == 0u ? s[0] : s[j / r.row];
+    const uint32_t idx = r.row == 0u ? 0u : __umulhi(j, r.magic) >> r.shift;
+    const float v = s[idx];
     const bool ok = v >= 0x1p-126f && v <= 0x1.fffffep127f;
-    return ok ? 1.0f / v : 0.0f;
+    return ok ? __builtin_amdgcn_rcpf(v) : 0.0f;
+}
+
+// The two reciprocal scales of a 16-code group (codes 0-7 and 8-15); one
+// lookup when the row length is a multiple of 16 (both halves in one row).
+__device__ __forceinline__ void group_inv_scales(const QTileRef& r, uint32_t e, float& inv0,
+                                                 float& inv1) {
+    inv0 = inv_scale(r, e);
+    inv1 = (r.row & 15u) == 0u ? inv0 : inv_scale(r, e + 8);
 }
 
 // One noise stream's scaled normals for the 16 codes of a group:
@@ -148,18 +166,26 @@ __device__ __forceinline__ void qgroup_axpy(uint32_t e, uint32_t tensor_id, uint
     }
 }
 
+// floor(x) as an integer in one instruction (the compiler emits a floor and
+// a conversion); x is within +-2^31 here.
+__device__ __forceinline__ int32_t floor_to_int(float x) {
+    int32_t r;
+    asm("v_cvt_flr_i32_f32 %0, %1" : "=v"(r) : "v"(x));
+    return r;
+}
+
 // New code: clamp(q + s * floor(d + r 2^-16), -127, 127) with s = -1 when
-// kNegate (a restore subtracts the offset its perturb added).  1 + r 2^-16 is
-// formed exactly from the draw's bits, so floor(d + r 2^-16) =
-// floor(d + (1 + r 2^-16)) - 1.  |d| is capped at 2^30 quanta, far beyond
-// what any code can absorb, so the integer arithmetic cannot overflow.
+// kNegate (a restore subtracts the offset its perturb added).  d + r 2^-16
+// is one fused multiply-add (one rounding of the exact sum).  |d| is capped
+// at 2^30 quanta, far beyond what any code can absorb, so the integer
+// arithmetic cannot overflow.
 template <bool kNegate>
 __device__ __forceinline__ int32_t qstep(int32_t q, float d, uint32_t draw16) {
-    const float one_plus = __uint_as_float((draw16 << 7) | 0x3F800000u);
-    const float dc = __builtin_fminf(__builtin_fmaxf(d, -0x1p30f), 0x1p30f);
-    const int32_t k = static_cast<int32_t>(__builtin_floorf(dc + one_plus)) - 1;
-    const int32_t v = kNegate ? q - k : q + k;
-    return min(max(v, -127), 127);
+    const float dc = __builtin_amdgcn_fmed3f(d, -0x1p30f, 0x1p30f);
+    const float v = __builtin_fmaf(static_cast<float>(draw16), 0x1p-16f, dc);
+    const int32_t k = floor_to_int(v);
+    const int32_t x = kNegate ? q - k : q + k;
+    return min(max(x, -127), 127);
 }
 
 }  // namespace esq

@@ -672,8 +672,8 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
         if (!kFast && e >= r.numel) break;
         uint32_t raw[4];
         esq::qload<kFast>(r.data, e, r.numel, raw);
-        const float inv0 = esq::inv_scale(r, e);
-        const float inv1 = esq::inv_scale(r, e + 8);
+        float inv0, inv1;
+        esq::group_inv_scales(r, e, inv0, inv1);
         float acc[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
@@ -1187,8 +1187,17 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
         const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
         const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
+        uint32_t magic = 0, shift = 0;
+        if (t.row != 0) {
+            // row index j / row = mulhi(j, magic) >> shift for all j < 2^31
+            uint32_t l = 0;
+            while ((uint64_t(1) << l) < t.row) ++l;
+            const uint64_t m = ((uint64_t(1) << (31 + l)) + t.row - 1) / t.row;
+            magic = static_cast<uint32_t>(m);
+            shift = l - 1;
+        }
         tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales, t.numel, n_full, n_tail,
-                                 t.row, t.tensor_id};
+                                 t.row, t.tensor_id, magic, shift, 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
         n_full += full;
         n_tail += tail;
@@ -1198,7 +1207,7 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
-    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu};
+    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu, 0u, 0u, 0u};
 
     es_qplan_t* p = new (std::nothrow) es_qplan_t;
     if (p == nullptr) return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation");
