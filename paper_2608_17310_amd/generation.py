@@ -8,7 +8,8 @@ regenerated from its seed; Section 3.1 sets sigma_t on a cosine schedule.
 
 With fused_swap the revert of member i and the apply of member i+1 are one
 pass (es_swap), so a generation of N members makes N + 1 passes over the
-parameters instead of 2N, plus the update.
+parameters instead of 2N, plus the update.  The same driver runs the int8
+path (esopt.QPlan), whose revert is exact and which has no fused swap.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is
@@ -51,8 +52,10 @@ def antithetic_seeds(base_seed, n_pairs):
 
 
 def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
-    """Apply member 0, visit it, move to member 1, ... and revert the last."""
+    """Apply member 0, visit it, move to member 1, ... and revert the last.
+    Plans without a fused swap (the int8 QPlan) revert and apply separately."""
     n = len(seeds)
+    fused_swap = fused_swap and hasattr(plan, "swap")
     plan.perturb(seeds[0], signs[0], sigma, stream=stream)
     for i in range(n):
         visit(i)

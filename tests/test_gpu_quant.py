@@ -259,3 +259,57 @@ def test_int8_27b_set_sampled():
         print("int8 27b", name, {"n": n, "bad": bad, "exact": exact / n})
         assert bad == 0, name
         assert exact / n >= 0.9999, name
+
+
+def test_int8_generation_replay_is_bit_exact():
+    """Four generations of the driver on the tiny set as int8 codes (revert
+    exact wherever nothing clamps, update rounded stochastically) are rebuilt
+    bit for bit from their records; the update-only replay equals the
+    oracle's chain of updates."""
+    from paper_2608_17310_amd.generation import run_generation, replay, antithetic_seeds
+    W = wl.TINY
+    host = wl.host_qparams(W)
+
+    def fresh():
+        codes = [_dev(q) for q, _, _ in host]
+        return codes, esopt.QPlan(codes, [_dev(s) for _, s, _ in host], [r for _, _, r in host])
+    codes, plan = fresh()
+    rng = np.random.default_rng(12)
+    records = []
+    for t in range(4):
+        seeds, signs = antithetic_seeds(50 * t, 3)
+        records.append(run_generation(plan, seeds, signs, 1e-3, 5e-3,
+                                      evaluate=lambda i: rng.random(), round_seed=500 + t))
+    torch.cuda.synchronize()
+    live = [_host(c) for c in codes]
+    plan.close()
+    codes2, plan2 = fresh()
+    replay(plan2, records)
+    torch.cuda.synchronize()
+    for a, b in zip(live, codes2):
+        np.testing.assert_array_equal(a, _host(b))
+    plan2.close()
+    codes3, plan3 = fresh()
+    replay(plan3, records, with_perturbations=False)
+    torch.cuda.synchronize()
+    for tid, ((q0, sc, row), dev) in enumerate(zip(host, codes3)):
+        x = q0
+        for rec in records:
+            x, st = oracle.qupdate(x, sc, row, tid, rec.seeds, rec.signs,
+                                   np.array(rec.rewards, np.float32), rec.alpha, rec.sigma,
+                                   round_seed=rec.round_seed)
+        assert np.mean(_host(dev) == x) >= 0.9999
+        assert np.max(np.abs(_host(dev).astype(np.int64) - x)) <= 1
+    plan3.close()
+    # the live run against the oracle's whole chain (walks and updates)
+    for tid, ((q0, sc, row), got) in enumerate(zip(host, live)):
+        x = q0
+        for rec in records:
+            for sd, sg in zip(rec.seeds, rec.signs):
+                x = oracle.qperturb(x, sc, row, sd, tid, sg, rec.sigma)
+                x = oracle.qrestore(x, sc, row, sd, tid, sg, rec.sigma)
+            x, st = oracle.qupdate(x, sc, row, tid, rec.seeds, rec.signs,
+                                   np.array(rec.rewards, np.float32), rec.alpha, rec.sigma,
+                                   round_seed=rec.round_seed)
+        assert np.mean(got == x) >= 0.9999
+        assert np.max(np.abs(got.astype(np.int64) - x)) <= 1
