@@ -239,6 +239,13 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
  * (0-based) uses sigma_t. Host-only helper. */
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T);
 
+/* Calibration pass: reads and rewrites every parameter of the plan unchanged
+ * with exactly the memory access pattern of es_perturb (same tiles, launch
+ * shape, pipelining and stores), so that its duration is the practical
+ * in-place streaming ceiling against which es_perturb is measured.  Every
+ * value is rewritten as itself (a NaN may come back quieted). */
+int es_stream_pass(es_plan_t* plan, es_stream_t stream);
+
 /* Test hooks exposing the device noise functions the kernels use.
  * es_philox_words: out_dev[4 i + k] = word k of the Philox call at counter
  *   (q & 0xffffffff, q >> 32, tensor_id, domain), q = quad0 + i,

@@ -28,9 +28,13 @@
 //     tiles; the loads of its next tile are issued before the current tile's
 //     arithmetic (software pipelining), and each tile's stores leave in one
 //     burst after all its arithmetic.  The update is VALU-bound (N noise
-//     streams per element): four workgroups per CU keep every wave slot busy,
-//     one 8-element group per lane at a time.  Both shapes were chosen by
-//     sweeping on MI355X.
+//     streams per element): eight workgroups per CU keep every wave slot
+//     busy, one 8-element group per lane at a time with the next group's
+//     load in flight.  Both shapes were chosen by sweeping on MI355X.  Swap
+//     is the perturb kernel with two streams and a bf16 rounding between
+//     them.
+//   * The int8 path (es_quant.hpp) has its own table and tiles of 16-code
+//     groups; all its passes are VALU-bound and use the update's shape.
 //   * Perturb/restore read and write each parameter once (4 bytes of HBM
 //     traffic per parameter).  The update regenerates the noise of all
 //     distinct member seeds for the same 8 elements in registers,
@@ -200,7 +204,9 @@ __device__ __forceinline__ void group_axpy(const uint32_t w[8], float scale_k, f
     }
 }
 
-// Noise streams applied by one perturb-style pass.  kM = 1: one stream,
+// Noise streams applied by one perturb-style pass.  kM = 0: none (a
+// calibration pass that rewrites every value unchanged with the same memory
+// access pattern).  kM = 1: one stream,
 // theta <- RNE(theta + c_0 eps_0) (perturb / restore).  kM = 2: two streams
 // applied in turn with a bf16 rounding in between,
 // theta <- RNE(RNE(theta + c_0 eps_0) + c_1 eps_1), which is es_restore of
@@ -629,9 +635,11 @@ PerturbKernel perturb_kernel_for(int threads, int groups) {
     return nullptr;
 }
 
-// streams: 1 (perturb / restore), 2 (swap, two keys), 3 (swap, one key)
+// streams: 0 (calibration pass), 1 (perturb / restore), 2 (swap, two keys),
+// 3 (swap, one key)
 PerturbKernel perturb_kernel(int streams, int threads, int groups) {
     switch (streams) {
+        case 0: return perturb_kernel_for<0>(threads, groups);
         case 1: return perturb_kernel_for<1>(threads, groups);
         case 2: return perturb_kernel_for<2>(threads, groups);
         case 3: return perturb_kernel_for<3>(threads, groups);
@@ -811,13 +819,13 @@ int check_device(const es_plan_t* p) {
 
 // One perturb-style pass applying `members` (1 or 2) noise streams with
 // coefficients coef[m] (sign sigma), nothing skipped.
-// One pass of the perturb kernel: streams = 1 (seed[0], coef[0]), 2 (two
-// keys) or 3 (both coefficients on seed[0]).
+// One pass of the perturb kernel: streams = 0 (no noise), 1 (seed[0],
+// coef[0]), 2 (two keys) or 3 (both coefficients on seed[0]).
 int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double* coef,
                    hipStream_t s) {
     if (p->n_full + p->n_tail == 0) return ES_OK;
     Streams st = {};
-    const int terms = streams == 1 ? 1 : 2;
+    const int terms = streams == 0 ? 0 : streams == 1 ? 1 : 2;
     for (int m = 0; m < terms; ++m) {
         const uint64_t sd = streams == 3 ? seed[0] : seed[m];
         st.k0[m] = static_cast<uint32_t>(sd);
@@ -1285,6 +1293,13 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
     ps.dk1 = static_cast<uint32_t>(opts->round_seed >> 32);
     ps.domain = es::kDomainRounding;
     return launch_qpass(plan, QKind::kUpdate, ps, s);
+}
+
+int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_stream_pass: null plan");
+    const int rc = check_device(plan);
+    if (rc != ES_OK) return rc;
+    return launch_streams(plan, 0, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T) {

@@ -59,6 +59,7 @@ SIGNATURES = {
     "es_perturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_restore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_swap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
+    "es_stream_pass": (ctypes.c_int, [_vp, _vp]),
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
@@ -183,6 +184,11 @@ class Plan:
     def restore(self, seed, sign, sigma, stream=None):
         _check(load().es_restore(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
                "es_restore")
+
+    def stream_pass(self, stream=None):
+        """Rewrite every parameter unchanged with es_perturb's access pattern
+        (the in-place streaming ceiling)."""
+        _check(load().es_stream_pass(self.handle, _stream(stream)), "es_stream_pass")
 
     def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
         """Revert member `from` and apply member `to` in one pass: the same

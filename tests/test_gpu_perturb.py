@@ -186,3 +186,16 @@ def test_results_do_not_depend_on_launch_shape(shape, monkeypatch):
     for a, b in zip(ref, got):
         for x, y in zip(a, b):
             np.testing.assert_array_equal(x, y)
+
+
+def test_stream_pass_rewrites_values_unchanged():
+    bits = [wl.random_bf16_bits(n, 95 + i) for i, n in enumerate([300001, 1 << 16, 9])]
+    bits[0][:6] = [0x0000, 0x8000, 0x7F80, 0xFF80, 0x0001, 0x807F]   # zeros, infinities, subnormals
+    ts = [to_device(b) for b in bits]
+    plan = esopt.Plan([ts[0][1:], ts[1], ts[2]])
+    plan.stream_pass()
+    plan.stream_pass()
+    torch.cuda.synchronize()
+    for b, t in zip(bits, ts):
+        np.testing.assert_array_equal(to_host(t), b)
+    plan.close()
