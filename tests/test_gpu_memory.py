@@ -1,0 +1,74 @@
+"""Memory stays at inference level (Section 3: only seeds are stored, the
+noise is regenerated): a plan costs its small tensor table and member scratch
+whatever the parameter count, and no pass allocates device memory.  Device
+free memory is read from the driver (the library allocates with hipMalloc,
+outside PyTorch's allocator)."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_17310_amd import esopt
+
+pytestmark = pytest.mark.gpu
+
+MB = 1 << 20
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _free():
+    torch.cuda.synchronize()
+    return torch.cuda.mem_get_info()[0]
+
+
+def test_plans_and_passes_allocate_no_parameter_sized_memory():
+    # 1 GiB of bf16 parameters and 512 MiB of int8 codes in a few tensors
+    params = [torch.randn(n, device="cuda").to(torch.bfloat16) for n in (1 << 28, 1 << 28, 12345)]
+    codes = [torch.randint(-127, 128, (n,), device="cuda", dtype=torch.int8) for n in (1 << 28, 1 << 28)]
+    scales = [torch.full(((1 << 28) // 4096,), 7e-4, device="cuda") for _ in codes]
+    rewards = torch.rand(32, device="cuda")
+    torch.cuda.empty_cache()
+
+    # warm up the runtime (code objects, kernel-argument pools) on a small plan
+    w = torch.zeros(4096, dtype=torch.bfloat16, device="cuda")
+    with esopt.Plan([w]) as p:
+        p.perturb(1, 1, 1e-3)
+        p.update(list(range(32)), [1] * 32, rewards, 5e-4)
+    with esopt.QPlan([torch.zeros(4096, dtype=torch.int8, device="cuda")],
+                     [torch.ones(1, device="cuda")], [0]) as q:
+        q.perturb(1, 1, 1e-3)
+        q.update(list(range(32)), [1] * 32, rewards, 5e-4)
+    torch.cuda.empty_cache()
+
+    f0 = _free()
+    plan = esopt.Plan(params)
+    qplan = esopt.QPlan(codes, scales, [4096, 4096])
+    f1 = _free()
+    print("plans took", (f0 - f1) / MB, "MiB")
+    assert f0 - f1 <= 8 * MB                      # tables + scratch, allocation granularity
+    seen = []
+    for rep in range(3):
+        plan.perturb(3, 1, 1e-3)
+        plan.swap(3, 1, 4, -1, 1e-3)
+        plan.restore(4, -1, 1e-3)
+        plan.update(list(range(32)), [1] * 32, rewards, 5e-4,
+                    flags=esopt.ES_UPDATE_STOCHASTIC_ROUND, round_seed=rep)
+        plan.stream_pass()
+        qplan.perturb(3, 1, 1e-3)
+        qplan.restore(3, 1, 1e-3)
+        qplan.update(list(range(32)), [1] * 32, rewards, 5e-4, round_seed=rep)
+        f2 = _free()
+        print("after passes", rep, (f1 - f2) / MB, "MiB")
+        seen.append(f2)
+        # the library allocates nothing in a pass; allow the HIP runtime a
+        # small one-off internal allocation on first use, then no growth
+        assert f1 - f2 <= 4 * MB
+    assert seen[1] == seen[0] and seen[2] == seen[0]
+    plan.close()
+    qplan.close()
+    assert _free() >= f1
