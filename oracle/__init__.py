@@ -35,21 +35,21 @@ are pinned (none is "parity unpinned").
 
 from .philox import philox4x32_10, philox4x32_10_bigint, MASK32
 from .noise import (key_words, counter_words, uniform_from_word, angle_from_word,
-                    box_muller, noise_words, normals, rounding_draws)
+                    box_muller, noise_words, normals, rounding_draws, spare_draws)
 from .bf16 import bf16_to_f64, f64_to_bf16_rne, f64_to_bf16_sr, bf16_ulp
 from .es import (perturb, restore, swap, zscore, update_coefficient, member_weights,
                  update, sigma_cosine, ES_UPDATE_DIV_SIGMA,
                  ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND)
-from .quant import (QMAX, row_scales, round_offset, offset_values, qperturb, qrestore,
-                    update_values, qupdate)
+from .quant import (QMAX, row_scales, round_offset, round_offset9, offset_values, qperturb,
+                    qrestore, update_values, qupdate)
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
     "key_words", "counter_words", "uniform_from_word", "angle_from_word", "box_muller",
-    "noise_words", "normals", "rounding_draws",
+    "noise_words", "normals", "rounding_draws", "spare_draws",
     "bf16_to_f64", "f64_to_bf16_rne", "f64_to_bf16_sr", "bf16_ulp",
     "perturb", "restore", "swap", "zscore", "update_coefficient", "member_weights",
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
     "ES_UPDATE_STOCHASTIC_ROUND",
-    "QMAX", "row_scales", "round_offset", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
+    "QMAX", "row_scales", "round_offset", "round_offset9", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
 ]

@@ -11,9 +11,8 @@ element of any tensor can be regenerated in isolation:
   counter = (q mod 2^32, q div 2^32, tensor_id, domain)    q = j div 4
   element j of tensor `tensor_id` uses the pair (w0, w1) of the call at
   counter q when j mod 4 is 0 or 1, and the pair (w2, w3) when it is 2 or 3.
-  domain is 0 for the perturbation noise, 1 for the draws of the update's
-  stochastic rounding and 2 for the draws that round the perturbation offsets
-  of quantized parameters (other values are reserved).
+  domain is 0 for the perturbation noise and 1 for the draws of the update's
+  stochastic rounding (other values are reserved).
 
   m(w) = w mod 2^23 (the low 23 bits of a word)
   radius uniform u(w) = (m(w) + 1/2) * 2^-23, in [2^-24, 1 - 2^-24]
@@ -24,6 +23,11 @@ element of any tensor can be regenerated in isolation:
       r   = sqrt(-2 ln u(wa)),  phi = 2 pi v(wb)
       first  element of the pair: r cos(phi)
       second element of the pair: r sin(phi)
+
+Spare bits: the uniform map reads only the low 23 bits of a word, so each
+word's top 9 bits are a free draw, independent of the normal it helps make.
+Element j's spare draw is the top 9 bits of word (j mod 4) of the call at its
+quad (the int8 path rounds perturbation offsets with it).
 
 Stochastic-rounding draws (domain 1, key from the update's rounding seed):
 one Philox call at counter (g mod 2^32, g div 2^32, tensor_id, 1), g = j div 8,
@@ -44,7 +48,6 @@ from .philox import philox4x32_10, MASK32
 
 DOMAIN_NOISE = 0
 DOMAIN_ROUNDING = 1
-DOMAIN_QUANT_OFFSET = 2
 
 
 def key_words(seed):
@@ -119,3 +122,13 @@ def rounding_draws(round_seed, tensor_id, elems, domain=DOMAIN_ROUNDING):
     picked = np.choose(word.astype(np.int64), [w[0], w[1], w[2], w[3]])
     shift = (elems & np.uint64(1)) * np.uint64(16)
     return ((picked >> shift) & np.uint64(0xFFFF)).astype(np.int64)
+
+
+def spare_draws(seed, tensor_id, elems):
+    """The 9-bit spare draw of each element index j: word (j mod 4) of the
+    noise call at quad j div 4, shifted right by 23 (int64 in [0, 511])."""
+    elems = np.atleast_1d(np.asarray(elems, dtype=np.uint64))
+    w = noise_words(seed, tensor_id, elems >> np.uint64(2))
+    lane = (elems & np.uint64(3)).astype(np.int64)
+    picked = np.choose(lane, [w[0], w[1], w[2], w[3]])
+    return (picked >> np.uint64(23)).astype(np.int64)

@@ -11,28 +11,31 @@ direction, for symmetric int8 codes:
 
 Perturbation in quantum units.  The real perturbation sign * sigma * eps_j is
 expressed in units of its row's quantum, d_j = sign * sigma * eps_j / s_r(j),
-and rounded stochastically to an integer offset with a 16-bit draw r_j:
+and rounded stochastically to an integer offset with a 9-bit draw r_j:
 
-  k_j = floor(d_j + r_j * 2^-16),      E[k_j] = d_j (to the 2^-16 grid)
+  k_j = floor(d_j + (2 r_j + 1) * 2^-10),   |E[k_j] - d_j| <= 2^-10
   q_j <- clamp(q_j + k_j, -127, 127)
 
 eps_j is the perturbation noise of the bf16 path (domain 0 under the member
-seed); r_j comes from domain 2 under the same seed, with the element-to-draw
-assignment of the update's rounding draws.  Because k_j is regenerated
-bit-for-bit from the seed, the revert q_j <- clamp(q_j - k_j) returns the
-exact code wherever the perturbation was not clamped: seed replay is exact in
-integers, with no drift.
+seed) and r_j the spare top 9 bits of element j's own noise word (see the
+noise module), so the rounding costs no generator calls.  Because k_j is
+regenerated bit-for-bit from the seed, the revert q_j <- clamp(q_j - k_j)
+returns the exact code wherever the perturbation was not clamped: seed replay
+is exact in integers, with no drift.
 
 Update in quantum units: delta_j = sum_d w_d eps_j(seed_d) / s_r(j) with the
-merged weights of the bf16 update, k_j = floor(delta_j + r_j * 2^-16) with r_j
-from domain 1 under the update's rounding seed, q_j <- clamp(q_j + k_j).  The
+merged weights of the bf16 update, k_j = floor(delta_j + r_j * 2^-16) with a
+16-bit r_j from domain 1 under the update's rounding seed (E[k_j] = delta_j to
+the 2^-16 grid), q_j <- clamp(q_j + k_j).  The
 rounding is always stochastic: the paper's update steps are a fraction of a
 quantum, and rounding to nearest would drop nearly all of them.
 
-Elements whose row scale is not a finite positive number are left unchanged.
+Elements whose row scale is not a normal positive finite binary32 value
+(2^-126 <= s < infinity) are left unchanged.
 
-Pins (tests/test_oracle_quant.py): the mean of k over all 65536 draws equals d
-exactly for d on the 2^-16 grid; every revert of an unclamped perturbation is
+Pins (tests/test_oracle_quant.py): the mean of k over all 65536 16-bit draws
+equals d exactly for d on the 2^-16 grid, and over all 512 9-bit draws lies
+within 2^-10 of d; every revert of an unclamped perturbation is
 exact; the variance of the offsets against the closed form
 (sigma/s)^2 + 1/6; a per-element pure-Python rendering (big-integer Philox,
 math.log / math.cos, explicit row lookup) agrees with the vectorised one; the
@@ -41,7 +44,7 @@ update's mean step against delta within its standard error; identities.
 
 import numpy as np
 
-from .noise import normals, rounding_draws, DOMAIN_QUANT_OFFSET, DOMAIN_ROUNDING
+from .noise import normals, rounding_draws, spare_draws, DOMAIN_ROUNDING
 from .es import zscore, update_coefficient, member_weights, ES_REWARDS_ARE_WEIGHTS
 
 QMAX = 127
@@ -62,14 +65,22 @@ def row_scales(scales, row, elems):
 
 
 def offset_values(scales, row, seed, tensor_id, sign, sigma, elems):
-    """d_j = sign sigma eps_j / s_r(j) (fp64), the draws r_j and the
-    validity of each element's scale; the offset is round_offset(d, r)."""
+    """d_j = sign sigma eps_j / s_r(j) (fp64), the 9-bit draws r_j and the
+    validity of each element's scale; the offset is round_offset9(d, r)."""
     el = np.asarray(elems, dtype=np.uint64)
     s = row_scales(scales, row, el)
-    ok = np.isfinite(s) & (s > 0)
+    ok = np.isfinite(s) & (s >= 2.0 ** -126)
     d = sign * _f32(sigma) * normals(seed, tensor_id, el) / np.where(ok, s, 1.0)
-    r = rounding_draws(seed, tensor_id, el, DOMAIN_QUANT_OFFSET)
-    return np.where(ok, d, 0.0), r, ok
+    return np.where(ok, d, 0.0), spare_draws(seed, tensor_id, el), ok
+
+
+def round_offset9(d, r9):
+    """k = floor(d + (2 r + 1) 2^-10): d rounded to an integer stochastically
+    with the 9-bit draw r (fp64 d, integer r in [0, 511])."""
+    r = np.asarray(r9, dtype=np.int64)
+    if np.any((r < 0) | (r > 511)):
+        raise ValueError("draws must be 9-bit integers")
+    return np.floor(np.asarray(d, dtype=np.float64) + (2 * r + 1) * 2.0 ** -10).astype(np.int64)
 
 
 def round_offset(d, r16):
@@ -88,7 +99,7 @@ def _apply(q, k, ok):
 
 
 def qperturb(q, scales, row, seed, tensor_id, sign, sigma, elems=None):
-    """q' = clamp(q + floor(sign sigma eps / s + r 2^-16), -127, 127)."""
+    """q' = clamp(q + floor(sign sigma eps / s + (2 r + 1) 2^-10), -127, 127)."""
     if sign not in (1, -1):
         raise ValueError("sign must be +1 or -1")
     q = np.asarray(q, dtype=np.int8).ravel()
@@ -96,7 +107,7 @@ def qperturb(q, scales, row, seed, tensor_id, sign, sigma, elems=None):
         return q.copy()
     el = np.arange(q.size, dtype=np.uint64) if elems is None else np.asarray(elems, np.uint64)
     d, r, ok = offset_values(scales, row, seed, tensor_id, sign, sigma, el)
-    return _apply(q, round_offset(d, r), ok)
+    return _apply(q, round_offset9(d, r), ok)
 
 
 def qrestore(q, scales, row, seed, tensor_id, sign, sigma, elems=None):
@@ -108,7 +119,7 @@ def qrestore(q, scales, row, seed, tensor_id, sign, sigma, elems=None):
         return q.copy()
     el = np.arange(q.size, dtype=np.uint64) if elems is None else np.asarray(elems, np.uint64)
     d, r, ok = offset_values(scales, row, seed, tensor_id, sign, sigma, el)
-    return _apply(q, -round_offset(d, r), ok)
+    return _apply(q, -round_offset9(d, r), ok)
 
 
 def update_values(scales, row, tensor_id, seeds, signs, rewards, alpha, sigma, flags=0,
@@ -127,7 +138,7 @@ def update_values(scales, row, tensor_id, seeds, signs, rewards, alpha, sigma, f
     distinct, w = member_weights([int(x) for x in seeds], [int(x) for x in signs], z, c)
     live = [(sd, wd) for sd, wd in zip(distinct, w) if wd != 0.0]
     s = row_scales(scales, row, el)
-    ok = np.isfinite(s) & (s > 0)
+    ok = np.isfinite(s) & (s >= 2.0 ** -126)
     delta = np.zeros(el.size)
     for sd, wd in live:
         delta += wd * normals(sd, tensor_id, el)

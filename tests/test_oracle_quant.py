@@ -9,7 +9,8 @@ import numpy as np
 import pytest
 
 import oracle
-from oracle import (round_offset, qperturb, qrestore, qupdate, philox4x32_10_bigint,
+from oracle import (round_offset, round_offset9, qperturb, qrestore, qupdate,
+                    philox4x32_10_bigint, spare_draws, noise_words,
                     ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_DIV_SIGMA)
 
 ALL_DRAWS = np.arange(65536, dtype=np.int64)
@@ -32,6 +33,39 @@ def test_round_offset_enumerated_draws(d):
 def test_round_offset_rejects_bad_draws():
     with pytest.raises(ValueError):
         round_offset(0.5, 65536)
+    with pytest.raises(ValueError):
+        round_offset9(0.5, 512)
+
+
+@pytest.mark.parametrize("d", [0.0, 0.5, -0.5, 2 ** -11, 1 - 2 ** -11, 3.3, -7.77, 126.999,
+                               -0.000244140625, 0.123456789])
+def test_round_offset9_enumerated_draws(d):
+    """Over all 512 draws: results floor(d) or floor(d) + 1, the step taken by
+    the top draws, exactly round(frac(d) * 512) of them when frac(d) * 512 is
+    not a half-integer, and the mean within 2^-10 of d."""
+    r = np.arange(512)
+    k = round_offset9(np.full(512, d), r)
+    lo = math.floor(d)
+    assert set(np.unique(k)) <= {lo, lo + 1}
+    ups = int(np.sum(k == lo + 1))
+    assert np.all(k[r >= 512 - ups] == lo + 1) and np.all(k[r < 512 - ups] == lo)
+    assert abs(np.sum(k) / 512.0 - d) <= 2.0 ** -10
+    frac = d - lo
+    if abs(frac * 512 - round(frac * 512) - 0.5) > 1e-9 and abs(frac * 512 % 1 - 0.5) > 1e-9:
+        assert ups == round(frac * 512)
+
+
+def test_spare_draws_are_the_top_bits_of_each_elements_own_word():
+    rng = np.random.default_rng(13)
+    for seed in (0, (1 << 64) - 1, 123456789):
+        el = np.concatenate([np.arange(12), rng.integers(0, 1 << 36, 30)]).astype(np.uint64)
+        w = noise_words(seed, 5, el >> np.uint64(2))
+        got = spare_draws(seed, 5, el)
+        for i, j in enumerate(el.tolist()):
+            assert got[i] == int(w[j & 3, i]) >> 23
+    d = spare_draws(77, 1, np.arange(1 << 18, dtype=np.uint64))
+    assert d.min() == 0 and d.max() == 511
+    assert abs(d.mean() - 255.5) < 5 * math.sqrt((512 ** 2 - 1) / 12 / d.size)
 
 
 def _codes(n, seed):
@@ -47,7 +81,7 @@ def test_revert_is_exact_wherever_nothing_clamps():
     p = qperturb(q, scales, row, 9, 3, 1, 1e-3)
     back = qrestore(p, scales, row, 9, 3, 1, 1e-3)
     d, r, ok = oracle.offset_values(scales, row, 9, 3, 1, 1e-3, np.arange(n, dtype=np.uint64))
-    k = round_offset(d, r)
+    k = round_offset9(d, r)
     unclamped = np.abs(q.astype(np.int64) + k) <= 127
     assert unclamped.mean() > 0.8 and (~unclamped).sum() > 100
     np.testing.assert_array_equal(back[unclamped], q[unclamped])
@@ -56,9 +90,10 @@ def test_revert_is_exact_wherever_nothing_clamps():
 
 
 def test_offsets_match_their_closed_form_distribution():
-    """With one scale, k = floor(d + r 2^-16), d = (sigma / s) eps: mean 0 and
-    variance (sigma / s)^2 + 1/6 (the stochastic rounding adds f(1 - f) with
-    the fractional part f uniform)."""
+    """With one scale, k = floor(d + (2 r + 1) 2^-10), d = (sigma / s) eps:
+    mean 0 and variance (sigma / s)^2 + 1/6 (the stochastic rounding adds
+    f(1 - f) with the fractional part f uniform; the 9-bit grid changes that
+    by under 1e-6)."""
     n = 1 << 20
     s = np.float32(7e-4)
     ratio = float(np.float32(1e-3)) / float(s)
@@ -109,7 +144,10 @@ def test_pure_python_rendering_matches_perturb_and_update():
             assert g == q[j]
             continue
         d = -sig * _eps(seed, tid, j) / s
-        k = math.floor(d + _draw(seed, tid, j, 2) * 2.0 ** -16)
+        qd = j >> 2
+        word = philox4x32_10_bigint((qd & 0xFFFFFFFF, qd >> 32, tid, 0),
+                                    (seed & 0xFFFFFFFF, seed >> 32))[j & 3]
+        k = math.floor(d + (2 * (word >> 23) + 1) * 2.0 ** -10)
         assert g == max(-127, min(127, int(q[j]) + k)), j
     # the update: two members, weights as given, domain-1 draws under round_seed
     seeds, signs, w = [3, 8], [1, -1], np.array([0.7, -0.2], np.float32)
