@@ -189,13 +189,10 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
  *
  * A quantized tensor holds symmetric int8 codes q_j in [-127, 127] with
  * binary32 scales: theta_j = s_r q_j, r = j / row (row == 0: one scale for
- * the tensor).  Every pass moves codes by integer offsets in units of the
- * quantum:  k_j = floor(d_j + r_j 2^-16),  q_j <- clamp(q_j +- k_j, -127, 127),
- * where d_j is the step in quanta and r_j a 16-bit draw, so E[k_j] = d_j.
- * Elements whose scale is not a normal positive finite binary32 value are
- * left unchanged.  Draws: Philox4x32-10 at counter (g lo, g hi, tensor_id,
- * domain), g = j >> 3, one call per 8 codes; code j takes word (j & 7) >> 1,
- * low half for even j, high half for odd j. */
+ * the tensor).  Every pass moves codes by an integer offset k_j, the step d_j
+ * in quanta rounded stochastically (E[k_j] = d_j), and clamps:
+ * q_j <- clamp(q_j +- k_j, -127, 127).  Elements whose scale is not a normal
+ * positive finite binary32 value are left unchanged. */
 typedef struct es_qtensor {
     void*        data;       /* device int8 codes, contiguous; any alignment
                                 (16-byte aligned data takes the vector path) */
@@ -216,16 +213,19 @@ int es_qplan_destroy(es_qplan_t* plan);
 uint64_t es_qplan_numel(const es_qplan_t* plan);
 
 /* Perturb (Section 3, in quanta): d_j = sign sigma eps_j(seed) / s_r with the
- * bf16 path's noise, draws of domain 2 under the same seed;
- * q_j <- clamp(q_j + k_j).  es_qrestore regenerates the same k_j and
- * subtracts it, so perturb then restore returns every code whose perturbed
- * value was not clamped exactly.  sigma finite and >= 0 (0: nothing runs). */
+ * bf16 path's noise, k_j = floor(d_j + (2 r_j + 1) 2^-10) with r_j the top 9
+ * bits of word j & 3 of element j's own noise call (bits the uniform map does
+ * not read); q_j <- clamp(q_j + k_j).  es_qrestore regenerates the same k_j
+ * and subtracts it, so perturb then restore returns every code whose
+ * perturbed value was not clamped exactly.  sigma finite and >= 0 (0: nothing
+ * runs). */
 int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
 int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
 
 /* Update (Section 3 / Appendix C.1, in quanta): the z-score, coefficient and
- * merged weights of es_update, d_j = sum_d w_d eps_j(seed_d) / s_r, draws of
- * domain 1 under opts->round_seed; q_j <- clamp(q_j + k_j).  The rounding is
+ * merged weights of es_update, d_j = sum_d w_d eps_j(seed_d) / s_r,
+ * k_j = floor(d_j + r_j 2^-16) with the 16-bit draws of es_update's
+ * stochastic rounding (domain 1 under opts->round_seed); q_j <- clamp(q_j + k_j).  The rounding is
  * always stochastic (steps are usually a fraction of a quantum, which
  * rounding to nearest would drop); ES_UPDATE_STOCHASTIC_ROUND is accepted
  * and changes nothing.  Other arguments, status and z_out as es_update. */

@@ -7,14 +7,16 @@
 //   k_j = floor(d_j + r_j 2^-16),   E[k_j] = d_j,
 // with a 16-bit draw r_j, and q_j <- clamp(q_j + k_j, -127, 127).
 //   * perturb / restore: d_j = sign sigma eps_j / s, eps_j the bf16 path's
-//     noise (domain 0) under the member seed, r_j from domain 2 under the same
-//     seed; restore subtracts the very same k_j, so it is exact wherever the
-//     perturbation did not clamp.
-//   * update: d_j = sum_d w_d eps_j(seed_d) / s, r_j from domain 1 under the
-//     update's rounding seed.
-// Draw assignment (both domains): one Philox call at counter
-// (g lo, g hi, tensor_id, domain), g = j >> 3, serves elements 8g .. 8g+7;
-// element j takes word (j & 7) >> 1, low half for even j, high half for odd.
+//     noise (domain 0) under the member seed, and
+//     k_j = floor(d_j + (2 r_j + 1) 2^-10) with r_j the top 9 bits of word
+//     j & 3 of element j's own noise call (the uniform map reads only the low
+//     23 bits, so these are free); restore subtracts the very same k_j, so it
+//     is exact wherever the perturbation did not clamp.
+//   * update: d_j = sum_d w_d eps_j(seed_d) / s and
+//     k_j = floor(d_j + r_j 2^-16) with a 16-bit r_j from domain 1 under the
+//     update's rounding seed: one Philox call at counter
+//     (g lo, g hi, tensor_id, 1), g = j >> 3, serves elements 8g .. 8g+7;
+//     element j takes word (j & 7) >> 1, low half for even j, high for odd.
 // Elements whose scale is not a normal positive finite binary32 value are
 // left unchanged.
 //
@@ -31,7 +33,6 @@
 namespace esq {
 
 constexpr int kQGroup = 16;                     // int8 codes per lane-group
-constexpr uint32_t kDomainQuantOffset = 2u;
 
 // Quantized tensor table entry.  Tiles are numbered as in the bf16 path:
 // full tiles (16-byte aligned base, in bounds) across all tensors, then tail
@@ -174,7 +175,22 @@ __device__ __forceinline__ int32_t floor_to_int(float x) {
     return r;
 }
 
-// New code: clamp(q + s * floor(d + r 2^-16), -127, 127) with s = -1 when
+// 1 + (2 r + 1) 2^-10 as a binary32 from the top 9 bits r of a noise word.
+__device__ __forceinline__ float spare_one_plus(uint32_t w) {
+    return __uint_as_float(((w >> 9) & 0x007FC000u) | 0x3F802000u);
+}
+
+// Perturb / restore code: clamp(q +- floor(d + (2 r + 1) 2^-10), -127, 127)
+// with f = 1 + (2 r + 1) 2^-10: floor(d + f) - 1 (one rounding of d + f).
+template <bool kNegate>
+__device__ __forceinline__ int32_t qstep9(int32_t q, float d, float f) {
+    const float dc = __builtin_amdgcn_fmed3f(d, -0x1p30f, 0x1p30f);
+    const int32_t k = floor_to_int(dc + f) - 1;
+    const int32_t x = kNegate ? q - k : q + k;
+    return min(max(x, -127), 127);
+}
+
+// Update code: clamp(q + s * floor(d + r 2^-16), -127, 127) with s = -1 when
 // kNegate (a restore subtracts the offset its perturb added).  d + r 2^-16
 // is one fused multiply-add (one rounding of the exact sum).  |d| is capped
 // at 2^30 quanta, far beyond what any code can absorb, so the integer

@@ -658,18 +658,48 @@ UpdateKernel update_kernel(int threads, int groups, bool stochastic) {
 
 // ---- int8 path (device code of the passes; helpers in es_quant.hpp) ----
 
-// Kernel arguments of one int8 pass: the key and domain of the rounding
+// Kernel arguments of one int8 pass: the key of the update's rounding
 // draws, and for perturb / restore the single member inline.
 struct QPass {
     uint32_t dk0, dk1;
-    uint32_t domain;
-    uint32_t pad;
+    uint32_t pad0, pad1;
     Member m;
 };
 
+// Perturb / restore of one 16-code group: per quad of codes one noise call,
+// whose words give the four normals and the four rounding draws.
+template <bool kNegate>
+__device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e,
+                                               uint32_t tensor_id, const Member& m, float inv0,
+                                               float inv1, uint32_t out[4]) {
+    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, m.k0, m.k1);
+        const float inv = c < 2 ? inv0 : inv1;
+        const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+        uint32_t o = 0;
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            float t, cs, sn;
+            es::scaled_pair(ws[2 * p], ws[2 * p + 1], m.w_k, t, cs, sn);
+            const float d[2] = {t * cs * inv, t * sn * inv};
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = 2 * p + h;
+                const int32_t qc = static_cast<int8_t>(raw[c] >> (8 * i));
+                const int32_t v =
+                    inv != 0.0f ? esq::qstep9<kNegate>(qc, d[h], esq::spare_one_plus(ws[i])) : qc;
+                o |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+            }
+        }
+        out[c] = o;
+    }
+}
+
 // One tile of an int8 pass: for each of the lane's 16-code groups in turn,
-// d = (sum over members of w eps) / s in binary32, then the stochastically
-// rounded integer offset and the clamped code.
+// the step d in quanta (binary32) and the stochastically rounded, clamped
+// code.
 template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate>
 __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
                                       uint32_t n_members, const QPass& ps) {
@@ -682,45 +712,46 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
         esq::qload<kFast>(r.data, e, r.numel, raw);
         float inv0, inv1;
         esq::group_inv_scales(r, e, inv0, inv1);
-        float acc[16];
+        uint32_t out[4];
+        if constexpr (!kTable) {
+            qperturb_group<kNegate>(raw, e, r.tensor_id, ps.m, inv0, inv1, out);
+        } else {
+            float acc[16];
 #pragma unroll
-        for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
-        if constexpr (kTable) {
+            for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
             for (uint32_t d = 0; d < n_members; ++d) {
                 const Member m = members[d];
                 if (m.w_k == 0.0f) continue;
                 esq::qgroup_axpy(e, r.tensor_id, m.k0, m.k1, m.w_k, acc);
             }
-        } else {
-            esq::qgroup_axpy(e, r.tensor_id, ps.m.k0, ps.m.k1, ps.m.w_k, acc);
-        }
-        const es::Words da = es::philox4x32_10(e >> 3, 0u, r.tensor_id, ps.domain, ps.dk0, ps.dk1);
-        const es::Words db = es::philox4x32_10((e >> 3) + 1u, 0u, r.tensor_id, ps.domain, ps.dk0,
-                                               ps.dk1);
-        const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
-        uint32_t out[4];
+            const es::Words da =
+                es::philox4x32_10(e >> 3, 0u, r.tensor_id, es::kDomainRounding, ps.dk0, ps.dk1);
+            const es::Words db = es::philox4x32_10((e >> 3) + 1u, 0u, r.tensor_id,
+                                                   es::kDomainRounding, ps.dk0, ps.dk1);
+            const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            uint32_t w = 0;
+            for (int k = 0; k < 4; ++k) {
+                uint32_t w = 0;
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int c = 4 * k + i;
-                const float inv = c < 8 ? inv0 : inv1;
-                const int32_t q = static_cast<int8_t>(raw[k] >> (8 * i));
-                const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
-                const int32_t v = inv != 0.0f ? esq::qstep<kNegate>(q, acc[c] * inv, draw) : q;
-                w |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+                for (int i = 0; i < 4; ++i) {
+                    const int c = 4 * k + i;
+                    const float inv = c < 8 ? inv0 : inv1;
+                    const int32_t q = static_cast<int8_t>(raw[k] >> (8 * i));
+                    const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
+                    const int32_t v = inv != 0.0f ? esq::qstep<false>(q, acc[c] * inv, draw) : q;
+                    w |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+                }
+                out[k] = w;
             }
-            out[k] = w;
         }
         esq::qstore<kFast>(r.data, e, r.numel, out);
     }
 }
 
 // An int8 pass over the whole quantized parameter list: perturb / restore
-// (one inline member, draws of domain 2 under its seed) or the update
-// (member table and header written by es_prepare_kernel, draws of domain 1
-// under the rounding seed).
+// (one inline member, draws from its own noise words) or the update (member
+// table and header written by es_prepare_kernel, draws of domain 1 under the
+// rounding seed).
 template <int kThreads, int kU, bool kTable, bool kNegate>
 __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTensor* __restrict__ tab,
                                                             uint64_t n_full, uint64_t n_tail,
@@ -888,10 +919,8 @@ int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_st
     if (rc != ES_OK) return rc;
     const double coef = sign > 0 ? double(sigma) : -double(sigma);
     QPass ps = {};
-    ps.dk0 = static_cast<uint32_t>(seed);
-    ps.dk1 = static_cast<uint32_t>(seed >> 32);
-    ps.domain = esq::kDomainQuantOffset;
-    ps.m = Member{ps.dk0, ps.dk1, static_cast<float>(coef * kSqrt2Ln2Double), 0u};
+    ps.m = Member{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                  static_cast<float>(coef * kSqrt2Ln2Double), 0u};
     return launch_qpass(p, kind, ps, static_cast<hipStream_t>(stream));
 }
 
@@ -1291,7 +1320,6 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
     QPass ps = {};
     ps.dk0 = static_cast<uint32_t>(opts->round_seed);
     ps.dk1 = static_cast<uint32_t>(opts->round_seed >> 32);
-    ps.domain = es::kDomainRounding;
     return launch_qpass(plan, QKind::kUpdate, ps, s);
 }
 

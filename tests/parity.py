@@ -83,10 +83,11 @@ def update_delta(tensor_id, seeds, signs, rewards, alpha, sigma, flags, elems, z
 
 
 # ------------------------------------------------------------------ int8 path --
-# The int8 passes turn a binary32 step d (in quanta) and a 16-bit draw r into
-# the integer floor(d + r 2^-16).  The GPU's d differs from the oracle's fp64
+# The int8 passes turn a binary32 step d (in quanta) and a draw into the
+# integer floor(v): v = d + (2 r + 1) 2^-10 for a perturbation (9-bit r),
+# v = d + r 2^-16 for an update (16-bit r).  The GPU's d differs from the oracle's fp64
 # d by the noise error (|d eps| <= 4e-6 + 2e-6 |eps| per unit weight) and a
-# few binary32 roundings, so where d + r 2^-16 lies within that bound of an
+# few binary32 roundings, so where v lies within that bound of an
 # integer both floor values are correct; everywhere else the code is unique.
 
 F32_EPS = 2.0 ** -23
@@ -99,12 +100,12 @@ def q_tolerance(abs_weight_sum, noise_abs_sum, d):
             + 4 * F32_EPS * (np.abs(d) + 2.0))
 
 
-def qreport(got, q_in, d, r, tol, ok, negate=False):
-    """Compare GPU codes with the oracle's rule code = clamp(q +- floor(d +
-    r 2^-16)); near-integer cases (within tol) accept either floor."""
+def qreport(got, q_in, v, tol, ok, negate=False):
+    """Compare GPU codes with the oracle's rule code = clamp(q +- floor(v)),
+    v the fp64 decision value (the step in quanta plus the draw's offset);
+    near-integer cases (within tol) accept either floor."""
     got = np.asarray(got, dtype=np.int8).astype(np.int64)
     q = np.asarray(q_in, dtype=np.int8).astype(np.int64)
-    v = d + np.asarray(r, dtype=np.int64) * 2.0 ** -16
     k = np.floor(v).astype(np.int64)
     near = np.abs(v - np.round(v)) <= tol
     alt = np.where(v - np.round(v) < 0, k + 1, k - 1)     # the other side of the integer

@@ -37,16 +37,18 @@ def _host(t):
 
 
 def _perturb_expect(scales, row, seed, tid, sign, sigma, el):
+    """(v, ok, tol): the oracle's decision value floor(v) = offset."""
     d, r, ok = oracle.offset_values(scales, row, seed, tid, sign, sigma, el)
     s = oracle.row_scales(scales, row, el)
     s = np.where(ok, s, 1.0)
     s32 = float(np.float32(sigma))
     eps = oracle.normals(seed, tid, el)
     tol = q_tolerance(s32 / s, np.abs(s32 * eps) / s, d)
-    return d, r, ok, tol
+    return d + (2 * r + 1) * 2.0 ** -10, ok, tol
 
 
 def _update_expect(scales, row, tid, seeds, signs, rewards, alpha, sigma, flags, el, rs):
+    """(v, ok, tol, live, status) of the update."""
     d, r, ok, live, st = oracle.update_values(scales, row, tid, seeds, signs, rewards, alpha,
                                               sigma, flags, elems=el, round_seed=rs)
     s = np.where(ok, oracle.row_scales(scales, row, el), 1.0)
@@ -55,7 +57,7 @@ def _update_expect(scales, row, tid, seeds, signs, rewards, alpha, sigma, flags,
     for sd, w in live:
         wsum += abs(w) / s
         nsum += np.abs(w * oracle.normals(sd, tid, el)) / s
-    return d, r, ok, q_tolerance(wsum, nsum, d), live, st
+    return d + r * 2.0 ** -16, ok, q_tolerance(wsum, nsum, d), live, st
 
 
 def _tensor_set():
@@ -98,11 +100,11 @@ def test_qperturb_and_restore_match_oracle():
     assert _host(bufs[-1][:3]).tolist() == [5, -5, 9]
     for i, (q, sc, row, tid) in enumerate(zip(codes, scales, rows, ids)):
         el = np.arange(q.size, dtype=np.uint64)
-        d, r, ok, tol = _perturb_expect(sc, row, seed, tid, sign, sigma, el)
-        rep = qreport(pert[i], q, d, r, tol, ok)
+        v, ok, tol = _perturb_expect(sc, row, seed, tid, sign, sigma, el)
+        rep = qreport(pert[i], q, v, tol, ok)
         print("qperturb", i, rep)
         assert_qparity(rep, f"qperturb tensor {i}")
-        rep = qreport(back[i], pert[i], d, r, tol, ok, negate=True)
+        rep = qreport(back[i], pert[i], v, tol, ok, negate=True)
         print("qrestore", i, rep)
         assert_qparity(rep, f"qrestore tensor {i}")
         # exact revert wherever the perturbed code was not at a clamp bound
@@ -130,10 +132,10 @@ def test_qupdate_matches_oracle(flags):
     assert int(status.item()) == 0
     for i, (q, sc, row, tid) in enumerate(zip(codes, scales, rows, ids)):
         el = np.arange(q.size, dtype=np.uint64)
-        d, rr, ok, tol, live, st = _update_expect(sc, row, tid, seeds, signs, r, alpha, 1e-3,
-                                                  flags, el, rs)
+        v, ok, tol, live, st = _update_expect(sc, row, tid, seeds, signs, r, alpha, 1e-3,
+                                              flags, el, rs)
         got = _host(views[i])
-        rep = qreport(got, q, d, rr, tol, ok)
+        rep = qreport(got, q, v, tol, ok)
         print("qupdate", flags, i, rep)
         assert_qparity(rep, f"qupdate flags={flags} tensor {i}")
         assert np.mean(got != q) > 0.05 or q.size < 100
@@ -150,8 +152,8 @@ def test_qupdate_large_population_and_oracle_function():
     plan.update(seeds, [1] * 64, _dev(r), 2e-2, round_seed=3)
     torch.cuda.synchronize()
     el = np.arange(q.size, dtype=np.uint64)
-    d, rr, ok, tol, live, st = _update_expect(sc, 1024, 0, seeds, [1] * 64, r, 2e-2, 0.0, 0, el, 3)
-    rep = qreport(_host(t), q, d, rr, tol, ok)
+    v, ok, tol, live, st = _update_expect(sc, 1024, 0, seeds, [1] * 64, r, 2e-2, 0.0, 0, el, 3)
+    rep = qreport(_host(t), q, v, tol, ok)
     print("qupdate N=64", rep)
     assert_qparity(rep, "qupdate N=64")
     exp, st = oracle.qupdate(q, sc, 1024, 0, seeds, [1] * 64, r, 2e-2, 0.0, round_seed=3)
@@ -242,17 +244,17 @@ def test_int8_27b_set_sampled():
     for t, el_i in enumerate(idx):
         el = el_i.astype(np.uint64)
         sc, row = host_scales[t], rows[t]
-        d, rr, ok, tol = _perturb_expect(sc, row, seed, t, 1, sigma, el)
+        v, ok, tol = _perturb_expect(sc, row, seed, t, 1, sigma, el)
         for name, got, base, neg in (("perturb", pert[t], q0[t], False),
                                      ("restore", back[t], pert[t], True)):
-            rep = qreport(got, base, d, rr, tol, ok, negate=neg)
+            rep = qreport(got, base, v, tol, ok, negate=neg)
             tot[name][0] += rep["n"]; tot[name][1] += rep["bad"]
             tot[name][2] += int(round(rep["exact"] * rep["n"]))
         free = np.abs(pert[t].astype(np.int64)) < 127
         np.testing.assert_array_equal(back[t][free], q0[t][free])
-        d, rr, ok, tol, live, st = _update_expect(sc, row, t, seeds, signs, r, W.alpha, sigma, 0,
-                                                  el, 77)
-        rep = qreport(upd[t], back[t], d, rr, tol, ok)
+        v, ok, tol, live, st = _update_expect(sc, row, t, seeds, signs, r, W.alpha, sigma, 0,
+                                              el, 77)
+        rep = qreport(upd[t], back[t], v, tol, ok)
         tot["update"][0] += rep["n"]; tot["update"][1] += rep["bad"]
         tot["update"][2] += int(round(rep["exact"] * rep["n"]))
     for name, (n, bad, exact) in tot.items():
