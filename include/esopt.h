@@ -24,7 +24,9 @@
  *
  * Parameters are bf16 (the paper states no dtype; its memory figures imply
  * 16-bit weights).  Each result is computed in binary32 and rounded to bf16
- * round-to-nearest-even, with exactly one read and one write per element.
+ * round-to-nearest-even (the update can instead round stochastically), with
+ * exactly one read and one write per element.  Int8 parameters with per-row
+ * scales have a plan of their own (es_qplan_*, further down).
  *
  * Conventions for every call:
  *   - Device pointers are HIP device memory of the device current at the
