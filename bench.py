@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
     ap.add_argument("--swap", action="store_true",
                     help="move between members with the fused es_swap (N+1 passes per step)")
+    ap.add_argument("--sweep-members", default=None, metavar="N1,N2,...",
+                    help="large-population sweep of the fused update on the 4B-shaped set "
+                         "(one JSON line per N)")
     ap.add_argument("--int8", action="store_true",
                     help="the int8 path: codes with per-row scales, es_qperturb / es_qrestore / "
                          "es_qupdate")
@@ -175,6 +178,46 @@ def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_te
 
 # ---------------------------------------------------------------- GPU leg --
 
+def run_sweep(args):
+    """The fused update alone on the 4B-shaped set for each population size N
+    (distinct seeds, rewards N(0,1)): where the update turns from HBM-bound
+    (4 B per parameter whatever N) to VALU-bound (N normals per parameter)."""
+    import torch
+    from paper_2608_17310_amd import esopt, workloads as wl
+    torch.cuda.set_device(0)
+    ns = [int(x) for x in args.sweep_members.split(",")]
+    W = wl.DENSE_4B
+    flat, views = wl.device_params(W)
+    plan = esopt.Plan(views)
+    P = plan.numel
+    stream = torch.cuda.current_stream()
+    for n in ns:
+        Wn = wl.sweep_workload(n)
+        r = torch.from_numpy(wl.rewards(Wn)).cuda()
+        seeds = list(Wn.seeds)
+        # one member z-scores to zero (no update): use its reward as the weight
+        flags = esopt.ES_REWARDS_ARE_WEIGHTS if n == 1 else 0
+        plan.update(seeds, list(Wn.signs), r, Wn.alpha, flags=flags)
+        ts = []
+        for _ in range(max(args.steps, 1)):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            plan.update(seeds, list(Wn.signs), r, Wn.alpha, flags=flags)
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1) / 1e3)
+        t = float(np.median(ts))
+        hbm_t = 4 * P / (HBM_PEAK_GBS * 1e9)
+        print(json.dumps({"sweep": "fused es_update", "workload": W.name, "params": P, "members": n,
+                          "ms": round(t * 1e3, 3), "params_per_s": P / t,
+                          "normals_per_s": n * P / t,
+                          "GBps_algorithmic": round(4 * P / t / 1e9, 1),
+                          "hbm_time_at_peak_ms": round(hbm_t * 1e3, 3),
+                          "bound": "hbm" if t < 1.25 * hbm_t else "valu"}), flush=True)
+    plan.close()
+
+
 def run_int8(args):
     """The int8 step on the workload's shapes: N x (es_qperturb + es_qrestore)
     + es_qupdate over codes with per-row scales, inputs resident in HBM."""
@@ -304,6 +347,8 @@ def main():
         print(json.dumps({"error": "this build runs the ES parameter path on one GPU; "
                                    "--gpus above 1 is not supported (see the sharding design)"}))
         sys.exit(2)
+    if args.sweep_members:
+        return run_sweep(args)
     if args.int8:
         return run_int8(args)
     import torch
