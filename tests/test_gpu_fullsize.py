@@ -113,3 +113,63 @@ def test_full_size_sampled_parity(name):
 
 def test_large_population_sweep_n256_on_4b_set():
     _run(wl.sweep_workload(256), samples_per_tensor=64)
+
+
+def test_single_tensor_beyond_2_34_elements():
+    """One bf16 tensor of 2^34 + 4099 elements (32 GiB): past element 2^34 the
+    quad index needs its high counter word and the draw group index passes
+    2^31; elements on both sides of that boundary, of the last full tile and
+    of the ragged tail are checked against the oracle after perturb, swap,
+    restore and both update roundings."""
+    n = (1 << 34) + 4099
+    t = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    t.normal_(0.0, 0.02, generator=g)
+    plan = esopt.Plan([t], tensor_ids=[77])
+    b = 1 << 34
+    idx = np.unique(np.concatenate([
+        np.arange(0, 16), np.arange(b - 24, b + 24), np.arange(n - 4099 - 8, n - 4099 + 8),
+        np.arange(n - 24, n), np.random.default_rng(1).integers(0, n, 400)]).astype(np.int64))
+    idx_dev = torch.from_numpy(idx).cuda()
+    el = idx.astype(np.uint64)
+
+    def gather():
+        torch.cuda.synchronize()
+        return to_host(t.index_select(0, idx_dev))
+    x0 = gather()
+    plan.perturb(11, -1, 1e-3)
+    x1 = gather()
+    plan.swap(11, -1, 12, 1, 1e-3)
+    x2 = gather()
+    plan.restore(12, 1, 1e-3)
+    x3 = gather()
+    r = np.array([0.2, 0.7, 0.4], np.float32)
+    plan.update([3, 4, 5], [1, 1, 1], torch.from_numpy(r).cuda(), 5e-4)
+    x4 = gather()
+    plan.update([3, 4, 5], [1, 1, 1], torch.from_numpy(r).cuda(), 5e-4,
+                flags=esopt.ES_UPDATE_STOCHASTIC_ROUND, round_seed=(1 << 63) + 9)
+    x5 = gather()
+    plan.close()
+    del t
+    torch.cuda.empty_cache()
+    checks = [
+        ("perturb", x1, oracle.perturb(x0, 11, 77, -1, 1e-3, elems=el), x0,
+         perturb_delta(11, 77, -1, 1e-3, el)),
+        ("swap", x2, oracle.swap(x1, 77, 11, -1, 1e-3, 12, 1, 1e-3, elems=el), x1,
+         perturb_delta(11, 77, 1, 1e-3, el) + perturb_delta(12, 77, 1, 1e-3, el)),
+        ("restore", x3, oracle.restore(x2, 12, 77, 1, 1e-3, elems=el), x2,
+         perturb_delta(12, 77, -1, 1e-3, el)),
+        ("update", x4, oracle.update(x3, 77, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el)[0], x3,
+         update_delta(77, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, 0, el)),
+        ("update_sr", x5, oracle.update(x4, 77, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el,
+                                        flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+                                        round_seed=(1 << 63) + 9)[0], x4,
+         update_delta(77, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, 0, el)),
+    ]
+    for name, got, exp, base, delta in checks:
+        rep = report(got, exp, base, delta)
+        print("2^34+", name, rep)
+        assert rep["max_ulp"] <= 1.0, (name, rep)
+        assert rep["exact"] >= 0.99, (name, rep)
+    assert np.mean(x1 != x0) > 0.5

@@ -315,3 +315,45 @@ def test_int8_generation_replay_is_bit_exact():
                                    round_seed=rec.round_seed)
         assert np.mean(got == x) >= 0.9999
         assert np.max(np.abs(got.astype(np.int64) - x)) <= 1
+
+
+def test_int8_tensor_at_the_code_limit():
+    """An int8 tensor of 2^31 - 9 codes (the largest accepted) with rows of 4096:
+    codes near the end, across the last full tile and in the ragged tail are
+    checked after perturb, restore and update."""
+    n = (1 << 31) - 9
+    row = 4096
+    q = torch.randint(-100, 101, (n,), dtype=torch.int8, device="cuda")
+    n_rows = -(-n // row)
+    sc_host = _scales(n_rows, 50)
+    sc = _dev(sc_host)
+    plan = esopt.QPlan([q], [sc], [row], tensor_ids=[3])
+    last_full = (n // 65536) * 65536
+    idx = np.unique(np.concatenate([np.arange(0, 32), np.arange(last_full - 32, last_full + 32),
+                                    np.arange(n - 40, n),
+                                    np.random.default_rng(2).integers(0, n, 300)]).astype(np.int64))
+    idx_dev = torch.from_numpy(idx).cuda()
+    el = idx.astype(np.uint64)
+
+    def gather():
+        torch.cuda.synchronize()
+        return _host(q.index_select(0, idx_dev))
+    q0 = gather()
+    plan.perturb(21, 1, 1e-3)
+    q1 = gather()
+    plan.restore(21, 1, 1e-3)
+    q2 = gather()
+    r = np.array([0.9, 0.1, 0.4, 0.6], np.float32)
+    plan.update([7, 8, 9, 10], [1, 1, 1, 1], _dev(r), 2e-2, round_seed=5)
+    q3 = gather()
+    plan.close()
+    del q
+    torch.cuda.empty_cache()
+    v, ok, tol = _perturb_expect(sc_host, row, 21, 3, 1, 1e-3, el)
+    assert_qparity(qreport(q1, q0, v, tol, ok), "perturb at the limit")
+    assert_qparity(qreport(q2, q1, v, tol, ok, negate=True), "restore at the limit")
+    free = np.abs(q1.astype(np.int64)) < 127
+    np.testing.assert_array_equal(q2[free], q0[free])
+    v, ok, tol, live, st = _update_expect(sc_host, row, 3, [7, 8, 9, 10], [1] * 4, r, 2e-2, 0.0,
+                                          0, el, 5)
+    assert_qparity(qreport(q3, q2, v, tol, ok), "update at the limit")
