@@ -106,7 +106,7 @@ def _run(W, n_members=None, samples_per_tensor=256):
         assert_parity(agg, f"{W.name} {k}")
 
 
-@pytest.mark.parametrize("name", ["dense-0.5b", "dense-4b", "dense-27b"])
+@pytest.mark.parametrize("name", ["dense-0.5b", "dense-4b", "dense-27b", "dense-27b-77l"])
 def test_full_size_sampled_parity(name):
     _run(wl.WORKLOADS[name])
 
