@@ -18,7 +18,8 @@ rebuilds the parameters bit for bit (the paper reconstructs its final models
 from the recorded update sequence the same way, Appendix D.2 and D.4).
 """
 
-from dataclasses import dataclass, field
+import json
+from dataclasses import asdict, dataclass, fields
 from typing import Callable, List
 
 import torch
@@ -37,6 +38,36 @@ class GenerationRecord:
     zscore_eps: float = 1e-8
     fused_swap: bool = True
     round_seed: int = 0             # key of the update's stochastic rounding
+
+
+LOG_FORMAT = "es-generation-log/1"
+
+
+def save_log(path, records, meta=None):
+    """Write generation records as a JSON seed log: with the starting
+    parameters it is everything replay() needs (Appendix D.2 and D.4 rebuild
+    the final models the same way).  Rewards are binary32 values, which JSON
+    round-trips exactly as decimal doubles."""
+    doc = {"format": LOG_FORMAT, "meta": dict(meta or {}),
+           "generations": [asdict(r) for r in records]}
+    with open(path, "w") as fh:
+        json.dump(doc, fh, indent=1)
+
+
+def load_log(path):
+    """Read a seed log written by save_log; returns (records, meta)."""
+    with open(path) as fh:
+        doc = json.load(fh)
+    if doc.get("format") != LOG_FORMAT:
+        raise ValueError(f"{path}: not an {LOG_FORMAT} file")
+    names = {f.name for f in fields(GenerationRecord)}
+    recs = []
+    for g in doc["generations"]:
+        unknown = set(g) - names
+        if unknown:
+            raise ValueError(f"{path}: unknown record fields {sorted(unknown)}")
+        recs.append(GenerationRecord(**g))
+    return recs, doc["meta"]
 
 
 def sigma_schedule(sigma0, sigma_T, T):

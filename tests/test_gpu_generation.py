@@ -9,7 +9,7 @@ import torch
 import oracle
 from paper_2608_17310_amd import esopt, workloads as wl
 from paper_2608_17310_amd.generation import (run_generation, replay, sigma_schedule,
-                                             antithetic_seeds)
+                                             antithetic_seeds, save_log, load_log)
 from parity import to_device, to_host, report, assert_parity
 
 pytestmark = pytest.mark.gpu
@@ -83,7 +83,7 @@ def _fresh(W, stream_seed=0):
 
 @pytest.mark.parametrize("fused,flags", [(True, 0), (False, 0),
                                          (True, esopt.ES_UPDATE_STOCHASTIC_ROUND)])
-def test_generation_replay_is_bit_exact(fused, flags):
+def test_generation_replay_is_bit_exact(fused, flags, tmp_path):
     W = wl.TINY
     host, live = _fresh(W)
     plan = esopt.Plan(live)
@@ -99,6 +99,9 @@ def test_generation_replay_is_bit_exact(fused, flags):
     torch.cuda.synchronize()
     live_bits = [to_host(t) for t in live]
     plan.close()
+    # through the seed log on disk, as a run is rebuilt from its base checkpoint
+    save_log(tmp_path / "log.json", records, meta={"workload": W.name})
+    records, meta = load_log(tmp_path / "log.json")
     _, again = _fresh(W)
     plan2 = esopt.Plan(again)
     replay(plan2, records)
