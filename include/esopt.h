@@ -37,6 +37,13 @@
  *   - `stream` is a hipStream_t (NULL: the default stream).  Every call is
  *     stream-ordered and returns without synchronising the host; launch
  *     errors are reported by the return code.
+ *   - Every device pointer a call receives (tensors and scales at plan
+ *     creation, rewards / z / status arrays and hook outputs per call) is
+ *     checked with the runtime before any launch: it must be device or
+ *     managed memory of the current device with the whole range inside one
+ *     allocation, or mapped pinned host memory; otherwise the call fails
+ *     with ES_ERR_INVALID_ARG.  (A plan's tensors are checked once, when it
+ *     is created.)
  *   - Return value: ES_OK (0) or a negative ES_ERR_* code; es_strerror()
  *     names a code, es_last_error() gives the detail of the last failure on
  *     the calling thread.  A call that fails validation launches nothing and

@@ -924,6 +924,63 @@ int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_st
     return launch_qpass(p, kind, ps, static_cast<hipStream_t>(stream));
 }
 
+// The `bytes` bytes at p must be memory that kernels on `device` can access:
+// device or managed memory of that device, the whole range inside one
+// allocation (checked when the runtime knows the allocation's extent), or
+// mapped pinned host memory.  Catches host pointers, other devices' memory
+// and overstated sizes before a kernel would fault on them.  A failed query
+// leaves no error behind for later launch checks.
+int check_access(const void* p, uint64_t bytes, int device, const std::string& what) {
+    if (bytes == 0) return ES_OK;
+    hipPointerAttribute_t a{};
+    hipError_t e = hipPointerGetAttributes(&a, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ES_ERR_INVALID_ARG, what + ": not memory the device can access");
+    }
+    if (a.type == hipMemoryTypeHost) {
+        if (a.devicePointer == nullptr)
+            return fail(ES_ERR_INVALID_ARG, what + ": host memory not mapped for the device");
+        return ES_OK;
+    }
+    if (a.type != hipMemoryTypeDevice && a.type != hipMemoryTypeManaged &&
+        a.type != hipMemoryTypeUnified)
+        return fail(ES_ERR_INVALID_ARG, what + ": not device memory");
+    if (a.type == hipMemoryTypeDevice && a.device != device)
+        return fail(ES_ERR_INVALID_ARG, what + ": memory of device " + std::to_string(a.device) +
+                                            ", not of device " + std::to_string(device));
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    e = hipMemGetAddressRange(&base, &size, const_cast<void*>(p));
+    if (e != hipSuccess) {                   // allocator that does not report extents
+        (void)hipGetLastError();
+        return ES_OK;
+    }
+    const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+    if (q < b || q - b > size || bytes > size - (q - b))
+        return fail(ES_ERR_INVALID_ARG, what + ": " + std::to_string(bytes) +
+                                            " bytes extend past the end of its allocation");
+    return ES_OK;
+}
+
+int current_device(int* dev) {
+    const hipError_t e = hipGetDevice(dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    return ES_OK;
+}
+
+// The device arrays of an update call: rewards and z (n floats), status.
+int check_update_arrays(const char* name, int device, const float* rewards_dev, uint32_t n,
+                        const float* z_out_dev, const int32_t* status_out_dev) {
+    const std::string nm(name);
+    int rc = check_access(rewards_dev, uint64_t(4) * n, device, nm + ": rewards");
+    if (rc == ES_OK && z_out_dev != nullptr)
+        rc = check_access(z_out_dev, uint64_t(4) * n, device, nm + ": z output");
+    if (rc == ES_OK && status_out_dev != nullptr)
+        rc = check_access(status_out_dev, 4, device, nm + ": status output");
+    return rc;
+}
+
 // Argument checks shared by es_update and es_qupdate.
 int validate_update(const char* name, const uint64_t* seeds, const int32_t* signs,
                     const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts) {
@@ -1055,10 +1112,17 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
             return fail(ES_ERR_INVALID_ARG, "es_plan_create: tensors overlap in memory");
     tab[n_tensors] = DevTensor{nullptr, 0, n_full, n_tail, 0xFFFFFFFFu, 0u, 0u};   // sentinel
 
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc != ES_OK) return rc;
+    for (uint32_t i = 0; i < n_tensors && rc == ES_OK; ++i)
+        rc = check_access(tensors[i].data, 2 * tensors[i].numel, device,
+                          "es_plan_create: tensor " + std::to_string(i));
+    if (rc != ES_OK) return rc;
     es_plan_t* p = new (std::nothrow) es_plan_t;
     if (p == nullptr) return fail(ES_ERR_NOMEM, "es_plan_create: host allocation");
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    p->device = device;
+    hipError_t e = hipSuccess;
     int cus = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
@@ -1127,6 +1191,10 @@ int es_zscore(const float* rewards_dev, uint32_t n, float eps, float* z_dev, int
     if (n == 0 || n > ES_MAX_MEMBERS) return fail(ES_ERR_INVALID_ARG, "es_zscore: n out of range");
     if (!std::isfinite(eps) || eps < 0.0f)
         return fail(ES_ERR_INVALID_ARG, "es_zscore: eps must be finite and >= 0");
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc == ES_OK) rc = check_update_arrays("es_zscore", device, rewards_dev, n, z_dev, status_dev);
+    if (rc != ES_OK) return rc;
     hipLaunchKernelGGL(es_zscore_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(stream),
                        rewards_dev, n, static_cast<double>(eps), z_dev, status_dev);
     const hipError_t e = hipGetLastError();
@@ -1141,6 +1209,9 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
     int rc = validate_update("es_update", seeds, signs, rewards_dev, n_members, opts);
     if (rc != ES_OK) return rc;
     rc = check_device(plan);
+    if (rc == ES_OK)
+        rc = check_update_arrays("es_update", plan->device, rewards_dev, n_members, z_out_dev,
+                                 status_out_dev);
     if (rc != ES_OK) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     rc = prepare_update(plan->d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
@@ -1246,10 +1317,22 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
             return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
     tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu, 0u, 0u, 0u};
 
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc != ES_OK) return rc;
+    for (uint32_t i = 0; i < n_tensors && rc == ES_OK; ++i) {
+        const es_qtensor_t& t = tensors[i];
+        const std::string where = "es_qplan_create: tensor " + std::to_string(i);
+        const uint64_t n_scales = t.row == 0 ? 1 : (t.numel + t.row - 1) / t.row;
+        rc = check_access(t.data, t.numel, device, where + " codes");
+        if (rc == ES_OK && t.numel > 0)
+            rc = check_access(t.scales, 4 * n_scales, device, where + " scales");
+    }
+    if (rc != ES_OK) return rc;
     es_qplan_t* p = new (std::nothrow) es_qplan_t;
     if (p == nullptr) return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation");
-    hipError_t e = hipGetDevice(&p->device);
-    if (e != hipSuccess) { delete p; return hip_fail(e, "hipGetDevice"); }
+    p->device = device;
+    hipError_t e = hipSuccess;
     int cus = 0;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
     if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
@@ -1312,6 +1395,9 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
     int rc = validate_update("es_qupdate", seeds, signs, rewards_dev, n_members, opts);
     if (rc != ES_OK) return rc;
     rc = check_qdevice(plan);
+    if (rc == ES_OK)
+        rc = check_update_arrays("es_qupdate", plan->device, rewards_dev, n_members, z_out_dev,
+                                 status_out_dev);
     if (rc != ES_OK) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
     rc = prepare_update(plan->d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
@@ -1342,6 +1428,10 @@ int es_philox_words(uint64_t seed, uint32_t tensor_id, uint32_t domain, uint64_t
     if (reinterpret_cast<uintptr_t>(out_dev) % 16 != 0)
         return fail(ES_ERR_ALIGN, "es_philox_words: output not 16-byte aligned");
     if (n_quads == 0) return ES_OK;
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc == ES_OK) rc = check_access(out_dev, 16 * n_quads, device, "es_philox_words: output");
+    if (rc != ES_OK) return rc;
     const uint32_t blocks = static_cast<uint32_t>((n_quads + kAuxBlock - 1) / kAuxBlock);
     hipLaunchKernelGGL(es_philox_words_kernel, dim3(blocks), dim3(kAuxBlock), 0,
                        static_cast<hipStream_t>(stream), static_cast<uint32_t>(seed),
@@ -1358,6 +1448,10 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, fl
     if (n > (uint64_t(1) << 30)) return fail(ES_ERR_INVALID_ARG, "es_normals: n too large");
     if (elem0 > (uint64_t(1) << 62) - n) return fail(ES_ERR_INVALID_ARG, "es_normals: element range beyond 2^62");
     if (n == 0) return ES_OK;
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc == ES_OK) rc = check_access(out_dev, 4 * n, device, "es_normals: output");
+    if (rc != ES_OK) return rc;
     const uint64_t quads = ((elem0 + n - 1) >> 2) - (elem0 >> 2) + 1;
     const uint32_t blocks = static_cast<uint32_t>((quads + kAuxBlock - 1) / kAuxBlock);
     hipLaunchKernelGGL(es_normals_kernel, dim3(blocks), dim3(kAuxBlock), 0,

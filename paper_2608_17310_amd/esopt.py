@@ -125,10 +125,12 @@ def _stream(stream):
 
 
 def _dev_ptr(t, dtype, what):
+    """Pointer of a contiguous tensor the device can read: on the GPU, or in
+    pinned (page-locked, device-mapped) host memory."""
     if t is None:
         return None
-    if not t.is_cuda or t.dtype != dtype or not t.is_contiguous():
-        raise ValueError(f"{what} must be a contiguous {dtype} tensor on the GPU")
+    if not (t.is_cuda or t.is_pinned()) or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous {dtype} tensor on the GPU or pinned")
     return ctypes.c_void_p(t.data_ptr())
 
 
