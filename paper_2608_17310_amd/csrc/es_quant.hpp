@@ -181,11 +181,12 @@ __device__ __forceinline__ float spare_one_plus(uint32_t w) {
 }
 
 // Perturb / restore code: clamp(q +- floor(d + (2 r + 1) 2^-10), -127, 127)
-// with f = 1 + (2 r + 1) 2^-10: floor(d + f) - 1 (one rounding of d + f).
+// from v = d + f, f = 1 + (2 r + 1) 2^-10 (formed by the caller as one FMA):
+// floor(v) - 1.  v is capped at +-2^30 quanta, far beyond what any code can
+// absorb, so the integer arithmetic cannot overflow.
 template <bool kNegate>
-__device__ __forceinline__ int32_t qstep9(int32_t q, float d, float f) {
-    const float dc = __builtin_amdgcn_fmed3f(d, -0x1p30f, 0x1p30f);
-    const int32_t k = floor_to_int(dc + f) - 1;
+__device__ __forceinline__ int32_t qstep9(int32_t q, float v) {
+    const int32_t k = floor_to_int(__builtin_amdgcn_fmed3f(v, -0x1p30f, 0x1p30f)) - 1;
     const int32_t x = kNegate ? q - k : q + k;
     return min(max(x, -127), 127);
 }

@@ -667,30 +667,32 @@ struct QPass {
 };
 
 // Perturb / restore of one 16-code group: per quad of codes one noise call,
-// whose words give the four normals and the four rounding draws.
+// whose words give the four normals and the four rounding draws.  The scale's
+// reciprocal is folded into the pair's radius factor, and d + f is one FMA.
 template <bool kNegate>
 __device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e,
                                                uint32_t tensor_id, const Member& m, float inv0,
                                                float inv1, uint32_t out[4]) {
     const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, m.k0, m.k1);
-        const float inv = c < 2 ? inv0 : inv1;
+        const bool valid = (c < 2 ? inv0 : inv1) != 0.0f;
         const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
         uint32_t o = 0;
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
             float t, cs, sn;
-            es::scaled_pair(ws[2 * p], ws[2 * p + 1], m.w_k, t, cs, sn);
-            const float d[2] = {t * cs * inv, t * sn * inv};
+            es::scaled_pair(ws[2 * p], ws[2 * p + 1], wk_inv[c >> 1], t, cs, sn);
+            const float trig[2] = {cs, sn};
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int i = 2 * p + h;
                 const int32_t qc = static_cast<int8_t>(raw[c] >> (8 * i));
-                const int32_t v =
-                    inv != 0.0f ? esq::qstep9<kNegate>(qc, d[h], esq::spare_one_plus(ws[i])) : qc;
-                o |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+                const float v = __builtin_fmaf(t, trig[h], esq::spare_one_plus(ws[i]));
+                const int32_t code = valid ? esq::qstep9<kNegate>(qc, v) : qc;
+                o |= (static_cast<uint32_t>(code) & 0xFFu) << (8 * i);
             }
         }
         out[c] = o;
