@@ -218,3 +218,48 @@ def test_stochastic_rounding_identities():
     np.testing.assert_array_equal(out[0], bits)
     out, st, _ = _run_update([bits], [1, 2], [1, 1], [0.1, 0.5], 0.0, flags=SR, round_seed=3)
     np.testing.assert_array_equal(out[0], bits)
+
+
+def test_update_magnitudes_match_paper_table_on_gpu():
+    """The protocol of the paper's update-magnitude table (Appendix A.1): 70
+    updates at G = 8, alpha = 2.5e-4 with z-scored random rewards, starting
+    from theta = 0, run through the GPU path on 2^20 parameters; the fractions
+    of |delta theta| under each threshold match the printed table within 2.5
+    points and the closed form N(0, T alpha^2 / G) within sampling error, and
+    equal the oracle's on the same seeds."""
+    import math
+    import os
+    golden = os.path.join(os.path.dirname(__file__), "golden", "update_magnitude.txt")
+    lines = [l.split() for l in open(golden) if l.strip() and not l.startswith("#")]
+    meta = {k: float(v) for k, v in lines[:4]}
+    rows = [(float(a), float(b)) for a, b in lines[4:]]
+    T, G, alpha = int(meta["updates"]), int(meta["population"]), meta["alpha"]
+    n = 1 << 20
+    theta = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
+    plan = esopt.Plan([theta])
+    rng = np.random.default_rng(2024)
+    rs = []
+    for t in range(T):
+        r = rng.random(G).astype(np.float32)
+        rs.append(r)
+        plan.update([1000 * t + i for i in range(G)], [1] * G, _rewards_dev(r), alpha,
+                    sigma=meta["sigma"])
+    torch.cuda.synchronize()
+    got = to_host(theta)
+    plan.close()
+    d = np.abs(oracle.bf16_to_f64(got))
+    std = math.sqrt(T / G) * float(np.float32(alpha))
+    for thr, paper_frac in rows:
+        frac = float(np.mean(d <= thr))
+        closed = math.erf(thr / (std * math.sqrt(2)))
+        se = math.sqrt(closed * (1 - closed) / n)
+        print("threshold", thr, "gpu", frac, "closed form", closed, "paper", paper_frac)
+        assert abs(frac - closed) < 5 * se + 2e-3
+        assert abs(frac - paper_frac) < 0.025
+    # element for element, on a sample, the oracle's chain of the same updates
+    idx = np.random.default_rng(3).integers(0, n, 4096).astype(np.uint64)
+    x = np.zeros(idx.size, dtype=np.uint16)
+    for t, r in enumerate(rs):
+        x, st = oracle.update(x, 0, [1000 * t + i for i in range(G)], [1] * G, r, alpha,
+                              meta["sigma"], elems=idx)
+    assert np.mean(got[idx.astype(np.int64)] == x) > 0.999
