@@ -319,6 +319,8 @@ def run_int8(args):
         "scaling": "weak", "vs_baseline": None, "dtype": "f32", "param_dtype": "int8",
         "data": "synthetic",
         "config": {"workload": label, "params": P, "tensors": len(views), "members": N,
+                   "param_bytes": P + 4 * sum(int(x.numel()) for x in scales),
+                   "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
                    "scales": "one binary32 scale per row of the last dimension, one per vector",
                    "counting": "value = (2N+1) P / step time: 2N perturb/restore passes and one "
@@ -496,6 +498,7 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "param_dtype": "bf16", "data": "synthetic",
         "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
+                   "param_bytes": 2 * P, "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
                    "member_moves": "es_swap" if args.swap else "es_perturb/es_restore",
                    "update_rounding": "stochastic" if args.stochastic_round else "nearest-even",

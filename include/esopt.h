@@ -109,6 +109,11 @@ int es_plan_destroy(es_plan_t* plan);
 uint64_t es_plan_numel(const es_plan_t* plan);
 uint64_t es_plan_tiles(const es_plan_t* plan);
 
+/* Device memory a plan allocates for itself (its tensor table and member
+ * scratch), in bytes: everything the method needs beyond the parameters
+ * (Section 3: memory stays at inference level).  0 for NULL. */
+uint64_t es_plan_device_bytes(const es_plan_t* plan);
+
 /* Perturb in place (Section 3; Appendix D.6):
  *   theta_j <- RNE_bf16(theta_j + sign * sigma * eps_j(seed))
  * for every element of every tensor of the plan, one kernel launch.
@@ -220,6 +225,7 @@ typedef struct es_qplan es_qplan_t;
 int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out);
 int es_qplan_destroy(es_qplan_t* plan);
 uint64_t es_qplan_numel(const es_qplan_t* plan);
+uint64_t es_qplan_device_bytes(const es_qplan_t* plan);   /* as es_plan_device_bytes */
 
 /* Perturb (Section 3, in quanta): d_j = sign sigma eps_j(seed) / s_r with the
  * bf16 path's noise, k_j = floor(d_j + (2 r_j + 1) 2^-10) with r_j the top 9

@@ -1174,6 +1174,10 @@ int es_plan_destroy(es_plan_t* plan) {
 }
 
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
+
+uint64_t es_plan_device_bytes(const es_plan_t* plan) {
+    return plan ? sizeof(DevTensor) * (plan->n_tensors + 1) + kScratchBytes : 0;
+}
 uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_full + plan->n_tail : 0; }
 
 int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
@@ -1381,6 +1385,10 @@ int es_qplan_destroy(es_qplan_t* plan) {
 }
 
 uint64_t es_qplan_numel(const es_qplan_t* plan) { return plan ? plan->numel : 0; }
+
+uint64_t es_qplan_device_bytes(const es_qplan_t* plan) {
+    return plan ? sizeof(esq::DevQTensor) * (plan->n_tensors + 1) + kScratchBytes : 0;
+}
 
 int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
     return qperturb_impl(plan, seed, sign, sigma, stream, QKind::kPerturb, "es_qperturb");

@@ -56,6 +56,7 @@ SIGNATURES = {
     "es_plan_destroy": (ctypes.c_int, [_vp]),
     "es_plan_numel": (_u64, [_vp]),
     "es_plan_tiles": (_u64, [_vp]),
+    "es_plan_device_bytes": (_u64, [_vp]),
     "es_perturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_restore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_swap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
@@ -66,6 +67,7 @@ SIGNATURES = {
     "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
+    "es_qplan_device_bytes": (_u64, [_vp]),
     "es_qperturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_qrestore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_qupdate": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
@@ -176,6 +178,11 @@ class Plan:
         return int(load().es_plan_tiles(self.handle))
 
     @property
+    def device_bytes(self):
+        """Device memory the plan allocates for itself (table and scratch)."""
+        return int(load().es_plan_device_bytes(self.handle))
+
+    @property
     def tensors(self):
         return list(self._tensors)
 
@@ -284,6 +291,11 @@ class QPlan:
     @property
     def numel(self):
         return int(load().es_qplan_numel(self.handle))
+
+    @property
+    def device_bytes(self):
+        """Device memory the plan allocates for itself (table and scratch)."""
+        return int(load().es_qplan_device_bytes(self.handle))
 
     def perturb(self, seed, sign, sigma, stream=None):
         _check(load().es_qperturb(self.handle, int(seed), int(sign), float(sigma),

@@ -50,6 +50,9 @@ def test_plans_and_passes_allocate_no_parameter_sized_memory():
     qplan = esopt.QPlan(codes, scales, [4096, 4096])
     f1 = _free()
     print("plans took", (f0 - f1) / MB, "MiB")
+    # what the plans report: a table entry per tensor plus the member scratch
+    assert plan.device_bytes < 64 * 1024 and qplan.device_bytes < 64 * 1024
+    assert qplan.device_bytes - plan.device_bytes == 64 * (len(codes) + 1) - 48 * (len(params) + 1)
     assert f0 - f1 <= 8 * MB                      # tables + scratch, allocation granularity
     seen = []
     for rep in range(3):
