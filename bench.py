@@ -608,7 +608,7 @@ def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload, int8=False):
         lines = [
             f"# {kind} on {label} ({P:,} {dtype} parameters)",
             "",
-            "Commands (run from the repository root on the GPU box, `cd /tmp && export TMPDIR=/tmp` first; "
+            "Commands (run from the repository root on an MI355X machine, `cd /tmp && export TMPDIR=/tmp` first; "
             "`<out>` is an output directory):",
             "",
         ] + [f"* `{c}`" for c in commands] + [
