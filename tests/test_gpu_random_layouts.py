@@ -1,0 +1,174 @@
+"""Randomised plan layouts against the oracle: many tensors of random sizes
+(empty to a few hundred thousand elements) at random 2-byte offsets inside
+shared buffers, random tensor ids, random tile shapes (environment
+overrides); every element of every tensor is checked after perturb, swap,
+restore and both update roundings.  Seeded, so every case is reproducible."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_17310_amd import esopt, workloads as wl
+from parity import to_host, report, assert_parity, perturb_delta, update_delta
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = [(256, 4), (256, 8), (512, 4), (512, 8), (1024, 4), (1024, 8)]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_layout(case, monkeypatch):
+    rng = np.random.default_rng(1000 + case)
+    threads, groups = SHAPES[rng.integers(len(SHAPES))]
+    monkeypatch.setenv("ESOPT_THREADS", str(threads))
+    monkeypatch.setenv("ESOPT_GROUPS", str(groups))
+    monkeypatch.setenv("ESOPT_PERTURB_WG_PER_CU", str(int(rng.integers(1, 4))))
+    monkeypatch.setenv("ESOPT_UPDATE_WG_PER_CU", str(int(rng.integers(1, 9))))
+    n_t = int(rng.integers(1, 25))
+    sizes = [int(x) for x in np.where(rng.random(n_t) < 0.15, rng.integers(0, 20, n_t),
+                                      rng.integers(1, 300_000, n_t))]
+    offsets = [int(x) for x in rng.integers(0, 9, n_t)]      # elements: 0 .. 16 bytes
+    ids = [int(x) for x in rng.choice(1 << 20, n_t, replace=False)]
+    print("case", case, "shape", threads, groups, "tensors", list(zip(sizes, offsets)))
+    host = [wl.random_bf16_bits(n, 7000 + 31 * case + i) for i, n in enumerate(sizes)]
+    # all tensors in one device buffer, each at its offset past a 16-byte boundary
+    starts, cur = [], 0
+    for n, off in zip(sizes, offsets):
+        cur = (cur + 7) // 8 * 8 + off
+        starts.append(cur)
+        cur += n
+    buf = torch.zeros(cur + 8, dtype=torch.bfloat16, device="cuda")
+    flat = np.zeros(cur + 8, dtype=np.uint16)
+    for s, h in zip(starts, host):
+        flat[s:s + h.size] = h
+    buf.copy_(torch.from_numpy(flat.view(np.int16)).view(torch.bfloat16))
+    views = [buf[s:s + n] for s, n in zip(starts, sizes)]
+    plan = esopt.Plan(views, tensor_ids=ids)
+    seeds = [int(x) for x in rng.integers(0, 1 << 62, 4)]
+    signs = [1, -1, 1, 1]
+    r = rng.random(4).astype(np.float32)
+    sigma, alpha = 1e-3, 5e-4
+    stages = []
+
+    def snap():
+        torch.cuda.synchronize()
+        return [to_host(v) for v in views]
+    x0 = snap()
+    plan.perturb(seeds[0], 1, sigma)
+    x1 = snap()
+    plan.swap(seeds[0], 1, seeds[1], -1, sigma)
+    x2 = snap()
+    plan.restore(seeds[1], -1, sigma)
+    x3 = snap()
+    plan.update(seeds, signs, torch.from_numpy(r).cuda(), alpha)
+    x4 = snap()
+    plan.update(seeds, signs, torch.from_numpy(r).cuda(), alpha,
+                flags=esopt.ES_UPDATE_STOCHASTIC_ROUND, round_seed=case)
+    x5 = snap()
+    plan.close()
+    # bytes outside the tensors are untouched
+    full = to_host(buf)
+    mask = np.ones(full.size, bool)
+    for s, n in zip(starts, sizes):
+        mask[s:s + n] = False
+    assert np.all(full[mask] == flat[mask])
+    for i, (tid, n) in enumerate(zip(ids, sizes)):
+        if n == 0:
+            continue
+        el = np.arange(n, dtype=np.uint64)
+        checks = [
+            (x1[i], oracle.perturb(x0[i], seeds[0], tid, 1, sigma), x0[i],
+             perturb_delta(seeds[0], tid, 1, sigma, el)),
+            (x2[i], oracle.swap(x1[i], tid, seeds[0], 1, sigma, seeds[1], -1, sigma), x1[i],
+             perturb_delta(seeds[0], tid, -1, sigma, el) + perturb_delta(seeds[1], tid, -1, sigma, el)),
+            (x3[i], oracle.restore(x2[i], seeds[1], tid, -1, sigma), x2[i],
+             perturb_delta(seeds[1], tid, 1, sigma, el)),
+            (x4[i], oracle.update(x3[i], tid, seeds, signs, r, alpha, sigma)[0], x3[i],
+             update_delta(tid, seeds, signs, r, alpha, sigma, 0, el)),
+            (x5[i], oracle.update(x4[i], tid, seeds, signs, r, alpha, sigma,
+                                  flags=esopt.ES_UPDATE_STOCHASTIC_ROUND, round_seed=case)[0],
+             x4[i], update_delta(tid, seeds, signs, r, alpha, sigma, 0, el)),
+        ]
+        for k, (got, exp, base, delta) in enumerate(checks):
+            rep = report(got, exp, base, delta)
+            assert rep["max_ulp"] <= 2.0 and rep["le1"] >= 0.999, (case, i, n, k, rep)
+            assert rep["exact"] >= (0.99 if n < 1000 else 0.999), (case, i, n, k, rep)
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_random_int8_layout(case, monkeypatch):
+    from parity import q_tolerance, qreport, assert_qparity
+    rng = np.random.default_rng(2000 + case)
+    threads, groups = SHAPES[rng.integers(len(SHAPES))]
+    monkeypatch.setenv("ESOPT_THREADS", str(threads))
+    monkeypatch.setenv("ESOPT_QGROUPS", str(groups))
+    monkeypatch.setenv("ESOPT_UPDATE_WG_PER_CU", str(int(rng.integers(1, 9))))
+    n_t = int(rng.integers(1, 16))
+    sizes = [int(x) for x in rng.integers(1, 400_000, n_t)]
+    rows = [int(rng.choice([0, 8, 24, 64, 1024, 5120])) for _ in range(n_t)]
+    offsets = [int(x) for x in rng.integers(0, 17, n_t)]     # bytes
+    ids = [int(x) for x in rng.choice(1 << 20, n_t, replace=False)]
+    print("case", case, "shape", threads, groups, list(zip(sizes, rows, offsets)))
+    codes = [rng.integers(-127, 128, n).astype(np.int8) for n in sizes]
+    scales = [rng.uniform(2e-4, 1e-3, 1 if r == 0 else -(-n // r)).astype(np.float32)
+              for n, r in zip(sizes, rows)]
+    for sc in scales:
+        if sc.size > 4:
+            sc[int(rng.integers(sc.size))] = 0.0                 # an invalid row
+    starts, cur = [], 0
+    for n, off in zip(sizes, offsets):
+        cur = (cur + 15) // 16 * 16 + off
+        starts.append(cur)
+        cur += n
+    flat = np.zeros(cur + 16, np.int8)
+    for s, c in zip(starts, codes):
+        flat[s:s + c.size] = c
+    buf = torch.from_numpy(flat).cuda()
+    views = [buf[s:s + n] for s, n in zip(starts, sizes)]
+    sdev = [torch.from_numpy(sc).cuda() for sc in scales]
+    plan = esopt.QPlan(views, sdev, rows, tensor_ids=ids)
+    seeds = [int(x) for x in rng.integers(0, 1 << 62, 3)]
+    r = rng.random(3).astype(np.float32)
+
+    def snap():
+        torch.cuda.synchronize()
+        return [v.cpu().numpy().copy() for v in views]
+    q0 = snap()
+    plan.perturb(seeds[0], -1, 1e-3)
+    q1 = snap()
+    plan.restore(seeds[0], -1, 1e-3)
+    q2 = snap()
+    plan.update(seeds, [1, 1, 1], torch.from_numpy(r).cuda(), 5e-3, round_seed=case)
+    q3 = snap()
+    plan.close()
+    full = buf.cpu().numpy()
+    mask = np.ones(full.size, bool)
+    for s, n in zip(starts, sizes):
+        mask[s:s + n] = False
+    assert np.all(full[mask] == flat[mask])
+    for i, (tid, n, row, sc) in enumerate(zip(ids, sizes, rows, scales)):
+        el = np.arange(n, dtype=np.uint64)
+        d, rr, ok = oracle.offset_values(sc, row, seeds[0], tid, -1, 1e-3, el)
+        s = np.where(ok, oracle.row_scales(sc, row, el), 1.0)
+        eps = oracle.normals(seeds[0], tid, el)
+        tol = q_tolerance(float(np.float32(1e-3)) / s, np.abs(float(np.float32(1e-3)) * eps) / s, d)
+        v = d + (2 * rr + 1) * 2.0 ** -10
+        assert_qparity(qreport(q1[i], q0[i], v, tol, ok), f"case {case} tensor {i} perturb")
+        assert_qparity(qreport(q2[i], q1[i], v, tol, ok, negate=True), f"case {case} tensor {i} restore")
+        d, rr, ok, live, st = oracle.update_values(sc, row, tid, seeds, [1, 1, 1], r, 5e-3, 0.0,
+                                                   elems=el, round_seed=case)
+        wsum = np.zeros(n)
+        nsum = np.zeros(n)
+        for sd, w in live:
+            wsum += abs(w) / s
+            nsum += np.abs(w * oracle.normals(sd, tid, el)) / s
+        v = d + rr * 2.0 ** -16
+        assert_qparity(qreport(q3[i], q2[i], v, q_tolerance(wsum, nsum, d), ok),
+                       f"case {case} tensor {i} update")
