@@ -36,7 +36,11 @@
  *     externally synchronised) because they share the plan's small scratch.
  *   - `stream` is a hipStream_t (NULL: the default stream).  Every call is
  *     stream-ordered and returns without synchronising the host; launch
- *     errors are reported by the return code.
+ *     errors are reported by the return code.  The passes (perturb, restore,
+ *     swap, update, z-score and their int8 counterparts) only launch kernels
+ *     on `stream` -- no memset, no host synchronisation, host arrays copied
+ *     into kernel arguments -- so they can be captured into a HIP graph; a
+ *     replay repeats the captured arguments (seeds, signs, sigma, alpha).
  *   - Every device pointer a call receives (tensors and scales at plan
  *     creation, rewards / z / status arrays and hook outputs per call) is
  *     checked with the runtime before any launch: it must be device or
