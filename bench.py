@@ -115,7 +115,7 @@ def cpu_baseline(W, seeds, signs, rewards, sigma, theta_samples, workers, budget
                       f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
 
 
-def host_samples(W, per_tensor=1 << 14):
+def host_samples(W, per_tensor=1 << 16):
     """A bounded element sample of every tensor of W: random element indices
     and N(0, 0.02) bf16 values drawn on the host (the oracle's cost does not
     depend on the values)."""
@@ -141,7 +141,7 @@ def _oracle_qchunk(args):
     return time.perf_counter() - t0
 
 
-def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_tensor=1 << 12):
+def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_tensor=1 << 14):
     """The oracle's int8 step on a bounded sample: random codes and indices,
     per-row scales of the workload's shapes (values do not change the cost)."""
     from paper_2608_17310_amd import workloads as wl
