@@ -29,6 +29,7 @@
 #include <cstdint>
 
 #include "es_noise.hpp"
+#include "es_table.hpp"
 
 namespace esq {
 
@@ -51,7 +52,8 @@ struct DevQTensor {
     uint32_t tensor_id;
     uint32_t magic;
     uint32_t shift;
-    uint64_t pad;
+    uint32_t n_tensors;                         // entries before the sentinel (same in all)
+    uint32_t aligned16;                         // base 16-byte aligned: vector tail groups
 };
 static_assert(sizeof(DevQTensor) == 64, "quantized tensor table entry layout");
 
@@ -64,35 +66,40 @@ struct QTileRef {
     uint32_t tensor_id;
     uint32_t magic;
     uint32_t shift;
+    uint32_t aligned16;
 };
 
 template <uint32_t kTileElems>
 __device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ tab, uint32_t& t,
                                                  uint64_t tile) {
-    while (tile >= tab[t + 1].first_full) ++t;
+    t = es::seek_tensor(t, tile, tab[0].n_tensors,
+                        [tab](uint32_t i) { return tab[i].first_full; });
     return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
                     static_cast<uint32_t>((tile - tab[t].first_full) * kTileElems), tab[t].row,
-                    tab[t].tensor_id, tab[t].magic, tab[t].shift};
+                    tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
 }
 
 template <uint32_t kTileElems>
 __device__ __forceinline__ QTileRef qlocate_tail(const DevQTensor* __restrict__ tab, uint32_t& t,
                                                  uint64_t tile) {
-    while (tile >= tab[t + 1].first_tail) ++t;
+    t = es::seek_tensor(t, tile, tab[0].n_tensors,
+                        [tab](uint32_t i) { return tab[i].first_tail; });
     const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
     return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
                     static_cast<uint32_t>((n_full + tile - tab[t].first_tail) * kTileElems),
-                    tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift};
+                    tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
 }
 
 typedef uint32_t q32x4_t __attribute__((ext_vector_type(4)));
 #define ESQ_GLOBAL __attribute__((address_space(1)))
 
-// 16 codes of one group in 4 words (byte i of word k is code 4k + i).
+// 16 codes of one group in 4 words (byte i of word k is code 4k + i).  The
+// checked path (tail tiles) uses the 16-byte access too when the tensor is
+// 16-byte aligned and the whole group is inside it.
 template <bool kFast>
 __device__ __forceinline__ void qload(const int8_t* __restrict__ p, uint32_t e, uint32_t numel,
-                                      uint32_t raw[4]) {
-    if constexpr (kFast) {
+                                      uint32_t raw[4], bool vec = false) {
+    if (kFast || (vec && e + 16 <= numel)) {
         const q32x4_t v = __builtin_nontemporal_load((const ESQ_GLOBAL q32x4_t*)(p + e));
         raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
     } else {
@@ -112,8 +119,8 @@ __device__ __forceinline__ void qload(const int8_t* __restrict__ p, uint32_t e, 
 
 template <bool kFast>
 __device__ __forceinline__ void qstore(int8_t* __restrict__ p, uint32_t e, uint32_t numel,
-                                       const uint32_t out[4]) {
-    if constexpr (kFast) {
+                                       const uint32_t out[4], bool vec = false) {
+    if (kFast || (vec && e + 16 <= numel)) {
         const q32x4_t v = {out[0], out[1], out[2], out[3]};
         __builtin_nontemporal_store(v, (ESQ_GLOBAL q32x4_t*)(p + e));
     } else {

@@ -58,6 +58,7 @@
 #include "../../include/esopt.h"
 #include "es_noise.hpp"
 #include "es_quant.hpp"
+#include "es_table.hpp"
 
 namespace {
 
@@ -83,8 +84,9 @@ struct DevTensor {
     uint64_t first_full;                    // global index of the tensor's first full tile
     uint64_t first_tail;                    // global index of its first tail tile
     uint32_t tensor_id;
-    uint32_t pad0;
-    uint64_t pad1;
+    uint32_t n_tensors;                     // entries before the sentinel (same in all)
+    uint32_t aligned16;                     // base 16-byte aligned: vector tail groups
+    uint32_t pad;
 };
 static_assert(sizeof(DevTensor) == 48, "tensor table entry layout");
 
@@ -144,11 +146,13 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 // Load the 8 bf16 of one group (packed in 4 words).  Fast path: one 16-byte
 // load (nontemporal when kNT: the parameters are streamed once per pass).
-// Checked path: element-wise 2-byte loads with bounds.
+// Checked path (tail tiles): the 16-byte load when the tensor is 16-byte
+// aligned and the whole group is inside it, element-wise 2-byte loads with
+// bounds otherwise.
 template <bool kFast, bool kNT>
 __device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint64_t e,
-                                           uint64_t numel, uint32_t raw[4]) {
-    if constexpr (kFast) {
+                                           uint64_t numel, uint32_t raw[4], bool vec = false) {
+    if (kFast || (vec && e + 8 <= numel)) {
         const ES_GLOBAL u32x4_t* a = (const ES_GLOBAL u32x4_t*)(p + e);
         const u32x4_t v = kNT ? __builtin_nontemporal_load(a) : *a;
         raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
@@ -165,8 +169,8 @@ __device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint6
 
 template <bool kFast, bool kNT>
 __device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e, uint64_t numel,
-                                            const uint32_t out[4]) {
-    if constexpr (kFast) {
+                                            const uint32_t out[4], bool vec = false) {
+    if (kFast || (vec && e + 8 <= numel)) {
         ES_GLOBAL u32x4_t* a = (ES_GLOBAL u32x4_t*)(p + e);
         const u32x4_t v = {out[0], out[1], out[2], out[3]};
         if constexpr (kNT) __builtin_nontemporal_store(v, a);
@@ -277,6 +281,7 @@ struct TileRef {
     uint64_t numel;
     uint64_t elem0;
     uint32_t tensor_id;
+    uint32_t aligned16;
 };
 
 // Tile lookup.  A workgroup's tiles increase monotonically, so its table
@@ -285,18 +290,20 @@ struct TileRef {
 template <uint64_t kTileElems>
 __device__ __forceinline__ TileRef locate_full(const DevTensor* __restrict__ tab, uint32_t& t,
                                                uint64_t tile) {
-    while (tile >= tab[t + 1].first_full) ++t;
+    t = es::seek_tensor(t, tile, tab[0].n_tensors,
+                        [tab](uint32_t i) { return tab[i].first_full; });
     return TileRef{tab[t].data, tab[t].numel, (tile - tab[t].first_full) * kTileElems,
-                   tab[t].tensor_id};
+                   tab[t].tensor_id, tab[t].aligned16};
 }
 
 template <uint64_t kTileElems>
 __device__ __forceinline__ TileRef locate_tail(const DevTensor* __restrict__ tab, uint32_t& t,
                                                uint64_t tile) {
-    while (tile >= tab[t + 1].first_tail) ++t;
+    t = es::seek_tensor(t, tile, tab[0].n_tensors,
+                        [tab](uint32_t i) { return tab[i].first_tail; });
     const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
     return TileRef{tab[t].data, tab[t].numel, (n_full + tile - tab[t].first_tail) * kTileElems,
-                   tab[t].tensor_id};
+                   tab[t].tensor_id, tab[t].aligned16};
 }
 
 template <int kThreads, int kU>
@@ -342,9 +349,9 @@ __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
         if (e >= r.numel) break;
         uint32_t raw[4], out[4];
-        load_group<false, true>(r.data, e, r.numel, raw);
+        load_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
         perturb_group<kM>(raw, e, q_hi, r.tensor_id, st, out);
-        store_group<false, true>(r.data, e, r.numel, out);
+        store_group<false, true>(r.data, e, r.numel, out, r.aligned16 != 0u);
     }
 }
 
@@ -426,7 +433,7 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
             for (int k = 0; k < 4; ++k) raw[k] = next[k];
             if (u + 1 < kU) load_group<true, kNT>(r.data, e + uint64_t(kThreads) * kGroupElems, r.numel, next);
         } else {
-            load_group<false, kNT>(r.data, e, r.numel, raw);
+            load_group<false, kNT>(r.data, e, r.numel, raw, r.aligned16 != 0u);
         }
         const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
         float acc[8];
@@ -454,7 +461,7 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
                 out[k] = es::pack_bf16x2(es::bf16_lo(raw[k]) + acc[2 * k],
                                          es::bf16_hi(raw[k]) + acc[2 * k + 1]);
         }
-        store_group<kFast, kNT>(r.data, e, r.numel, out);
+        store_group<kFast, kNT>(r.data, e, r.numel, out, r.aligned16 != 0u);
     }
 }
 
@@ -711,7 +718,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
         const uint32_t e = e0 + uint32_t(u) * kThreads * esq::kQGroup;
         if (!kFast && e >= r.numel) break;
         uint32_t raw[4];
-        esq::qload<kFast>(r.data, e, r.numel, raw);
+        esq::qload<kFast>(r.data, e, r.numel, raw, r.aligned16 != 0u);
         float inv0, inv1;
         esq::group_inv_scales(r, e, inv0, inv1);
         uint32_t out[4];
@@ -746,7 +753,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
                 out[k] = w;
             }
         }
-        esq::qstore<kFast>(r.data, e, r.numel, out);
+        esq::qstore<kFast>(r.data, e, r.numel, out, r.aligned16 != 0u);
     }
 }
 
@@ -1102,7 +1109,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
         const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
         tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, n_full, n_tail, t.tensor_id,
-                           0u, 0u};
+                           n_tensors, (a % 16 == 0) ? 1u : 0u, 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
         n_full += full;
         n_tail += tail;
@@ -1112,7 +1119,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_plan_create: tensors overlap in memory");
-    tab[n_tensors] = DevTensor{nullptr, 0, n_full, n_tail, 0xFFFFFFFFu, 0u, 0u};   // sentinel
+    tab[n_tensors] = DevTensor{nullptr, 0, n_full, n_tail, 0xFFFFFFFFu, n_tensors, 0u, 0u};   // sentinel
 
     int device = -1;
     int rc = current_device(&device);
@@ -1311,7 +1318,8 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
             shift = l - 1;
         }
         tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales, t.numel, n_full, n_tail,
-                                 t.row, t.tensor_id, magic, shift, 0u};
+                                 t.row, t.tensor_id, magic, shift, n_tensors,
+                                 (a % 16 == 0) ? 1u : 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
         n_full += full;
         n_tail += tail;
@@ -1321,7 +1329,8 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
-    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu, 0u, 0u, 0u};
+    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu, 0u, 0u,
+                                     n_tensors, 0u};
 
     int device = -1;
     int rc = current_device(&device);

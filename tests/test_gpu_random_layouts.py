@@ -172,3 +172,75 @@ def test_random_int8_layout(case, monkeypatch):
         v = d + rr * 2.0 ** -16
         assert_qparity(qreport(q3[i], q2[i], v, q_tolerance(wsum, nsum, d), ok),
                        f"case {case} tensor {i} update")
+
+
+def test_many_tiny_tensors():
+    """20 000 tensors of 1-200 elements at random 2-byte offsets (a tile per
+    tensor, most of them tails): the galloping tile-to-tensor lookup; 400
+    tensors checked element by element after perturb and update, and every
+    byte between tensors untouched."""
+    rng = np.random.default_rng(77)
+    n_t = 20000
+    sizes = rng.integers(1, 201, n_t)
+    offsets = rng.integers(0, 9, n_t)
+    starts, cur = [], 0
+    for n, off in zip(sizes, offsets):
+        cur = (cur + 7) // 8 * 8 + int(off)
+        starts.append(cur)
+        cur += int(n)
+    flat = wl.random_bf16_bits(cur + 8, 78)
+    buf = torch.from_numpy(flat.view(np.int16)).view(torch.bfloat16).cuda()
+    views = [buf[s:s + int(n)] for s, n in zip(starts, sizes)]
+    plan = esopt.Plan(views)
+    r = rng.random(5).astype(np.float32)
+    plan.perturb(9, -1, 1e-3)
+    torch.cuda.synchronize()
+    mid = to_host(buf)
+    plan.update([1, 2, 3, 4, 5], [1] * 5, torch.from_numpy(r).cuda(), 5e-4)
+    torch.cuda.synchronize()
+    out = to_host(buf)
+    plan.close()
+    mask = np.ones(flat.size, bool)
+    for s, n in zip(starts, sizes):
+        mask[s:s + int(n)] = False
+    assert np.all(out[mask] == flat[mask])
+    for i in rng.choice(n_t, 400, replace=False):
+        s, n = starts[i], int(sizes[i])
+        el = np.arange(n, dtype=np.uint64)
+        rep = report(mid[s:s + n], oracle.perturb(flat[s:s + n], 9, int(i), -1, 1e-3), flat[s:s + n],
+                     perturb_delta(9, int(i), -1, 1e-3, el))
+        assert rep["max_ulp"] <= 1.0, (i, rep)
+        exp, _ = oracle.update(mid[s:s + n], int(i), [1, 2, 3, 4, 5], [1] * 5, r, 5e-4, 1e-3)
+        rep = report(out[s:s + n], exp, mid[s:s + n],
+                     update_delta(int(i), [1, 2, 3, 4, 5], [1] * 5, r, 5e-4, 1e-3, 0, el))
+        assert rep["max_ulp"] <= 1.0, (i, rep)
+
+
+def test_many_tiny_int8_tensors():
+    from parity import q_tolerance, qreport, assert_qparity
+    rng = np.random.default_rng(79)
+    n_t = 20000
+    sizes = rng.integers(1, 300, n_t)
+    starts, cur = [], 0
+    for n in sizes:
+        cur = (cur + 15) // 16 * 16 + int(rng.integers(0, 17))
+        starts.append(cur)
+        cur += int(n)
+    flat = rng.integers(-127, 128, cur + 16).astype(np.int8)
+    buf = torch.from_numpy(flat).cuda()
+    sc = torch.full((1,), 6e-4, device="cuda")
+    views = [buf[s:s + int(n)] for s, n in zip(starts, sizes)]
+    plan = esopt.QPlan(views, [sc] * n_t, [0] * n_t)
+    plan.perturb(4, 1, 1e-3)
+    torch.cuda.synchronize()
+    out = buf.cpu().numpy()
+    plan.close()
+    for i in rng.choice(n_t, 300, replace=False):
+        s, n = starts[i], int(sizes[i])
+        el = np.arange(n, dtype=np.uint64)
+        d, rr, ok = oracle.offset_values([6e-4], 0, 4, int(i), 1, 1e-3, el)
+        eps = oracle.normals(4, int(i), el)
+        s32 = float(np.float32(1e-3)) / float(np.float32(6e-4))
+        tol = q_tolerance(np.full(n, s32), np.abs(s32 * eps), d)
+        assert_qparity(qreport(out[s:s + n], flat[s:s + n], d + (2 * rr + 1) * 2.0 ** -10, tol, ok),
+                       f"tiny int8 tensor {i}")
