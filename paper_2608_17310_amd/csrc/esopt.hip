@@ -359,6 +359,12 @@ __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st
 // workgroup's next tile into `next_buf`, then perturb the current tile from
 // `cur_buf`, so the memory pipe does not idle through the Philox /
 // Box-Muller arithmetic.  Returns true when the workgroup has no next tile.
+//
+// The loads are issued on every step, the last one reloading its own tile
+// into the idle buffer (128 KB per workgroup per pass, never used): the
+// compiler's wait before the current tile's arithmetic is path-insensitive,
+// and a path without loads after the current tile's made it wait for the
+// next tile's loads as well.
 template <int kThreads, int kU, int kM>
 __device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, uint32_t& t,
                                              uint64_t& tile, uint64_t n_full, TileRef& cur,
@@ -368,10 +374,10 @@ __device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, 
     const uint64_t next = tile + gridDim.x;
     const bool more = next < n_full;
     TileRef nxt = cur;
-    if (more) {
-        nxt = locate_full<kTileElems>(tab, t, next);
-        load_tile<kThreads, kU>(nxt, next_buf);
-    }
+    if (more) nxt = locate_full<kTileElems>(tab, t, next);
+    __builtin_amdgcn_sched_barrier(0);
+    load_tile<kThreads, kU>(nxt, next_buf);
+    __builtin_amdgcn_sched_barrier(0);
     perturb_loaded<kThreads, kU, kM>(cur, cur_buf, st);
     if (!more) return true;
     tile = next;
@@ -381,7 +387,10 @@ __device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, 
 
 // One pass over the whole parameter list applying kM noise streams: full
 // tiles first (16-byte nontemporal accesses, software-pipelined: two register
-// buffers alternate, the loop unrolled twice), then tail tiles.
+// buffers alternate, the loop unrolled twice), then tail tiles.  The first
+// step is peeled off so that every step inside the loop starts with the same
+// memory operations outstanding (the previous tile's stores, then the next
+// tile's loads): the wait for the current tile then leaves both in flight.
 template <int kThreads, int kU, int kM>
 __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* __restrict__ tab,
                                                               uint64_t n_full, uint64_t n_tail,
@@ -393,9 +402,11 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
         TileRef cur = locate_full<kTileElems>(tab, t, tile);
         uint32_t a[kU][4], b[kU][4];
         load_tile<kThreads, kU>(cur, a);
-        for (;;) {
-            if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) break;
-            if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, b, a, st)) break;
+        if (!perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) {
+            for (;;) {
+                if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, b, a, st)) break;
+                if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) break;
+            }
         }
     }
     uint32_t t = 0;
