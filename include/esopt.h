@@ -105,8 +105,10 @@ typedef struct es_plan es_plan_t;
  * 48 * (n_tensors + 1) bytes and ~42 KB of scratch, freed by es_plan_destroy. */
 int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out);
 
-/* Free a plan (NULL is a no-op).  Synchronises the device first so that no
- * queued launch still reads the plan's tables. */
+/* Free a plan (NULL is a no-op).  Synchronises the plan's device first (made
+ * current for the call; the caller's current device is restored) so that no
+ * queued launch still reads the plan's tables.  The plan is freed even when a
+ * step fails; the first failure is returned. */
 int es_plan_destroy(es_plan_t* plan);
 
 /* Total number of bf16 elements and number of tiles of a plan. */

@@ -130,8 +130,8 @@ int fail(int code, const std::string& msg) {
     return code;
 }
 
-int hip_fail(hipError_t e, const char* what) {
-    return fail(ES_ERR_HIP, std::string(what) + ": " + hipGetErrorString(e));
+int hip_fail(hipError_t e, const std::string& what) {
+    return fail(ES_ERR_HIP, what + ": " + hipGetErrorString(e));
 }
 
 // ------------------------------------------------------------------------
@@ -868,8 +868,6 @@ int check_device(const es_plan_t* p) {
     return ES_OK;
 }
 
-// One perturb-style pass applying `members` (1 or 2) noise streams with
-// coefficients coef[m] (sign sigma), nothing skipped.
 // One pass of the perturb kernel: streams = 0 (no noise), 1 (seed[0],
 // coef[0]), 2 (two keys) or 3 (both coefficients on seed[0]).
 int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double* coef,
@@ -981,6 +979,34 @@ int check_access(const void* p, uint64_t bytes, int device, const std::string& w
         return fail(ES_ERR_INVALID_ARG, what + ": " + std::to_string(bytes) +
                                             " bytes extend past the end of its allocation");
     return ES_OK;
+}
+
+// Free a plan's table and scratch on the plan's device: that device is made
+// current for the call (the caller's is restored) and synchronised first, so
+// no queued launch still reads them.  Every step runs; the first error is
+// returned.
+int release_device_memory(int device, void* tab, void* scratch, const char* name) {
+    const std::string nm(name);
+    int rc = ES_OK;
+    int caller = -1;
+    hipError_t e = hipGetDevice(&caller);
+    if (e != hipSuccess) rc = hip_fail(e, nm + ": hipGetDevice");
+    const bool switched = e == hipSuccess && caller != device;
+    if (switched) {
+        e = hipSetDevice(device);
+        if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, nm + ": hipSetDevice");
+    }
+    e = hipDeviceSynchronize();
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, nm + ": hipDeviceSynchronize");
+    e = hipFree(tab);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, nm + ": hipFree");
+    e = hipFree(scratch);
+    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, nm + ": hipFree");
+    if (switched) {
+        e = hipSetDevice(caller);
+        if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, nm + ": hipSetDevice");
+    }
+    return rc;
 }
 
 int current_device(int* dev) {
@@ -1180,13 +1206,8 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
 
 int es_plan_destroy(es_plan_t* plan) {
     if (plan == nullptr) return ES_OK;
-    int rc = ES_OK;
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) rc = hip_fail(e, "es_plan_destroy: hipDeviceSynchronize");
-    e = hipFree(plan->d_tab);
-    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_plan_destroy: hipFree");
-    e = hipFree(plan->d_scratch);
-    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_plan_destroy: hipFree");
+    const int rc = release_device_memory(plan->device, plan->d_tab, plan->d_scratch,
+                                         "es_plan_destroy");
     delete plan;
     return rc;
 }
@@ -1393,13 +1414,8 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
 
 int es_qplan_destroy(es_qplan_t* plan) {
     if (plan == nullptr) return ES_OK;
-    int rc = ES_OK;
-    hipError_t e = hipDeviceSynchronize();
-    if (e != hipSuccess) rc = hip_fail(e, "es_qplan_destroy: hipDeviceSynchronize");
-    e = hipFree(plan->d_tab);
-    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_qplan_destroy: hipFree");
-    e = hipFree(plan->d_scratch);
-    if (e != hipSuccess && rc == ES_OK) rc = hip_fail(e, "es_qplan_destroy: hipFree");
+    const int rc = release_device_memory(plan->device, plan->d_tab, plan->d_scratch,
+                                         "es_qplan_destroy");
     delete plan;
     return rc;
 }
