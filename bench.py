@@ -452,8 +452,9 @@ def main():
     value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
 
-    # the practical ceiling of es_perturb's access pattern: the same kernel,
-    # tiles and launch with no noise (es_stream_pass), timed after the step
+    # the practical in-place streaming ceiling over the same memory: the same
+    # tiles and launch, loads and stores only, not pipelined (es_stream_pass),
+    # timed after the step
     plan.stream_pass()
     ts = []
     for _ in range(3):
@@ -475,7 +476,7 @@ def main():
                 "algorithmic_bytes_per_launch": 4 * P,
                 "ceiling": {"GBps": round(ceiling_gbs, 1),
                             "frac_of_ceiling": round(perturb_gbs / ceiling_gbs, 4),
-                            "kernel": "es_perturb_kernel with no noise stream (es_stream_pass)"}}
+                            "kernel": "es_stream_kernel: in-place copy of every parameter, same tiles (es_stream_pass)"}}
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
               "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
               "normals_per_s": n_distinct * P / t_upd, "distinct_seeds": n_distinct}

@@ -260,11 +260,12 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
  * (0-based) uses sigma_t. Host-only helper. */
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T);
 
-/* Calibration pass: reads and rewrites every parameter of the plan unchanged
- * with exactly the memory access pattern of es_perturb (same tiles, launch
- * shape, pipelining and stores), so that its duration is the practical
- * in-place streaming ceiling against which es_perturb is measured.  Every
- * value is rewritten as itself (a NaN may come back quieted). */
+/* Calibration pass: reads every parameter of the plan and writes it back
+ * unchanged, bit for bit, with the tiles, 16-byte nontemporal accesses and
+ * launch shape of es_perturb but no arithmetic and no software pipelining
+ * (each workgroup loads a whole tile, then stores it) -- the fastest
+ * in-place stream over the plan's memory, so its duration is the practical
+ * ceiling against which es_perturb's bandwidth is measured. */
 int es_stream_pass(es_plan_t* plan, es_stream_t stream);
 
 /* Test hooks exposing the device noise functions the kernels use.

@@ -208,9 +208,7 @@ __device__ __forceinline__ void group_axpy(const uint32_t w[8], float scale_k, f
     }
 }
 
-// Noise streams applied by one perturb-style pass.  kM = 0: none (a
-// calibration pass that rewrites every value unchanged with the same memory
-// access pattern).  kM = 1: one stream,
+// Noise streams applied by one perturb-style pass.  kM = 1: one stream,
 // theta <- RNE(theta + c_0 eps_0) (perturb / restore).  kM = 2: two streams
 // applied in turn with a bf16 rounding in between,
 // theta <- RNE(RNE(theta + c_0 eps_0) + c_1 eps_1), which is es_restore of
@@ -412,6 +410,52 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
     uint32_t t = 0;
     for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x)
         perturb_tail<kThreads, kU, kM>(locate_tail<kTileElems>(tab, t, tl), st);
+}
+
+// The in-place streaming ceiling of a plan (es_stream_pass): every element
+// is read and written back as itself (XOR with `flip`, which the host passes
+// as 0, so the compiler keeps the stores), over the same tiles and 16-byte
+// nontemporal accesses as the passes above but without arithmetic and
+// without software pipelining -- each workgroup loads a whole tile, then
+// stores it.  On MI355X this is the fastest in-place stream measured (about
+// 3 % above the same stream pipelined), so it bounds what any pass over the
+// plan can reach.
+template <int kThreads, int kU>
+__global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTensor* __restrict__ tab,
+                                                             uint64_t n_full, uint64_t n_tail,
+                                                             uint32_t flip) {
+    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
+    uint32_t t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
+        const TileRef r = locate_full<kTileElems>(tab, t, tile);
+        uint32_t raw[kU][4];
+        load_tile<kThreads, kU>(r, raw);
+        __builtin_amdgcn_sched_barrier(0);      // all loads issued before the first wait
+#pragma unroll
+        for (int u = 0; u < kU; ++u)
+#pragma unroll
+            for (int k = 0; k < 4; ++k) raw[u][k] ^= flip;
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            store_group<true, true>(r.data, e, r.numel, raw[u]);
+        }
+    }
+    t = 0;
+    for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x) {
+        const TileRef r = locate_tail<kTileElems>(tab, t, tl);
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            if (e >= r.numel) break;
+            uint32_t raw[4];
+            load_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) raw[k] ^= flip;
+            store_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+        }
+    }
 }
 
 // One tile of the fused update: for each of the lane's groups in turn,
@@ -653,11 +697,18 @@ PerturbKernel perturb_kernel_for(int threads, int groups) {
     return nullptr;
 }
 
-// streams: 0 (calibration pass), 1 (perturb / restore), 2 (swap, two keys),
-// 3 (swap, one key)
+using StreamKernel = void (*)(const DevTensor*, uint64_t, uint64_t, uint32_t);
+
+StreamKernel stream_kernel(int threads, int groups) {
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_stream_kernel<T, U>;
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
+// streams: 1 (perturb / restore), 2 (swap, two keys), 3 (swap, one key)
 PerturbKernel perturb_kernel(int streams, int threads, int groups) {
     switch (streams) {
-        case 0: return perturb_kernel_for<0>(threads, groups);
         case 1: return perturb_kernel_for<1>(threads, groups);
         case 2: return perturb_kernel_for<2>(threads, groups);
         case 3: return perturb_kernel_for<3>(threads, groups);
@@ -868,13 +919,13 @@ int check_device(const es_plan_t* p) {
     return ES_OK;
 }
 
-// One pass of the perturb kernel: streams = 0 (no noise), 1 (seed[0],
-// coef[0]), 2 (two keys) or 3 (both coefficients on seed[0]).
+// One pass of the perturb kernel: streams = 1 (seed[0], coef[0]), 2 (two
+// keys) or 3 (both coefficients on seed[0]).
 int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double* coef,
                    hipStream_t s) {
     if (p->n_full + p->n_tail == 0) return ES_OK;
     Streams st = {};
-    const int terms = streams == 0 ? 0 : streams == 1 ? 1 : 2;
+    const int terms = streams == 1 ? 1 : 2;
     for (int m = 0; m < terms; ++m) {
         const uint64_t sd = streams == 3 ? seed[0] : seed[m];
         st.k0[m] = static_cast<uint32_t>(sd);
@@ -1459,7 +1510,13 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
     if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_stream_pass: null plan");
     const int rc = check_device(plan);
     if (rc != ES_OK) return rc;
-    return launch_streams(plan, 0, nullptr, nullptr, static_cast<hipStream_t>(stream));
+    if (plan->n_full + plan->n_tail == 0) return ES_OK;
+    hipLaunchKernelGGL(stream_kernel(plan->threads, plan->groups), dim3(plan->grid_perturb),
+                       dim3(plan->threads), 0, static_cast<hipStream_t>(stream), plan->d_tab,
+                       plan->n_full, plan->n_tail, 0u);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
+    return ES_OK;
 }
 
 double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T) {

@@ -195,8 +195,8 @@ class Plan:
                "es_restore")
 
     def stream_pass(self, stream=None):
-        """Rewrite every parameter unchanged with es_perturb's access pattern
-        (the in-place streaming ceiling)."""
+        """Read every parameter and write it back unchanged over es_perturb's
+        tiles, with no arithmetic (the in-place streaming ceiling)."""
         _check(load().es_stream_pass(self.handle, _stream(stream)), "es_stream_pass")
 
     def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):

@@ -190,7 +190,8 @@ def test_results_do_not_depend_on_launch_shape(shape, monkeypatch):
 
 def test_stream_pass_rewrites_values_unchanged():
     bits = [wl.random_bf16_bits(n, 95 + i) for i, n in enumerate([300001, 1 << 16, 9])]
-    bits[0][:6] = [0x0000, 0x8000, 0x7F80, 0xFF80, 0x0001, 0x807F]   # zeros, infinities, subnormals
+    # zeros, infinities, subnormals and NaNs with payloads: written back bit for bit
+    bits[0][:9] = [0x0000, 0x8000, 0x7F80, 0xFF80, 0x0001, 0x807F, 0x7FC1, 0xFF81, 0x7F81]
     ts = [to_device(b) for b in bits]
     plan = esopt.Plan([ts[0][1:], ts[1], ts[2]])
     plan.stream_pass()
