@@ -126,6 +126,22 @@ def _stream(stream):
     return ctypes.c_void_p(int(stream))
 
 
+def _u64_arg(x, what):
+    """An integer argument of a uint64_t parameter, range-checked (ctypes
+    would wrap a negative or oversized value silently)."""
+    v = int(x)
+    if not 0 <= v < (1 << 64):
+        raise ValueError(f"{what} must be in [0, 2^64), got {v}")
+    return v
+
+
+def _u32_arg(x, what):
+    v = int(x)
+    if not 0 <= v < (1 << 32):
+        raise ValueError(f"{what} must be in [0, 2^32), got {v}")
+    return v
+
+
 def _dev_ptr(t, dtype, what):
     """Pointer of a contiguous tensor the device can read: on the GPU, or in
     pinned (page-locked, device-mapped) host memory."""
@@ -147,7 +163,8 @@ class Plan:
         tensors = list(tensors)
         if not tensors:
             raise ValueError("empty tensor list")
-        ids = list(range(len(tensors))) if tensor_ids is None else [int(i) for i in tensor_ids]
+        ids = (list(range(len(tensors))) if tensor_ids is None
+               else [_u32_arg(i, "tensor_id") for i in tensor_ids])
         if len(ids) != len(tensors):
             raise ValueError("tensor_ids must match tensors")
         arr = (EsTensor * len(tensors))()
@@ -187,12 +204,12 @@ class Plan:
         return list(self._tensors)
 
     def perturb(self, seed, sign, sigma, stream=None):
-        _check(load().es_perturb(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
-               "es_perturb")
+        _check(load().es_perturb(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
+                                 _stream(stream)), "es_perturb")
 
     def restore(self, seed, sign, sigma, stream=None):
-        _check(load().es_restore(self.handle, int(seed), int(sign), float(sigma), _stream(stream)),
-               "es_restore")
+        _check(load().es_restore(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
+                                 _stream(stream)), "es_restore")
 
     def stream_pass(self, stream=None):
         """Read every parameter and write it back unchanged over es_perturb's
@@ -203,9 +220,9 @@ class Plan:
         """Revert member `from` and apply member `to` in one pass: the same
         bits as restore(from) followed by perturb(to)."""
         sigma_to = sigma if sigma_to is None else sigma_to
-        _check(load().es_swap(self.handle, int(seed_from), int(sign_from), float(sigma),
-                              int(seed_to), int(sign_to), float(sigma_to), _stream(stream)),
-               "es_swap")
+        _check(load().es_swap(self.handle, _u64_arg(seed_from, "seed_from"), int(sign_from),
+                              float(sigma), _u64_arg(seed_to, "seed_to"), int(sign_to),
+                              float(sigma_to), _stream(stream)), "es_swap")
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                z_out=None, status_out=None, stream=None, round_seed=0):
@@ -239,11 +256,10 @@ def _call_update(fn, what, handle, seeds, signs, rewards, alpha, sigma, zscore_e
         raise ValueError("seeds and signs differ in length")
     if rewards.numel() != n:
         raise ValueError("rewards must have one entry per member")
-    c_seeds = (_u64 * max(n, 1))(*[int(s) for s in seeds])
+    c_seeds = (_u64 * max(n, 1))(*[_u64_arg(s, "seed") for s in seeds])
     c_signs = (_i32 * max(n, 1))(*[int(s) for s in signs])
-    if not 0 <= int(round_seed) < (1 << 64):
-        raise ValueError("round_seed must be in [0, 2^64)")
-    opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), int(flags), int(round_seed))
+    opts = EsUpdateOpts(float(alpha), float(sigma), float(zscore_eps), _u32_arg(flags, "flags"),
+                        _u64_arg(round_seed, "round_seed"))
     _check(fn(handle, c_seeds, c_signs, _dev_ptr(rewards, torch.float32, "rewards"), n,
               ctypes.byref(opts), _dev_ptr(z_out, torch.float32, "z_out"),
               _dev_ptr(status_out, torch.int32, "status_out"), _stream(stream)), what)
@@ -259,7 +275,8 @@ class QPlan:
         codes, scales, rows = list(codes), list(scales), [int(r) for r in rows]
         if not codes or len(scales) != len(codes) or len(rows) != len(codes):
             raise ValueError("codes, scales and rows must be non-empty and of equal length")
-        ids = list(range(len(codes))) if tensor_ids is None else [int(i) for i in tensor_ids]
+        ids = (list(range(len(codes))) if tensor_ids is None
+               else [_u32_arg(i, "tensor_id") for i in tensor_ids])
         if len(ids) != len(codes):
             raise ValueError("tensor_ids must match tensors")
         arr = (EsQTensor * len(codes))()
@@ -298,11 +315,11 @@ class QPlan:
         return int(load().es_qplan_device_bytes(self.handle))
 
     def perturb(self, seed, sign, sigma, stream=None):
-        _check(load().es_qperturb(self.handle, int(seed), int(sign), float(sigma),
+        _check(load().es_qperturb(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
                                   _stream(stream)), "es_qperturb")
 
     def restore(self, seed, sign, sigma, stream=None):
-        _check(load().es_qrestore(self.handle, int(seed), int(sign), float(sigma),
+        _check(load().es_qrestore(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
                                   _stream(stream)), "es_qrestore")
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
@@ -347,15 +364,17 @@ def philox_words(seed, tensor_id, quad0, n_quads, domain=0, device="cuda", strea
     """Raw Philox words as an int32 CUDA tensor of shape (n_quads, 4)
     (reinterpret as uint32)."""
     out = torch.empty((n_quads, 4), dtype=torch.int32, device=device)
-    _check(load().es_philox_words(int(seed), int(tensor_id), int(domain), int(quad0),
-                                  int(n_quads), ctypes.c_void_p(out.data_ptr()), _stream(stream)),
-           "es_philox_words")
+    _check(load().es_philox_words(_u64_arg(seed, "seed"), _u32_arg(tensor_id, "tensor_id"),
+                                  _u32_arg(domain, "domain"), _u64_arg(quad0, "quad0"),
+                                  _u64_arg(n_quads, "n_quads"), ctypes.c_void_p(out.data_ptr()),
+                                  _stream(stream)), "es_philox_words")
     return out
 
 
 def normals(seed, tensor_id, elem0, n, device="cuda", stream=None):
     """eps_j for j = elem0 .. elem0 + n - 1 of one tensor, float32 CUDA tensor."""
     out = torch.empty(n, dtype=torch.float32, device=device)
-    _check(load().es_normals(int(seed), int(tensor_id), int(elem0), int(n),
+    _check(load().es_normals(_u64_arg(seed, "seed"), _u32_arg(tensor_id, "tensor_id"),
+                             _u64_arg(elem0, "elem0"), _u64_arg(n, "n"),
                              ctypes.c_void_p(out.data_ptr()), _stream(stream)), "es_normals")
     return out

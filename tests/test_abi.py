@@ -185,3 +185,17 @@ def test_quantized_plan_validation_without_gpu(lib):
     assert lib.es_qupdate(fake, seeds, signs, fake, 2, ctypes.byref(bad), None, None, None) == E
     assert lib.es_qplan_destroy(None) == esopt.ES_OK
     assert lib.es_qplan_numel(None) == 0
+
+
+def test_binding_range_checks_integer_arguments():
+    """ctypes would wrap a negative or oversized seed, id or flag word
+    silently; the binding refuses them before any call."""
+    assert esopt._u64_arg(0, "seed") == 0
+    assert esopt._u64_arg((1 << 64) - 1, "seed") == (1 << 64) - 1
+    assert esopt._u32_arg((1 << 32) - 1, "tensor_id") == (1 << 32) - 1
+    for bad in (-1, 1 << 64):
+        with pytest.raises(ValueError, match="seed"):
+            esopt._u64_arg(bad, "seed")
+    for bad in (-1, 1 << 32):
+        with pytest.raises(ValueError, match="tensor_id"):
+            esopt._u32_arg(bad, "tensor_id")
