@@ -12,9 +12,8 @@ parameters instead of 2N, plus the update.  The same driver runs the int8
 path (esopt.QPlan), whose revert is exact and which has no fused swap.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
-recorded; because every kernel is
-deterministic, replaying the records from the same starting parameters
-rebuilds the parameters bit for bit (the paper reconstructs its final models
+recorded; because every kernel is deterministic, replaying the records from
+the same starting parameters rebuilds the parameters bit for bit (the paper reconstructs its final models
 from the recorded update sequence the same way, Appendix D.2 and D.4).
 """
 
@@ -117,10 +116,24 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
     return rec
 
 
+def _torch_stream(stream, device):
+    if stream is None:
+        return torch.cuda.current_stream(device)
+    if isinstance(stream, torch.cuda.Stream):
+        return stream
+    return torch.cuda.ExternalStream(int(stream), device=device)
+
+
 def apply_update(plan, rec: GenerationRecord, stream=None):
-    r = torch.tensor(rec.rewards, dtype=torch.float32, device=plan.device)
-    plan.update(rec.seeds, rec.signs, r, rec.alpha, sigma=rec.sigma, zscore_eps=rec.zscore_eps,
-                flags=rec.flags, stream=stream, round_seed=rec.round_seed)
+    # the rewards are staged on the stream the update runs on, so PyTorch's
+    # caching allocator does not hand their memory out again before the
+    # update has read it
+    s = _torch_stream(stream, plan.device)
+    with torch.cuda.stream(s):
+        r = torch.tensor(rec.rewards, dtype=torch.float32, device=plan.device)
+        plan.update(rec.seeds, rec.signs, r, rec.alpha, sigma=rec.sigma,
+                    zscore_eps=rec.zscore_eps, flags=rec.flags, stream=s,
+                    round_seed=rec.round_seed)
 
 
 def replay(plan, records, with_perturbations=True, stream=None):

@@ -189,3 +189,26 @@ def test_drift_study_matches_oracle_walk(capsys):
     swap = [r for r in rows if r.get("walk") == "swap" and r["generation"] == 2][0]
     rest = [r for r in rows if r.get("walk") == "restore" and r["generation"] == 2][0]
     assert swap["roundings"] == 10 and rest["roundings"] == 16
+
+
+def test_generation_on_a_side_stream_matches_default_stream():
+    """A generation issued on a stream of its own (torch Stream or raw
+    handle) gives the bits of the same generation on the current stream; the
+    update's rewards are staged on that stream."""
+    W = wl.TINY
+    _, ref = _fresh(W)
+    seeds, signs = antithetic_seeds(40, 3)
+    scores = [0.3, 0.8, 0.1, 0.6, 0.9, 0.2]
+    with esopt.Plan(ref) as p:
+        run_generation(p, seeds, signs, 1e-3, 5e-4, evaluate=lambda i: scores[i])
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    for handle in (side, side.cuda_stream):
+        _, ts = _fresh(W)
+        torch.cuda.synchronize()
+        with esopt.Plan(ts) as p:
+            run_generation(p, seeds, signs, 1e-3, 5e-4, evaluate=lambda i: scores[i],
+                           stream=handle)
+            side.synchronize()
+        for a, b in zip(ref, ts):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16))
