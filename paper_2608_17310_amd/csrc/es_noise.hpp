@@ -19,7 +19,9 @@
 //   * the two three-way XORs of a round are single v_bitop3_b32 (truth table
 //     0x96) from the third round on; the first two rounds keep plain XORs,
 //     where the counter's high words, the tensor id and the key are
-//     wave-uniform and the compiler moves those parts to the scalar unit;
+//     wave-uniform and the compiler moves those parts to the scalar unit, and
+//     so does the third round's second XOR, whose two other operands are
+//     still uniform (a bitop3 may read only one scalar register);
 //   * OR-ing the low 23 bits of a word into the exponent of 1.0 (one
 //     v_and_or_b32) gives f = 1 + m 2^-23 in [1, 2); u = f - (1 - 2^-24) is
 //     exact, and v_sin_f32 / v_cos_f32 take turns and are periodic, so f
@@ -48,20 +50,22 @@ struct Words {
 
 constexpr float kSqrt2Ln2 = 1.17741002251547466f;       // sqrt(2 ln 2)
 
-// One Philox round: two 32x32->64 products, two three-way XORs.
-template <bool kBitop3>
+// One Philox round: two 32x32->64 products, two three-way XORs (each a
+// single bitop3 when its flag is set).
+template <bool kBitop0, bool kBitop2>
 __device__ __forceinline__ void philox_round(uint32_t& c0, uint32_t& c1, uint32_t& c2,
                                              uint32_t& c3, uint32_t k0, uint32_t k1) {
     const uint64_t p0 = static_cast<uint64_t>(kPhiloxM0) * c0;
     const uint64_t p1 = static_cast<uint64_t>(kPhiloxM1) * c2;
     uint32_t n0, n2;
-    if constexpr (kBitop3) {
+    if constexpr (kBitop0)
         n0 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(p1 >> 32), c1, k0, 0x96);
-        n2 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(p0 >> 32), c3, k1, 0x96);
-    } else {
+    else
         n0 = static_cast<uint32_t>(p1 >> 32) ^ c1 ^ k0;
+    if constexpr (kBitop2)
+        n2 = __builtin_amdgcn_bitop3_b32(static_cast<uint32_t>(p0 >> 32), c3, k1, 0x96);
+    else
         n2 = static_cast<uint32_t>(p0 >> 32) ^ c3 ^ k1;
-    }
     c1 = static_cast<uint32_t>(p1);
     c3 = static_cast<uint32_t>(p0);
     c0 = n0;
@@ -72,11 +76,12 @@ __device__ __forceinline__ void philox_round(uint32_t& c0, uint32_t& c1, uint32_
 // increments between rounds.
 __device__ __forceinline__ Words philox4x32_10(uint32_t c0, uint32_t c1, uint32_t c2,
                                                uint32_t c3, uint32_t k0, uint32_t k1) {
-    philox_round<false>(c0, c1, c2, c3, k0, k1);
-    philox_round<false>(c0, c1, c2, c3, k0 + kWeyl0, k1 + kWeyl1);
+    philox_round<false, false>(c0, c1, c2, c3, k0, k1);
+    philox_round<false, false>(c0, c1, c2, c3, k0 + kWeyl0, k1 + kWeyl1);
+    philox_round<true, false>(c0, c1, c2, c3, k0 + 2 * kWeyl0, k1 + 2 * kWeyl1);
 #pragma unroll
-    for (uint32_t round = 2; round < 10; ++round)
-        philox_round<true>(c0, c1, c2, c3, k0 + round * kWeyl0, k1 + round * kWeyl1);
+    for (uint32_t round = 3; round < 10; ++round)
+        philox_round<true, true>(c0, c1, c2, c3, k0 + round * kWeyl0, k1 + round * kWeyl1);
     return Words{c0, c1, c2, c3};
 }
 

@@ -174,6 +174,16 @@ __device__ __forceinline__ void qgroup_axpy(uint32_t e, uint32_t tensor_id, uint
     }
 }
 
+// The low bytes of four 32-bit codes packed into one word (code i in byte
+// i): two byte permutes and an OR.
+__device__ __forceinline__ uint32_t pack_codes(int32_t c0, int32_t c1, int32_t c2, int32_t c3) {
+    // v_perm_b32 numbers the second operand's bytes 0-3 and the first's 4-7;
+    // selector byte 0x0c yields zero
+    const uint32_t lo = __builtin_amdgcn_perm(uint32_t(c1), uint32_t(c0), 0x0c0c0400u);
+    const uint32_t hi = __builtin_amdgcn_perm(uint32_t(c3), uint32_t(c2), 0x04000c0cu);
+    return lo | hi;
+}
+
 // floor(x) as an integer in one instruction (the compiler emits a floor and
 // a conversion); x is within +-2^31 here.
 __device__ __forceinline__ int32_t floor_to_int(float x) {
@@ -183,19 +193,36 @@ __device__ __forceinline__ int32_t floor_to_int(float x) {
 }
 
 // 1 + (2 r + 1) 2^-10 as a binary32 from the top 9 bits r of a noise word.
-__device__ __forceinline__ float spare_one_plus(uint32_t w) {
-    return __uint_as_float(((w >> 9) & 0x007FC000u) | 0x3F802000u);
+// `one_plus_half_step` is 0x3F802000 (1 + 2^-10) held in a vector register
+// by the caller: with the mask in a scalar register the masking and the OR
+// are then one v_and_or_b32 (a VOP3 instruction reads at most one scalar
+// register or literal on this architecture).
+__device__ __forceinline__ float spare_one_plus(uint32_t w, uint32_t one_plus_half_step) {
+    return __uint_as_float(((w >> 9) & 0x007FC000u) | one_plus_half_step);
 }
 
-// Perturb / restore code: clamp(q +- floor(d + (2 r + 1) 2^-10), -127, 127)
+// 0x3F802000 in a vector register (see spare_one_plus).
+__device__ __forceinline__ uint32_t one_plus_half_step_vgpr() {
+    uint32_t c = 0x3F802000u;
+    asm volatile("" : "+v"(c));
+    return c;
+}
+
+// Perturb / restore code: clamp(q +- floor(d + (2 r + 1) 2^-10), lo, 127)
 // from v = d + f, f = 1 + (2 r + 1) 2^-10 (formed by the caller as one FMA):
 // floor(v) - 1.  v is capped at +-2^30 quanta, far beyond what any code can
-// absorb, so the integer arithmetic cannot overflow.
+// absorb, so the integer arithmetic cannot overflow.  lo is -127; a caller
+// whose scale is invalid passes d = 0 (so the step is 0) and lo = -128, which
+// returns every code unchanged without a branch.
 template <bool kNegate>
-__device__ __forceinline__ int32_t qstep9(int32_t q, float v) {
+__device__ __forceinline__ int32_t qstep9(int32_t q, float v, int32_t lo) {
     const int32_t k = floor_to_int(__builtin_amdgcn_fmed3f(v, -0x1p30f, 0x1p30f)) - 1;
     const int32_t x = kNegate ? q - k : q + k;
-    return min(max(x, -127), 127);
+    // min(max(x, lo), 127) in one v_med3_i32 (lo <= 127 always; the compiler
+    // only forms the median for constant bounds)
+    int32_t r;
+    asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "s"(127));
+    return r;
 }
 
 // Update code: clamp(q + s * floor(d + r 2^-16), -127, 127) with s = -1 when

@@ -458,6 +458,12 @@ __global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTensor* __
     }
 }
 
+// w == +-0, tested on the bit pattern so that the member loop's skip stays on
+// the scalar unit (a binary32 compare would be a vector instruction).
+__device__ __forceinline__ bool is_zero_weight(float w) {
+    return (__float_as_uint(w) << 1) == 0u;
+}
+
 // One tile of the fused update: for each of the lane's groups in turn,
 // acc = sum_d w_d eps_d (binary32, members in table order, zero weights
 // skipped), theta <- round(theta + acc), store it.  Rounding is to nearest
@@ -496,7 +502,7 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
         for (uint32_t d = 0; d < n_distinct; ++d) {
             const Member m = members[d];
-            if (m.w_k == 0.0f) continue;
+            if (is_zero_weight(m.w_k)) continue;
             uint32_t w[8];
             group_words(q_lo, q_hi, r.tensor_id, m.k0, m.k1, w);
             group_axpy(w, m.w_k, acc);
@@ -743,13 +749,16 @@ __device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e
                                                uint32_t tensor_id, const Member& m, float inv0,
                                                float inv1, uint32_t out[4]) {
     const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    // an invalid scale has inv = 0: its step is 0 and its codes clamp to
+    // [-128, 127], i.e. they are left as they are
     const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
+    const int32_t lo[2] = {inv0 != 0.0f ? -127 : -128, inv1 != 0.0f ? -127 : -128};
+    const uint32_t one_plus = esq::one_plus_half_step_vgpr();
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, m.k0, m.k1);
-        const bool valid = (c < 2 ? inv0 : inv1) != 0.0f;
         const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
-        uint32_t o = 0;
+        int32_t code[4];
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
             float t, cs, sn;
@@ -759,12 +768,11 @@ __device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e
             for (int h = 0; h < 2; ++h) {
                 const int i = 2 * p + h;
                 const int32_t qc = static_cast<int8_t>(raw[c] >> (8 * i));
-                const float v = __builtin_fmaf(t, trig[h], esq::spare_one_plus(ws[i]));
-                const int32_t code = valid ? esq::qstep9<kNegate>(qc, v) : qc;
-                o |= (static_cast<uint32_t>(code) & 0xFFu) << (8 * i);
+                const float v = __builtin_fmaf(t, trig[h], esq::spare_one_plus(ws[i], one_plus));
+                code[i] = esq::qstep9<kNegate>(qc, v, lo[c >> 1]);
             }
         }
-        out[c] = o;
+        out[c] = esq::pack_codes(code[0], code[1], code[2], code[3]);
     }
 }
 
@@ -792,7 +800,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
             for (int i = 0; i < 16; ++i) acc[i] = 0.0f;
             for (uint32_t d = 0; d < n_members; ++d) {
                 const Member m = members[d];
-                if (m.w_k == 0.0f) continue;
+                if (is_zero_weight(m.w_k)) continue;
                 esq::qgroup_axpy(e, r.tensor_id, m.k0, m.k1, m.w_k, acc);
             }
             const es::Words da =

@@ -73,6 +73,9 @@ def _tensor_set():
         scales.append(sc)
     scales[1][[3, 50, 51]] = [0.0, np.inf, 1e-40]     # invalid: left unchanged
     scales[1][[7, 8]] = 2e-6                           # offsets large enough to clamp
+    # -128 (outside the clamp range): kept in rows with an invalid scale,
+    # clamped into [-127, 127] by a step in a valid row (row 10)
+    codes[1][[3 * 8, 3 * 8 + 5, 50 * 8 + 1, 51 * 8 + 7, 10 * 8 + 2]] = -128
     return codes, scales, rows, ids
 
 
@@ -108,7 +111,8 @@ def test_qperturb_and_restore_match_oracle():
         print("qrestore", i, rep)
         assert_qparity(rep, f"qrestore tensor {i}")
         # exact revert wherever the perturbed code was not at a clamp bound
-        free = np.abs(pert[i].astype(np.int64)) < 127
+        # (and the code was inside the clamp range to begin with)
+        free = (np.abs(pert[i].astype(np.int64)) < 127) & (q > -128)
         np.testing.assert_array_equal(back[i][free], q[free])
     assert np.mean(pert[0] != codes[0]) > 0.5
     plan.close()

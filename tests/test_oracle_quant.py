@@ -235,3 +235,16 @@ def test_identities_and_validation():
     np.testing.assert_array_equal(a, b)
     with pytest.raises(ValueError):
         qperturb(q, sc, 64, 1, 0, 2, 1e-3)
+
+
+def test_out_of_range_code_is_kept_under_an_invalid_scale_and_clamped_otherwise():
+    # -128 lies outside the clamp range [-127, 127]: a step under a valid
+    # scale clamps it into the range (even a zero offset), and a row whose
+    # scale is not a normal positive finite value is left exactly as it is
+    q = np.full(16, -128, dtype=np.int8)
+    scales = np.array([7e-4, 0.0], dtype=np.float32)       # row 0 valid, row 1 invalid
+    out = qperturb(q, scales, 8, 5, 0, 1, 1e-3)
+    assert np.all(out[:8] >= -127)
+    assert np.all(out[8:] == -128)
+    back = qrestore(out, scales, 8, 5, 0, 1, 1e-3)
+    assert np.all(back[8:] == -128)
