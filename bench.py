@@ -110,6 +110,7 @@ def cpu_baseline(W, seeds, signs, rewards, sigma, theta_samples, workers, budget
     wall = time.perf_counter() - t0
     rate = (2 * n + 1) * n_elems / wall
     return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            "full_step_s_extrapolated": round((2 * n + 1) * W.n_params / rate, 1),
             "sample": f"{n_elems} elements sampled across {len(jobs)} tensors of {W.name}, "
                       f"one full step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 "
                       f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
@@ -169,8 +170,9 @@ def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_te
     with mp.get_context("fork").Pool(workers) as pool:
         pool.map(_oracle_qchunk, jobs, chunksize=1)
     wall = time.perf_counter() - t0
-    return {"value": (2 * n + 1) * n_elems / wall, "unit": "params/s", "cores": workers,
-            "kind": "oracle",
+    rate = (2 * n + 1) * n_elems / wall
+    return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            "full_step_s_extrapolated": round((2 * n + 1) * W.n_params / rate, 1),
             "sample": f"{n_elems} int8 codes sampled across {len(jobs)} tensors of {W.name}, one "
                       f"full int8 step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 NumPy "
                       f"over {workers} worker processes, {wall:.1f} s wall"}
