@@ -101,8 +101,10 @@ typedef struct es_plan es_plan_t;
  * INVALID_ARG for a null pointer, n_tensors out of range, duplicate
  * tensor_id, nonzero reserved field, null data with numel > 0, or tensors
  * whose byte ranges overlap; ALIGN for odd addresses; NOMEM / HIP for
- * allocation failures.  On success *out owns a device table of
- * 48 * (n_tensors + 1) bytes and ~42 KB of scratch, freed by es_plan_destroy. */
+ * allocation failures.  On success *out owns 32 bytes of device memory per
+ * tile of 65 536 elements (0.024 % of the parameter bytes; see
+ * es_tile_layout) and ~42 KB of scratch, freed by es_plan_destroy;
+ * es_plan_device_bytes reports the total. */
 int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out);
 
 /* Free a plan (NULL is a no-op).  Synchronises the plan's device first (made
@@ -115,8 +117,8 @@ int es_plan_destroy(es_plan_t* plan);
 uint64_t es_plan_numel(const es_plan_t* plan);
 uint64_t es_plan_tiles(const es_plan_t* plan);
 
-/* Device memory a plan allocates for itself (its tensor table and member
- * scratch), in bytes: everything the method needs beyond the parameters
+/* Device memory a plan allocates for itself (its tile descriptors and
+ * member scratch), in bytes: everything the method needs beyond the parameters
  * (Section 3: memory stays at inference level).  0 for NULL. */
 uint64_t es_plan_device_bytes(const es_plan_t* plan);
 
@@ -279,6 +281,23 @@ int es_philox_words(uint64_t seed, uint32_t tensor_id, uint32_t domain,
                     es_stream_t stream);
 int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n,
                float* out_dev, es_stream_t stream);
+
+/* Test hook of the host-side tiling (no device access; the address is never
+ * dereferenced): the tiles es_plan_create lays out for one bf16 tensor of
+ * `numel` elements at address `addr`, with the plan's launch shape.  Tile i
+ * covers elements [elem0, end) of the tensor; full tiles come first (full =
+ * 1: tile-sized, starting where the address is a multiple of the tile's byte
+ * size), then tail tiles.  Writes min(cap, count) entries to `out` (which may
+ * be NULL when cap is 0) and the count to *n_tiles.  Errors: INVALID_ARG for
+ * a null n_tiles, numel > 2^60 or an odd address (ALIGN). */
+typedef struct es_tile_info {
+    uint64_t elem0;
+    uint64_t end;
+    uint32_t full;
+    uint32_t aligned16;
+} es_tile_info_t;
+int es_tile_layout(uint64_t addr, uint64_t numel, es_tile_info_t* out, uint64_t cap,
+                   uint64_t* n_tiles);
 
 /* Static name of an error code; detail of the calling thread's last error. */
 const char* es_strerror(int code);

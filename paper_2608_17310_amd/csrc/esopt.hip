@@ -74,21 +74,24 @@ constexpr int kDefaultUpdateWgPerCu = 8;
 constexpr int kDefaultQGroups = 4;          // int8 tiles: 1024 x 4 x 16 codes (64 KB)
 constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
-// Device tensor table entry.  Tiles are numbered in two sequences: full
-// tiles (16-byte aligned, entirely inside the tensor) and tail tiles (the
-// partial last tile, or every tile of a tensor whose base is not 16-byte
-// aligned).  A sentinel entry closes both sequences.
-struct DevTensor {
-    uint16_t* data;
-    uint64_t numel;
-    uint64_t first_full;                    // global index of the tensor's first full tile
-    uint64_t first_tail;                    // global index of its first tail tile
+// Tile descriptor.  A plan lists its tiles in two runs, indexed by tile
+// number: full tiles first (kThreads * kU * 8 elements of one tensor, starting
+// on a tile-sized boundary of the address space), then tail tiles (the part
+// of a tensor before its first such boundary, the part after its last full
+// tile, or every tile of a tensor whose base is not 16-byte aligned).  A
+// workgroup reads one descriptor per tile with a single scalar load and no
+// search (searching a per-tensor table is a chain of dependent scalar loads).
+// Full tiles aligned to the address space, not to their tensor's base: with
+// hundreds of tensors at unrelated offsets, tiles at mixed offsets streamed
+// ~4 % slower.  32 bytes per 65 536-element tile.
+struct DevTile {
+    uint16_t* data;                         // the tensor's base
+    uint64_t elem0;                         // the tile's first element in its tensor
+    uint64_t limit;                         // one past the last element a tail tile may touch
     uint32_t tensor_id;
-    uint32_t n_tensors;                     // entries before the sentinel (same in all)
-    uint32_t aligned16;                     // base 16-byte aligned: vector tail groups
-    uint32_t pad;
+    uint32_t aligned16;                     // base 16-byte aligned: whole groups 16-byte accesses
 };
-static_assert(sizeof(DevTensor) == 48, "tensor table entry layout");
+static_assert(sizeof(DevTile) == 32, "tile descriptor layout");
 
 struct MemberIn {                           // one population member, CSR order
     uint32_t reward_index;
@@ -273,35 +276,27 @@ __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e,
     for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
 }
 
-// A tile: kThreads * kU * 8 consecutive elements of one tensor.
+// A tile: up to kThreads * kU * 8 consecutive elements of one tensor, from
+// element elem0 on; accesses of a tail tile stay below `limit`.  Every field
+// is wave-uniform (scalar registers).
 struct TileRef {
     uint16_t* data;
-    uint64_t numel;
+    uint64_t limit;
     uint64_t elem0;
     uint32_t tensor_id;
     uint32_t aligned16;
 };
 
-// Tile lookup.  A workgroup's tiles increase monotonically, so its table
-// index t only moves forward; t, the table entries and the tile are
-// wave-uniform (scalar registers and scalar loads).
-template <uint64_t kTileElems>
-__device__ __forceinline__ TileRef locate_full(const DevTensor* __restrict__ tab, uint32_t& t,
-                                               uint64_t tile) {
-    t = es::seek_tensor(t, tile, tab[0].n_tensors,
-                        [tab](uint32_t i) { return tab[i].first_full; });
-    return TileRef{tab[t].data, tab[t].numel, (tile - tab[t].first_full) * kTileElems,
-                   tab[t].tensor_id, tab[t].aligned16};
+__device__ __forceinline__ TileRef tile_ref(const DevTile& d) {
+    return TileRef{d.data, d.limit, d.elem0, d.tensor_id, d.aligned16};
 }
 
-template <uint64_t kTileElems>
-__device__ __forceinline__ TileRef locate_tail(const DevTensor* __restrict__ tab, uint32_t& t,
-                                               uint64_t tile) {
-    t = es::seek_tensor(t, tile, tab[0].n_tensors,
-                        [tab](uint32_t i) { return tab[i].first_tail; });
-    const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
-    return TileRef{tab[t].data, tab[t].numel, (n_full + tile - tab[t].first_tail) * kTileElems,
-                   tab[t].tensor_id, tab[t].aligned16};
+// Keep a prefetched descriptor in scalar registers: without this the
+// compiler may drop it and load it again where it is used, exposing the
+// load's latency there.  Placed after the work that hides the load, so the
+// wait it implies costs nothing.
+__device__ __forceinline__ void keep_in_sgprs(DevTile& d) {
+    asm volatile("" : "+s"(d.data), "+s"(d.elem0), "+s"(d.tensor_id));
 }
 
 template <int kThreads, int kU>
@@ -309,7 +304,7 @@ __device__ __forceinline__ void load_tile(const TileRef& r, uint32_t raw[kU][4])
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-        load_group<true, true>(r.data, e, r.numel, raw[u]);
+        load_group<true, true>(r.data, e, r.limit, raw[u]);
     }
 }
 
@@ -334,7 +329,7 @@ __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-        store_group<true, true>(r.data, e, r.numel, raw[u]);
+        store_group<true, true>(r.data, e, r.limit, raw[u]);
     }
 }
 
@@ -345,41 +340,44 @@ __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-        if (e >= r.numel) break;
+        if (e >= r.limit) break;
         uint32_t raw[4], out[4];
-        load_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+        load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
         perturb_group<kM>(raw, e, q_hi, r.tensor_id, st, out);
-        store_group<false, true>(r.data, e, r.numel, out, r.aligned16 != 0u);
+        store_group<false, true>(r.data, e, r.limit, out, r.aligned16 != 0u);
     }
 }
 
 // One software-pipeline step over full tiles: issue the 16-byte loads of the
-// workgroup's next tile into `next_buf`, then perturb the current tile from
-// `cur_buf`, so the memory pipe does not idle through the Philox /
-// Box-Muller arithmetic.  Returns true when the workgroup has no next tile.
+// workgroup's next tile (`nxt`) into `next_buf`, read the descriptor of the
+// tile after it, then perturb the current tile from `cur_buf`, so the memory
+// pipe does not idle through the Philox / Box-Muller arithmetic and the
+// descriptor's scalar load completes under it.  Returns true when the
+// workgroup has no next tile.
 //
 // The loads are issued on every step, the last one reloading its own tile
-// into the idle buffer (128 KB per workgroup per pass, never used): the
-// compiler's wait before the current tile's arithmetic is path-insensitive,
-// and a path without loads after the current tile's made it wait for the
-// next tile's loads as well.
+// into the idle buffer (128 KB per workgroup per pass, never used), and the
+// descriptor index is clamped rather than tested: the compiler's wait before
+// the current tile's arithmetic is path-insensitive, and a path without loads
+// after the current tile's made it wait for the next tile's loads as well.
 template <int kThreads, int kU, int kM>
-__device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, uint32_t& t,
-                                             uint64_t& tile, uint64_t n_full, TileRef& cur,
+__device__ __forceinline__ bool perturb_step(const DevTile* __restrict__ tiles, uint64_t& tile,
+                                             uint64_t n_full, TileRef& cur, TileRef& nxt,
                                              uint32_t cur_buf[kU][4], uint32_t next_buf[kU][4],
                                              const Streams& st) {
-    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
     const uint64_t next = tile + gridDim.x;
     const bool more = next < n_full;
-    TileRef nxt = cur;
-    if (more) nxt = locate_full<kTileElems>(tab, t, next);
     __builtin_amdgcn_sched_barrier(0);
-    load_tile<kThreads, kU>(nxt, next_buf);
+    load_tile<kThreads, kU>(more ? nxt : cur, next_buf);
+    __builtin_amdgcn_sched_barrier(0);
+    DevTile after = tiles[min(next + gridDim.x, n_full - 1)];
     __builtin_amdgcn_sched_barrier(0);
     perturb_loaded<kThreads, kU, kM>(cur, cur_buf, st);
+    keep_in_sgprs(after);
     if (!more) return true;
     tile = next;
     cur = nxt;
+    nxt = tile_ref(after);
     return false;
 }
 
@@ -390,26 +388,24 @@ __device__ __forceinline__ bool perturb_step(const DevTensor* __restrict__ tab, 
 // memory operations outstanding (the previous tile's stores, then the next
 // tile's loads): the wait for the current tile then leaves both in flight.
 template <int kThreads, int kU, int kM>
-__global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* __restrict__ tab,
+__global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTile* __restrict__ tiles,
                                                               uint64_t n_full, uint64_t n_tail,
                                                               Streams st) {
-    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
     uint64_t tile = blockIdx.x;
     if (tile < n_full) {
-        uint32_t t = 0;
-        TileRef cur = locate_full<kTileElems>(tab, t, tile);
+        TileRef cur = tile_ref(tiles[tile]);
+        TileRef nxt = tile_ref(tiles[min(tile + gridDim.x, n_full - 1)]);
         uint32_t a[kU][4], b[kU][4];
         load_tile<kThreads, kU>(cur, a);
-        if (!perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) {
+        if (!perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, a, b, st)) {
             for (;;) {
-                if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, b, a, st)) break;
-                if (perturb_step<kThreads, kU, kM>(tab, t, tile, n_full, cur, a, b, st)) break;
+                if (perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, b, a, st)) break;
+                if (perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, a, b, st)) break;
             }
         }
     }
-    uint32_t t = 0;
     for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x)
-        perturb_tail<kThreads, kU, kM>(locate_tail<kTileElems>(tab, t, tl), st);
+        perturb_tail<kThreads, kU, kM>(tile_ref(tiles[n_full + tl]), st);
 }
 
 // The in-place streaming ceiling of a plan (es_stream_pass): every element
@@ -421,15 +417,16 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTensor* _
 // 3 % above the same stream pipelined), so it bounds what any pass over the
 // plan can reach.
 template <int kThreads, int kU>
-__global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTensor* __restrict__ tab,
+__global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              uint32_t flip) {
-    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
-    uint32_t t = 0;
+    TileRef r{};
+    if (blockIdx.x < n_full) r = tile_ref(tiles[blockIdx.x]);
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
-        const TileRef r = locate_full<kTileElems>(tab, t, tile);
         uint32_t raw[kU][4];
         load_tile<kThreads, kU>(r, raw);
+        // the next tile's descriptor, read under this tile's loads
+        DevTile next = tiles[min(tile + gridDim.x, n_full - 1)];
         __builtin_amdgcn_sched_barrier(0);      // all loads issued before the first wait
 #pragma unroll
         for (int u = 0; u < kU; ++u)
@@ -439,21 +436,22 @@ __global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTensor* __
 #pragma unroll
         for (int u = 0; u < kU; ++u) {
             const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            store_group<true, true>(r.data, e, r.numel, raw[u]);
+            store_group<true, true>(r.data, e, r.limit, raw[u]);
         }
+        keep_in_sgprs(next);
+        r = tile_ref(next);
     }
-    t = 0;
     for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x) {
-        const TileRef r = locate_tail<kTileElems>(tab, t, tl);
+        const TileRef r = tile_ref(tiles[n_full + tl]);
 #pragma unroll 1
         for (int u = 0; u < kU; ++u) {
             const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            if (e >= r.numel) break;
+            if (e >= r.limit) break;
             uint32_t raw[4];
-            load_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+            load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
 #pragma unroll
             for (int k = 0; k < 4; ++k) raw[k] ^= flip;
-            store_group<false, true>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+            store_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
         }
     }
 }
@@ -483,18 +481,18 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
     const uint32_t g_hi = static_cast<uint32_t>(r.elem0 >> 35);
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
     uint32_t next[4];
-    if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.numel, next);
+    if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.limit, next);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = e0 + uint64_t(u) * kThreads * kGroupElems;
-        if (!kFast && e >= r.numel) break;
+        if (!kFast && e >= r.limit) break;
         uint32_t raw[4];
         if constexpr (kFast) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) raw[k] = next[k];
-            if (u + 1 < kU) load_group<true, kNT>(r.data, e + uint64_t(kThreads) * kGroupElems, r.numel, next);
+            if (u + 1 < kU) load_group<true, kNT>(r.data, e + uint64_t(kThreads) * kGroupElems, r.limit, next);
         } else {
-            load_group<false, kNT>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+            load_group<false, kNT>(r.data, e, r.limit, raw, r.aligned16 != 0u);
         }
         const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
         float acc[8];
@@ -522,28 +520,24 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
                 out[k] = es::pack_bf16x2(es::bf16_lo(raw[k]) + acc[2 * k],
                                          es::bf16_hi(raw[k]) + acc[2 * k + 1]);
         }
-        store_group<kFast, kNT>(r.data, e, r.numel, out, r.aligned16 != 0u);
+        store_group<kFast, kNT>(r.data, e, r.limit, out, r.aligned16 != 0u);
     }
 }
 
 // Fused update over the whole parameter list (member table and header
 // written by es_prepare_kernel): full tiles, then tail tiles.
 template <int kThreads, int kU, bool kNT, bool kSR>
-__global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTensor* __restrict__ tab,
+__global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              const Member* __restrict__ members,
                                                              const UpdateHeader* __restrict__ hdr,
                                                              RoundKey rk) {
-    constexpr uint64_t kTileElems = uint64_t(kThreads) * kU * kGroupElems;
     if (hdr->n_live == 0u) return;          // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
-    uint32_t t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        update_tile<kThreads, kU, true, kNT, kSR>(locate_full<kTileElems>(tab, t, tile), members,
-                                                  n_distinct, rk);
-    t = 0;
+        update_tile<kThreads, kU, true, kNT, kSR>(tile_ref(tiles[tile]), members, n_distinct, rk);
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        update_tile<kThreads, kU, false, kNT, kSR>(locate_tail<kTileElems>(tab, t, tile), members,
+        update_tile<kThreads, kU, false, kNT, kSR>(tile_ref(tiles[n_full + tile]), members,
                                                    n_distinct, rk);
 }
 
@@ -688,8 +682,8 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
     }
 }
 
-using PerturbKernel = void (*)(const DevTensor*, uint64_t, uint64_t, Streams);
-using UpdateKernel = void (*)(const DevTensor*, uint64_t, uint64_t, const Member*,
+using PerturbKernel = void (*)(const DevTile*, uint64_t, uint64_t, Streams);
+using UpdateKernel = void (*)(const DevTile*, uint64_t, uint64_t, const Member*,
                               const UpdateHeader*, RoundKey);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
@@ -703,7 +697,7 @@ PerturbKernel perturb_kernel_for(int threads, int groups) {
     return nullptr;
 }
 
-using StreamKernel = void (*)(const DevTensor*, uint64_t, uint64_t, uint32_t);
+using StreamKernel = void (*)(const DevTile*, uint64_t, uint64_t, uint32_t);
 
 StreamKernel stream_kernel(int threads, int groups) {
 #define ES_CASE(T, U) if (threads == T && groups == U) return es_stream_kernel<T, U>;
@@ -889,7 +883,7 @@ struct es_plan {
     int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
     int groups = kDefaultGroups;    // 8-element groups per lane per tile
     uint64_t tile_elems = 0;        // threads * groups * 8
-    DevTensor* d_tab = nullptr;     // n_tensors + 1 entries
+    DevTile* d_tiles = nullptr;     // n_full full-tile then n_tail tail-tile descriptors
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
 
@@ -941,8 +935,8 @@ int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double
         st.coef_k[m] = static_cast<float>(coef[m] * kSqrt2Ln2Double);
     }
     const PerturbKernel kernel = perturb_kernel(streams, p->threads, p->groups);
-    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tab, p->n_full,
-                       p->n_tail, st);
+    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tiles,
+                       p->n_full, p->n_tail, st);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_perturb_kernel launch");
     return ES_OK;
@@ -1068,6 +1062,54 @@ int release_device_memory(int device, void* tab, void* scratch, const char* name
     return rc;
 }
 
+// Launch shape of the bf16 tile kernels: the defaults, or overrides for
+// launch-shape sweeps.
+void launch_shape(int& threads, int& groups) {
+    threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
+    groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
+    if (update_kernel(threads, groups, false) == nullptr) {
+        threads = kDefaultThreads;
+        groups = kDefaultGroups;
+    }
+}
+
+// The tiles of one bf16 tensor (see DevTile), appended to `full` and `tail`.
+// Full tiles start where the address is a multiple of the tile's byte size
+// (the tensor's base is 16-byte aligned, so such an element index is a
+// multiple of 8 and groups keep their Philox quads); the elements before the
+// first one and after the last one are tail tiles.  Every tile keeps its
+// counter's high word uniform: a tile that would cross a multiple of 2^34
+// elements is split there into tail tiles.
+void tile_tensor(uint16_t* data, uint64_t numel, uint32_t tensor_id, uint64_t tile_elems,
+                 std::vector<DevTile>& full, std::vector<DevTile>& tail) {
+    if (numel == 0) return;
+    constexpr uint64_t kHiBlock = uint64_t(1) << 34;      // elements per counter high word
+    auto add_tail = [&](uint64_t e0, uint64_t e1, uint32_t aligned) {
+        while (e0 < e1) {                                   // split at high-word boundaries
+            const uint64_t cut = std::min(e1, (e0 / kHiBlock + 1) * kHiBlock);
+            tail.push_back(DevTile{data, e0, cut, tensor_id, aligned});
+            e0 = cut;
+        }
+    };
+    const uintptr_t a = reinterpret_cast<uintptr_t>(data);
+    if (a % 16 != 0) {                                      // element-wise accesses throughout
+        for (uint64_t e0 = 0; e0 < numel; e0 += tile_elems)
+            add_tail(e0, std::min(numel, e0 + tile_elems), 0u);
+        return;
+    }
+    const uint64_t tile_bytes = 2 * tile_elems;
+    const uint64_t head = std::min<uint64_t>(numel, ((tile_bytes - a % tile_bytes) % tile_bytes) / 2);
+    add_tail(0, head, 1u);
+    uint64_t e0 = head;
+    for (; e0 + tile_elems <= numel; e0 += tile_elems) {
+        if (e0 / kHiBlock != (e0 + tile_elems - 1) / kHiBlock)
+            add_tail(e0, e0 + tile_elems, 1u);
+        else
+            full.push_back(DevTile{data, e0, e0 + tile_elems, tensor_id, 1u});
+    }
+    add_tail(e0, numel, 1u);
+}
+
 int current_device(int* dev) {
     const hipError_t e = hipGetDevice(dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
@@ -1179,18 +1221,12 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null tensor list");
     if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
         return fail(ES_ERR_INVALID_ARG, "es_plan_create: n_tensors out of range");
-    // Launch shape: the defaults, or overrides for launch-shape sweeps.
-    int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
-    int groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
-    if (update_kernel(threads, groups, false) == nullptr) {
-        threads = kDefaultThreads;
-        groups = kDefaultGroups;
-    }
+    int threads = 0, groups = 0;
+    launch_shape(threads, groups);
     const uint64_t tile_elems = uint64_t(threads) * groups * kGroupElems;
-    std::vector<DevTensor> tab(n_tensors + 1);
     std::unordered_map<uint32_t, uint32_t> ids;
     std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
-    uint64_t n_full = 0, n_tail = 0, numel = 0;
+    uint64_t numel = 0;
     for (uint32_t i = 0; i < n_tensors; ++i) {
         const es_tensor_t& t = tensors[i];
         const std::string where = "es_plan_create: tensor " + std::to_string(i);
@@ -1201,21 +1237,13 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         if (t.numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, where + ": numel too large");
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
         if (t.numel > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
-        // full tiles need a 16-byte aligned base; the rest are tail tiles
-        const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
-        const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
-        tab[i] = DevTensor{static_cast<uint16_t*>(t.data), t.numel, n_full, n_tail, t.tensor_id,
-                           n_tensors, (a % 16 == 0) ? 1u : 0u, 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
-        n_full += full;
-        n_tail += tail;
         numel += t.numel;
     }
     std::sort(ranges.begin(), ranges.end());
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_plan_create: tensors overlap in memory");
-    tab[n_tensors] = DevTensor{nullptr, 0, n_full, n_tail, 0xFFFFFFFFu, n_tensors, 0u, 0u};   // sentinel
 
     int device = -1;
     int rc = current_device(&device);
@@ -1224,6 +1252,14 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         rc = check_access(tensors[i].data, 2 * tensors[i].numel, device,
                           "es_plan_create: tensor " + std::to_string(i));
     if (rc != ES_OK) return rc;
+    // the tile descriptors (built after the accesses are known to be valid:
+    // every tensor lies inside one device allocation)
+    std::vector<DevTile> tiles, tail;
+    for (uint32_t i = 0; i < n_tensors; ++i)
+        tile_tensor(static_cast<uint16_t*>(tensors[i].data), tensors[i].numel,
+                    tensors[i].tensor_id, tile_elems, tiles, tail);
+    const uint64_t n_full = tiles.size(), n_tail = tail.size();
+    tiles.insert(tiles.end(), tail.begin(), tail.end());
     es_plan_t* p = new (std::nothrow) es_plan_t;
     if (p == nullptr) return fail(ES_ERR_NOMEM, "es_plan_create: host allocation");
     p->device = device;
@@ -1243,21 +1279,23 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
     p->grid_perturb = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_perturb));
     p->grid_update = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_update));
-    e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(DevTensor) * tab.size());
+    const size_t tile_bytes = sizeof(DevTile) * std::max<size_t>(tiles.size(), 1);
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_tiles), tile_bytes);
     if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
     e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
     if (e != hipSuccess) {
-        (void)hipFree(p->d_tab);
+        (void)hipFree(p->d_tiles);
         delete p;
         return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
     }
-    e = hipMemcpy(p->d_tab, tab.data(), sizeof(DevTensor) * tab.size(), hipMemcpyHostToDevice);
+    if (!tiles.empty())
+        e = hipMemcpy(p->d_tiles, tiles.data(), sizeof(DevTile) * tiles.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
     if (e != hipSuccess) {
-        (void)hipFree(p->d_tab);
+        (void)hipFree(p->d_tiles);
         (void)hipFree(p->d_scratch);
         delete p;
-        return hip_fail(e, "es_plan_create: table upload");
+        return hip_fail(e, "es_plan_create: tile table upload");
     }
     *out = p;
     return ES_OK;
@@ -1265,7 +1303,7 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
 
 int es_plan_destroy(es_plan_t* plan) {
     if (plan == nullptr) return ES_OK;
-    const int rc = release_device_memory(plan->device, plan->d_tab, plan->d_scratch,
+    const int rc = release_device_memory(plan->device, plan->d_tiles, plan->d_scratch,
                                          "es_plan_destroy");
     delete plan;
     return rc;
@@ -1274,7 +1312,9 @@ int es_plan_destroy(es_plan_t* plan) {
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
 
 uint64_t es_plan_device_bytes(const es_plan_t* plan) {
-    return plan ? sizeof(DevTensor) * (plan->n_tensors + 1) + kScratchBytes : 0;
+    return plan ? sizeof(DevTile) * std::max<uint64_t>(plan->n_full + plan->n_tail, 1) +
+                      kScratchBytes
+                : 0;
 }
 uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_full + plan->n_tail : 0; }
 
@@ -1326,7 +1366,7 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
     const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
                       static_cast<uint32_t>(opts->round_seed >> 32)};
     const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
-    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tab,
+    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tiles,
                        plan->n_full, plan->n_tail,
                        reinterpret_cast<const Member*>(plan->d_scratch + kOffMembers),
                        reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffHeader), rk);
@@ -1520,7 +1560,7 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
     if (rc != ES_OK) return rc;
     if (plan->n_full + plan->n_tail == 0) return ES_OK;
     hipLaunchKernelGGL(stream_kernel(plan->threads, plan->groups), dim3(plan->grid_perturb),
-                       dim3(plan->threads), 0, static_cast<hipStream_t>(stream), plan->d_tab,
+                       dim3(plan->threads), 0, static_cast<hipStream_t>(stream), plan->d_tiles,
                        plan->n_full, plan->n_tail, 0u);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
@@ -1570,6 +1610,27 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, fl
                        static_cast<uint32_t>(seed >> 32), tensor_id, elem0, n, out_dev);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_normals_kernel launch");
+    return ES_OK;
+}
+
+int es_tile_layout(uint64_t addr, uint64_t numel, es_tile_info_t* out, uint64_t cap,
+                   uint64_t* n_tiles) {
+    if (n_tiles == nullptr) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: null n_tiles");
+    *n_tiles = 0;
+    if (numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: numel too large");
+    if (cap > 0 && out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: null output");
+    if (numel > 0 && (addr & 1u)) return fail(ES_ERR_ALIGN, "es_tile_layout: address not 2-byte aligned");
+    int threads = 0, groups = 0;
+    launch_shape(threads, groups);
+    std::vector<DevTile> full, tail;
+    tile_tensor(reinterpret_cast<uint16_t*>(static_cast<uintptr_t>(addr)), numel, 0u,
+                uint64_t(threads) * groups * kGroupElems, full, tail);
+    const uint64_t n = full.size() + tail.size();
+    for (uint64_t i = 0; i < std::min(cap, n); ++i) {
+        const DevTile& d = i < full.size() ? full[i] : tail[i - full.size()];
+        out[i] = es_tile_info_t{d.elem0, d.limit, i < full.size() ? 1u : 0u, d.aligned16};
+    }
+    *n_tiles = n;
     return ES_OK;
 }
 

@@ -46,6 +46,10 @@ class EsQTensor(ctypes.Structure):
                 ("tensor_id", _u32)]
 
 
+class EsTileInfo(ctypes.Structure):
+    _fields_ = [("elem0", _u64), ("end", _u64), ("full", _u32), ("aligned16", _u32)]
+
+
 class EsUpdateOpts(ctypes.Structure):
     _fields_ = [("alpha", _f32), ("sigma", _f32), ("zscore_eps", _f32), ("flags", _u32),
                 ("round_seed", _u64)]
@@ -75,6 +79,8 @@ SIGNATURES = {
     "es_sigma_cosine": (_f64, [_f64, _f64, _u32, _u32]),
     "es_philox_words": (ctypes.c_int, [_u64, _u32, _u32, _u64, _u64, _vp, _vp]),
     "es_normals": (ctypes.c_int, [_u64, _u32, _u64, _u64, _vp, _vp]),
+    "es_tile_layout": (ctypes.c_int, [_u64, _u64, ctypes.POINTER(EsTileInfo), _u64,
+                                      ctypes.POINTER(_u64)]),
     "es_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "es_last_error": (ctypes.c_char_p, []),
 }
@@ -369,6 +375,20 @@ def philox_words(seed, tensor_id, quad0, n_quads, domain=0, device="cuda", strea
                                   _u64_arg(n_quads, "n_quads"), ctypes.c_void_p(out.data_ptr()),
                                   _stream(stream)), "es_philox_words")
     return out
+
+
+def tile_layout(addr, numel):
+    """The tiles a plan lays out for one bf16 tensor of `numel` elements at
+    device address `addr` (host-side tiling only; nothing is accessed):
+    a list of (elem0, end, full, aligned16), full tiles first."""
+    lib = load()
+    n = _u64(0)
+    _check(lib.es_tile_layout(_u64_arg(addr, "addr"), _u64_arg(numel, "numel"), None, 0,
+                              ctypes.byref(n)), "es_tile_layout")
+    out = (EsTileInfo * max(n.value, 1))()
+    _check(lib.es_tile_layout(int(addr), int(numel), out, n.value, ctypes.byref(n)),
+           "es_tile_layout")
+    return [(t.elem0, t.end, t.full, t.aligned16) for t in out[:n.value]]
 
 
 def normals(seed, tensor_id, elem0, n, device="cuda", stream=None):

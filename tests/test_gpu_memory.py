@@ -1,6 +1,6 @@
 """Memory stays at inference level (Section 3: only seeds are stored, the
-noise is regenerated): a plan costs its small tensor table and member scratch
-whatever the parameter count, and no pass allocates device memory.  Device
+noise is regenerated): a plan costs its member scratch and 32 bytes per 128 KB
+tile of parameters, and no pass allocates device memory.  Device
 free memory is read from the driver (the library allocates with hipMalloc,
 outside PyTorch's allocator)."""
 import numpy as np
@@ -50,9 +50,14 @@ def test_plans_and_passes_allocate_no_parameter_sized_memory():
     qplan = esopt.QPlan(codes, scales, [4096, 4096])
     f1 = _free()
     print("plans took", (f0 - f1) / MB, "MiB")
-    # what the plans report: a table entry per tensor plus the member scratch
-    assert plan.device_bytes < 64 * 1024 and qplan.device_bytes < 64 * 1024
-    assert qplan.device_bytes - plan.device_bytes == 64 * (len(codes) + 1) - 48 * (len(params) + 1)
+    # what the plans report: the member scratch plus, for the int8 plan, a
+    # table entry per tensor and, for the bf16 plan, a 32-byte descriptor per
+    # tile (65 536 elements)
+    assert qplan.device_bytes < 64 * 1024
+    scratch = qplan.device_bytes - 64 * (len(codes) + 1)
+    assert plan.device_bytes == 32 * plan.tiles + scratch
+    assert plan.tiles <= sum(-(-p.numel() // 65536) + 1 for p in params)
+    assert plan.device_bytes < 512 * 1024                   # for 1 GiB of parameters
     assert f0 - f1 <= 8 * MB                      # tables + scratch, allocation granularity
     seen = []
     for rep in range(3):
