@@ -11,19 +11,19 @@
 // Layout and launch shape:
 //   * A plan cuts every tensor into tiles of T x U x 8 elements (T lanes per
 //     workgroup, U 8-element groups per lane; by default 1024 x 8 x 8 =
-//     65536 elements, 128 KB) and numbers the full tiles of all tensors
-//     consecutively, then the tail tiles (partial or unaligned).  One launch
-//     covers the whole parameter list: a grid of (CUs x WGs-per-CU)
-//     workgroups strides over the full tiles, then the tails.  Each workgroup
-//     keeps the index of its current tensor in a scalar register and
-//     advances it through a small tensor table read with scalar loads, so a
-//     tile's tensor, address and noise identity are wave-uniform.
+//     65536 elements, 128 KB): full tiles on tile-sized boundaries of the
+//     address space, then tail tiles (each tensor's head and remainder, or
+//     every tile of an unaligned tensor), each described by a 32-byte
+//     descriptor.  One launch covers the whole parameter list: a grid of
+//     (CUs x WGs-per-CU) workgroups strides over the full tiles, then the
+//     tails, reading one descriptor per tile with a scalar load, so a tile's
+//     tensor, address and noise identity are wave-uniform.
 //   * Within a tile, lane l of group slot u owns elements
-//     8 (u * T + l) .. +7: one 16-byte load and one 16-byte store, 64 lanes
-//     covering 1 KB contiguous per instruction.  Its two Philox calls are
-//     the quads 2 g and 2 g + 1 of that group; since tiles start at
-//     multiples of a power-of-two tile size, the counter's high word is
-//     uniform per tile.
+//     elem0 + 8 (u * T + l) .. +7: one 16-byte load and one 16-byte store, 64
+//     lanes covering 1 KB contiguous per instruction.  Its two Philox calls
+//     are the quads 2 g and 2 g + 1 of that group (tiles start at multiples
+//     of 8 elements); no tile crosses a multiple of 2^34 elements, so the
+//     counter's high word is uniform per tile.
 //   * Perturb is HBM-bound: one 1024-lane workgroup per CU streams 128 KB
 //     tiles; the loads of its next tile are issued before the current tile's
 //     arithmetic (software pipelining), and each tile's stores leave in one
@@ -33,16 +33,17 @@
 //     load in flight.  Both shapes were chosen by sweeping on MI355X.  Swap
 //     is the perturb kernel with two streams and a bf16 rounding between
 //     them.
-//   * The int8 path (es_quant.hpp) has its own table and tiles of 16-code
-//     groups; all its passes are VALU-bound and use the update's shape.
+//   * The int8 path (es_quant.hpp) has a tensor table searched per tile and
+//     tiles of 16-code groups; all its passes are VALU-bound and use the
+//     update's shape.
 //   * Perturb/restore read and write each parameter once (4 bytes of HBM
 //     traffic per parameter).  The update regenerates the noise of all
 //     distinct member seeds for the same 8 elements in registers,
 //     accumulates sum_d w_d eps_d in binary32, and then does the single
 //     read-modify-write, so its HBM traffic does not depend on N.
-//   * Tiles that are partial (tensor tails) or belong to a tensor whose
-//     address is not 16-byte aligned take a bounds-checked 2-byte path with
-//     identical arithmetic.
+//   * Tail tiles take a bounds-checked path with identical arithmetic:
+//     16-byte accesses for whole groups of an aligned tensor, 2-byte accesses
+//     for a partial group or an unaligned tensor.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -1034,7 +1035,7 @@ int check_access(const void* p, uint64_t bytes, int device, const std::string& w
     return ES_OK;
 }
 
-// Free a plan's table and scratch on the plan's device: that device is made
+// Free a plan's tile table and scratch on the plan's device: that device is made
 // current for the call (the caller's is restored) and synchronised first, so
 // no queued launch still reads them.  Every step runs; the first error is
 // returned.
