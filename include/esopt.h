@@ -213,8 +213,9 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
  * binary32 scales: theta_j = s_r q_j, r = j / row (row == 0: one scale for
  * the tensor).  Every pass moves codes by an integer offset k_j, the step d_j
  * in quanta rounded stochastically (E[k_j] = d_j), and clamps:
- * q_j <- clamp(q_j +- k_j, -127, 127).  Elements whose scale is not a normal
- * positive finite binary32 value are left unchanged. */
+ * q_j <- clamp(q_j +- k_j, -127, 127) (so a code of -128 is clamped into the
+ * range).  Elements whose scale is not a normal positive finite binary32
+ * value are left unchanged, -128 included. */
 typedef struct es_qtensor {
     void*        data;       /* device int8 codes, contiguous; any alignment
                                 (16-byte aligned data takes the vector path) */
