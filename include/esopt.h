@@ -84,12 +84,17 @@ typedef void* es_stream_t;          /* hipStream_t */
  * `data` (2-byte aligned; 16-byte alignment takes the vector path).
  * `tensor_id` is the tensor's noise identity (counter word 2) and must be
  * unique within a plan and stable across calls; the list index is the usual
- * choice.  `reserved` must be 0.  numel may be 0 (the tensor is skipped). */
+ * choice.  numel may be 0 (the tensor is skipped).
+ * `offset8` places a shard: element i of `data` carries the noise of element
+ * 8 * offset8 + i of the whole tensor `tensor_id`, so a shard holding a
+ * contiguous range of a tensor (a row-parallel slice, a flat-parameter
+ * shard) regenerates exactly the whole tensor's noise there, with no
+ * communication.  0 for a tensor that is not sharded. */
 typedef struct es_tensor {
     void*    data;
     uint64_t numel;
     uint32_t tensor_id;
-    uint32_t reserved;
+    uint32_t offset8;
 } es_tensor_t;
 
 /* Opaque plan: the tensor list laid out as tiles for one launch per pass,
@@ -99,8 +104,8 @@ typedef struct es_plan es_plan_t;
 /* Build a plan over `n_tensors` tensors (1 .. ES_MAX_TENSORS) on the current
  * device.  Copies the list; does not touch the tensors' values.  Errors:
  * INVALID_ARG for a null pointer, n_tensors out of range, duplicate
- * tensor_id, nonzero reserved field, null data with numel > 0, or tensors
- * whose byte ranges overlap; ALIGN for odd addresses; NOMEM / HIP for
+ * tensor_id, null data with numel > 0, 8 * offset8 + numel above 2^60, or
+ * tensors whose byte ranges overlap; ALIGN for odd addresses; NOMEM / HIP for
  * allocation failures.  On success *out owns 32 bytes of device memory per
  * tile of 65 536 elements (0.024 % of the parameter bytes; see
  * es_tile_layout) and ~42 KB of scratch, freed by es_plan_destroy;
@@ -285,20 +290,22 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n,
 
 /* Test hook of the host-side tiling (no device access; the address is never
  * dereferenced): the tiles es_plan_create lays out for one bf16 tensor of
- * `numel` elements at address `addr`, with the plan's launch shape.  Tile i
- * covers elements [elem0, end) of the tensor; full tiles come first (full =
- * 1: tile-sized, starting where the address is a multiple of the tile's byte
- * size), then tail tiles.  Writes min(cap, count) entries to `out` (which may
- * be NULL when cap is 0) and the count to *n_tiles.  Errors: INVALID_ARG for
- * a null n_tiles, numel > 2^60 or an odd address (ALIGN). */
+ * `numel` elements at address `addr` with shard offset `offset8`, with the
+ * plan's launch shape.  Tile i covers elements [elem0, end) of the whole
+ * tensor (8 * offset8 onwards); full tiles come first (full = 1:
+ * tile-sized, starting where the address is a multiple of the tile's byte
+ * size), then tail tiles.  Writes min(cap, count) entries to `out` (which
+ * may be NULL when cap is 0) and the count to *n_tiles.  Errors: INVALID_ARG
+ * for a null n_tiles or 8 * offset8 + numel > 2^60, ALIGN for an odd
+ * address. */
 typedef struct es_tile_info {
     uint64_t elem0;
     uint64_t end;
     uint32_t full;
     uint32_t aligned16;
 } es_tile_info_t;
-int es_tile_layout(uint64_t addr, uint64_t numel, es_tile_info_t* out, uint64_t cap,
-                   uint64_t* n_tiles);
+int es_tile_layout(uint64_t addr, uint64_t numel, uint32_t offset8, es_tile_info_t* out,
+                   uint64_t cap, uint64_t* n_tiles);
 
 /* Static name of an error code; detail of the calling thread's last error. */
 const char* es_strerror(int code);

@@ -1078,17 +1078,28 @@ void launch_shape(int& threads, int& groups) {
 // Full tiles start where the address is a multiple of the tile's byte size
 // (the tensor's base is 16-byte aligned, so such an element index is a
 // multiple of 8 and groups keep their Philox quads); the elements before the
-// first one and after the last one are tail tiles.  Every tile keeps its
-// counter's high word uniform: a tile that would cross a multiple of 2^34
-// elements is split there into tail tiles.
-void tile_tensor(uint16_t* data, uint64_t numel, uint32_t tensor_id, uint64_t tile_elems,
-                 std::vector<DevTile>& full, std::vector<DevTile>& tail) {
+// first one and after the last one are tail tiles.  A shard (`offset`
+// elements into its whole tensor, a multiple of 8) is tiled by address the
+// same way, but its descriptors count elements of the whole tensor: elem0
+// and limit are offset, and the base is moved back by as many elements, so
+// base + element is still the address and the element is the noise index.
+// Every tile keeps its counter's high word uniform: a tile that would cross
+// a multiple of 2^34 elements of the whole tensor is split there into tail
+// tiles.
+void tile_tensor(uint16_t* data, uint64_t numel, uint64_t offset, uint32_t tensor_id,
+                 uint64_t tile_elems, std::vector<DevTile>& full, std::vector<DevTile>& tail) {
     if (numel == 0) return;
     constexpr uint64_t kHiBlock = uint64_t(1) << 34;      // elements per counter high word
-    auto add_tail = [&](uint64_t e0, uint64_t e1, uint32_t aligned) {
+    // base - offset, as an address: the kernels only ever add an element
+    // index of at least `offset` to it
+    uint16_t* const base =
+        reinterpret_cast<uint16_t*>(reinterpret_cast<uintptr_t>(data) - 2 * offset);
+    auto add_tail = [&](uint64_t e0, uint64_t e1, uint32_t aligned) {   // local indices
+        e0 += offset;
+        e1 += offset;
         while (e0 < e1) {                                   // split at high-word boundaries
             const uint64_t cut = std::min(e1, (e0 / kHiBlock + 1) * kHiBlock);
-            tail.push_back(DevTile{data, e0, cut, tensor_id, aligned});
+            tail.push_back(DevTile{base, e0, cut, tensor_id, aligned});
             e0 = cut;
         }
     };
@@ -1103,10 +1114,11 @@ void tile_tensor(uint16_t* data, uint64_t numel, uint32_t tensor_id, uint64_t ti
     add_tail(0, head, 1u);
     uint64_t e0 = head;
     for (; e0 + tile_elems <= numel; e0 += tile_elems) {
-        if (e0 / kHiBlock != (e0 + tile_elems - 1) / kHiBlock)
+        const uint64_t g0 = offset + e0;
+        if (g0 / kHiBlock != (g0 + tile_elems - 1) / kHiBlock)
             add_tail(e0, e0 + tile_elems, 1u);
         else
-            full.push_back(DevTile{data, e0, e0 + tile_elems, tensor_id, 1u});
+            full.push_back(DevTile{base, g0, g0 + tile_elems, tensor_id, 1u});
     }
     add_tail(e0, numel, 1u);
 }
@@ -1231,11 +1243,11 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     for (uint32_t i = 0; i < n_tensors; ++i) {
         const es_tensor_t& t = tensors[i];
         const std::string where = "es_plan_create: tensor " + std::to_string(i);
-        if (t.reserved != 0) return fail(ES_ERR_INVALID_ARG, where + ": reserved field must be 0");
         if (!ids.emplace(t.tensor_id, i).second)
             return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
         if (t.numel > 0 && t.data == nullptr) return fail(ES_ERR_INVALID_ARG, where + ": null data");
-        if (t.numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, where + ": numel too large");
+        if (t.numel > (uint64_t(1) << 60) - 8 * uint64_t(t.offset8))
+            return fail(ES_ERR_INVALID_ARG, where + ": 8 * offset8 + numel above 2^60");
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
         if (t.numel > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
         if (t.numel > 0) ranges.emplace_back(a, a + 2 * t.numel);
@@ -1258,7 +1270,8 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     std::vector<DevTile> tiles, tail;
     for (uint32_t i = 0; i < n_tensors; ++i)
         tile_tensor(static_cast<uint16_t*>(tensors[i].data), tensors[i].numel,
-                    tensors[i].tensor_id, tile_elems, tiles, tail);
+                    8 * uint64_t(tensors[i].offset8), tensors[i].tensor_id, tile_elems, tiles,
+                    tail);
     const uint64_t n_full = tiles.size(), n_tail = tail.size();
     tiles.insert(tiles.end(), tail.begin(), tail.end());
     es_plan_t* p = new (std::nothrow) es_plan_t;
@@ -1614,18 +1627,19 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, fl
     return ES_OK;
 }
 
-int es_tile_layout(uint64_t addr, uint64_t numel, es_tile_info_t* out, uint64_t cap,
-                   uint64_t* n_tiles) {
+int es_tile_layout(uint64_t addr, uint64_t numel, uint32_t offset8, es_tile_info_t* out,
+                   uint64_t cap, uint64_t* n_tiles) {
     if (n_tiles == nullptr) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: null n_tiles");
     *n_tiles = 0;
-    if (numel > (uint64_t(1) << 60)) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: numel too large");
+    if (numel > (uint64_t(1) << 60) - 8 * uint64_t(offset8))
+        return fail(ES_ERR_INVALID_ARG, "es_tile_layout: 8 * offset8 + numel above 2^60");
     if (cap > 0 && out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: null output");
     if (numel > 0 && (addr & 1u)) return fail(ES_ERR_ALIGN, "es_tile_layout: address not 2-byte aligned");
     int threads = 0, groups = 0;
     launch_shape(threads, groups);
     std::vector<DevTile> full, tail;
-    tile_tensor(reinterpret_cast<uint16_t*>(static_cast<uintptr_t>(addr)), numel, 0u,
-                uint64_t(threads) * groups * kGroupElems, full, tail);
+    tile_tensor(reinterpret_cast<uint16_t*>(static_cast<uintptr_t>(addr)), numel,
+                8 * uint64_t(offset8), 0u, uint64_t(threads) * groups * kGroupElems, full, tail);
     const uint64_t n = full.size() + tail.size();
     for (uint64_t i = 0; i < std::min(cap, n); ++i) {
         const DevTile& d = i < full.size() ? full[i] : tail[i - full.size()];

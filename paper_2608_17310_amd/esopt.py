@@ -38,7 +38,7 @@ _vp = ctypes.c_void_p
 
 
 class EsTensor(ctypes.Structure):
-    _fields_ = [("data", _vp), ("numel", _u64), ("tensor_id", _u32), ("reserved", _u32)]
+    _fields_ = [("data", _vp), ("numel", _u64), ("tensor_id", _u32), ("offset8", _u32)]
 
 
 class EsQTensor(ctypes.Structure):
@@ -79,7 +79,7 @@ SIGNATURES = {
     "es_sigma_cosine": (_f64, [_f64, _f64, _u32, _u32]),
     "es_philox_words": (ctypes.c_int, [_u64, _u32, _u32, _u64, _u64, _vp, _vp]),
     "es_normals": (ctypes.c_int, [_u64, _u32, _u64, _u64, _vp, _vp]),
-    "es_tile_layout": (ctypes.c_int, [_u64, _u64, ctypes.POINTER(EsTileInfo), _u64,
+    "es_tile_layout": (ctypes.c_int, [_u64, _u64, _u32, ctypes.POINTER(EsTileInfo), _u64,
                                       ctypes.POINTER(_u64)]),
     "es_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "es_last_error": (ctypes.c_char_p, []),
@@ -161,11 +161,14 @@ def _dev_ptr(t, dtype, what):
 class Plan:
     """A list of bf16 parameter tensors prepared for single-launch passes.
 
-    tensor_ids defaults to the list index.  The plan holds references to the
-    tensors so their storage stays alive and in place while it exists.
+    tensor_ids defaults to the list index.  offsets (multiples of 8, default
+    0) place shards: element i of tensors[k] carries the noise of element
+    offsets[k] + i of the whole tensor tensor_ids[k].  The plan holds
+    references to the tensors so their storage stays alive and in place
+    while it exists.
     """
 
-    def __init__(self, tensors, tensor_ids=None):
+    def __init__(self, tensors, tensor_ids=None, offsets=None):
         tensors = list(tensors)
         if not tensors:
             raise ValueError("empty tensor list")
@@ -173,11 +176,14 @@ class Plan:
                else [_u32_arg(i, "tensor_id") for i in tensor_ids])
         if len(ids) != len(tensors):
             raise ValueError("tensor_ids must match tensors")
+        offs = [0] * len(tensors) if offsets is None else [_offset8(o) for o in offsets]
+        if len(offs) != len(tensors):
+            raise ValueError("offsets must match tensors")
         arr = (EsTensor * len(tensors))()
-        for i, (t, tid) in enumerate(zip(tensors, ids)):
+        for i, (t, tid, o8) in enumerate(zip(tensors, ids, offs)):
             if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
                 raise ValueError(f"tensor {i} must be a contiguous bf16 CUDA tensor")
-            arr[i] = EsTensor(t.data_ptr() if t.numel() else None, t.numel(), tid, 0)
+            arr[i] = EsTensor(t.data_ptr() if t.numel() else None, t.numel(), tid, o8)
         self._tensors = tensors
         self.tensor_ids = ids
         self.device = tensors[0].device
@@ -377,18 +383,29 @@ def philox_words(seed, tensor_id, quad0, n_quads, domain=0, device="cuda", strea
     return out
 
 
-def tile_layout(addr, numel):
+def tile_layout(addr, numel, offset=0):
     """The tiles a plan lays out for one bf16 tensor of `numel` elements at
-    device address `addr` (host-side tiling only; nothing is accessed):
-    a list of (elem0, end, full, aligned16), full tiles first."""
+    device address `addr`, a shard starting `offset` elements into its whole
+    tensor (host-side tiling only; nothing is accessed): a list of
+    (elem0, end, full, aligned16) in elements of the whole tensor, full
+    tiles first."""
     lib = load()
     n = _u64(0)
-    _check(lib.es_tile_layout(_u64_arg(addr, "addr"), _u64_arg(numel, "numel"), None, 0,
+    off8 = _offset8(offset)
+    _check(lib.es_tile_layout(_u64_arg(addr, "addr"), _u64_arg(numel, "numel"), off8, None, 0,
                               ctypes.byref(n)), "es_tile_layout")
     out = (EsTileInfo * max(n.value, 1))()
-    _check(lib.es_tile_layout(int(addr), int(numel), out, n.value, ctypes.byref(n)),
+    _check(lib.es_tile_layout(int(addr), int(numel), off8, out, n.value, ctypes.byref(n)),
            "es_tile_layout")
     return [(t.elem0, t.end, t.full, t.aligned16) for t in out[:n.value]]
+
+
+def _offset8(offset):
+    """A shard's element offset in units of 8 elements (the ABI's offset8)."""
+    v = int(offset)
+    if v < 0 or v % 8 or v // 8 >= (1 << 32):
+        raise ValueError(f"shard offset must be a multiple of 8 in [0, 2^35), got {v}")
+    return v // 8
 
 
 def normals(seed, tensor_id, elem0, n, device="cuda", stream=None):

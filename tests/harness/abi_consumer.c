@@ -9,9 +9,9 @@
 #include "esopt.h"
 
 int main(void) {
-    printf("es_tensor_t %zu data %zu numel %zu tensor_id %zu reserved %zu\n", sizeof(es_tensor_t),
+    printf("es_tensor_t %zu data %zu numel %zu tensor_id %zu offset8 %zu\n", sizeof(es_tensor_t),
            offsetof(es_tensor_t, data), offsetof(es_tensor_t, numel),
-           offsetof(es_tensor_t, tensor_id), offsetof(es_tensor_t, reserved));
+           offsetof(es_tensor_t, tensor_id), offsetof(es_tensor_t, offset8));
     printf("es_qtensor_t %zu data %zu scales %zu numel %zu row %zu tensor_id %zu\n",
            sizeof(es_qtensor_t), offsetof(es_qtensor_t, data), offsetof(es_qtensor_t, scales),
            offsetof(es_qtensor_t, numel), offsetof(es_qtensor_t, row),

@@ -59,8 +59,8 @@ def test_plan_create_validation(lib):
     assert rc == esopt.ES_ERR_INVALID_ARG and "n_tensors" in msg
     rc, msg = _create(lib, [(0x1000, 10, 0, 0), (0x2000, 10, 0, 0)])
     assert rc == esopt.ES_ERR_INVALID_ARG and "duplicate" in msg
-    rc, msg = _create(lib, [(0x1000, 10, 0, 7)])
-    assert rc == esopt.ES_ERR_INVALID_ARG and "reserved" in msg
+    rc, msg = _create(lib, [(0x1000, (1 << 60) - 8 * 7 + 1, 0, 7)])
+    assert rc == esopt.ES_ERR_INVALID_ARG and "offset8" in msg
     rc, msg = _create(lib, [(None, 10, 0, 0)])
     assert rc == esopt.ES_ERR_INVALID_ARG and "null data" in msg
     rc, msg = _create(lib, [(0x1001, 10, 0, 0)])

@@ -3,8 +3,9 @@ access): every element of a tensor lies in exactly one tile, full tiles are
 tile-sized and start on a tile-sized boundary of the address space, every tile
 starts on an 8-element group and keeps its Philox counter's high word (element
 index >> 34) constant, and a tensor whose base is not 16-byte aligned has only
-tail tiles.  These are the invariants the kernels rely on for bit-identical
-noise whatever the layout."""
+tail tiles; a shard's tiles carry the whole tensor's element numbers.  These
+are the invariants the kernels rely on for bit-identical noise whatever the
+layout."""
 import numpy as np
 import pytest
 
@@ -14,8 +15,10 @@ TILE = 1024 * 8 * 8            # default launch shape: 1024 lanes x 8 groups x 8
 HI = 1 << 34
 
 
-def _check(addr, numel):
-    tiles = esopt.tile_layout(addr, numel)
+def _check(addr, numel, offset=0):
+    """Invariants of one tensor's tiles; elements are numbered in the whole
+    tensor, the shard starting `offset` elements into it."""
+    tiles = esopt.tile_layout(addr, numel, offset)
     if numel == 0:
         assert tiles == []
         return tiles
@@ -23,7 +26,7 @@ def _check(addr, numel):
     tail = [t for t in tiles if not t[2]]
     assert tiles == full + tail                        # full tiles first
     spans = sorted((t[0], t[1]) for t in tiles)
-    assert spans[0][0] == 0 and spans[-1][1] == numel
+    assert spans[0][0] == offset and spans[-1][1] == offset + numel
     for (a0, a1), (b0, b1) in zip(spans, spans[1:]):
         assert a1 == b0                                # disjoint, no gap
     for e0, e1, is_full, aligned in tiles:
@@ -33,7 +36,8 @@ def _check(addr, numel):
         assert aligned == (1 if addr % 16 == 0 else 0)
         if is_full:
             assert e1 - e0 == TILE
-            assert (addr + 2 * e0) % (2 * TILE) == 0   # on a tile-sized address boundary
+            # on a tile-sized boundary of the address space (the shard's own addresses)
+            assert (addr + 2 * (e0 - offset)) % (2 * TILE) == 0
     if addr % 16:
         assert not full
     return tiles
@@ -71,10 +75,26 @@ def test_tiles_split_at_the_counter_high_word():
     assert any(t[1] == HI for t in tiles)
 
 
+@pytest.mark.parametrize("offset", [8, 5120 * 640, 65536 * 3 + 8, (1 << 34) - 65536 * 2 + 40])
+@pytest.mark.parametrize("addr", [0x10000000, 0x10000000 + 2048, 0x10000000 + 2])
+def test_shard_tiles_use_the_whole_tensors_element_numbers(addr, offset):
+    # a row shard of a [5120, 5120] matrix, and shards near 2^34 elements of
+    # their whole tensor: tiles are placed by the shard's own addresses, and
+    # still never straddle a multiple of 2^34 elements of the whole tensor
+    tiles = _check(addr, 5120 * 640 + 24, offset)
+    whole = offset + 5120 * 640 + 24
+    if offset < (1 << 34) < whole:
+        assert any(t[0] == 1 << 34 for t in tiles)
+
+
 def test_validation():
     lib = esopt.load()
     n = esopt._u64(0)
-    assert lib.es_tile_layout(3, 10, None, 0, esopt.ctypes.byref(n)) == esopt.ES_ERR_ALIGN
-    assert lib.es_tile_layout(2, 10, None, 0, None) == esopt.ES_ERR_INVALID_ARG
-    assert lib.es_tile_layout(2, (1 << 60) + 1, None, 0, esopt.ctypes.byref(n)) == esopt.ES_ERR_INVALID_ARG
-    assert lib.es_tile_layout(2, 10, None, 5, esopt.ctypes.byref(n)) == esopt.ES_ERR_INVALID_ARG
+    br = esopt.ctypes.byref
+    assert lib.es_tile_layout(3, 10, 0, None, 0, br(n)) == esopt.ES_ERR_ALIGN
+    assert lib.es_tile_layout(2, 10, 0, None, 0, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_tile_layout(2, (1 << 60) + 1, 0, None, 0, br(n)) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_tile_layout(2, (1 << 60) - 7, 1, None, 0, br(n)) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_tile_layout(2, 10, 0, None, 5, br(n)) == esopt.ES_ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        esopt.tile_layout(2, 10, offset=4)              # not a multiple of 8
