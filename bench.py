@@ -688,13 +688,13 @@ def _counters_for(path, kind, label):
 
 
 def _kernel_source_hash():
-    """Hash of the device code the counters describe: the noise and int8
-    headers and the device section of esopt.hip (host-side edits leave the
-    kernels, and so the counters, unchanged)."""
+    """Hash of the device code the counters describe: the noise, int8 and
+    table-search headers and the device section of esopt.hip (host-side edits
+    leave the kernels, and so the counters, unchanged)."""
     import hashlib
     csrc = os.path.join(REPO, "paper_2608_17310_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("es_noise.hpp", "es_quant.hpp"):
+    for f in ("es_noise.hpp", "es_quant.hpp", "es_table.hpp"):
         h.update(open(os.path.join(csrc, f), "rb").read())
     src = open(os.path.join(csrc, "esopt.hip"), "rb").read()
     start, end = src.index(b"// Device code"), src.index(b"// Host side")

@@ -143,9 +143,9 @@ int hip_fail(hipError_t e, const std::string& what) {
 // ------------------------------------------------------------------------
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-// The tensor table holds generic pointers; every parameter lives in global
-// memory, and saying so lets the compiler use global_load / global_store
-// (vector-memory counters only) instead of flat accesses.
+// Tile descriptors and tensor tables hold generic pointers; every parameter
+// lives in global memory, and saying so lets the compiler use global_load /
+// global_store (vector-memory counters only) instead of flat accesses.
 #define ES_GLOBAL __attribute__((address_space(1)))
 
 // Load the 8 bf16 of one group (packed in 4 words).  Fast path: one 16-byte
