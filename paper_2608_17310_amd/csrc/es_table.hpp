@@ -1,4 +1,5 @@
-// Tile-to-tensor lookup shared by the bf16 and int8 tensor tables.
+// Tile-to-tensor lookup of the int8 tensor table (bf16 plans read a
+// descriptor per tile instead).
 #pragma once
 
 #include <hip/hip_runtime.h>

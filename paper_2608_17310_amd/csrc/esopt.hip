@@ -151,12 +151,12 @@ typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 // Load the 8 bf16 of one group (packed in 4 words).  Fast path: one 16-byte
 // load (nontemporal when kNT: the parameters are streamed once per pass).
 // Checked path (tail tiles): the 16-byte load when the tensor is 16-byte
-// aligned and the whole group is inside it, element-wise 2-byte loads with
-// bounds otherwise.
+// aligned and the whole group lies below the bound `limit`, element-wise
+// 2-byte loads below the bound otherwise.
 template <bool kFast, bool kNT>
 __device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint64_t e,
-                                           uint64_t numel, uint32_t raw[4], bool vec = false) {
-    if (kFast || (vec && e + 8 <= numel)) {
+                                           uint64_t limit, uint32_t raw[4], bool vec = false) {
+    if (kFast || (vec && e + 8 <= limit)) {
         const ES_GLOBAL u32x4_t* a = (const ES_GLOBAL u32x4_t*)(p + e);
         const u32x4_t v = kNT ? __builtin_nontemporal_load(a) : *a;
         raw[0] = v.x; raw[1] = v.y; raw[2] = v.z; raw[3] = v.w;
@@ -164,17 +164,17 @@ __device__ __forceinline__ void load_group(const uint16_t* __restrict__ p, uint6
         const ES_GLOBAL uint16_t* g = (const ES_GLOBAL uint16_t*)p;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            const uint32_t lo = (e + 2 * k < numel) ? g[e + 2 * k] : 0u;
-            const uint32_t hi = (e + 2 * k + 1 < numel) ? g[e + 2 * k + 1] : 0u;
+            const uint32_t lo = (e + 2 * k < limit) ? g[e + 2 * k] : 0u;
+            const uint32_t hi = (e + 2 * k + 1 < limit) ? g[e + 2 * k + 1] : 0u;
             raw[k] = lo | (hi << 16);
         }
     }
 }
 
 template <bool kFast, bool kNT>
-__device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e, uint64_t numel,
+__device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e, uint64_t limit,
                                             const uint32_t out[4], bool vec = false) {
-    if (kFast || (vec && e + 8 <= numel)) {
+    if (kFast || (vec && e + 8 <= limit)) {
         ES_GLOBAL u32x4_t* a = (ES_GLOBAL u32x4_t*)(p + e);
         const u32x4_t v = {out[0], out[1], out[2], out[3]};
         if constexpr (kNT) __builtin_nontemporal_store(v, a);
@@ -183,8 +183,8 @@ __device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e
         ES_GLOBAL uint16_t* g = (ES_GLOBAL uint16_t*)p;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
-            if (e + 2 * k < numel) g[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
-            if (e + 2 * k + 1 < numel) g[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
+            if (e + 2 * k < limit) g[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
+            if (e + 2 * k + 1 < limit) g[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
         }
     }
 }
@@ -334,7 +334,8 @@ __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU
     }
 }
 
-// Perturb a tail tile group by group with bounds-checked 2-byte accesses.
+// Perturb a tail tile group by group, with bounds-checked accesses (16-byte
+// for whole groups of an aligned tensor, 2-byte otherwise).
 template <int kThreads, int kU, int kM>
 __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st) {
     const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
