@@ -69,6 +69,21 @@ def step_seeds(W, t, n_members):
     return [int(s) + 1_000_003 * (t + 1) for s in base]
 
 
+def live_seeds(seeds, signs, rewards):
+    """Distinct seeds whose noise the update generates: those whose merged
+    weight, proportional to the sum of sign_i (R_i - mean R) over the seed's
+    members, is nonzero (none when every reward is equal).  The kernel skips
+    the others, so they count no normals.  Reporting only."""
+    r = np.asarray(rewards, np.float64)
+    if np.all(r == r[0]):
+        return 0
+    mu = r.mean()
+    acc = {}
+    for s, sg, x in zip(seeds, signs, r):
+        acc[s] = acc.get(s, 0.0) + sg * (x - mu)
+    return sum(1 for v in acc.values() if v != 0.0)
+
+
 def sigma_at(W, t):
     if W.sigma0 == W.sigma_T:
         return W.sigma0
@@ -262,7 +277,8 @@ def run_int8(args):
     P = plan.numel
     stream = torch.cuda.current_stream()
     total_steps = args.warmup + args.steps
-    rewards_all = torch.from_numpy(np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])).cuda()
+    rewards_np = np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])
+    rewards_all = torch.from_numpy(rewards_np).cuda()
     torch.cuda.synchronize()
     if args.profile_pass:
         seeds = step_seeds(W, 0, n_members)
@@ -322,6 +338,8 @@ def run_int8(args):
     t_upd = float(np.mean(per["es_qupdate"])) / 1e3
     value = (2 * N + 1) * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
+    n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
+                            for t in range(args.warmup, total_steps)]))
     label = W.name + "-int8"
     c_pert = _counters_for(args.counters_json, "es_qperturb", label)
     c_upd = _counters_for(args.counters_json, "es_qupdate", label)
@@ -357,8 +375,8 @@ def run_int8(args):
             "es_qperturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
                             "GBps_algorithmic": round(2 * P / t_pert / 1e9, 1)},
             "es_qupdate": {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
-                           "normals_per_s": n_distinct * P / t_upd,
-                           "distinct_seeds": n_distinct}},
+                           "normals_per_s": n_live * P / t_upd,
+                           "distinct_seeds": n_distinct, "live_seeds": round(n_live, 3)}},
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
@@ -372,8 +390,9 @@ def main():
         summarize(*args.summarize, workload=args.workload, int8=args.int8)
         return
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs the ES parameter path on one GPU; "
-                                   "--gpus above 1 is not supported (see the sharding design)"}))
+        print(json.dumps({"error": "the ES parameter path runs on one GPU; --gpus above 1 is "
+                                   "not supported (population parallelism across GPUs is not "
+                                   "implemented)"}))
         sys.exit(2)
     if args.sweep_members:
         return run_sweep(args)
@@ -402,7 +421,8 @@ def main():
     P = plan.numel
     stream = torch.cuda.current_stream()
     total_steps = args.warmup + args.steps
-    rewards_all = torch.from_numpy(np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])).cuda()
+    rewards_np = np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])
+    rewards_all = torch.from_numpy(rewards_np).cuda()
     torch.cuda.synchronize()
 
     if args.profile_pass:
@@ -482,6 +502,8 @@ def main():
     passes = (N + 2) if args.swap else (2 * N + 1)
     value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
+    n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
+                            for t in range(args.warmup, total_steps)]))
 
     # the practical in-place streaming ceiling over the same memory: the same
     # tiles and launch, loads and stores only, not pipelined (es_stream_pass),
@@ -510,7 +532,8 @@ def main():
                             "kernel": "es_stream_kernel: in-place copy of every parameter, same tiles (es_stream_pass)"}}
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
               "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
-              "normals_per_s": n_distinct * P / t_upd, "distinct_seeds": n_distinct}
+              "normals_per_s": n_live * P / t_upd, "distinct_seeds": n_distinct,
+              "live_seeds": round(n_live, 3)}
     # The update is VALU-bound: its roofline is the VALU issue rate.  The
     # instruction count per launch is a counter measurement (SQ_INSTS_VALU,
     # same workload and kernel sources); the duration is live.

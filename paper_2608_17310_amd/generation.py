@@ -83,24 +83,36 @@ def antithetic_seeds(base_seed, n_pairs):
 
 def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
     """Apply member 0, visit it, move to member 1, ... and revert the last.
-    Plans without a fused swap (the int8 QPlan) revert and apply separately."""
+    Plans without a fused swap (the int8 QPlan) revert and apply separately.
+    When the passes run on a stream other than PyTorch's current one, each
+    visit is ordered after its member's pass and the next pass after the
+    visit's work on the current stream, so an evaluation that reads the
+    parameters there sees exactly member i applied."""
     n = len(seeds)
     fused_swap = fused_swap and hasattr(plan, "swap")
-    plan.perturb(seeds[0], signs[0], sigma, stream=stream)
+    s = _torch_stream(stream, plan.device)
+    cur = torch.cuda.current_stream(plan.device)
+    side = s.cuda_stream != cur.cuda_stream
+    plan.perturb(seeds[0], signs[0], sigma, stream=s)
     for i in range(n):
+        if side:
+            cur.wait_stream(s)
         visit(i)
+        if side:
+            s.wait_stream(cur)
         if i + 1 < n and fused_swap:
-            plan.swap(seeds[i], signs[i], seeds[i + 1], signs[i + 1], sigma, stream=stream)
+            plan.swap(seeds[i], signs[i], seeds[i + 1], signs[i + 1], sigma, stream=s)
         else:
-            plan.restore(seeds[i], signs[i], sigma, stream=stream)
+            plan.restore(seeds[i], signs[i], sigma, stream=s)
             if i + 1 < n:
-                plan.perturb(seeds[i + 1], signs[i + 1], sigma, stream=stream)
+                plan.perturb(seeds[i + 1], signs[i + 1], sigma, stream=s)
 
 
 def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], float],
                    flags=0, zscore_eps=1e-8, fused_swap=True, stream=None, round_seed=0):
     """Run one generation; evaluate(i) scores the parameters while member i is
-    applied and returns a float.  With ES_UPDATE_STOCHASTIC_ROUND in flags the
+    applied and returns a float.  Its GPU work goes on PyTorch's current
+    stream (or is finished when it returns); the passes go on `stream`.  With ES_UPDATE_STOCHASTIC_ROUND in flags the
     update is rounded with the draws of round_seed (use a new one per
     generation).  Returns the GenerationRecord."""
     if len(seeds) != len(signs) or not seeds:

@@ -212,3 +212,36 @@ def test_generation_on_a_side_stream_matches_default_stream():
             side.synchronize()
         for a, b in zip(ref, ts):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_side_stream_evaluation_sees_each_member_applied():
+    """The passes on a side stream, the evaluation reading the parameters on
+    the current stream: each evaluation sees exactly its member applied, even
+    when the side stream is held back by other work queued on it."""
+    W = wl.TINY
+    seeds, signs = antithetic_seeds(50, 3)
+    busy = torch.empty(1 << 28, dtype=torch.uint8, device="cuda")
+
+    def run(stream, hold):
+        _, ts = _fresh(W)
+        torch.cuda.synchronize()
+
+        def evaluate(i):
+            v = float(ts[0].float().sum() + ts[3].float().sum())
+            if hold:                        # queue work ahead of the next pass
+                with torch.cuda.stream(stream):
+                    for _ in range(4):
+                        busy.add_(1)
+            return v
+        with esopt.Plan(ts) as p:
+            rec = run_generation(p, seeds, signs, 1e-3, 5e-4, evaluate=evaluate, stream=stream)
+            torch.cuda.synchronize()
+        return rec.rewards, [to_host(t) for t in ts]
+
+    ref_r, ref_t = run(None, False)
+    assert len(set(ref_r)) == len(ref_r)        # every member scored differently
+    side = torch.cuda.Stream()
+    got_r, got_t = run(side, True)
+    assert got_r == ref_r
+    for a, b in zip(ref_t, got_t):
+        np.testing.assert_array_equal(a, b)

@@ -12,7 +12,7 @@ import torch
 
 import oracle
 from paper_2608_17310_amd import esopt, workloads as wl
-from parity import to_device, to_host, report, assert_parity, perturb_delta
+from parity import to_device, to_host, report, assert_parity, perturb_delta, update_delta
 
 pytestmark = pytest.mark.gpu
 
@@ -90,6 +90,54 @@ def test_shard_perturb_matches_oracle_at_whole_tensor_indices():
         p.perturb(11, -1, 2e-3)
     torch.cuda.synchronize()
     assert np.mean(to_host(plain) != to_host(shard)) > 0.5
+
+
+def test_shard_across_element_2_34_matches_oracle_everywhere():
+    """A shard of a 2^34+ element tensor that straddles element 2^34 (where
+    the counter's high word changes and the tile split happens), checked
+    element by element against the oracle after every pass, without the
+    32 GiB tensor itself."""
+    a = (1 << 34) - 200_000
+    n = 500_017
+    el = np.arange(a, a + n, dtype=np.uint64)
+    x0 = wl.random_bf16_bits(n, 44)
+    buf = torch.zeros(n + 16, dtype=torch.bfloat16, device="cuda")
+    shard = buf[8:8 + n]
+    shard.copy_(to_device(x0))
+    r = np.array([0.2, 0.7, 0.4], np.float32)
+    xs = [x0]
+    with esopt.Plan([shard], tensor_ids=[TID], offsets=[a]) as p:
+        for step in (lambda: p.perturb(11, -1, 1e-3),
+                     lambda: p.swap(11, -1, 12, 1, 1e-3),
+                     lambda: p.restore(12, 1, 1e-3),
+                     lambda: p.update([3, 4, 5], [1, 1, 1], torch.from_numpy(r).cuda(), 5e-4),
+                     lambda: p.update([3, 4, 5], [1, 1, 1], torch.from_numpy(r).cuda(), 5e-4,
+                                      flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+                                      round_seed=(1 << 63) + 9)):
+            step()
+            torch.cuda.synchronize()
+            xs.append(to_host(shard))
+    assert torch.count_nonzero(buf[:8].float()) == 0
+    assert torch.count_nonzero(buf[8 + n:].float()) == 0
+    x0, x1, x2, x3, x4, x5 = xs
+    upd = update_delta(TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, 0, el)
+    checks = [
+        ("perturb", x1, oracle.perturb(x0, 11, TID, -1, 1e-3, elems=el), x0,
+         perturb_delta(11, TID, -1, 1e-3, el)),
+        ("swap", x2, oracle.swap(x1, TID, 11, -1, 1e-3, 12, 1, 1e-3, elems=el), x1,
+         perturb_delta(11, TID, 1, 1e-3, el) + perturb_delta(12, TID, 1, 1e-3, el)),
+        ("restore", x3, oracle.restore(x2, 12, TID, 1, 1e-3, elems=el), x2,
+         perturb_delta(12, TID, -1, 1e-3, el)),
+        ("update", x4, oracle.update(x3, TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3,
+                                     elems=el)[0], x3, upd),
+        ("update_sr", x5, oracle.update(x4, TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el,
+                                        flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+                                        round_seed=(1 << 63) + 9)[0], x4, upd),
+    ]
+    for name, got, exp, base, delta in checks:
+        rep = report(got, exp, base, delta)
+        print("shard across 2^34:", name, rep)
+        assert_parity(rep, name)
 
 
 def test_offsets_are_validated():
