@@ -126,10 +126,25 @@ def cpu_baseline(W, seeds, signs, rewards, sigma, theta_samples, workers, budget
     wall = time.perf_counter() - t0
     rate = (2 * n + 1) * n_elems / wall
     return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            **host_cpu(),
             "full_step_s_extrapolated": round((2 * n + 1) * W.n_params / rate, 1),
             "sample": f"{n_elems} elements sampled across {len(jobs)} tensors of {W.name}, "
                       f"one full step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 "
                       f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
+
+
+def host_cpu():
+    """The host's CPU model (from /proc/cpuinfo) and logical CPU count."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"cpu_model": model, "host_logical_cpus": os.cpu_count()}
 
 
 def host_samples(W, per_tensor=1 << 16):
@@ -188,6 +203,7 @@ def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_te
     wall = time.perf_counter() - t0
     rate = (2 * n + 1) * n_elems / wall
     return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
+            **host_cpu(),
             "full_step_s_extrapolated": round((2 * n + 1) * W.n_params / rate, 1),
             "sample": f"{n_elems} int8 codes sampled across {len(jobs)} tensors of {W.name}, one "
                       f"full int8 step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 NumPy "

@@ -32,3 +32,9 @@ def test_more_than_one_gpu_is_refused():
     assert r.returncode == 2
     msg = json.loads(r.stdout.strip().splitlines()[-1])
     assert "one GPU" in msg["error"]
+
+
+def test_host_cpu_is_reported():
+    h = bench.host_cpu()
+    assert h["host_logical_cpus"] == os.cpu_count()
+    assert h["cpu_model"] is None or isinstance(h["cpu_model"], str)
