@@ -211,6 +211,23 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const es_update_opts_t* opts, float* z_out_dev,
               int32_t* status_out_dev, es_stream_t stream);
 
+/* 64-bit checksum of a plan's parameters, written to *out_dev (device
+ * memory, 8-byte aligned):
+ *   H = sum over elements of mix64(j K_J + tensor_id K_T + b K_B)  mod 2^64
+ * with j the element's index in its whole tensor (shard offset included), b
+ * its 16 bits, K_J = 0x9E3779B97F4A7C15, K_T = 0xC2B2AE3D27D4EB4F,
+ * K_B = 0x165667B19E3779F9, and mix64 the finalizer of SplitMix64 (Steele,
+ * Lea and Flood, OOPSLA 2014):
+ *   z ^= z >> 30; z *= 0xBF58476D1CE4E5B9; z ^= z >> 27;
+ *   z *= 0x94D049BB133111EB; z ^= z >> 31.
+ * It serves the seed replay of Section 3 and Appendix D.6 (a run rebuilt from
+ * its seed log can be checked against checksums recorded with it) and
+ * replicas that must stay identical after each update.  The sum does not
+ * depend on the launch shape, and the checksums of disjoint shards of a
+ * tensor add up (mod 2^64) to the whole tensor's.  Reads the parameters once
+ * (two launches: one clears *out_dev, one sums); an empty plan gives 0. */
+int es_plan_checksum(es_plan_t* plan, uint64_t* out_dev, es_stream_t stream);
+
 /* ---- int8 parameters (quantized ES; the paper lists it as future work,
  * Appendix A.2: scale-aware noise, stable updates, seed replay) ----
  *

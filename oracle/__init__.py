@@ -25,6 +25,9 @@ The paper names no generator and no transform; Philox4x32-10 is the published
 generator of Salmon, Moraes, Dror and Shaw (SC'11) and Box-Muller the textbook
 transform of Box and Muller (1958).
 
+checksum.py sums a 64-bit mix of every element's index, tensor id and bits
+mod 2^64: the library's parameter checksum, used to check a replayed run.
+
 The int8 path (quant.py) perturbs and updates symmetric int8 codes with
 per-row scales in units of the quantum, rounding offsets stochastically; the
 paper lists quantized ES as future work (Appendix A.2).
@@ -42,6 +45,7 @@ from .es import (perturb, restore, swap, zscore, update_coefficient, member_weig
                  ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND)
 from .quant import (QMAX, row_scales, round_offset, round_offset9, offset_values, qperturb,
                     qrestore, update_values, qupdate)
+from .checksum import mix64, checksum, plan_checksum
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
@@ -52,4 +56,5 @@ __all__ = [
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
     "ES_UPDATE_STOCHASTIC_ROUND",
     "QMAX", "row_scales", "round_offset", "round_offset9", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
+    "mix64", "checksum", "plan_checksum",
 ]

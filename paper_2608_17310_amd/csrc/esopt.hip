@@ -458,6 +458,79 @@ __global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTile* __re
     }
 }
 
+// Parameter checksum (es_plan_checksum):
+//   H = sum over every element of mix64(j K_J + tensor_id K_T + b K_B)  mod 2^64
+// with j the element's index in its whole tensor, b its 16 bits and mix64
+// the 64-bit finalizer of SplitMix64 (Steele, Lea and Flood, OOPSLA 2014).
+// Addition mod 2^64 does not depend on the order of its terms, so H does not
+// depend on the launch shape, and the checksums of disjoint shards of a tensor
+// add up to the whole tensor's.  Read-only and VALU-bound (about 30
+// instructions per element: 64-bit products and shifts on 32-bit lanes).
+constexpr uint64_t kSumJ = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t kSumT = 0xC2B2AE3D27D4EB4Full;
+constexpr uint64_t kSumB = 0x165667B19E3779F9ull;
+
+__device__ __forceinline__ uint64_t mix64(uint64_t z) {
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) x += __shfl_xor(x, off, 64);
+    return x;
+}
+
+// Each lane sums its groups' terms; every tile is bounds-checked per element
+// (a full tile's bound is its end), so one loop serves full and tail tiles.
+// The workgroup's sum is added to *out with one 64-bit atomic.
+template <int kThreads, int kU>
+__global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __restrict__ tiles,
+                                                               uint64_t n_full, uint64_t n_tiles,
+                                                               unsigned long long* __restrict__ out) {
+    uint64_t acc = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+        const TileRef r = tile_ref(tiles[tile]);
+        const bool full = tile < n_full;
+        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            if (e >= r.limit) break;
+            uint32_t raw[4];
+            if (full)
+                load_group<true, true>(r.data, e, r.limit, raw);
+            else
+                load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
+            uint64_t x = e * kSumJ + salt;
+#pragma unroll
+            for (int k = 0; k < kGroupElems; ++k) {
+                const uint64_t b = (raw[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
+                const uint64_t f = mix64(x + b * kSumB);
+                acc += (e + k < r.limit) ? f : 0ull;
+                x += kSumJ;
+            }
+        }
+    }
+    __shared__ uint64_t part[kThreads / 64];
+    acc = wave_sum_u64(acc);
+    if ((threadIdx.x & 63u) == 0u) part[threadIdx.x / 64] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint64_t s = 0;
+#pragma unroll
+        for (int w = 0; w < kThreads / 64; ++w) s += part[w];
+        atomicAdd(out, static_cast<unsigned long long>(s));
+    }
+}
+
+// *p = 0 before a checksum's atomics (a kernel, not a memset, so the call
+// stays capturable into a HIP graph).
+__global__ __launch_bounds__(64) void es_zero_u64_kernel(unsigned long long* __restrict__ p) {
+    if (threadIdx.x == 0) *p = 0ull;
+}
+
 // w == +-0, tested on the bit pattern so that the member loop's skip stays on
 // the scalar unit (a binary32 compare would be a vector instruction).
 __device__ __forceinline__ bool is_zero_weight(float w) {
@@ -703,6 +776,15 @@ using StreamKernel = void (*)(const DevTile*, uint64_t, uint64_t, uint32_t);
 
 StreamKernel stream_kernel(int threads, int groups) {
 #define ES_CASE(T, U) if (threads == T && groups == U) return es_stream_kernel<T, U>;
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
+using ChecksumKernel = void (*)(const DevTile*, uint64_t, uint64_t, unsigned long long*);
+
+ChecksumKernel checksum_kernel(int threads, int groups) {
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_checksum_kernel<T, U>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -1579,6 +1661,28 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
                        plan->n_full, plan->n_tail, 0u);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
+    return ES_OK;
+}
+
+int es_plan_checksum(es_plan_t* plan, uint64_t* out_dev, es_stream_t stream) {
+    if (plan == nullptr || out_dev == nullptr)
+        return fail(ES_ERR_INVALID_ARG, "es_plan_checksum: null pointer");
+    if (reinterpret_cast<uintptr_t>(out_dev) % 8 != 0)
+        return fail(ES_ERR_ALIGN, "es_plan_checksum: output not 8-byte aligned");
+    int rc = check_device(plan);
+    if (rc == ES_OK) rc = check_access(out_dev, 8, plan->device, "es_plan_checksum: output");
+    if (rc != ES_OK) return rc;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned long long* out = reinterpret_cast<unsigned long long*>(out_dev);
+    hipLaunchKernelGGL(es_zero_u64_kernel, dim3(1), dim3(64), 0, s, out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_zero_u64_kernel launch");
+    const uint64_t n_tiles = plan->n_full + plan->n_tail;
+    if (n_tiles == 0) return ES_OK;
+    hipLaunchKernelGGL(checksum_kernel(plan->threads, plan->groups), dim3(plan->grid_update),
+                       dim3(plan->threads), 0, s, plan->d_tiles, plan->n_full, n_tiles, out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_checksum_kernel launch");
     return ES_OK;
 }
 

@@ -10,6 +10,7 @@ call raises (there is no fallback).
     plan.restore(seed, sign, sigma)      # theta -= sign sigma eps(seed)
     plan.swap(seed_a, sign_a, seed_b, sign_b, sigma)   # restore a + perturb b, one pass
     plan.update(seeds, signs, rewards, alpha)   # fused z-score + N-member update
+    plan.checksum()                      # 64-bit checksum of the parameters
 """
 
 import ctypes
@@ -65,6 +66,7 @@ SIGNATURES = {
     "es_restore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_swap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
     "es_stream_pass": (ctypes.c_int, [_vp, _vp]),
+    "es_plan_checksum": (ctypes.c_int, [_vp, _vp, _vp]),
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
@@ -227,6 +229,24 @@ class Plan:
         """Read every parameter and write it back unchanged over es_perturb's
         tiles, with no arithmetic (the in-place streaming ceiling)."""
         _check(load().es_stream_pass(self.handle, _stream(stream)), "es_stream_pass")
+
+    def checksum(self, out=None, stream=None):
+        """64-bit checksum of the parameters (es_plan_checksum).  Without
+        `out`, returns it as a Python int (synchronising); with `out`, a
+        one-element int64 tensor on the plan's device, the value (its bits)
+        is left there, stream-ordered, and `out` is returned."""
+        ret = out is None
+        if ret:
+            out = torch.empty(1, dtype=torch.int64, device=self.device)
+        elif out.numel() != 1 or out.device != self.device:
+            raise ValueError("out must be a one-element tensor on the plan's device")
+        _check(load().es_plan_checksum(self.handle, _dev_ptr(out, torch.int64, "out"),
+                                       _stream(stream)), "es_plan_checksum")
+        if not ret:
+            return out
+        if stream is not None:
+            torch.cuda.synchronize(self.device)
+        return int(out.item()) & ((1 << 64) - 1)
 
     def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
         """Revert member `from` and apply member `to` in one pass: the same

@@ -14,12 +14,14 @@ path (esopt.QPlan), whose revert is exact and which has no fused swap.
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
 the same starting parameters rebuilds the parameters bit for bit (the paper reconstructs its final models
-from the recorded update sequence the same way, Appendix D.2 and D.4).
+from the recorded update sequence the same way, Appendix D.2 and D.4).  A record
+can also carry the parameters' 64-bit checksum after its update, which replay
+checks.
 """
 
 import json
 from dataclasses import asdict, dataclass, fields
-from typing import Callable, List
+from typing import Callable, List, Optional
 
 import torch
 
@@ -37,6 +39,7 @@ class GenerationRecord:
     zscore_eps: float = 1e-8
     fused_swap: bool = True
     round_seed: int = 0             # key of the update's stochastic rounding
+    checksum: Optional[int] = None  # es_plan_checksum after the update, if recorded
 
 
 LOG_FORMAT = "es-generation-log/1"
@@ -109,14 +112,19 @@ def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
 
 
 def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], float],
-                   flags=0, zscore_eps=1e-8, fused_swap=True, stream=None, round_seed=0):
+                   flags=0, zscore_eps=1e-8, fused_swap=True, stream=None, round_seed=0,
+                   checksum=False):
     """Run one generation; evaluate(i) scores the parameters while member i is
     applied and returns a float.  Its GPU work goes on PyTorch's current
     stream (or is finished when it returns); the passes go on `stream`.  With ES_UPDATE_STOCHASTIC_ROUND in flags the
     update is rounded with the draws of round_seed (use a new one per
-    generation).  Returns the GenerationRecord."""
+    generation).  With checksum, the parameters' checksum after the update
+    is recorded (a bf16 Plan only), so that replay() can verify the rebuilt
+    parameters.  Returns the GenerationRecord."""
     if len(seeds) != len(signs) or not seeds:
         raise ValueError("seeds and signs must be non-empty and of equal length")
+    if checksum and not hasattr(plan, "checksum"):
+        raise ValueError("this plan has no checksum")
     rewards = []
     _walk(plan, seeds, signs, sigma, fused_swap, lambda i: rewards.append(float(evaluate(i))),
           stream)
@@ -125,6 +133,8 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
                            float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap,
                            int(round_seed))
     apply_update(plan, rec, stream)
+    if checksum:
+        rec.checksum = plan.checksum(stream=stream)
     return rec
 
 
@@ -148,12 +158,24 @@ def apply_update(plan, rec: GenerationRecord, stream=None):
                     round_seed=rec.round_seed)
 
 
-def replay(plan, records, with_perturbations=True, stream=None):
+class ReplayMismatch(RuntimeError):
+    """A replayed generation's parameters differ from the recorded checksum."""
+
+
+def replay(plan, records, with_perturbations=True, stream=None, verify=True):
     """Re-apply recorded generations.  With with_perturbations (default) the
     perturb / swap / restore passes are replayed too, which reproduces the
     live run bit for bit (their bf16 rounding residues included); without,
-    only the updates are applied."""
-    for rec in records:
+    only the updates are applied.  With verify (default), every record that
+    carries a checksum is checked after its update (replays with
+    perturbations only: without them the bits differ by design), raising
+    ReplayMismatch at the first generation that differs."""
+    for g, rec in enumerate(records):
         if with_perturbations:
             _walk(plan, rec.seeds, rec.signs, rec.sigma, rec.fused_swap, lambda i: None, stream)
         apply_update(plan, rec, stream)
+        if verify and with_perturbations and rec.checksum is not None:
+            got = plan.checksum(stream=stream)
+            if got != rec.checksum:
+                raise ReplayMismatch(f"generation {g}: checksum {got:#018x}, "
+                                     f"recorded {rec.checksum:#018x}")

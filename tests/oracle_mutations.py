@@ -4,7 +4,7 @@ wrong constant, a swapped index or operand, a dropped term, an off-by-one in
 a rounding rule -- and runs the CPU test suite on the copy; every mistake must
 make at least one test fail.
 
-    python tests/oracle_mutations.py        # about 30 s per mutation
+    python tests/oracle_mutations.py [file-substring]   # about 30 s per mutation
 """
 import os
 import shutil
@@ -57,18 +57,45 @@ MUTS = [
  ("oracle/quant.py", "return _apply(q, -round_offset9(d, r), ok)", "return _apply(q, round_offset9(-d, r), ok)"),
  ("oracle/quant.py", "d = np.where(ok, delta / np.where(ok, s, 1.0), 0.0)", "d = np.where(ok, delta / np.where(ok, s, 1.0) / 2, 0.0)"),
  ("oracle/quant.py", "rounding_draws(round_seed, tensor_id, el, DOMAIN_ROUNDING), ok, live, 0", "rounding_draws(round_seed + 1, tensor_id, el, DOMAIN_ROUNDING), ok, live, 0"),
+ ("oracle/checksum.py", "z = (z ^ (z >> np.uint64(30)))", "z = (z ^ (z >> np.uint64(31)))"),
+ ("oracle/checksum.py", "MIX_M2 = 0x94D049BB133111EB", "MIX_M2 = 0x94D049BB133111EF"),
+ ("oracle/checksum.py", "x = j * np.uint64(K_J) + salt + b * np.uint64(K_B)", "x = j * np.uint64(K_J) + b * np.uint64(K_B)"),
+ ("oracle/checksum.py", "+ np.uint64(int(elem0) + c0)", "+ np.uint64(c0)"),
+ ("oracle/checksum.py", "b = b_all[c0:c0 + chunk].astype(np.uint64)", "b = (b_all[c0:c0 + chunk] & np.uint16(0x7FFF)).astype(np.uint64)"),
 
 ]
 
 
+def _copy(tmp):
+    for d in ("oracle", "tests", "paper_2608_17310_amd", "include"):
+        shutil.copytree(os.path.join(REPO, d), os.path.join(tmp, d))
+    for f in ("pytest.ini", "bench.py"):
+        shutil.copy(os.path.join(REPO, f), tmp)
+
+
+def _suite(tmp):
+    return subprocess.run([sys.executable, "-m", "pytest", "tests", "-q", "-m", "not gpu",
+                           "-p", "no:cacheprovider"], cwd=tmp, capture_output=True, text=True)
+
+
 def main():
+    only = sys.argv[1] if len(sys.argv) > 1 else ""
+    muts = [m for m in MUTS if only in m[0]]
+    # the unmutated copy must pass, or a failure would prove nothing
+    tmp = tempfile.mkdtemp(prefix="oracle_mut_")
+    try:
+        _copy(tmp)
+        r = _suite(tmp)
+        if r.returncode != 0:
+            print("the unmutated copy fails:", (r.stdout.strip().splitlines() or [""])[-1])
+            return 2
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
     missed = 0
-    for f, a, b in MUTS:
+    for f, a, b in muts:
         tmp = tempfile.mkdtemp(prefix="oracle_mut_")
         try:
-            for d in ("oracle", "tests", "paper_2608_17310_amd"):
-                shutil.copytree(os.path.join(REPO, d), os.path.join(tmp, d))
-            shutil.copy(os.path.join(REPO, "pytest.ini"), tmp)
+            _copy(tmp)
             path = os.path.join(tmp, f)
             text = open(path).read()
             if a not in text:
@@ -76,16 +103,16 @@ def main():
                 missed += 1
                 continue
             open(path, "w").write(text.replace(a, b, 1))
-            r = subprocess.run([sys.executable, "-m", "pytest", "tests", "-q", "-m", "not gpu",
-                                "-p", "no:cacheprovider"], cwd=tmp, capture_output=True, text=True)
-            caught = r.returncode != 0
+            r = _suite(tmp)
+            # a failed test, not a collection error, counts as caught
+            caught = r.returncode == 1
             missed += not caught
             last = (r.stdout.strip().splitlines() or [""])[-1]
             print("CAUGHT " if caught else "MISSED ", b.replace("\n", " ")[:70], "|", last,
                   flush=True)
         finally:
             shutil.rmtree(tmp, ignore_errors=True)
-    print(f"{len(MUTS)} mutations, missed: {missed}")
+    print(f"{len(muts)} mutations, missed: {missed}")
     return 1 if missed else 0
 
 

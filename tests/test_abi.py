@@ -104,6 +104,9 @@ def test_call_validation_without_device(lib):
     assert lib.es_philox_words(1, 0, 0, 0, 0, fake, None) == esopt.ES_OK
     assert lib.es_normals(1, 0, 0, 0, fake, None) == esopt.ES_OK
     assert lib.es_stream_pass(None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_plan_checksum(None, fake, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_plan_checksum(fake, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_plan_checksum(fake, ctypes.c_void_p(0x1004), None) == esopt.ES_ERR_ALIGN
     assert lib.es_plan_destroy(None) == esopt.ES_OK
     assert lib.es_plan_numel(None) == 0
 

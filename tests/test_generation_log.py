@@ -1,5 +1,6 @@
 """The seed log: generation records survive a JSON round trip exactly (the
-binary32 rewards included), and a log of another format is refused."""
+binary32 rewards and 64-bit checksums included), and a log of another format
+is refused."""
 import json
 
 import numpy as np
@@ -17,7 +18,8 @@ def test_seed_log_round_trip(tmp_path):
                                      signs=[1, 1, -1, 1, -1, 1], rewards=rew,
                                      sigma=float(np.float32(1e-3 * (t + 1) / 3)), alpha=5e-4,
                                      flags=4 if t % 2 else 0, zscore_eps=1e-8,
-                                     fused_swap=bool(t % 2), round_seed=(1 << 63) + t))
+                                     fused_swap=bool(t % 2), round_seed=(1 << 63) + t,
+                                     checksum=None if t == 2 else (1 << 64) - 1 - 977 * t))
     path = tmp_path / "log.json"
     save_log(path, recs, meta={"workload": "tiny-1m", "base": "checkpoint-0"})
     back, meta = load_log(path)
