@@ -279,6 +279,11 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
                const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
                float* z_out_dev, int32_t* status_out_dev, es_stream_t stream);
 
+/* Checksum of an int8 plan's codes, as es_plan_checksum with b the code's 8
+ * bits (0 .. 255) and j its index in its tensor; the scales are not included
+ * (no pass changes them). */
+int es_qplan_checksum(es_qplan_t* plan, uint64_t* out_dev, es_stream_t stream);
+
 /* Cosine schedule of the perturbation radius (Section 3.1):
  *   sigma_t = sigma_T + (sigma_0 - sigma_T) (1 + cos(pi t / T)) / 2,
  * 0 <= t <= T, T >= 1; returns NaN for arguments out of range.  Update t

@@ -45,7 +45,7 @@ from .es import (perturb, restore, swap, zscore, update_coefficient, member_weig
                  ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND)
 from .quant import (QMAX, row_scales, round_offset, round_offset9, offset_values, qperturb,
                     qrestore, update_values, qupdate)
-from .checksum import mix64, checksum, plan_checksum
+from .checksum import mix64, checksum, qchecksum, plan_checksum
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
@@ -56,5 +56,5 @@ __all__ = [
     "update", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
     "ES_UPDATE_STOCHASTIC_ROUND",
     "QMAX", "row_scales", "round_offset", "round_offset9", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
-    "mix64", "checksum", "plan_checksum",
+    "mix64", "checksum", "qchecksum", "plan_checksum",
 ]

@@ -1,7 +1,7 @@
 """Parameter checksum (oracle; test-only).
 
-The library's checksum of a set of bf16 tensors, written out from its
-definition: every element contributes mix64(j K_J + id K_T + b K_B) and the
+The library's checksum of a set of bf16 tensors (or of int8 codes), written
+out from its definition: every element contributes mix64(j K_J + id K_T + b K_B) and the
 contributions are added mod 2^64, where j is the element's index in its
 whole tensor, id the tensor's noise identity, b the element's 16 bits, and
 mix64 the 64-bit finalizer of SplitMix64 (Steele, Lea and Flood, "Fast
@@ -43,7 +43,16 @@ def checksum(bits, tensor_id, elem0=0, chunk=1 << 22):
     """Checksum (a Python int in [0, 2^64)) of the bf16 elements `bits`
     (uint16) that sit at whole-tensor indices elem0, elem0 + 1, ... of tensor
     `tensor_id`."""
-    b_all = np.asarray(bits, dtype=np.uint16).ravel()
+    return _sum(np.asarray(bits, dtype=np.uint16).ravel(), tensor_id, elem0, chunk)
+
+
+def qchecksum(codes, tensor_id, chunk=1 << 22):
+    """Checksum of the int8 codes of one tensor: the same sum with b the
+    code's 8 bits read as an unsigned byte."""
+    return _sum(np.asarray(codes, dtype=np.int8).ravel().view(np.uint8), tensor_id, 0, chunk)
+
+
+def _sum(b_all, tensor_id, elem0, chunk):
     salt = np.uint64((int(tensor_id) * K_T) & MASK64)
     total = 0
     for c0 in range(0, b_all.size, chunk):

@@ -464,7 +464,7 @@ __global__ __launch_bounds__(kThreads) void es_stream_kernel(const DevTile* __re
 // the 64-bit finalizer of SplitMix64 (Steele, Lea and Flood, OOPSLA 2014).
 // Addition mod 2^64 does not depend on the order of its terms, so H does not
 // depend on the launch shape, and the checksums of disjoint shards of a tensor
-// add up to the whole tensor's.  Read-only and VALU-bound (about 30
+// add up to the whole tensor's.  Read-only and VALU-bound (about 24
 // instructions per element: 64-bit products and shifts on 32-bit lanes).
 constexpr uint64_t kSumJ = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t kSumT = 0xC2B2AE3D27D4EB4Full;
@@ -482,37 +482,30 @@ __device__ __forceinline__ uint64_t wave_sum_u64(uint64_t x) {
     return x;
 }
 
-// Each lane sums its groups' terms; every tile is bounds-checked per element
-// (a full tile's bound is its end), so one loop serves full and tail tiles.
-// The workgroup's sum is added to *out with one 64-bit atomic.
-template <int kThreads, int kU>
-__global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __restrict__ tiles,
-                                                               uint64_t n_full, uint64_t n_tiles,
-                                                               unsigned long long* __restrict__ out) {
-    uint64_t acc = 0;
-    for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
-        const TileRef r = tile_ref(tiles[tile]);
-        const bool full = tile < n_full;
-        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
-#pragma unroll 1
-        for (int u = 0; u < kU; ++u) {
-            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-            if (e >= r.limit) break;
-            uint32_t raw[4];
-            if (full)
-                load_group<true, true>(r.data, e, r.limit, raw);
-            else
-                load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
-            uint64_t x = e * kSumJ + salt;
+// The checksum terms of kN consecutive elements from whole-tensor index e,
+// their values taken kBits at a time from `raw` (element k in bits
+// kBits*k.. of the word array); with kChecked only elements below `limit`
+// count.
+template <int kN, int kBits, bool kChecked>
+__device__ __forceinline__ uint64_t checksum_terms(const uint32_t* raw, uint64_t e,
+                                                   uint64_t limit, uint64_t salt) {
+    constexpr int kPerWord = 32 / kBits;
+    constexpr uint32_t kMask = (1u << kBits) - 1u;
+    uint64_t x = e * kSumJ + salt, acc = 0;
 #pragma unroll
-            for (int k = 0; k < kGroupElems; ++k) {
-                const uint64_t b = (raw[k >> 1] >> (16 * (k & 1))) & 0xFFFFu;
-                const uint64_t f = mix64(x + b * kSumB);
-                acc += (e + k < r.limit) ? f : 0ull;
-                x += kSumJ;
-            }
-        }
+    for (int k = 0; k < kN; ++k) {
+        const uint64_t b = (raw[k / kPerWord] >> (kBits * (k % kPerWord))) & kMask;
+        const uint64_t f = mix64(x + b * kSumB);
+        acc += (!kChecked || e + k < limit) ? f : 0ull;
+        x += kSumJ;
     }
+    return acc;
+}
+
+// Adds the workgroup's lane sums to *out: a lane-shuffle sum per wave, then
+// one 64-bit atomic per workgroup.
+template <int kThreads>
+__device__ __forceinline__ void add_workgroup_sum(uint64_t acc, unsigned long long* out) {
     __shared__ uint64_t part[kThreads / 64];
     acc = wave_sum_u64(acc);
     if ((threadIdx.x & 63u) == 0u) part[threadIdx.x / 64] = acc;
@@ -523,6 +516,39 @@ __global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __
         for (int w = 0; w < kThreads / 64; ++w) s += part[w];
         atomicAdd(out, static_cast<unsigned long long>(s));
     }
+}
+
+// bf16 plan: full tiles with 16-byte loads and no per-element bound, then
+// tail tiles bounds-checked.
+template <int kThreads, int kU>
+__global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __restrict__ tiles,
+                                                               uint64_t n_full, uint64_t n_tail,
+                                                               unsigned long long* __restrict__ out) {
+    uint64_t acc = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
+        const TileRef r = tile_ref(tiles[tile]);
+        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            uint32_t raw[4];
+            load_group<true, true>(r.data, e, r.limit, raw);
+            acc += checksum_terms<kGroupElems, 16, false>(raw, e, r.limit, salt);
+        }
+    }
+    for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x) {
+        const TileRef r = tile_ref(tiles[n_full + tl]);
+        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            if (e >= r.limit) break;
+            uint32_t raw[4];
+            load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
+            acc += checksum_terms<kGroupElems, 16, true>(raw, e, r.limit, salt);
+        }
+    }
+    add_workgroup_sum<kThreads>(acc, out);
 }
 
 // *p = 0 before a checksum's atomics (a kernel, not a memset, so the call
@@ -945,6 +971,51 @@ QPassKernel qpass_kernel(int threads, int groups, QKind kind) {
             case QKind::kUpdate: return es_qpass_kernel<T, U, true, false>;      \
         }                                                                        \
     }
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
+// int8 plan: the same sum with b the code's 8 bits (int8 tensors are never
+// shards, so an element's index in its tensor is its whole-tensor index).
+template <int kThreads, int kU>
+__global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
+    const esq::DevQTensor* __restrict__ tab, uint64_t n_full, uint64_t n_tail,
+    unsigned long long* __restrict__ out) {
+    constexpr uint32_t kTileElems = uint32_t(kThreads) * kU * esq::kQGroup;
+    uint64_t acc = 0;
+    uint32_t t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
+        const esq::QTileRef r = esq::qlocate_full<kTileElems>(tab, t, tile);
+        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint32_t e = r.elem0 + (uint32_t(u) * kThreads + threadIdx.x) * esq::kQGroup;
+            uint32_t raw[4];
+            esq::qload<true>(r.data, e, r.numel, raw);
+            acc += checksum_terms<esq::kQGroup, 8, false>(raw, e, r.numel, salt);
+        }
+    }
+    t = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x) {
+        const esq::QTileRef r = esq::qlocate_tail<kTileElems>(tab, t, tile);
+        const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint32_t e = r.elem0 + (uint32_t(u) * kThreads + threadIdx.x) * esq::kQGroup;
+            if (e >= r.numel) break;
+            uint32_t raw[4];
+            esq::qload<false>(r.data, e, r.numel, raw, r.aligned16 != 0u);
+            acc += checksum_terms<esq::kQGroup, 8, true>(raw, e, r.numel, salt);
+        }
+    }
+    add_workgroup_sum<kThreads>(acc, out);
+}
+
+using QChecksumKernel = void (*)(const esq::DevQTensor*, uint64_t, uint64_t, unsigned long long*);
+
+QChecksumKernel qchecksum_kernel(int threads, int groups) {
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_qchecksum_kernel<T, U>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -1677,12 +1748,32 @@ int es_plan_checksum(es_plan_t* plan, uint64_t* out_dev, es_stream_t stream) {
     hipLaunchKernelGGL(es_zero_u64_kernel, dim3(1), dim3(64), 0, s, out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_zero_u64_kernel launch");
-    const uint64_t n_tiles = plan->n_full + plan->n_tail;
-    if (n_tiles == 0) return ES_OK;
+    if (plan->n_full + plan->n_tail == 0) return ES_OK;
     hipLaunchKernelGGL(checksum_kernel(plan->threads, plan->groups), dim3(plan->grid_update),
-                       dim3(plan->threads), 0, s, plan->d_tiles, plan->n_full, n_tiles, out);
+                       dim3(plan->threads), 0, s, plan->d_tiles, plan->n_full, plan->n_tail, out);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_checksum_kernel launch");
+    return ES_OK;
+}
+
+int es_qplan_checksum(es_qplan_t* plan, uint64_t* out_dev, es_stream_t stream) {
+    if (plan == nullptr || out_dev == nullptr)
+        return fail(ES_ERR_INVALID_ARG, "es_qplan_checksum: null pointer");
+    if (reinterpret_cast<uintptr_t>(out_dev) % 8 != 0)
+        return fail(ES_ERR_ALIGN, "es_qplan_checksum: output not 8-byte aligned");
+    int rc = check_qdevice(plan);
+    if (rc == ES_OK) rc = check_access(out_dev, 8, plan->device, "es_qplan_checksum: output");
+    if (rc != ES_OK) return rc;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    unsigned long long* out = reinterpret_cast<unsigned long long*>(out_dev);
+    hipLaunchKernelGGL(es_zero_u64_kernel, dim3(1), dim3(64), 0, s, out);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_zero_u64_kernel launch");
+    if (plan->n_full + plan->n_tail == 0) return ES_OK;
+    hipLaunchKernelGGL(qchecksum_kernel(plan->threads, plan->groups), dim3(plan->grid),
+                       dim3(plan->threads), 0, s, plan->d_tab, plan->n_full, plan->n_tail, out);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_qchecksum_kernel launch");
     return ES_OK;
 }
 

@@ -74,6 +74,7 @@ SIGNATURES = {
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
     "es_qplan_device_bytes": (_u64, [_vp]),
+    "es_qplan_checksum": (ctypes.c_int, [_vp, _vp, _vp]),
     "es_qperturb": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_qrestore": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_qupdate": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
@@ -235,18 +236,7 @@ class Plan:
         `out`, returns it as a Python int (synchronising); with `out`, a
         one-element int64 tensor on the plan's device, the value (its bits)
         is left there, stream-ordered, and `out` is returned."""
-        ret = out is None
-        if ret:
-            out = torch.empty(1, dtype=torch.int64, device=self.device)
-        elif out.numel() != 1 or out.device != self.device:
-            raise ValueError("out must be a one-element tensor on the plan's device")
-        _check(load().es_plan_checksum(self.handle, _dev_ptr(out, torch.int64, "out"),
-                                       _stream(stream)), "es_plan_checksum")
-        if not ret:
-            return out
-        if stream is not None:
-            torch.cuda.synchronize(self.device)
-        return int(out.item()) & ((1 << 64) - 1)
+        return _call_checksum(load().es_plan_checksum, "es_plan_checksum", self, out, stream)
 
     def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
         """Revert member `from` and apply member `to` in one pass: the same
@@ -279,6 +269,20 @@ class Plan:
 
     def __exit__(self, *exc):
         self.close()
+
+
+def _call_checksum(fn, what, plan, out, stream):
+    ret = out is None
+    if ret:
+        out = torch.empty(1, dtype=torch.int64, device=plan.device)
+    elif out.numel() != 1 or out.device != plan.device:
+        raise ValueError("out must be a one-element tensor on the plan's device")
+    _check(fn(plan.handle, _dev_ptr(out, torch.int64, "out"), _stream(stream)), what)
+    if not ret:
+        return out
+    if stream is not None:
+        torch.cuda.synchronize(plan.device)
+    return int(out.item()) & ((1 << 64) - 1)
 
 
 def _call_update(fn, what, handle, seeds, signs, rewards, alpha, sigma, zscore_eps, flags,
@@ -353,6 +357,10 @@ class QPlan:
     def restore(self, seed, sign, sigma, stream=None):
         _check(load().es_qrestore(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
                                   _stream(stream)), "es_qrestore")
+
+    def checksum(self, out=None, stream=None):
+        """64-bit checksum of the codes (es_qplan_checksum); as Plan.checksum."""
+        return _call_checksum(load().es_qplan_checksum, "es_qplan_checksum", self, out, stream)
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                z_out=None, status_out=None, stream=None, round_seed=0):

@@ -148,3 +148,48 @@ def test_replay_verifies_recorded_checksums():
     records[1].rewards[0] += 0.25          # a wrong log entry
     with esopt.Plan(bad) as p, pytest.raises(ReplayMismatch, match="generation 1"):
         replay(p, records)
+
+
+def _qset():
+    """int8 codes of ragged sizes, one at byte offset 3 of its buffer, with
+    per-row and per-tensor scales."""
+    rng = np.random.default_rng(12)
+    sizes, rows = [1, 15, 16 * 4096 + 5, 65536 * 2 + 7, 300_001], [0, 8, 16, 1024, 0]
+    codes = [rng.integers(-128, 128, size=n).astype(np.int8) for n in sizes]
+    bufs = [torch.from_numpy(np.concatenate([np.zeros(3, np.int8), c])).cuda() for c in codes]
+    views = [b[3:] if i == 3 else b[3:].clone() for i, b in enumerate(bufs)]
+    scales = [torch.full((1 if r == 0 else -(-n // r),), 2e-4, dtype=torch.float32, device="cuda")
+              for n, r in zip(sizes, rows)]
+    return codes, views, scales, rows, [4, 0, 9, 2, 77]
+
+
+def test_int8_plan_checksum_matches_oracle():
+    codes, views, scales, rows, ids = _qset()
+    with esopt.QPlan(views, scales, rows, tensor_ids=ids) as p:
+        got = p.checksum()
+        p.perturb(3, 1, 1e-3)
+        moved = p.checksum()
+    torch.cuda.synchronize()
+    exp = 0
+    for c, i in zip(codes, ids):
+        exp = (exp + oracle.qchecksum(c, i)) & M
+    assert got == exp
+    after = 0
+    for v, i in zip(views, ids):
+        after = (after + oracle.qchecksum(v.cpu().numpy(), i)) & M
+    assert moved == after != got
+
+
+def test_int8_replay_verifies_recorded_checksums():
+    codes, views, scales, rows, ids = _qset()
+    rng = np.random.default_rng(5)
+    with esopt.QPlan(views, scales, rows, tensor_ids=ids) as p:
+        records = [run_generation(p, *antithetic_seeds(20 * t, 2), 1e-3, 5e-4,
+                                  evaluate=lambda i: rng.random(), checksum=True,
+                                  round_seed=500 + t) for t in range(3)]
+        final = p.checksum()
+    assert records[-1].checksum == final
+    _, again, scales2, _, _ = _qset()
+    with esopt.QPlan(again, scales2, rows, tensor_ids=ids) as p:
+        replay(p, records)
+        assert p.checksum() == final
