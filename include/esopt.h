@@ -318,8 +318,9 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n,
  * tile-sized, starting where the address is a multiple of the tile's byte
  * size), then tail tiles.  Writes min(cap, count) entries to `out` (which
  * may be NULL when cap is 0) and the count to *n_tiles.  Errors: INVALID_ARG
- * for a null n_tiles or 8 * offset8 + numel > 2^60, ALIGN for an odd
- * address. */
+ * for a null n_tiles, 8 * offset8 + numel > 2^60, or more than 2^22 tiles
+ * (2^38 elements with the default tiles: the hook builds the whole list on
+ * the host), ALIGN for an odd address. */
 typedef struct es_tile_info {
     uint64_t elem0;
     uint64_t end;

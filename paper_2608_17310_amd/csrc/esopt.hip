@@ -51,6 +51,7 @@
 #include <cstdlib>
 #include <cstddef>
 #include <cstring>
+#include <new>
 #include <string>
 #include <unordered_map>
 #include <vector>
@@ -123,6 +124,7 @@ constexpr size_t kOffHeader = kOffMembers + sizeof(Member) * ES_MAX_MEMBERS;
 constexpr size_t kScratchBytes = kOffHeader + 256;
 
 constexpr int kStageWords = 256;            // 1 KB of kernel arguments per launch
+constexpr uint64_t kMaxLayoutTiles = uint64_t(1) << 22;   // es_tile_layout's bound
 struct StageChunk {
     uint32_t words[kStageWords];
 };
@@ -1382,7 +1384,7 @@ int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* sig
 
 extern "C" {
 
-int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out) {
+int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out) try {
     if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null output pointer");
     *out = nullptr;
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create: null tensor list");
@@ -1467,6 +1469,8 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     }
     *out = p;
     return ES_OK;
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_plan_create: host allocation failed");
 }
 
 int es_plan_destroy(es_plan_t* plan) {
@@ -1516,7 +1520,7 @@ int es_zscore(const float* rewards_dev, uint32_t n, float eps, float* z_dev, int
 
 int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
-              float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) {
+              float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) try {
     if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_update: null plan");
     int rc = validate_update("es_update", seeds, signs, rewards_dev, n_members, opts);
     if (rc != ES_OK) return rc;
@@ -1541,6 +1545,8 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
     return ES_OK;
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_update: host allocation failed");
 }
 
 int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
@@ -1573,7 +1579,7 @@ int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_
     return launch_streams(plan, streams, sd, cf, static_cast<hipStream_t>(stream));
 }
 
-int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out) {
+int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out) try {
     if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null output pointer");
     *out = nullptr;
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null tensor list");
@@ -1677,6 +1683,8 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
     }
     *out = p;
     return ES_OK;
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation failed");
 }
 
 int es_qplan_destroy(es_qplan_t* plan) {
@@ -1703,7 +1711,7 @@ int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_s
 
 int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
                const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
-               float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) {
+               float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) try {
     if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qupdate: null plan");
     int rc = validate_update("es_qupdate", seeds, signs, rewards_dev, n_members, opts);
     if (rc != ES_OK) return rc;
@@ -1720,6 +1728,8 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
     ps.dk0 = static_cast<uint32_t>(opts->round_seed);
     ps.dk1 = static_cast<uint32_t>(opts->round_seed >> 32);
     return launch_qpass(plan, QKind::kUpdate, ps, s);
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_qupdate: host allocation failed");
 }
 
 int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
@@ -1824,7 +1834,7 @@ int es_normals(uint64_t seed, uint32_t tensor_id, uint64_t elem0, uint64_t n, fl
 }
 
 int es_tile_layout(uint64_t addr, uint64_t numel, uint32_t offset8, es_tile_info_t* out,
-                   uint64_t cap, uint64_t* n_tiles) {
+                   uint64_t cap, uint64_t* n_tiles) try {
     if (n_tiles == nullptr) return fail(ES_ERR_INVALID_ARG, "es_tile_layout: null n_tiles");
     *n_tiles = 0;
     if (numel > (uint64_t(1) << 60) - 8 * uint64_t(offset8))
@@ -1833,9 +1843,12 @@ int es_tile_layout(uint64_t addr, uint64_t numel, uint32_t offset8, es_tile_info
     if (numel > 0 && (addr & 1u)) return fail(ES_ERR_ALIGN, "es_tile_layout: address not 2-byte aligned");
     int threads = 0, groups = 0;
     launch_shape(threads, groups);
+    const uint64_t tile_elems = uint64_t(threads) * groups * kGroupElems;
+    if (numel / tile_elems > kMaxLayoutTiles)
+        return fail(ES_ERR_INVALID_ARG, "es_tile_layout: more than 2^22 tiles");
     std::vector<DevTile> full, tail;
     tile_tensor(reinterpret_cast<uint16_t*>(static_cast<uintptr_t>(addr)), numel,
-                8 * uint64_t(offset8), 0u, uint64_t(threads) * groups * kGroupElems, full, tail);
+                8 * uint64_t(offset8), 0u, tile_elems, full, tail);
     const uint64_t n = full.size() + tail.size();
     for (uint64_t i = 0; i < std::min(cap, n); ++i) {
         const DevTile& d = i < full.size() ? full[i] : tail[i - full.size()];
@@ -1843,6 +1856,8 @@ int es_tile_layout(uint64_t addr, uint64_t numel, uint32_t offset8, es_tile_info
     }
     *n_tiles = n;
     return ES_OK;
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_tile_layout: host allocation failed");
 }
 
 const char* es_strerror(int code) {

@@ -96,5 +96,8 @@ def test_validation():
     assert lib.es_tile_layout(2, (1 << 60) + 1, 0, None, 0, br(n)) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_tile_layout(2, (1 << 60) - 7, 1, None, 0, br(n)) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_tile_layout(2, 10, 0, None, 5, br(n)) == esopt.ES_ERR_INVALID_ARG
+    # the host-side list is bounded: 2^40 elements would be 2^24 tiles
+    assert lib.es_tile_layout(2, 1 << 40, 0, None, 0, br(n)) == esopt.ES_ERR_INVALID_ARG
+    assert "2^22" in esopt.last_error()
     with pytest.raises(ValueError):
         esopt.tile_layout(2, 10, offset=4)              # not a multiple of 8
