@@ -133,6 +133,34 @@ def cpu_baseline(W, seeds, signs, rewards, sigma, theta_samples, workers, budget
                       f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
 
 
+def flat_ceilings(esopt, stream, gib=16):
+    """Read-only, write-only and in-place rates of the device's memory over a
+    flat buffer (es_hbm_calibrate: the perturb's tile shape and launch),
+    medians of three passes each; the in-place rate counts read and written
+    bytes, like the passes' algorithmic rates."""
+    import torch
+    cal = torch.empty(gib << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = {"buffer_bytes": cal.numel()}
+    for name, mode, factor in (("read_GBps", esopt.CALIBRATE_READ, 1),
+                               ("write_GBps", esopt.CALIBRATE_WRITE, 1),
+                               ("in_place_GBps", esopt.CALIBRATE_READ_WRITE, 2)):
+        esopt.hbm_calibrate(cal, mode, sink)
+        ts = []
+        for _ in range(3):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            esopt.hbm_calibrate(cal, mode, sink)
+            e1.record(stream)
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        out[name] = round(factor * cal.numel() / (float(np.median(ts)) / 1e3) / 1e9, 1)
+    del cal
+    torch.cuda.empty_cache()
+    return out
+
+
 def host_cpu():
     """The host's CPU model (from /proc/cpuinfo) and logical CPU count."""
     model = None
@@ -535,6 +563,7 @@ def main():
         e1.synchronize()
         ts.append(e0.elapsed_time(e1))
     ceiling_gbs = 4 * P / (float(np.median(ts)) / 1e3) / 1e9
+    flat_rates = flat_ceilings(esopt, stream)
     c_pert = _counters_for(args.counters_json, "es_perturb", W.name)
     c_upd = _counters_for(args.counters_json, "es_update", W.name)
     traffic = c_pert["bytes_per_launch"] if c_pert else None
@@ -545,7 +574,8 @@ def main():
                 "algorithmic_bytes_per_launch": 4 * P,
                 "ceiling": {"GBps": round(ceiling_gbs, 1),
                             "frac_of_ceiling": round(perturb_gbs / ceiling_gbs, 4),
-                            "kernel": "es_stream_kernel: in-place copy of every parameter, same tiles (es_stream_pass)"}}
+                            "kernel": "es_stream_kernel: in-place copy of every parameter, same tiles (es_stream_pass)"},
+                "flat_buffer_ceilings": flat_rates}
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
               "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
               "normals_per_s": n_live * P / t_upd, "distinct_seeds": n_distinct,

@@ -298,6 +298,21 @@ double es_sigma_cosine(double sigma0, double sigma_T, uint32_t t, uint32_t T);
  * ceiling against which es_perturb's bandwidth is measured. */
 int es_stream_pass(es_plan_t* plan, es_stream_t stream);
 
+/* HBM calibration over a caller's flat device buffer of `bytes` bytes (a
+ * positive multiple of 131072, 16-byte aligned), with the tile shape and
+ * launch of es_perturb: 1024 lanes x 8 16-byte words per tile, one workgroup
+ * per compute unit, nontemporal accesses, each tile loaded whole, then
+ * stored.  mode 0 reads every word (their XOR is folded into *sink_dev, a
+ * device uint32, with one atomic per wave, so the reads are not dead code);
+ * mode 1 writes every word (the buffer's contents become a pattern: the
+ * 16-byte word of lane l in group u of tile t holds (t, u, l, 0)); mode 2
+ * reads every word and writes it back unchanged.  With es_stream_pass these
+ * give the practical read, write and in-place ceilings of the device's
+ * memory against which the passes' bandwidth is read.  sink_dev is ignored
+ * unless mode is 0. */
+int es_hbm_calibrate(void* buf_dev, uint64_t bytes, int32_t mode, uint32_t* sink_dev,
+                     es_stream_t stream);
+
 /* Test hooks exposing the device noise functions the kernels use.
  * es_philox_words: out_dev[4 i + k] = word k of the Philox call at counter
  *   (q & 0xffffffff, q >> 32, tensor_id, domain), q = quad0 + i,

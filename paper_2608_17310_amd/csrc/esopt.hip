@@ -559,6 +559,50 @@ __global__ __launch_bounds__(64) void es_zero_u64_kernel(unsigned long long* __r
     if (threadIdx.x == 0) *p = 0ull;
 }
 
+// HBM calibration over a caller's flat buffer (es_hbm_calibrate), with the
+// perturb's workgroup and tile shape: kThreads lanes x kU 16-byte words per
+// tile, nontemporal accesses, each tile loaded whole and then stored.  kMode
+// 0 reads every word (their XOR leaves in one atomic per wave, so the loads
+// are live), 1 writes every word (the pattern tile, u, lane, 0), 2 reads
+// every word and writes it back (XOR with `flip`, which the host passes as
+// 0, so the stores are kept).
+template <int kThreads, int kU, int kMode>
+__global__ __launch_bounds__(kThreads) void es_calibrate_kernel(u32x4_t* __restrict__ buf,
+                                                                uint64_t n_tiles,
+                                                                uint32_t* __restrict__ sink,
+                                                                uint32_t flip) {
+    uint32_t acc = 0;
+    for (uint64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+        ES_GLOBAL u32x4_t* base =
+            (ES_GLOBAL u32x4_t*)buf + tile * (uint64_t(kThreads) * kU) + threadIdx.x;
+        u32x4_t v[kU];
+        if constexpr (kMode != 1) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(base + u * kThreads);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (kMode == 0) {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+        } else {
+#pragma unroll
+            for (int u = 0; u < kU; ++u) {
+                if constexpr (kMode == 1) {
+                    v[u] = u32x4_t{static_cast<uint32_t>(tile), uint32_t(u), threadIdx.x, 0u};
+                } else {
+                    v[u].x ^= flip; v[u].y ^= flip; v[u].z ^= flip; v[u].w ^= flip;
+                }
+                __builtin_nontemporal_store(v[u], base + u * kThreads);
+            }
+        }
+    }
+    if constexpr (kMode == 0) {
+#pragma unroll
+        for (int off = 32; off > 0; off >>= 1) acc ^= __shfl_xor(acc, off, 64);
+        if ((threadIdx.x & 63u) == 0u) atomicXor(sink, acc);
+    }
+}
+
 // w == +-0, tested on the bit pattern so that the member loop's skip stays on
 // the scalar unit (a binary32 compare would be a vector instruction).
 __device__ __forceinline__ bool is_zero_weight(float w) {
@@ -1742,6 +1786,44 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
                        plan->n_full, plan->n_tail, 0u);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
+    return ES_OK;
+}
+
+int es_hbm_calibrate(void* buf_dev, uint64_t bytes, int32_t mode, uint32_t* sink_dev,
+                     es_stream_t stream) {
+    constexpr uint64_t kTileBytes = uint64_t(kDefaultThreads) * kDefaultGroups * 16;
+    if (buf_dev == nullptr || (mode == 0 && sink_dev == nullptr))
+        return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: null pointer");
+    if (mode < 0 || mode > 2) return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: mode not 0, 1 or 2");
+    if (bytes == 0 || bytes % kTileBytes != 0)
+        return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: bytes not a positive multiple of 131072");
+    if (reinterpret_cast<uintptr_t>(buf_dev) % 16 != 0 ||
+        (mode == 0 && reinterpret_cast<uintptr_t>(sink_dev) % 4 != 0))
+        return fail(ES_ERR_ALIGN, "es_hbm_calibrate: buffer not 16-byte aligned");
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc == ES_OK) rc = check_access(buf_dev, bytes, device, "es_hbm_calibrate: buffer");
+    if (rc == ES_OK && mode == 0)
+        rc = check_access(sink_dev, 4, device, "es_hbm_calibrate: sink");
+    if (rc != ES_OK) return rc;
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+    if (e != hipSuccess) return hip_fail(e, "hipDeviceGetAttribute");
+    const uint64_t n_tiles = bytes / kTileBytes;
+    const dim3 grid(static_cast<uint32_t>(std::min<uint64_t>(n_tiles, uint64_t(cus))));
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    u32x4_t* buf = static_cast<u32x4_t*>(buf_dev);
+    if (mode == 0)
+        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 0>), grid,
+                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
+    else if (mode == 1)
+        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 1>), grid,
+                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
+    else
+        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 2>), grid,
+                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
+    e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "es_calibrate_kernel launch");
     return ES_OK;
 }
 

@@ -67,6 +67,7 @@ SIGNATURES = {
     "es_swap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
     "es_stream_pass": (ctypes.c_int, [_vp, _vp]),
     "es_plan_checksum": (ctypes.c_int, [_vp, _vp, _vp]),
+    "es_hbm_calibrate": (ctypes.c_int, [_vp, _u64, _i32, _vp, _vp]),
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
@@ -394,6 +395,22 @@ def zscore(rewards, eps=1e-8, out=None, status=None, stream=None):
                             float(eps), _dev_ptr(out, torch.float32, "out"),
                             _dev_ptr(status, torch.int32, "status"), _stream(stream)), "es_zscore")
     return out
+
+
+CALIBRATE_READ, CALIBRATE_WRITE, CALIBRATE_READ_WRITE = 0, 1, 2
+
+
+def hbm_calibrate(buf, mode, sink=None, stream=None):
+    """One es_hbm_calibrate pass over the contiguous CUDA tensor `buf` (its
+    byte size a multiple of 131072): mode CALIBRATE_READ (the words' XOR is
+    folded into `sink`, a one-element int32 CUDA tensor), CALIBRATE_WRITE (buf
+    is overwritten) or CALIBRATE_READ_WRITE (buf unchanged)."""
+    if not buf.is_cuda or not buf.is_contiguous():
+        raise ValueError("buf must be a contiguous CUDA tensor")
+    sp = None if sink is None else _dev_ptr(sink, torch.int32, "sink")
+    _check(load().es_hbm_calibrate(ctypes.c_void_p(buf.data_ptr()),
+                                   buf.numel() * buf.element_size(), int(mode), sp,
+                                   _stream(stream)), "es_hbm_calibrate")
 
 
 def sigma_cosine(sigma0, sigma_T, t, T):

@@ -107,6 +107,13 @@ def test_call_validation_without_device(lib):
     assert lib.es_plan_checksum(None, fake, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_plan_checksum(fake, None, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_plan_checksum(fake, ctypes.c_void_p(0x1004), None) == esopt.ES_ERR_ALIGN
+    C = lib.es_hbm_calibrate
+    assert C(None, 1 << 17, 1, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert C(fake, 1 << 17, 0, None, None) == esopt.ES_ERR_INVALID_ARG      # read needs a sink
+    assert C(fake, 1 << 17, 3, fake, None) == esopt.ES_ERR_INVALID_ARG
+    assert C(fake, (1 << 17) + 16, 1, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert C(fake, 0, 1, None, None) == esopt.ES_ERR_INVALID_ARG
+    assert C(ctypes.c_void_p(0x1008), 1 << 17, 1, None, None) == esopt.ES_ERR_ALIGN
     assert lib.es_plan_destroy(None) == esopt.ES_OK
     assert lib.es_plan_numel(None) == 0
 
