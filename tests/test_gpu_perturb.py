@@ -53,6 +53,10 @@ def test_tiny_config_perturb_restore():
                                      seed, i, sign, W.sigma0)
             el = np.arange(got.size, dtype=np.uint64)
             rep = report(got, chained, before[i], perturb_delta(seed, i, sign, W.sigma0, el))
+            # two roundings compound here (a perturb-stage 1-ulp tie carries
+            # into the restore), so the share allowed above 1 ulp is the
+            # bar's 1e-4 per pass, twice; the isolated check above holds the
+            # restore alone to the bar itself
             assert rep["max_ulp"] <= 2.0 and rep["le1"] >= 0.9998, rep
             drift = np.mean(got != before[i])
             assert drift < 0.1, drift
