@@ -41,8 +41,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="dense-27b")
     ap.add_argument("--members", type=int, default=None, help="override N (distinct seeds)")
-    ap.add_argument("--swap", action="store_true",
-                    help="move between members with the fused es_swap (N+1 passes per step)")
+    ap.add_argument("--no-swap-walk", action="store_true",
+                    help="do not time the same generations with fused swaps")
     ap.add_argument("--sweep-members", default=None, metavar="N1,N2,...",
                     help="large-population sweep of the fused update on the 4B-shaped set "
                          "(one JSON line per N)")
@@ -55,11 +55,16 @@ def parse():
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-pass", action="store_true",
-                    help="run one perturb, one update and a calibration copy, for rocprofv3")
+                    help="launch every kernel once per label for rocprofv3 (with --sweep-members: "
+                         "one update per N)")
+    ap.add_argument("--labels-dir", default=None,
+                    help="where a profile pass writes labels.json")
     ap.add_argument("--counters-json", default=os.path.join(REPO, "profiles", "counters.json"),
                     help="per-launch counter values measured with rocprofv3 (see --summarize)")
-    ap.add_argument("--summarize", nargs=4, metavar=("TRACE_DIR", "FETCH_DIR", "WRITE_DIR", "VALU_DIR"),
-                    help="turn rocprofv3 CSV output of the profiling runs into profiles/")
+    ap.add_argument("--summarize", default=None, metavar="OUT_DIR",
+                    help="turn the rocprofv3 runs of a profile pass (OUT_DIR/trace, fetch, write, "
+                         "valu) into profiles/")
+
     return ap.parse_args()
 
 
@@ -84,10 +89,25 @@ def live_seeds(seeds, signs, rewards):
     return sum(1 for v in acc.values() if v != 0.0)
 
 
-def sigma_at(W, t):
-    if W.sigma0 == W.sigma_T:
-        return W.sigma0
-    return W.sigma_T + (W.sigma0 - W.sigma_T) * (1 + math.cos(math.pi * (t % W.T) / W.T)) / 2
+def sigma_at(sigma_cosine, W, t):
+    """sigma_t of generation t on the cosine schedule of Section 3.1, from the
+    library's es_sigma_cosine (the GPU leg) or the oracle's (the CPU leg);
+    generations past the schedule's last update keep sigma_T."""
+    return sigma_cosine(W.sigma0, W.sigma_T, min(t, W.T), W.T)
+
+
+CPU_WORKER_CAP = 16    # CPU share of one GPU slot on a shared host
+
+
+def cpu_workers():
+    """Worker processes of the CPU leg: every CPU this process may run on
+    (its affinity mask), capped at CPU_WORKER_CAP.  Returns (workers,
+    available CPUs)."""
+    try:
+        avail = len(os.sched_getaffinity(0))
+    except AttributeError:
+        avail = os.cpu_count() or 1
+    return max(1, min(avail, CPU_WORKER_CAP)), avail
 
 
 # ---------------------------------------------------------------- CPU leg --
@@ -162,7 +182,8 @@ def flat_ceilings(esopt, stream, gib=16):
 
 
 def host_cpu():
-    """The host's CPU model (from /proc/cpuinfo) and logical CPU count."""
+    """The host's CPU model (from /proc/cpuinfo), its logical CPU count, the
+    CPUs this process may use and the cap on worker processes."""
     model = None
     try:
         with open("/proc/cpuinfo") as fh:
@@ -172,7 +193,8 @@ def host_cpu():
                     break
     except OSError:
         pass
-    return {"cpu_model": model, "host_logical_cpus": os.cpu_count()}
+    return {"cpu_model": model, "host_logical_cpus": os.cpu_count(),
+            "cpus_available": cpu_workers()[1], "worker_cap": CPU_WORKER_CAP}
 
 
 def host_samples(W, per_tensor=1 << 16):
@@ -267,6 +289,27 @@ def run_sweep(args):
             ts.append(e0.elapsed_time(e1))
         return float(np.median(ts))
 
+    if args.profile_pass:
+        log = ProfileLog(args.labels_dir)
+        log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
+                plan.stream_pass, members=0)
+        for n in ns:
+            Wn = wl.sweep_workload(n)
+            r = torch.from_numpy(wl.rewards(Wn)).cuda()
+            flags = esopt.ES_REWARDS_ARE_WEIGHTS if n == 1 else 0
+            log.add(f"es_update (N={n})", "update", P, 4 * P, n * P, plan.update, list(Wn.seeds),
+                    list(Wn.signs), r, Wn.alpha, flags=flags, members=n)
+        torch.cuda.synchronize()
+        plan.close()
+        del flat, views
+        torch.cuda.empty_cache()
+        calibration_copy(torch)
+        torch.cuda.synchronize()
+        log.write({"sweep": True, "workload": W.name, "params": P,
+                   "source_hash": _kernel_source_hash(),
+                   "pass_args": f"--sweep-members {args.sweep_members} --profile-pass"})
+        print(json.dumps({"profile_pass": W.name + " sweep", "launches": len(log.rows)}))
+        return
     # the practical HBM floor of any pass over these tiles: the in-place copy
     stream_t = median_ms(plan.stream_pass) / 1e3
     for n in ns:
@@ -308,10 +351,12 @@ def run_int8(args):
     signs = list(W.signs) if n_members is None else [1] * n_members
     N = len(signs)
     cpu = None
-    if not args.no_cpu_baseline and not args.profile_pass:
+    if not args.no_cpu_baseline:
+        import oracle
         cpu = cpu_baseline_int8(W, step_seeds(W, args.warmup, n_members), signs,
-                                wl.rewards(W, args.warmup, n=N), sigma_at(W, args.warmup),
-                                min(16, os.cpu_count() or 1), args.cpu_seconds)
+                                wl.rewards(W, args.warmup, n=N),
+                                sigma_at(oracle.sigma_cosine, W, args.warmup),
+                                cpu_workers()[0], args.cpu_seconds)
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU"}))
         sys.exit(1)
@@ -324,62 +369,24 @@ def run_int8(args):
     rewards_np = np.stack([wl.rewards(W, t, n=N) for t in range(total_steps)])
     rewards_all = torch.from_numpy(rewards_np).cuda()
     torch.cuda.synchronize()
-    if args.profile_pass:
-        seeds = step_seeds(W, 0, n_members)
-        plan.perturb(seeds[0], signs[0], W.sigma0)
-        plan.restore(seeds[0], signs[0], W.sigma0)
-        plan.update(seeds, signs, rewards_all[0], W.alpha, sigma=W.sigma0, round_seed=1)
-        calib = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")     # 1 GiB copy
-        torch.empty_like(calib).copy_(calib)
-        torch.cuda.synchronize()
-        print(json.dumps({"profile_pass": W.name + "-int8", "params": P, "members": N,
-                          "calibration_copy_bytes": 1 << 30}))
-        return
-    ev = []
-
-    def timed(kind, record, fn, *a, **kw):
-        if record:
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn(*a, **kw)
-            e1.record(stream)
-            ev.append((kind, e0, e1))
-        else:
-            fn(*a, **kw)
+    log = EventLog(torch, stream)
 
     def run_step(t, record):
         seeds = step_seeds(W, t, n_members)
-        sigma = sigma_at(W, t)
+        sigma = sigma_at(esopt.sigma_cosine, W, t)
         for sd, sg in zip(seeds, signs):
-            timed("es_qperturb", record, plan.perturb, sd, sg, sigma)
-            timed("es_qrestore", record, plan.restore, sd, sg, sigma)
-        timed("es_qupdate", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
-              sigma=sigma, round_seed=1000 + t)
+            log.call("es_qperturb", record, plan.perturb, sd, sg, sigma)
+            log.call("es_qrestore", record, plan.restore, sd, sg, sigma)
+        log.call("es_qupdate", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
+                 sigma=sigma, round_seed=1000 + t)
 
     for t in range(args.warmup):
         run_step(t, record=False)
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    # no garbage-collector pause inside the timed region (one measured 35 ms
-    # on a small set, where the GPU waits on the host)
-    gc.collect()
-    gc.disable()
-    t_wall0 = time.perf_counter()
-    start.record(stream)
-    for t in range(args.warmup, total_steps):
-        run_step(t, record=True)
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall0
-    gc.enable()
-    ms_step = start.elapsed_time(end) / args.steps
-    per = {}
-    for kind, a, b in ev:
-        per.setdefault(kind, []).append(a.elapsed_time(b))
-    t_pert = float(np.mean(per["es_qperturb"] + per["es_qrestore"])) / 1e3
-    t_upd = float(np.mean(per["es_qupdate"])) / 1e3
+    ms_step, wall = timed_region(torch, stream, args.steps,
+                                 lambda i: run_step(args.warmup + i, record=True))
+    per = log.ms()
+    t_pert = median_s(per["es_qperturb"] + per["es_qrestore"])
+    t_upd = median_s(per["es_qupdate"])
     value = (2 * N + 1) * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
@@ -421,6 +428,7 @@ def run_int8(args):
             "es_qupdate": {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
                            "normals_per_s": n_live * P / t_upd,
                            "distinct_seeds": n_distinct, "live_seeds": round(n_live, 3)}},
+        "timing": "per-kernel figures are medians of HIP event pairs on the launch stream",
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
@@ -428,10 +436,59 @@ def run_int8(args):
     plan.close()
 
 
+class EventLog:
+    """HIP events recorded on the launch stream around each timed launch;
+    per-kind durations are reported as medians."""
+
+    def __init__(self, torch, stream):
+        self.torch, self.stream, self.ev = torch, stream, []
+
+    def call(self, kind, record, fn, *a, **kw):
+        if not record:
+            return fn(*a, **kw)
+        e0 = self.torch.cuda.Event(enable_timing=True)
+        e1 = self.torch.cuda.Event(enable_timing=True)
+        e0.record(self.stream)
+        out = fn(*a, **kw)
+        e1.record(self.stream)
+        self.ev.append((kind, e0, e1))
+        return out
+
+    def ms(self):
+        per = {}
+        for kind, a, b in self.ev:
+            per.setdefault(kind, []).append(a.elapsed_time(b))
+        return per
+
+
+def median_s(xs_ms):
+    return float(np.median(xs_ms)) / 1e3
+
+
+def timed_region(torch, stream, steps, fn):
+    """Run fn(i) for i < steps between two events on the launch stream, with
+    the host's garbage collector off (a 35 ms collector pause was once seen
+    inside a short step); returns (ms per step, wall seconds)."""
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    gc.collect()
+    gc.disable()
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for i in range(steps):
+        fn(i)
+    end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall0
+    gc.enable()
+    return start.elapsed_time(end) / steps, wall
+
+
 def main():
     args = parse()
     if args.summarize:
-        summarize(*args.summarize, workload=args.workload, int8=args.int8)
+        summarize(args.summarize)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the ES parameter path runs on one GPU; --gpus above 1 is "
@@ -440,22 +497,29 @@ def main():
         sys.exit(2)
     if args.sweep_members:
         return run_sweep(args)
+    if args.profile_pass:
+        return run_profile_pass(args)
     if args.int8:
         return run_int8(args)
     import torch
-    from paper_2608_17310_amd import esopt, workloads as wl
+    from paper_2608_17310_amd import workloads as wl
 
     W = wl.WORKLOADS[args.workload]
     n_members = args.members
     signs = list(W.signs) if n_members is None else [1] * n_members
     N = len(signs)
     cpu = None
-    if not args.no_cpu_baseline and not args.profile_pass:
-        # before the GPU is touched: worker processes fork from a clean parent
+    if not args.no_cpu_baseline:
+        # before the GPU (or the HIP library) is touched: worker processes
+        # fork from a clean parent; sigma from the oracle's schedule
+        import oracle
+        workers, _ = cpu_workers()
         cpu = cpu_baseline(W, step_seeds(W, args.warmup, n_members), signs,
-                           wl.rewards(W, args.warmup, n=N), sigma_at(W, args.warmup),
-                           host_samples(W), min(16, os.cpu_count() or 1), args.cpu_seconds)
+                           wl.rewards(W, args.warmup, n=N),
+                           sigma_at(oracle.sigma_cosine, W, args.warmup),
+                           host_samples(W), workers, args.cpu_seconds)
 
+    from paper_2608_17310_amd import esopt
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU"}))
         sys.exit(1)
@@ -469,127 +533,101 @@ def main():
     rewards_all = torch.from_numpy(rewards_np).cuda()
     torch.cuda.synchronize()
 
-    if args.profile_pass:
-        seeds = step_seeds(W, 0, n_members)
-        plan.perturb(seeds[0], signs[0], W.sigma0)
-        plan.restore(seeds[0], signs[0], W.sigma0)
-        plan.update(seeds, signs, rewards_all[0], W.alpha, sigma=W.sigma0)
-        calib = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")     # 1 GiB copy
-        calib2 = torch.empty_like(calib)
-        calib2.copy_(calib)
-        torch.cuda.synchronize()
-        print(json.dumps({"profile_pass": W.name, "params": P, "members": N,
-                          "calibration_copy_bytes": 1 << 30}))
-        return
-
-    ev = []   # (kind, start, end) event pairs inside the timed region
+    log = EventLog(torch, stream)
     update_flags = esopt.ES_UPDATE_STOCHASTIC_ROUND if args.stochastic_round else 0
 
-    def timed_call(kind, record, fn, *a):
-        if record:
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn(*a)
-            e1.record(stream)
-            ev.append((kind, e0, e1))
-        else:
-            fn(*a)
-
-    def run_step(t, record):
+    def run_step(t, record, swap):
+        """One generation's parameter work: every member applied and reverted
+        (separate passes, or perturb, N - 1 fused swaps and restore), then the
+        fused update."""
         seeds = step_seeds(W, t, n_members)
-        sigma = sigma_at(W, t)
-        if args.swap:
-            timed_call("es_perturb", record, plan.perturb, seeds[0], signs[0], sigma)
+        sigma = sigma_at(esopt.sigma_cosine, W, t)
+        if swap:
+            log.call("es_perturb", record, plan.perturb, seeds[0], signs[0], sigma)
             for i in range(N - 1):
-                timed_call("es_swap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
-                           signs[i + 1], sigma)
-            timed_call("es_restore", record, plan.restore, seeds[-1], signs[-1], sigma)
+                log.call("es_swap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
+                         signs[i + 1], sigma)
+            log.call("es_restore", record, plan.restore, seeds[-1], signs[-1], sigma)
         else:
-            for s, sg in zip(seeds, signs):
-                timed_call("es_perturb", record, plan.perturb, s, sg, sigma)
-                timed_call("es_restore", record, plan.restore, s, sg, sigma)
-        if record:
-            a = torch.cuda.Event(enable_timing=True)
-            b = torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-        plan.update(seeds, signs, rewards_all[t], W.alpha, sigma=sigma, flags=update_flags,
-                    round_seed=1000 + t)
-        if record:
-            b.record(stream)
-            ev.append(("es_update", a, b))
+            for sd, sg in zip(seeds, signs):
+                log.call("es_perturb", record, plan.perturb, sd, sg, sigma)
+                log.call("es_restore", record, plan.restore, sd, sg, sigma)
+        log.call("es_update_swap" if swap else "es_update", record, plan.update, seeds, signs,
+                 rewards_all[t], W.alpha, sigma=sigma, flags=update_flags, round_seed=1000 + t)
 
     for t in range(args.warmup):
-        run_step(t, record=False)
-    torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    # no garbage-collector pause inside the timed region (one measured 35 ms
-    # on a small set, where the GPU waits on the host)
-    gc.collect()
-    gc.disable()
-    t_wall0 = time.perf_counter()
-    start.record(stream)
-    for t in range(args.warmup, total_steps):
-        run_step(t, record=True)
-    end.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t_wall0
-    gc.enable()
-    ms_total = start.elapsed_time(end)
-    ms_step = ms_total / args.steps
-    per = {}
-    for kind, a, b in ev:
-        per.setdefault(kind, []).append(a.elapsed_time(b))
-    t_pert = float(np.mean(per["es_perturb"] + per["es_restore"])) / 1e3
-    t_upd = float(np.mean(per["es_update"])) / 1e3
-    passes = (N + 2) if args.swap else (2 * N + 1)
-    value = passes * P / (ms_step / 1e3)
+        run_step(t, record=False, swap=False)
+    ms_step, wall = timed_region(torch, stream, args.steps,
+                                 lambda i: run_step(args.warmup + i, record=True, swap=False))
+    per = log.ms()
+    t_pert = median_s(per["es_perturb"] + per["es_restore"])
+    t_upd = median_s(per["es_update"])
+    value = (2 * N + 1) * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
                             for t in range(args.warmup, total_steps)]))
 
+    # the same generations with the members moved by fused swaps (perturb,
+    # N - 1 swaps, restore, update), timed in the same run after one untimed
+    # generation
+    swap = None
+    if not args.no_swap_walk and N > 1:
+        log.ev = []
+        run_step(args.warmup, record=False, swap=True)
+        ms_swap, wall_swap = timed_region(
+            torch, stream, args.steps, lambda i: run_step(args.warmup + i, record=True, swap=True))
+        per_sw = log.ms()
+        swap = {"ms_step": ms_swap, "wall": wall_swap, "t_swap": median_s(per_sw["es_swap"]),
+                "calls": len(per_sw["es_swap"])}
+
     # the practical in-place streaming ceiling over the same memory: the same
     # tiles and launch, loads and stores only, not pipelined (es_stream_pass),
-    # timed after the step
+    # timed after the steps; then the flat-buffer read / write / in-place rates
     plan.stream_pass()
-    ts = []
-    for _ in range(3):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        plan.stream_pass()
-        e1.record(stream)
-        e1.synchronize()
-        ts.append(e0.elapsed_time(e1))
-    ceiling_gbs = 4 * P / (float(np.median(ts)) / 1e3) / 1e9
+    log.ev = []
+    for _ in range(5):
+        log.call("es_stream_pass", True, plan.stream_pass)
+    t_stream = median_s(log.ms()["es_stream_pass"])
+    ceiling_gbs = 4 * P / t_stream / 1e9
     flat_rates = flat_ceilings(esopt, stream)
     c_pert = _counters_for(args.counters_json, "es_perturb", W.name)
     c_upd = _counters_for(args.counters_json, "es_update", W.name)
-    traffic = c_pert["bytes_per_launch"] if c_pert else None
+    c_swap = _counters_for(args.counters_json, "es_swap", W.name)
     perturb_gbs = 4 * P / t_pert / 1e9
     roofline = {"bound": "hbm", "achieved": round(perturb_gbs, 1), "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": round(perturb_gbs / HBM_PEAK_GBS, 4),
-                "traffic": traffic, "kernel": "es_perturb_kernel (es_perturb / es_restore)",
+                "traffic": c_pert["bytes_per_launch"] if c_pert else None,
+                "kernel": "es_perturb_kernel (es_perturb / es_restore)",
                 "algorithmic_bytes_per_launch": 4 * P,
                 "ceiling": {"GBps": round(ceiling_gbs, 1),
                             "frac_of_ceiling": round(perturb_gbs / ceiling_gbs, 4),
-                            "kernel": "es_stream_kernel: in-place copy of every parameter, same tiles (es_stream_pass)"},
+                            "kernel": "es_stream_kernel: in-place copy of every parameter, same "
+                                      "tiles (es_stream_pass)"},
                 "flat_buffer_ceilings": flat_rates}
+
+    def valu_roofline(c, t, kernel, comparable):
+        """A VALU-bound kernel against the VALU issue peak: instructions per
+        launch from counters (same workload and kernel sources), duration
+        live."""
+        r = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
+             "achieved": None, "frac": None, "kernel": kernel,
+             "traffic": c["bytes_per_launch"] if c else None}
+        if c and comparable:
+            ach = c["valu_insts_per_launch"] * 64 / t / 1e12
+            r.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
+        return r
+    default_pop = N == len(W.seeds) and n_members is None
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
               "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
               "normals_per_s": n_live * P / t_upd, "distinct_seeds": n_distinct,
               "live_seeds": round(n_live, 3)}
-    # The update is VALU-bound: its roofline is the VALU issue rate.  The
-    # instruction count per launch is a counter measurement (SQ_INSTS_VALU,
-    # same workload and kernel sources); the duration is live.
-    roofline_update = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
-                       "achieved": None, "frac": None,
-                       "kernel": "es_update_kernel (fused N-member update)",
-                       "traffic": c_upd["bytes_per_launch"] if c_upd else None}
-    if c_upd and N == len(W.seeds) and n_members is None and not args.stochastic_round:
-        ach = c_upd["valu_insts_per_launch"] * 64 / t_upd / 1e12
-        roofline_update.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
+    per_kernel = {
+        "es_perturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
+                       "GBps_algorithmic": round(perturb_gbs, 1),
+                       "frac_hbm_peak": round(perturb_gbs / HBM_PEAK_GBS, 4)},
+        "es_update": update,
+        "es_stream_pass": {"ms": round(t_stream * 1e3, 3), "GBps": round(ceiling_gbs, 1)},
+    }
     out = {
         "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
         "value": value,
@@ -601,26 +639,30 @@ def main():
         "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
                    "param_bytes": 2 * P, "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
-                   "member_moves": "es_swap" if args.swap else "es_perturb/es_restore",
+                   "member_moves": "es_perturb/es_restore",
                    "update_rounding": "stochastic" if args.stochastic_round else "nearest-even",
-                   "counting": ("value = (N+2) P / step time: perturb, N-1 fused swaps, restore "
-                                "and one fused N-member update pass per step") if args.swap else
-                               ("value = (2N+1) P / step time: 2N perturb/restore passes "
-                                "and one fused N-member update pass per step")},
+                   "counting": "value = (2N+1) P / step time: 2N perturb/restore passes "
+                               "and one fused N-member update pass per step"},
         "roofline": roofline,
-        "roofline_update": roofline_update,
-        "per_kernel": {
-            "es_perturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
-                           "GBps_algorithmic": round(perturb_gbs, 1),
-                           "frac_hbm_peak": round(perturb_gbs / HBM_PEAK_GBS, 4)},
-            "es_update": update,
-            **({"es_swap": {"ms": round(float(np.mean(per["es_swap"])), 3),
-                            "params_per_s": P / (float(np.mean(per["es_swap"])) / 1e3),
-                            "GBps_algorithmic": round(4 * P / (float(np.mean(per["es_swap"])) / 1e3) / 1e9, 1)}}
-               if "es_swap" in per else {}),
-        },
+        "roofline_update": valu_roofline(c_upd, t_upd, "es_update_kernel (fused N-member update)",
+                                         default_pop and not args.stochastic_round),
+        "per_kernel": per_kernel,
+        "timing": "per-kernel figures are medians of HIP event pairs on the launch stream",
         "wall_s_timed": round(wall, 3),
     }
+    if swap is not None:
+        t_sw = swap["t_swap"]
+        per_kernel["es_swap"] = {"ms": round(t_sw * 1e3, 3), "params_per_s": P / t_sw,
+                                 "GBps_algorithmic": round(4 * P / t_sw / 1e9, 1),
+                                 "normals_per_s": 2 * P / t_sw, "calls": swap["calls"]}
+        out["ms_per_step_swap"] = round(swap["ms_step"], 3)
+        out["swap_walk"] = {
+            "member_moves": "es_perturb, N-1 fused es_swap, es_restore",
+            "ms_per_step": round(swap["ms_step"], 3),
+            "speedup_vs_perturb_restore": round(ms_step / swap["ms_step"], 4),
+            "wall_s_timed": round(swap["wall"], 3),
+            "roofline": valu_roofline(c_swap, t_sw, "es_perturb_kernel<..., 2> (es_swap, two keys)",
+                                      True)}
     if cpu is not None:
         out["cpu_baseline"] = cpu
     plan.close()
@@ -628,121 +670,347 @@ def main():
 
 
 # ------------------------------------------------------------ profiling --
+#
+# A profile pass launches each of the library's kernels once per label (no
+# timing of its own) and writes the labels, in launch order, to
+# <dir>/labels.json.  rocprofv3 runs the same pass several times -- a kernel
+# trace and one run per counter set -- and --summarize matches the k-th
+# dispatch of a library kernel in each run's CSV to the k-th label.
 
-PROFILE_COMMANDS = {
-    "trace": "rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o trace -- "
-             "python3 bench.py --steps 2 --warmup 1 --no-cpu-baseline",
-    "fetch": "rocprofv3 --pmc FETCH_SIZE -f csv -d <out>/fetch -o fetch -- "
-             "python3 bench.py --profile-pass",
-    "write": "rocprofv3 --pmc WRITE_SIZE -f csv -d <out>/write -o write -- "
-             "python3 bench.py --profile-pass",
-    "valu": "rocprofv3 --pmc SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_VALU_TRANS_F32 SQ_WAVES "
-            "SQ_BUSY_CYCLES GRBM_GUI_ACTIVE -f csv -d <out>/valu -o valu -- "
-            "python3 bench.py --profile-pass",
+LIBRARY_KERNELS = ("es_perturb_kernel", "es_update_kernel", "es_stream_kernel",
+                   "es_calibrate_kernel", "es_qpass_kernel", "es_checksum_kernel",
+                   "es_qchecksum_kernel")
+COUNTER_SETS = {
+    "fetch": "FETCH_SIZE",
+    "write": "WRITE_SIZE",
+    "valu": "SQ_INSTS_VALU SQ_ACTIVE_INST_VALU SQ_INSTS_VALU_TRANS_F32 SQ_WAVES SQ_BUSY_CYCLES "
+            "GRBM_GUI_ACTIVE",
 }
+CALIBRATION_COPY_BYTES = 1 << 30
 
 
-def _kind(name):
-    if "es_qpass_kernel" in name:
-        if "true, false>" in name:
-            return "es_qupdate"
-        if "false, true>" in name:
-            return "es_qrestore"
-        return "es_qperturb"
-    if "es_perturb_kernel" in name:
-        return "es_perturb"
-    if "es_update_kernel" in name:
-        return "es_update"
-    if "copyBuffer" in name:
-        return "copy"
-    return None
+def profile_commands(pass_args):
+    """The rocprofv3 runs behind a summary (<out>: an output directory)."""
+    cmds = [f"rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o trace -- python3 bench.py "
+            f"{pass_args} --labels-dir <out>/trace"]
+    for run, counters in COUNTER_SETS.items():
+        cmds.append(f"timeout -s KILL 300 rocprofv3 --pmc {counters} -f csv -d <out>/{run} -o {run} "
+                    f"-- python3 bench.py {pass_args} --labels-dir <out>/{run}")
+    return cmds
 
 
-def _counter_rows(d):
+class ProfileLog:
+    """Labels of the library-kernel launches of a profile pass, in order."""
+
+    def __init__(self, out_dir):
+        self.out_dir, self.rows = out_dir, []
+
+    def add(self, label, group, params, bytes_, normals, fn, *a, members=None, **kw):
+        """Launch fn (exactly one library kernel) under `label`; bytes_ is the
+        algorithmic memory traffic, normals the Gaussian draws per launch."""
+        fn(*a, **kw)
+        self.rows.append({"label": label, "group": group, "params": params,
+                          "algorithmic_bytes": bytes_, "normals": normals, "members": members})
+
+    def write(self, extra):
+        if self.out_dir:
+            os.makedirs(self.out_dir, exist_ok=True)
+            with open(os.path.join(self.out_dir, "labels.json"), "w") as fh:
+                json.dump({"launches": self.rows, **extra}, fh, indent=1)
+
+
+def calibration_copy(torch):
+    """The device copy whose FETCH_SIZE / WRITE_SIZE readings scale the
+    counters to bytes (a plain copy of known size)."""
+    calib = torch.empty(CALIBRATION_COPY_BYTES, dtype=torch.uint8, device="cuda")
+    torch.empty_like(calib).copy_(calib)
+
+
+def run_profile_pass(args):
+    """Every kernel of the step once on the workload (bf16 passes, the int8
+    passes on the same shapes), the in-place stream over the plan, the six
+    flat-buffer calibration passes and the calibration copy."""
+    import torch
+    from paper_2608_17310_amd import esopt, workloads as wl
+    torch.cuda.set_device(0)
+    W = wl.WORKLOADS[args.workload]
+    log = ProfileLog(args.labels_dir)
+    seeds, signs = step_seeds(W, 0, None), list(W.signs)
+    N = len(seeds)
+    rewards = torch.from_numpy(wl.rewards(W, 0, n=N)).cuda()
+    flat, views = wl.device_params(W)
+    plan = esopt.Plan(views)
+    P = plan.numel
+    nd = len(dict.fromkeys(seeds))
+    s0 = W.sigma0
+    other = seeds[1] if N > 1 else seeds[0] + 1
+    log.add("es_perturb", "perturb", P, 4 * P, P, plan.perturb, seeds[0], signs[0], s0)
+    log.add("es_restore", "perturb", P, 4 * P, P, plan.restore, seeds[0], signs[0], s0)
+    log.add("es_swap (two keys)", "swap", P, 4 * P, 2 * P, plan.swap, seeds[0], 1, other, 1, s0)
+    log.add("es_swap (one key, antithetic)", "swap", P, 4 * P, P, plan.swap, other, 1, other, -1,
+            s0)
+    log.add(f"es_update (N={N}, nearest-even)", "update", P, 4 * P, nd * P, plan.update, seeds,
+            signs, rewards, W.alpha, sigma=s0)
+    log.add(f"es_update (N={N}, stochastic rounding)", "update", P, 4 * P, nd * P, plan.update,
+            seeds, signs, rewards, W.alpha, sigma=s0, flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+            round_seed=1)
+    log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
+            plan.stream_pass)
+    out = torch.zeros(1, dtype=torch.int64, device="cuda")
+    log.add("es_plan_checksum", "checksum", P, 2 * P, 0, plan.checksum, out)
+    torch.cuda.synchronize()
+    plan.close()
+    del flat, views
+    torch.cuda.empty_cache()
+
+    qflat, qviews, scales, rows = wl.device_qparams(W)
+    qplan = esopt.QPlan(qviews, scales, rows)
+    QP = qplan.numel
+    log.add("es_qperturb", "int8", QP, 2 * QP, QP, qplan.perturb, seeds[0], signs[0], s0)
+    log.add("es_qrestore", "int8", QP, 2 * QP, QP, qplan.restore, seeds[0], signs[0], s0)
+    log.add(f"es_qupdate (N={N})", "int8", QP, 2 * QP, nd * QP, qplan.update, seeds, signs,
+            rewards, W.alpha, sigma=s0, round_seed=1)
+    torch.cuda.synchronize()
+    qplan.close()
+    del qflat, qviews, scales
+    torch.cuda.empty_cache()
+
+    cal = torch.empty(16 << 30, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    B = cal.numel()
+    for pol, pname in ((0, "nontemporal"), (esopt.CALIBRATE_TEMPORAL, "ordinary")):
+        for mode, mname, factor in ((esopt.CALIBRATE_READ, "read", 1),
+                                    (esopt.CALIBRATE_WRITE, "write", 1),
+                                    (esopt.CALIBRATE_READ_WRITE, "in-place", 2)):
+            log.add(f"es_hbm_calibrate {mname}, {pname} accesses (16 GiB)", "ceiling", 0,
+                    factor * B, 0, esopt.hbm_calibrate, cal, mode | pol, sink)
+    torch.cuda.synchronize()
+    del cal
+    torch.cuda.empty_cache()
+    calibration_copy(torch)
+    torch.cuda.synchronize()
+    log.write({"workload": W.name, "params": P, "members": N, "distinct_seeds": nd,
+               "source_hash": _kernel_source_hash(),
+               "pass_args": "--profile-pass" + ("" if args.workload == "dense-27b"
+                                                 else f" --workload {args.workload}")})
+    print(json.dumps({"profile_pass": W.name, "launches": len(log.rows)}))
+
+
+def _library_dispatches(rows, name_key, id_key):
+    """Library-kernel dispatches of one run in dispatch order, one entry per
+    dispatch: (dispatch id, kernel name, row or rows)."""
+    by_id = {}
+    for r in rows:
+        name = r[name_key]
+        if any(k in name for k in LIBRARY_KERNELS):
+            by_id.setdefault(int(r[id_key]), (name, []))[1].append(r)
+    return [(i, by_id[i][0], by_id[i][1]) for i in sorted(by_id)]
+
+
+def _read_csv(d, suffix):
     import csv
     import glob
-    f = glob.glob(os.path.join(d, "*counter_collection.csv"))[0]
-    out = {}
-    for r in csv.DictReader(open(f)):
-        k = _kind(r["Kernel_Name"])
-        if k:
-            out.setdefault((k, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
-    return out
+    files = glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+    if not files:
+        raise FileNotFoundError(f"no *{suffix} under {d}")
+    return list(csv.DictReader(open(files[0])))
 
 
-def summarize(trace_dir, fetch_dir, write_dir, valu_dir, workload, int8=False):
-    """Write profiles/<kernel>_<workload>.md and merge the kernels' entries
-    into profiles/counters.json from the CSV output of the four rocprofv3 runs
-    in PROFILE_COMMANDS (with --int8 added for the int8 path)."""
-    import csv
-    import glob
-    stats = list(csv.DictReader(open(glob.glob(os.path.join(trace_dir, "*kernel_stats.csv"))[0])))
-    fetch, write, valu = _counter_rows(fetch_dir), _counter_rows(write_dir), _counter_rows(valu_dir)
-    # calibration: the largest copyBuffer dispatch of the profile pass is the 1 GiB device copy
-    copy_bytes = 1 << 30
-    f_copy = max(fetch[("copy", "FETCH_SIZE")]) * 1024
-    w_copy = max(write[("copy", "WRITE_SIZE")]) * 1024
-    f_scale, w_scale = copy_bytes / f_copy, copy_bytes / w_copy
-    from paper_2608_17310_amd import workloads as wl
-    P = wl.WORKLOADS[workload].n_params
-    label = workload + ("-int8" if int8 else "")
-    bytes_per_param = 2 if int8 else 4
-    dtype = "int8" if int8 else "bf16"
-    path = os.path.join(REPO, "profiles", "counters.json")
-    counters = json.load(open(path)) if os.path.exists(path) else {}
-    counters = {k: v for k, v in counters.items() if isinstance(v, dict) and "source_hash" in v}
-    suffix = " --int8" if int8 else ""
-    commands = [c.replace("bench.py --", "bench.py" + suffix + " --") for c in PROFILE_COMMANDS.values()]
-    for kind in (("es_qperturb", "es_qupdate") if int8 else ("es_perturb", "es_update")):
-        st = [r for r in stats if _kind(r["Name"]) == kind][0]
-        fb = float(np.mean(fetch[(kind, "FETCH_SIZE")])) * 1024 * f_scale
-        wb = float(np.mean(write[(kind, "WRITE_SIZE")])) * 1024 * w_scale
-        v = {c: float(np.mean(valu[(kind, c)])) for c in
-             ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_WAVES",
-              "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")}
-        counters[kind] = {"source_hash": _kernel_source_hash(), "workload": label, "params": P,
-                          "calibration": {"copy_bytes": copy_bytes, "fetch_scale": f_scale,
-                                          "write_scale": w_scale},
-                          "bytes_per_launch": fb + wb, "fetch_bytes": fb, "write_bytes": wb,
-                          "valu_insts_per_launch": v["SQ_INSTS_VALU"], "counters": v,
-                          "avg_ns": float(st["AverageNs"]), "calls": int(st["Calls"])}
-        lines = [
-            f"# {kind} on {label} ({P:,} {dtype} parameters)",
-            "",
-            "Commands (run from the repository root on an MI355X machine, `cd /tmp && export TMPDIR=/tmp` first; "
-            "`<out>` is an output directory):",
-            "",
-        ] + [f"* `{c}`" for c in commands] + [
-            "",
-            f"Kernel-sources hash: `{_kernel_source_hash()}`",
-            "",
-            "## Kernel trace (--stats)",
-            "",
-            "| kernel | calls | average ns | min ns | max ns |",
-            "|---|---|---|---|---|",
-            f"| `{st['Name'][:90]}` | {st['Calls']} | {float(st['AverageNs']):.0f} | {st['MinNs']} | {st['MaxNs']} |",
-            "",
-            "## HBM traffic per launch (FETCH_SIZE / WRITE_SIZE, KiB counters scaled by a 1 GiB copy)",
-            "",
-            f"* calibration copy of {copy_bytes} B read {f_copy:.0f} B by FETCH_SIZE and {w_copy:.0f} B by "
-            f"WRITE_SIZE: scale factors {f_scale:.3f} and {w_scale:.3f}",
-            f"* fetched {fb:.4e} B, written {wb:.4e} B, total {fb + wb:.4e} B = {(fb + wb) / P:.3f} B per "
-            f"parameter (algorithmic: {bytes_per_param})",
-            "",
-            "## VALU counters per launch",
-            "",
-        ] + [f"* {k}: {val:.4e}" for k, val in v.items()] + [
-            f"* VALU instructions per parameter: {v['SQ_INSTS_VALU'] * 64 / P:.2f} (wave instructions x 64 lanes / P)",
-            f"* of which transcendental: {v['SQ_INSTS_VALU_TRANS_F32'] * 64 / P:.2f}",
-            f"* VALU lane-instruction rate: {v['SQ_INSTS_VALU'] * 64 / (float(st['AverageNs']) * 1e-9) / 1e12:.2f} "
-            f"T/s of {VALU_PEAK_TINST:.1f} T/s peak",
-            "",
-        ]
-        with open(os.path.join(REPO, "profiles", f"{kind}_{label}.md"), "w") as fh:
-            fh.write("\n".join(lines))
-    with open(path, "w") as fh:
+def _labels(d):
+    with open(os.path.join(d, "labels.json")) as fh:
+        return json.load(fh)
+
+
+def _match(labels, dispatches, what):
+    if len(labels["launches"]) != len(dispatches):
+        raise RuntimeError(f"{what}: {len(labels['launches'])} labelled launches but "
+                           f"{len(dispatches)} library-kernel dispatches")
+    return list(zip(labels["launches"], dispatches))
+
+
+def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
+    """Turn the trace and counter runs of one profile pass (out_dir/trace,
+    out_dir/fetch, out_dir/write, out_dir/valu) into summaries and
+    counters.json entries under profiles_dir."""
+    lab = _labels(os.path.join(out_dir, "trace"))
+    if "sweep" in lab:
+        return summarize_sweep(out_dir, lab, profiles_dir)
+    per = _per_label(out_dir)
+    src = lab["source_hash"]
+    if src != _kernel_source_hash():
+        raise RuntimeError("profile taken on other kernel sources than the working tree's")
+    wname, P = lab["workload"], lab["params"]
+    cmds = profile_commands(lab["pass_args"])
+    header = ["Commands (from the repository root on an MI355X machine, after "
+              "`cd /tmp && export TMPDIR=/tmp`; `<out>` is an output directory; then "
+              f"`python3 bench.py --summarize <out>`):", ""] + [f"* `{c}`" for c in cmds] + [
+        "", f"Kernel-sources hash: `{src}`", "", CALIBRATION_NOTE.format(**per["_calibration"]), ""]
+    groups = {
+        "perturb": ("es_perturb", f"es_perturb / es_restore on {wname} ({P:,} bf16 parameters)"),
+        "swap": ("es_swap", f"es_swap on {wname} ({P:,} bf16 parameters)"),
+        "update": ("es_update", f"es_update on {wname} ({P:,} bf16 parameters, "
+                                f"N = {lab['members']}, {lab['distinct_seeds']} distinct seeds)"),
+        "int8": ("es_qpass", f"int8 passes on {wname}-int8 (the same shapes as int8 codes with "
+                             f"per-row scales)"),
+        "ceiling": ("hbm_ceilings", f"HBM ceilings: the in-place stream over the {wname} plan and "
+                                    f"the flat-buffer calibration passes"),
+        "checksum": ("es_plan_checksum", f"es_plan_checksum on {wname}"),
+    }
+    counters_path = os.path.join(profiles_dir, "counters.json")
+    counters = json.load(open(counters_path)) if os.path.exists(counters_path) else {}
+    keys = {"es_perturb": "es_perturb", f"es_update (N={lab['members']}, nearest-even)": "es_update",
+            "es_swap (two keys)": "es_swap", "es_qperturb": "es_qperturb",
+            f"es_qupdate (N={lab['members']})": "es_qupdate"}
+    for group, (stem, title) in groups.items():
+        rows = [r for r in per["_rows"] if r["group"] == group]
+        if not rows:
+            continue
+        lines = [f"# {title}", ""] + header + _table(rows)
+        fname = f"{stem}_{wname}{'-int8' if group == 'int8' else ''}.md"
+        with open(os.path.join(profiles_dir, fname), "w") as fh:
+            fh.write("\n".join(lines) + "\n")
+        for r in rows:
+            k = keys.get(r["label"])
+            if k:
+                counters[k] = {"source_hash": src,
+                               "workload": wname + ("-int8" if group == "int8" else ""),
+                               "params": r["params"], "bytes_per_launch": r["fetch"] + r["write"],
+                               "fetch_bytes": r["fetch"], "write_bytes": r["write"],
+                               "valu_insts_per_launch": r["SQ_INSTS_VALU"], "avg_ns": r["ns"],
+                               "counters": {c: r[c] for c in VALU_COUNTERS}}
+    with open(counters_path, "w") as fh:
         json.dump(counters, fh, indent=1)
     print(json.dumps({k: v["bytes_per_launch"] for k, v in counters.items()}))
+
+
+VALU_COUNTERS = ("SQ_INSTS_VALU", "SQ_ACTIVE_INST_VALU", "SQ_INSTS_VALU_TRANS_F32", "SQ_WAVES",
+                 "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE")
+CALIBRATION_NOTE = ("Counter calibration: a plain {copy_bytes} B device copy read {f_copy:.0f} B by "
+                    "FETCH_SIZE and {w_copy:.0f} B by WRITE_SIZE (KiB counters x 1024), so fetched "
+                    "bytes are FETCH_SIZE x 1024 x {f_scale:.3f} and written bytes WRITE_SIZE x "
+                    "1024 x {w_scale:.3f}.  Durations are the kernel trace's; the shader clock is "
+                    "GRBM_GUI_ACTIVE / 8 XCDs over the duration of the same dispatch in the counter "
+                    "run; VALU issue is SQ_INSTS_VALU x 64 lanes over the trace duration against "
+                    "39.32 T lane-instructions/s (256 CUs x 64 lanes x 2.4 GHz), and per cycle "
+                    "against one wave instruction per CU per cycle at the measured clock.")
+
+
+def _per_label(out_dir):
+    """Join the four runs on the labels: per labelled launch the trace
+    duration, scaled fetch / write bytes and the VALU counters."""
+    res = {}
+    trace_lab = _labels(os.path.join(out_dir, "trace"))
+    tr = _library_dispatches(_read_csv(os.path.join(out_dir, "trace"), "kernel_trace.csv"),
+                             "Kernel_Name", "Dispatch_Id")
+    runs = {}
+    for run in COUNTER_SETS:
+        d = os.path.join(out_dir, run)
+        rows = _read_csv(d, "counter_collection.csv")
+        runs[run] = (_labels(d), _library_dispatches(rows, "Kernel_Name", "Dispatch_Id"), rows)
+    # calibration from the largest device copy of the fetch / write runs
+    def copy_max(rows, counter):
+        return max(float(r["Counter_Value"]) for r in rows
+                   if "copyBuffer" in r["Kernel_Name"] and r["Counter_Name"] == counter) * 1024
+    f_copy = copy_max(runs["fetch"][2], "FETCH_SIZE")
+    w_copy = copy_max(runs["write"][2], "WRITE_SIZE")
+    cal = {"copy_bytes": CALIBRATION_COPY_BYTES, "f_copy": f_copy, "w_copy": w_copy,
+           "f_scale": CALIBRATION_COPY_BYTES / f_copy, "w_scale": CALIBRATION_COPY_BYTES / w_copy}
+    out = []
+    agg = {}
+    for l, (i, name, r) in _match(trace_lab, tr, "trace"):
+        ns = int(r[0]["End_Timestamp"]) - int(r[0]["Start_Timestamp"])
+        agg.setdefault(l["label"], {**l, "kernel": name, "ns_list": []})["ns_list"].append(ns)
+    for run, (labs, disp, _) in runs.items():
+        for l, (i, name, rs) in _match(labs, disp, run):
+            e = agg[l["label"]]
+            for r in rs:
+                e.setdefault(r["Counter_Name"] + "_list", []).append(float(r["Counter_Value"]))
+            if run == "valu":
+                e.setdefault("valu_ns_list", []).append(
+                    int(rs[0]["End_Timestamp"]) - int(rs[0]["Start_Timestamp"]))
+    for label, e in agg.items():
+        e["ns"] = float(np.mean(e["ns_list"]))
+        e["fetch"] = float(np.mean(e["FETCH_SIZE_list"])) * 1024 * cal["f_scale"]
+        e["write"] = float(np.mean(e["WRITE_SIZE_list"])) * 1024 * cal["w_scale"]
+        for c in VALU_COUNTERS:
+            e[c] = float(np.mean(e[c + "_list"]))
+        e["valu_ns"] = float(np.mean(e["valu_ns_list"]))
+        out.append(e)
+    res["_rows"] = out
+    res["_calibration"] = cal
+    return res
+
+
+def _table(rows):
+    lines = ["| launch | kernel | calls | trace ns | algorithmic GB/s | fetched B | written B | "
+             "counted / algorithmic bytes | B per param | VALU instr per param | per normal | "
+             "of which transcendental (per param) | VALU issue (of 39.32 T/s) | shader clock GHz | "
+             "VALU issue per CU-cycle at that clock |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for e in rows:
+        P, ns = e["params"], e["ns"]
+        vi = e["SQ_INSTS_VALU"]
+        clock = e["GRBM_GUI_ACTIVE"] / 8 / e["valu_ns"]
+        kname = e["kernel"].replace("void (anonymous namespace)::", "", 1).split("(")[0]
+        tot = e["fetch"] + e["write"]
+        lines.append(
+            f"| {e['label']} | `{kname}` | {len(e['ns_list'])} | {ns:.0f} | "
+            f"{e['algorithmic_bytes'] / ns:.1f} | {e['fetch']:.4e} | {e['write']:.4e} | "
+            f"{tot / e['algorithmic_bytes']:.4f} | "
+            + (f"{tot / P:.3f} | {vi * 64 / P:.2f} | " if P else "— | — | ")
+            + (f"{vi * 64 / e['normals']:.2f} | " if e["normals"] else "— | ")
+            + (f"{e['SQ_INSTS_VALU_TRANS_F32'] * 64 / P:.2f} | " if P else "— | ")
+            + f"{vi * 64 / (ns * 1e-9) / 1e12 / VALU_PEAK_TINST:.3f} | {clock:.3f} | "
+            f"{vi / (256 * e['GRBM_GUI_ACTIVE'] / 8):.3f} |")
+    lines += ["", "Raw counters per launch (means over the launches of each label):", ""]
+    for e in rows:
+        lines.append(f"* {e['label']}: " + ", ".join(f"{c} {e[c]:.4e}" for c in VALU_COUNTERS)
+                     + f"; counter-run duration {e['valu_ns']:.0f} ns")
+    return lines
+
+
+def summarize_sweep(out_dir, lab, profiles_dir):
+    """profiles/es_update_<workload>-sweep.md from a sweep profile pass."""
+    per = _per_label(out_dir)
+    src = lab["source_hash"]
+    if src != _kernel_source_hash():
+        raise RuntimeError("profile taken on other kernel sources than the working tree's")
+    cmds = profile_commands(lab["pass_args"])
+    rows = sorted(per["_rows"], key=lambda e: e["members"])
+    lines = [f"# Fused es_update population sweep on {lab['workload']} ({lab['params']:,} bf16 "
+             f"parameters, rewards N(0,1), distinct seeds)", "",
+             "Commands (from the repository root on an MI355X machine, after "
+             "`cd /tmp && export TMPDIR=/tmp`; `<out>` is an output directory; then "
+             "`python3 bench.py --summarize <out>`):", ""] + [f"* `{c}`" for c in cmds] + [
+        "", f"Kernel-sources hash: `{src}`", "", CALIBRATION_NOTE.format(**per["_calibration"]), "",
+        "| N | trace ms | algorithmic TB/s | B per param (counted) | VALU instr per param | "
+        "VALU instr per normal | VALU issue (of 39.32 T/s) | shader clock GHz | VALU issue per "
+        "CU-cycle | bound |",
+        "|---|---|---|---|---|---|---|---|---|---|"]
+    stream = [e for e in rows if e["group"] == "ceiling"]
+    t_stream = stream[0]["ns"] if stream else None
+    for e in rows:
+        if e["group"] != "update":
+            continue
+        P, ns, vi = e["params"], e["ns"], e["SQ_INSTS_VALU"]
+        clock = e["GRBM_GUI_ACTIVE"] / 8 / e["valu_ns"]
+        issue = vi * 64 / (ns * 1e-9) / 1e12 / VALU_PEAK_TINST
+        bound = "hbm" if t_stream and ns < 1.5 * t_stream else "valu"
+        lines.append(f"| {e['members']} | {ns / 1e6:.3f} | {4 * P / ns / 1e3:.3f} | "
+                     f"{(e['fetch'] + e['write']) / P:.3f} | {vi * 64 / P:.1f} | "
+                     f"{vi * 64 / e['normals']:.2f} | {issue:.3f} | {clock:.3f} | "
+                     f"{vi / (256 * e['GRBM_GUI_ACTIVE'] / 8):.3f} | {bound} |")
+    if stream:
+        s = stream[0]
+        lines += ["", f"In-place copy of the same memory (es_stream_pass): {s['ns'] / 1e6:.3f} ms, "
+                      f"{4 * s['params'] / s['ns'] / 1e3:.3f} TB/s, "
+                      f"{(s['fetch'] + s['write']) / s['params']:.3f} B per param counted; "
+                      "'bound' is hbm where the update takes under 1.5x this time."]
+    lines += [""] + _table(rows)[-len(rows) - 3:]
+    path = os.path.join(profiles_dir, f"es_update_{lab['workload']}-sweep.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(path)
 
 
 def _counters_for(path, kind, label):
@@ -757,13 +1025,13 @@ def _counters_for(path, kind, label):
 
 
 def _kernel_source_hash():
-    """Hash of the device code the counters describe: the noise, int8 and
-    table-search headers and the device section of esopt.hip (host-side edits
-    leave the kernels, and so the counters, unchanged)."""
+    """Hash of the device code the counters describe: the device headers and
+    the device section of esopt.hip (host-side edits leave the kernels, and so
+    the counters, unchanged)."""
     import hashlib
     csrc = os.path.join(REPO, "paper_2608_17310_amd", "csrc")
     h = hashlib.sha256()
-    for f in ("es_noise.hpp", "es_quant.hpp", "es_table.hpp"):
+    for f in sorted(x for x in os.listdir(csrc) if x.endswith(".hpp")):
         h.update(open(os.path.join(csrc, f), "rb").read())
     src = open(os.path.join(csrc, "esopt.hip"), "rb").read()
     start, end = src.index(b"// Device code"), src.index(b"// Host side")

@@ -301,8 +301,9 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream);
 /* HBM calibration over a caller's flat device buffer of `bytes` bytes (a
  * positive multiple of 131072, 16-byte aligned), with the tile shape and
  * launch of es_perturb: 1024 lanes x 8 16-byte words per tile, one workgroup
- * per compute unit, nontemporal accesses, each tile loaded whole, then
- * stored.  mode 0 reads every word (their XOR is folded into *sink_dev, a
+ * per compute unit, nontemporal accesses (the passes' policy; with
+ * ES_CALIBRATE_TEMPORAL or-ed into `mode`, ordinary loads and stores), each
+ * tile loaded whole, then stored.  mode 0 reads every word (their XOR is folded into *sink_dev, a
  * device uint32, with one atomic per wave, so the reads are not dead code);
  * mode 1 writes every word (the buffer's contents become a pattern: the
  * 16-byte word of lane l in group u of tile t holds (t, u, l, 0)); mode 2
@@ -310,6 +311,7 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream);
  * give the practical read, write and in-place ceilings of the device's
  * memory against which the passes' bandwidth is read.  sink_dev is ignored
  * unless mode is 0. */
+#define ES_CALIBRATE_TEMPORAL 4   /* es_hbm_calibrate: ordinary, not nontemporal, accesses */
 int es_hbm_calibrate(void* buf_dev, uint64_t bytes, int32_t mode, uint32_t* sink_dev,
                      es_stream_t stream);
 

@@ -561,12 +561,23 @@ __global__ __launch_bounds__(64) void es_zero_u64_kernel(unsigned long long* __r
 
 // HBM calibration over a caller's flat buffer (es_hbm_calibrate), with the
 // perturb's workgroup and tile shape: kThreads lanes x kU 16-byte words per
-// tile, nontemporal accesses, each tile loaded whole and then stored.  kMode
-// 0 reads every word (their XOR leaves in one atomic per wave, so the loads
-// are live), 1 writes every word (the pattern tile, u, lane, 0), 2 reads
-// every word and writes it back (XOR with `flip`, which the host passes as
-// 0, so the stores are kept).
-template <int kThreads, int kU, int kMode>
+// tile, each tile loaded whole and then stored, with nontemporal accesses
+// (kNT, the passes' policy) or ordinary ones.  kMode 0 reads every word
+// (their XOR leaves in one atomic per wave, so the loads are live), 1 writes
+// every word (the pattern tile, u, lane, 0), 2 reads every word and writes it
+// back (XOR with `flip`, which the host passes as 0, so the stores are kept).
+template <bool kNT>
+__device__ __forceinline__ u32x4_t cal_load(const ES_GLOBAL u32x4_t* a) {
+    if constexpr (kNT) return __builtin_nontemporal_load(a);
+    else return *a;
+}
+template <bool kNT>
+__device__ __forceinline__ void cal_store(u32x4_t v, ES_GLOBAL u32x4_t* a) {
+    if constexpr (kNT) __builtin_nontemporal_store(v, a);
+    else *a = v;
+}
+
+template <int kThreads, int kU, int kMode, bool kNT>
 __global__ __launch_bounds__(kThreads) void es_calibrate_kernel(u32x4_t* __restrict__ buf,
                                                                 uint64_t n_tiles,
                                                                 uint32_t* __restrict__ sink,
@@ -578,7 +589,7 @@ __global__ __launch_bounds__(kThreads) void es_calibrate_kernel(u32x4_t* __restr
         u32x4_t v[kU];
         if constexpr (kMode != 1) {
 #pragma unroll
-            for (int u = 0; u < kU; ++u) v[u] = __builtin_nontemporal_load(base + u * kThreads);
+            for (int u = 0; u < kU; ++u) v[u] = cal_load<kNT>(base + u * kThreads);
         }
         __builtin_amdgcn_sched_barrier(0);
         if constexpr (kMode == 0) {
@@ -592,7 +603,7 @@ __global__ __launch_bounds__(kThreads) void es_calibrate_kernel(u32x4_t* __restr
                 } else {
                     v[u].x ^= flip; v[u].y ^= flip; v[u].z ^= flip; v[u].w ^= flip;
                 }
-                __builtin_nontemporal_store(v[u], base + u * kThreads);
+                cal_store<kNT>(v[u], base + u * kThreads);
             }
         }
     }
@@ -1792,18 +1803,22 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
 int es_hbm_calibrate(void* buf_dev, uint64_t bytes, int32_t mode, uint32_t* sink_dev,
                      es_stream_t stream) {
     constexpr uint64_t kTileBytes = uint64_t(kDefaultThreads) * kDefaultGroups * 16;
-    if (buf_dev == nullptr || (mode == 0 && sink_dev == nullptr))
+    const int32_t kind = mode & ~ES_CALIBRATE_TEMPORAL;
+    const bool nt = (mode & ES_CALIBRATE_TEMPORAL) == 0;
+    if (mode < 0 || kind > 2)
+        return fail(ES_ERR_INVALID_ARG,
+                    "es_hbm_calibrate: mode not 0, 1 or 2 (optionally | ES_CALIBRATE_TEMPORAL)");
+    if (buf_dev == nullptr || (kind == 0 && sink_dev == nullptr))
         return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: null pointer");
-    if (mode < 0 || mode > 2) return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: mode not 0, 1 or 2");
     if (bytes == 0 || bytes % kTileBytes != 0)
         return fail(ES_ERR_INVALID_ARG, "es_hbm_calibrate: bytes not a positive multiple of 131072");
     if (reinterpret_cast<uintptr_t>(buf_dev) % 16 != 0 ||
-        (mode == 0 && reinterpret_cast<uintptr_t>(sink_dev) % 4 != 0))
+        (kind == 0 && reinterpret_cast<uintptr_t>(sink_dev) % 4 != 0))
         return fail(ES_ERR_ALIGN, "es_hbm_calibrate: buffer not 16-byte aligned");
     int device = -1;
     int rc = current_device(&device);
     if (rc == ES_OK) rc = check_access(buf_dev, bytes, device, "es_hbm_calibrate: buffer");
-    if (rc == ES_OK && mode == 0)
+    if (rc == ES_OK && kind == 0)
         rc = check_access(sink_dev, 4, device, "es_hbm_calibrate: sink");
     if (rc != ES_OK) return rc;
     int cus = 0;
@@ -1813,15 +1828,15 @@ int es_hbm_calibrate(void* buf_dev, uint64_t bytes, int32_t mode, uint32_t* sink
     const dim3 grid(static_cast<uint32_t>(std::min<uint64_t>(n_tiles, uint64_t(cus))));
     const hipStream_t s = static_cast<hipStream_t>(stream);
     u32x4_t* buf = static_cast<u32x4_t*>(buf_dev);
-    if (mode == 0)
-        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 0>), grid,
-                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
-    else if (mode == 1)
-        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 1>), grid,
-                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
-    else
-        hipLaunchKernelGGL((es_calibrate_kernel<kDefaultThreads, kDefaultGroups, 2>), grid,
-                           dim3(kDefaultThreads), 0, s, buf, n_tiles, sink_dev, 0u);
+    using CalKernel = void (*)(u32x4_t*, uint64_t, uint32_t*, uint32_t);
+    constexpr int kT = kDefaultThreads, kG = kDefaultGroups;
+    const CalKernel kernels[2][3] = {
+        {es_calibrate_kernel<kT, kG, 0, false>, es_calibrate_kernel<kT, kG, 1, false>,
+         es_calibrate_kernel<kT, kG, 2, false>},
+        {es_calibrate_kernel<kT, kG, 0, true>, es_calibrate_kernel<kT, kG, 1, true>,
+         es_calibrate_kernel<kT, kG, 2, true>}};
+    hipLaunchKernelGGL(kernels[nt ? 1 : 0][kind], grid, dim3(kDefaultThreads), 0, s, buf, n_tiles,
+                       sink_dev, 0u);
     e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_calibrate_kernel launch");
     return ES_OK;

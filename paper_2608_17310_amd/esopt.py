@@ -398,13 +398,15 @@ def zscore(rewards, eps=1e-8, out=None, status=None, stream=None):
 
 
 CALIBRATE_READ, CALIBRATE_WRITE, CALIBRATE_READ_WRITE = 0, 1, 2
+CALIBRATE_TEMPORAL = 4      # or-ed into a mode: ordinary instead of nontemporal accesses
 
 
 def hbm_calibrate(buf, mode, sink=None, stream=None):
     """One es_hbm_calibrate pass over the contiguous CUDA tensor `buf` (its
     byte size a multiple of 131072): mode CALIBRATE_READ (the words' XOR is
     folded into `sink`, a one-element int32 CUDA tensor), CALIBRATE_WRITE (buf
-    is overwritten) or CALIBRATE_READ_WRITE (buf unchanged)."""
+    is overwritten) or CALIBRATE_READ_WRITE (buf unchanged), each optionally
+    | CALIBRATE_TEMPORAL (ordinary loads and stores instead of nontemporal)."""
     if not buf.is_cuda or not buf.is_contiguous():
         raise ValueError("buf must be a contiguous CUDA tensor")
     sp = None if sink is None else _dev_ptr(sink, torch.int32, "sink")

@@ -1,6 +1,7 @@
 """es_hbm_calibrate: the read pass folds every word into the sink (their
 XOR), the write pass leaves the documented pattern, the in-place pass leaves
-the buffer bit for bit unchanged, and invalid buffers are refused."""
+the buffer bit for bit unchanged -- with nontemporal and with ordinary
+accesses -- and invalid buffers and modes are refused."""
 import numpy as np
 import pytest
 import torch
@@ -25,24 +26,29 @@ def _buf(n_tiles, seed):
     return host, torch.from_numpy(host).cuda()
 
 
+POLICIES = [0, esopt.CALIBRATE_TEMPORAL]
+
+
+@pytest.mark.parametrize("policy", POLICIES)
 @pytest.mark.parametrize("n_tiles", [1, 300, 1000])      # fewer and more tiles than CUs
-def test_read_folds_every_word_into_the_sink(n_tiles):
+def test_read_folds_every_word_into_the_sink(n_tiles, policy):
     host, buf = _buf(n_tiles, n_tiles)
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
-    esopt.hbm_calibrate(buf, esopt.CALIBRATE_READ, sink)
+    esopt.hbm_calibrate(buf, esopt.CALIBRATE_READ | policy, sink)
     torch.cuda.synchronize()
     exp = np.bitwise_xor.reduce(host.view(np.uint32))
     assert np.uint32(sink.cpu().numpy().view(np.uint32)[0]) == exp
     assert torch.equal(buf.cpu(), torch.from_numpy(host))
 
 
+@pytest.mark.parametrize("policy", POLICIES)
 @pytest.mark.parametrize("n_tiles", [1, 300])
-def test_write_leaves_the_pattern_and_in_place_changes_nothing(n_tiles):
+def test_write_leaves_the_pattern_and_in_place_changes_nothing(n_tiles, policy):
     host, buf = _buf(n_tiles, 7 + n_tiles)
-    esopt.hbm_calibrate(buf, esopt.CALIBRATE_READ_WRITE)
+    esopt.hbm_calibrate(buf, esopt.CALIBRATE_READ_WRITE | policy)
     torch.cuda.synchronize()
     assert torch.equal(buf.cpu(), torch.from_numpy(host))
-    esopt.hbm_calibrate(buf, esopt.CALIBRATE_WRITE)
+    esopt.hbm_calibrate(buf, esopt.CALIBRATE_WRITE | policy)
     torch.cuda.synchronize()
     got = buf.cpu().numpy().view(np.uint32).reshape(n_tiles, 8, 1024, 4)
     t, u, l = np.meshgrid(np.arange(n_tiles), np.arange(8), np.arange(1024), indexing="ij")
@@ -56,3 +62,6 @@ def test_invalid_buffers_are_refused():
         esopt.hbm_calibrate(buf, esopt.CALIBRATE_WRITE)          # not whole tiles
     with pytest.raises(esopt.EsError):
         esopt.hbm_calibrate(buf[4:4 + TILE // 4], esopt.CALIBRATE_WRITE - 1)   # read: no sink
+    for bad in (-1, 3, 7, 8):
+        with pytest.raises(esopt.EsError):
+            esopt.hbm_calibrate(buf[4:4 + TILE // 4], bad)
