@@ -587,6 +587,7 @@ def main():
     log.ev = []
     for _ in range(5):
         log.call("es_stream_pass", True, plan.stream_pass)
+    torch.cuda.synchronize()
     t_stream = median_s(log.ms()["es_stream_pass"])
     ceiling_gbs = 4 * P / t_stream / 1e9
     flat_rates = flat_ceilings(esopt, stream)
