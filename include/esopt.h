@@ -211,6 +211,28 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const es_update_opts_t* opts, float* z_out_dev,
               int32_t* status_out_dev, es_stream_t stream);
 
+/* es_update for callers that cannot allocate (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * arguments, checks, results and errors as es_update, bit for bit, but the
+ * member tables, merged weights and header of the update live in a static
+ * device array of 41 216 bytes (room for ES_MAX_MEMBERS members) instead of
+ * the plan's scratch, and a successful call allocates no device or host
+ * memory (the member tables are built in fixed arrays on the calling
+ * thread's stack, about 52 KB).  n_members above ES_MAX_MEMBERS is refused
+ * with ES_ERR_INVALID_ARG.  Each device holds its own copy of the array until
+ * the process ends; the first call on a device looks up its address there
+ * (with that device current) and keeps it.  Every call on one device shares
+ * that array: calls that overlap on one GPU (on different streams, or from
+ * different threads without ordering) race and give undefined results, so
+ * order them like calls on one plan.  The array keeps the last call's
+ * contents; nothing in it needs clearing, since each call writes every
+ * entry it reads.  A failed call records its message with es_last_error
+ * (formatting it may allocate host memory). */
+int es_update_noalloc(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
+                      const float* rewards_dev, uint32_t n_members,
+                      const es_update_opts_t* opts, float* z_out_dev,
+                      int32_t* status_out_dev, es_stream_t stream);
+
 /* 64-bit checksum of a plan's parameters, written to *out_dev (device
  * memory, 8-byte aligned):
  *   H = sum over elements of mix64(j K_J + tensor_id K_T + b K_B)  mod 2^64

@@ -51,6 +51,8 @@
 #include <cstdlib>
 #include <cstddef>
 #include <cstring>
+#include <atomic>
+#include <mutex>
 #include <new>
 #include <string>
 #include <unordered_map>
@@ -138,6 +140,12 @@ int fail(int code, const std::string& msg) {
 
 int hip_fail(hipError_t e, const std::string& what) {
     return fail(ES_ERR_HIP, what + ": " + hipGetErrorString(e));
+}
+
+// A failure of call `name`: the message is formatted only here, so a call
+// that succeeds builds no strings (no host allocation on its way).
+int fail_in(int code, const char* name, const char* msg) {
+    return fail(code, std::string(name) + ": " + msg);
 }
 
 // ------------------------------------------------------------------------
@@ -699,6 +707,13 @@ __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __re
                                                    n_distinct, rk);
 }
 
+// The scratch of es_update_noalloc: one update's staged member tables, merged
+// weights and header (the layout of a plan's scratch), in a fixed device
+// array instead of memory allocated with a plan.  Each device holds its own
+// copy until the process ends; host code reaches it only through the address
+// hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
 // Copy up to 1 KB of host-packed words (passed as kernel arguments) into
 // device scratch: how es_update hands its member tables to the device
 // without a host-side staging buffer or synchronisation.
@@ -1213,24 +1228,27 @@ int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_st
 // mapped pinned host memory.  Catches host pointers, other devices' memory
 // and overstated sizes before a kernel would fault on them.  A failed query
 // leaves no error behind for later launch checks.
-int check_access(const void* p, uint64_t bytes, int device, const std::string& what) {
+// (The name of the checked array is `name` followed by `part`; it is
+// formatted only on failure.)
+int check_access(const void* p, uint64_t bytes, int device, const char* name, const char* part) {
     if (bytes == 0) return ES_OK;
+    auto what = [&]() { return std::string(name) + part; };
     hipPointerAttribute_t a{};
     hipError_t e = hipPointerGetAttributes(&a, p);
     if (e != hipSuccess) {
         (void)hipGetLastError();
-        return fail(ES_ERR_INVALID_ARG, what + ": not memory the device can access");
+        return fail(ES_ERR_INVALID_ARG, what() + ": not memory the device can access");
     }
     if (a.type == hipMemoryTypeHost) {
         if (a.devicePointer == nullptr)
-            return fail(ES_ERR_INVALID_ARG, what + ": host memory not mapped for the device");
+            return fail(ES_ERR_INVALID_ARG, what() + ": host memory not mapped for the device");
         return ES_OK;
     }
     if (a.type != hipMemoryTypeDevice && a.type != hipMemoryTypeManaged &&
         a.type != hipMemoryTypeUnified)
-        return fail(ES_ERR_INVALID_ARG, what + ": not device memory");
+        return fail(ES_ERR_INVALID_ARG, what() + ": not device memory");
     if (a.type == hipMemoryTypeDevice && a.device != device)
-        return fail(ES_ERR_INVALID_ARG, what + ": memory of device " + std::to_string(a.device) +
+        return fail(ES_ERR_INVALID_ARG, what() + ": memory of device " + std::to_string(a.device) +
                                             ", not of device " + std::to_string(device));
     hipDeviceptr_t base = nullptr;
     size_t size = 0;
@@ -1241,9 +1259,12 @@ int check_access(const void* p, uint64_t bytes, int device, const std::string& w
     }
     const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
     if (q < b || q - b > size || bytes > size - (q - b))
-        return fail(ES_ERR_INVALID_ARG, what + ": " + std::to_string(bytes) +
+        return fail(ES_ERR_INVALID_ARG, what() + ": " + std::to_string(bytes) +
                                             " bytes extend past the end of its allocation");
     return ES_OK;
+}
+int check_access(const void* p, uint64_t bytes, int device, const std::string& what) {
+    return check_access(p, bytes, device, what.c_str(), "");
 }
 
 // Free a plan's tile table and scratch on the plan's device: that device is made
@@ -1343,64 +1364,93 @@ int current_device(int* dev) {
 // The device arrays of an update call: rewards and z (n floats), status.
 int check_update_arrays(const char* name, int device, const float* rewards_dev, uint32_t n,
                         const float* z_out_dev, const int32_t* status_out_dev) {
-    const std::string nm(name);
-    int rc = check_access(rewards_dev, uint64_t(4) * n, device, nm + ": rewards");
+    int rc = check_access(rewards_dev, uint64_t(4) * n, device, name, ": rewards");
     if (rc == ES_OK && z_out_dev != nullptr)
-        rc = check_access(z_out_dev, uint64_t(4) * n, device, nm + ": z output");
+        rc = check_access(z_out_dev, uint64_t(4) * n, device, name, ": z output");
     if (rc == ES_OK && status_out_dev != nullptr)
-        rc = check_access(status_out_dev, 4, device, nm + ": status output");
+        rc = check_access(status_out_dev, 4, device, name, ": status output");
     return rc;
 }
 
-// Argument checks shared by es_update and es_qupdate.
+// Argument checks shared by the update entry points.
 int validate_update(const char* name, const uint64_t* seeds, const int32_t* signs,
                     const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts) {
-    const std::string nm(name);
     if (seeds == nullptr || signs == nullptr || rewards_dev == nullptr || opts == nullptr)
-        return fail(ES_ERR_INVALID_ARG, nm + ": null pointer");
+        return fail_in(ES_ERR_INVALID_ARG, name, "null pointer");
     if (n_members == 0 || n_members > ES_MAX_MEMBERS)
-        return fail(ES_ERR_INVALID_ARG, nm + ": n_members out of range");
+        return fail_in(ES_ERR_INVALID_ARG, name, "n_members out of range (1 .. 1024)");
     if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
                          ES_UPDATE_STOCHASTIC_ROUND)) != 0)
-        return fail(ES_ERR_INVALID_ARG, nm + ": unknown flags");
-    if (!std::isfinite(opts->alpha)) return fail(ES_ERR_INVALID_ARG, nm + ": alpha not finite");
+        return fail_in(ES_ERR_INVALID_ARG, name, "unknown flags");
+    if (!std::isfinite(opts->alpha)) return fail_in(ES_ERR_INVALID_ARG, name, "alpha not finite");
     if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
-        return fail(ES_ERR_INVALID_ARG, nm + ": sigma must be finite and > 0 with ES_UPDATE_DIV_SIGMA");
+        return fail_in(ES_ERR_INVALID_ARG, name,
+                       "sigma must be finite and > 0 with ES_UPDATE_DIV_SIGMA");
     if (!std::isfinite(opts->zscore_eps) || opts->zscore_eps < 0.0f)
-        return fail(ES_ERR_INVALID_ARG, nm + ": zscore_eps must be finite and >= 0");
+        return fail_in(ES_ERR_INVALID_ARG, name, "zscore_eps must be finite and >= 0");
     for (uint32_t i = 0; i < n_members; ++i)
         if (signs[i] != 1 && signs[i] != -1)
-            return fail(ES_ERR_INVALID_ARG, nm + ": signs must be +1 or -1");
+            return fail_in(ES_ERR_INVALID_ARG, name, "signs must be +1 or -1");
     return ES_OK;
 }
 
-// Hand the population to the device: distinct seeds in order of first
-// appearance with their members grouped by seed (CSR, member order within a
-// seed) are staged into the scratch through kernel arguments, then one wave
-// z-scores the rewards and merges the weights per distinct seed, leaving the
-// weighted member table and its header in the scratch.
+// The population as tables (host side, fixed arrays, no allocation):
+// distinct seeds in order of first appearance, each with its members grouped
+// in member order (CSR).  Members are sorted by (seed, index) in place, each
+// run of one seed is a distinct seed whose first appearance is its smallest
+// index, and the runs are ordered by that index.
+struct MemberTables {
+    MemberIn min[ES_MAX_MEMBERS];
+    DistinctIn din[ES_MAX_MEMBERS];
+    uint32_t n_distinct;
+};
+
+void build_member_tables(const uint64_t* seeds, const int32_t* signs, uint32_t n,
+                         MemberTables& t) {
+    struct SeedIndex {
+        uint64_t seed;
+        uint32_t index;
+    };
+    struct Run {
+        uint32_t first, start, count;       // smallest member index, position in `order`, size
+    };
+    SeedIndex order[ES_MAX_MEMBERS];
+    Run runs[ES_MAX_MEMBERS];
+    for (uint32_t i = 0; i < n; ++i) order[i] = SeedIndex{seeds[i], i};
+    std::sort(order, order + n, [](const SeedIndex& a, const SeedIndex& b) {
+        return a.seed != b.seed ? a.seed < b.seed : a.index < b.index;
+    });
+    uint32_t nd = 0;
+    for (uint32_t i = 0; i < n;) {
+        uint32_t j = i + 1;
+        while (j < n && order[j].seed == order[i].seed) ++j;
+        runs[nd++] = Run{order[i].index, i, j - i};
+        i = j;
+    }
+    std::sort(runs, runs + nd, [](const Run& a, const Run& b) { return a.first < b.first; });
+    uint32_t pos = 0;
+    for (uint32_t d = 0; d < nd; ++d) {
+        const uint64_t sd = order[runs[d].start].seed;
+        t.din[d] = DistinctIn{static_cast<uint32_t>(sd), static_cast<uint32_t>(sd >> 32), pos,
+                              runs[d].count};
+        for (uint32_t k = 0; k < runs[d].count; ++k) {
+            const uint32_t m = order[runs[d].start + k].index;
+            t.min[pos++] = MemberIn{m, signs[m]};
+        }
+    }
+    t.n_distinct = nd;
+}
+
+// Hand the population to the device: the member tables are staged into the
+// scratch through kernel arguments, then one wave z-scores the rewards and
+// merges the weights per distinct seed, leaving the weighted member table
+// and its header in the scratch.  Allocates nothing.
 int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* signs,
                    const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
                    float* z_out_dev, int32_t* status_out_dev, hipStream_t s) {
-    std::unordered_map<uint64_t, uint32_t> index;
-    std::vector<uint64_t> distinct;
-    std::vector<uint32_t> of(n_members);
-    for (uint32_t i = 0; i < n_members; ++i) {
-        auto it = index.emplace(seeds[i], static_cast<uint32_t>(distinct.size()));
-        if (it.second) distinct.push_back(seeds[i]);
-        of[i] = it.first->second;
-    }
-    const uint32_t nd = static_cast<uint32_t>(distinct.size());
-    std::vector<uint32_t> count(nd, 0), first(nd, 0);
-    for (uint32_t i = 0; i < n_members; ++i) ++count[of[i]];
-    for (uint32_t d = 1; d < nd; ++d) first[d] = first[d - 1] + count[d - 1];
-    std::vector<MemberIn> min(n_members);
-    std::vector<uint32_t> fill(first);
-    for (uint32_t i = 0; i < n_members; ++i) min[fill[of[i]]++] = MemberIn{i, signs[i]};
-    std::vector<DistinctIn> din(nd);
-    for (uint32_t d = 0; d < nd; ++d)
-        din[d] = DistinctIn{static_cast<uint32_t>(distinct[d]),
-                            static_cast<uint32_t>(distinct[d] >> 32), first[d], count[d]};
+    MemberTables t;
+    build_member_tables(seeds, signs, n_members, t);
+    const uint32_t nd = t.n_distinct;
 
     // 1 KB of kernel arguments per staging launch
     auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
@@ -1417,8 +1467,8 @@ int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* sig
         }
         return ES_OK;
     };
-    int rc = stage(kOffMembersIn, min.data(), sizeof(MemberIn) * n_members);
-    if (rc == ES_OK) rc = stage(kOffDistinctIn, din.data(), sizeof(DistinctIn) * nd);
+    int rc = stage(kOffMembersIn, t.min, sizeof(MemberIn) * n_members);
+    if (rc == ES_OK) rc = stage(kOffDistinctIn, t.din, sizeof(DistinctIn) * nd);
     if (rc != ES_OK) return rc;
 
     double c = static_cast<double>(opts->alpha) / static_cast<double>(n_members);
@@ -1432,6 +1482,55 @@ int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* sig
                        status_out_dev);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_prepare_kernel launch");
+    return ES_OK;
+}
+
+// The fused update of a bf16 plan with its member tables in `d_scratch`
+// (the plan's, or the static array of es_update_noalloc).
+int update_impl(const char* name, es_plan_t* plan, uint8_t* d_scratch, const uint64_t* seeds,
+                const int32_t* signs, const float* rewards_dev, uint32_t n_members,
+                const es_update_opts_t* opts, float* z_out_dev, int32_t* status_out_dev,
+                hipStream_t s) {
+    int rc = prepare_update(d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
+                            status_out_dev, s);
+    if (rc != ES_OK) return rc;
+    if (plan->n_full + plan->n_tail == 0) return ES_OK;
+    const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
+    const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
+                      static_cast<uint32_t>(opts->round_seed >> 32)};
+    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
+    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tiles,
+                       plan->n_full, plan->n_tail,
+                       reinterpret_cast<const Member*>(d_scratch + kOffMembers),
+                       reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, std::string(name) + ": es_update_kernel launch");
+    return ES_OK;
+}
+
+// Per-device address of the static scratch, looked up once per device (with
+// that device current) and kept; a fixed table, so lookups allocate nothing.
+constexpr int kMaxScratchDevices = 64;
+std::atomic<uint8_t*> g_static_scratch[kMaxScratchDevices];
+std::mutex g_static_scratch_mutex;
+
+int static_scratch(int device, uint8_t** out) {
+    if (device < 0 || device >= kMaxScratchDevices)
+        return fail_in(ES_ERR_DEVICE, "es_update_noalloc", "device index above 63");
+    uint8_t* p = g_static_scratch[device].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        std::lock_guard<std::mutex> lock(g_static_scratch_mutex);
+        p = g_static_scratch[device].load(std::memory_order_relaxed);
+        if (p == nullptr) {
+            void* addr = nullptr;
+            const hipError_t e = hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch));
+            if (e != hipSuccess || addr == nullptr)
+                return hip_fail(e, "es_update_noalloc: hipGetSymbolAddress of the static scratch");
+            p = static_cast<uint8_t*>(addr);
+            g_static_scratch[device].store(p, std::memory_order_release);
+        }
+    }
+    *out = p;
     return ES_OK;
 }
 
@@ -1584,24 +1683,30 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
         rc = check_update_arrays("es_update", plan->device, rewards_dev, n_members, z_out_dev,
                                  status_out_dev);
     if (rc != ES_OK) return rc;
-    hipStream_t s = static_cast<hipStream_t>(stream);
-    rc = prepare_update(plan->d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
-                        status_out_dev, s);
-    if (rc != ES_OK) return rc;
-    if (plan->n_full + plan->n_tail == 0) return ES_OK;
-    const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
-    const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
-                      static_cast<uint32_t>(opts->round_seed >> 32)};
-    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
-    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tiles,
-                       plan->n_full, plan->n_tail,
-                       reinterpret_cast<const Member*>(plan->d_scratch + kOffMembers),
-                       reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffHeader), rk);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_update_kernel launch");
-    return ES_OK;
+    return update_impl("es_update", plan, plan->d_scratch, seeds, signs, rewards_dev, n_members,
+                       opts, z_out_dev, status_out_dev, static_cast<hipStream_t>(stream));
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_update: host allocation failed");
+}
+
+int es_update_noalloc(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
+                      const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+                      float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) try {
+    if (plan == nullptr) return fail_in(ES_ERR_INVALID_ARG, "es_update_noalloc", "null plan");
+    int rc = validate_update("es_update_noalloc", seeds, signs, rewards_dev, n_members, opts);
+    if (rc != ES_OK) return rc;
+    rc = check_device(plan);
+    if (rc == ES_OK)
+        rc = check_update_arrays("es_update_noalloc", plan->device, rewards_dev, n_members,
+                                 z_out_dev, status_out_dev);
+    uint8_t* d_scratch = nullptr;
+    if (rc == ES_OK) rc = static_scratch(plan->device, &d_scratch);
+    if (rc != ES_OK) return rc;
+    return update_impl("es_update_noalloc", plan, d_scratch, seeds, signs, rewards_dev,
+                       n_members, opts, z_out_dev, status_out_dev,
+                       static_cast<hipStream_t>(stream));
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_update_noalloc: host allocation failed (error reporting)");
 }
 
 int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,

@@ -71,6 +71,8 @@ SIGNATURES = {
     "es_zscore": (ctypes.c_int, [_vp, _u32, _f32, _vp, _vp, _vp]),
     "es_update": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp, _u32,
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
+    "es_update_noalloc": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp,
+                                         _u32, ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
     "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
@@ -253,6 +255,14 @@ class Plan:
         round_seed keys the draws of ES_UPDATE_STOCHASTIC_ROUND."""
         _call_update(load().es_update, "es_update", self.handle, seeds, signs, rewards, alpha,
                      sigma, zscore_eps, flags, z_out, status_out, stream, round_seed)
+
+    def update_noalloc(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
+                       z_out=None, status_out=None, stream=None, round_seed=0):
+        """update() through es_update_noalloc: the member tables in the
+        library's static device array (for callers that cannot allocate)."""
+        _call_update(load().es_update_noalloc, "es_update_noalloc", self.handle, seeds, signs,
+                     rewards, alpha, sigma, zscore_eps, flags, z_out, status_out, stream,
+                     round_seed)
 
     def close(self):
         if self._h is not None:

@@ -85,16 +85,17 @@ def test_call_validation_without_device(lib):
     signs = (ctypes.c_int32 * 2)(1, 1)
     bad_signs = (ctypes.c_int32 * 2)(1, 0)
     opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0)
-    U = lib.es_update
-    assert U(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
-    assert U(fake, seeds, signs, fake, 0, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
-    assert U(fake, seeds, signs, fake, 1025, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
-    assert U(fake, seeds, bad_signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
-    for o in [esopt.EsUpdateOpts(float("inf"), 1e-3, 1e-8, 0),
-              esopt.EsUpdateOpts(5e-4, 0.0, 1e-8, esopt.ES_UPDATE_DIV_SIGMA),
-              esopt.EsUpdateOpts(5e-4, 1e-3, -1.0, 0),
-              esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8)]:
-        assert U(fake, seeds, signs, fake, 2, ctypes.byref(o), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    for U, name in ((lib.es_update, "es_update"), (lib.es_update_noalloc, "es_update_noalloc")):
+        assert U(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+        assert U(fake, seeds, signs, fake, 0, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+        assert U(fake, seeds, signs, fake, 1025, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+        assert esopt.last_error() == f"{name}: n_members out of range (1 .. 1024)"
+        assert U(fake, seeds, bad_signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
+        for o in [esopt.EsUpdateOpts(float("inf"), 1e-3, 1e-8, 0),
+                  esopt.EsUpdateOpts(5e-4, 0.0, 1e-8, esopt.ES_UPDATE_DIV_SIGMA),
+                  esopt.EsUpdateOpts(5e-4, 1e-3, -1.0, 0),
+                  esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8)]:
+            assert U(fake, seeds, signs, fake, 2, ctypes.byref(o), None, None, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_philox_words(1, 0, 0, 0, 4, None, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_philox_words(1, 0, 0, 0, 4, ctypes.c_void_p(0x1004), None) == esopt.ES_ERR_ALIGN
     assert lib.es_philox_words(1, 0, 0, 0, 1 << 29, fake, None) == esopt.ES_ERR_INVALID_ARG
