@@ -61,6 +61,8 @@ def parse():
                     help="where a profile pass writes labels.json")
     ap.add_argument("--counters-json", default=os.path.join(REPO, "profiles", "counters.json"),
                     help="per-launch counter values measured with rocprofv3 (see --summarize)")
+    ap.add_argument("--summarize-trace", default=None, metavar="TRACE_DIR",
+                    help="turn a kernel trace of the bench command into profiles/")
     ap.add_argument("--summarize", default=None, metavar="OUT_DIR",
                     help="turn the rocprofv3 runs of a profile pass (OUT_DIR/trace, fetch, write, "
                          "valu) into profiles/")
@@ -490,6 +492,9 @@ def main():
     if args.summarize:
         summarize(args.summarize)
         return
+    if args.summarize_trace:
+        summarize_bench_trace(args.summarize_trace, workload=args.workload)
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "the ES parameter path runs on one GPU; --gpus above 1 is "
                                    "not supported (population parallelism across GPUs is not "
@@ -688,6 +693,8 @@ COUNTER_SETS = {
             "GRBM_GUI_ACTIVE",
 }
 CALIBRATION_COPY_BYTES = 1 << 30
+# counters are collected for the library's kernels and the calibration copy only
+COUNTER_KERNEL_REGEX = "es_[a-z0-9_]*kernel|copyBuffer"
 
 
 def profile_commands(pass_args):
@@ -695,7 +702,8 @@ def profile_commands(pass_args):
     cmds = [f"rocprofv3 --kernel-trace --stats -f csv -d <out>/trace -o trace -- python3 bench.py "
             f"{pass_args} --labels-dir <out>/trace"]
     for run, counters in COUNTER_SETS.items():
-        cmds.append(f"timeout -s KILL 300 rocprofv3 --pmc {counters} -f csv -d <out>/{run} -o {run} "
+        cmds.append(f"timeout -s KILL 300 rocprofv3 --pmc {counters} --kernel-include-regex "
+                    f"'{COUNTER_KERNEL_REGEX}' -f csv -d <out>/{run} -o {run} "
                     f"-- python3 bench.py {pass_args} --labels-dir <out>/{run}")
     return cmds
 
@@ -809,12 +817,17 @@ def _library_dispatches(rows, name_key, id_key):
 
 
 def _read_csv(d, suffix):
+    """The rows of the one *suffix (or *suffix.gz) file under d."""
     import csv
     import glob
-    files = glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+    import gzip
+    files = (glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
+             or glob.glob(os.path.join(d, "**", f"*{suffix}.gz"), recursive=True))
     if not files:
         raise FileNotFoundError(f"no *{suffix} under {d}")
-    return list(csv.DictReader(open(files[0])))
+    opener = gzip.open if files[0].endswith(".gz") else open
+    with opener(files[0], "rt", newline="") as fh:
+        return list(csv.DictReader(fh))
 
 
 def _labels(d):
@@ -952,7 +965,7 @@ def _table(rows):
         P, ns = e["params"], e["ns"]
         vi = e["SQ_INSTS_VALU"]
         clock = e["GRBM_GUI_ACTIVE"] / 8 / e["valu_ns"]
-        kname = e["kernel"].replace("void (anonymous namespace)::", "", 1).split("(")[0]
+        kname = _short_name(e["kernel"])
         tot = e["fetch"] + e["write"]
         lines.append(
             f"| {e['label']} | `{kname}` | {len(e['ns_list'])} | {ns:.0f} | "
@@ -1009,6 +1022,43 @@ def summarize_sweep(out_dir, lab, profiles_dir):
                       "'bound' is hbm where the update takes under 1.5x this time."]
     lines += [""] + _table(rows)[-len(rows) - 3:]
     path = os.path.join(profiles_dir, f"es_update_{lab['workload']}-sweep.md")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    print(path)
+
+
+def _short_name(name, width=90):
+    """A kernel's name without return type, anonymous namespace and
+    argument list, cut to `width` characters."""
+    n = name.replace("(anonymous namespace)::", "")
+    if n.startswith("void "):
+        n = n[5:]
+    n = n.split("(")[0]
+    return n if len(n) <= width else n[:width - 3] + "..."
+
+
+BENCH_TRACE_COMMAND = ("rocprofv3 --kernel-trace --stats -f csv -d <out> -o bench -- python3 "
+                       "bench.py --steps 2 --warmup 1 --no-cpu-baseline")
+
+
+def summarize_bench_trace(trace_dir, profiles_dir=os.path.join(REPO, "profiles"),
+                          workload="dense-27b"):
+    """profiles/bench_kernel_stats_<workload>.md: the --stats table of a
+    kernel trace of the default bench command (every kernel the timed step,
+    the swap walk and the ceiling passes launch)."""
+    stats = _read_csv(trace_dir, "kernel_stats.csv")
+    lines = [f"# Kernel statistics of the benchmark command on {workload}", "",
+             "Command (from the repository root on an MI355X machine, after "
+             "`cd /tmp && export TMPDIR=/tmp`; `<out>` is an output directory; then "
+             "`python3 bench.py --summarize-trace <out>`):", "",
+             f"* `{BENCH_TRACE_COMMAND}`", "", f"Kernel-sources hash: `{_kernel_source_hash()}`",
+             "", "| kernel | calls | average ns | min ns | max ns | share of GPU time |",
+             "|---|---|---|---|---|---|"]
+    for r in stats:
+        name = _short_name(r["Name"])
+        lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']):.0f} | {r['MinNs']} | "
+                     f"{r['MaxNs']} | {float(r['Percentage']):.2f} % |")
+    path = os.path.join(profiles_dir, f"bench_kernel_stats_{workload}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print(path)
