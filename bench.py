@@ -59,6 +59,8 @@ def parse():
                          "one update per N)")
     ap.add_argument("--labels-dir", default=None,
                     help="where a profile pass writes labels.json")
+    ap.add_argument("--profile-repeat", type=int, default=3,
+                    help="launches per label in a profile pass")
     ap.add_argument("--counters-json", default=os.path.join(REPO, "profiles", "counters.json"),
                     help="per-launch counter values measured with rocprofv3 (see --summarize)")
     ap.add_argument("--summarize-trace", default=None, metavar="TRACE_DIR",
@@ -293,14 +295,16 @@ def run_sweep(args):
 
     if args.profile_pass:
         log = ProfileLog(args.labels_dir)
+        R = args.profile_repeat
+        log.add("warm-up in-place copy", "warmup", P, 4 * P, 0, plan.stream_pass, members=-1)
         log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
-                plan.stream_pass, members=0)
+                plan.stream_pass, members=0, repeat=R)
         for n in ns:
             Wn = wl.sweep_workload(n)
             r = torch.from_numpy(wl.rewards(Wn)).cuda()
             flags = esopt.ES_REWARDS_ARE_WEIGHTS if n == 1 else 0
             log.add(f"es_update (N={n})", "update", P, 4 * P, n * P, plan.update, list(Wn.seeds),
-                    list(Wn.signs), r, Wn.alpha, flags=flags, members=n)
+                    list(Wn.signs), r, Wn.alpha, flags=flags, members=n, repeat=R)
         torch.cuda.synchronize()
         plan.close()
         del flat, views
@@ -714,12 +718,15 @@ class ProfileLog:
     def __init__(self, out_dir):
         self.out_dir, self.rows = out_dir, []
 
-    def add(self, label, group, params, bytes_, normals, fn, *a, members=None, **kw):
-        """Launch fn (exactly one library kernel) under `label`; bytes_ is the
-        algorithmic memory traffic, normals the Gaussian draws per launch."""
-        fn(*a, **kw)
-        self.rows.append({"label": label, "group": group, "params": params,
-                          "algorithmic_bytes": bytes_, "normals": normals, "members": members})
+    def add(self, label, group, params, bytes_, normals, fn, *a, members=None, repeat=1, **kw):
+        """Launch fn (exactly one library kernel) `repeat` times under
+        `label`; bytes_ is the algorithmic memory traffic, normals the
+        Gaussian draws per launch."""
+        for _ in range(repeat):
+            fn(*a, **kw)
+            self.rows.append({"label": label, "group": group, "params": params,
+                              "algorithmic_bytes": bytes_, "normals": normals,
+                              "members": members})
 
     def write(self, extra):
         if self.out_dir:
@@ -752,21 +759,31 @@ def run_profile_pass(args):
     P = plan.numel
     nd = len(dict.fromkeys(seeds))
     s0 = W.sigma0
+    R = args.profile_repeat
     other = seeds[1] if N > 1 else seeds[0] + 1
-    log.add("es_perturb", "perturb", P, 4 * P, P, plan.perturb, seeds[0], signs[0], s0)
-    log.add("es_restore", "perturb", P, 4 * P, P, plan.restore, seeds[0], signs[0], s0)
-    log.add("es_swap (two keys)", "swap", P, 4 * P, 2 * P, plan.swap, seeds[0], 1, other, 1, s0)
-    log.add("es_swap (one key, antithetic)", "swap", P, 4 * P, P, plan.swap, other, 1, other, -1,
-            s0)
+    # a first pass over freshly written parameters runs slower: warm up (its
+    # launches are labelled and left out of the summaries)
+    log.add("warm-up perturb", "warmup", P, 4 * P, P, plan.perturb, seeds[0], signs[0], s0)
+    log.add("warm-up restore", "warmup", P, 4 * P, P, plan.restore, seeds[0], signs[0], s0)
+    for _ in range(R):         # alternating, so the parameters stay where they were
+        log.add("es_perturb", "perturb", P, 4 * P, P, plan.perturb, seeds[0], signs[0], s0)
+        log.add("es_restore", "perturb", P, 4 * P, P, plan.restore, seeds[0], signs[0], s0)
+    for _ in range(R):
+        log.add("es_swap (two keys)", "swap", P, 4 * P, 2 * P, plan.swap, seeds[0], 1, other, 1,
+                s0)
+        log.add("es_swap (two keys)", "swap", P, 4 * P, 2 * P, plan.swap, other, 1, seeds[0], 1,
+                s0)
+    log.add("es_swap (one key, antithetic)", "swap", P, 4 * P, P, plan.swap, seeds[0], 1,
+            seeds[0], -1, s0, repeat=2 * R)
     log.add(f"es_update (N={N}, nearest-even)", "update", P, 4 * P, nd * P, plan.update, seeds,
-            signs, rewards, W.alpha, sigma=s0)
+            signs, rewards, W.alpha, sigma=s0, repeat=R)
     log.add(f"es_update (N={N}, stochastic rounding)", "update", P, 4 * P, nd * P, plan.update,
             seeds, signs, rewards, W.alpha, sigma=s0, flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
-            round_seed=1)
+            round_seed=1, repeat=R)
     log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
-            plan.stream_pass)
+            plan.stream_pass, repeat=R)
     out = torch.zeros(1, dtype=torch.int64, device="cuda")
-    log.add("es_plan_checksum", "checksum", P, 2 * P, 0, plan.checksum, out)
+    log.add("es_plan_checksum", "checksum", P, 2 * P, 0, plan.checksum, out, repeat=R)
     torch.cuda.synchronize()
     plan.close()
     del flat, views
@@ -775,10 +792,11 @@ def run_profile_pass(args):
     qflat, qviews, scales, rows = wl.device_qparams(W)
     qplan = esopt.QPlan(qviews, scales, rows)
     QP = qplan.numel
-    log.add("es_qperturb", "int8", QP, 2 * QP, QP, qplan.perturb, seeds[0], signs[0], s0)
-    log.add("es_qrestore", "int8", QP, 2 * QP, QP, qplan.restore, seeds[0], signs[0], s0)
+    for _ in range(R):
+        log.add("es_qperturb", "int8", QP, 2 * QP, QP, qplan.perturb, seeds[0], signs[0], s0)
+        log.add("es_qrestore", "int8", QP, 2 * QP, QP, qplan.restore, seeds[0], signs[0], s0)
     log.add(f"es_qupdate (N={N})", "int8", QP, 2 * QP, nd * QP, qplan.update, seeds, signs,
-            rewards, W.alpha, sigma=s0, round_seed=1)
+            rewards, W.alpha, sigma=s0, round_seed=1, repeat=R)
     torch.cuda.synchronize()
     qplan.close()
     del qflat, qviews, scales
@@ -792,7 +810,7 @@ def run_profile_pass(args):
                                     (esopt.CALIBRATE_WRITE, "write", 1),
                                     (esopt.CALIBRATE_READ_WRITE, "in-place", 2)):
             log.add(f"es_hbm_calibrate {mname}, {pname} accesses (16 GiB)", "ceiling", 0,
-                    factor * B, 0, esopt.hbm_calibrate, cal, mode | pol, sink)
+                    factor * B, 0, esopt.hbm_calibrate, cal, mode | pol, sink, repeat=R)
     torch.cuda.synchronize()
     del cal
     torch.cuda.empty_cache()
@@ -990,7 +1008,7 @@ def summarize_sweep(out_dir, lab, profiles_dir):
     if src != _kernel_source_hash():
         raise RuntimeError("profile taken on other kernel sources than the working tree's")
     cmds = profile_commands(lab["pass_args"])
-    rows = sorted(per["_rows"], key=lambda e: e["members"])
+    rows = sorted((e for e in per["_rows"] if e["group"] != "warmup"), key=lambda e: e["members"])
     lines = [f"# Fused es_update population sweep on {lab['workload']} ({lab['params']:,} bf16 "
              f"parameters, rewards N(0,1), distinct seeds)", "",
              "Commands (from the repository root on an MI355X machine, after "
