@@ -840,11 +840,12 @@ def _read_csv(d, suffix):
     import glob
     import gzip
     files = (glob.glob(os.path.join(d, "**", f"*{suffix}"), recursive=True)
-             or glob.glob(os.path.join(d, "**", f"*{suffix}.gz"), recursive=True))
+             + glob.glob(os.path.join(d, "**", f"*{suffix}.gz"), recursive=True))
     if not files:
         raise FileNotFoundError(f"no *{suffix} under {d}")
-    opener = gzip.open if files[0].endswith(".gz") else open
-    with opener(files[0], "rt", newline="") as fh:
+    path = max(files, key=os.path.getmtime)          # the latest run's file
+    opener = gzip.open if path.endswith(".gz") else open
+    with opener(path, "rt", newline="") as fh:
         return list(csv.DictReader(fh))
 
 
