@@ -1295,6 +1295,17 @@ int release_device_memory(int device, void* tab, void* scratch, const char* name
     return rc;
 }
 
+// Division by a row length r >= 2 as a multiply-high and a shift:
+// j / r = mulhi(j, magic) >> shift for every j < 2^31 (Granlund and
+// Montgomery, 1994: magic = ceil(2^(31 + l) / r) with 2^(l-1) < r <= 2^l,
+// which lies in [2^31, 2^32)).
+void row_divisor(uint32_t r, uint32_t& magic, uint32_t& shift) {
+    uint32_t l = 0;
+    while ((uint64_t(1) << l) < r) ++l;
+    magic = static_cast<uint32_t>(((uint64_t(1) << (31 + l)) + r - 1) / r);
+    shift = l - 1;
+}
+
 // Launch shape of the bf16 tile kernels: the defaults, or overrides for
 // launch-shape sweeps.
 void launch_shape(int& threads, int& groups) {
@@ -1774,14 +1785,7 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
         const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
         const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
         uint32_t magic = 0, shift = 0;
-        if (t.row != 0) {
-            // row index j / row = mulhi(j, magic) >> shift for all j < 2^31
-            uint32_t l = 0;
-            while ((uint64_t(1) << l) < t.row) ++l;
-            const uint64_t m = ((uint64_t(1) << (31 + l)) + t.row - 1) / t.row;
-            magic = static_cast<uint32_t>(m);
-            shift = l - 1;
-        }
+        if (t.row != 0) row_divisor(t.row, magic, shift);
         tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales, t.numel, n_full, n_tail,
                                  t.row, t.tensor_id, magic, shift, n_tensors,
                                  (a % 16 == 0) ? 1u : 0u};

@@ -1,0 +1,237 @@
+// Host-side checks of the library's own host code, built with AddressSanitizer
+// and UndefinedBehaviorSanitizer (host pass only, no device code): the
+// population tables of the update, the tiling of tensors, the int8 row
+// divisor, and every argument check that fails before the device is touched.
+// The library source is compiled into this translation unit, so its internal
+// (anonymous-namespace) routines are reachable; each is compared with a plain
+// reference written here.  Prints "ok" and exits 0, or names the first
+// failure and exits 1.
+#include "../../paper_2608_17310_amd/csrc/esopt.hip"
+
+#include <cstdio>
+#include <random>
+
+namespace {
+
+int g_failures = 0;
+
+void check(bool ok, const char* what) {
+    if (!ok && g_failures++ < 20) std::printf("FAIL: %s\n", what);
+}
+
+// Population tables: distinct seeds in order of first appearance, members
+// grouped by seed in member order.
+void test_member_tables(std::mt19937_64& rng) {
+    for (int trial = 0; trial < 400; ++trial) {
+        const uint32_t n = trial < 4 ? uint32_t(trial == 3 ? ES_MAX_MEMBERS : trial + 1)
+                                     : uint32_t(1 + rng() % ES_MAX_MEMBERS);
+        const uint64_t pool = 1 + rng() % (trial % 3 == 0 ? 4 : n + 3);   // repeats likely
+        std::vector<uint64_t> seeds(n);
+        std::vector<int32_t> signs(n);
+        for (uint32_t i = 0; i < n; ++i) {
+            seeds[i] = (rng() % pool) * 0x9E3779B97F4A7C15ull;              // spread over 64 bits
+            signs[i] = (rng() & 1) ? 1 : -1;
+        }
+        MemberTables t;
+        build_member_tables(seeds.data(), signs.data(), n, t);
+        // reference: first appearances by a quadratic scan
+        std::vector<uint64_t> distinct;
+        for (uint32_t i = 0; i < n; ++i) {
+            bool seen = false;
+            for (uint64_t d : distinct) seen |= (d == seeds[i]);
+            if (!seen) distinct.push_back(seeds[i]);
+        }
+        check(t.n_distinct == distinct.size(), "member tables: distinct count");
+        uint32_t pos = 0;
+        for (uint32_t d = 0; d < t.n_distinct && d < distinct.size(); ++d) {
+            const uint64_t key = uint64_t(t.din[d].k0) | (uint64_t(t.din[d].k1) << 32);
+            check(key == distinct[d], "member tables: distinct order");
+            check(t.din[d].first == pos, "member tables: CSR offsets");
+            uint32_t expect_count = 0;
+            for (uint32_t i = 0; i < n; ++i) {
+                if (seeds[i] != distinct[d]) continue;
+                check(t.min[pos + expect_count].reward_index == i, "member tables: member order");
+                check(t.min[pos + expect_count].sign == signs[i], "member tables: signs");
+                ++expect_count;
+            }
+            check(t.din[d].count == expect_count, "member tables: counts");
+            pos += expect_count;
+        }
+        check(pos == n, "member tables: every member once");
+    }
+}
+
+// Tiling: every element in exactly one tile, tiles sorted full-then-tail,
+// full tiles whole and on tile-sized address boundaries.
+void test_tiling(std::mt19937_64& rng) {
+    const uint64_t tile = uint64_t(kDefaultThreads) * kDefaultGroups * kGroupElems;
+    std::vector<es_tile_info_t> out;
+    for (int trial = 0; trial < 600; ++trial) {
+        const uint64_t addr = (rng() % (uint64_t(1) << 40)) & ~uint64_t(trial % 4 == 0 ? 1 : 15);
+        const uint64_t numel = trial % 5 == 0 ? rng() % 20 : rng() % (5 * tile + 3);
+        const uint32_t off8 = trial % 7 == 0 ? uint32_t(rng() % (1u << 31)) : 0u;
+        uint64_t n = 0;
+        check(es_tile_layout(addr, numel, off8, nullptr, 0, &n) == ES_OK, "tile layout: count");
+        out.assign(n + 1, es_tile_info_t{});
+        uint64_t n2 = 0;
+        check(es_tile_layout(addr, numel, off8, out.data(), n, &n2) == ES_OK && n2 == n,
+              "tile layout: list");
+        std::vector<uint8_t> cover(numel, 0);
+        bool tails = false;
+        for (uint64_t i = 0; i < n; ++i) {
+            const es_tile_info_t& ti = out[i];
+            const uint64_t base = 8 * uint64_t(off8);
+            check(ti.elem0 >= base && ti.end <= base + numel && ti.elem0 < ti.end,
+                  "tile layout: tile inside the tensor");
+            if (ti.full) {
+                check(!tails, "tile layout: full tiles first");
+                check(ti.end - ti.elem0 == tile, "tile layout: full tile size");
+                check((addr + 2 * (ti.elem0 - base)) % (2 * tile) == 0,
+                      "tile layout: full tile on an address boundary");
+            } else {
+                tails = true;
+                check(ti.end - ti.elem0 <= tile, "tile layout: tail tile size");
+            }
+            for (uint64_t e = ti.elem0; e < ti.end && e - base < numel; ++e) ++cover[e - base];
+        }
+        bool once = true;
+        for (uint8_t c : cover) once &= (c == 1);
+        check(once, "tile layout: every element in exactly one tile");
+        // a short output array receives only `cap` entries
+        if (n > 1) {
+            es_tile_info_t one[1];
+            check(es_tile_layout(addr, numel, off8, one, 1, &n2) == ES_OK && n2 == n,
+                  "tile layout: capped output");
+        }
+    }
+    uint64_t n = 0;
+    check(es_tile_layout(1, 10, 0, nullptr, 0, &n) == ES_ERR_ALIGN, "tile layout: odd address");
+    check(es_tile_layout(0, 10, 0, nullptr, 0, nullptr) == ES_ERR_INVALID_ARG,
+          "tile layout: null count");
+    check(es_tile_layout(0, uint64_t(1) << 61, 0, nullptr, 0, &n) == ES_ERR_INVALID_ARG,
+          "tile layout: above 2^60");
+    check(es_tile_layout(0, 10, 0, nullptr, 5, &n) == ES_ERR_INVALID_ARG,
+          "tile layout: null output with a capacity");
+}
+
+// Row divisor: exact for every j < 2^31 (boundaries of every row, and random j).
+void test_row_divisor(std::mt19937_64& rng) {
+    std::vector<uint32_t> rows = {8, 16, 24, 64, 1000, 1024, 5120, 17408, 151936, 1u << 20,
+                                  (1u << 30) + 8, 0x7FFFFFF8u};
+    for (int i = 0; i < 200; ++i) rows.push_back(8 * uint32_t(1 + rng() % (1u << 27)));
+    for (uint32_t r : rows) {
+        uint32_t magic = 0, shift = 0;
+        row_divisor(r, magic, shift);
+        auto q = [&](uint32_t j) {
+            return uint32_t((uint64_t(j) * magic) >> 32) >> shift;
+        };
+        bool ok = true;
+        for (uint64_t k = 0; k * r < (uint64_t(1) << 31) && k < 4096; ++k) {
+            const uint64_t j = k * r;
+            ok &= q(uint32_t(j)) == k;
+            if (j > 0) ok &= q(uint32_t(j - 1)) == k - 1;
+        }
+        const uint32_t top = 0x7FFFFFFFu;
+        ok &= q(top) == top / r;
+        ok &= q(top - top % r) == top / r;
+        for (int t = 0; t < 2000; ++t) {
+            const uint32_t j = uint32_t(rng() % (uint64_t(1) << 31));
+            ok &= q(j) == j / r;
+        }
+        check(ok, "row divisor: exact below 2^31");
+    }
+}
+
+// Argument checks that must fail before any device access.
+void test_validation() {
+    const uint64_t seeds[3] = {1, 2, 3};
+    const int32_t signs[3] = {1, -1, 1}, bad_signs[3] = {1, 0, 1};
+    es_update_opts_t o{5e-4f, 1e-3f, 1e-8f, 0u, 0u};
+    const float* fake = reinterpret_cast<const float*>(uintptr_t(0x1000));
+    check(validate_update("t", seeds, signs, fake, 3, &o) == ES_OK, "validate: good call");
+    check(validate_update("t", nullptr, signs, fake, 3, &o) == ES_ERR_INVALID_ARG, "validate: seeds");
+    check(validate_update("t", seeds, bad_signs, fake, 3, &o) == ES_ERR_INVALID_ARG, "validate: signs");
+    check(validate_update("t", seeds, signs, fake, 0, &o) == ES_ERR_INVALID_ARG, "validate: n = 0");
+    check(validate_update("t", seeds, signs, fake, ES_MAX_MEMBERS + 1, &o) == ES_ERR_INVALID_ARG,
+          "validate: n too large");
+    es_update_opts_t bad = o;
+    bad.flags = 64;
+    check(validate_update("t", seeds, signs, fake, 3, &bad) == ES_ERR_INVALID_ARG, "validate: flags");
+    bad = o;
+    bad.alpha = NAN;
+    check(validate_update("t", seeds, signs, fake, 3, &bad) == ES_ERR_INVALID_ARG, "validate: alpha");
+    check(std::string(es_last_error()) == "t: alpha not finite", "validate: message");
+    check(es_update(nullptr, seeds, signs, fake, 3, &o, nullptr, nullptr, nullptr) ==
+              ES_ERR_INVALID_ARG, "es_update: null plan");
+    check(es_update_noalloc(nullptr, seeds, signs, fake, 3, &o, nullptr, nullptr, nullptr) ==
+              ES_ERR_INVALID_ARG, "es_update_noalloc: null plan");
+
+    es_plan_t* plan = reinterpret_cast<es_plan_t*>(uintptr_t(0xdead));
+    check(es_plan_create(nullptr, 1, &plan) == ES_ERR_INVALID_ARG && plan == nullptr,
+          "plan create: null list");
+    alignas(16) static uint16_t buf[64];
+    es_tensor_t ts[3] = {{buf, 8, 0, 0}, {buf + 8, 8, 0, 0}, {buf + 16, 8, 2, 0}};
+    check(es_plan_create(ts, 2, &plan) == ES_ERR_INVALID_ARG, "plan create: duplicate ids");
+    ts[1].tensor_id = 1;
+    ts[1].data = buf + 4;
+    check(es_plan_create(ts, 2, &plan) == ES_ERR_INVALID_ARG, "plan create: overlap");
+    ts[1].data = reinterpret_cast<uint8_t*>(buf + 20) + 1;
+    check(es_plan_create(ts, 2, &plan) == ES_ERR_ALIGN, "plan create: odd address");
+    ts[1].data = nullptr;
+    check(es_plan_create(ts, 2, &plan) == ES_ERR_INVALID_ARG, "plan create: null data");
+    ts[1].data = buf + 20;
+    ts[1].numel = uint64_t(1) << 61;
+    check(es_plan_create(ts, 2, &plan) == ES_ERR_INVALID_ARG, "plan create: too large");
+    check(es_plan_create(ts, 0, &plan) == ES_ERR_INVALID_ARG, "plan create: no tensors");
+    check(es_plan_create(ts, 1, nullptr) == ES_ERR_INVALID_ARG, "plan create: null output");
+
+    alignas(16) static int8_t codes[64];
+    alignas(4) static float scales[8];
+    es_qtensor_t qt[2] = {{codes, scales, 16, 8, 0}, {codes + 16, scales, 16, 8, 0}};
+    es_qplan_t* qp = nullptr;
+    check(es_qplan_create(qt, 2, &qp) == ES_ERR_INVALID_ARG, "qplan create: duplicate ids");
+    qt[1].tensor_id = 1;
+    qt[1].row = 12;
+    check(es_qplan_create(qt, 2, &qp) == ES_ERR_INVALID_ARG, "qplan create: row");
+    qt[1].row = 8;
+    qt[1].data = codes + 8;
+    check(es_qplan_create(qt, 2, &qp) == ES_ERR_INVALID_ARG, "qplan create: overlap");
+    qt[1].data = codes + 16;
+    qt[1].scales = reinterpret_cast<const float*>(reinterpret_cast<const char*>(scales) + 2);
+    check(es_qplan_create(qt, 2, &qp) == ES_ERR_ALIGN, "qplan create: scales alignment");
+    qt[1].scales = scales;
+    qt[1].numel = uint64_t(1) << 31;
+    check(es_qplan_create(qt, 2, &qp) == ES_ERR_INVALID_ARG, "qplan create: numel");
+
+    check(es_perturb(nullptr, 1, 1, 1e-3f, nullptr) == ES_ERR_INVALID_ARG, "perturb: null plan");
+    check(es_swap(nullptr, 1, 1, 1e-3f, 2, 1, 1e-3f, nullptr) == ES_ERR_INVALID_ARG, "swap: null");
+    check(es_zscore(nullptr, 4, 1e-8f, nullptr, nullptr, nullptr) == ES_ERR_INVALID_ARG, "zscore");
+    check(es_hbm_calibrate(nullptr, 1 << 17, 1, nullptr, nullptr) == ES_ERR_INVALID_ARG,
+          "calibrate: null");
+    check(es_hbm_calibrate(buf, 1 << 17, 7, nullptr, nullptr) == ES_ERR_INVALID_ARG,
+          "calibrate: mode");
+    check(es_philox_words(1, 0, 0, 0, 4, nullptr, nullptr) == ES_ERR_INVALID_ARG, "words: null");
+    check(es_normals(1, 0, 0, 4, nullptr, nullptr) == ES_ERR_INVALID_ARG, "normals: null");
+    for (int code = -6; code <= 0; ++code) check(es_strerror(code) != nullptr, "strerror");
+
+    check(std::isnan(es_sigma_cosine(1e-3, 1e-4, 5, 4)), "sigma: t > T");
+    check(std::isnan(es_sigma_cosine(1e-3, 1e-4, 0, 0)), "sigma: T = 0");
+    check(es_sigma_cosine(1e-3, 1e-4, 0, 100) == 1e-3, "sigma: t = 0");
+    check(es_sigma_cosine(1e-3, 1e-4, 100, 100) == 1e-4, "sigma: t = T");
+}
+
+}  // namespace
+
+int main() {
+    std::mt19937_64 rng(20261202);
+    test_member_tables(rng);
+    test_tiling(rng);
+    test_row_divisor(rng);
+    test_validation();
+    if (g_failures) {
+        std::printf("%d failures\n", g_failures);
+        return 1;
+    }
+    std::printf("ok\n");
+    return 0;
+}
