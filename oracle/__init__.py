@@ -30,7 +30,9 @@ mod 2^64: the library's parameter checksum, used to check a replayed run.
 
 The int8 path (quant.py) perturbs and updates symmetric int8 codes with
 per-row scales in units of the quantum, rounding offsets stochastically; the
-paper lists quantized ES as future work (Appendix A.2).
+fp8 path (fp8.py) does the same on the grid of the E4M3 format, rounding the
+scaled value stochastically onto it; the paper lists quantized ES as future
+work (Appendix A.2).
 
 Pin status of every function is listed in the module docstrings; all functions
 are pinned (none is "parity unpinned").
@@ -46,6 +48,9 @@ from .es import (perturb, restore, swap, zscore, update_coefficient, member_weig
 from .quant import (QMAX, row_scales, round_offset, round_offset9, offset_values, qperturb,
                     qrestore, update_values, qupdate)
 from .checksum import mix64, checksum, qchecksum, plan_checksum
+from . import fp8
+from .fp8 import (E4M3_MAX, e4m3_decode, e4m3_encode, grid_floor, round_onto_grid, f8perturb,
+                  f8restore, f8update_values, f8update)
 
 __all__ = [
     "philox4x32_10", "philox4x32_10_bigint", "MASK32",
@@ -57,4 +62,6 @@ __all__ = [
     "ES_UPDATE_STOCHASTIC_ROUND",
     "QMAX", "row_scales", "round_offset", "round_offset9", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",
     "mix64", "checksum", "qchecksum", "plan_checksum",
+    "fp8", "E4M3_MAX", "e4m3_decode", "e4m3_encode", "grid_floor", "round_onto_grid",
+    "f8perturb", "f8restore", "f8update_values", "f8update",
 ]
