@@ -49,6 +49,8 @@ def parse():
     ap.add_argument("--int8", action="store_true",
                     help="the int8 path: codes with per-row scales, es_qperturb / es_qrestore / "
                          "es_qupdate")
+    ap.add_argument("--fp8", action="store_true",
+                    help="the fp8 path: E4M3 codes with per-row scales (es_qplan_create_format)")
     ap.add_argument("--stochastic-round", action="store_true",
                     help="round the update stochastically (ES_UPDATE_STOCHASTIC_ROUND)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
@@ -215,41 +217,54 @@ def host_samples(W, per_tensor=1 << 16):
 
 
 def _oracle_qchunk(args):
-    """The oracle's work of one int8 step on a sample of one tensor's codes."""
+    """The oracle's work of one int8 or fp8 step on a sample of one tensor's
+    codes."""
     import oracle
-    q, scales, row, tid, elems, seeds, signs, rewards, alpha, sigma = args
+    q, scales, row, tid, elems, seeds, signs, rewards, alpha, sigma, fmt = args
+    if fmt == "e4m3":
+        perturb, restore, update = oracle.f8perturb, oracle.f8restore, oracle.f8update
+    else:
+        perturb, restore, update = oracle.qperturb, oracle.qrestore, oracle.qupdate
     t0 = time.perf_counter()
     for s, sg in zip(seeds, signs):
-        p = oracle.qperturb(q, scales, row, s, tid, sg, sigma, elems=elems)
-        q = oracle.qrestore(p, scales, row, s, tid, sg, sigma, elems=elems)
-    q, _ = oracle.qupdate(q, scales, row, tid, seeds, signs, rewards, alpha, sigma, elems=elems,
-                          round_seed=1)
+        p = perturb(q, scales, row, s, tid, sg, sigma, elems=elems)
+        q = restore(p, scales, row, s, tid, sg, sigma, elems=elems)
+    q, _ = update(q, scales, row, tid, seeds, signs, rewards, alpha, sigma, elems=elems,
+                  round_seed=1)
     return time.perf_counter() - t0
 
 
-def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_tensor=1 << 14):
-    """The oracle's int8 step on a bounded sample: random codes and indices,
-    per-row scales of the workload's shapes (values do not change the cost)."""
+def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_tensor=1 << 14,
+                      fmt="int8"):
+    """The oracle's int8 (or fp8) step on a bounded sample: random codes and
+    indices, per-row scales of the workload's shapes (values do not change
+    the cost)."""
     from paper_2608_17310_amd import workloads as wl
     rng = np.random.default_rng(0)
     samples = []
     for tid, (n, shape) in enumerate(zip(W.numels, W.shapes)):
         row = wl.row_of(shape)
         idx = np.unique(rng.integers(0, n, size=min(n, per_tensor))).astype(np.uint64)
-        scales = rng.uniform(3e-4, 1e-3, 1 if row == 0 else n // row).astype(np.float32)
-        codes = rng.integers(-127, 128, size=idx.size).astype(np.int8)
+        if fmt == "e4m3":
+            scales = rng.uniform(1.5e-4, 3e-4, 1 if row == 0 else n // row).astype(np.float32)
+            codes = rng.integers(0, 0x7E, size=idx.size).astype(np.uint8) | \
+                (rng.integers(0, 2, size=idx.size).astype(np.uint8) << 7)
+        else:
+            scales = rng.uniform(3e-4, 1e-3, 1 if row == 0 else n // row).astype(np.float32)
+            codes = rng.integers(-127, 128, size=idx.size).astype(np.int8)
         samples.append((codes, scales, row, tid, idx))
     n = len(seeds)
     c0 = samples[0]
     t_small = _oracle_qchunk((c0[0][:1024], c0[1], c0[2], c0[3], c0[4][:1024], seeds, signs,
-                              rewards, W.alpha, sigma))
+                              rewards, W.alpha, sigma, fmt))
     per_elem = t_small / 1024
     total = sum(x[4].size for x in samples)
     frac = min(1.0, int(budget_s * workers / per_elem) / total)
     jobs = []
     for codes, scales, row, tid, idx in samples:
         k = max(1, int(idx.size * frac))
-        jobs.append((codes[:k], scales, row, tid, idx[:k], seeds, signs, rewards, W.alpha, sigma))
+        jobs.append((codes[:k], scales, row, tid, idx[:k], seeds, signs, rewards, W.alpha, sigma,
+                     fmt))
     n_elems = sum(j[4].size for j in jobs)
     t0 = time.perf_counter()
     with mp.get_context("fork").Pool(workers) as pool:
@@ -259,9 +274,9 @@ def cpu_baseline_int8(W, seeds, signs, rewards, sigma, workers, budget_s, per_te
     return {"value": rate, "unit": "params/s", "cores": workers, "kind": "oracle",
             **host_cpu(),
             "full_step_s_extrapolated": round((2 * n + 1) * W.n_params / rate, 1),
-            "sample": f"{n_elems} int8 codes sampled across {len(jobs)} tensors of {W.name}, one "
-                      f"full int8 step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 NumPy "
-                      f"over {workers} worker processes, {wall:.1f} s wall"}
+            "sample": f"{n_elems} {fmt} codes sampled across {len(jobs)} tensors of {W.name}, "
+                      f"one full {fmt} step (N={n}: {2 * n} perturb/restore + 1 update) in fp64 "
+                      f"NumPy over {workers} worker processes, {wall:.1f} s wall"}
 
 
 # ---------------------------------------------------------------- GPU leg --
@@ -348,10 +363,13 @@ def run_sweep(args):
 
 
 def run_int8(args):
-    """The int8 step on the workload's shapes: N x (es_qperturb + es_qrestore)
-    + es_qupdate over codes with per-row scales, inputs resident in HBM."""
+    """The int8 (or, with --fp8, the E4M3) step on the workload's shapes:
+    N x (es_qperturb + es_qrestore) + es_qupdate over codes with per-row
+    scales, inputs resident in HBM."""
     import torch
     from paper_2608_17310_amd import esopt, workloads as wl
+    fmt = "e4m3" if args.fp8 else "int8"
+    tag = "fp8" if args.fp8 else "int8"
     W = wl.WORKLOADS[args.workload]
     n_members = args.members
     signs = list(W.signs) if n_members is None else [1] * n_members
@@ -362,13 +380,13 @@ def run_int8(args):
         cpu = cpu_baseline_int8(W, step_seeds(W, args.warmup, n_members), signs,
                                 wl.rewards(W, args.warmup, n=N),
                                 sigma_at(oracle.sigma_cosine, W, args.warmup),
-                                cpu_workers()[0], args.cpu_seconds)
+                                cpu_workers()[0], args.cpu_seconds, fmt=fmt)
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU"}))
         sys.exit(1)
     torch.cuda.set_device(0)
-    flat, views, scales, rows = wl.device_qparams(W)
-    plan = esopt.QPlan(views, scales, rows)
+    flat, views, scales, rows = (wl.device_f8params if args.fp8 else wl.device_qparams)(W)
+    plan = esopt.QPlan(views, scales, rows, format=fmt)
     P = plan.numel
     stream = torch.cuda.current_stream()
     total_steps = args.warmup + args.steps
@@ -397,9 +415,9 @@ def run_int8(args):
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
                             for t in range(args.warmup, total_steps)]))
-    label = W.name + "-int8"
-    c_pert = _counters_for(args.counters_json, "es_qperturb", label)
-    c_upd = _counters_for(args.counters_json, "es_qupdate", label)
+    label = f"{W.name}-{tag}"
+    c_pert = _counters_for(args.counters_json, f"es_{'f8' if args.fp8 else 'q'}perturb", label)
+    c_upd = _counters_for(args.counters_json, f"es_{'f8' if args.fp8 else 'q'}update", label)
 
     def alu_roofline(c, t, kernel, extra):
         r = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
@@ -413,21 +431,25 @@ def run_int8(args):
         return r
     same_config = N == len(W.seeds) and n_members is None
     out = {
-        "metric": "params/s of the int8 ES step (es_qperturb/es_qrestore and fused es_qupdate, "
-                  "N members)",
+        "metric": f"params/s of the {tag} ES step (es_qperturb/es_qrestore and fused "
+                  f"es_qupdate, N members)",
         "value": value, "unit": "params/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 3), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "param_dtype": "int8",
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "param_dtype": "e4m3" if args.fp8 else "int8",
         "data": "synthetic",
         "config": {"workload": label, "params": P, "tensors": len(views), "members": N,
                    "param_bytes": P + 4 * sum(int(x.numel()) for x in scales),
                    "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
-                   "scales": "one binary32 scale per row of the last dimension, one per vector",
+                   "scales": "one binary32 scale per row of the last dimension, one per vector"
+                             + (" (absmax / 448)" if args.fp8 else " (absmax / 127)"),
                    "counting": "value = (2N+1) P / step time: 2N perturb/restore passes and one "
                                "fused N-member update pass per step"},
-        "roofline": alu_roofline(c_pert, t_pert, "es_qpass_kernel (es_qperturb / es_qrestore)", True),
-        "roofline_update": alu_roofline(c_upd, t_upd, "es_qpass_kernel (es_qupdate)", same_config),
+        "roofline": alu_roofline(c_pert, t_pert, f"es_qpass_kernel, {fmt} "
+                                 "(es_qperturb / es_qrestore)", True),
+        "roofline_update": alu_roofline(c_upd, t_upd, f"es_qpass_kernel, {fmt} (es_qupdate)",
+                                        same_config),
         "per_kernel": {
             "es_qperturb": {"ms": round(t_pert * 1e3, 3), "params_per_s": P / t_pert,
                             "GBps_algorithmic": round(2 * P / t_pert / 1e9, 1)},
@@ -508,7 +530,7 @@ def main():
         return run_sweep(args)
     if args.profile_pass:
         return run_profile_pass(args)
-    if args.int8:
+    if args.int8 or args.fp8:
         return run_int8(args)
     import torch
     from paper_2608_17310_amd import workloads as wl
@@ -802,6 +824,18 @@ def run_profile_pass(args):
     del qflat, qviews, scales
     torch.cuda.empty_cache()
 
+    fflat, fviews, fscales, frows = wl.device_f8params(W)
+    fplan = esopt.QPlan(fviews, fscales, frows, format="e4m3")
+    for _ in range(R):
+        log.add("es_f8perturb", "fp8", QP, 2 * QP, QP, fplan.perturb, seeds[0], signs[0], s0)
+        log.add("es_f8restore", "fp8", QP, 2 * QP, QP, fplan.restore, seeds[0], signs[0], s0)
+    log.add(f"es_f8update (N={N})", "fp8", QP, 2 * QP, nd * QP, fplan.update, seeds, signs,
+            rewards, W.alpha, sigma=s0, round_seed=1, repeat=R)
+    torch.cuda.synchronize()
+    fplan.close()
+    del fflat, fviews, fscales
+    torch.cuda.empty_cache()
+
     cal = torch.empty(16 << 30, dtype=torch.uint8, device="cuda")
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
     B = cal.numel()
@@ -885,6 +919,8 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
                                 f"N = {lab['members']}, {lab['distinct_seeds']} distinct seeds)"),
         "int8": ("es_qpass", f"int8 passes on {wname}-int8 (the same shapes as int8 codes with "
                              f"per-row scales)"),
+        "fp8": ("es_qpass", f"fp8 passes on {wname}-fp8 (the same shapes as E4M3 codes with "
+                            f"per-row scales)"),
         "ceiling": ("hbm_ceilings", f"HBM ceilings: the in-place stream over the {wname} plan and "
                                     f"the flat-buffer calibration passes"),
         "checksum": ("es_plan_checksum", f"es_plan_checksum on {wname}"),
@@ -893,20 +929,22 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
     counters = json.load(open(counters_path)) if os.path.exists(counters_path) else {}
     keys = {"es_perturb": "es_perturb", f"es_update (N={lab['members']}, nearest-even)": "es_update",
             "es_swap (two keys)": "es_swap", "es_qperturb": "es_qperturb",
-            f"es_qupdate (N={lab['members']})": "es_qupdate"}
+            f"es_qupdate (N={lab['members']})": "es_qupdate", "es_f8perturb": "es_f8perturb",
+            f"es_f8update (N={lab['members']})": "es_f8update"}
     for group, (stem, title) in groups.items():
         rows = [r for r in per["_rows"] if r["group"] == group]
         if not rows:
             continue
         lines = [f"# {title}", ""] + header + _table(rows)
-        fname = f"{stem}_{wname}{'-int8' if group == 'int8' else ''}.md"
+        suffix = {"int8": "-int8", "fp8": "-fp8"}.get(group, "")
+        fname = f"{stem}_{wname}{suffix}.md"
         with open(os.path.join(profiles_dir, fname), "w") as fh:
             fh.write("\n".join(lines) + "\n")
         for r in rows:
             k = keys.get(r["label"])
             if k:
                 counters[k] = {"source_hash": src,
-                               "workload": wname + ("-int8" if group == "int8" else ""),
+                               "workload": wname + suffix,
                                "params": r["params"], "bytes_per_launch": r["fetch"] + r["write"],
                                "fetch_bytes": r["fetch"], "write_bytes": r["write"],
                                "valu_insts_per_launch": r["SQ_INSTS_VALU"], "avg_ns": r["ns"],

@@ -276,6 +276,42 @@ typedef struct es_qplan es_qplan_t;
  * es_plan_create; overlapping code ranges and duplicate ids are rejected;
  * scales may be shared). */
 int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out);
+
+/* Code formats of a quantized plan (one format per plan). */
+#define ES_QFORMAT_INT8  0u   /* symmetric int8 codes (above) */
+#define ES_QFORMAT_E4M3  1u   /* fp8 E4M3 codes (below) */
+
+/* A plan over fp8 E4M3 codes (format ES_QFORMAT_E4M3; ES_QFORMAT_INT8 is
+ * es_qplan_create).  Each es_qtensor_t then holds one-byte codes of the OCP
+ * 8-bit floating-point format with 4 exponent and 3 mantissa bits, bias 7
+ * (PyTorch's float8_e4m3fn): theta_j = s_r v(c_j), v up to +-448, codes 0x7F
+ * and 0xFF not a number; the scales, rows, ids and limits are as for int8.
+ * The passes of the plan (es_qperturb, es_qrestore, es_qupdate,
+ * es_qplan_checksum) then work on the E4M3 grid (Appendix A.2's quantized
+ * ES, the library's reading): a pass forms x = v(c) + step, in scale units
+ * and binary32, and rounds it onto the grid stochastically --
+ *   lo = the largest grid value <= x, h the spacing to the next one,
+ *   f = (x - lo) / h;  result = lo + h if f >= thr (perturb, update) or
+ *   f > thr (restore), else lo;  clamped to [-448, 448]
+ * -- with
+ *   perturb: x = v + sign sigma eps_j / s, thr = 1 - u,
+ *            u = (2 r + 1) 2^-10, r the top 9 bits of word j & 3 of element
+ *            j's own noise call (as es_qperturb's int8 draw);
+ *   restore: y = v - sign sigma eps_j / s, thr = u (the same u), which
+ *            returns the original code exactly wherever the perturbation's
+ *            x, the perturbed value and y stay in one binade of the grid, x
+ *            below 448 (a perturbation into
+ *            a coarser binade maps two codes to one, and its revert is off by
+ *            at most one step of the coarser grid);
+ *   update:  x = v + sum_d w_d eps_j(seed_d) / s with es_update's merged
+ *            weights, thr = 1 - r 2^-16 with es_update's 16-bit stochastic
+ *            rounding draws (domain 1 under opts->round_seed); always
+ *            stochastic.
+ * Not-a-number codes and the codes of invalid scales are left unchanged; a
+ * zero result is +0 (code 0x00).  Errors as es_qplan_create, and
+ * ES_ERR_INVALID_ARG for an unknown format. */
+int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint32_t format,
+                           es_qplan_t** out);
 int es_qplan_destroy(es_qplan_t* plan);
 uint64_t es_qplan_numel(const es_qplan_t* plan);
 uint64_t es_qplan_device_bytes(const es_qplan_t* plan);   /* as es_plan_device_bytes */

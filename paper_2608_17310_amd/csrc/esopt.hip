@@ -60,6 +60,7 @@
 #include <algorithm>
 
 #include "../../include/esopt.h"
+#include "es_fp8.hpp"
 #include "es_noise.hpp"
 #include "es_quant.hpp"
 #include "es_table.hpp"
@@ -952,10 +953,53 @@ __device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e
     }
 }
 
+// Code formats of a quantized plan.
+constexpr int kFmtInt8 = 0;
+constexpr int kFmtE4M3 = 1;
+
+// fp8 perturb / restore of one 16-code group: per quad of codes one noise
+// call, whose words give the four normals and the four spare draws.  The
+// scale's reciprocal is folded into the pair's radius factor; x = v -+ d is
+// one fused multiply-add, and the restore rounds with the complementary
+// rule, so it undoes the perturbation inside a binade.
+template <bool kNegate>
+__device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t e,
+                                                uint32_t tensor_id, const Member& m, float inv0,
+                                                float inv1, uint32_t out[4]) {
+    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
+    const uint32_t one_plus = esq::one_plus_half_step_vgpr();
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+        const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, m.k0, m.k1);
+        const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
+        float v[4], res[4];
+        esf::decode4(raw[c], v);
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+            float t, cs, sn;
+            es::scaled_pair(ws[2 * p], ws[2 * p + 1], wk_inv[c >> 1], t, cs, sn);
+            const float trig[2] = {cs, sn};
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int i = 2 * p + h;
+                const float one_plus_u = esq::spare_one_plus(ws[i], one_plus);   // 1 + u, exact
+                if constexpr (kNegate)
+                    res[i] = esf::round_grid<true>(__builtin_fmaf(-t, trig[h], v[i]),
+                                                   one_plus_u - 1.0f);
+                else
+                    res[i] = esf::round_grid<false>(__builtin_fmaf(t, trig[h], v[i]),
+                                                    2.0f - one_plus_u);
+            }
+        }
+        out[c] = esf::encode4(res);
+    }
+}
+
 // One tile of an int8 pass: for each of the lane's 16-code groups in turn,
 // the step d in quanta (binary32) and the stochastically rounded, clamped
 // code.
-template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate>
+template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate, int kFmt>
 __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
                                       uint32_t n_members, const QPass& ps) {
     const uint32_t e0 = r.elem0 + threadIdx.x * esq::kQGroup;
@@ -968,7 +1012,10 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
         float inv0, inv1;
         esq::group_inv_scales(r, e, inv0, inv1);
         uint32_t out[4];
-        if constexpr (!kTable) {
+        if constexpr (!kTable && kFmt == kFmtE4M3) {
+            f8perturb_group<kNegate>(raw, e, r.tensor_id, ps.m, inv0, inv1, out);
+            esf::keep_special(raw, inv0, inv1, out);
+        } else if constexpr (!kTable) {
             qperturb_group<kNegate>(raw, e, r.tensor_id, ps.m, inv0, inv1, out);
         } else {
             float acc[16];
@@ -984,19 +1031,40 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
             const es::Words db = es::philox4x32_10((e >> 3) + 1u, 0u, r.tensor_id,
                                                    es::kDomainRounding, ps.dk0, ps.dk1);
             const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
+            if constexpr (kFmt == kFmtE4M3) {
+                // x = v + acc / s (one fused multiply-add), rounded onto the
+                // grid with the threshold 1 - r 2^-16
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                uint32_t w = 0;
+                for (int k = 0; k < 4; ++k) {
+                    float v[4], res[4];
+                    esf::decode4(raw[k], v);
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int c = 4 * k + i;
-                    const float inv = c < 8 ? inv0 : inv1;
-                    const int32_t q = static_cast<int8_t>(raw[k] >> (8 * i));
-                    const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
-                    const int32_t v = inv != 0.0f ? esq::qstep<false>(q, acc[c] * inv, draw) : q;
-                    w |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+                    for (int i = 0; i < 4; ++i) {
+                        const int c = 4 * k + i;
+                        const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
+                        res[i] = esf::round_grid<false>(
+                            __builtin_fmaf(acc[c], c < 8 ? inv0 : inv1, v[i]),
+                            2.0f - esf::one_plus_draw16(draw));
+                    }
+                    out[k] = esf::encode4(res);
                 }
-                out[k] = w;
+                esf::keep_special(raw, inv0, inv1, out);
+            } else {
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint32_t w = 0;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int c = 4 * k + i;
+                        const float inv = c < 8 ? inv0 : inv1;
+                        const int32_t q = static_cast<int8_t>(raw[k] >> (8 * i));
+                        const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
+                        const int32_t v =
+                            inv != 0.0f ? esq::qstep<false>(q, acc[c] * inv, draw) : q;
+                        w |= (static_cast<uint32_t>(v) & 0xFFu) << (8 * i);
+                    }
+                    out[k] = w;
+                }
             }
         }
         esq::qstore<kFast>(r.data, e, r.numel, out, r.aligned16 != 0u);
@@ -1007,7 +1075,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
 // (one inline member, draws from its own noise words) or the update (member
 // table and header written by es_prepare_kernel, draws of domain 1 under the
 // rounding seed).
-template <int kThreads, int kU, bool kTable, bool kNegate>
+template <int kThreads, int kU, bool kTable, bool kNegate, int kFmt>
 __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTensor* __restrict__ tab,
                                                             uint64_t n_full, uint64_t n_tail,
                                                             const Member* __restrict__ members,
@@ -1021,12 +1089,12 @@ __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTenso
     }
     uint32_t t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        qtile<kThreads, kU, true, kTable, kNegate>(esq::qlocate_full<kTileElems>(tab, t, tile),
-                                                   members, n_members, ps);
+        qtile<kThreads, kU, true, kTable, kNegate, kFmt>(
+            esq::qlocate_full<kTileElems>(tab, t, tile), members, n_members, ps);
     t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        qtile<kThreads, kU, false, kTable, kNegate>(esq::qlocate_tail<kTileElems>(tab, t, tile),
-                                                    members, n_members, ps);
+        qtile<kThreads, kU, false, kTable, kNegate, kFmt>(
+            esq::qlocate_tail<kTileElems>(tab, t, tile), members, n_members, ps);
 }
 
 using QPassKernel = void (*)(const esq::DevQTensor*, uint64_t, uint64_t, const Member*,
@@ -1034,18 +1102,24 @@ using QPassKernel = void (*)(const esq::DevQTensor*, uint64_t, uint64_t, const M
 
 enum class QKind { kPerturb, kRestore, kUpdate };
 
-QPassKernel qpass_kernel(int threads, int groups, QKind kind) {
-#define ES_CASE(T, U)                                                            \
-    if (threads == T && groups == U) {                                           \
-        switch (kind) {                                                          \
-            case QKind::kPerturb: return es_qpass_kernel<T, U, false, false>;    \
-            case QKind::kRestore: return es_qpass_kernel<T, U, false, true>;     \
-            case QKind::kUpdate: return es_qpass_kernel<T, U, true, false>;      \
-        }                                                                        \
+template <int kFmt>
+QPassKernel qpass_kernel_for(int threads, int groups, QKind kind) {
+#define ES_CASE(T, U)                                                                  \
+    if (threads == T && groups == U) {                                                 \
+        switch (kind) {                                                                \
+            case QKind::kPerturb: return es_qpass_kernel<T, U, false, false, kFmt>;    \
+            case QKind::kRestore: return es_qpass_kernel<T, U, false, true, kFmt>;     \
+            case QKind::kUpdate: return es_qpass_kernel<T, U, true, false, kFmt>;      \
+        }                                                                              \
     }
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
+}
+
+QPassKernel qpass_kernel(int threads, int groups, QKind kind, int format) {
+    return format == kFmtE4M3 ? qpass_kernel_for<kFmtE4M3>(threads, groups, kind)
+                              : qpass_kernel_for<kFmtInt8>(threads, groups, kind);
 }
 
 // int8 plan: the same sum with b the code's 8 bits (int8 tensors are never
@@ -1123,6 +1197,7 @@ struct es_qplan {
     uint32_t grid = 0;              // workgroups of every int8 pass
     int threads = kDefaultThreads;
     int groups = kDefaultQGroups;   // 16-code groups per lane per tile
+    int format = kFmtInt8;          // ES_QFORMAT_INT8 or ES_QFORMAT_E4M3 (one per plan)
     esq::DevQTensor* d_tab = nullptr;
     uint8_t* d_scratch = nullptr;   // kScratchBytes, as the bf16 plan's
 };
@@ -1196,7 +1271,7 @@ int check_qdevice(const es_qplan_t* p) {
 
 int launch_qpass(es_qplan_t* p, QKind kind, const QPass& ps, hipStream_t s) {
     if (p->n_full + p->n_tail == 0) return ES_OK;
-    const QPassKernel kernel = qpass_kernel(p->threads, p->groups, kind);
+    const QPassKernel kernel = qpass_kernel(p->threads, p->groups, kind, p->format);
     hipLaunchKernelGGL(kernel, dim3(p->grid), dim3(p->threads), 0, s, p->d_tab, p->n_full,
                        p->n_tail, reinterpret_cast<const Member*>(p->d_scratch + kOffMembers),
                        reinterpret_cast<const UpdateHeader*>(p->d_scratch + kOffHeader), ps);
@@ -1750,15 +1825,23 @@ int es_swap(es_plan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_
     return launch_streams(plan, streams, sd, cf, static_cast<hipStream_t>(stream));
 }
 
-int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out) try {
+int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t** out) {
+    return es_qplan_create_format(tensors, n_tensors, ES_QFORMAT_INT8, out);
+}
+
+int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint32_t format,
+                           es_qplan_t** out) try {
     if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null output pointer");
     *out = nullptr;
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null tensor list");
     if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
         return fail(ES_ERR_INVALID_ARG, "es_qplan_create: n_tensors out of range");
+    if (format != ES_QFORMAT_INT8 && format != ES_QFORMAT_E4M3)
+        return fail(ES_ERR_INVALID_ARG, "es_qplan_create: format not ES_QFORMAT_INT8 or "
+                                        "ES_QFORMAT_E4M3");
     int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
     int groups = env_int("ESOPT_QGROUPS", kDefaultQGroups, 2, 8);
-    if (qpass_kernel(threads, groups, QKind::kUpdate) == nullptr) {
+    if (qpass_kernel(threads, groups, QKind::kUpdate, static_cast<int>(format)) == nullptr) {
         threads = kDefaultThreads;
         groups = kDefaultQGroups;
     }
@@ -1823,6 +1906,7 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
     const int wg = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
     p->threads = threads;
     p->groups = groups;
+    p->format = static_cast<int>(format);
     p->n_tensors = n_tensors;
     p->numel = numel;
     p->n_full = n_full;

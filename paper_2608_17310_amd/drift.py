@@ -16,6 +16,13 @@ also prints the RMS of one update step, alpha / sqrt(G) for z-scored rewards.
 
     python -m paper_2608_17310_amd.drift --workload dense-4b --generations 70 --members 8
 
+With --format int8 or --format e4m3 the same walk runs on the quantized
+codes of the set (per-row scales; es_qperturb / es_qrestore), and the drift
+is measured on the dequantized values s * v(c), in units of sigma and of the
+format's own grid spacing at the larger of the start and end values (one
+quantum for int8; 2^(e-3) scale units on the binade [2^e, 2^(e+1)) of E4M3,
+2^-9 below 2^-6).
+
 Every pass runs in the library's kernels; the statistics are PyTorch
 reductions on the device.  One JSON line per (walk, checkpoint).
 """
@@ -72,6 +79,77 @@ def drift_stats(views, start, sigma):
     }
 
 
+def _code_values(codes, fmt):
+    """Code values v(c) (float32 tensor) of int8 or E4M3 codes."""
+    if fmt == "int8":
+        return codes.reshape(-1).float()
+    return codes.reshape(-1).view(torch.float8_e4m3fn).float()
+
+
+def _grid_spacing(m, fmt):
+    """Grid spacing of the format at magnitude m >= 0 (code units)."""
+    if fmt == "int8":
+        return torch.ones_like(m)
+    _, e = torch.frexp(m)
+    ke = torch.clamp(e.to(torch.int32) - 4, min=-9)
+    ke = torch.where(m == 0, torch.full_like(ke, -9), ke)
+    return torch.ldexp(torch.ones_like(m), ke.to(torch.float32))
+
+
+def qdrift_stats(views, start, scales, rows, sigma, fmt):
+    """drift_stats for quantized codes, on the dequantized values."""
+    n = changed = over_one = 0
+    sq = ulps_sum = ulps_max = mag = 0.0
+    for v, s0, sc, row in zip(views, start, scales, rows):
+        a = _code_values(v, fmt)
+        b = _code_values(s0, fmt)
+        scale = sc.float().repeat_interleave(row)[:a.numel()] if row else sc.float().expand(
+            a.numel())
+        d = (a - b) * scale
+        n += a.numel()
+        changed += int((v.reshape(-1).view(torch.uint8) != s0.reshape(-1).view(torch.uint8)).sum())
+        sq += float((d.double() ** 2).sum())
+        u = (a - b).abs() / _grid_spacing(torch.maximum(a.abs(), b.abs()), fmt)
+        ulps_sum += float(u.double().sum())
+        ulps_max = max(ulps_max, float(u.max()))
+        over_one += int((u > 1.0).sum())
+        mag += float(((a.abs() - b.abs()) * scale).double().sum())
+    return {
+        "changed": changed / n,
+        "rms_over_sigma": math.sqrt(sq / n) / sigma,
+        "mean_spacings": ulps_sum / n,
+        "max_spacings": ulps_max,
+        "beyond_one_spacing": over_one / n,
+        "mean_magnitude_change_over_sigma": mag / n / sigma,
+    }
+
+
+def quantized_main(args, W):
+    fmt = args.format
+    make = wl.device_f8params if fmt == "e4m3" else wl.device_qparams
+    flat, views, scales, rows = make(W)
+    start_flat = flat.clone()
+    offs, _ = wl.flat_layout(W.numels, align=256)
+    start = [start_flat[o:o + n] for o, n in zip(offs, W.numels)]
+    print(json.dumps({"workload": W.name, "format": fmt, "params": W.n_params,
+                      "members": args.members, "sigma": args.sigma,
+                      "update_step_rms": args.alpha / math.sqrt(args.members)}), flush=True)
+    plan = esopt.QPlan(views, scales, rows, format=fmt)
+    for g in range(1, args.generations + 1):
+        for i in range(args.members):
+            seed = 1_000_003 * g + i
+            plan.perturb(seed, 1, args.sigma)
+            plan.restore(seed, 1, args.sigma)
+        if g in CHECKPOINTS or g == args.generations:
+            torch.cuda.synchronize()
+            row = {"walk": "restore", "format": fmt, "generation": g,
+                   "roundings": g * 2 * args.members}
+            row.update(qdrift_stats(views, start, scales, rows, args.sigma, fmt))
+            print(json.dumps(row), flush=True)
+    plan.close()
+    return 0
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--workload", default="dense-4b", choices=sorted(wl.WORKLOADS))
@@ -80,9 +158,12 @@ def main(argv=None):
     ap.add_argument("--sigma", type=float, default=1e-3)
     ap.add_argument("--alpha", type=float, default=5e-4)
     ap.add_argument("--walks", default="restore,swap")
+    ap.add_argument("--format", default="bf16", choices=("bf16", "int8", "e4m3"))
     args = ap.parse_args(argv)
     W = wl.WORKLOADS[args.workload]
     torch.cuda.set_device(0)
+    if args.format != "bf16":
+        return quantized_main(args, W)
     flat, views = wl.device_params(W)
     start_flat = flat.clone()
     offs, _ = wl.flat_layout(W.numels)

@@ -74,6 +74,8 @@ SIGNATURES = {
     "es_update_noalloc": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp,
                                          _u32, ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
     "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
+    "es_qplan_create_format": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, _u32,
+                                              ctypes.POINTER(_vp)]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
     "es_qplan_device_bytes": (_u64, [_vp]),
@@ -312,13 +314,24 @@ def _call_update(fn, what, handle, seeds, signs, rewards, alpha, sigma, zscore_e
               _dev_ptr(status_out, torch.int32, "status_out"), _stream(stream)), what)
 
 
-class QPlan:
-    """A list of int8 parameter tensors with binary32 scales (theta = s q,
-    one scale per `row` consecutive codes, row a multiple of 8, 0 for one
-    scale per tensor), prepared for single-launch passes.  The plan keeps
-    references to the codes and scales."""
+QFORMAT_INT8, QFORMAT_E4M3 = 0, 1
+_QFORMATS = {"int8": QFORMAT_INT8, "e4m3": QFORMAT_E4M3}
 
-    def __init__(self, codes, scales, rows, tensor_ids=None):
+
+class QPlan:
+    """A list of quantized parameter tensors with binary32 scales (theta =
+    s v(c), one scale per `row` consecutive codes, row a multiple of 8, 0 for
+    one scale per tensor), prepared for single-launch passes.  format "int8":
+    int8 codes, v(c) = c; format "e4m3": fp8 E4M3 codes (torch.float8_e4m3fn,
+    or their bytes as torch.uint8).  The plan keeps references to the codes
+    and scales."""
+
+    def __init__(self, codes, scales, rows, tensor_ids=None, format="int8"):
+        if format not in _QFORMATS:
+            raise ValueError(f"format must be one of {sorted(_QFORMATS)}")
+        self.format = format
+        code_dtypes = ((torch.int8,) if format == "int8"
+                       else (torch.float8_e4m3fn, torch.uint8))
         codes, scales, rows = list(codes), list(scales), [int(r) for r in rows]
         if not codes or len(scales) != len(codes) or len(rows) != len(codes):
             raise ValueError("codes, scales and rows must be non-empty and of equal length")
@@ -328,8 +341,9 @@ class QPlan:
             raise ValueError("tensor_ids must match tensors")
         arr = (EsQTensor * len(codes))()
         for i, (q, sc, row, tid) in enumerate(zip(codes, scales, rows, ids)):
-            if q.dtype != torch.int8 or not q.is_cuda or not q.is_contiguous():
-                raise ValueError(f"codes {i} must be a contiguous int8 CUDA tensor")
+            if q.dtype not in code_dtypes or not q.is_cuda or not q.is_contiguous():
+                raise ValueError(f"codes {i} must be a contiguous CUDA tensor of "
+                                 f"{' or '.join(str(d) for d in code_dtypes)}")
             if sc.dtype != torch.float32 or not sc.is_cuda or not sc.is_contiguous():
                 raise ValueError(f"scales {i} must be a contiguous float32 CUDA tensor")
             need = 1 if row == 0 else -(-q.numel() // row)
@@ -342,8 +356,8 @@ class QPlan:
         self.device = codes[0].device
         handle = ctypes.c_void_p()
         with torch.cuda.device(self.device):
-            _check(load().es_qplan_create(arr, len(codes), ctypes.byref(handle)),
-                   "es_qplan_create")
+            _check(load().es_qplan_create_format(arr, len(codes), _QFORMATS[format],
+                                                 ctypes.byref(handle)), "es_qplan_create")
         self._h = handle
 
     @property
@@ -375,8 +389,8 @@ class QPlan:
 
     def update(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                z_out=None, status_out=None, stream=None, round_seed=0):
-        """Update in quanta, always stochastically rounded with the draws of
-        round_seed; rewards is a float32 CUDA tensor of len(seeds)."""
+        """Update in scale units, always stochastically rounded with the draws
+        of round_seed; rewards is a float32 CUDA tensor of len(seeds)."""
         _call_update(load().es_qupdate, "es_qupdate", self.handle, seeds, signs, rewards, alpha,
                      sigma, zscore_eps, flags, z_out, status_out, stream, round_seed)
 

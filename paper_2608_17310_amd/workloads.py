@@ -269,3 +269,60 @@ def device_qparams(wl, device="cuda", seed=1234):
         scales.append(s)
         rows.append(row)
     return flat, views, scales, rows
+
+
+# ------------------------------------------------------------------ fp8 sets --
+# The fp8 path's inputs: the same synthetic weights, N(0, 0.02), quantized to
+# E4M3 codes (PyTorch's float8_e4m3fn, round to nearest) with one binary32
+# scale per row of the last dimension chosen so the row's largest magnitude
+# maps to 448, the format's largest value (absmax / 448), and one scale per
+# tensor for vectors -- a per-channel fp8 checkpoint.  This prepares inputs
+# only.
+
+E4M3_MAX = 448.0
+
+
+def quantize_rows_e4m3(w, row):
+    """(codes as uint8 bytes of float8_e4m3fn, scales float32) of a float32
+    array quantized per `row` consecutive values (row == 0: one scale),
+    scale absmax / 448; an all-zero row gets scale 1."""
+    import torch
+    t = torch.as_tensor(w, dtype=torch.float32).reshape(-1)
+    g = t.reshape(1, -1) if row == 0 else t.reshape(-1, row)
+    amax = g.abs().amax(dim=1)
+    s = torch.where(amax > 0, amax / E4M3_MAX, torch.ones_like(amax))
+    c = (g / s[:, None]).clamp(-E4M3_MAX, E4M3_MAX).to(torch.float8_e4m3fn)
+    return c.view(torch.uint8).reshape(-1), s.contiguous()
+
+
+def host_f8params(wl, stream=0):
+    """Host E4M3 code bytes, scales and rows of a workload (numpy)."""
+    out = []
+    for i, s in enumerate(wl.shapes):
+        c, sc = quantize_rows_e4m3(host_tensor_values(s, i, stream), row_of(s))
+        out.append((c.numpy(), sc.numpy(), row_of(s)))
+    return out
+
+
+def device_f8params(wl, device="cuda", seed=1234):
+    """The workload's weights drawn on the device (as device_params) and
+    quantized per row into one flat buffer of E4M3 code bytes (tensors
+    256-byte aligned).  Returns (flat_codes, [code views], [scales], [rows])."""
+    import torch
+    offs, total = flat_layout(wl.numels, align=256)
+    flat = torch.empty(total, dtype=torch.uint8, device=device)
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    views, scales, rows = [], [], []
+    for off, n, shape in zip(offs, wl.numels, wl.shapes):
+        w = torch.empty(n, dtype=torch.float32, device=device)
+        w.normal_(0.0, WEIGHT_STD, generator=gen)
+        row = row_of(shape)
+        c, s = quantize_rows_e4m3(w, row)
+        del w
+        v = flat[off:off + n]
+        v.copy_(c)
+        views.append(v)
+        scales.append(s)
+        rows.append(row)
+    return flat, views, scales, rows

@@ -124,3 +124,48 @@ def qreport(got, q_in, v, tol, ok, negate=False):
 def assert_qparity(rep, what=""):
     assert rep["bad"] == 0, (what, rep)
     assert rep["exact"] >= 0.9999, (what, rep)
+
+
+# ------------------------------------------------------------------- fp8 path --
+# An fp8 pass decides between the two grid neighbours lo and lo + h of
+# x = v + step (binary32) by comparing f = (x - lo) / h with a threshold.
+# The GPU's x differs from the oracle's by the noise error and binary32
+# roundings, so where the oracle's f lies within that bound (over h) of the
+# threshold both neighbours are correct; everywhere else the code is unique.
+# (Where x is near a grid point instead, both sides reach that grid point.)
+
+
+def f8_tolerance(abs_weight_sum, noise_abs_sum, x):
+    """Bound on |x_gpu - x_oracle| in scale units: abs_weight_sum =
+    sum_d |w_d| / s, noise_abs_sum = sum_d |w_d eps_d| / s (fp64 arrays)."""
+    return (abs_weight_sum * 4e-6 + noise_abs_sum * (2e-6 + 8 * F32_EPS)
+            + 4 * F32_EPS * (np.abs(x) + 2.0 ** -9))
+
+
+def f8report(got, exp, x32, thr, tol, ok):
+    """GPU codes against the oracle's codes `exp`: equal, or -- where the
+    oracle's decision value is within tol of its threshold -- the other grid
+    neighbour.  x32: the oracle's binary32 x (fp64 array), thr: the threshold
+    of each element, ok: elements a pass may change."""
+    from oracle import fp8 as of
+    got = np.asarray(got, dtype=np.uint8).ravel()
+    exp = np.asarray(exp, dtype=np.uint8).ravel()
+    x32 = np.asarray(x32, dtype=np.float64)
+    inside = ok & (np.abs(x32) < of.E4M3_MAX)
+    xc = np.where(inside, x32, 0.0)
+    lo, h = of.grid_floor(xc)
+    f = (xc - lo) / h
+    near = inside & (np.abs(f - thr) <= tol / h)
+    v_exp = of.e4m3_decode(exp)
+    alt_v = np.where(v_exp == lo, lo + h, lo)
+    alt = of.e4m3_encode(np.where(near, alt_v, 0.0))
+    good = (got == exp) | (near & (got == alt))
+    n = got.size
+    return {"n": n, "exact": float(np.mean(got == exp)) if n else 1.0,
+            "near": int(near.sum()), "bad": int((~good).sum()),
+            "first_bad": np.flatnonzero(~good)[:5].tolist()}
+
+
+def assert_f8parity(rep, what=""):
+    assert rep["bad"] == 0, (what, rep)
+    assert rep["exact"] >= 0.9999, (what, rep)
