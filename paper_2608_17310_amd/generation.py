@@ -8,8 +8,8 @@ regenerated from its seed; Section 3.1 sets sigma_t on a cosine schedule.
 
 With fused_swap the revert of member i and the apply of member i+1 are one
 pass (es_swap), so a generation of N members makes N + 1 passes over the
-parameters instead of 2N, plus the update.  The same driver runs the int8
-path (esopt.QPlan), whose revert is exact and which has no fused swap.
+parameters instead of 2N, plus the update.  The same driver runs the
+quantized paths (esopt.QPlan, int8 or E4M3 codes), which have no fused swap.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
@@ -86,7 +86,7 @@ def antithetic_seeds(base_seed, n_pairs):
 
 def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
     """Apply member 0, visit it, move to member 1, ... and revert the last.
-    Plans without a fused swap (the int8 QPlan) revert and apply separately.
+    Plans without a fused swap (the quantized QPlan) revert and apply separately.
     When the passes run on a stream other than PyTorch's current one, each
     visit is ordered after its member's pass and the next pass after the
     visit's work on the current stream, so an evaluation that reads the

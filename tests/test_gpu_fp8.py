@@ -342,3 +342,51 @@ def test_f8_27b_set_sampled():
             bad += rep["bad"]
             assert rep["bad"] == 0, (t, rep)
     assert bad == 0
+
+
+def test_f8_generation_replay_is_bit_exact():
+    """Four generations of the driver on the tiny set as E4M3 codes are
+    rebuilt bit for bit from their records (seeds, signs, rewards, sigma,
+    alpha, rounding seed), and the update-only replay matches the oracle's
+    chain of updates to the fp8 parity bar (each link checked against the
+    oracle applied to the GPU's previous codes)."""
+    from paper_2608_17310_amd.generation import run_generation, replay, antithetic_seeds
+    W = wl.TINY
+    host = wl.host_f8params(W)
+
+    def fresh():
+        codes = [_dev(c) for c, _, _ in host]
+        return codes, esopt.QPlan(codes, [_dev(s) for _, s, _ in host],
+                                  [r for _, _, r in host], format="e4m3")
+    codes, plan = fresh()
+    rng = np.random.default_rng(12)
+    records = []
+    for t in range(4):
+        seeds, signs = antithetic_seeds(50 * t, 3)
+        records.append(run_generation(plan, seeds, signs, 1e-3, 5e-4,
+                                      evaluate=lambda i: rng.random(), round_seed=500 + t))
+    torch.cuda.synchronize()
+    live = [_host(c) for c in codes]
+    assert any(np.mean(a != c) > 0.05 for a, (c, _, _) in zip(live, host))
+    plan.close()
+    codes2, plan2 = fresh()
+    replay(plan2, records)
+    torch.cuda.synchronize()
+    for a, b in zip(live, codes2):
+        np.testing.assert_array_equal(a, _host(b))
+    plan2.close()
+    # update-only replay, one update at a time against the oracle
+    codes3, plan3 = fresh()
+    prev = [c.copy() for c, _, _ in host]
+    for rec in records:
+        replay(plan3, [rec], with_perturbations=False)
+        torch.cuda.synchronize()
+        for tid, ((_, sc, row), dev) in enumerate(zip(host, codes3)):
+            got = _host(dev)
+            el = np.arange(got.size, dtype=np.uint64)
+            rep = _update_report(got, prev[tid], sc, row, tid, rec.seeds, rec.signs,
+                                 np.array(rec.rewards, np.float32), rec.alpha, rec.sigma, 0, el,
+                                 rec.round_seed)
+            assert_f8parity(rep, f"replayed update tensor {tid}")
+            prev[tid] = got
+    plan3.close()
