@@ -362,7 +362,7 @@ def run_sweep(args):
     plan.close()
 
 
-def run_int8(args):
+def run_quantized(args):
     """The int8 (or, with --fp8, the E4M3) step on the workload's shapes:
     N x (es_qperturb + es_qrestore) + es_qupdate over codes with per-row
     scales, inputs resident in HBM."""
@@ -531,7 +531,7 @@ def main():
     if args.profile_pass:
         return run_profile_pass(args)
     if args.int8 or args.fp8:
-        return run_int8(args)
+        return run_quantized(args)
     import torch
     from paper_2608_17310_amd import workloads as wl
 

@@ -400,3 +400,28 @@ def test_identities():
     eps = oracle.normals(9, 0, np.arange(256, dtype=np.uint64))
     assert np.all(np.isfinite(fp8.e4m3_decode(up)))
     assert np.all(up[eps > 0] == 0x7E) and np.all(fp8.e4m3_decode(up[eps < -0.5]) < 448)
+
+
+def test_parity_report_accepts_only_near_threshold_neighbours():
+    """The fp8 parity check (tests/parity.py): a result equal to the oracle's
+    passes; the other grid neighbour passes only where the oracle's decision
+    lies within the tolerance of its threshold; any other code fails."""
+    from parity import f8report
+    x = np.array([1.0 + 0.5 * 0.125, 1.0 + 0.3 * 0.125, 100.0 + 0.9 * 8, -3.0 - 0.2 * 0.25])
+    thr = np.array([0.5 + 1e-9, 0.6, 0.1, 0.7])            # element 0 sits on its threshold
+    ok = np.ones(4, bool)
+    exp = fp8.e4m3_encode(fp8.round_onto_grid(x, "update", 1.0 - thr))
+    tol = np.full(4, 1e-6)
+    assert f8report(exp, exp, x, thr, tol, ok)["bad"] == 0
+    lo, h = fp8.grid_floor(x)
+    v = fp8.e4m3_decode(exp)
+    other = fp8.e4m3_encode(np.where(v == lo, lo + h, lo))
+    got = exp.copy()
+    got[0] = other[0]                                        # near its threshold: accepted
+    rep = f8report(got, exp, x, thr, tol, ok)
+    assert rep["bad"] == 0 and rep["near"] == 1
+    got[1] = other[1]                                        # far from it: rejected
+    assert f8report(got, exp, x, thr, tol, ok)["bad"] == 1
+    got = exp.copy()
+    got[2] = fp8.e4m3_encode(np.array([lo[2] - 8.0]))[0]     # two steps away: rejected
+    assert f8report(got, exp, x, thr, tol, ok)["bad"] == 1
