@@ -765,9 +765,10 @@ def calibration_copy(torch):
 
 
 def run_profile_pass(args):
-    """Every kernel of the step once on the workload (bf16 passes, the int8
-    passes on the same shapes), the in-place stream over the plan, the six
-    flat-buffer calibration passes and the calibration copy."""
+    """Every kernel of the step once on the workload (bf16 passes, the same
+    passes over the matrices as column blocks, the int8 and fp8 passes on the
+    same shapes), the in-place stream over the plan, the six flat-buffer
+    calibration passes and the calibration copy."""
     import torch
     from paper_2608_17310_amd import esopt, workloads as wl
     torch.cuda.set_device(0)
@@ -808,7 +809,33 @@ def run_profile_pass(args):
     log.add("es_plan_checksum", "checksum", P, 2 * P, 0, plan.checksum, out, repeat=R)
     torch.cuda.synchronize()
     plan.close()
-    del flat, views
+    # the same matrices as column blocks (es_plan_create_blocks): each 2-D
+    # tensor's memory read as 8 consecutive [rows, cols / 8] blocks, block k
+    # holding columns k cols / 8 .. of the tensor, so every pass takes the
+    # strided launch with its row maps over the same bytes
+    blocks = []
+    for i, v in enumerate(views):
+        if v.dim() != 2:
+            continue
+        r_, c_ = v.shape
+        w = c_ // 8
+        flat_v = v.reshape(-1)
+        blocks += [esopt.Block(flat_v[k * r_ * w:(k + 1) * r_ * w].view(r_, w), 8 * i + k, c_, 0,
+                               k * w) for k in range(8)]
+    bplan = esopt.Plan(blocks=blocks)
+    PB = bplan.numel
+    for _ in range(R):
+        log.add("es_perturb (column blocks)", "blocks", PB, 4 * PB, PB, bplan.perturb, seeds[0],
+                signs[0], s0)
+        log.add("es_restore (column blocks)", "blocks", PB, 4 * PB, PB, bplan.restore, seeds[0],
+                signs[0], s0)
+    log.add(f"es_update (N={N}, nearest-even, column blocks)", "blocks", PB, 4 * PB, nd * PB,
+            bplan.update, seeds, signs, rewards, W.alpha, sigma=s0, repeat=R)
+    log.add("es_stream_pass (column blocks)", "blocks", PB, 4 * PB, 0, bplan.stream_pass,
+            repeat=R)
+    torch.cuda.synchronize()
+    bplan.close()
+    del flat, views, blocks
     torch.cuda.empty_cache()
 
     qflat, qviews, scales, rows = wl.device_qparams(W)
@@ -924,6 +951,9 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
         "ceiling": ("hbm_ceilings", f"HBM ceilings: the in-place stream over the {wname} plan and "
                                     f"the flat-buffer calibration passes"),
         "checksum": ("es_plan_checksum", f"es_plan_checksum on {wname}"),
+        "blocks": ("es_blocks", f"Column blocks of {wname}'s matrices (es_plan_create_blocks: "
+                                f"each matrix as 8 blocks of rows x cols/8, the strided launch "
+                                f"with row maps)"),
     }
     counters_path = os.path.join(profiles_dir, "counters.json")
     counters = json.load(open(counters_path)) if os.path.exists(counters_path) else {}

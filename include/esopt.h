@@ -112,6 +112,44 @@ typedef struct es_plan es_plan_t;
  * es_plan_device_bytes reports the total. */
 int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** out);
 
+/* A rectangular block of a row-major bf16 tensor, as one GPU holds it under
+ * tensor parallelism when the split runs across columns (a row-parallel
+ * layer's weight: a range of every row): `rows` x `cols` values stored
+ * contiguously at `data` (block row i at data + i * cols elements), which are
+ * the whole tensor's elements (row0 + i) * row_len + col0 + j, i < rows,
+ * j < cols.  Each carries the noise of that whole-tensor index (Section 3:
+ * the noise is regenerated from the seed and the element's place), so every
+ * pass over the block leaves exactly the values the same pass over the whole
+ * tensor leaves there, and block checksums add up to the whole tensor's.
+ * Requirements: col0 + cols <= row_len; the first index row0 * row_len + col0
+ * is a multiple of 8; a block that is not one contiguous range of the tensor
+ * (rows > 1 and cols < row_len) also has cols and row_len multiples of 8
+ * (every hidden and intermediate size of the paper's models is); every index
+ * is below 2^60.  A whole tensor is {data, 1, numel, numel, 0, 0}; an
+ * es_tensor_t shard is {data, 1, numel, its tensor's numel, 0, 8 * offset8}.
+ * rows * cols may be 0 (the block is skipped). */
+typedef struct es_block {
+    void*    data;
+    uint64_t rows;
+    uint64_t cols;
+    uint64_t row_len;       /* the whole tensor's row length */
+    uint64_t row0;          /* the block's first row in the whole tensor */
+    uint64_t col0;          /* the block's first column in the whole tensor */
+    uint32_t tensor_id;     /* as in es_tensor_t: unique within a plan */
+    uint32_t reserved;      /* must be 0 */
+} es_block_t;
+
+/* es_plan_create over blocks (Section 3, the same passes: es_perturb,
+ * es_restore, es_swap, es_update, es_update_noalloc, es_plan_checksum and
+ * es_stream_pass accept the plan).  Blocks that are one contiguous range of
+ * their tensor are laid out exactly as es_plan_create lays out tensors and
+ * shards; the others are cut into pieces of whole rows (under 2^31 elements
+ * each) whose tiles carry the piece's row map, and the passes run over them
+ * in a second launch.  Errors: as es_plan_create (n_blocks for n_tensors),
+ * plus INVALID_ARG for a block that breaks a requirement above or has
+ * reserved != 0, and for rows * cols above 2^60. */
+int es_plan_create_blocks(const es_block_t* blocks, uint32_t n_blocks, es_plan_t** out);
+
 /* Free a plan (NULL is a no-op).  Synchronises the plan's device first (made
  * current for the call; the caller's current device is restored) so that no
  * queued launch still reads the plan's tables.  The plan is freed even when a

@@ -98,6 +98,34 @@ struct DevTile {
 };
 static_assert(sizeof(DevTile) == 32, "tile descriptor layout");
 
+// Row map of a tile of a strided block (es_block_t with rows > 1 and
+// cols < row_len): the block is cut into pieces of whole rows, each tiled by
+// address as a tensor of its own, so a tile's element index e is local to
+// its piece (e < 2^31), and local element e is whole-tensor element
+//   n0 + e + (e / cols) (row_len - cols),
+// n0 being the piece's first whole-tensor index.  cols is a multiple of 8, so
+// a group of 8 never spans two rows and its elements keep consecutive
+// indices (one quad pair).  The row division is a multiply-high and a shift
+// and skip = row_len - cols is below 2^32, so the map costs one 32 x 32-bit
+// multiply-add and a 64-bit add per group.  One entry per tile, beside its
+// descriptor.
+struct DevRows {
+    uint64_t n0;
+    uint32_t skip;                          // row_len - cols
+    uint32_t magic, shift;                  // e / cols = mulhi(e, magic) >> shift
+    uint32_t pad[3];
+};
+static_assert(sizeof(DevRows) == 32, "row map layout");
+
+// Whole-tensor index of local element e (< 2^31) under a row map; the host
+// tests call this same function.
+__host__ __device__ __forceinline__ uint64_t rows_index(uint64_t n0, uint32_t skip, uint32_t magic,
+                                                        uint32_t shift, uint64_t e) {
+    const uint32_t el = static_cast<uint32_t>(e);
+    const uint32_t row = static_cast<uint32_t>((uint64_t(el) * magic) >> 32) >> shift;
+    return n0 + (uint64_t(row) * skip + el);
+}
+
 struct MemberIn {                           // one population member, CSR order
     uint32_t reward_index;
     int32_t sign;
@@ -289,18 +317,43 @@ __device__ __forceinline__ void perturb_group(const uint32_t raw[4], uint64_t e,
 }
 
 // A tile: up to kThreads * kU * 8 consecutive elements of one tensor, from
-// element elem0 on; accesses of a tail tile stay below `limit`.  Every field
-// is wave-uniform (scalar registers).
+// element elem0 on; accesses of a tail tile stay below `limit`.  A tile of a
+// strided block also carries its piece's row map (DevRows): its elements are
+// then addressed by elem0 + ... and draw the noise of their whole-tensor
+// index.  Every field is wave-uniform (scalar registers).
 struct TileRef {
     uint16_t* data;
     uint64_t limit;
     uint64_t elem0;
     uint32_t tensor_id;
     uint32_t aligned16;
+    uint64_t n0 = 0;                        // row map (strided blocks only)
+    uint32_t skip = 0, magic = 0, shift = 0;
 };
 
 __device__ __forceinline__ TileRef tile_ref(const DevTile& d) {
     return TileRef{d.data, d.limit, d.elem0, d.tensor_id, d.aligned16};
+}
+
+__device__ __forceinline__ TileRef tile_ref(const DevTile& d, const DevRows& m) {
+    return TileRef{d.data, d.limit, d.elem0, d.tensor_id, d.aligned16, m.n0, m.skip, m.magic,
+                   m.shift};
+}
+
+// Tile i of a launch: its descriptor, and with kRows its row map.
+template <bool kRows>
+__device__ __forceinline__ TileRef load_ref(const DevTile* __restrict__ tiles,
+                                            const DevRows* __restrict__ rows, uint64_t i) {
+    if constexpr (kRows) return tile_ref(tiles[i], rows[i]);
+    else return tile_ref(tiles[i]);
+}
+
+// Noise index of the group starting at element e of a tile: e itself, or
+// the whole-tensor index through the tile's row map.
+template <bool kRows>
+__device__ __forceinline__ uint64_t noise_index(const TileRef& r, uint64_t e) {
+    if constexpr (kRows) return rows_index(r.n0, r.skip, r.magic, r.shift, e);
+    else return e;
 }
 
 // Keep a prefetched descriptor in scalar registers: without this the
@@ -309,6 +362,9 @@ __device__ __forceinline__ TileRef tile_ref(const DevTile& d) {
 // wait it implies costs nothing.
 __device__ __forceinline__ void keep_in_sgprs(DevTile& d) {
     asm volatile("" : "+s"(d.data), "+s"(d.elem0), "+s"(d.tensor_id));
+}
+__device__ __forceinline__ void keep_in_sgprs(DevRows& m) {
+    asm volatile("" : "+s"(m.n0), "+s"(m.skip), "+s"(m.magic), "+s"(m.shift));
 }
 
 template <int kThreads, int kU>
@@ -325,15 +381,17 @@ __device__ __forceinline__ void load_tile(const TileRef& r, uint32_t raw[kU][4])
 // an in-place stream whose writes come in per-tile bursts sustains ~6.2 TB/s,
 // against ~5.5 TB/s when each group's store is interleaved with the next
 // group's arithmetic.
-template <int kThreads, int kU, int kM>
+template <int kThreads, int kU, int kM, bool kRows>
 __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU][4],
                                                const Streams& st) {
-    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t tile_hi = static_cast<uint32_t>(r.elem0 >> 34);
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+        const uint64_t n = noise_index<kRows>(r, e);
         uint32_t out[4];
-        perturb_group<kM>(raw[u], e, q_hi, r.tensor_id, st, out);
+        perturb_group<kM>(raw[u], n, kRows ? static_cast<uint32_t>(n >> 34) : tile_hi,
+                          r.tensor_id, st, out);
 #pragma unroll
         for (int k = 0; k < 4; ++k) raw[u][k] = out[k];
     }
@@ -347,16 +405,18 @@ __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU
 
 // Perturb a tail tile group by group, with bounds-checked accesses (16-byte
 // for whole groups of an aligned tensor, 2-byte otherwise).
-template <int kThreads, int kU, int kM>
+template <int kThreads, int kU, int kM, bool kRows>
 __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st) {
-    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t tile_hi = static_cast<uint32_t>(r.elem0 >> 34);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
         if (e >= r.limit) break;
+        const uint64_t n = noise_index<kRows>(r, e);
         uint32_t raw[4], out[4];
         load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
-        perturb_group<kM>(raw, e, q_hi, r.tensor_id, st, out);
+        perturb_group<kM>(raw, n, kRows ? static_cast<uint32_t>(n >> 34) : tile_hi, r.tensor_id,
+                          st, out);
         store_group<false, true>(r.data, e, r.limit, out, r.aligned16 != 0u);
     }
 }
@@ -373,8 +433,9 @@ __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st
 // descriptor index is clamped rather than tested: the compiler's wait before
 // the current tile's arithmetic is path-insensitive, and a path without loads
 // after the current tile's made it wait for the next tile's loads as well.
-template <int kThreads, int kU, int kM>
-__device__ __forceinline__ bool perturb_step(const DevTile* __restrict__ tiles, uint64_t& tile,
+template <int kThreads, int kU, int kM, bool kRows>
+__device__ __forceinline__ bool perturb_step(const DevTile* __restrict__ tiles,
+                                             const DevRows* __restrict__ rows, uint64_t& tile,
                                              uint64_t n_full, TileRef& cur, TileRef& nxt,
                                              uint32_t cur_buf[kU][4], uint32_t next_buf[kU][4],
                                              const Streams& st) {
@@ -383,14 +444,19 @@ __device__ __forceinline__ bool perturb_step(const DevTile* __restrict__ tiles, 
     __builtin_amdgcn_sched_barrier(0);
     load_tile<kThreads, kU>(more ? nxt : cur, next_buf);
     __builtin_amdgcn_sched_barrier(0);
-    DevTile after = tiles[min(next + gridDim.x, n_full - 1)];
+    const uint64_t after_i = min(next + gridDim.x, n_full - 1);
+    DevTile after = tiles[after_i];
+    DevRows after_rows{};
+    if constexpr (kRows) after_rows = rows[after_i];
     __builtin_amdgcn_sched_barrier(0);
-    perturb_loaded<kThreads, kU, kM>(cur, cur_buf, st);
+    perturb_loaded<kThreads, kU, kM, kRows>(cur, cur_buf, st);
     keep_in_sgprs(after);
+    if constexpr (kRows) keep_in_sgprs(after_rows);
     if (!more) return true;
     tile = next;
     cur = nxt;
-    nxt = tile_ref(after);
+    if constexpr (kRows) nxt = tile_ref(after, after_rows);
+    else nxt = tile_ref(after);
     return false;
 }
 
@@ -400,25 +466,34 @@ __device__ __forceinline__ bool perturb_step(const DevTile* __restrict__ tiles, 
 // step is peeled off so that every step inside the loop starts with the same
 // memory operations outstanding (the previous tile's stores, then the next
 // tile's loads): the wait for the current tile then leaves both in flight.
-template <int kThreads, int kU, int kM>
+//
+// kRows: the launch over the tiles of strided blocks, each with its row map
+// in `rows` (same index as its descriptor); otherwise `rows` is unused.
+template <int kThreads, int kU, int kM, bool kRows>
 __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTile* __restrict__ tiles,
                                                               uint64_t n_full, uint64_t n_tail,
+                                                              const DevRows* __restrict__ rows,
                                                               Streams st) {
     uint64_t tile = blockIdx.x;
     if (tile < n_full) {
-        TileRef cur = tile_ref(tiles[tile]);
-        TileRef nxt = tile_ref(tiles[min(tile + gridDim.x, n_full - 1)]);
+        TileRef cur = load_ref<kRows>(tiles, rows, tile);
+        TileRef nxt = load_ref<kRows>(tiles, rows, min(tile + gridDim.x, n_full - 1));
         uint32_t a[kU][4], b[kU][4];
         load_tile<kThreads, kU>(cur, a);
-        if (!perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, a, b, st)) {
+        if (!perturb_step<kThreads, kU, kM, kRows>(tiles, rows, tile, n_full, cur, nxt, a, b,
+                                                   st)) {
             for (;;) {
-                if (perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, b, a, st)) break;
-                if (perturb_step<kThreads, kU, kM>(tiles, tile, n_full, cur, nxt, a, b, st)) break;
+                if (perturb_step<kThreads, kU, kM, kRows>(tiles, rows, tile, n_full, cur, nxt, b,
+                                                          a, st))
+                    break;
+                if (perturb_step<kThreads, kU, kM, kRows>(tiles, rows, tile, n_full, cur, nxt, a,
+                                                          b, st))
+                    break;
             }
         }
     }
     for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x)
-        perturb_tail<kThreads, kU, kM>(tile_ref(tiles[n_full + tl]), st);
+        perturb_tail<kThreads, kU, kM, kRows>(load_ref<kRows>(tiles, rows, n_full + tl), st);
 }
 
 // The in-place streaming ceiling of a plan (es_stream_pass): every element
@@ -530,25 +605,28 @@ __device__ __forceinline__ void add_workgroup_sum(uint64_t acc, unsigned long lo
 }
 
 // bf16 plan: full tiles with 16-byte loads and no per-element bound, then
-// tail tiles bounds-checked.
-template <int kThreads, int kU>
+// tail tiles bounds-checked.  With kRows (tiles of strided blocks) each
+// term takes the element's whole-tensor index from the tile's row map.
+template <int kThreads, int kU, bool kRows>
 __global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __restrict__ tiles,
                                                                uint64_t n_full, uint64_t n_tail,
+                                                               const DevRows* __restrict__ rows,
                                                                unsigned long long* __restrict__ out) {
     uint64_t acc = 0;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
-        const TileRef r = tile_ref(tiles[tile]);
+        const TileRef r = load_ref<kRows>(tiles, rows, tile);
         const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
 #pragma unroll 1
         for (int u = 0; u < kU; ++u) {
             const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
             uint32_t raw[4];
             load_group<true, true>(r.data, e, r.limit, raw);
-            acc += checksum_terms<kGroupElems, 16, false>(raw, e, r.limit, salt);
+            acc += checksum_terms<kGroupElems, 16, false>(raw, noise_index<kRows>(r, e), r.limit,
+                                                          salt);
         }
     }
     for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x) {
-        const TileRef r = tile_ref(tiles[n_full + tl]);
+        const TileRef r = load_ref<kRows>(tiles, rows, n_full + tl);
         const uint64_t salt = uint64_t(r.tensor_id) * kSumT;
 #pragma unroll 1
         for (int u = 0; u < kU; ++u) {
@@ -556,7 +634,10 @@ __global__ __launch_bounds__(kThreads) void es_checksum_kernel(const DevTile* __
             if (e >= r.limit) break;
             uint32_t raw[4];
             load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
-            acc += checksum_terms<kGroupElems, 16, true>(raw, e, r.limit, salt);
+            const uint64_t n = noise_index<kRows>(r, e);
+            // the bound moves with the index: n + (limit - e) for a row map
+            acc += checksum_terms<kGroupElems, 16, true>(raw, n, kRows ? n + (r.limit - e) : r.limit,
+                                                         salt);
         }
     }
     add_workgroup_sum<kThreads>(acc, out);
@@ -641,11 +722,11 @@ struct RoundKey {
     uint32_t k0, k1;
 };
 
-template <int kThreads, int kU, bool kFast, bool kNT, bool kSR>
+template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct, RoundKey rk) {
-    const uint32_t q_hi = static_cast<uint32_t>(r.elem0 >> 34);
-    const uint32_t g_hi = static_cast<uint32_t>(r.elem0 >> 35);
+    const uint32_t tile_q_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t tile_g_hi = static_cast<uint32_t>(r.elem0 >> 35);
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
     uint32_t next[4];
     if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.limit, next);
@@ -661,7 +742,9 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         } else {
             load_group<false, kNT>(r.data, e, r.limit, raw, r.aligned16 != 0u);
         }
-        const uint32_t q_lo = static_cast<uint32_t>(e >> 2);
+        const uint64_t n = noise_index<kRows>(r, e);
+        const uint32_t q_lo = static_cast<uint32_t>(n >> 2);
+        const uint32_t q_hi = kRows ? static_cast<uint32_t>(n >> 34) : tile_q_hi;
         float acc[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
@@ -674,7 +757,8 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         }
         uint32_t out[4];
         if constexpr (kSR) {
-            const es::Words d = es::philox4x32_10(static_cast<uint32_t>(e >> 3), g_hi, r.tensor_id,
+            const uint32_t g_hi = kRows ? static_cast<uint32_t>(n >> 35) : tile_g_hi;
+            const es::Words d = es::philox4x32_10(static_cast<uint32_t>(n >> 3), g_hi, r.tensor_id,
                                                   es::kDomainRounding, rk.k0, rk.k1);
             const uint32_t draws[4] = {d.w0, d.w1, d.w2, d.w3};
 #pragma unroll
@@ -692,20 +776,23 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
 }
 
 // Fused update over the whole parameter list (member table and header
-// written by es_prepare_kernel): full tiles, then tail tiles.
-template <int kThreads, int kU, bool kNT, bool kSR>
+// written by es_prepare_kernel): full tiles, then tail tiles; with kRows the
+// tiles of strided blocks, through their row maps.
+template <int kThreads, int kU, bool kNT, bool kSR, bool kRows>
 __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
+                                                             const DevRows* __restrict__ rows,
                                                              const Member* __restrict__ members,
                                                              const UpdateHeader* __restrict__ hdr,
                                                              RoundKey rk) {
     if (hdr->n_live == 0u) return;          // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        update_tile<kThreads, kU, true, kNT, kSR>(tile_ref(tiles[tile]), members, n_distinct, rk);
+        update_tile<kThreads, kU, true, kNT, kSR, kRows>(load_ref<kRows>(tiles, rows, tile),
+                                                         members, n_distinct, rk);
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        update_tile<kThreads, kU, false, kNT, kSR>(tile_ref(tiles[n_full + tile]), members,
-                                                   n_distinct, rk);
+        update_tile<kThreads, kU, false, kNT, kSR, kRows>(
+            load_ref<kRows>(tiles, rows, n_full + tile), members, n_distinct, rk);
 }
 
 // The scratch of es_update_noalloc: one update's staged member tables, merged
@@ -856,16 +943,16 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
     }
 }
 
-using PerturbKernel = void (*)(const DevTile*, uint64_t, uint64_t, Streams);
-using UpdateKernel = void (*)(const DevTile*, uint64_t, uint64_t, const Member*,
+using PerturbKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, Streams);
+using UpdateKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, const Member*,
                               const UpdateHeader*, RoundKey);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
 #define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
 
-template <int kM>
+template <int kM, bool kRows>
 PerturbKernel perturb_kernel_for(int threads, int groups) {
-#define ES_CASE(T, U) if (threads == T && groups == U) return es_perturb_kernel<T, U, kM>;
+#define ES_CASE(T, U) if (threads == T && groups == U) return es_perturb_kernel<T, U, kM, kRows>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -880,29 +967,41 @@ StreamKernel stream_kernel(int threads, int groups) {
     return nullptr;
 }
 
-using ChecksumKernel = void (*)(const DevTile*, uint64_t, uint64_t, unsigned long long*);
+using ChecksumKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*,
+                                unsigned long long*);
 
-ChecksumKernel checksum_kernel(int threads, int groups) {
-#define ES_CASE(T, U) if (threads == T && groups == U) return es_checksum_kernel<T, U>;
+ChecksumKernel checksum_kernel(int threads, int groups, bool rows) {
+#define ES_CASE(T, U)                                                                     \
+    if (threads == T && groups == U)                                                      \
+        return rows ? es_checksum_kernel<T, U, true> : es_checksum_kernel<T, U, false>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
 }
 
-// streams: 1 (perturb / restore), 2 (swap, two keys), 3 (swap, one key)
-PerturbKernel perturb_kernel(int streams, int threads, int groups) {
-    switch (streams) {
-        case 1: return perturb_kernel_for<1>(threads, groups);
-        case 2: return perturb_kernel_for<2>(threads, groups);
-        case 3: return perturb_kernel_for<3>(threads, groups);
+// streams: 1 (perturb / restore), 2 (swap, two keys), 3 (swap, one key);
+// rows: the launch over strided blocks' tiles.
+PerturbKernel perturb_kernel(int streams, int threads, int groups, bool rows) {
+    switch (streams * 2 + (rows ? 1 : 0)) {
+        case 2: return perturb_kernel_for<1, false>(threads, groups);
+        case 3: return perturb_kernel_for<1, true>(threads, groups);
+        case 4: return perturb_kernel_for<2, false>(threads, groups);
+        case 5: return perturb_kernel_for<2, true>(threads, groups);
+        case 6: return perturb_kernel_for<3, false>(threads, groups);
+        case 7: return perturb_kernel_for<3, true>(threads, groups);
         default: return nullptr;
     }
 }
 
-UpdateKernel update_kernel(int threads, int groups, bool stochastic) {
+UpdateKernel update_kernel(int threads, int groups, bool stochastic, bool rows) {
 #define ES_CASE(T, U)                                                                     \
-    if (threads == T && groups == U)                                                      \
-        return stochastic ? es_update_kernel<T, U, true, true> : es_update_kernel<T, U, true, false>;
+    if (threads == T && groups == U) {                                                    \
+        if (rows)                                                                         \
+            return stochastic ? es_update_kernel<T, U, true, true, true>                  \
+                              : es_update_kernel<T, U, true, false, true>;                \
+        return stochastic ? es_update_kernel<T, U, true, true, false>                     \
+                          : es_update_kernel<T, U, true, false, false>;                   \
+    }
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -1179,12 +1278,18 @@ struct es_plan {
     uint64_t numel = 0;
     uint64_t n_full = 0;            // full tiles (16-byte path)
     uint64_t n_tail = 0;            // tail tiles (bounds-checked path)
+    uint64_t n_rfull = 0;           // full and tail tiles of strided blocks, after the
+    uint64_t n_rtail = 0;           //   others, each with a row map
     uint32_t grid_perturb = 0;      // workgroups of the perturb / restore launch
     uint32_t grid_update = 0;       // workgroups of the update launch
+    uint32_t grid_perturb_rows = 0; // the same for the strided blocks' launch
+    uint32_t grid_update_rows = 0;
     int threads = kDefaultThreads;  // lanes per workgroup of the tile kernels
     int groups = kDefaultGroups;    // 8-element groups per lane per tile
     uint64_t tile_elems = 0;        // threads * groups * 8
-    DevTile* d_tiles = nullptr;     // n_full full-tile then n_tail tail-tile descriptors
+    DevTile* d_tiles = nullptr;     // n_full full-tile then n_tail tail-tile descriptors, then
+                                    //   n_rfull + n_rtail of strided blocks
+    DevRows* d_rows = nullptr;      // their row maps (same allocation, after the descriptors)
     uint8_t* d_scratch = nullptr;   // kScratchBytes
 };
 
@@ -1223,11 +1328,31 @@ int check_device(const es_plan_t* p) {
     return ES_OK;
 }
 
+// The launches of a pass over a plan: one over the tiles of tensors and
+// contiguous blocks, and one over the tiles of strided blocks with their
+// row maps; a part with no tiles is left out.
+struct Segment {
+    const DevTile* tiles;
+    uint64_t n_full, n_tail;
+    const DevRows* rows;            // null for the first part
+    uint32_t grid_perturb, grid_update;
+};
+
+int plan_segments(const es_plan_t* p, Segment seg[2]) {
+    int n = 0;
+    if (p->n_full + p->n_tail > 0)
+        seg[n++] = Segment{p->d_tiles, p->n_full, p->n_tail, nullptr, p->grid_perturb,
+                           p->grid_update};
+    if (p->n_rfull + p->n_rtail > 0)
+        seg[n++] = Segment{p->d_tiles + p->n_full + p->n_tail, p->n_rfull, p->n_rtail, p->d_rows,
+                           p->grid_perturb_rows, p->grid_update_rows};
+    return n;
+}
+
 // One pass of the perturb kernel: streams = 1 (seed[0], coef[0]), 2 (two
 // keys) or 3 (both coefficients on seed[0]).
 int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double* coef,
                    hipStream_t s) {
-    if (p->n_full + p->n_tail == 0) return ES_OK;
     Streams st = {};
     const int terms = streams == 1 ? 1 : 2;
     for (int m = 0; m < terms; ++m) {
@@ -1236,11 +1361,16 @@ int launch_streams(es_plan_t* p, int streams, const uint64_t* seed, const double
         st.k1[m] = static_cast<uint32_t>(sd >> 32);
         st.coef_k[m] = static_cast<float>(coef[m] * kSqrt2Ln2Double);
     }
-    const PerturbKernel kernel = perturb_kernel(streams, p->threads, p->groups);
-    hipLaunchKernelGGL(kernel, dim3(p->grid_perturb), dim3(p->threads), 0, s, p->d_tiles,
-                       p->n_full, p->n_tail, st);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_perturb_kernel launch");
+    Segment seg[2];
+    const int n_seg = plan_segments(p, seg);
+    for (int k = 0; k < n_seg; ++k) {
+        const Segment& g = seg[k];
+        const PerturbKernel kernel = perturb_kernel(streams, p->threads, p->groups, g.rows != nullptr);
+        hipLaunchKernelGGL(kernel, dim3(g.grid_perturb), dim3(p->threads), 0, s, g.tiles, g.n_full,
+                           g.n_tail, g.rows, st);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "es_perturb_kernel launch");
+    }
     return ES_OK;
 }
 
@@ -1386,7 +1516,7 @@ void row_divisor(uint32_t r, uint32_t& magic, uint32_t& shift) {
 void launch_shape(int& threads, int& groups) {
     threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
     groups = env_int("ESOPT_GROUPS", kDefaultGroups, 2, 8);
-    if (update_kernel(threads, groups, false) == nullptr) {
+    if (update_kernel(threads, groups, false, false) == nullptr) {
         threads = kDefaultThreads;
         groups = kDefaultGroups;
     }
@@ -1580,17 +1710,21 @@ int update_impl(const char* name, es_plan_t* plan, uint8_t* d_scratch, const uin
     int rc = prepare_update(d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
                             status_out_dev, s);
     if (rc != ES_OK) return rc;
-    if (plan->n_full + plan->n_tail == 0) return ES_OK;
     const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
     const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
                       static_cast<uint32_t>(opts->round_seed >> 32)};
-    const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr);
-    hipLaunchKernelGGL(kernel, dim3(plan->grid_update), dim3(plan->threads), 0, s, plan->d_tiles,
-                       plan->n_full, plan->n_tail,
-                       reinterpret_cast<const Member*>(d_scratch + kOffMembers),
-                       reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, std::string(name) + ": es_update_kernel launch");
+    Segment seg[2];
+    const int n_seg = plan_segments(plan, seg);
+    for (int k = 0; k < n_seg; ++k) {
+        const Segment& g = seg[k];
+        const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr, g.rows != nullptr);
+        hipLaunchKernelGGL(kernel, dim3(g.grid_update), dim3(plan->threads), 0, s, g.tiles,
+                           g.n_full, g.n_tail, g.rows,
+                           reinterpret_cast<const Member*>(d_scratch + kOffMembers),
+                           reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, std::string(name) + ": es_update_kernel launch");
+    }
     return ES_OK;
 }
 
@@ -1618,6 +1752,143 @@ int static_scratch(int device, uint8_t** out) {
     }
     *out = p;
     return ES_OK;
+}
+
+// The tiles of a plan under construction: those of tensors and contiguous
+// blocks, and those of strided blocks with one row map each.
+struct PlanTiles {
+    std::vector<DevTile> full, tail;
+    std::vector<DevTile> rfull, rtail;
+    std::vector<DevRows> rows_full, rows_tail;
+};
+
+// Strided blocks are cut into pieces of at most this many elements, so that
+// a piece's local element indices stay below 2^31 (the row division's
+// range).  A block whose rows are longer than half of that, or whose rows lie
+// 2^32 or more elements apart, is laid out row by row instead, each row a
+// contiguous shard of its own.
+constexpr uint64_t kPieceElems = uint64_t(1) << 31;
+
+// Tiles of one block (already validated).  A block that is one contiguous
+// range of its tensor is tiled as a shard at its first index.  A strided
+// block is cut into pieces of whole rows, each tiled by address with local
+// element indices, and every tile of a piece gets the piece's row map.
+void tile_block(const es_block_t& b, uint64_t tile_elems, PlanTiles& t) {
+    const uint64_t numel = b.rows * b.cols;
+    if (numel == 0) return;
+    uint16_t* const data = static_cast<uint16_t*>(b.data);
+    const uint64_t n0 = b.row0 * b.row_len + b.col0;
+    if (b.rows == 1 || b.cols == b.row_len) {
+        tile_tensor(data, numel, n0, b.tensor_id, tile_elems, t.full, t.tail);
+        return;
+    }
+    if (b.cols > kPieceElems / 2 || b.row_len - b.cols > 0xFFFFFFFFull) {
+        for (uint64_t i = 0; i < b.rows; ++i)
+            tile_tensor(data + i * b.cols, b.cols, n0 + i * b.row_len, b.tensor_id, tile_elems,
+                        t.full, t.tail);
+        return;
+    }
+    DevRows m{};
+    m.skip = static_cast<uint32_t>(b.row_len - b.cols);
+    row_divisor(static_cast<uint32_t>(b.cols), m.magic, m.shift);
+    const uint64_t piece_rows = kPieceElems / b.cols;
+    for (uint64_t r = 0; r < b.rows; r += piece_rows) {
+        const uint64_t nr = std::min(piece_rows, b.rows - r);
+        m.n0 = n0 + r * b.row_len;
+        const size_t f0 = t.rfull.size(), t0 = t.rtail.size();
+        tile_tensor(data + r * b.cols, nr * b.cols, 0, b.tensor_id, tile_elems, t.rfull, t.rtail);
+        t.rows_full.insert(t.rows_full.end(), t.rfull.size() - f0, m);
+        t.rows_tail.insert(t.rows_tail.end(), t.rtail.size() - t0, m);
+    }
+}
+
+// A plan over tiles laid out by the caller (es_plan_create,
+// es_plan_create_blocks): launch grids, one device allocation for the
+// descriptors and row maps, the scratch.
+int finish_plan(const char* name, int device, uint32_t n_tensors, uint64_t numel, int threads,
+                int groups, PlanTiles& t, es_plan_t** out) {
+    const std::string nm(name);
+    const uint64_t n_full = t.full.size(), n_tail = t.tail.size();
+    const uint64_t n_rfull = t.rfull.size(), n_rtail = t.rtail.size();
+    std::vector<DevTile> tiles;
+    tiles.reserve(n_full + n_tail + n_rfull + n_rtail);
+    tiles.insert(tiles.end(), t.full.begin(), t.full.end());
+    tiles.insert(tiles.end(), t.tail.begin(), t.tail.end());
+    tiles.insert(tiles.end(), t.rfull.begin(), t.rfull.end());
+    tiles.insert(tiles.end(), t.rtail.begin(), t.rtail.end());
+    std::vector<DevRows> rows;
+    rows.reserve(n_rfull + n_rtail);
+    rows.insert(rows.end(), t.rows_full.begin(), t.rows_full.end());
+    rows.insert(rows.end(), t.rows_tail.begin(), t.rows_tail.end());
+    es_plan_t* p = new (std::nothrow) es_plan_t;
+    if (p == nullptr) return fail(ES_ERR_NOMEM, nm + ": host allocation");
+    p->device = device;
+    int cus = 0;
+    hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
+    const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
+    const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
+    p->threads = threads;
+    p->groups = groups;
+    p->tile_elems = uint64_t(threads) * groups * kGroupElems;
+    p->n_tensors = n_tensors;
+    p->numel = numel;
+    p->n_full = n_full;
+    p->n_tail = n_tail;
+    p->n_rfull = n_rfull;
+    p->n_rtail = n_rtail;
+    auto grid = [&](uint64_t a, uint64_t b, int per_cu) {
+        const uint64_t cap = std::max<uint64_t>(std::max(a, b), 1);
+        return static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * per_cu));
+    };
+    p->grid_perturb = grid(n_full, n_tail, wg_perturb);
+    p->grid_update = grid(n_full, n_tail, wg_update);
+    p->grid_perturb_rows = grid(n_rfull, n_rtail, wg_perturb);
+    p->grid_update_rows = grid(n_rfull, n_rtail, wg_update);
+    const size_t tile_bytes = sizeof(DevTile) * std::max<size_t>(tiles.size(), 1);
+    const size_t rows_bytes = sizeof(DevRows) * rows.size();
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_tiles), tile_bytes + rows_bytes);
+    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
+    p->d_rows = rows.empty() ? nullptr
+                             : reinterpret_cast<DevRows*>(reinterpret_cast<uint8_t*>(p->d_tiles) +
+                                                          tile_bytes);
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tiles);
+        delete p;
+        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    if (!tiles.empty())
+        e = hipMemcpy(p->d_tiles, tiles.data(), sizeof(DevTile) * tiles.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess && !rows.empty())
+        e = hipMemcpy(p->d_rows, rows.data(), rows_bytes, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tiles);
+        (void)hipFree(p->d_scratch);
+        delete p;
+        return hip_fail(e, nm + ": tile table upload");
+    }
+    *out = p;
+    return ES_OK;
+}
+
+// Checks of one block's geometry (es_block_t's requirements), in 128-bit
+// arithmetic so that no product or sum wraps; an empty string when it holds.
+std::string block_geometry_error(const es_block_t& b) {
+    typedef unsigned __int128 u128;
+    const u128 two60 = u128(1) << 60;
+    const u128 numel = u128(b.rows) * b.cols;
+    if (numel > two60) return "rows * cols above 2^60";
+    if (numel == 0) return "";
+    if (u128(b.col0) + b.cols > b.row_len) return "col0 + cols above row_len";
+    const u128 first = u128(b.row0) * b.row_len + b.col0;
+    const u128 end = u128(b.row0 + u128(b.rows - 1)) * b.row_len + b.col0 + b.cols;
+    if (end > two60) return "an element index at or above 2^60";
+    if (first % 8 != 0) return "first index row0 * row_len + col0 not a multiple of 8";
+    if (b.rows > 1 && b.cols < b.row_len && (b.cols % 8 != 0 || b.row_len % 8 != 0))
+        return "strided block: cols and row_len must be multiples of 8";
+    return "";
 }
 
 }  // namespace
@@ -1663,54 +1934,60 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
     if (rc != ES_OK) return rc;
     // the tile descriptors (built after the accesses are known to be valid:
     // every tensor lies inside one device allocation)
-    std::vector<DevTile> tiles, tail;
+    PlanTiles t;
     for (uint32_t i = 0; i < n_tensors; ++i)
         tile_tensor(static_cast<uint16_t*>(tensors[i].data), tensors[i].numel,
-                    8 * uint64_t(tensors[i].offset8), tensors[i].tensor_id, tile_elems, tiles,
-                    tail);
-    const uint64_t n_full = tiles.size(), n_tail = tail.size();
-    tiles.insert(tiles.end(), tail.begin(), tail.end());
-    es_plan_t* p = new (std::nothrow) es_plan_t;
-    if (p == nullptr) return fail(ES_ERR_NOMEM, "es_plan_create: host allocation");
-    p->device = device;
-    hipError_t e = hipSuccess;
-    int cus = 0;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
-    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
-    const int wg_perturb = env_int("ESOPT_PERTURB_WG_PER_CU", kDefaultPerturbWgPerCu, 1, 32);
-    const int wg_update = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
-    p->threads = threads;
-    p->groups = groups;
-    p->tile_elems = tile_elems;
-    p->n_tensors = n_tensors;
-    p->numel = numel;
-    p->n_full = n_full;
-    p->n_tail = n_tail;
-    const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
-    p->grid_perturb = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_perturb));
-    p->grid_update = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg_update));
-    const size_t tile_bytes = sizeof(DevTile) * std::max<size_t>(tiles.size(), 1);
-    e = hipMalloc(reinterpret_cast<void**>(&p->d_tiles), tile_bytes);
-    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
-    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
-    if (e != hipSuccess) {
-        (void)hipFree(p->d_tiles);
-        delete p;
-        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
-    }
-    if (!tiles.empty())
-        e = hipMemcpy(p->d_tiles, tiles.data(), sizeof(DevTile) * tiles.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
-    if (e != hipSuccess) {
-        (void)hipFree(p->d_tiles);
-        (void)hipFree(p->d_scratch);
-        delete p;
-        return hip_fail(e, "es_plan_create: tile table upload");
-    }
-    *out = p;
-    return ES_OK;
+                    8 * uint64_t(tensors[i].offset8), tensors[i].tensor_id, tile_elems, t.full,
+                    t.tail);
+    return finish_plan("es_plan_create", device, n_tensors, numel, threads, groups, t, out);
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_plan_create: host allocation failed");
+}
+
+int es_plan_create_blocks(const es_block_t* blocks, uint32_t n_blocks, es_plan_t** out) try {
+    if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create_blocks: null output pointer");
+    *out = nullptr;
+    if (blocks == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_create_blocks: null block list");
+    if (n_blocks == 0 || n_blocks > ES_MAX_TENSORS)
+        return fail(ES_ERR_INVALID_ARG, "es_plan_create_blocks: n_blocks out of range");
+    int threads = 0, groups = 0;
+    launch_shape(threads, groups);
+    const uint64_t tile_elems = uint64_t(threads) * groups * kGroupElems;
+    std::unordered_map<uint32_t, uint32_t> ids;
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    uint64_t numel = 0;
+    for (uint32_t i = 0; i < n_blocks; ++i) {
+        const es_block_t& b = blocks[i];
+        const std::string where = "es_plan_create_blocks: block " + std::to_string(i);
+        if (b.reserved != 0) return fail(ES_ERR_INVALID_ARG, where + ": reserved field not 0");
+        if (!ids.emplace(b.tensor_id, i).second)
+            return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(b.tensor_id));
+        const std::string bad = block_geometry_error(b);
+        if (!bad.empty()) return fail(ES_ERR_INVALID_ARG, where + ": " + bad);
+        const uint64_t n = b.rows * b.cols;
+        if (n > 0 && b.data == nullptr) return fail(ES_ERR_INVALID_ARG, where + ": null data");
+        const uintptr_t a = reinterpret_cast<uintptr_t>(b.data);
+        if (n > 0 && (a & 1u)) return fail(ES_ERR_ALIGN, where + ": data not 2-byte aligned");
+        if (n > 0) ranges.emplace_back(a, a + 2 * n);
+        numel += n;
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+        if (ranges[i].first < ranges[i - 1].second)
+            return fail(ES_ERR_INVALID_ARG, "es_plan_create_blocks: blocks overlap in memory");
+
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc != ES_OK) return rc;
+    for (uint32_t i = 0; i < n_blocks && rc == ES_OK; ++i)
+        rc = check_access(blocks[i].data, 2 * blocks[i].rows * blocks[i].cols, device,
+                          "es_plan_create_blocks: block " + std::to_string(i));
+    if (rc != ES_OK) return rc;
+    PlanTiles t;
+    for (uint32_t i = 0; i < n_blocks; ++i) tile_block(blocks[i], tile_elems, t);
+    return finish_plan("es_plan_create_blocks", device, n_blocks, numel, threads, groups, t, out);
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_plan_create_blocks: host allocation failed");
 }
 
 int es_plan_destroy(es_plan_t* plan) {
@@ -1724,11 +2001,14 @@ int es_plan_destroy(es_plan_t* plan) {
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
 
 uint64_t es_plan_device_bytes(const es_plan_t* plan) {
-    return plan ? sizeof(DevTile) * std::max<uint64_t>(plan->n_full + plan->n_tail, 1) +
-                      kScratchBytes
+    return plan ? sizeof(DevTile) * std::max<uint64_t>(plan->n_full + plan->n_tail +
+                                                           plan->n_rfull + plan->n_rtail, 1) +
+                      sizeof(DevRows) * (plan->n_rfull + plan->n_rtail) + kScratchBytes
                 : 0;
 }
-uint64_t es_plan_tiles(const es_plan_t* plan) { return plan ? plan->n_full + plan->n_tail : 0; }
+uint64_t es_plan_tiles(const es_plan_t* plan) {
+    return plan ? plan->n_full + plan->n_tail + plan->n_rfull + plan->n_rtail : 0;
+}
 
 int es_perturb(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
     return perturb_impl(plan, seed, sign, sigma, stream, "es_perturb");
@@ -1984,12 +2264,16 @@ int es_stream_pass(es_plan_t* plan, es_stream_t stream) {
     if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_stream_pass: null plan");
     const int rc = check_device(plan);
     if (rc != ES_OK) return rc;
-    if (plan->n_full + plan->n_tail == 0) return ES_OK;
-    hipLaunchKernelGGL(stream_kernel(plan->threads, plan->groups), dim3(plan->grid_perturb),
-                       dim3(plan->threads), 0, static_cast<hipStream_t>(stream), plan->d_tiles,
-                       plan->n_full, plan->n_tail, 0u);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
+    Segment seg[2];
+    const int n_seg = plan_segments(plan, seg);
+    for (int k = 0; k < n_seg; ++k) {
+        const Segment& g = seg[k];
+        hipLaunchKernelGGL(stream_kernel(plan->threads, plan->groups), dim3(g.grid_perturb),
+                           dim3(plan->threads), 0, static_cast<hipStream_t>(stream), g.tiles,
+                           g.n_full, g.n_tail, 0u);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "es_stream_kernel launch");
+    }
     return ES_OK;
 }
 
@@ -2048,11 +2332,16 @@ int es_plan_checksum(es_plan_t* plan, uint64_t* out_dev, es_stream_t stream) {
     hipLaunchKernelGGL(es_zero_u64_kernel, dim3(1), dim3(64), 0, s, out);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "es_zero_u64_kernel launch");
-    if (plan->n_full + plan->n_tail == 0) return ES_OK;
-    hipLaunchKernelGGL(checksum_kernel(plan->threads, plan->groups), dim3(plan->grid_update),
-                       dim3(plan->threads), 0, s, plan->d_tiles, plan->n_full, plan->n_tail, out);
-    e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "es_checksum_kernel launch");
+    Segment seg[2];
+    const int n_seg = plan_segments(plan, seg);
+    for (int k = 0; k < n_seg; ++k) {
+        const Segment& g = seg[k];
+        hipLaunchKernelGGL(checksum_kernel(plan->threads, plan->groups, g.rows != nullptr),
+                           dim3(g.grid_update), dim3(plan->threads), 0, s, g.tiles, g.n_full,
+                           g.n_tail, g.rows, out);
+        e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "es_checksum_kernel launch");
+    }
     return ES_OK;
 }
 

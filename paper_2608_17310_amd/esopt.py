@@ -42,6 +42,11 @@ class EsTensor(ctypes.Structure):
     _fields_ = [("data", _vp), ("numel", _u64), ("tensor_id", _u32), ("offset8", _u32)]
 
 
+class EsBlock(ctypes.Structure):
+    _fields_ = [("data", _vp), ("rows", _u64), ("cols", _u64), ("row_len", _u64),
+                ("row0", _u64), ("col0", _u64), ("tensor_id", _u32), ("reserved", _u32)]
+
+
 class EsQTensor(ctypes.Structure):
     _fields_ = [("data", _vp), ("scales", _vp), ("numel", _u64), ("row", _u32),
                 ("tensor_id", _u32)]
@@ -58,6 +63,8 @@ class EsUpdateOpts(ctypes.Structure):
 
 SIGNATURES = {
     "es_plan_create": (ctypes.c_int, [ctypes.POINTER(EsTensor), _u32, ctypes.POINTER(_vp)]),
+    "es_plan_create_blocks": (ctypes.c_int, [ctypes.POINTER(EsBlock), _u32,
+                                             ctypes.POINTER(_vp)]),
     "es_plan_destroy": (ctypes.c_int, [_vp]),
     "es_plan_numel": (_u64, [_vp]),
     "es_plan_tiles": (_u64, [_vp]),
@@ -166,18 +173,35 @@ def _dev_ptr(t, dtype, what):
     return ctypes.c_void_p(t.data_ptr())
 
 
+class Block(tuple):
+    """One block of es_plan_create_blocks: Block(tensor, tensor_id, row_len,
+    row0=0, col0=0), the whole tensor's rows row0.. and columns col0.. of a
+    row-major tensor with row_len columns, stored as `tensor` ([rows, cols]
+    contiguous, or 1-D for one row)."""
+
+    def __new__(cls, tensor, tensor_id, row_len, row0=0, col0=0):
+        return super().__new__(cls, (tensor, tensor_id, row_len, row0, col0))
+
+
 class Plan:
     """A list of bf16 parameter tensors prepared for single-launch passes.
 
     tensor_ids defaults to the list index.  offsets (multiples of 8, default
     0) place shards: element i of tensors[k] carries the noise of element
-    offsets[k] + i of the whole tensor tensor_ids[k].  The plan holds
+    offsets[k] + i of the whole tensor tensor_ids[k].  Plan(blocks=[Block...])
+    plans rectangular blocks of row-major tensors instead (column or
+    row-and-column shards; es_plan_create_blocks).  The plan holds
     references to the tensors so their storage stays alive and in place
     while it exists.
     """
 
-    def __init__(self, tensors, tensor_ids=None, offsets=None):
-        tensors = list(tensors)
+    def __init__(self, tensors=None, tensor_ids=None, offsets=None, blocks=None):
+        if blocks is not None:
+            if tensors is not None or tensor_ids is not None or offsets is not None:
+                raise ValueError("give either tensors or blocks")
+            self._init_blocks(list(blocks))
+            return
+        tensors = list(tensors if tensors is not None else [])
         if not tensors:
             raise ValueError("empty tensor list")
         ids = (list(range(len(tensors))) if tensor_ids is None
@@ -198,6 +222,40 @@ class Plan:
         handle = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             _check(load().es_plan_create(arr, len(tensors), ctypes.byref(handle)), "es_plan_create")
+        self._h = handle
+
+    def _init_blocks(self, blocks):
+        """es_plan_create_blocks.  Each block is (tensor, tensor_id, row_len,
+        row0, col0): `tensor` a contiguous bf16 CUDA tensor of shape
+        [rows, cols] (1-D: one row) holding the whole tensor's rows
+        row0.. and columns col0.. of a row-major tensor with row_len columns
+        (Block names the fields)."""
+        if not blocks:
+            raise ValueError("empty block list")
+        arr = (EsBlock * len(blocks))()
+        tensors, ids = [], []
+        for i, b in enumerate(blocks):
+            t, tid, row_len, row0, col0 = b
+            if t.dtype != torch.bfloat16 or not t.is_cuda or not t.is_contiguous():
+                raise ValueError(f"block {i} must be a contiguous bf16 CUDA tensor")
+            if t.dim() == 1:
+                rows, cols = 1, t.numel()
+            elif t.dim() == 2:
+                rows, cols = t.shape
+            else:
+                raise ValueError(f"block {i} must be 1-D or 2-D")
+            arr[i] = EsBlock(t.data_ptr() if t.numel() else None, rows, cols,
+                             _u64_arg(row_len, "row_len"), _u64_arg(row0, "row0"),
+                             _u64_arg(col0, "col0"), _u32_arg(tid, "tensor_id"), 0)
+            tensors.append(t)
+            ids.append(int(tid))
+        self._tensors = tensors
+        self.tensor_ids = ids
+        self.device = tensors[0].device
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(load().es_plan_create_blocks(arr, len(blocks), ctypes.byref(handle)),
+                   "es_plan_create_blocks")
         self._h = handle
 
     @property

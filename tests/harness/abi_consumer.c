@@ -16,6 +16,12 @@ int main(void) {
            sizeof(es_qtensor_t), offsetof(es_qtensor_t, data), offsetof(es_qtensor_t, scales),
            offsetof(es_qtensor_t, numel), offsetof(es_qtensor_t, row),
            offsetof(es_qtensor_t, tensor_id));
+    printf("es_block_t %zu data %zu rows %zu cols %zu row_len %zu row0 %zu col0 %zu "
+           "tensor_id %zu reserved %zu\n",
+           sizeof(es_block_t), offsetof(es_block_t, data), offsetof(es_block_t, rows),
+           offsetof(es_block_t, cols), offsetof(es_block_t, row_len), offsetof(es_block_t, row0),
+           offsetof(es_block_t, col0), offsetof(es_block_t, tensor_id),
+           offsetof(es_block_t, reserved));
     printf("es_update_opts_t %zu alpha %zu sigma %zu zscore_eps %zu flags %zu round_seed %zu\n",
            sizeof(es_update_opts_t), offsetof(es_update_opts_t, alpha),
            offsetof(es_update_opts_t, sigma), offsetof(es_update_opts_t, zscore_eps),
@@ -24,6 +30,7 @@ int main(void) {
            ES_UPDATE_STOCHASTIC_ROUND, ES_MAX_MEMBERS);
     es_plan_t* plan = NULL;
     printf("plan_create_null %d\n", es_plan_create(NULL, 1, &plan));
+    printf("plan_create_blocks_null %d\n", es_plan_create_blocks(NULL, 1, &plan));
     printf("perturb_null %d\n", es_perturb(NULL, 1, 1, 1e-3f, NULL));
     es_qplan_t* qplan = NULL;
     printf("qplan_create_null %d\n", es_qplan_create(NULL, 1, &qplan));

@@ -1,7 +1,8 @@
 // Host-side checks of the library's own host code, built with AddressSanitizer
 // and UndefinedBehaviorSanitizer (host pass only, no device code): the
-// population tables of the update, the tiling of tensors, the int8 row
-// divisor, and every argument check that fails before the device is touched.
+// population tables of the update, the tiling of tensors and of blocks, the
+// int8 row divisor, and every argument check that fails before the device is
+// touched.
 // The library source is compiled into this translation unit, so its internal
 // (anonymous-namespace) routines are reachable; each is compared with a plain
 // reference written here.  Prints "ok" and exits 0, or names the first
@@ -112,6 +113,144 @@ void test_tiling(std::mt19937_64& rng) {
           "tile layout: above 2^60");
     check(es_tile_layout(0, 10, 0, nullptr, 5, &n) == ES_ERR_INVALID_ARG,
           "tile layout: null output with a capacity");
+}
+
+// Block tiling (es_plan_create_blocks): every element of a block lies in
+// exactly one tile, at its own address, and the index the kernels give it is
+// its whole-tensor index (row0 + i) row_len + col0 + j.  The kernels take a
+// group's index at its first element (tile start + a multiple of 8) and
+// count on from there: the descriptor's element itself for a contiguous
+// layout, rows_index through the row map for a strided piece.
+struct BlockCheck {
+    const es_block_t& b;
+    uintptr_t addr;
+    uint64_t numel;
+    std::vector<uint8_t>* cover;           // null: sampled check only
+    uint64_t expected(uint64_t local) const {
+        return (b.row0 + local / b.cols) * b.row_len + b.col0 + local % b.cols;
+    }
+    // element e of a tile: its address gives its place in the block
+    void element(const DevTile& d, const DevRows* m, uint64_t e) {
+        const uintptr_t a = reinterpret_cast<uintptr_t>(d.data) + 2 * e;
+        check(a >= addr && (a - addr) / 2 < numel, "block tiling: address inside the block");
+        if (a < addr || (a - addr) / 2 >= numel) return;
+        const uint64_t local = (a - addr) / 2;
+        if (cover) ++(*cover)[local];
+        const uint64_t g = d.elem0 + ((e - d.elem0) & ~uint64_t(7));
+        const uint64_t n = m ? rows_index(m->n0, m->skip, m->magic, m->shift, g) + (e - g)
+                             : e;
+        check(n == expected(local), "block tiling: whole-tensor index");
+        if (m) check(e < (uint64_t(1) << 31), "block tiling: piece index below 2^31");
+        // the counter's high word is taken per tile for a contiguous layout
+        if (!m) check((d.elem0 >> 34) == (e >> 34), "block tiling: uniform high word");
+    }
+    void tiles(const std::vector<DevTile>& v, const std::vector<DevRows>* rows, bool full,
+               uint64_t tile, bool sampled) {
+        for (size_t i = 0; i < v.size(); ++i) {
+            const DevTile& d = v[i];
+            const DevRows* m = rows ? &(*rows)[i] : nullptr;
+            check(d.elem0 < d.limit && d.limit - d.elem0 <= tile, "block tiling: tile size");
+            if (full) {
+                check(d.limit - d.elem0 == tile, "block tiling: full tile size");
+                check((reinterpret_cast<uintptr_t>(d.data) + 2 * d.elem0) % (2 * tile) == 0,
+                      "block tiling: full tile on an address boundary");
+            }
+            check(d.elem0 % 8 == 0 || d.aligned16 == 0, "block tiling: group starts");
+            if (sampled) {
+                for (uint64_t e : {d.elem0, d.elem0 + 7, (d.elem0 + d.limit) / 2, d.limit - 1})
+                    if (e < d.limit) element(d, m, e);
+            } else {
+                for (uint64_t e = d.elem0; e < d.limit; ++e) element(d, m, e);
+            }
+        }
+    }
+};
+
+void test_block_tiling(std::mt19937_64& rng) {
+    const uint64_t tile = uint64_t(kDefaultThreads) * kDefaultGroups * kGroupElems;
+    int strided_seen = 0, row_by_row_seen = 0;
+    for (int trial = 0; trial < 240; ++trial) {
+        es_block_t b{};
+        const int kind = trial % 6;
+        if (kind == 0) {                                  // one row, any length
+            b.rows = 1;
+            b.cols = rng() % (3 * tile);
+            b.row_len = b.cols + rng() % 5000;
+            b.col0 = rng() % (b.row_len - b.cols + 1);
+            b.row0 = rng() % 1000;
+            const uint64_t first = b.row0 * b.row_len + b.col0;
+            b.col0 -= std::min(b.col0, first % 8);        // first index a multiple of 8
+            if ((b.row0 * b.row_len + b.col0) % 8 != 0) b.row0 = 0, b.col0 = 0;
+        } else if (kind == 1) {                           // whole rows, any row length
+            b.cols = b.row_len = 1 + rng() % 3000;
+            b.rows = 1 + rng() % 60;
+            b.row0 = 8 * (rng() % 1000);
+        } else if (kind == 5) {                           // rows 2^32 or more apart
+            b.cols = 8 * (1 + rng() % 40);
+            b.row_len = (uint64_t(1) << 32) + 8 * (rng() % 1000) + b.cols;
+            b.rows = 2 + rng() % 6;
+            b.row0 = rng() % 1000;
+            b.col0 = 8 * (rng() % 100);
+        } else {                                          // column / 2-D shards
+            b.cols = 8 * (1 + rng() % (kind == 2 ? 4 : 700));
+            b.row_len = b.cols + 8 * (1 + rng() % 2000);
+            b.col0 = 8 * (rng() % ((b.row_len - b.cols) / 8 + 1));
+            b.rows = 2 + rng() % (kind == 2 ? 3000 : 150);
+            // some blocks straddle whole-tensor element 2^34
+            b.row0 = kind == 4 ? (uint64_t(1) << 34) / b.row_len - b.rows / 2 : rng() % 100000;
+        }
+        const uintptr_t addr =
+            uintptr_t(0x100000000000ull + (rng() % (uint64_t(1) << 40))) &
+            ~uintptr_t(trial % 5 == 0 ? 1 : 15);
+        b.data = reinterpret_cast<void*>(addr);
+        b.tensor_id = uint32_t(trial);
+        check(block_geometry_error(b).empty(), "block tiling: generated geometry is valid");
+        PlanTiles t;
+        tile_block(b, tile, t);
+        check(t.rows_full.size() == t.rfull.size() && t.rows_tail.size() == t.rtail.size(),
+              "block tiling: one row map per strided tile");
+        const bool contiguous = b.rows == 1 || b.cols == b.row_len;
+        check(!contiguous || t.rfull.empty() && t.rtail.empty(),
+              "block tiling: contiguous blocks take the plain layout");
+        strided_seen += !t.rfull.empty() || !t.rtail.empty();
+        row_by_row_seen += kind == 5 && t.rfull.empty() && t.rtail.empty() && !t.tail.empty();
+        const uint64_t numel = b.rows * b.cols;
+        std::vector<uint8_t> cover(numel, 0);
+        BlockCheck c{b, addr, numel, &cover};
+        c.tiles(t.full, nullptr, true, tile, false);
+        c.tiles(t.tail, nullptr, false, tile, false);
+        c.tiles(t.rfull, &t.rows_full, true, tile, false);
+        c.tiles(t.rtail, &t.rows_tail, false, tile, false);
+        bool once = true;
+        for (uint8_t k : cover) once &= (k == 1);
+        check(once, "block tiling: every element in exactly one tile");
+    }
+    check(strided_seen > 100 && row_by_row_seen > 20, "block tiling: every layout exercised");
+
+    // a block of more than 2^31 elements is cut into pieces of whole rows:
+    // sampled elements of every tile, and the tiles' sizes add up
+    es_block_t b{};
+    b.rows = 3000;
+    b.cols = uint64_t(1) << 20;
+    b.row_len = b.cols + 5120;
+    b.col0 = 2560;
+    b.row0 = 17;
+    b.data = reinterpret_cast<void*>(uintptr_t(0x200000000000ull + 4096));
+    PlanTiles t;
+    tile_block(b, tile, t);
+    uint64_t total = 0;
+    for (const auto* v : {&t.full, &t.tail, &t.rfull, &t.rtail})
+        for (const DevTile& d : *v) total += d.limit - d.elem0;
+    check(total == b.rows * b.cols, "block tiling: pieces add up to the block");
+    check(t.full.empty() && t.tail.empty(), "block tiling: pieces are strided");
+    std::vector<uint64_t> n0s;
+    for (const DevRows& m : t.rows_full) n0s.push_back(m.n0);
+    std::sort(n0s.begin(), n0s.end());
+    n0s.erase(std::unique(n0s.begin(), n0s.end()), n0s.end());
+    check(n0s.size() == 2, "block tiling: two pieces of 2048 and 952 rows");
+    BlockCheck c{b, reinterpret_cast<uintptr_t>(b.data), b.rows * b.cols, nullptr};
+    c.tiles(t.rfull, &t.rows_full, true, tile, true);
+    c.tiles(t.rtail, &t.rows_tail, false, tile, true);
 }
 
 // Row divisor: exact for every j < 2^31 (boundaries of every row, and random j).
@@ -226,6 +365,7 @@ int main() {
     std::mt19937_64 rng(20261202);
     test_member_tables(rng);
     test_tiling(rng);
+    test_block_tiling(rng);
     test_row_divisor(rng);
     test_validation();
     if (g_failures) {

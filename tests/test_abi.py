@@ -69,6 +69,48 @@ def test_plan_create_validation(lib):
     assert rc == esopt.ES_ERR_INVALID_ARG and "overlap" in msg
 
 
+def _create_blocks(lib, specs):
+    # spec: (data, rows, cols, row_len, row0, col0, tensor_id[, reserved])
+    arr = (esopt.EsBlock * max(len(specs), 1))(
+        *[esopt.EsBlock(*(tuple(s) + (0,) * (8 - len(s)))) for s in specs])
+    h = ctypes.c_void_p()
+    return lib.es_plan_create_blocks(arr, len(specs), ctypes.byref(h)), esopt.last_error()
+
+
+def test_block_plan_validation(lib):
+    """es_plan_create_blocks rejects every geometry es_block_t forbids, before
+    any device call."""
+    h = ctypes.c_void_p()
+    assert lib.es_plan_create_blocks(None, 1, ctypes.byref(h)) == esopt.ES_ERR_INVALID_ARG
+    assert lib.es_plan_create_blocks((esopt.EsBlock * 1)(), 1, None) == esopt.ES_ERR_INVALID_ARG
+    bad = [
+        ([], "n_blocks"),
+        ([(0x1000, 4, 64, 256, 0, 0, 0, 1)], "reserved"),
+        ([(0x1000, 4, 64, 256, 0, 0, 0), (0x9000, 4, 64, 256, 4, 0, 0)], "duplicate"),
+        ([(0x1000, 4, 64, 256, 0, 200, 0)], "col0 + cols"),
+        ([(0x1000, 4, 64, 256, 0, 4, 0)], "multiple of 8"),            # first index 4
+        ([(0x1000, 1, 64, 256, 1, 4, 0)], "multiple of 8"),            # 260
+        ([(0x1000, 4, 60, 256, 0, 0, 0)], "strided"),                  # cols % 8
+        ([(0x1000, 4, 64, 260, 0, 0, 0)], "strided"),                  # row_len % 8
+        ([(0x1000, 1 << 31, 1 << 30, 1 << 30, 0, 0, 0)], "2^60"),      # rows * cols
+        ([(0x1000, 2, 8, 1 << 59, 1, 0, 0)], "2^60"),                  # last index
+        ([(0x1000, 3, 1 << 62, 1 << 62, 0, 0, 0)], "2^60"),            # 64-bit product wraps
+        ([(None, 4, 64, 256, 0, 0, 0)], "null data"),
+        ([(0x1000, 4, 64, 256, 0, 0, 0), (0x1000 + 2 * 255, 1, 8, 8, 0, 0, 1)], "overlap"),
+    ]
+    for spec, word in bad:
+        rc, msg = _create_blocks(lib, spec)
+        assert rc == esopt.ES_ERR_INVALID_ARG and word in msg, (spec, msg)
+    rc, _ = _create_blocks(lib, [(0x1001, 4, 64, 256, 0, 0, 0)])
+    assert rc == esopt.ES_ERR_ALIGN
+    # geometries that need no multiple of 8 beyond the first index: one row,
+    # whole rows; an empty block needs nothing (these fail only at the device)
+    for spec in ([(0x1000, 1, 61, 1000, 3, 0, 0)], [(0x1000, 5, 61, 61, 8, 0, 0)],
+                 [(None, 0, 61, 7, 3, 1, 0)]):
+        rc, msg = _create_blocks(lib, spec)
+        assert "block 0" not in msg or rc != esopt.ES_ERR_INVALID_ARG, (spec, msg)
+
+
 def test_call_validation_without_device(lib):
     assert lib.es_perturb(None, 1, 1, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_restore(None, 1, 1, 1e-3, None) == esopt.ES_ERR_INVALID_ARG
@@ -157,6 +199,8 @@ def test_plain_c_consumer_of_header(lib, tmp_path):
     assert rows["es_tensor_t"] == layout(esopt.EsTensor)
     assert rows["es_update_opts_t"] == layout(esopt.EsUpdateOpts)
     assert rows["es_qtensor_t"] == layout(esopt.EsQTensor)
+    assert rows["es_block_t"] == layout(esopt.EsBlock)
+    assert rows["plan_create_blocks_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["qplan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
                              str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
