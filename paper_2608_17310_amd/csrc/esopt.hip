@@ -107,13 +107,16 @@ static_assert(sizeof(DevTile) == 32, "tile descriptor layout");
 // a group of 8 never spans two rows and its elements keep consecutive
 // indices (one quad pair).  The row division is a multiply-high and a shift
 // and skip = row_len - cols is below 2^32, so the map costs one 32 x 32-bit
-// multiply-add and a 64-bit add per group.  One entry per tile, beside its
-// descriptor.
+// multiply-add and a 64-bit add per group.  As with contiguous tiles, no tile
+// spans a multiple of 2^34 whole-tensor elements (the host splits it there),
+// so the counter's high word `hi` is the tile's, wave-uniform.  One entry per
+// tile, beside its descriptor.
 struct DevRows {
     uint64_t n0;
     uint32_t skip;                          // row_len - cols
     uint32_t magic, shift;                  // e / cols = mulhi(e, magic) >> shift
-    uint32_t pad[3];
+    uint32_t hi;                            // whole-tensor index >> 34, the same for the tile
+    uint32_t pad[2];
 };
 static_assert(sizeof(DevRows) == 32, "row map layout");
 
@@ -328,7 +331,7 @@ struct TileRef {
     uint32_t tensor_id;
     uint32_t aligned16;
     uint64_t n0 = 0;                        // row map (strided blocks only)
-    uint32_t skip = 0, magic = 0, shift = 0;
+    uint32_t skip = 0, magic = 0, shift = 0, hi = 0;
 };
 
 __device__ __forceinline__ TileRef tile_ref(const DevTile& d) {
@@ -337,7 +340,7 @@ __device__ __forceinline__ TileRef tile_ref(const DevTile& d) {
 
 __device__ __forceinline__ TileRef tile_ref(const DevTile& d, const DevRows& m) {
     return TileRef{d.data, d.limit, d.elem0, d.tensor_id, d.aligned16, m.n0, m.skip, m.magic,
-                   m.shift};
+                   m.shift, m.hi};
 }
 
 // Tile i of a launch: its descriptor, and with kRows its row map.
@@ -356,6 +359,13 @@ __device__ __forceinline__ uint64_t noise_index(const TileRef& r, uint64_t e) {
     else return e;
 }
 
+// The counter's high word (whole-tensor index >> 34), uniform over a tile.
+template <bool kRows>
+__device__ __forceinline__ uint32_t tile_high_word(const TileRef& r) {
+    if constexpr (kRows) return r.hi;
+    else return static_cast<uint32_t>(r.elem0 >> 34);
+}
+
 // Keep a prefetched descriptor in scalar registers: without this the
 // compiler may drop it and load it again where it is used, exposing the
 // load's latency there.  Placed after the work that hides the load, so the
@@ -364,7 +374,7 @@ __device__ __forceinline__ void keep_in_sgprs(DevTile& d) {
     asm volatile("" : "+s"(d.data), "+s"(d.elem0), "+s"(d.tensor_id));
 }
 __device__ __forceinline__ void keep_in_sgprs(DevRows& m) {
-    asm volatile("" : "+s"(m.n0), "+s"(m.skip), "+s"(m.magic), "+s"(m.shift));
+    asm volatile("" : "+s"(m.n0), "+s"(m.skip), "+s"(m.magic), "+s"(m.shift), "+s"(m.hi));
 }
 
 template <int kThreads, int kU>
@@ -384,14 +394,12 @@ __device__ __forceinline__ void load_tile(const TileRef& r, uint32_t raw[kU][4])
 template <int kThreads, int kU, int kM, bool kRows>
 __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU][4],
                                                const Streams& st) {
-    const uint32_t tile_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t q_hi = tile_high_word<kRows>(r);
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
-        const uint64_t n = noise_index<kRows>(r, e);
         uint32_t out[4];
-        perturb_group<kM>(raw[u], n, kRows ? static_cast<uint32_t>(n >> 34) : tile_hi,
-                          r.tensor_id, st, out);
+        perturb_group<kM>(raw[u], noise_index<kRows>(r, e), q_hi, r.tensor_id, st, out);
 #pragma unroll
         for (int k = 0; k < 4; ++k) raw[u][k] = out[k];
     }
@@ -407,16 +415,14 @@ __device__ __forceinline__ void perturb_loaded(const TileRef& r, uint32_t raw[kU
 // for whole groups of an aligned tensor, 2-byte otherwise).
 template <int kThreads, int kU, int kM, bool kRows>
 __device__ __forceinline__ void perturb_tail(const TileRef& r, const Streams& st) {
-    const uint32_t tile_hi = static_cast<uint32_t>(r.elem0 >> 34);
+    const uint32_t q_hi = tile_high_word<kRows>(r);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
         if (e >= r.limit) break;
-        const uint64_t n = noise_index<kRows>(r, e);
         uint32_t raw[4], out[4];
         load_group<false, true>(r.data, e, r.limit, raw, r.aligned16 != 0u);
-        perturb_group<kM>(raw, n, kRows ? static_cast<uint32_t>(n >> 34) : tile_hi, r.tensor_id,
-                          st, out);
+        perturb_group<kM>(raw, noise_index<kRows>(r, e), q_hi, r.tensor_id, st, out);
         store_group<false, true>(r.data, e, r.limit, out, r.aligned16 != 0u);
     }
 }
@@ -725,8 +731,8 @@ struct RoundKey {
 template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct, RoundKey rk) {
-    const uint32_t tile_q_hi = static_cast<uint32_t>(r.elem0 >> 34);
-    const uint32_t tile_g_hi = static_cast<uint32_t>(r.elem0 >> 35);
+    const uint32_t q_hi = tile_high_word<kRows>(r);
+    const uint32_t g_hi = q_hi >> 1;                     // index >> 35
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
     uint32_t next[4];
     if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.limit, next);
@@ -744,7 +750,6 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         }
         const uint64_t n = noise_index<kRows>(r, e);
         const uint32_t q_lo = static_cast<uint32_t>(n >> 2);
-        const uint32_t q_hi = kRows ? static_cast<uint32_t>(n >> 34) : tile_q_hi;
         float acc[8];
 #pragma unroll
         for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
@@ -757,7 +762,6 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         }
         uint32_t out[4];
         if constexpr (kSR) {
-            const uint32_t g_hi = kRows ? static_cast<uint32_t>(n >> 35) : tile_g_hi;
             const es::Words d = es::philox4x32_10(static_cast<uint32_t>(n >> 3), g_hi, r.tensor_id,
                                                   es::kDomainRounding, rk.k0, rk.k1);
             const uint32_t draws[4] = {d.w0, d.w1, d.w2, d.w3};
@@ -1769,6 +1773,42 @@ struct PlanTiles {
 // contiguous shard of its own.
 constexpr uint64_t kPieceElems = uint64_t(1) << 31;
 
+// Appends a tile of a strided piece with its row map, cut into tail tiles
+// where the whole-tensor index reaches a multiple of 2^34 (so that the
+// counter's high word is the tile's).  Such a multiple lies at the start of
+// a group: indices within a row are consecutive from a multiple of 8 and
+// rows start at multiples of 8.  The index is increasing in e, so each cut
+// is found by bisection over the tile's groups.
+void split_at_high_words(const DevTile& d, DevRows m, bool full, PlanTiles& t) {
+    constexpr uint64_t kHiBlock = uint64_t(1) << 34;
+    auto index = [&](uint64_t e) { return rows_index(m.n0, m.skip, m.magic, m.shift, e); };
+    uint64_t e0 = d.elem0;
+    const uint64_t hi_last = index(d.limit - 1) / kHiBlock;
+    if (index(e0) / kHiBlock == hi_last) {
+        m.hi = static_cast<uint32_t>(hi_last);
+        (full ? t.rfull : t.rtail).push_back(d);
+        (full ? t.rows_full : t.rows_tail).push_back(m);
+        return;
+    }
+    while (e0 < d.limit) {
+        const uint64_t hi = index(e0) / kHiBlock;
+        uint64_t lo_g = (e0 - d.elem0) / 8, hi_g = (d.limit - d.elem0 + 7) / 8;  // groups
+        while (lo_g + 1 < hi_g) {          // last group of [e0, ...) still on `hi`
+            const uint64_t mid = (lo_g + hi_g) / 2;
+            if (index(d.elem0 + 8 * mid) / kHiBlock == hi) lo_g = mid;
+            else hi_g = mid;
+        }
+        const uint64_t cut = std::min(d.limit, d.elem0 + 8 * hi_g);
+        DevTile part = d;
+        part.elem0 = e0;
+        part.limit = cut;
+        m.hi = static_cast<uint32_t>(hi);
+        t.rtail.push_back(part);
+        t.rows_tail.push_back(m);
+        e0 = cut;
+    }
+}
+
 // Tiles of one block (already validated).  A block that is one contiguous
 // range of its tensor is tiled as a shard at its first index.  A strided
 // block is cut into pieces of whole rows, each tiled by address with local
@@ -1792,13 +1832,15 @@ void tile_block(const es_block_t& b, uint64_t tile_elems, PlanTiles& t) {
     m.skip = static_cast<uint32_t>(b.row_len - b.cols);
     row_divisor(static_cast<uint32_t>(b.cols), m.magic, m.shift);
     const uint64_t piece_rows = kPieceElems / b.cols;
+    std::vector<DevTile> full, tail;
     for (uint64_t r = 0; r < b.rows; r += piece_rows) {
         const uint64_t nr = std::min(piece_rows, b.rows - r);
         m.n0 = n0 + r * b.row_len;
-        const size_t f0 = t.rfull.size(), t0 = t.rtail.size();
-        tile_tensor(data + r * b.cols, nr * b.cols, 0, b.tensor_id, tile_elems, t.rfull, t.rtail);
-        t.rows_full.insert(t.rows_full.end(), t.rfull.size() - f0, m);
-        t.rows_tail.insert(t.rows_tail.end(), t.rtail.size() - t0, m);
+        full.clear();
+        tail.clear();
+        tile_tensor(data + r * b.cols, nr * b.cols, 0, b.tensor_id, tile_elems, full, tail);
+        for (int k = 0; k < 2; ++k)
+            for (const DevTile& d : k == 0 ? full : tail) split_at_high_words(d, m, k == 0, t);
     }
 }
 

@@ -141,6 +141,8 @@ struct BlockCheck {
                              : e;
         check(n == expected(local), "block tiling: whole-tensor index");
         if (m) check(e < (uint64_t(1) << 31), "block tiling: piece index below 2^31");
+        // a strided tile's high word is its row map's
+        if (m) check((n >> 34) == m->hi, "block tiling: high word of a strided tile");
         // the counter's high word is taken per tile for a contiguous layout
         if (!m) check((d.elem0 >> 34) == (e >> 34), "block tiling: uniform high word");
     }
@@ -168,10 +170,10 @@ struct BlockCheck {
 
 void test_block_tiling(std::mt19937_64& rng) {
     const uint64_t tile = uint64_t(kDefaultThreads) * kDefaultGroups * kGroupElems;
-    int strided_seen = 0, row_by_row_seen = 0;
-    for (int trial = 0; trial < 240; ++trial) {
+    int strided_seen = 0, row_by_row_seen = 0, high_word_cuts = 0;
+    for (int trial = 0; trial < 280; ++trial) {
         es_block_t b{};
-        const int kind = trial % 6;
+        const int kind = trial % 7;
         if (kind == 0) {                                  // one row, any length
             b.rows = 1;
             b.cols = rng() % (3 * tile);
@@ -190,6 +192,12 @@ void test_block_tiling(std::mt19937_64& rng) {
             b.row_len = (uint64_t(1) << 32) + 8 * (rng() % 1000) + b.cols;
             b.rows = 2 + rng() % 6;
             b.row0 = rng() % 1000;
+            b.col0 = 8 * (rng() % 100);
+        } else if (kind == 6) {                           // rows just under 2^32 apart: the
+            b.cols = 8 * (1 + rng() % 8);                 // index passes a multiple of 2^34
+            b.row_len = (uint64_t(1) << 32) - 8 * (rng() % 1000);   // every ~4 rows
+            b.rows = 2 + rng() % 100;
+            b.row0 = rng() % 50;
             b.col0 = 8 * (rng() % 100);
         } else {                                          // column / 2-D shards
             b.cols = 8 * (1 + rng() % (kind == 2 ? 4 : 700));
@@ -213,6 +221,9 @@ void test_block_tiling(std::mt19937_64& rng) {
         check(!contiguous || t.rfull.empty() && t.rtail.empty(),
               "block tiling: contiguous blocks take the plain layout");
         strided_seen += !t.rfull.empty() || !t.rtail.empty();
+        for (size_t i = 1; i < t.rows_tail.size(); ++i)
+            high_word_cuts += t.rows_tail[i].hi != t.rows_tail[i - 1].hi &&
+                              t.rtail[i].elem0 == t.rtail[i - 1].limit;
         row_by_row_seen += kind == 5 && t.rfull.empty() && t.rtail.empty() && !t.tail.empty();
         const uint64_t numel = b.rows * b.cols;
         std::vector<uint8_t> cover(numel, 0);
@@ -225,7 +236,8 @@ void test_block_tiling(std::mt19937_64& rng) {
         for (uint8_t k : cover) once &= (k == 1);
         check(once, "block tiling: every element in exactly one tile");
     }
-    check(strided_seen > 100 && row_by_row_seen > 20, "block tiling: every layout exercised");
+    check(strided_seen > 100 && row_by_row_seen > 20 && high_word_cuts > 200,
+          "block tiling: every layout exercised");
 
     // a block of more than 2^31 elements is cut into pieces of whole rows:
     // sampled elements of every tile, and the tiles' sizes add up

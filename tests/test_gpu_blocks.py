@@ -156,21 +156,24 @@ def test_block_checksums_add_up_to_the_whole_matrix():
     assert total == whole
 
 
-def _oracle_chain(x0, el, r):
-    """The oracle's results of the passes below at whole-tensor indices el."""
+def _oracle_steps(xs, el, r):
+    """Each pass below checked on its own: the oracle applied to the GPU's
+    state before the pass (xs[k - 1]) at whole-tensor indices el, so that a
+    legitimate 1-ulp tie of one pass is not carried into the next one's
+    expected values."""
     upd = update_delta(TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, 0, el)
-    x1 = oracle.perturb(x0, 11, TID, -1, 1e-3, elems=el)
-    x2 = oracle.swap(x1, TID, 11, -1, 1e-3, 12, 1, 1e-3, elems=el)
-    x3 = oracle.restore(x2, 12, TID, 1, 1e-3, elems=el)
-    x4 = oracle.update(x3, TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el)[0]
-    x5 = oracle.update(x4, TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el,
-                       flags=esopt.ES_UPDATE_STOCHASTIC_ROUND, round_seed=(1 << 63) + 9)[0]
     return [
-        ("perturb", x1, x0, perturb_delta(11, TID, -1, 1e-3, el)),
-        ("swap", x2, x1, perturb_delta(11, TID, 1, 1e-3, el) + perturb_delta(12, TID, 1, 1e-3, el)),
-        ("restore", x3, x2, perturb_delta(12, TID, -1, 1e-3, el)),
-        ("update", x4, x3, upd),
-        ("update_sr", x5, x4, upd),
+        ("perturb", oracle.perturb(xs[0], 11, TID, -1, 1e-3, elems=el), xs[0],
+         perturb_delta(11, TID, -1, 1e-3, el)),
+        ("swap", oracle.swap(xs[1], TID, 11, -1, 1e-3, 12, 1, 1e-3, elems=el), xs[1],
+         perturb_delta(11, TID, 1, 1e-3, el) + perturb_delta(12, TID, 1, 1e-3, el)),
+        ("restore", oracle.restore(xs[2], 12, TID, 1, 1e-3, elems=el), xs[2],
+         perturb_delta(12, TID, -1, 1e-3, el)),
+        ("update", oracle.update(xs[3], TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el)[0],
+         xs[3], upd),
+        ("update_sr", oracle.update(xs[4], TID, [3, 4, 5], [1, 1, 1], r, 5e-4, 1e-3, elems=el,
+                                    flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+                                    round_seed=(1 << 63) + 9)[0], xs[4], upd),
     ]
 
 
@@ -216,10 +219,37 @@ def test_block_matches_oracle_at_whole_tensor_indices_across_2_34(pad):
     with esopt.Plan(blocks=[esopt.Block(blk, TID, row_len, row0, col0)]) as p:
         (xs,) = _run_chain(p, [blk], r)
     assert torch.count_nonzero(buf[:pad].float()) == 0
-    for (name, exp, base, delta), got in zip(_oracle_chain(x0, el, r), xs[1:]):
+    for (name, exp, base, delta), got in zip(_oracle_steps(xs, el, r), xs[1:]):
         rep = report(got, exp, base, delta)
         print(f"block across 2^34 (pad {pad}):", name, rep)
         assert_parity(rep, name)
+
+
+def test_block_whose_rows_pass_many_multiples_of_2_34():
+    """Rows just under 2^32 elements apart: the whole-tensor index passes a
+    multiple of 2^34 every four rows, so the block's tiles are cut there (the
+    counter's high word is per tile); every pass and the checksum match the
+    oracle element by element."""
+    row_len = (1 << 32) - 64
+    rows, cols, row0, col0 = 96, 64, 5, 128
+    el = _block_indices(rows, cols, row_len, row0, col0)
+    assert len(np.unique(el >> np.uint64(34))) > 20
+    x0 = wl.random_bf16_bits(rows * cols, 70)
+    r = np.array([0.6, 0.1, 0.9], np.float32)
+    blk = to_device(x0, (rows, cols))
+    with esopt.Plan(blocks=[esopt.Block(blk, TID, row_len, row0, col0)]) as p:
+        assert p.tiles > 20
+        (xs,) = _run_chain(p, [blk], r)
+        got_sum = p.checksum()
+    for (name, exp, base, delta), got in zip(_oracle_steps(xs, el, r), xs[1:]):
+        rep = report(got, exp, base, delta)
+        print("rows 2^32 apart:", name, rep)
+        assert_parity(rep, name)
+    host = xs[-1].reshape(rows, cols)
+    exp_sum = 0
+    for i in range(rows):
+        exp_sum = (exp_sum + oracle.checksum(host[i], TID, (row0 + i) * row_len + col0)) & M64
+    assert got_sum == exp_sum
 
 
 def test_large_block_in_two_row_pieces():
