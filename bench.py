@@ -569,8 +569,8 @@ def main():
 
     def run_step(t, record, swap):
         """One generation's parameter work: every member applied and reverted
-        (separate passes, or perturb, N - 1 fused swaps and restore), then the
-        fused update."""
+        (separate passes, then the fused update; or perturb, N - 1 fused swaps,
+        and the last member's revert fused into the update)."""
         seeds = step_seeds(W, t, n_members)
         sigma = sigma_at(esopt.sigma_cosine, W, t)
         if swap:
@@ -578,13 +578,16 @@ def main():
             for i in range(N - 1):
                 log.call("es_swap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
                          signs[i + 1], sigma)
-            log.call("es_restore", record, plan.restore, seeds[-1], signs[-1], sigma)
+            log.call("es_restore_update", record, plan.restore_update, seeds[-1], signs[-1],
+                     sigma, seeds, signs, rewards_all[t], W.alpha, sigma=sigma,
+                     flags=update_flags, round_seed=1000 + t)
+            return
         else:
             for sd, sg in zip(seeds, signs):
                 log.call("es_perturb", record, plan.perturb, sd, sg, sigma)
                 log.call("es_restore", record, plan.restore, sd, sg, sigma)
-        log.call("es_update_swap" if swap else "es_update", record, plan.update, seeds, signs,
-                 rewards_all[t], W.alpha, sigma=sigma, flags=update_flags, round_seed=1000 + t)
+        log.call("es_update", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
+                 sigma=sigma, flags=update_flags, round_seed=1000 + t)
 
     for t in range(args.warmup):
         run_step(t, record=False, swap=False)
@@ -599,8 +602,8 @@ def main():
                             for t in range(args.warmup, total_steps)]))
 
     # the same generations with the members moved by fused swaps (perturb,
-    # N - 1 swaps, restore, update), timed in the same run after one untimed
-    # generation
+    # N - 1 swaps, the last revert and the update in one pass), timed in the
+    # same run after one untimed generation
     swap = None
     if not args.no_swap_walk and N > 1:
         log.ev = []
@@ -609,7 +612,8 @@ def main():
             torch, stream, args.steps, lambda i: run_step(args.warmup + i, record=True, swap=True))
         per_sw = log.ms()
         swap = {"ms_step": ms_swap, "wall": wall_swap, "t_swap": median_s(per_sw["es_swap"]),
-                "calls": len(per_sw["es_swap"])}
+                "calls": len(per_sw["es_swap"]),
+                "t_restore_update": median_s(per_sw["es_restore_update"])}
 
     # the practical in-place streaming ceiling over the same memory: the same
     # tiles and launch, loads and stores only, not pipelined (es_stream_pass),
@@ -688,8 +692,12 @@ def main():
                                  "GBps_algorithmic": round(4 * P / t_sw / 1e9, 1),
                                  "normals_per_s": 2 * P / t_sw, "calls": swap["calls"]}
         out["ms_per_step_swap"] = round(swap["ms_step"], 3)
+        per_kernel["es_restore_update"] = {
+            "ms": round(swap["t_restore_update"] * 1e3, 3),
+            "ms_over_update": round(swap["t_restore_update"] / t_upd, 4)}
         out["swap_walk"] = {
-            "member_moves": "es_perturb, N-1 fused es_swap, es_restore",
+            "member_moves": "es_perturb, N-1 fused es_swap, then the last revert and the update "
+                            "in one pass (es_restore_update)",
             "ms_per_step": round(swap["ms_step"], 3),
             "speedup_vs_perturb_restore": round(ms_step / swap["ms_step"], 4),
             "wall_s_timed": round(swap["wall"], 3),
@@ -803,6 +811,9 @@ def run_profile_pass(args):
     log.add(f"es_update (N={N}, stochastic rounding)", "update", P, 4 * P, nd * P, plan.update,
             seeds, signs, rewards, W.alpha, sigma=s0, flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
             round_seed=1, repeat=R)
+    log.add(f"es_restore_update (N={N}, nearest-even; the last member reverted in the pass)",
+            "update", P, 4 * P, nd * P, plan.restore_update, seeds[-1], signs[-1], s0, seeds,
+            signs, rewards, W.alpha, sigma=s0, repeat=R)
     log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
             plan.stream_pass, repeat=R)
     out = torch.zeros(1, dtype=torch.int64, device="cuda")
@@ -824,6 +835,12 @@ def run_profile_pass(args):
                                k * w) for k in range(8)]
     bplan = esopt.Plan(blocks=blocks)
     PB = bplan.numel
+    # the first launches of a new plan and kernel run cold (left out of the
+    # summaries, as above)
+    log.add("warm-up perturb (column blocks)", "warmup", PB, 4 * PB, PB, bplan.perturb, seeds[0],
+            signs[0], s0)
+    log.add("warm-up restore (column blocks)", "warmup", PB, 4 * PB, PB, bplan.restore, seeds[0],
+            signs[0], s0)
     for _ in range(R):
         log.add("es_perturb (column blocks)", "blocks", PB, 4 * PB, PB, bplan.perturb, seeds[0],
                 signs[0], s0)

@@ -249,6 +249,26 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
               const es_update_opts_t* opts, float* z_out_dev,
               int32_t* status_out_dev, es_stream_t stream);
 
+/* The last member's revert and the update in one pass (Section 3; Appendix
+ * D.6: after the last member is evaluated its perturbation is reverted, then
+ * the update regenerates every member's noise).  The same bits as
+ *   es_restore(plan, restore_seed, restore_sign, restore_sigma, stream);
+ *   es_update(plan, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
+ *             status_out_dev, stream);
+ * theta is read and written once instead of twice: the restored member's
+ * noise is generated once per element for both (its seed must be one of
+ * `seeds`, else INVALID_ARG), the revert is rounded to bf16 in registers
+ * exactly as es_restore rounds it, and the update is added to the result.
+ * When the update adds nothing (no nonzero weight, or a non-finite reward:
+ * status word 1) the reverted values are stored, as the two calls would
+ * leave them.  restore_sign is +1 or -1, restore_sigma finite and >= 0
+ * (0: the call is es_update).  Other arguments and errors as es_update. */
+int es_restore_update(es_plan_t* plan, uint64_t restore_seed, int32_t restore_sign,
+                      float restore_sigma, const uint64_t* seeds, const int32_t* signs,
+                      const float* rewards_dev, uint32_t n_members,
+                      const es_update_opts_t* opts, float* z_out_dev,
+                      int32_t* status_out_dev, es_stream_t stream);
+
 /* es_update for callers that cannot allocate (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the same
  * arguments, checks, results and errors as es_update, bit for bit, but the

@@ -44,6 +44,11 @@
 //   * Tail tiles take a bounds-checked path with identical arithmetic:
 //     16-byte accesses for whole groups of an aligned tensor, 2-byte accesses
 //     for a partial group or an unaligned tensor.
+//   * Blocks of row-major tensors that are not one contiguous range (column
+//     shards) are tiled by address like tensors; their tiles carry a row map
+//     from the element's place in the block to its whole-tensor index, the
+//     noise index, and run in a second launch of the same kernels
+//     instantiated with it (kRows).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -79,13 +84,16 @@ constexpr int kDefaultUpdateWgPerCu = 8;
 constexpr int kDefaultQGroups = 4;          // int8 tiles: 1024 x 4 x 16 codes (64 KB)
 constexpr double kSqrt2Ln2Double = 1.1774100225154746910;   // sqrt(2 ln 2)
 
-// Tile descriptor.  A plan lists its tiles in two runs, indexed by tile
-// number: full tiles first (kThreads * kU * 8 elements of one tensor, starting
-// on a tile-sized boundary of the address space), then tail tiles (the part
-// of a tensor before its first such boundary, the part after its last full
-// tile, or every tile of a tensor whose base is not 16-byte aligned).  A
-// workgroup reads one descriptor per tile with a single scalar load and no
-// search (searching a per-tensor table is a chain of dependent scalar loads).
+// Tile descriptor.  A plan lists its tiles in runs, indexed by tile number:
+// full tiles first (kThreads * kU * 8 elements of one tensor, starting on a
+// tile-sized boundary of the address space), then tail tiles (the part of a
+// tensor before its first such boundary, the part after its last full tile,
+// or every tile of a tensor whose base is not 16-byte aligned); the tiles of
+// strided blocks (es_plan_create_blocks) follow in two more runs of the same
+// kinds, each with a row map (DevRows), and are passed over in a second
+// launch.  A workgroup reads one descriptor per tile with a single scalar
+// load and no search (searching a per-tensor table is a chain of dependent
+// scalar loads).
 // Full tiles aligned to the address space, not to their tensor's base: with
 // hundreds of tensors at unrelated offsets, tiles at mixed offsets streamed
 // ~4 % slower.  32 bytes per 65 536-element tile.
@@ -728,9 +736,39 @@ struct RoundKey {
     uint32_t k0, k1;
 };
 
-template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows>
+// The member reverted in the same pass as an update (es_restore_update): its
+// entry in the distinct-seed table and coef * sqrt(2 ln 2), coef = -sign sigma.
+struct RestoreArg {
+    uint32_t d;
+    float coef_k;
+};
+
+// The restore of one member on a group in registers, theta <- RNE(theta +
+// coef eps), exactly as the perturb kernel computes it (group_axpy on the
+// binary32 values, then RNE).  The member's update term is added by the
+// member loop's own group_axpy from the same words, so the loop keeps one
+// accumulation path (two paths merging into the accumulators cost register
+// moves on every member); the Box-Muller transcendentals of this one member
+// are evaluated twice.
+__device__ __forceinline__ void restore_group(const uint32_t w[8], float coef_k, uint32_t raw[4]) {
+    float x[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        x[2 * k] = es::bf16_lo(raw[k]);
+        x[2 * k + 1] = es::bf16_hi(raw[k]);
+    }
+    group_axpy(w, coef_k, x);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) raw[k] = es::pack_bf16x2(x[2 * k], x[2 * k + 1]);
+}
+
+// kRestore: one member (rst) is reverted first, in registers, and the update
+// is added to the reverted values; with no live weight (add == false) the
+// reverted values are stored as they are, as es_update would then leave them.
+template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows, bool kRestore>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
-                                            uint32_t n_distinct, RoundKey rk) {
+                                            uint32_t n_distinct, RoundKey rk, RestoreArg rst,
+                                            bool add) {
     const uint32_t q_hi = tile_high_word<kRows>(r);
     const uint32_t g_hi = q_hi >> 1;                     // index >> 35
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
@@ -755,13 +793,25 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
         for (uint32_t d = 0; d < n_distinct; ++d) {
             const Member m = members[d];
-            if (is_zero_weight(m.w_k)) continue;
+            const bool live = !is_zero_weight(m.w_k);
+            if constexpr (kRestore) {
+                if (!live && d != rst.d) continue;
+            } else {
+                if (!live) continue;
+            }
             uint32_t w[8];
             group_words(q_lo, q_hi, r.tensor_id, m.k0, m.k1, w);
+            if constexpr (kRestore) {
+                if (d == rst.d) restore_group(w, rst.coef_k, raw);
+                if (!live) continue;
+            }
             group_axpy(w, m.w_k, acc);
         }
         uint32_t out[4];
-        if constexpr (kSR) {
+        if (kRestore && !add) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) out[k] = raw[k];
+        } else if constexpr (kSR) {
             const es::Words d = es::philox4x32_10(static_cast<uint32_t>(n >> 3), g_hi, r.tensor_id,
                                                   es::kDomainRounding, rk.k0, rk.k1);
             const uint32_t draws[4] = {d.w0, d.w1, d.w2, d.w3};
@@ -781,22 +831,24 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
 
 // Fused update over the whole parameter list (member table and header
 // written by es_prepare_kernel): full tiles, then tail tiles; with kRows the
-// tiles of strided blocks, through their row maps.
-template <int kThreads, int kU, bool kNT, bool kSR, bool kRows>
+// tiles of strided blocks, through their row maps; with kRestore the member
+// rst reverted in the same pass.
+template <int kThreads, int kU, bool kNT, bool kSR, bool kRows, bool kRestore>
 __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              const DevRows* __restrict__ rows,
                                                              const Member* __restrict__ members,
                                                              const UpdateHeader* __restrict__ hdr,
-                                                             RoundKey rk) {
-    if (hdr->n_live == 0u) return;          // nothing to add: theta is not written
+                                                             RoundKey rk, RestoreArg rst) {
+    const bool add = hdr->n_live != 0u;
+    if (!kRestore && !add) return;          // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        update_tile<kThreads, kU, true, kNT, kSR, kRows>(load_ref<kRows>(tiles, rows, tile),
-                                                         members, n_distinct, rk);
+        update_tile<kThreads, kU, true, kNT, kSR, kRows, kRestore>(
+            load_ref<kRows>(tiles, rows, tile), members, n_distinct, rk, rst, add);
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        update_tile<kThreads, kU, false, kNT, kSR, kRows>(
-            load_ref<kRows>(tiles, rows, n_full + tile), members, n_distinct, rk);
+        update_tile<kThreads, kU, false, kNT, kSR, kRows, kRestore>(
+            load_ref<kRows>(tiles, rows, n_full + tile), members, n_distinct, rk, rst, add);
 }
 
 // The scratch of es_update_noalloc: one update's staged member tables, merged
@@ -949,7 +1001,7 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
 
 using PerturbKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, Streams);
 using UpdateKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, const Member*,
-                              const UpdateHeader*, RoundKey);
+                              const UpdateHeader*, RoundKey, RestoreArg);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
 #define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
@@ -997,18 +1049,26 @@ PerturbKernel perturb_kernel(int streams, int threads, int groups, bool rows) {
     }
 }
 
-UpdateKernel update_kernel(int threads, int groups, bool stochastic, bool rows) {
+template <bool kRestore>
+UpdateKernel update_kernel_for(int threads, int groups, bool stochastic, bool rows) {
 #define ES_CASE(T, U)                                                                     \
     if (threads == T && groups == U) {                                                    \
         if (rows)                                                                         \
-            return stochastic ? es_update_kernel<T, U, true, true, true>                  \
-                              : es_update_kernel<T, U, true, false, true>;                \
-        return stochastic ? es_update_kernel<T, U, true, true, false>                     \
-                          : es_update_kernel<T, U, true, false, false>;                   \
+            return stochastic ? es_update_kernel<T, U, true, true, true, kRestore>        \
+                              : es_update_kernel<T, U, true, false, true, kRestore>;      \
+        return stochastic ? es_update_kernel<T, U, true, true, false, kRestore>           \
+                          : es_update_kernel<T, U, true, false, false, kRestore>;         \
     }
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
+}
+
+// restore: the update with one member reverted in the same pass.
+UpdateKernel update_kernel(int threads, int groups, bool stochastic, bool rows,
+                           bool restore = false) {
+    return restore ? update_kernel_for<true>(threads, groups, stochastic, rows)
+                   : update_kernel_for<false>(threads, groups, stochastic, rows);
 }
 
 // ---- int8 path (device code of the passes; helpers in es_quant.hpp) ----
@@ -1664,13 +1724,24 @@ void build_member_tables(const uint64_t* seeds, const int32_t* signs, uint32_t n
 // Hand the population to the device: the member tables are staged into the
 // scratch through kernel arguments, then one wave z-scores the rewards and
 // merges the weights per distinct seed, leaving the weighted member table
-// and its header in the scratch.  Allocates nothing.
+// and its header in the scratch.  Allocates nothing.  With `find`, *found is
+// set to the distinct-table entry of seed *find before anything is launched
+// (or the call fails with INVALID_ARG when no member has that seed).
 int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* signs,
                    const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
-                   float* z_out_dev, int32_t* status_out_dev, hipStream_t s) {
+                   float* z_out_dev, int32_t* status_out_dev, hipStream_t s,
+                   const uint64_t* find = nullptr, uint32_t* found = nullptr) {
     MemberTables t;
     build_member_tables(seeds, signs, n_members, t);
     const uint32_t nd = t.n_distinct;
+    if (find != nullptr) {
+        uint32_t d = 0;
+        while (d < nd && (uint64_t(t.din[d].k0) | (uint64_t(t.din[d].k1) << 32)) != *find) ++d;
+        if (d == nd)
+            return fail(ES_ERR_INVALID_ARG,
+                        "es_restore_update: the restored member's seed is not among the seeds");
+        *found = d;
+    }
 
     // 1 KB of kernel arguments per staging launch
     auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
@@ -1705,15 +1776,25 @@ int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* sig
     return ES_OK;
 }
 
+// The member es_restore_update reverts: its seed and the perturbation
+// coefficient es_restore would apply (-sign sigma).
+struct RestoreMember {
+    uint64_t seed;
+    double coef;
+};
+
 // The fused update of a bf16 plan with its member tables in `d_scratch`
-// (the plan's, or the static array of es_update_noalloc).
+// (the plan's, or the static array of es_update_noalloc); with `restore`,
+// that member reverted in the same pass.
 int update_impl(const char* name, es_plan_t* plan, uint8_t* d_scratch, const uint64_t* seeds,
                 const int32_t* signs, const float* rewards_dev, uint32_t n_members,
                 const es_update_opts_t* opts, float* z_out_dev, int32_t* status_out_dev,
-                hipStream_t s) {
+                hipStream_t s, const RestoreMember* restore = nullptr) {
+    RestoreArg rst{0u, 0.0f};
     int rc = prepare_update(d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
-                            status_out_dev, s);
+                            status_out_dev, s, restore ? &restore->seed : nullptr, &rst.d);
     if (rc != ES_OK) return rc;
+    if (restore) rst.coef_k = static_cast<float>(restore->coef * kSqrt2Ln2Double);
     const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
     const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
                       static_cast<uint32_t>(opts->round_seed >> 32)};
@@ -1721,11 +1802,13 @@ int update_impl(const char* name, es_plan_t* plan, uint8_t* d_scratch, const uin
     const int n_seg = plan_segments(plan, seg);
     for (int k = 0; k < n_seg; ++k) {
         const Segment& g = seg[k];
-        const UpdateKernel kernel = update_kernel(plan->threads, plan->groups, sr, g.rows != nullptr);
+        const UpdateKernel kernel =
+            update_kernel(plan->threads, plan->groups, sr, g.rows != nullptr, restore != nullptr);
         hipLaunchKernelGGL(kernel, dim3(g.grid_update), dim3(plan->threads), 0, s, g.tiles,
                            g.n_full, g.n_tail, g.rows,
                            reinterpret_cast<const Member*>(d_scratch + kOffMembers),
-                           reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk);
+                           reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk,
+                           rst);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, std::string(name) + ": es_update_kernel launch");
     }
@@ -2095,6 +2178,33 @@ int es_update(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,
                        opts, z_out_dev, status_out_dev, static_cast<hipStream_t>(stream));
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_update: host allocation failed");
+}
+
+int es_restore_update(es_plan_t* plan, uint64_t restore_seed, int32_t restore_sign,
+                      float restore_sigma, const uint64_t* seeds, const int32_t* signs,
+                      const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
+                      float* z_out_dev, int32_t* status_out_dev, es_stream_t stream) try {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_restore_update: null plan");
+    if (restore_sign != 1 && restore_sign != -1)
+        return fail(ES_ERR_INVALID_ARG, "es_restore_update: restore_sign must be +1 or -1");
+    if (!std::isfinite(restore_sigma) || restore_sigma < 0.0f)
+        return fail(ES_ERR_INVALID_ARG,
+                    "es_restore_update: restore_sigma must be finite and >= 0");
+    int rc = validate_update("es_restore_update", seeds, signs, rewards_dev, n_members, opts);
+    if (rc != ES_OK) return rc;
+    rc = check_device(plan);
+    if (rc == ES_OK)
+        rc = check_update_arrays("es_restore_update", plan->device, rewards_dev, n_members,
+                                 z_out_dev, status_out_dev);
+    if (rc != ES_OK) return rc;
+    // es_restore with sigma 0 changes nothing: the update alone, as es_update
+    const RestoreMember rm{restore_seed, restore_sign > 0 ? -double(restore_sigma)
+                                                          : double(restore_sigma)};
+    return update_impl("es_restore_update", plan, plan->d_scratch, seeds, signs, rewards_dev,
+                       n_members, opts, z_out_dev, status_out_dev,
+                       static_cast<hipStream_t>(stream), restore_sigma != 0.0f ? &rm : nullptr);
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_restore_update: host allocation failed");
 }
 
 int es_update_noalloc(es_plan_t* plan, const uint64_t* seeds, const int32_t* signs,

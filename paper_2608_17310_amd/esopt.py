@@ -80,6 +80,9 @@ SIGNATURES = {
                                  ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
     "es_update_noalloc": (ctypes.c_int, [_vp, ctypes.POINTER(_u64), ctypes.POINTER(_i32), _vp,
                                          _u32, ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
+    "es_restore_update": (ctypes.c_int, [_vp, _u64, _i32, _f32, ctypes.POINTER(_u64),
+                                         ctypes.POINTER(_i32), _vp, _u32,
+                                         ctypes.POINTER(EsUpdateOpts), _vp, _vp, _vp]),
     "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
     "es_qplan_create_format": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, _u32,
                                               ctypes.POINTER(_vp)]),
@@ -315,6 +318,20 @@ class Plan:
         round_seed keys the draws of ES_UPDATE_STOCHASTIC_ROUND."""
         _call_update(load().es_update, "es_update", self.handle, seeds, signs, rewards, alpha,
                      sigma, zscore_eps, flags, z_out, status_out, stream, round_seed)
+
+    def restore_update(self, restore_seed, restore_sign, restore_sigma, seeds, signs, rewards,
+                       alpha, sigma=0.0, zscore_eps=1e-8, flags=0, z_out=None, status_out=None,
+                       stream=None, round_seed=0):
+        """restore(restore_seed, restore_sign, restore_sigma) followed by
+        update(seeds, ...), the same bits in one pass (es_restore_update);
+        the restored seed must be one of `seeds`."""
+        rs, rsign, rsig = _u64_arg(restore_seed, "restore_seed"), int(restore_sign), \
+            float(restore_sigma)
+
+        def fn(handle, *rest):
+            return load().es_restore_update(handle, rs, rsign, rsig, *rest)
+        _call_update(fn, "es_restore_update", self.handle, seeds, signs, rewards, alpha, sigma,
+                     zscore_eps, flags, z_out, status_out, stream, round_seed)
 
     def update_noalloc(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                        z_out=None, status_out=None, stream=None, round_seed=0):

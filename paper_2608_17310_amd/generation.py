@@ -7,9 +7,11 @@ population apply the z-scored, reward-weighted update with each eps_i
 regenerated from its seed; Section 3.1 sets sigma_t on a cosine schedule.
 
 With fused_swap the revert of member i and the apply of member i+1 are one
-pass (es_swap), so a generation of N members makes N + 1 passes over the
-parameters instead of 2N, plus the update.  The same driver runs the
-quantized paths (esopt.QPlan, int8 or E4M3 codes), which have no fused swap.
+pass (es_swap), and the last member's revert is made in the update's pass
+(es_restore_update), so a generation of N members makes N passes over the
+parameters instead of 2N, plus the update; the bits are those of the
+separate passes.  The same driver runs the quantized paths (esopt.QPlan, int8
+or E4M3 codes), which have no fused passes.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
@@ -84,8 +86,15 @@ def antithetic_seeds(base_seed, n_pairs):
     return seeds, signs
 
 
-def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
-    """Apply member 0, visit it, move to member 1, ... and revert the last.
+def _fuses_last_revert(plan, fused_swap):
+    """Whether the walk leaves the last member applied for the update to
+    revert in its own pass (es_restore_update)."""
+    return fused_swap and hasattr(plan, "restore_update")
+
+
+def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream, revert_last=True):
+    """Apply member 0, visit it, move to member 1, ... and revert the last
+    (unless revert_last is false: the update then reverts it).
     Plans without a fused swap (the quantized QPlan) revert and apply separately.
     When the passes run on a stream other than PyTorch's current one, each
     visit is ordered after its member's pass and the next pass after the
@@ -105,10 +114,11 @@ def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream):
             s.wait_stream(cur)
         if i + 1 < n and fused_swap:
             plan.swap(seeds[i], signs[i], seeds[i + 1], signs[i + 1], sigma, stream=s)
-        else:
+        elif i + 1 < n:
             plan.restore(seeds[i], signs[i], sigma, stream=s)
-            if i + 1 < n:
-                plan.perturb(seeds[i + 1], signs[i + 1], sigma, stream=s)
+            plan.perturb(seeds[i + 1], signs[i + 1], sigma, stream=s)
+        elif revert_last:
+            plan.restore(seeds[i], signs[i], sigma, stream=s)
 
 
 def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], float],
@@ -126,13 +136,14 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
     if checksum and not hasattr(plan, "checksum"):
         raise ValueError("this plan has no checksum")
     rewards = []
+    fuse = _fuses_last_revert(plan, fused_swap)
     _walk(plan, seeds, signs, sigma, fused_swap, lambda i: rewards.append(float(evaluate(i))),
-          stream)
+          stream, revert_last=not fuse)
     rec = GenerationRecord(list(map(int, seeds)), list(map(int, signs)),
                            [float(torch.tensor(r, dtype=torch.float32)) for r in rewards],
                            float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap,
                            int(round_seed))
-    apply_update(plan, rec, stream)
+    apply_update(plan, rec, stream, revert_last=fuse)
     if checksum:
         rec.checksum = plan.checksum(stream=stream)
     return rec
@@ -146,16 +157,22 @@ def _torch_stream(stream, device):
     return torch.cuda.ExternalStream(int(stream), device=device)
 
 
-def apply_update(plan, rec: GenerationRecord, stream=None):
+def apply_update(plan, rec: GenerationRecord, stream=None, revert_last=False):
+    """The record's update; with revert_last, the last member (left applied
+    by the walk) is reverted in the same pass (es_restore_update)."""
     # the rewards are staged on the stream the update runs on, so PyTorch's
     # caching allocator does not hand their memory out again before the
     # update has read it
     s = _torch_stream(stream, plan.device)
     with torch.cuda.stream(s):
         r = torch.tensor(rec.rewards, dtype=torch.float32, device=plan.device)
-        plan.update(rec.seeds, rec.signs, r, rec.alpha, sigma=rec.sigma,
-                    zscore_eps=rec.zscore_eps, flags=rec.flags, stream=s,
-                    round_seed=rec.round_seed)
+        kw = dict(sigma=rec.sigma, zscore_eps=rec.zscore_eps, flags=rec.flags, stream=s,
+                  round_seed=rec.round_seed)
+        if revert_last:
+            plan.restore_update(rec.seeds[-1], rec.signs[-1], rec.sigma, rec.seeds, rec.signs,
+                                r, rec.alpha, **kw)
+        else:
+            plan.update(rec.seeds, rec.signs, r, rec.alpha, **kw)
 
 
 class ReplayMismatch(RuntimeError):
@@ -171,9 +188,11 @@ def replay(plan, records, with_perturbations=True, stream=None, verify=True):
     perturbations only: without them the bits differ by design), raising
     ReplayMismatch at the first generation that differs."""
     for g, rec in enumerate(records):
+        fuse = with_perturbations and _fuses_last_revert(plan, rec.fused_swap)
         if with_perturbations:
-            _walk(plan, rec.seeds, rec.signs, rec.sigma, rec.fused_swap, lambda i: None, stream)
-        apply_update(plan, rec, stream)
+            _walk(plan, rec.seeds, rec.signs, rec.sigma, rec.fused_swap, lambda i: None, stream,
+                  revert_last=not fuse)
+        apply_update(plan, rec, stream, revert_last=fuse)
         if verify and with_perturbations and rec.checksum is not None:
             got = plan.checksum(stream=stream)
             if got != rec.checksum:

@@ -127,7 +127,10 @@ def test_call_validation_without_device(lib):
     signs = (ctypes.c_int32 * 2)(1, 1)
     bad_signs = (ctypes.c_int32 * 2)(1, 0)
     opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0)
-    for U, name in ((lib.es_update, "es_update"), (lib.es_update_noalloc, "es_update_noalloc")):
+    def RU(plan, *rest):                     # es_restore_update, reverting member (1, +1)
+        return lib.es_restore_update(plan, 1, 1, 1e-3, *rest)
+    for U, name in ((lib.es_update, "es_update"), (lib.es_update_noalloc, "es_update_noalloc"),
+                    (RU, "es_restore_update")):
         assert U(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
         assert U(fake, seeds, signs, fake, 0, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
         assert U(fake, seeds, signs, fake, 1025, ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
@@ -138,6 +141,9 @@ def test_call_validation_without_device(lib):
                   esopt.EsUpdateOpts(5e-4, 1e-3, -1.0, 0),
                   esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8)]:
             assert U(fake, seeds, signs, fake, 2, ctypes.byref(o), None, None, None) == esopt.ES_ERR_INVALID_ARG
+    for sign, sigma in ((0, 1e-3), (2, 1e-3), (1, float("nan")), (1, -1e-3)):
+        assert lib.es_restore_update(fake, 1, sign, sigma, seeds, signs, fake, 2,
+                                     ctypes.byref(opts), None, None, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_philox_words(1, 0, 0, 0, 4, None, None) == esopt.ES_ERR_INVALID_ARG
     assert lib.es_philox_words(1, 0, 0, 0, 4, ctypes.c_void_p(0x1004), None) == esopt.ES_ERR_ALIGN
     assert lib.es_philox_words(1, 0, 0, 0, 1 << 29, fake, None) == esopt.ES_ERR_INVALID_ARG

@@ -308,3 +308,33 @@ def test_block_geometry_is_validated():
         esopt.Plan(blocks=[esopt.Block(t, 0, 256)], tensor_ids=[0])
     with pytest.raises(ValueError):
         esopt.Plan(blocks=[esopt.Block(t.t(), 0, 256)])     # not contiguous
+
+
+def test_random_block_grids_match_the_whole_matrix():
+    """Random matrices cut into random grids of blocks (row cuts anywhere,
+    column cuts at multiples of 8, blocks copied to random sub-16-byte and
+    larger offsets), each block through a plan of its own: every block
+    bit-identical to the same block of the whole-matrix pass."""
+    rng = np.random.default_rng(2026)
+    for case in range(12):
+        rows = int(rng.integers(1, 700))
+        cols = 8 * int(rng.integers(1, 900))
+        bits = wl.random_bf16_bits(rows * cols, 500 + case)
+        whole = _whole(bits, rows, cols)
+        src = to_device(bits, (rows, cols))
+        rc = sorted(set([0, rows] + [int(x) for x in rng.integers(0, rows, int(rng.integers(0, 4)))]))
+        cc = sorted(set([0, cols] + [8 * int(x) for x in rng.integers(0, cols // 8,
+                                                                      int(rng.integers(0, 5)))]))
+        for r0, r1 in zip(rc, rc[1:]):
+            for c0, c1 in zip(cc, cc[1:]):
+                pad = int(rng.choice([0, 1, 3, 8, 13, 64, 4096 + 5]))
+                buf, blk = _block_buffer(src[r0:r1, c0:c1].contiguous(), pad)
+                with esopt.Plan(blocks=[esopt.Block(blk, TID, cols, r0, c0)]) as p:
+                    _passes(p, _rewards())
+                torch.cuda.synchronize()
+                assert torch.equal(blk.view(torch.int16),
+                                   whole[r0:r1, c0:c1].view(torch.int16)), \
+                    f"case {case}: [{rows}, {cols}] block rows [{r0}, {r1}) cols [{c0}, {c1}) pad {pad}"
+                n = (r1 - r0) * (c1 - c0)
+                assert torch.count_nonzero(buf[:pad].float()) == 0
+                assert torch.count_nonzero(buf[pad + n:].float()) == 0

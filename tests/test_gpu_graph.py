@@ -89,3 +89,42 @@ def test_captured_int8_passes_replay_like_eager_calls():
             assert torch.equal(a, b)
     plan.close()
     plan_twin.close()
+
+
+def test_captured_block_passes_replay_like_eager_calls():
+    """A plan holding a strided column block and a whole vector runs every
+    pass as two launches (plain tiles, then the tiles with row maps); both
+    are captured, and the checksum's two accumulating launches too."""
+    a_bits = wl.random_bf16_bits(96 * 1024, 310)
+    v_bits = wl.random_bf16_bits(5000, 311)
+
+    def make():
+        a = to_device(a_bits, (96, 1024))[:, 256:512].contiguous()
+        v = to_device(v_bits)
+        return [a, v], esopt.Plan(blocks=[esopt.Block(a, 1, 1024, 0, 256),
+                                          esopt.Block(v, 2, 5000)])
+    live, plan = make()
+    twin, plan_twin = make()
+    rewards = torch.tensor([0.3, 0.9, 0.1, 0.6], device="cuda")
+    z_live = torch.zeros(4, device="cuda")
+    z_twin = torch.zeros(4, device="cuda")
+    c_live = torch.zeros(1, dtype=torch.int64, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        _calls(plan, rewards, z_live)
+        plan.checksum(out=c_live, stream=s)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        _calls(plan_twin, rewards, z_twin)
+        c_twin = plan_twin.checksum()
+        torch.cuda.synchronize()
+        for a, b in zip(live, twin):
+            np.testing.assert_array_equal(to_host(a), to_host(b))
+        assert torch.equal(z_live, z_twin)
+        assert int(c_live.item()) & ((1 << 64) - 1) == c_twin
+    plan.close()
+    plan_twin.close()
