@@ -16,6 +16,11 @@ also prints the RMS of one update step, alpha / sqrt(G) for z-scored rewards.
 
     python -m paper_2608_17310_amd.drift --workload dense-4b --generations 70 --members 8
 
+With --norms-one the norm vectors hold 1.0, as in a trained model, instead of
+N(0, 0.02), and each checkpoint adds a row over those vectors alone: 1.0 is a
+binade boundary of bf16 (the grid steps by 2^-7 above it and 2^-8 below), so
+an element whose perturbation rounds away can come back one step below 1.
+
 With --format int8 or --format e4m3 the same walk runs on the quantized
 codes of the set (per-row scales; es_qperturb / es_qrestore), and the drift
 is measured on the dequantized values s * v(c), in units of sigma and of the
@@ -159,17 +164,23 @@ def main(argv=None):
     ap.add_argument("--alpha", type=float, default=5e-4)
     ap.add_argument("--walks", default="restore,swap")
     ap.add_argument("--format", default="bf16", choices=("bf16", "int8", "e4m3"))
+    ap.add_argument("--norms-one", action="store_true",
+                    help="norm vectors at 1.0 (bf16 only), with a row over them alone")
     args = ap.parse_args(argv)
     W = wl.WORKLOADS[args.workload]
+    if args.norms_one and args.format != "bf16":
+        ap.error("--norms-one applies to bf16 parameters")
     torch.cuda.set_device(0)
     if args.format != "bf16":
         return quantized_main(args, W)
-    flat, views = wl.device_params(W)
+    flat, views = wl.device_params(W, norm_value=1.0 if args.norms_one else None)
     start_flat = flat.clone()
     offs, _ = wl.flat_layout(W.numels)
     start = [start_flat[o:o + n] for o, n in zip(offs, W.numels)]
+    vec = [i for i, shp in enumerate(W.shapes) if len(shp) == 1]
     print(json.dumps({"workload": W.name, "params": W.n_params, "members": args.members,
-                      "sigma": args.sigma, "update_step_rms": args.alpha / math.sqrt(args.members)}),
+                      "sigma": args.sigma, "update_step_rms": args.alpha / math.sqrt(args.members),
+                      "norms": 1.0 if args.norms_one else "N(0, 0.02)"}),
           flush=True)
     for walk in args.walks.split(","):
         flat.copy_(start_flat)
@@ -184,6 +195,11 @@ def main(argv=None):
                        "roundings": g * (2 * args.members if walk == "restore" else args.members + 1)}
                 row.update(drift_stats(views, start, args.sigma))
                 print(json.dumps(row), flush=True)
+                if args.norms_one:
+                    row = {"walk": walk, "generation": g, "subset": "norm vectors"}
+                    row.update(drift_stats([views[i] for i in vec], [start[i] for i in vec],
+                                           args.sigma))
+                    print(json.dumps(row), flush=True)
         plan.close()
     return 0
 

@@ -196,9 +196,11 @@ def flat_layout(numels, align=ALIGN_ELEMS):
     return offs, cur
 
 
-def device_params(wl, device="cuda", seed=1234):
+def device_params(wl, device="cuda", seed=1234, norm_value=None):
     """Materialise the parameter set on a device as views into one flat bf16
-    buffer, values N(0, 0.02) from PyTorch's seeded device generator.
+    buffer, values N(0, 0.02) from PyTorch's seeded device generator.  With
+    norm_value, the vectors (RMSNorm weights) hold that value instead (1.0 as
+    in a trained model; the matrices are the same as without it).
     Returns (flat_buffer, [tensor views])."""
     import torch
     offs, total = flat_layout(wl.numels)
@@ -209,6 +211,8 @@ def device_params(wl, device="cuda", seed=1234):
     for off, n, shape in zip(offs, wl.numels, wl.shapes):
         v = flat[off:off + n]
         v.normal_(0.0, WEIGHT_STD, generator=gen)
+        if norm_value is not None and len(shape) == 1:
+            v.fill_(norm_value)
         views.append(v.view(shape))
     return flat, views
 

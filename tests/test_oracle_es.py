@@ -63,6 +63,31 @@ def test_inplace_bf16_round_trip_drift_is_small():
     assert np.all(d <= bound)
 
 
+def test_unit_norm_weights_round_trip_closed_forms():
+    """RMSNorm weights at 1.0 (as in a trained model) sit on a binade boundary
+    of bf16: the neighbours are 1 - 2^-8 below and 1 + 2^-7 above, so
+    RNE(1 + d) = 1 exactly when -2^-9 <= d <= 2^-8 (ties go to the even 1).
+    With d = s eps and s = 1e-3 (binary32): the perturbation leaves
+    P(-2^-9/s <= eps <= 2^-8/s) of the elements unchanged, and the revert of
+    an unchanged element, RNE(1 - d), misses 1 (lands on 1 - 2^-8) exactly
+    when 2^-9 < d <= 2^-8; a changed element always comes back to 1.  Both
+    fractions against the normal CDF within five standard errors."""
+    n = 1 << 20
+    ones = f64_to_bf16_rne(np.ones(n))
+    s = float(np.float32(1e-3))
+    lo, hi = 2.0 ** -9 / s, 2.0 ** -8 / s
+    p = perturb(ones, 21, 4, 1, 1e-3)
+    back = restore(p, 21, 4, 1, 1e-3)
+    for frac, expect in [(np.mean(p == ones[0]), stats.norm.cdf(hi) - stats.norm.cdf(-lo)),
+                         (np.mean(back != ones[0]), stats.norm.cdf(hi) - stats.norm.cdf(lo))]:
+        se = math.sqrt(expect * (1 - expect) / n)
+        assert abs(frac - expect) < 5 * se, (frac, expect)
+    # every miss is the one value below 1, and only after an unchanged perturbation
+    miss = back != ones[0]
+    assert np.all(bf16_to_f64(back[miss]) == 1 - 2.0 ** -8)
+    assert np.all(p[miss] == ones[0])
+
+
 def test_sigma_zero_identity_and_sign():
     theta = random_bf16_bits(4096, 3)
     theta[:3] = [0x8000, 0x0000, 0x0001]
