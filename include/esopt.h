@@ -25,8 +25,9 @@
  * Parameters are bf16 (the paper states no dtype; its memory figures imply
  * 16-bit weights).  Each result is computed in binary32 and rounded to bf16
  * round-to-nearest-even (the update can instead round stochastically), with
- * exactly one read and one write per element.  Int8 parameters with per-row
- * scales have a plan of their own (es_qplan_*, further down).
+ * exactly one read and one write per element.  Int8 and fp8 (E4M3)
+ * parameters with per-row scales have a plan of their own (es_qplan_*,
+ * further down).
  *
  * Conventions for every call:
  *   - Device pointers are HIP device memory of the device current at the
@@ -37,7 +38,7 @@
  *   - `stream` is a hipStream_t (NULL: the default stream).  Every call is
  *     stream-ordered and returns without synchronising the host; launch
  *     errors are reported by the return code.  The passes (perturb, restore,
- *     swap, update, z-score and their int8 counterparts) only launch kernels
+ *     swap, update, z-score and their quantized counterparts) only launch kernels
  *     on `stream` -- no memset, no host synchronisation, host arrays copied
  *     into kernel arguments -- so they can be captured into a HIP graph; a
  *     replay repeats the captured arguments (seeds, signs, sigma, alpha).
@@ -395,9 +396,9 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
                const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
                float* z_out_dev, int32_t* status_out_dev, es_stream_t stream);
 
-/* Checksum of an int8 plan's codes, as es_plan_checksum with b the code's 8
- * bits (0 .. 255) and j its index in its tensor; the scales are not included
- * (no pass changes them). */
+/* Checksum of a quantized plan's codes (int8 or E4M3), as es_plan_checksum
+ * with b the code's 8 bits (0 .. 255) and j its index in its tensor; the
+ * scales are not included (no pass changes them). */
 int es_qplan_checksum(es_qplan_t* plan, uint64_t* out_dev, es_stream_t stream);
 
 /* Cosine schedule of the perturbation radius (Section 3.1):

@@ -33,9 +33,9 @@
 //     load in flight.  Both shapes were chosen by sweeping on MI355X.  Swap
 //     is the perturb kernel with two streams and a bf16 rounding between
 //     them.
-//   * The int8 path (es_quant.hpp) has a tensor table searched per tile and
-//     tiles of 16-code groups; all its passes are VALU-bound and use the
-//     update's shape.
+//   * The quantized path (int8 codes, es_quant.hpp; fp8 E4M3 codes,
+//     es_fp8.hpp) has a tensor table searched per tile and tiles of 16-code
+//     groups; all its passes are VALU-bound and use the update's shape.
 //   * Perturb/restore read and write each parameter once (4 bytes of HBM
 //     traffic per parameter).  The update regenerates the noise of all
 //     distinct member seeds for the same 8 elements in registers,
@@ -1363,7 +1363,7 @@ struct es_qplan {
     uint64_t numel = 0;
     uint64_t n_full = 0;
     uint64_t n_tail = 0;
-    uint32_t grid = 0;              // workgroups of every int8 pass
+    uint32_t grid = 0;              // workgroups of every quantized pass
     int threads = kDefaultThreads;
     int groups = kDefaultQGroups;   // 16-code groups per lane per tile
     int format = kFmtInt8;          // ES_QFORMAT_INT8 or ES_QFORMAT_E4M3 (one per plan)
