@@ -12,12 +12,26 @@
 // undoes the perturbation inside a binade), and 1 - r 2^-16 for an update
 // (16-bit draw of domain 1 under the rounding seed).
 //
-// On gfx950 the grid is reached with the exponent unit: for x = m 2^e,
-// |m| in [0.5, 1), the spacing is h = 2^max(e - 4, -9) (the subnormal band
-// below 2^-6 keeps 2^-9), t = x / h = ldexp(x, -log2 h) is exact, floor(t)
-// and t - floor(t) are exact, and the result k h = ldexp(k, log2 h) is a grid
-// point (or +-448 after the clamp), which the hardware conversion encodes
-// exactly.  Codes decode with the hardware conversion as well.
+// On gfx950 the rounding is the hardware's stochastically rounded
+// conversion (v_cvt_sr_fp8_f32).  It rounds |x| away from zero exactly when
+// F + R >= 2^32, with F the fraction of |x| above the grid point below it in
+// units of the spacing, as 32-bit fixed point (truncated), and R its 32-bit
+// random operand; checked on MI355X against that rule for every kind of input
+// (normal and subnormal results, exact carry boundaries, signed zeros, values
+// next to 448).  A rule on the signed f of x (f = F / 2^32 for x >= 0,
+// 1 - F / 2^32 for x < 0 off the grid) maps onto it with one exclusive-or: for
+// a threshold thr with 2^32 thr a multiple of 2^16,
+//   f >= thr: R = 2^32 - 2^32 thr  for x >= 0,  R = 2^32 thr - 1   for x < 0,
+//   f >  thr: R = 2^32 - 2^32 thr - 1,           R = 2^32 thr,
+// that is R = A ^ s, s = all ones for x < 0, with A = U for a perturbation
+// (thr = 1 - u, U = 2^32 u), ~U for a restore (thr = u, strict) and r 2^16
+// for an update (thr = 1 - r 2^-16).  The only inputs where this differs
+// from the rule on the exact f are |x| < 2^-18 (below 2^-9 of the smallest
+// subnormal) whose fraction lies less than 2^-32 beyond the threshold of a
+// comparison that is strict on |x| (a restore with x >= 0, a perturbation or
+// update with x < 0): the hardware sees F truncated to 32 bits, and only
+// such tiny values have fraction bits below 2^-32.  x is clamped to +-448 first, so no result exceeds the
+// format.  Codes decode with the hardware conversion as well.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,31 +50,34 @@ __device__ __forceinline__ void decode4(uint32_t w, float v[4]) {
     v[0] = lo.x; v[1] = lo.y; v[2] = hi.x; v[3] = hi.y;
 }
 
-// Four grid values (each exactly representable) as the codes of one word.
-__device__ __forceinline__ uint32_t encode4(const float v[4]) {
-    int w = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
-    w = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], w, true);
-    return static_cast<uint32_t>(w);
+// A = U = 2^32 u, u = (2 r + 1) 2^-10, r the word's top 9 bits (the spare
+// draw of a perturbation or restore).
+__device__ __forceinline__ uint32_t draw9_fixed(uint32_t w) {
+    return (w & 0xFF800000u) | 0x00400000u;
 }
 
-// x rounded onto the grid: lo + h when the fraction f of the step from lo
-// to the next grid point satisfies f >= thr (f > thr with kStrict), else
-// lo; clamped to +-448.  A zero result is +0.
-template <bool kStrict>
-__device__ __forceinline__ float round_grid(float x, float thr) {
-    const int e = __builtin_amdgcn_frexp_expf(x);          // 0 for x = 0
-    const int ke = max(e - 4, -9);                           // h = 2^ke
-    const float t = __builtin_amdgcn_ldexpf(x, -ke);
-    const float fl = __builtin_floorf(t);
-    const float f = t - fl;
-    const bool step = kStrict ? (f > thr) : (f >= thr);
-    const float k = fl + (step ? 1.0f : 0.0f);
-    return __builtin_amdgcn_fmed3f(__builtin_amdgcn_ldexpf(k, ke), -kE4M3Max, kE4M3Max);
-}
-
-// 1 + r 2^-16 as a binary32 from a 16-bit draw r (exact).
-__device__ __forceinline__ float one_plus_draw16(uint32_t r16) {
-    return __uint_as_float((r16 << 7) | 0x3F800000u);
+// Four values rounded onto the grid by the rules above, a[i] the operand for
+// x[i] >= 0 (its complement serves x[i] < 0), as the codes of one word.  A
+// zero result is +0 (the conversion gives -0 for a negative x that rounds to
+// zero; its sign is cleared).
+__device__ __forceinline__ uint32_t round4(const float x[4], const uint32_t a[4]) {
+    float xc[4];
+    uint32_t rn[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        xc[i] = __builtin_amdgcn_fmed3f(x[i], -kE4M3Max, kE4M3Max);
+        const uint32_t s = static_cast<uint32_t>(static_cast<int32_t>(__float_as_uint(xc[i])) >> 31);
+        rn[i] = a[i] ^ s;
+    }
+    int w = __builtin_amdgcn_cvt_sr_fp8_f32(xc[0], static_cast<int>(rn[0]), 0, 0);
+    w = __builtin_amdgcn_cvt_sr_fp8_f32(xc[1], static_cast<int>(rn[1]), w, 1);
+    w = __builtin_amdgcn_cvt_sr_fp8_f32(xc[2], static_cast<int>(rn[2]), w, 2);
+    w = __builtin_amdgcn_cvt_sr_fp8_f32(xc[3], static_cast<int>(rn[3]), w, 3);
+    const uint32_t u = static_cast<uint32_t>(w);
+    // bit 7 of each byte of nz: its magnitude (low 7 bits) is nonzero; the
+    // low bits cannot carry out of their byte
+    const uint32_t nz = (u & 0x7F7F7F7Fu) + 0x7F7F7F7Fu;
+    return u & (nz | 0x7F7F7F7Fu);
 }
 
 // Codes that must keep their bytes: not-a-number codes (0x7F, 0xFF) and the

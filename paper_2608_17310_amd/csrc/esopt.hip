@@ -1124,19 +1124,19 @@ constexpr int kFmtE4M3 = 1;
 // call, whose words give the four normals and the four spare draws.  The
 // scale's reciprocal is folded into the pair's radius factor; x = v -+ d is
 // one fused multiply-add, and the restore rounds with the complementary
-// rule, so it undoes the perturbation inside a binade.
+// rule (operand ~U for U), so it undoes the perturbation inside a binade.
 template <bool kNegate>
 __device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t e,
                                                 uint32_t tensor_id, const Member& m, float inv0,
                                                 float inv1, uint32_t out[4]) {
     const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
     const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
-    const uint32_t one_plus = esq::one_plus_half_step_vgpr();
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, m.k0, m.k1);
         const uint32_t ws[4] = {w.w0, w.w1, w.w2, w.w3};
-        float v[4], res[4];
+        float v[4], x[4];
+        uint32_t a[4];
         esf::decode4(raw[c], v);
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -1146,16 +1146,12 @@ __device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t 
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int i = 2 * p + h;
-                const float one_plus_u = esq::spare_one_plus(ws[i], one_plus);   // 1 + u, exact
-                if constexpr (kNegate)
-                    res[i] = esf::round_grid<true>(__builtin_fmaf(-t, trig[h], v[i]),
-                                                   one_plus_u - 1.0f);
-                else
-                    res[i] = esf::round_grid<false>(__builtin_fmaf(t, trig[h], v[i]),
-                                                    2.0f - one_plus_u);
+                const uint32_t u = esf::draw9_fixed(ws[i]);
+                x[i] = __builtin_fmaf(kNegate ? -t : t, trig[h], v[i]);
+                a[i] = kNegate ? ~u : u;
             }
         }
-        out[c] = esf::encode4(res);
+        out[c] = esf::round4(x, a);
     }
 }
 
@@ -1196,20 +1192,20 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
             const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
             if constexpr (kFmt == kFmtE4M3) {
                 // x = v + acc / s (one fused multiply-add), rounded onto the
-                // grid with the threshold 1 - r 2^-16
+                // grid with the threshold 1 - r 2^-16 (operand r 2^16)
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    float v[4], res[4];
+                    float v[4], x[4];
+                    uint32_t a[4];
                     esf::decode4(raw[k], v);
 #pragma unroll
                     for (int i = 0; i < 4; ++i) {
                         const int c = 4 * k + i;
-                        const uint32_t draw = (dw[c >> 1] >> (16 * (c & 1))) & 0xFFFFu;
-                        res[i] = esf::round_grid<false>(
-                            __builtin_fmaf(acc[c], c < 8 ? inv0 : inv1, v[i]),
-                            2.0f - esf::one_plus_draw16(draw));
+                        const uint32_t d = dw[c >> 1];
+                        a[i] = (c & 1) ? (d & 0xFFFF0000u) : (d << 16);
+                        x[i] = __builtin_fmaf(acc[c], c < 8 ? inv0 : inv1, v[i]);
                     }
-                    out[k] = esf::encode4(res);
+                    out[k] = esf::round4(x, a);
                 }
                 esf::keep_special(raw, inv0, inv1, out);
             } else {
