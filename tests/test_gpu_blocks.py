@@ -338,3 +338,25 @@ def test_random_block_grids_match_the_whole_matrix():
                 n = (r1 - r0) * (c1 - c0)
                 assert torch.count_nonzero(buf[:pad].float()) == 0
                 assert torch.count_nonzero(buf[pad + n:].float()) == 0
+
+
+def test_allocation_free_update_on_a_block_plan():
+    """es_update_noalloc on a plan with a strided block and a whole vector
+    (two launches, the static scratch) leaves the bits es_update leaves."""
+    rows, cols = 200, 1024
+    bits = wl.random_bf16_bits(rows * cols, 71)
+    v_bits = wl.random_bf16_bits(3000, 72)
+    r = torch.tensor([0.4, 0.9, 0.2], device="cuda")
+    out = []
+    for noalloc in (False, True):
+        a = to_device(bits, (rows, cols))[:, 256:768].contiguous()
+        v = to_device(v_bits)
+        with esopt.Plan(blocks=[esopt.Block(a, 1, cols, 0, 256), esopt.Block(v, 2, 3000)]) as p:
+            fn = p.update_noalloc if noalloc else p.update
+            fn([4, 5, 6], [1, -1, 1], r, 5e-4)
+            fn([7, 8, 9], [1, 1, 1], r, 5e-4, flags=esopt.ES_UPDATE_STOCHASTIC_ROUND,
+               round_seed=3)
+        torch.cuda.synchronize()
+        out.append((to_host(a), to_host(v)))
+    for x, y in zip(*out):
+        np.testing.assert_array_equal(x, y)
