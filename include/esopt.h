@@ -371,6 +371,25 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
  * ES_ERR_INVALID_ARG for an unknown format. */
 int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint32_t format,
                            es_qplan_t** out);
+
+/* A quantized plan over shards of tensors (the int8 and E4M3 counterpart of
+ * es_tensor_t.offset8; Section 3: each element's noise is regenerated from
+ * the seed and its place in its whole tensor, so a GPU holding a contiguous
+ * range of a tensor needs no communication).  Code i of tensors[k] is code
+ * elem0[k] + i of the whole tensor tensors[k].tensor_id: it takes that
+ * code's noise, rounding draws (perturb and update) and checksum term, so
+ * every pass over the shard leaves exactly the codes the same pass over the
+ * whole tensor leaves there, and the checksums of disjoint shards add up
+ * (mod 2^64) to the whole tensor's.  tensors[k].scales holds the shard's own
+ * scales: scale r serves the shard's codes r row .. r row + row - 1 (the
+ * whole tensor's scale elem0[k] / row + r); with row == 0 the one scale of
+ * the tensor.  Requirements: elem0[k] a multiple of 16, and of row when
+ * row > 0 (a shard starts on a row of scales); elem0[k] + numel below 2^31.
+ * elem0 may be null (every shard starts at 0: es_qplan_create_format).
+ * Errors as es_qplan_create_format, and ES_ERR_INVALID_ARG for an elem0 that
+ * breaks a requirement. */
+int es_qplan_create_shards(const es_qtensor_t* tensors, const uint64_t* elem0, uint32_t n_tensors,
+                           uint32_t format, es_qplan_t** out);
 int es_qplan_destroy(es_qplan_t* plan);
 uint64_t es_qplan_numel(const es_qplan_t* plan);
 uint64_t es_qplan_device_bytes(const es_qplan_t* plan);   /* as es_plan_device_bytes */

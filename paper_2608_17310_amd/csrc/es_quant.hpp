@@ -37,15 +37,20 @@ constexpr int kQGroup = 16;                     // int8 codes per lane-group
 
 // Quantized tensor table entry.  Tiles are numbered as in the bf16 path:
 // full tiles (16-byte aligned base, in bounds) across all tensors, then tail
-// tiles.  numel < 2^31, so element indices within a tensor (and the end of
-// its last tile) fit 32 bits.  The row index j / row is computed as
+// tiles.  noise0 + numel < 2^31, so element indices within a tensor, the
+// whole-tensor indices of a shard's elements (noise0 + j, which select the
+// noise, the rounding draws and the checksum term) and the end of the last
+// tile fit 32 bits.  noise0 is a multiple of 16, so a 16-code group of the
+// shard is a 16-code group of the whole tensor.  The row index j / row (of
+// the local index: the shard's scales start at its first row) is computed as
 // mulhi(j, magic) >> shift, exact for every j < 2^31 (Granlund and
 // Montgomery, 1994: magic = ceil(2^(31 + l) / row), l = ceil(log2 row),
 // shift = l - 1).
 struct DevQTensor {
     int8_t* data;
     const float* scales;
-    uint64_t numel;
+    uint32_t numel;
+    uint32_t noise0;                            // whole-tensor index of element 0
     uint64_t first_full;
     uint64_t first_tail;
     uint32_t row;                               // codes per scale; 0: one scale
@@ -61,6 +66,7 @@ struct QTileRef {
     int8_t* data;
     const float* scales;
     uint32_t numel;
+    uint32_t noise0;
     uint32_t elem0;
     uint32_t row;
     uint32_t tensor_id;
@@ -74,7 +80,7 @@ __device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ 
                                                  uint64_t tile) {
     t = es::seek_tensor(t, tile, tab[0].n_tensors,
                         [tab](uint32_t i) { return tab[i].first_full; });
-    return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
+    return QTileRef{tab[t].data, tab[t].scales, tab[t].numel, tab[t].noise0,
                     static_cast<uint32_t>((tile - tab[t].first_full) * kTileElems), tab[t].row,
                     tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
 }
@@ -85,7 +91,7 @@ __device__ __forceinline__ QTileRef qlocate_tail(const DevQTensor* __restrict__ 
     t = es::seek_tensor(t, tile, tab[0].n_tensors,
                         [tab](uint32_t i) { return tab[i].first_tail; });
     const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
-    return QTileRef{tab[t].data, tab[t].scales, static_cast<uint32_t>(tab[t].numel),
+    return QTileRef{tab[t].data, tab[t].scales, tab[t].numel, tab[t].noise0,
                     static_cast<uint32_t>((n_full + tile - tab[t].first_tail) * kTileElems),
                     tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
 }
@@ -156,11 +162,12 @@ __device__ __forceinline__ void group_inv_scales(const QTileRef& r, uint32_t e, 
     inv1 = (r.row & 15u) == 0u ? inv0 : inv_scale(r, e + 8);
 }
 
-// One noise stream's scaled normals for the 16 codes of a group:
-// acc[i] += w_k * (normal of element e + i), w_k = weight * sqrt(2 ln 2).
-__device__ __forceinline__ void qgroup_axpy(uint32_t e, uint32_t tensor_id, uint32_t k0,
+// One noise stream's scaled normals for the 16 codes of a group whose first
+// code has whole-tensor index n: acc[i] += w_k * (normal of element n + i),
+// w_k = weight * sqrt(2 ln 2).
+__device__ __forceinline__ void qgroup_axpy(uint32_t n, uint32_t tensor_id, uint32_t k0,
                                             uint32_t k1, float w_k, float acc[16]) {
-    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    const uint32_t q = n >> 2;                  // multiple of 4: q + 3 does not carry
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
         const es::Words w = es::philox4x32_10(q + c, 0u, tensor_id, es::kDomainNoise, k0, k1);

@@ -1081,14 +1081,15 @@ struct QPass {
     Member m;
 };
 
-// Perturb / restore of one 16-code group: per quad of codes one noise call,
-// whose words give the four normals and the four rounding draws.  The scale's
-// reciprocal is folded into the pair's radius factor, and d + f is one FMA.
+// Perturb / restore of one 16-code group (n: the whole-tensor index of its
+// first code): per quad of codes one noise call, whose words give the four
+// normals and the four rounding draws.  The scale's reciprocal is folded into
+// the pair's radius factor, and d + f is one FMA.
 template <bool kNegate>
-__device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e,
+__device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t n,
                                                uint32_t tensor_id, const Member& m, float inv0,
                                                float inv1, uint32_t out[4]) {
-    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    const uint32_t q = n >> 2;                  // multiple of 4: q + 3 does not carry
     // an invalid scale has inv = 0: its step is 0 and its codes clamp to
     // [-128, 127], i.e. they are left as they are
     const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
@@ -1120,16 +1121,16 @@ __device__ __forceinline__ void qperturb_group(const uint32_t raw[4], uint32_t e
 constexpr int kFmtInt8 = 0;
 constexpr int kFmtE4M3 = 1;
 
-// fp8 perturb / restore of one 16-code group: per quad of codes one noise
+// fp8 perturb / restore of one 16-code group (n as above): per quad of codes one noise
 // call, whose words give the four normals and the four spare draws.  The
 // scale's reciprocal is folded into the pair's radius factor; x = v -+ d is
 // one fused multiply-add, and the restore rounds with the complementary
 // rule (operand ~U for U), so it undoes the perturbation inside a binade.
 template <bool kNegate>
-__device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t e,
+__device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t n,
                                                 uint32_t tensor_id, const Member& m, float inv0,
                                                 float inv1, uint32_t out[4]) {
-    const uint32_t q = e >> 2;                  // multiple of 4: q + 3 does not carry
+    const uint32_t q = n >> 2;                  // multiple of 4: q + 3 does not carry
     const float wk_inv[2] = {m.w_k * inv0, m.w_k * inv1};
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
@@ -1157,7 +1158,8 @@ __device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t 
 
 // One tile of an int8 pass: for each of the lane's 16-code groups in turn,
 // the step d in quanta (binary32) and the stochastically rounded, clamped
-// code.
+// code.  e indexes the codes and scales at hand; n = noise0 + e, the
+// whole-tensor index, selects the noise and the rounding draws.
 template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate, int kFmt>
 __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
                                       uint32_t n_members, const QPass& ps) {
@@ -1166,16 +1168,17 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
     for (int u = 0; u < kU; ++u) {
         const uint32_t e = e0 + uint32_t(u) * kThreads * esq::kQGroup;
         if (!kFast && e >= r.numel) break;
+        const uint32_t n = r.noise0 + e;
         uint32_t raw[4];
         esq::qload<kFast>(r.data, e, r.numel, raw, r.aligned16 != 0u);
         float inv0, inv1;
         esq::group_inv_scales(r, e, inv0, inv1);
         uint32_t out[4];
         if constexpr (!kTable && kFmt == kFmtE4M3) {
-            f8perturb_group<kNegate>(raw, e, r.tensor_id, ps.m, inv0, inv1, out);
+            f8perturb_group<kNegate>(raw, n, r.tensor_id, ps.m, inv0, inv1, out);
             esf::keep_special(raw, inv0, inv1, out);
         } else if constexpr (!kTable) {
-            qperturb_group<kNegate>(raw, e, r.tensor_id, ps.m, inv0, inv1, out);
+            qperturb_group<kNegate>(raw, n, r.tensor_id, ps.m, inv0, inv1, out);
         } else {
             float acc[16];
 #pragma unroll
@@ -1183,11 +1186,11 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
             for (uint32_t d = 0; d < n_members; ++d) {
                 const Member m = members[d];
                 if (is_zero_weight(m.w_k)) continue;
-                esq::qgroup_axpy(e, r.tensor_id, m.k0, m.k1, m.w_k, acc);
+                esq::qgroup_axpy(n, r.tensor_id, m.k0, m.k1, m.w_k, acc);
             }
             const es::Words da =
-                es::philox4x32_10(e >> 3, 0u, r.tensor_id, es::kDomainRounding, ps.dk0, ps.dk1);
-            const es::Words db = es::philox4x32_10((e >> 3) + 1u, 0u, r.tensor_id,
+                es::philox4x32_10(n >> 3, 0u, r.tensor_id, es::kDomainRounding, ps.dk0, ps.dk1);
+            const es::Words db = es::philox4x32_10((n >> 3) + 1u, 0u, r.tensor_id,
                                                    es::kDomainRounding, ps.dk0, ps.dk1);
             const uint32_t dw[8] = {da.w0, da.w1, da.w2, da.w3, db.w0, db.w1, db.w2, db.w3};
             if constexpr (kFmt == kFmtE4M3) {
@@ -1281,8 +1284,8 @@ QPassKernel qpass_kernel(int threads, int groups, QKind kind, int format) {
                               : qpass_kernel_for<kFmtInt8>(threads, groups, kind);
 }
 
-// int8 plan: the same sum with b the code's 8 bits (int8 tensors are never
-// shards, so an element's index in its tensor is its whole-tensor index).
+// Quantized plan: the same sum with b the code's 8 bits and j the element's
+// whole-tensor index (noise0 + its index in the shard).
 template <int kThreads, int kU>
 __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
     const esq::DevQTensor* __restrict__ tab, uint64_t n_full, uint64_t n_tail,
@@ -1298,7 +1301,8 @@ __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
             const uint32_t e = r.elem0 + (uint32_t(u) * kThreads + threadIdx.x) * esq::kQGroup;
             uint32_t raw[4];
             esq::qload<true>(r.data, e, r.numel, raw);
-            acc += checksum_terms<esq::kQGroup, 8, false>(raw, e, r.numel, salt);
+            acc += checksum_terms<esq::kQGroup, 8, false>(raw, r.noise0 + e, r.noise0 + r.numel,
+                                                          salt);
         }
     }
     t = 0;
@@ -1311,7 +1315,8 @@ __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
             if (e >= r.numel) break;
             uint32_t raw[4];
             esq::qload<false>(r.data, e, r.numel, raw, r.aligned16 != 0u);
-            acc += checksum_terms<esq::kQGroup, 8, true>(raw, e, r.numel, salt);
+            acc += checksum_terms<esq::kQGroup, 8, true>(raw, r.noise0 + e, r.noise0 + r.numel,
+                                                         salt);
         }
     }
     add_workgroup_sum<kThreads>(acc, out);
@@ -2258,7 +2263,12 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
 }
 
 int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint32_t format,
-                           es_qplan_t** out) try {
+                           es_qplan_t** out) {
+    return es_qplan_create_shards(tensors, nullptr, n_tensors, format, out);
+}
+
+int es_qplan_create_shards(const es_qtensor_t* tensors, const uint64_t* elem0, uint32_t n_tensors,
+                           uint32_t format, es_qplan_t** out) try {
     if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null output pointer");
     *out = nullptr;
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null tensor list");
@@ -2283,13 +2293,21 @@ int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint
         const std::string where = "es_qplan_create: tensor " + std::to_string(i);
         if (!ids.emplace(t.tensor_id, i).second)
             return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
-        // element indices, and the end of the last tile, stay below 2^32
+        // whole-tensor element indices, and the end of the last tile, stay
+        // below 2^32
+        const uint64_t n0 = elem0 == nullptr ? 0 : elem0[i];
         if (t.numel >= (uint64_t(1) << 31))
             return fail(ES_ERR_INVALID_ARG, where + ": numel must be below 2^31");
+        if (n0 >= (uint64_t(1) << 31) - t.numel)
+            return fail(ES_ERR_INVALID_ARG, where + ": elem0 + numel must be below 2^31");
         if (t.numel > 0 && (t.data == nullptr || t.scales == nullptr))
             return fail(ES_ERR_INVALID_ARG, where + ": null data or scales");
         if (t.row % 8 != 0)
             return fail(ES_ERR_INVALID_ARG, where + ": row must be a multiple of 8 (or 0)");
+        if (n0 % 16 != 0)
+            return fail(ES_ERR_INVALID_ARG, where + ": elem0 must be a multiple of 16");
+        if (t.row != 0 && n0 % t.row != 0)
+            return fail(ES_ERR_INVALID_ARG, where + ": elem0 must be a multiple of row");
         if (t.numel > 0 && (reinterpret_cast<uintptr_t>(t.scales) & 3u))
             return fail(ES_ERR_ALIGN, where + ": scales not 4-byte aligned");
         const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
@@ -2297,8 +2315,9 @@ int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint
         const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
         uint32_t magic = 0, shift = 0;
         if (t.row != 0) row_divisor(t.row, magic, shift);
-        tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales, t.numel, n_full, n_tail,
-                                 t.row, t.tensor_id, magic, shift, n_tensors,
+        tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales,
+                                 static_cast<uint32_t>(t.numel), static_cast<uint32_t>(n0),
+                                 n_full, n_tail, t.row, t.tensor_id, magic, shift, n_tensors,
                                  (a % 16 == 0) ? 1u : 0u};
         if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
         n_full += full;
@@ -2309,8 +2328,8 @@ int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint
     for (size_t i = 1; i < ranges.size(); ++i)
         if (ranges[i].first < ranges[i - 1].second)
             return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
-    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0, n_full, n_tail, 0u, 0xFFFFFFFFu, 0u, 0u,
-                                     n_tensors, 0u};
+    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0u, 0u, n_full, n_tail, 0u, 0xFFFFFFFFu,
+                                     0u, 0u, n_tensors, 0u};
 
     int device = -1;
     int rc = current_device(&device);

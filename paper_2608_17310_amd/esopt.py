@@ -86,6 +86,9 @@ SIGNATURES = {
     "es_qplan_create": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, ctypes.POINTER(_vp)]),
     "es_qplan_create_format": (ctypes.c_int, [ctypes.POINTER(EsQTensor), _u32, _u32,
                                               ctypes.POINTER(_vp)]),
+    "es_qplan_create_shards": (ctypes.c_int, [ctypes.POINTER(EsQTensor),
+                                              ctypes.POINTER(ctypes.c_uint64), _u32, _u32,
+                                              ctypes.POINTER(_vp)]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
     "es_qplan_device_bytes": (_u64, [_vp]),
@@ -398,10 +401,13 @@ class QPlan:
     s v(c), one scale per `row` consecutive codes, row a multiple of 8, 0 for
     one scale per tensor), prepared for single-launch passes.  format "int8":
     int8 codes, v(c) = c; format "e4m3": fp8 E4M3 codes (torch.float8_e4m3fn,
-    or their bytes as torch.uint8).  The plan keeps references to the codes
-    and scales."""
+    or their bytes as torch.uint8).  offsets places shards: codes[k] holds
+    elements offsets[k] .. of its whole tensor (a multiple of 16, and of the
+    row length when rows[k] > 0; scales[k] are the shard's own rows of
+    scales), as es_qplan_create_shards.  The plan keeps references to the
+    codes and scales."""
 
-    def __init__(self, codes, scales, rows, tensor_ids=None, format="int8"):
+    def __init__(self, codes, scales, rows, tensor_ids=None, format="int8", offsets=None):
         if format not in _QFORMATS:
             raise ValueError(f"format must be one of {sorted(_QFORMATS)}")
         self.format = format
@@ -414,6 +420,12 @@ class QPlan:
                else [_u32_arg(i, "tensor_id") for i in tensor_ids])
         if len(ids) != len(codes):
             raise ValueError("tensor_ids must match tensors")
+        elem0 = None
+        if offsets is not None:
+            offs = [_u64_arg(o, "offset") for o in offsets]
+            if len(offs) != len(codes):
+                raise ValueError("offsets must match tensors")
+            elem0 = (ctypes.c_uint64 * len(offs))(*offs)
         arr = (EsQTensor * len(codes))()
         for i, (q, sc, row, tid) in enumerate(zip(codes, scales, rows, ids)):
             if q.dtype not in code_dtypes or not q.is_cuda or not q.is_contiguous():
@@ -431,7 +443,7 @@ class QPlan:
         self.device = codes[0].device
         handle = ctypes.c_void_p()
         with torch.cuda.device(self.device):
-            _check(load().es_qplan_create_format(arr, len(codes), _QFORMATS[format],
+            _check(load().es_qplan_create_shards(arr, elem0, len(codes), _QFORMATS[format],
                                                  ctypes.byref(handle)), "es_qplan_create")
         self._h = handle
 

@@ -34,6 +34,8 @@ int main(void) {
     printf("perturb_null %d\n", es_perturb(NULL, 1, 1, 1e-3f, NULL));
     es_qplan_t* qplan = NULL;
     printf("qplan_create_null %d\n", es_qplan_create(NULL, 1, &qplan));
+    printf("qplan_create_shards_null %d\n",
+           es_qplan_create_shards(NULL, NULL, 1, ES_QFORMAT_E4M3, &qplan));
     printf("strerror %s\n", es_strerror(ES_ERR_INVALID_ARG));
     printf("sigma_cosine %.17g\n", es_sigma_cosine(1e-3, 1e-4, 50, 100));
     return 0;

@@ -208,6 +208,7 @@ def test_plain_c_consumer_of_header(lib, tmp_path):
     assert rows["es_block_t"] == layout(esopt.EsBlock)
     assert rows["plan_create_blocks_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["qplan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
+    assert rows["qplan_create_shards_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
                              str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
     assert rows["plan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
@@ -246,6 +247,32 @@ def test_quantized_plan_validation_without_gpu(lib):
     assert lib.es_qupdate(fake, seeds, signs, fake, 2, ctypes.byref(bad), None, None, None) == E
     assert lib.es_qplan_destroy(None) == esopt.ES_OK
     assert lib.es_qplan_numel(None) == 0
+
+
+def test_quantized_shard_validation_without_gpu(lib):
+    """es_qplan_create_shards rejects a shard start that is not a multiple
+    of 16, or of the row length, and whole-tensor indices that reach 2^31,
+    before any device call."""
+    fake = ctypes.c_void_p(0x10000)
+    out = ctypes.c_void_p()
+    T = esopt.EsQTensor
+    E = esopt.ES_ERR_INVALID_ARG
+
+    def create(t, n0, fmt=esopt.QFORMAT_INT8):
+        off = (ctypes.c_uint64 * 1)(n0)
+        return lib.es_qplan_create_shards((T * 1)(t), off, 1, fmt, ctypes.byref(out))
+    assert create(T(fake, fake, 100, 0, 0), 8) == E                # not a multiple of 16
+    assert create(T(fake, fake, 100, 48, 0), 16) == E              # not on a row of scales
+    assert create(T(fake, fake, 100, 48, 0), 40) == E              # neither
+    assert create(T(fake, fake, 100, 0, 0), (1 << 31) - 96) == E   # reaches 2^31
+    assert create(T(fake, fake, 0, 0, 0), 1 << 31) == E            # empty, index out of range
+    assert create(T(fake, fake, 100, 0, 0), 1 << 63, esopt.QFORMAT_E4M3) == E
+    assert create(T(fake, fake, 100, 12, 0), 0) == E               # the per-tensor rules too
+    assert lib.es_qplan_create_shards((T * 1)(T(fake, fake, 100, 0, 0)), None, 1, 7,
+                                      ctypes.byref(out)) == E       # unknown format
+    assert lib.es_qplan_create_shards(None, None, 1, 0, ctypes.byref(out)) == E
+    assert lib.es_qplan_create_shards((T * 1)(T(fake, fake, 100, 0, 0)), None, 1, 0,
+                                      None) == E
 
 
 def test_binding_range_checks_integer_arguments():
