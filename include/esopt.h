@@ -390,6 +390,45 @@ int es_qplan_create_format(const es_qtensor_t* tensors, uint32_t n_tensors, uint
  * breaks a requirement. */
 int es_qplan_create_shards(const es_qtensor_t* tensors, const uint64_t* elem0, uint32_t n_tensors,
                            uint32_t format, es_qplan_t** out);
+
+/* A rectangular block of a row-major quantized tensor (the int8 / E4M3
+ * counterpart of es_block_t, for column and row-and-column shards):
+ * rows x cols one-byte codes stored contiguously at `data` (block row i at
+ * data + i * cols), which are the whole tensor's codes
+ * (row0 + i) * row_len + col0 + j, i < rows, j < cols.  Each takes the
+ * noise, rounding draws and checksum term of that whole-tensor index
+ * (Section 3), so every pass over the block leaves exactly the codes the
+ * same pass over the whole tensor leaves there, and block checksums add up
+ * to the whole tensor's.  `scales` and `row` describe the block's own codes
+ * as in es_qtensor_t, in the block's storage order (scale r serves codes
+ * r row .. r row + row - 1 of the block): a matrix with one scale per
+ * row, split by columns, gives row = cols and the block's rows of scales;
+ * one scale per g consecutive codes of a row (g dividing cols and col0)
+ * gives row = g and the block's [rows, cols / g] scales.
+ * Requirements: col0 + cols <= row_len; rows * cols below 2^31;
+ * (row0 + rows - 1) * row_len + col0 + cols below 2^31; the first index
+ * row0 * row_len + col0 a multiple of 16; a block that is not one
+ * contiguous range of its tensor (rows > 1 and cols < row_len) also has
+ * cols and row_len multiples of 16; row a multiple of 8, or 0.  rows * cols
+ * may be 0 (the block is skipped). */
+typedef struct es_qblock {
+    void*        data;       /* device codes (any alignment, as es_qtensor_t) */
+    const float* scales;     /* device binary32 scales of the block's codes */
+    uint64_t     rows;
+    uint64_t     cols;
+    uint64_t     row_len;    /* codes per row of the whole tensor */
+    uint64_t     row0;       /* the block's first row and column in it */
+    uint64_t     col0;
+    uint32_t     row;        /* codes per scale in the block's storage order */
+    uint32_t     tensor_id;  /* noise identity, unique within a plan */
+} es_qblock_t;
+
+/* A quantized plan over blocks (format as es_qplan_create_format; blocks and
+ * tensors share the passes, es_qplan_numel and es_qplan_checksum).  Errors as
+ * es_qplan_create_format, and ES_ERR_INVALID_ARG for a block that breaks a
+ * requirement above or overlaps another in memory. */
+int es_qplan_create_blocks(const es_qblock_t* blocks, uint32_t n_blocks, uint32_t format,
+                           es_qplan_t** out);
 int es_qplan_destroy(es_qplan_t* plan);
 uint64_t es_qplan_numel(const es_qplan_t* plan);
 uint64_t es_qplan_device_bytes(const es_qplan_t* plan);   /* as es_plan_device_bytes */

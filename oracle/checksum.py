@@ -46,10 +46,11 @@ def checksum(bits, tensor_id, elem0=0, chunk=1 << 22):
     return _sum(np.asarray(bits, dtype=np.uint16).ravel(), tensor_id, elem0, chunk)
 
 
-def qchecksum(codes, tensor_id, chunk=1 << 22):
-    """Checksum of the int8 codes of one tensor: the same sum with b the
+def qchecksum(codes, tensor_id, elem0=0, chunk=1 << 22):
+    """Checksum of one-byte codes (int8 or E4M3) at whole-tensor indices
+    elem0, elem0 + 1, ... of tensor `tensor_id`: the same sum with b the
     code's 8 bits read as an unsigned byte."""
-    return _sum(np.asarray(codes, dtype=np.int8).ravel().view(np.uint8), tensor_id, 0, chunk)
+    return _sum(np.asarray(codes, dtype=np.int8).ravel().view(np.uint8), tensor_id, elem0, chunk)
 
 
 def _sum(b_all, tensor_id, elem0, chunk):

@@ -35,16 +35,20 @@ namespace esq {
 
 constexpr int kQGroup = 16;                     // int8 codes per lane-group
 
-// Quantized tensor table entry.  Tiles are numbered as in the bf16 path:
-// full tiles (16-byte aligned base, in bounds) across all tensors, then tail
-// tiles.  noise0 + numel < 2^31, so element indices within a tensor, the
-// whole-tensor indices of a shard's elements (noise0 + j, which select the
-// noise, the rounding draws and the checksum term) and the end of the last
-// tile fit 32 bits.  noise0 is a multiple of 16, so a 16-code group of the
-// shard is a 16-code group of the whole tensor.  The row index j / row (of
-// the local index: the shard's scales start at its first row) is computed as
-// mulhi(j, magic) >> shift, exact for every j < 2^31 (Granlund and
-// Montgomery, 1994: magic = ceil(2^(31 + l) / row), l = ceil(log2 row),
+// Quantized tensor table entry (a tensor, a contiguous shard of one or a
+// strided block of one).  Tiles are numbered as in the bf16 path: full tiles
+// (16-byte aligned base, in bounds) across all tensors, then tail tiles.
+// Element j of the entry (its index in the entry's own storage) is element
+//   n(j) = noise0 + j + (j / cols) * skip
+// of its whole tensor: skip = 0 for a tensor or a contiguous shard; a block
+// of rows of `cols` codes out of rows of cols + skip has skip > 0.  n(j)
+// selects the noise, the rounding draws and the checksum term; j selects the
+// code and its scale.  Every n(j) < 2^31 and numel < 2^31, so indices, and
+// the end of the last tile, fit 32 bits.  n(0) and, for a block, cols and
+// skip are multiples of 16, so a 16-code group of the entry is a 16-code
+// group of the whole tensor.  The divisions j / row (scale index) and
+// j / cols are mulhi(j, magic) >> shift, exact for every j < 2^31 (Granlund
+// and Montgomery, 1994: magic = ceil(2^(31 + l) / d), l = ceil(log2 d),
 // shift = l - 1).
 struct DevQTensor {
     int8_t* data;
@@ -59,8 +63,12 @@ struct DevQTensor {
     uint32_t shift;
     uint32_t n_tensors;                         // entries before the sentinel (same in all)
     uint32_t aligned16;                         // base 16-byte aligned: vector tail groups
+    uint32_t skip;                              // 0, or whole-tensor codes between block rows
+    uint32_t cmagic;                            // j / cols (read only when skip > 0)
+    uint32_t cshift;
+    uint32_t pad;
 };
-static_assert(sizeof(DevQTensor) == 64, "quantized tensor table entry layout");
+static_assert(sizeof(DevQTensor) == 80, "quantized tensor table entry layout");
 
 struct QTileRef {
     int8_t* data;
@@ -73,7 +81,17 @@ struct QTileRef {
     uint32_t magic;
     uint32_t shift;
     uint32_t aligned16;
+    uint32_t skip;
+    uint32_t cmagic;
+    uint32_t cshift;
 };
+
+// n(e) of the entry above: the whole-tensor index of local element e.
+__device__ __forceinline__ uint32_t qnoise_index(const QTileRef& r, uint32_t e) {
+    uint32_t n = r.noise0 + e;
+    if (r.skip != 0u) n += (__umulhi(e, r.cmagic) >> r.cshift) * r.skip;
+    return n;
+}
 
 template <uint32_t kTileElems>
 __device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ tab, uint32_t& t,
@@ -82,7 +100,8 @@ __device__ __forceinline__ QTileRef qlocate_full(const DevQTensor* __restrict__ 
                         [tab](uint32_t i) { return tab[i].first_full; });
     return QTileRef{tab[t].data, tab[t].scales, tab[t].numel, tab[t].noise0,
                     static_cast<uint32_t>((tile - tab[t].first_full) * kTileElems), tab[t].row,
-                    tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
+                    tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16,
+                    tab[t].skip, tab[t].cmagic, tab[t].cshift};
 }
 
 template <uint32_t kTileElems>
@@ -93,7 +112,8 @@ __device__ __forceinline__ QTileRef qlocate_tail(const DevQTensor* __restrict__ 
     const uint64_t n_full = tab[t + 1].first_full - tab[t].first_full;
     return QTileRef{tab[t].data, tab[t].scales, tab[t].numel, tab[t].noise0,
                     static_cast<uint32_t>((n_full + tile - tab[t].first_tail) * kTileElems),
-                    tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16};
+                    tab[t].row, tab[t].tensor_id, tab[t].magic, tab[t].shift, tab[t].aligned16,
+                    tab[t].skip, tab[t].cmagic, tab[t].cshift};
 }
 
 typedef uint32_t q32x4_t __attribute__((ext_vector_type(4)));

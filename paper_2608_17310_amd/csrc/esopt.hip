@@ -1158,8 +1158,8 @@ __device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t 
 
 // One tile of an int8 pass: for each of the lane's 16-code groups in turn,
 // the step d in quanta (binary32) and the stochastically rounded, clamped
-// code.  e indexes the codes and scales at hand; n = noise0 + e, the
-// whole-tensor index, selects the noise and the rounding draws.
+// code.  e indexes the codes and scales at hand; n, the whole-tensor index
+// of code e, selects the noise and the rounding draws.
 template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate, int kFmt>
 __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
                                       uint32_t n_members, const QPass& ps) {
@@ -1168,7 +1168,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
     for (int u = 0; u < kU; ++u) {
         const uint32_t e = e0 + uint32_t(u) * kThreads * esq::kQGroup;
         if (!kFast && e >= r.numel) break;
-        const uint32_t n = r.noise0 + e;
+        const uint32_t n = esq::qnoise_index(r, e);
         uint32_t raw[4];
         esq::qload<kFast>(r.data, e, r.numel, raw, r.aligned16 != 0u);
         float inv0, inv1;
@@ -1285,7 +1285,8 @@ QPassKernel qpass_kernel(int threads, int groups, QKind kind, int format) {
 }
 
 // Quantized plan: the same sum with b the code's 8 bits and j the element's
-// whole-tensor index (noise0 + its index in the shard).
+// whole-tensor index (qnoise_index; a 16-code group's indices are
+// consecutive).
 template <int kThreads, int kU>
 __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
     const esq::DevQTensor* __restrict__ tab, uint64_t n_full, uint64_t n_tail,
@@ -1301,8 +1302,7 @@ __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
             const uint32_t e = r.elem0 + (uint32_t(u) * kThreads + threadIdx.x) * esq::kQGroup;
             uint32_t raw[4];
             esq::qload<true>(r.data, e, r.numel, raw);
-            acc += checksum_terms<esq::kQGroup, 8, false>(raw, r.noise0 + e, r.noise0 + r.numel,
-                                                          salt);
+            acc += checksum_terms<esq::kQGroup, 8, false>(raw, esq::qnoise_index(r, e), 0, salt);
         }
     }
     t = 0;
@@ -1315,7 +1315,8 @@ __global__ __launch_bounds__(kThreads) void es_qchecksum_kernel(
             if (e >= r.numel) break;
             uint32_t raw[4];
             esq::qload<false>(r.data, e, r.numel, raw, r.aligned16 != 0u);
-            acc += checksum_terms<esq::kQGroup, 8, true>(raw, r.noise0 + e, r.noise0 + r.numel,
+            const uint32_t n = esq::qnoise_index(r, e);
+            acc += checksum_terms<esq::kQGroup, 8, true>(raw, n, uint64_t(n) + (r.numel - e),
                                                          salt);
         }
     }
@@ -2017,6 +2018,143 @@ std::string block_geometry_error(const es_block_t& b) {
     return "";
 }
 
+
+// One entry of a quantized plan, from an es_qtensor_t (with a shard start)
+// or an es_qblock_t: `numel` codes at `data` with their scales, the
+// whole-tensor index n0 of code 0 and, for a strided block, rows of `cols`
+// codes that lie cols + skip apart in the whole tensor (skip 0 otherwise).
+struct QSpec {
+    void* data;
+    const float* scales;
+    uint64_t numel;
+    uint32_t row, tensor_id;
+    uint64_t n0, cols, skip;
+};
+
+// The geometry of a quantized block as a QSpec, or what is wrong with it.
+std::string qblock_geometry(const es_qblock_t& b, QSpec& spec) {
+    typedef unsigned __int128 u128;
+    const u128 two31 = u128(1) << 31;
+    const u128 numel = u128(b.rows) * b.cols;
+    if (numel >= two31) return "rows * cols must be below 2^31";
+    spec = QSpec{b.data, b.scales, uint64_t(numel), b.row, b.tensor_id, 0, b.cols, 0};
+    if (numel == 0) return "";
+    if (u128(b.col0) + b.cols > b.row_len) return "col0 + cols above row_len";
+    const u128 first = u128(b.row0) * b.row_len + b.col0;
+    const u128 end = (u128(b.row0) + b.rows - 1) * b.row_len + b.col0 + b.cols;
+    if (end >= two31) return "(row0 + rows - 1) * row_len + col0 + cols must be below 2^31";
+    if (first % 16 != 0) return "first index row0 * row_len + col0 not a multiple of 16";
+    const bool strided = b.rows > 1 && b.cols < b.row_len;
+    if (strided && (b.cols % 16 != 0 || b.row_len % 16 != 0))
+        return "strided block: cols and row_len must be multiples of 16";
+    spec.n0 = uint64_t(first);
+    spec.skip = strided ? b.row_len - b.cols : 0;
+    return "";
+}
+
+// A quantized plan over checked entries (whole-tensor indices below 2^31):
+// the per-entry rules shared by tensors and blocks, the table, the device
+// checks and the allocations.  `name` and `kind` label the errors.
+int qplan_build(const std::vector<QSpec>& specs, uint32_t format, es_qplan_t** out,
+                const char* name, const char* kind) {
+    const std::string nm(name);
+    if (format != ES_QFORMAT_INT8 && format != ES_QFORMAT_E4M3)
+        return fail(ES_ERR_INVALID_ARG, nm + ": format not ES_QFORMAT_INT8 or ES_QFORMAT_E4M3");
+    int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
+    int groups = env_int("ESOPT_QGROUPS", kDefaultQGroups, 2, 8);
+    if (qpass_kernel(threads, groups, QKind::kUpdate, static_cast<int>(format)) == nullptr) {
+        threads = kDefaultThreads;
+        groups = kDefaultQGroups;
+    }
+    const uint64_t tile_elems = uint64_t(threads) * groups * esq::kQGroup;
+    const uint32_t n_tensors = static_cast<uint32_t>(specs.size());
+    std::vector<esq::DevQTensor> tab(n_tensors + 1);
+    std::unordered_map<uint32_t, uint32_t> ids;
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    uint64_t n_full = 0, n_tail = 0, numel = 0;
+    for (uint32_t i = 0; i < n_tensors; ++i) {
+        const QSpec& t = specs[i];
+        const std::string where = nm + ": " + kind + " " + std::to_string(i);
+        if (!ids.emplace(t.tensor_id, i).second)
+            return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
+        if (t.numel > 0 && (t.data == nullptr || t.scales == nullptr))
+            return fail(ES_ERR_INVALID_ARG, where + ": null data or scales");
+        if (t.row % 8 != 0)
+            return fail(ES_ERR_INVALID_ARG, where + ": row must be a multiple of 8 (or 0)");
+        if (t.numel > 0 && (reinterpret_cast<uintptr_t>(t.scales) & 3u))
+            return fail(ES_ERR_ALIGN, where + ": scales not 4-byte aligned");
+        const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
+        const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
+        const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
+        uint32_t magic = 0, shift = 0, cmagic = 0, cshift = 0;
+        if (t.row != 0) row_divisor(t.row, magic, shift);
+        if (t.skip != 0) row_divisor(static_cast<uint32_t>(t.cols), cmagic, cshift);
+        tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales,
+                                 static_cast<uint32_t>(t.numel), static_cast<uint32_t>(t.n0),
+                                 n_full, n_tail, t.row, t.tensor_id, magic, shift, n_tensors,
+                                 (a % 16 == 0) ? 1u : 0u, static_cast<uint32_t>(t.skip), cmagic,
+                                 cshift, 0u};
+        if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
+        n_full += full;
+        n_tail += tail;
+        numel += t.numel;
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+        if (ranges[i].first < ranges[i - 1].second)
+            return fail(ES_ERR_INVALID_ARG, nm + ": " + kind + "s overlap in memory");
+    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0u, 0u, n_full, n_tail, 0u, 0xFFFFFFFFu,
+                                     0u, 0u, n_tensors, 0u, 0u, 0u, 0u, 0u};
+
+    int device = -1;
+    int rc = current_device(&device);
+    if (rc != ES_OK) return rc;
+    for (uint32_t i = 0; i < n_tensors && rc == ES_OK; ++i) {
+        const QSpec& t = specs[i];
+        const std::string where = nm + ": " + kind + " " + std::to_string(i);
+        const uint64_t n_scales = t.row == 0 ? 1 : (t.numel + t.row - 1) / t.row;
+        rc = check_access(t.data, t.numel, device, where + " codes");
+        if (rc == ES_OK && t.numel > 0)
+            rc = check_access(t.scales, 4 * n_scales, device, where + " scales");
+    }
+    if (rc != ES_OK) return rc;
+    es_qplan_t* p = new (std::nothrow) es_qplan_t;
+    if (p == nullptr) return fail(ES_ERR_NOMEM, nm + ": host allocation");
+    p->device = device;
+    hipError_t e = hipSuccess;
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
+    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
+    const int wg = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
+    p->threads = threads;
+    p->groups = groups;
+    p->format = static_cast<int>(format);
+    p->n_tensors = n_tensors;
+    p->numel = numel;
+    p->n_full = n_full;
+    p->n_tail = n_tail;
+    const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
+    p->grid = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg));
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(esq::DevQTensor) * tab.size());
+    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
+    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        delete p;
+        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    }
+    e = hipMemcpy(p->d_tab, tab.data(), sizeof(esq::DevQTensor) * tab.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
+    if (e != hipSuccess) {
+        (void)hipFree(p->d_tab);
+        (void)hipFree(p->d_scratch);
+        delete p;
+        return hip_fail(e, nm + ": table upload");
+    }
+    *out = p;
+    return ES_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -2274,112 +2412,43 @@ int es_qplan_create_shards(const es_qtensor_t* tensors, const uint64_t* elem0, u
     if (tensors == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create: null tensor list");
     if (n_tensors == 0 || n_tensors > ES_MAX_TENSORS)
         return fail(ES_ERR_INVALID_ARG, "es_qplan_create: n_tensors out of range");
-    if (format != ES_QFORMAT_INT8 && format != ES_QFORMAT_E4M3)
-        return fail(ES_ERR_INVALID_ARG, "es_qplan_create: format not ES_QFORMAT_INT8 or "
-                                        "ES_QFORMAT_E4M3");
-    int threads = env_int("ESOPT_THREADS", kDefaultThreads, 256, 1024);
-    int groups = env_int("ESOPT_QGROUPS", kDefaultQGroups, 2, 8);
-    if (qpass_kernel(threads, groups, QKind::kUpdate, static_cast<int>(format)) == nullptr) {
-        threads = kDefaultThreads;
-        groups = kDefaultQGroups;
-    }
-    const uint64_t tile_elems = uint64_t(threads) * groups * esq::kQGroup;
-    std::vector<esq::DevQTensor> tab(n_tensors + 1);
-    std::unordered_map<uint32_t, uint32_t> ids;
-    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
-    uint64_t n_full = 0, n_tail = 0, numel = 0;
+    std::vector<QSpec> specs(n_tensors);
     for (uint32_t i = 0; i < n_tensors; ++i) {
         const es_qtensor_t& t = tensors[i];
         const std::string where = "es_qplan_create: tensor " + std::to_string(i);
-        if (!ids.emplace(t.tensor_id, i).second)
-            return fail(ES_ERR_INVALID_ARG, where + ": duplicate tensor_id " + std::to_string(t.tensor_id));
-        // whole-tensor element indices, and the end of the last tile, stay
-        // below 2^32
         const uint64_t n0 = elem0 == nullptr ? 0 : elem0[i];
         if (t.numel >= (uint64_t(1) << 31))
             return fail(ES_ERR_INVALID_ARG, where + ": numel must be below 2^31");
         if (n0 >= (uint64_t(1) << 31) - t.numel)
             return fail(ES_ERR_INVALID_ARG, where + ": elem0 + numel must be below 2^31");
-        if (t.numel > 0 && (t.data == nullptr || t.scales == nullptr))
-            return fail(ES_ERR_INVALID_ARG, where + ": null data or scales");
-        if (t.row % 8 != 0)
-            return fail(ES_ERR_INVALID_ARG, where + ": row must be a multiple of 8 (or 0)");
         if (n0 % 16 != 0)
             return fail(ES_ERR_INVALID_ARG, where + ": elem0 must be a multiple of 16");
         if (t.row != 0 && n0 % t.row != 0)
             return fail(ES_ERR_INVALID_ARG, where + ": elem0 must be a multiple of row");
-        if (t.numel > 0 && (reinterpret_cast<uintptr_t>(t.scales) & 3u))
-            return fail(ES_ERR_ALIGN, where + ": scales not 4-byte aligned");
-        const uintptr_t a = reinterpret_cast<uintptr_t>(t.data);
-        const uint64_t full = (a % 16 == 0) ? t.numel / tile_elems : 0;
-        const uint64_t tail = (t.numel - full * tile_elems + tile_elems - 1) / tile_elems;
-        uint32_t magic = 0, shift = 0;
-        if (t.row != 0) row_divisor(t.row, magic, shift);
-        tab[i] = esq::DevQTensor{static_cast<int8_t*>(t.data), t.scales,
-                                 static_cast<uint32_t>(t.numel), static_cast<uint32_t>(n0),
-                                 n_full, n_tail, t.row, t.tensor_id, magic, shift, n_tensors,
-                                 (a % 16 == 0) ? 1u : 0u};
-        if (t.numel > 0) ranges.emplace_back(a, a + t.numel);
-        n_full += full;
-        n_tail += tail;
-        numel += t.numel;
+        specs[i] = QSpec{t.data, t.scales, t.numel, t.row, t.tensor_id, n0, t.numel, 0};
     }
-    std::sort(ranges.begin(), ranges.end());
-    for (size_t i = 1; i < ranges.size(); ++i)
-        if (ranges[i].first < ranges[i - 1].second)
-            return fail(ES_ERR_INVALID_ARG, "es_qplan_create: tensors overlap in memory");
-    tab[n_tensors] = esq::DevQTensor{nullptr, nullptr, 0u, 0u, n_full, n_tail, 0u, 0xFFFFFFFFu,
-                                     0u, 0u, n_tensors, 0u};
-
-    int device = -1;
-    int rc = current_device(&device);
-    if (rc != ES_OK) return rc;
-    for (uint32_t i = 0; i < n_tensors && rc == ES_OK; ++i) {
-        const es_qtensor_t& t = tensors[i];
-        const std::string where = "es_qplan_create: tensor " + std::to_string(i);
-        const uint64_t n_scales = t.row == 0 ? 1 : (t.numel + t.row - 1) / t.row;
-        rc = check_access(t.data, t.numel, device, where + " codes");
-        if (rc == ES_OK && t.numel > 0)
-            rc = check_access(t.scales, 4 * n_scales, device, where + " scales");
-    }
-    if (rc != ES_OK) return rc;
-    es_qplan_t* p = new (std::nothrow) es_qplan_t;
-    if (p == nullptr) return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation");
-    p->device = device;
-    hipError_t e = hipSuccess;
-    int cus = 0;
-    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, p->device);
-    if (e != hipSuccess) { delete p; return hip_fail(e, "hipDeviceGetAttribute"); }
-    const int wg = env_int("ESOPT_UPDATE_WG_PER_CU", kDefaultUpdateWgPerCu, 1, 32);
-    p->threads = threads;
-    p->groups = groups;
-    p->format = static_cast<int>(format);
-    p->n_tensors = n_tensors;
-    p->numel = numel;
-    p->n_full = n_full;
-    p->n_tail = n_tail;
-    const uint64_t cap = std::max<uint64_t>(std::max(n_full, n_tail), 1);
-    p->grid = static_cast<uint32_t>(std::min<uint64_t>(cap, uint64_t(cus) * wg));
-    e = hipMalloc(reinterpret_cast<void**>(&p->d_tab), sizeof(esq::DevQTensor) * tab.size());
-    if (e != hipSuccess) { delete p; return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e)); }
-    e = hipMalloc(reinterpret_cast<void**>(&p->d_scratch), kScratchBytes);
-    if (e != hipSuccess) {
-        (void)hipFree(p->d_tab);
-        delete p;
-        return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
-    }
-    e = hipMemcpy(p->d_tab, tab.data(), sizeof(esq::DevQTensor) * tab.size(), hipMemcpyHostToDevice);
-    if (e == hipSuccess) e = hipMemset(p->d_scratch, 0, kScratchBytes);
-    if (e != hipSuccess) {
-        (void)hipFree(p->d_tab);
-        (void)hipFree(p->d_scratch);
-        delete p;
-        return hip_fail(e, "es_qplan_create: table upload");
-    }
-    *out = p;
-    return ES_OK;
+    return qplan_build(specs, format, out, "es_qplan_create", "tensor");
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_qplan_create: host allocation failed");
+}
+
+int es_qplan_create_blocks(const es_qblock_t* blocks, uint32_t n_blocks, uint32_t format,
+                           es_qplan_t** out) try {
+    if (out == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create_blocks: null output pointer");
+    *out = nullptr;
+    if (blocks == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qplan_create_blocks: null block list");
+    if (n_blocks == 0 || n_blocks > ES_MAX_TENSORS)
+        return fail(ES_ERR_INVALID_ARG, "es_qplan_create_blocks: n_blocks out of range");
+    std::vector<QSpec> specs(n_blocks);
+    for (uint32_t i = 0; i < n_blocks; ++i) {
+        const std::string bad = qblock_geometry(blocks[i], specs[i]);
+        if (!bad.empty())
+            return fail(ES_ERR_INVALID_ARG,
+                        "es_qplan_create_blocks: block " + std::to_string(i) + ": " + bad);
+    }
+    return qplan_build(specs, format, out, "es_qplan_create_blocks", "block");
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_qplan_create_blocks: host allocation failed");
 }
 
 int es_qplan_destroy(es_qplan_t* plan) {

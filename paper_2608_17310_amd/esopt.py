@@ -52,6 +52,12 @@ class EsQTensor(ctypes.Structure):
                 ("tensor_id", _u32)]
 
 
+class EsQBlock(ctypes.Structure):
+    _fields_ = [("data", _vp), ("scales", _vp), ("rows", _u64), ("cols", _u64),
+                ("row_len", _u64), ("row0", _u64), ("col0", _u64), ("row", _u32),
+                ("tensor_id", _u32)]
+
+
 class EsTileInfo(ctypes.Structure):
     _fields_ = [("elem0", _u64), ("end", _u64), ("full", _u32), ("aligned16", _u32)]
 
@@ -88,6 +94,8 @@ SIGNATURES = {
                                               ctypes.POINTER(_vp)]),
     "es_qplan_create_shards": (ctypes.c_int, [ctypes.POINTER(EsQTensor),
                                               ctypes.POINTER(ctypes.c_uint64), _u32, _u32,
+                                              ctypes.POINTER(_vp)]),
+    "es_qplan_create_blocks": (ctypes.c_int, [ctypes.POINTER(EsQBlock), _u32, _u32,
                                               ctypes.POINTER(_vp)]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
@@ -396,6 +404,17 @@ QFORMAT_INT8, QFORMAT_E4M3 = 0, 1
 _QFORMATS = {"int8": QFORMAT_INT8, "e4m3": QFORMAT_E4M3}
 
 
+class QBlock(tuple):
+    """One block of es_qplan_create_blocks: QBlock(codes, scales, row,
+    tensor_id, row_len, row0=0, col0=0), the whole tensor's rows row0.. and
+    columns col0.. of a row-major quantized tensor with row_len codes per row,
+    stored as `codes` ([rows, cols] contiguous, or 1-D for one row), with the
+    block's own scales, one per `row` codes in its storage order."""
+
+    def __new__(cls, codes, scales, row, tensor_id, row_len, row0=0, col0=0):
+        return super().__new__(cls, (codes, scales, row, tensor_id, row_len, row0, col0))
+
+
 class QPlan:
     """A list of quantized parameter tensors with binary32 scales (theta =
     s v(c), one scale per `row` consecutive codes, row a multiple of 8, 0 for
@@ -404,15 +423,25 @@ class QPlan:
     or their bytes as torch.uint8).  offsets places shards: codes[k] holds
     elements offsets[k] .. of its whole tensor (a multiple of 16, and of the
     row length when rows[k] > 0; scales[k] are the shard's own rows of
-    scales), as es_qplan_create_shards.  The plan keeps references to the
-    codes and scales."""
+    scales), as es_qplan_create_shards.  QPlan(blocks=[QBlock...]) plans
+    rectangular blocks of row-major tensors instead (column or
+    row-and-column shards; es_qplan_create_blocks).  The plan keeps
+    references to the codes and scales."""
 
-    def __init__(self, codes, scales, rows, tensor_ids=None, format="int8", offsets=None):
+    def __init__(self, codes=None, scales=None, rows=None, tensor_ids=None, format="int8",
+                 offsets=None, blocks=None):
         if format not in _QFORMATS:
             raise ValueError(f"format must be one of {sorted(_QFORMATS)}")
         self.format = format
         code_dtypes = ((torch.int8,) if format == "int8"
                        else (torch.float8_e4m3fn, torch.uint8))
+        if blocks is not None:
+            if any(a is not None for a in (codes, scales, rows, tensor_ids, offsets)):
+                raise ValueError("give either codes, scales and rows, or blocks")
+            self._init_blocks(list(blocks), code_dtypes)
+            return
+        if codes is None or scales is None or rows is None:
+            raise ValueError("codes, scales and rows are required")
         codes, scales, rows = list(codes), list(scales), [int(r) for r in rows]
         if not codes or len(scales) != len(codes) or len(rows) != len(codes):
             raise ValueError("codes, scales and rows must be non-empty and of equal length")
@@ -445,6 +474,44 @@ class QPlan:
         with torch.cuda.device(self.device):
             _check(load().es_qplan_create_shards(arr, elem0, len(codes), _QFORMATS[format],
                                                  ctypes.byref(handle)), "es_qplan_create")
+        self._h = handle
+
+    def _init_blocks(self, blocks, code_dtypes):
+        if not blocks:
+            raise ValueError("empty block list")
+        arr = (EsQBlock * len(blocks))()
+        codes, scales, ids = [], [], []
+        for i, (q, sc, row, tid, row_len, row0, col0) in enumerate(blocks):
+            if q.dtype not in code_dtypes or not q.is_cuda or not q.is_contiguous():
+                raise ValueError(f"block {i} must be a contiguous CUDA tensor of "
+                                 f"{' or '.join(str(d) for d in code_dtypes)}")
+            if q.dim() == 1:
+                n_rows, n_cols = 1, q.numel()
+            elif q.dim() == 2:
+                n_rows, n_cols = q.shape
+            else:
+                raise ValueError(f"block {i} must be 1-D or 2-D")
+            if sc.dtype != torch.float32 or not sc.is_cuda or not sc.is_contiguous():
+                raise ValueError(f"scales {i} must be a contiguous float32 CUDA tensor")
+            row = int(row)
+            need = 1 if row == 0 else -(-q.numel() // row)
+            if q.numel() and sc.numel() < need:
+                raise ValueError(f"scales {i} has {sc.numel()} entries, needs {need}")
+            arr[i] = EsQBlock(q.data_ptr() if q.numel() else None,
+                              sc.data_ptr() if q.numel() else None, n_rows, n_cols,
+                              _u64_arg(row_len, "row_len"), _u64_arg(row0, "row0"),
+                              _u64_arg(col0, "col0"), _u32_arg(row, "row"),
+                              _u32_arg(tid, "tensor_id"))
+            codes.append(q)
+            scales.append(sc)
+            ids.append(int(tid))
+        self._keep = (codes, scales)
+        self.tensor_ids = ids
+        self.device = codes[0].device
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            _check(load().es_qplan_create_blocks(arr, len(blocks), _QFORMATS[self.format],
+                                                 ctypes.byref(handle)), "es_qplan_create_blocks")
         self._h = handle
 
     @property

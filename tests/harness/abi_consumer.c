@@ -28,6 +28,13 @@ int main(void) {
            offsetof(es_update_opts_t, flags), offsetof(es_update_opts_t, round_seed));
     printf("flags %u %u %u max_members %u\n", ES_UPDATE_DIV_SIGMA, ES_REWARDS_ARE_WEIGHTS,
            ES_UPDATE_STOCHASTIC_ROUND, ES_MAX_MEMBERS);
+    printf("es_qblock_t %zu data %zu scales %zu rows %zu cols %zu row_len %zu row0 %zu "
+           "col0 %zu row %zu tensor_id %zu\n",
+           sizeof(es_qblock_t), offsetof(es_qblock_t, data), offsetof(es_qblock_t, scales),
+           offsetof(es_qblock_t, rows), offsetof(es_qblock_t, cols),
+           offsetof(es_qblock_t, row_len), offsetof(es_qblock_t, row0),
+           offsetof(es_qblock_t, col0), offsetof(es_qblock_t, row),
+           offsetof(es_qblock_t, tensor_id));
     es_plan_t* plan = NULL;
     printf("plan_create_null %d\n", es_plan_create(NULL, 1, &plan));
     printf("plan_create_blocks_null %d\n", es_plan_create_blocks(NULL, 1, &plan));
@@ -36,6 +43,8 @@ int main(void) {
     printf("qplan_create_null %d\n", es_qplan_create(NULL, 1, &qplan));
     printf("qplan_create_shards_null %d\n",
            es_qplan_create_shards(NULL, NULL, 1, ES_QFORMAT_E4M3, &qplan));
+    printf("qplan_create_blocks_null %d\n",
+           es_qplan_create_blocks(NULL, 1, ES_QFORMAT_INT8, &qplan));
     printf("strerror %s\n", es_strerror(ES_ERR_INVALID_ARG));
     printf("sigma_cosine %.17g\n", es_sigma_cosine(1e-3, 1e-4, 50, 100));
     return 0;

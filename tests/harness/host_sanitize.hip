@@ -1,8 +1,8 @@
 // Host-side checks of the library's own host code, built with AddressSanitizer
 // and UndefinedBehaviorSanitizer (host pass only, no device code): the
 // population tables of the update, the tiling of tensors and of blocks, the
-// int8 row divisor, and every argument check that fails before the device is
-// touched.
+// int8 row divisor, the geometry of quantized blocks, and every argument
+// check that fails before the device is touched.
 // The library source is compiled into this translation unit, so its internal
 // (anonymous-namespace) routines are reachable; each is compared with a plain
 // reference written here.  Prints "ok" and exits 0, or names the first
@@ -293,6 +293,63 @@ void test_row_divisor(std::mt19937_64& rng) {
     }
 }
 
+// Quantized blocks: the geometry rules of es_qblock_t against a plain
+// statement of them, and for every accepted block the kernels' index map
+// n0 + j + (j / cols) skip (the division as the device computes it) against
+// the whole-tensor index (row0 + i) row_len + col0 + c, j = i cols + c.
+void test_qblock_geometry(std::mt19937_64& rng) {
+    const uint64_t lim = uint64_t(1) << 31;
+    auto pick = [&](uint64_t hi) { return hi == 0 ? 0 : rng() % hi; };
+    int accepted = 0;
+    for (int t = 0; t < 20000; ++t) {
+        es_qblock_t b{};
+        const int scale = int(rng() % 4);
+        const uint64_t grain = (rng() % 4 == 0) ? 1 : 16;
+        b.row_len = grain * (1 + pick(scale == 3 ? (uint64_t(1) << 27) : 4096 / grain));
+        b.cols = 1 + pick(b.row_len + 2);
+        b.col0 = pick(b.row_len + 1);
+        if (rng() % 4 != 0) {                   // mostly blocks the rules allow
+            b.cols = std::max<uint64_t>(16, (b.cols / 16) * 16);
+            b.col0 = (b.col0 / 16) * 16;
+            if (b.col0 + b.cols > b.row_len) b.col0 = b.row_len >= b.cols ? (b.row_len - b.cols) / 16 * 16 : 0;
+        }
+        b.rows = pick(scale == 0 ? 3 : scale == 1 ? 64 : (uint64_t(1) << 16));
+        b.row0 = pick(scale == 3 ? (uint64_t(1) << 5) : (uint64_t(1) << 12));
+        if (rng() % 8 == 0) b.rows = (uint64_t(1) << 40) + pick(5);
+        QSpec spec{};
+        const std::string err = qblock_geometry(b, spec);
+        // the rules, stated plainly (products kept below 2^64 by the ranges above)
+        const uint64_t n = (b.rows == 0 || b.cols == 0) ? 0
+                           : (b.rows < lim && b.cols < lim) ? b.rows * b.cols : lim;
+        bool ok = n < lim;
+        if (ok && n > 0) {
+            const uint64_t first = b.row0 * b.row_len + b.col0;
+            const uint64_t end = (b.row0 + b.rows - 1) * b.row_len + b.col0 + b.cols;
+            const bool strided = b.rows > 1 && b.cols < b.row_len;
+            ok = b.col0 + b.cols <= b.row_len && end < lim && first % 16 == 0 &&
+                 (!strided || (b.cols % 16 == 0 && b.row_len % 16 == 0));
+        }
+        check(ok == err.empty(), "qblock geometry: accepted exactly when the rules hold");
+        if (!ok || n == 0) continue;
+        ++accepted;
+        check(spec.numel == n, "qblock geometry: numel");
+        uint32_t cmagic = 0, cshift = 0;
+        if (spec.skip != 0) row_divisor(uint32_t(spec.cols), cmagic, cshift);
+        bool map_ok = true;
+        for (int k = 0; k < 64; ++k) {
+            const uint64_t j = k < 2 ? (k == 0 ? 0 : n - 1) : pick(n);
+            uint64_t got = spec.n0 + j;
+            if (spec.skip != 0)
+                got += uint64_t((uint32_t((uint64_t(uint32_t(j)) * cmagic) >> 32) >> cshift)) *
+                       spec.skip;
+            const uint64_t exp = (b.row0 + j / b.cols) * b.row_len + b.col0 + j % b.cols;
+            map_ok &= got == exp && exp < lim;
+        }
+        check(map_ok, "qblock geometry: index map");
+    }
+    check(accepted > 5000, "qblock geometry: enough accepted blocks");
+}
+
 // Argument checks that must fail before any device access.
 void test_validation() {
     const uint64_t seeds[3] = {1, 2, 3};
@@ -379,6 +436,7 @@ int main() {
     test_tiling(rng);
     test_block_tiling(rng);
     test_row_divisor(rng);
+    test_qblock_geometry(rng);
     test_validation();
     if (g_failures) {
         std::printf("%d failures\n", g_failures);

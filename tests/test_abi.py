@@ -206,9 +206,11 @@ def test_plain_c_consumer_of_header(lib, tmp_path):
     assert rows["es_update_opts_t"] == layout(esopt.EsUpdateOpts)
     assert rows["es_qtensor_t"] == layout(esopt.EsQTensor)
     assert rows["es_block_t"] == layout(esopt.EsBlock)
+    assert rows["es_qblock_t"] == layout(esopt.EsQBlock)
     assert rows["plan_create_blocks_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["qplan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["qplan_create_shards_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
+    assert rows["qplan_create_blocks_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
                              str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
     assert rows["plan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
@@ -273,6 +275,37 @@ def test_quantized_shard_validation_without_gpu(lib):
     assert lib.es_qplan_create_shards(None, None, 1, 0, ctypes.byref(out)) == E
     assert lib.es_qplan_create_shards((T * 1)(T(fake, fake, 100, 0, 0)), None, 1, 0,
                                       None) == E
+
+
+def test_quantized_block_validation_without_gpu(lib):
+    """es_qplan_create_blocks rejects geometry the kernels cannot take (the
+    rules of es_qblock_t in the header) before any device call."""
+    fake = ctypes.c_void_p(0x10000)
+    out = ctypes.c_void_p()
+    B = esopt.EsQBlock
+    E = esopt.ES_ERR_INVALID_ARG
+
+    def create(*bs, fmt=esopt.QFORMAT_INT8):
+        return lib.es_qplan_create_blocks((B * len(bs))(*bs), len(bs), fmt, ctypes.byref(out))
+
+    def blk(rows, cols, row_len, row0=0, col0=0, row=0, tid=0, data=fake):
+        return B(data, fake, rows, cols, row_len, row0, col0, row, tid)
+    assert create(blk(4, 64, 100, 0, 48)) == E                     # col0 + cols > row_len
+    assert create(blk(1 << 16, 1 << 15, 1 << 16)) == E              # rows * cols = 2^31
+    assert create(blk(2, 64, 1 << 30, 1, 0)) == E                   # last index reaches 2^31
+    assert create(blk(4, 64, 256, 0, 8)) == E                       # first index not / 16
+    assert create(blk(4, 24, 256, 0, 16)) == E                      # strided, cols not / 16
+    assert create(blk(4, 64, 264, 0, 16)) == E                      # strided, row_len not / 16
+    assert create(blk(4, 64, 256, 0, 16, row=12)) == E              # row not / 8
+    assert create(blk(4, 64, 256, data=None)) == E                  # null codes
+    assert create(blk(4, 64, 256, tid=3), blk(4, 64, 256, tid=3,
+                                             data=ctypes.c_void_p(0x20000))) == E  # duplicate id
+    assert create(blk(4, 64, 256, tid=1), blk(4, 64, 256, tid=2,
+                                             data=ctypes.c_void_p(0x10010))) == E  # overlap
+    assert create(blk(4, 64, 256), fmt=9) == E                      # unknown format
+    assert lib.es_qplan_create_blocks(None, 1, 0, ctypes.byref(out)) == E
+    assert lib.es_qplan_create_blocks((B * 1)(blk(4, 64, 256)), 0, 0, ctypes.byref(out)) == E
+    assert lib.es_qplan_create_blocks((B * 1)(blk(4, 64, 256)), 1, 0, None) == E
 
 
 def test_binding_range_checks_integer_arguments():

@@ -1,0 +1,170 @@
+"""Quantized plans over blocks (es_qplan_create_blocks): column shards of a
+matrix with one scale per row, a 2 x 2 grid of ragged blocks of a matrix
+with a scale per 64 codes of a row, and one-row pieces of a vector, as the
+GPUs of a tensor-parallel group hold them.  Every int8 and E4M3 pass over
+each GPU's blocks leaves exactly the codes the same pass over the whole
+tensors leaves there; block checksums add up to the whole plan's and match
+the oracle's at whole-tensor indices; and a column block matches the oracle
+element by element at whole-tensor indices (Section 3)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_17310_amd import esopt
+from parity import assert_qparity, qreport
+from test_gpu_fp8 import _codes as _f8codes
+from test_gpu_quant import _codes as _i8codes, _perturb_expect
+
+pytestmark = pytest.mark.gpu
+
+MASK = (1 << 64) - 1
+R1, C1 = 300, 2048                  # one scale per row
+R2, C2, G2 = 96, 640, 64            # one scale per 64 codes of a row
+N3 = 5000                           # one scale
+IDS = [7, 8, 9]
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _dev(a, pad=0):
+    """A device copy of the bytes of a, at byte offset pad of its allocation."""
+    a = np.ascontiguousarray(a)
+    buf = torch.zeros(a.size + pad + 16, dtype=torch.uint8, device="cuda")
+    v = buf[pad:pad + a.size]
+    v.copy_(torch.from_numpy(a.reshape(-1).view(np.uint8)).cuda())
+    return v.view(a.shape)
+
+
+def _f32dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32).reshape(-1)).cuda()
+
+
+def _host(t):
+    return t.cpu().numpy().copy()
+
+
+def _set(fmt, seed):
+    make = (lambda n, s: _i8codes(n, s).view(np.uint8)) if fmt == "int8" else _f8codes
+    rng = np.random.default_rng(seed)
+    lo, hi = (2e-4, 1e-3) if fmt == "int8" else (1.5e-4, 3e-4)
+    codes = [make(R1 * C1, seed).reshape(R1, C1), make(R2 * C2, seed + 1).reshape(R2, C2),
+             make(N3, seed + 2)]
+    scales = [rng.uniform(lo, hi, R1), rng.uniform(lo, hi, (R2, C2 // G2)),
+              rng.uniform(lo, hi, 1)]
+    return codes, [s.astype(np.float32) for s in scales]
+
+
+def _gpu_blocks(codes, scales, k):
+    """GPU k's share, as (codes, scales, row, row_len, row0, col0, pad) per
+    tensor: a 512-column shard of matrix 1, one block of the 2 x 2 grid of
+    matrix 2, a one-row piece of the vector."""
+    c1 = 512
+    rs, cs = [(0, 40), (40, R2)], [(0, 320), (320, C2)]
+    (r0, r1), (a, b) = rs[k // 2], cs[k % 2]
+    cuts = [0, 1296, 2512, 3760, N3]
+    return [
+        (codes[0][:, c1 * k:c1 * (k + 1)], scales[0], c1, C1, 0, c1 * k, [0, 3, 16, 1][k]),
+        (codes[1][r0:r1, a:b], scales[1][r0:r1, a // G2:b // G2], G2, C2, r0, a, 0),
+        (codes[2][cuts[k]:cuts[k + 1]], scales[2], 0, N3, 0, cuts[k], k),
+    ]
+
+
+def _views(parts, fmt):
+    out = []
+    for c, *_, pad in parts:
+        v = _dev(c, pad)
+        out.append(v.view(torch.int8) if fmt == "int8" else v)
+    return out
+
+
+def _passes(plan):
+    r = torch.tensor([0.4, 0.9, 0.1, 0.6], device="cuda")
+    plan.perturb(11, 1, 1e-3)
+    plan.restore(11, 1, 1e-3)
+    plan.perturb(12, -1, 1.5e-3)
+    plan.update([12, 13, 13, 14], [-1, 1, -1, 1], r, 5e-4, sigma=1e-3, round_seed=7)
+    plan.update([15, 16], [1, 1], r[:2], 2e-3, sigma=1e-3, round_seed=(1 << 40) + 3,
+                flags=esopt.ES_UPDATE_DIV_SIGMA)
+
+
+def _whole_indices(shape, row_len, row0, col0):
+    rows, cols = shape if len(shape) == 2 else (1, shape[0])
+    i = np.arange(rows, dtype=np.uint64)[:, None] + np.uint64(row0)
+    j = np.arange(cols, dtype=np.uint64)[None, :] + np.uint64(col0)
+    return (i * np.uint64(row_len) + j).reshape(-1)
+
+
+@pytest.mark.parametrize("fmt", ["int8", "e4m3"])
+def test_blocks_leave_the_whole_plans_codes(fmt):
+    codes, scales = _set(fmt, 70)
+    whole = _views([(c, None, None, None, None, None, 0) for c in codes], fmt)
+    flat = [w.reshape(-1) for w in whole]
+    with esopt.QPlan(flat, [_f32dev(s) for s in scales], [C1, G2, 0], tensor_ids=IDS,
+                     format=fmt) as pw:
+        _passes(pw)
+        total = pw.checksum()
+    torch.cuda.synchronize()
+    expect = [_host(w).view(np.uint8) for w in whole]
+    sums = 0
+    for k in range(4):
+        parts = _gpu_blocks(codes, scales, k)
+        views = _views(parts, fmt)
+        blocks = [esopt.QBlock(v, _f32dev(sc), row, tid, row_len, r0, c0)
+                  for v, (_, sc, row, row_len, r0, c0, _), tid in zip(views, parts, IDS)]
+        with esopt.QPlan(blocks=blocks, format=fmt) as pb:
+            assert pb.numel == sum(v.numel() for v in views)
+            _passes(pb)
+            got = pb.checksum()
+        torch.cuda.synchronize()
+        sums = (sums + got) & MASK
+        exp_sum = 0
+        for i, (v, (c, _, _, row_len, r0, c0, _)) in enumerate(zip(views, parts)):
+            el = _whole_indices(c.shape, row_len, r0, c0)
+            np.testing.assert_array_equal(_host(v).view(np.uint8).reshape(-1),
+                                          expect[i].reshape(-1)[el.astype(np.int64)],
+                                          err_msg=f"{fmt} GPU {k} tensor {i}")
+            b = _host(v).view(np.uint8).reshape(-1)
+            exp_sum += sum(oracle.qchecksum(b[s:s + c.shape[-1]], IDS[i], int(e))
+                           for s, e in zip(range(0, b.size, c.shape[-1]),
+                                           el[::c.shape[-1]]))
+        assert got == exp_sum & MASK
+    assert sums == total
+    assert np.mean(expect[0] != codes[0]) > 0.3          # the passes moved codes
+
+
+def test_int8_column_block_matches_oracle_at_whole_tensor_indices():
+    codes, scales = _set("int8", 80)
+    c, sc, row, row_len, r0, c0, _ = _gpu_blocks(codes, scales, 2)[0]
+    q = c.view(np.int8)
+    v = _dev(q, 3).view(torch.int8)
+    with esopt.QPlan(blocks=[esopt.QBlock(v, _f32dev(sc), row, 21, row_len, r0, c0)]) as p:
+        p.perturb(31, -1, 1e-3)
+    torch.cuda.synchronize()
+    el = _whole_indices(c.shape, row_len, r0, c0)
+    d, ok, tol = _perturb_expect(scales[0], C1, 31, 21, -1, 1e-3, el)
+    rep = qreport(_host(v).reshape(-1), q.reshape(-1), d, tol, ok)
+    print("int8 column block vs oracle:", rep)
+    assert_qparity(rep, "int8 column block")
+
+
+def test_block_arguments_are_checked_by_the_binding():
+    q = torch.zeros(4, 64, dtype=torch.int8, device="cuda")
+    s = torch.ones(4, device="cuda")
+    with pytest.raises(ValueError):
+        esopt.QPlan([q.reshape(-1)], [s], [0], blocks=[esopt.QBlock(q, s, 64, 0, 256)])
+    with pytest.raises(ValueError):
+        esopt.QPlan(blocks=[esopt.QBlock(q.float(), s, 64, 0, 256)])
+    with pytest.raises(ValueError):
+        esopt.QPlan(blocks=[esopt.QBlock(q, s[:1], 64, 0, 256)])        # too few scales
+    with pytest.raises(esopt.EsError):
+        esopt.QPlan(blocks=[esopt.QBlock(q, s, 64, 0, 256, 0, 8)])      # first index
+    with pytest.raises(esopt.EsError):
+        esopt.QPlan(blocks=[esopt.QBlock(q, s, 64, 0, 48)])             # cols > row_len
+    with esopt.QPlan(blocks=[esopt.QBlock(q, s, 64, 0, 256, 3, 192)], format="int8") as p:
+        assert p.numel == 256

@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 from paper_2608_17310_amd import esopt
 from parity import assert_f8parity, assert_qparity, qreport
 from test_gpu_fp8 import _codes as _f8codes, _perturb_report as _f8perturb_report
@@ -106,11 +107,14 @@ def test_shards_leave_the_whole_plans_codes(fmt):
                          format=fmt, offsets=offs) as ps:
             assert ps.numel == sum(c.size for c in cs)
             _passes(ps)
-            sums = (sums + ps.checksum()) & MASK
+            got = ps.checksum()
+            sums = (sums + got) & MASK
         torch.cuda.synchronize()
         for i, (v, (n, row, cuts)) in enumerate(zip(views, TENSORS)):
             np.testing.assert_array_equal(_host(v).view(np.uint8), expect[i][cuts[k]:cuts[k + 1]],
                                           err_msg=f"{fmt} shard {k} of tensor {i}")
+        assert got == sum(oracle.qchecksum(_host(v), tid, o)
+                          for v, tid, o in zip(views, ids, offs)) & MASK
     assert sums == total
     assert np.mean(expect[0] != codes[0]) > 0.3          # the passes moved codes
 

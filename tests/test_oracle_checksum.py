@@ -112,6 +112,11 @@ def test_int8_codes_are_summed_as_unsigned_bytes():
     codes = np.random.default_rng(8).integers(-128, 128, size=999).astype(np.int8)
     assert oracle.qchecksum(codes, 6) == _bigint_checksum(codes.view(np.uint8), 6, 0)
     assert oracle.qchecksum(codes, 6, chunk=100) == oracle.qchecksum(codes, 6)
+    assert oracle.qchecksum(codes, 6, 1 << 30) == _bigint_checksum(codes.view(np.uint8), 6,
+                                                                    1 << 30)
+    cut = 512                                   # a shard at a whole-tensor offset
+    assert (oracle.qchecksum(codes[:cut], 6) + oracle.qchecksum(codes[cut:], 6, cut)) & M == \
+        oracle.qchecksum(codes, 6)
     x = codes.copy()
     x[17] = -x[17] if x[17] not in (0, -128) else 5
     assert oracle.qchecksum(x, 6) != oracle.qchecksum(codes, 6)
