@@ -395,12 +395,19 @@ def run_quantized(args):
     torch.cuda.synchronize()
     log = EventLog(torch, stream)
 
-    def run_step(t, record):
+    def run_step(t, record, swap=False):
         seeds = step_seeds(W, t, n_members)
         sigma = sigma_at(esopt.sigma_cosine, W, t)
-        for sd, sg in zip(seeds, signs):
-            log.call("es_qperturb", record, plan.perturb, sd, sg, sigma)
-            log.call("es_qrestore", record, plan.restore, sd, sg, sigma)
+        if swap:
+            log.call("es_qperturb", record, plan.perturb, seeds[0], signs[0], sigma)
+            for i in range(N - 1):
+                log.call("es_qswap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
+                         signs[i + 1], sigma)
+            log.call("es_qrestore", record, plan.restore, seeds[-1], signs[-1], sigma)
+        else:
+            for sd, sg in zip(seeds, signs):
+                log.call("es_qperturb", record, plan.perturb, sd, sg, sigma)
+                log.call("es_qrestore", record, plan.restore, sd, sg, sigma)
         log.call("es_qupdate", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
                  sigma=sigma, round_seed=1000 + t)
 
@@ -411,6 +418,18 @@ def run_quantized(args):
     per = log.ms()
     t_pert = median_s(per["es_qperturb"] + per["es_qrestore"])
     t_upd = median_s(per["es_qupdate"])
+    # the same generations with the members moved by fused swaps (es_qperturb,
+    # N - 1 es_qswap, es_qrestore, es_qupdate), timed in the same run after
+    # one untimed generation
+    swap = None
+    if not args.no_swap_walk and N > 1:
+        log.ev = []
+        run_step(args.warmup, record=False, swap=True)
+        ms_swap, wall_swap = timed_region(
+            torch, stream, args.steps, lambda i: run_step(args.warmup + i, record=True, swap=True))
+        per_sw = log.ms()
+        swap = {"ms_step": ms_swap, "wall": wall_swap, "t_swap": median_s(per_sw["es_qswap"]),
+                "calls": len(per_sw["es_qswap"])}
     value = (2 * N + 1) * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
@@ -418,6 +437,7 @@ def run_quantized(args):
     label = f"{W.name}-{tag}"
     c_pert = _counters_for(args.counters_json, f"es_{'f8' if args.fp8 else 'q'}perturb", label)
     c_upd = _counters_for(args.counters_json, f"es_{'f8' if args.fp8 else 'q'}update", label)
+    c_swap = _counters_for(args.counters_json, f"es_{'f8' if args.fp8 else 'q'}swap", label)
 
     def alu_roofline(c, t, kernel, extra):
         r = {"bound": "alu", "unit": "T lane-instr/s", "peak": round(VALU_PEAK_TINST, 2),
@@ -460,6 +480,18 @@ def run_quantized(args):
         "wall_s_timed": round(wall, 3),
         "cpu_baseline": cpu,
     }
+    if swap is not None:
+        t_sw = swap["t_swap"]
+        out["per_kernel"]["es_qswap"] = {"ms": round(t_sw * 1e3, 3), "params_per_s": P / t_sw,
+                                         "normals_per_s": 2 * P / t_sw, "calls": swap["calls"],
+                                         "ms_over_perturb_restore": round(t_sw / (2 * t_pert), 4)}
+        out["ms_per_step_swap"] = round(swap["ms_step"], 3)
+        out["swap_walk"] = {
+            "member_moves": "es_qperturb, N-1 fused es_qswap, es_qrestore, then es_qupdate",
+            "ms_per_step": round(swap["ms_step"], 3),
+            "speedup_vs_perturb_restore": round(ms_step / swap["ms_step"], 4),
+            "wall_s_timed": round(swap["wall"], 3),
+            "roofline": alu_roofline(c_swap, t_sw, f"es_qpass_kernel, {fmt} (es_qswap)", True)}
     print(json.dumps(out))
     plan.close()
 
@@ -860,7 +892,9 @@ def run_profile_pass(args):
     QP = qplan.numel
     for _ in range(R):
         log.add("es_qperturb", "int8", QP, 2 * QP, QP, qplan.perturb, seeds[0], signs[0], s0)
-        log.add("es_qrestore", "int8", QP, 2 * QP, QP, qplan.restore, seeds[0], signs[0], s0)
+        log.add("es_qswap", "int8", QP, 2 * QP, 2 * QP, qplan.swap, seeds[0], signs[0],
+                seeds[1], signs[1], s0)
+        log.add("es_qrestore", "int8", QP, 2 * QP, QP, qplan.restore, seeds[1], signs[1], s0)
     log.add(f"es_qupdate (N={N})", "int8", QP, 2 * QP, nd * QP, qplan.update, seeds, signs,
             rewards, W.alpha, sigma=s0, round_seed=1, repeat=R)
     torch.cuda.synchronize()
@@ -872,7 +906,9 @@ def run_profile_pass(args):
     fplan = esopt.QPlan(fviews, fscales, frows, format="e4m3")
     for _ in range(R):
         log.add("es_f8perturb", "fp8", QP, 2 * QP, QP, fplan.perturb, seeds[0], signs[0], s0)
-        log.add("es_f8restore", "fp8", QP, 2 * QP, QP, fplan.restore, seeds[0], signs[0], s0)
+        log.add("es_f8swap", "fp8", QP, 2 * QP, 2 * QP, fplan.swap, seeds[0], signs[0],
+                seeds[1], signs[1], s0)
+        log.add("es_f8restore", "fp8", QP, 2 * QP, QP, fplan.restore, seeds[1], signs[1], s0)
     log.add(f"es_f8update (N={N})", "fp8", QP, 2 * QP, nd * QP, fplan.update, seeds, signs,
             rewards, W.alpha, sigma=s0, round_seed=1, repeat=R)
     torch.cuda.synchronize()
@@ -977,7 +1013,8 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
     keys = {"es_perturb": "es_perturb", f"es_update (N={lab['members']}, nearest-even)": "es_update",
             "es_swap (two keys)": "es_swap", "es_qperturb": "es_qperturb",
             f"es_qupdate (N={lab['members']})": "es_qupdate", "es_f8perturb": "es_f8perturb",
-            f"es_f8update (N={lab['members']})": "es_f8update"}
+            f"es_f8update (N={lab['members']})": "es_f8update", "es_qswap": "es_qswap",
+            "es_f8swap": "es_f8swap"}
     for group, (stem, title) in groups.items():
         rows = [r for r in per["_rows"] if r["group"] == group]
         if not rows:

@@ -345,7 +345,7 @@ int es_qplan_create(const es_qtensor_t* tensors, uint32_t n_tensors, es_qplan_t*
  * 8-bit floating-point format with 4 exponent and 3 mantissa bits, bias 7
  * (PyTorch's float8_e4m3fn): theta_j = s_r v(c_j), v up to +-448, codes 0x7F
  * and 0xFF not a number; the scales, rows, ids and limits are as for int8.
- * The passes of the plan (es_qperturb, es_qrestore, es_qupdate,
+ * The passes of the plan (es_qperturb, es_qrestore, es_qswap, es_qupdate,
  * es_qplan_checksum) then work on the E4M3 grid (Appendix A.2's quantized
  * ES, the library's reading): a pass forms x = v(c) + step, in scale units
  * and binary32, and rounds it onto the grid stochastically --
@@ -442,6 +442,17 @@ uint64_t es_qplan_device_bytes(const es_qplan_t* plan);   /* as es_plan_device_b
  * runs). */
 int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
 int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream);
+
+/* Revert one member and apply the next in one pass over the codes (the move
+ * between candidates of Section 3 and Appendix D.6, as es_swap): exactly the
+ * codes of es_qrestore(seed_from, sign_from, sigma_from) followed by
+ * es_qperturb(seed_to, sign_to, sigma_to), both computed per code in
+ * registers.  The passes are VALU-bound, so the fusion saves the second
+ * pass's load, decode, pack and store (not its noise).  A zero sigma makes
+ * its half the identity (the other half runs alone); both zero launches
+ * nothing.  Signs +1 or -1; sigmas finite and >= 0. */
+int es_qswap(es_qplan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
+             uint64_t seed_to, int32_t sign_to, float sigma_to, es_stream_t stream);
 
 /* Update (Section 3 / Appendix C.1, in quanta): the z-score, coefficient and
  * merged weights of es_update, d_j = sum_d w_d eps_j(seed_d) / s_r,

@@ -1073,12 +1073,14 @@ UpdateKernel update_kernel(int threads, int groups, bool stochastic, bool rows,
 
 // ---- int8 path (device code of the passes; helpers in es_quant.hpp) ----
 
-// Kernel arguments of one int8 pass: the key of the update's rounding
-// draws, and for perturb / restore the single member inline.
+// Kernel arguments of one quantized pass: the key of the update's rounding
+// draws, and for perturb / restore the single member inline (for a swap, m is
+// the member applied and m_from the member reverted before it).
 struct QPass {
     uint32_t dk0, dk1;
     uint32_t pad0, pad1;
     Member m;
+    Member m_from;
 };
 
 // Perturb / restore of one 16-code group (n: the whole-tensor index of its
@@ -1156,11 +1158,27 @@ __device__ __forceinline__ void f8perturb_group(const uint32_t raw[4], uint32_t 
     }
 }
 
+// Perturb (kNegate false) or restore of one 16-code group in the plan's
+// format, codes with an invalid scale or a not-a-number code left as they are.
+template <bool kNegate, int kFmt>
+__device__ __forceinline__ void qmember_group(const uint32_t raw[4], uint32_t n,
+                                              uint32_t tensor_id, const Member& m, float inv0,
+                                              float inv1, uint32_t out[4]) {
+    if constexpr (kFmt == kFmtE4M3) {
+        f8perturb_group<kNegate>(raw, n, tensor_id, m, inv0, inv1, out);
+        esf::keep_special(raw, inv0, inv1, out);
+    } else {
+        qperturb_group<kNegate>(raw, n, tensor_id, m, inv0, inv1, out);
+    }
+}
+
 // One tile of an int8 pass: for each of the lane's 16-code groups in turn,
 // the step d in quanta (binary32) and the stochastically rounded, clamped
 // code.  e indexes the codes and scales at hand; n, the whole-tensor index
 // of code e, selects the noise and the rounding draws.
-template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate, int kFmt>
+// kSwap: the member ps.m_from reverted and ps.m applied in registers, the
+// codes of the two separate passes.
+template <int kThreads, int kU, bool kFast, bool kTable, bool kNegate, int kFmt, bool kSwap>
 __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __restrict__ members,
                                       uint32_t n_members, const QPass& ps) {
     const uint32_t e0 = r.elem0 + threadIdx.x * esq::kQGroup;
@@ -1174,11 +1192,12 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
         float inv0, inv1;
         esq::group_inv_scales(r, e, inv0, inv1);
         uint32_t out[4];
-        if constexpr (!kTable && kFmt == kFmtE4M3) {
-            f8perturb_group<kNegate>(raw, n, r.tensor_id, ps.m, inv0, inv1, out);
-            esf::keep_special(raw, inv0, inv1, out);
+        if constexpr (kSwap) {
+            uint32_t mid[4];
+            qmember_group<true, kFmt>(raw, n, r.tensor_id, ps.m_from, inv0, inv1, mid);
+            qmember_group<false, kFmt>(mid, n, r.tensor_id, ps.m, inv0, inv1, out);
         } else if constexpr (!kTable) {
-            qperturb_group<kNegate>(raw, n, r.tensor_id, ps.m, inv0, inv1, out);
+            qmember_group<kNegate, kFmt>(raw, n, r.tensor_id, ps.m, inv0, inv1, out);
         } else {
             float acc[16];
 #pragma unroll
@@ -1237,7 +1256,7 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
 // (one inline member, draws from its own noise words) or the update (member
 // table and header written by es_prepare_kernel, draws of domain 1 under the
 // rounding seed).
-template <int kThreads, int kU, bool kTable, bool kNegate, int kFmt>
+template <int kThreads, int kU, bool kTable, bool kNegate, int kFmt, bool kSwap>
 __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTensor* __restrict__ tab,
                                                             uint64_t n_full, uint64_t n_tail,
                                                             const Member* __restrict__ members,
@@ -1251,28 +1270,29 @@ __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTenso
     }
     uint32_t t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        qtile<kThreads, kU, true, kTable, kNegate, kFmt>(
+        qtile<kThreads, kU, true, kTable, kNegate, kFmt, kSwap>(
             esq::qlocate_full<kTileElems>(tab, t, tile), members, n_members, ps);
     t = 0;
     for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        qtile<kThreads, kU, false, kTable, kNegate, kFmt>(
+        qtile<kThreads, kU, false, kTable, kNegate, kFmt, kSwap>(
             esq::qlocate_tail<kTileElems>(tab, t, tile), members, n_members, ps);
 }
 
 using QPassKernel = void (*)(const esq::DevQTensor*, uint64_t, uint64_t, const Member*,
                              const UpdateHeader*, QPass);
 
-enum class QKind { kPerturb, kRestore, kUpdate };
+enum class QKind { kPerturb, kRestore, kUpdate, kSwap };
 
 template <int kFmt>
 QPassKernel qpass_kernel_for(int threads, int groups, QKind kind) {
-#define ES_CASE(T, U)                                                                  \
-    if (threads == T && groups == U) {                                                 \
-        switch (kind) {                                                                \
-            case QKind::kPerturb: return es_qpass_kernel<T, U, false, false, kFmt>;    \
-            case QKind::kRestore: return es_qpass_kernel<T, U, false, true, kFmt>;     \
-            case QKind::kUpdate: return es_qpass_kernel<T, U, true, false, kFmt>;      \
-        }                                                                              \
+#define ES_CASE(T, U)                                                                      \
+    if (threads == T && groups == U) {                                                     \
+        switch (kind) {                                                                    \
+            case QKind::kPerturb: return es_qpass_kernel<T, U, false, false, kFmt, false>; \
+            case QKind::kRestore: return es_qpass_kernel<T, U, false, true, kFmt, false>;  \
+            case QKind::kUpdate: return es_qpass_kernel<T, U, true, false, kFmt, false>;   \
+            case QKind::kSwap: return es_qpass_kernel<T, U, false, false, kFmt, true>;     \
+        }                                                                                  \
     }
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
@@ -1476,6 +1496,14 @@ int launch_qpass(es_qplan_t* p, QKind kind, const QPass& ps, hipStream_t s) {
     return ES_OK;
 }
 
+// The kernel argument of one perturbation member of a quantized pass: its
+// key and sign * sigma * sqrt(2 ln 2) (a restore negates in the kernel).
+Member qmember(uint64_t seed, int32_t sign, float sigma) {
+    const double coef = sign > 0 ? double(sigma) : -double(sigma);
+    return Member{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                  static_cast<float>(coef * kSqrt2Ln2Double), 0u};
+}
+
 int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_stream_t stream,
                   QKind kind, const char* name) {
     if (p == nullptr) return fail(ES_ERR_INVALID_ARG, std::string(name) + ": null plan");
@@ -1486,10 +1514,8 @@ int qperturb_impl(es_qplan_t* p, uint64_t seed, int32_t sign, float sigma, es_st
     if (sigma == 0.0f) return ES_OK;
     const int rc = check_qdevice(p);
     if (rc != ES_OK) return rc;
-    const double coef = sign > 0 ? double(sigma) : -double(sigma);
     QPass ps = {};
-    ps.m = Member{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
-                  static_cast<float>(coef * kSqrt2Ln2Double), 0u};
+    ps.m = qmember(seed, sign, sigma);
     return launch_qpass(p, kind, ps, static_cast<hipStream_t>(stream));
 }
 
@@ -2471,6 +2497,29 @@ int es_qperturb(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_s
 
 int es_qrestore(es_qplan_t* plan, uint64_t seed, int32_t sign, float sigma, es_stream_t stream) {
     return qperturb_impl(plan, seed, sign, sigma, stream, QKind::kRestore, "es_qrestore");
+}
+
+int es_qswap(es_qplan_t* plan, uint64_t seed_from, int32_t sign_from, float sigma_from,
+             uint64_t seed_to, int32_t sign_to, float sigma_to, es_stream_t stream) {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qswap: null plan");
+    if ((sign_from != 1 && sign_from != -1) || (sign_to != 1 && sign_to != -1))
+        return fail(ES_ERR_INVALID_ARG, "es_qswap: signs must be +1 or -1");
+    if (!std::isfinite(sigma_from) || sigma_from < 0.0f || !std::isfinite(sigma_to) ||
+        sigma_to < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, "es_qswap: sigmas must be finite and >= 0");
+    // es_qrestore(from) then es_qperturb(to); a zero sigma makes its half the
+    // identity, as in those calls (its pass would still clamp codes)
+    if (sigma_from == 0.0f)
+        return qperturb_impl(plan, seed_to, sign_to, sigma_to, stream, QKind::kPerturb, "es_qswap");
+    if (sigma_to == 0.0f)
+        return qperturb_impl(plan, seed_from, sign_from, sigma_from, stream, QKind::kRestore,
+                             "es_qswap");
+    const int rc = check_qdevice(plan);
+    if (rc != ES_OK) return rc;
+    QPass ps = {};
+    ps.m = qmember(seed_to, sign_to, sigma_to);
+    ps.m_from = qmember(seed_from, sign_from, sigma_from);
+    return launch_qpass(plan, QKind::kSwap, ps, static_cast<hipStream_t>(stream));
 }
 
 int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,

@@ -97,6 +97,7 @@ SIGNATURES = {
                                               ctypes.POINTER(_vp)]),
     "es_qplan_create_blocks": (ctypes.c_int, [ctypes.POINTER(EsQBlock), _u32, _u32,
                                               ctypes.POINTER(_vp)]),
+    "es_qswap": (ctypes.c_int, [_vp, _u64, _i32, _f32, _u64, _i32, _f32, _vp]),
     "es_qplan_destroy": (ctypes.c_int, [_vp]),
     "es_qplan_numel": (_u64, [_vp]),
     "es_qplan_device_bytes": (_u64, [_vp]),
@@ -536,6 +537,14 @@ class QPlan:
     def restore(self, seed, sign, sigma, stream=None):
         _check(load().es_qrestore(self.handle, _u64_arg(seed, "seed"), int(sign), float(sigma),
                                   _stream(stream)), "es_qrestore")
+
+    def swap(self, seed_from, sign_from, seed_to, sign_to, sigma, sigma_to=None, stream=None):
+        """Revert member `from` and apply member `to` in one pass: the same
+        codes as restore(from) followed by perturb(to)."""
+        sigma_to = sigma if sigma_to is None else sigma_to
+        _check(load().es_qswap(self.handle, _u64_arg(seed_from, "seed_from"), int(sign_from),
+                               float(sigma), _u64_arg(seed_to, "seed_to"), int(sign_to),
+                               float(sigma_to), _stream(stream)), "es_qswap")
 
     def checksum(self, out=None, stream=None):
         """64-bit checksum of the codes (es_qplan_checksum); as Plan.checksum."""

@@ -11,7 +11,8 @@ pass (es_swap), and the last member's revert is made in the update's pass
 (es_restore_update), so a generation of N members makes N passes over the
 parameters instead of 2N, plus the update; the bits are those of the
 separate passes.  The same driver runs the quantized paths (esopt.QPlan, int8
-or E4M3 codes), which have no fused passes.
+or E4M3 codes), whose swaps are fused too (es_qswap); their last member is
+reverted in a pass of its own.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
@@ -95,7 +96,6 @@ def _fuses_last_revert(plan, fused_swap):
 def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream, revert_last=True):
     """Apply member 0, visit it, move to member 1, ... and revert the last
     (unless revert_last is false: the update then reverts it).
-    Plans without a fused swap (the quantized QPlan) revert and apply separately.
     When the passes run on a stream other than PyTorch's current one, each
     visit is ordered after its member's pass and the next pass after the
     visit's work on the current stream, so an evaluation that reads the
@@ -129,8 +129,7 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
     stream (or is finished when it returns); the passes go on `stream`.  With ES_UPDATE_STOCHASTIC_ROUND in flags the
     update is rounded with the draws of round_seed (use a new one per
     generation).  With checksum, the parameters' checksum after the update
-    is recorded (a bf16 Plan only), so that replay() can verify the rebuilt
-    parameters.  Returns the GenerationRecord."""
+    is recorded, so that replay() can verify the rebuilt parameters.  Returns the GenerationRecord."""
     if len(seeds) != len(signs) or not seeds:
         raise ValueError("seeds and signs must be non-empty and of equal length")
     if checksum and not hasattr(plan, "checksum"):

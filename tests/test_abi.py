@@ -241,6 +241,10 @@ def test_quantized_plan_validation_without_gpu(lib):
     assert lib.es_qrestore(None, 1, 1, 1e-3, None) == E
     assert lib.es_qperturb(fake, 1, 0, 1e-3, None) == E
     assert lib.es_qperturb(fake, 1, 1, float("nan"), None) == E
+    assert lib.es_qswap(None, 1, 1, 1e-3, 2, 1, 1e-3, None) == E
+    assert lib.es_qswap(fake, 1, 2, 1e-3, 2, 1, 1e-3, None) == E          # sign
+    assert lib.es_qswap(fake, 1, 1, 1e-3, 2, -1, -1e-3, None) == E        # sigma
+    assert lib.es_qswap(fake, 1, 1, float("inf"), 2, 1, 1e-3, None) == E
     seeds = (ctypes.c_uint64 * 2)(1, 2)
     signs = (ctypes.c_int32 * 2)(1, 1)
     opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0, 0)
