@@ -50,11 +50,11 @@ def test_plans_and_passes_allocate_no_parameter_sized_memory():
     qplan = esopt.QPlan(codes, scales, [4096, 4096])
     f1 = _free()
     print("plans took", (f0 - f1) / MB, "MiB")
-    # what the plans report: the member scratch plus, for the int8 plan, a
-    # table entry per tensor and, for the bf16 plan, a 32-byte descriptor per
-    # tile (65 536 elements)
+    # what the plans report: the member scratch plus, for the int8 plan, an
+    # 80-byte table entry per tensor (and a sentinel) and, for the bf16 plan,
+    # a 32-byte descriptor per tile (65 536 elements)
     assert qplan.device_bytes < 64 * 1024
-    scratch = qplan.device_bytes - 64 * (len(codes) + 1)
+    scratch = qplan.device_bytes - 80 * (len(codes) + 1)
     assert plan.device_bytes == 32 * plan.tiles + scratch
     assert plan.tiles <= sum(-(-p.numel() // 65536) + 1 for p in params)
     assert plan.device_bytes < 512 * 1024                   # for 1 GiB of parameters
