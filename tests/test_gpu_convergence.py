@@ -1,0 +1,104 @@
+"""End to end: the library's passes, driven by the generation driver,
+optimise a synthetic objective by ES (Section 3: apply, evaluate, revert,
+z-score, update).  The reward of a parameter vector theta (65 536 values in
+two tensors) is -||B theta - y||^2 for a fixed random 4 x 65 536 matrix B,
+so, as in the paper's setting, a few directions of a large parameter space
+decide the reward.  Over 60 one-sided generations of 32 members the loss
+falls well below its start for bf16 (nearest-even and stochastically rounded
+updates), int8 and E4M3 codes; with the reward's sign flipped it rises (the
+update climbs the reward, it does not merely move)."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_17310_amd import esopt
+from paper_2608_17310_amd.generation import run_generation
+
+pytestmark = pytest.mark.gpu
+
+P, K, N, G = 1 << 16, 4, 32, 60
+SIGMA, ALPHA = 2e-3, 1e-2
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    torch.cuda.set_device(0)
+
+
+def _problem():
+    rng = np.random.default_rng(2026)
+    B = torch.from_numpy(rng.standard_normal((K, P)) / np.sqrt(P)).float().cuda()
+    y = torch.from_numpy(rng.normal(0.0, 0.5, K)).float().cuda()
+    return B, y
+
+
+def _run(make, theta_of, flags=0, climb=True):
+    """Loss before and after G generations; make() returns (plan, tensors)."""
+    B, y = _problem()
+    plan, _ = make()
+
+    def loss():
+        return float(((B @ theta_of()) - y).square().sum())
+
+    def evaluate(i):
+        return -loss() if climb else loss()
+    start = loss()
+    for g in range(G):
+        seeds = [100_000 * (g + 1) + i for i in range(N)]
+        run_generation(plan, seeds, [1] * N, SIGMA, ALPHA, evaluate, flags=flags,
+                       round_seed=g)
+    end = loss()
+    plan.close()
+    print(f"loss {start:.4f} -> {end:.4f} ({end / start:.3f})")
+    return start, end
+
+
+def _bf16():
+    ts = [torch.zeros(P // 2, dtype=torch.bfloat16, device="cuda") for _ in range(2)]
+    return esopt.Plan(ts), ts
+
+
+@pytest.mark.parametrize("flags", [0, esopt.ES_UPDATE_STOCHASTIC_ROUND],
+                         ids=["nearest-even", "stochastic"])
+def test_bf16_es_reduces_the_loss(flags):
+    holder = {}
+
+    def make():
+        holder["plan"], holder["ts"] = _bf16()
+        return holder["plan"], holder["ts"]
+    start, end = _run(make, lambda: torch.cat([t.float() for t in holder["ts"]]), flags)
+    assert end < 0.3 * start             # measured 0.13, as an fp64 simulation of the same run
+
+
+def test_reward_sign_decides_the_direction():
+    holder = {}
+
+    def make():
+        holder["plan"], holder["ts"] = _bf16()
+        return holder["plan"], holder["ts"]
+    start, end = _run(make, lambda: torch.cat([t.float() for t in holder["ts"]]), climb=False)
+    assert end > 2 * start               # measured 2.7
+
+
+@pytest.mark.parametrize("fmt", ["int8", "e4m3"])
+def test_quantized_es_reduces_the_loss(fmt):
+    """Codes with one scale per 1024 codes (int8: 1e-3 per quantum, so a
+    step is a few quanta; E4M3: 1e-4 per unit)."""
+    holder = {}
+    scale = 1e-3 if fmt == "int8" else 1e-4
+    dt = torch.int8 if fmt == "int8" else torch.uint8
+
+    def make():
+        codes = [torch.zeros(P // 2, dtype=dt, device="cuda") for _ in range(2)]
+        scales = [torch.full((P // 2 // 1024,), scale, device="cuda") for _ in range(2)]
+        holder["codes"] = codes
+        return esopt.QPlan(codes, scales, [1024, 1024], format=fmt), codes
+
+    def theta():
+        c = torch.cat(holder["codes"])
+        v = c.float() if fmt == "int8" else c.view(torch.float8_e4m3fn).float()
+        return v * scale
+    start, end = _run(make, theta)
+    assert end < 0.6 * start             # measured: int8 0.14, E4M3 0.45 (its coarser grid)
