@@ -168,3 +168,44 @@ def test_block_arguments_are_checked_by_the_binding():
         esopt.QPlan(blocks=[esopt.QBlock(q, s, 64, 0, 48)])             # cols > row_len
     with esopt.QPlan(blocks=[esopt.QBlock(q, s, 64, 0, 256, 3, 192)], format="int8") as p:
         assert p.numel == 256
+
+
+@pytest.mark.parametrize("fmt", ["int8", "e4m3"])
+def test_block_at_the_top_of_the_index_range(fmt):
+    """Whole rows 1 and 2 (columns 0-15) of a tensor with rows of 2^30 - 16
+    codes: the last whole-tensor index is 2^31 - 17, so the row map's
+    division and the noise counter run at the largest indices a plan accepts;
+    against the oracle element by element, checksum included."""
+    from oracle import fp8 as of
+    row_len, cols = (1 << 30) - 16, 16
+    rng = np.random.default_rng(95)
+    q = (rng.integers(-127, 128, 2 * cols).astype(np.int8) if fmt == "int8"
+         else _f8codes(2 * cols, 96).view(np.int8))
+    sc = np.array([4e-4, 7e-4], np.float32)                 # one scale per block row
+    dt = torch.int8 if fmt == "int8" else torch.uint8
+    v = torch.from_numpy(q.reshape(2, cols)).cuda().view(dt)
+    with esopt.QPlan(blocks=[esopt.QBlock(v, _f32dev(sc), cols, 5, row_len, 1, 0)],
+                     format=fmt) as p:
+        p.perturb(41, 1, 1e-3)
+        torch.cuda.synchronize()
+        got = _host(v).reshape(-1)
+        chk = p.checksum()
+    el = _whole_indices((2, cols), row_len, 1, 0)
+    assert int(el[-1]) == (1 << 31) - 17
+    # the oracle's scales at whole-tensor indices: row r of the block is whole row r + 1
+    whole_scales = np.array([1.0, 4e-4, 7e-4], np.float32)
+    if fmt == "int8":
+        d, ok, tol = _perturb_expect(whole_scales, row_len, 41, 5, 1, 1e-3, el)
+        rep = qreport(got.view(np.int8), q, d, tol, ok)
+        assert_qparity(rep, "int8 block at 2^31")
+    else:
+        from test_gpu_fp8 import _perturb_report
+        rep = _perturb_report(got.view(np.uint8), q.view(np.uint8), whole_scales, row_len, 41,
+                              5, 1, 1e-3, el)
+        from parity import assert_f8parity
+        assert_f8parity(rep, "e4m3 block at 2^31")
+    print(fmt, "block at 2^31:", rep)
+    b = got.view(np.uint8)
+    assert chk == (oracle.qchecksum(b[:cols], 5, int(el[0]))
+                   + oracle.qchecksum(b[cols:], 5, int(el[cols]))) & MASK
+
