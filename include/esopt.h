@@ -65,7 +65,7 @@ extern "C" {
 
 #define ES_OK                0
 #define ES_ERR_INVALID_ARG  -1   /* null pointer, bad size, sign, sigma, flags */
-#define ES_ERR_ALIGN        -2   /* data not 2-byte aligned */
+#define ES_ERR_ALIGN        -2   /* bf16 data not 2-byte aligned, scales not 4-byte aligned */
 #define ES_ERR_HIP          -3   /* a HIP runtime call or launch failed */
 #define ES_ERR_DEVICE       -4   /* current device differs from the plan's */
 #define ES_ERR_NOMEM        -5   /* device or host allocation failed */
