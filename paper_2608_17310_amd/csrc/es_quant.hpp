@@ -1,9 +1,11 @@
-// Device code of the int8 path: ES on symmetric int8 codes with per-row
-// binary32 scales, theta_j = s_r(j) q_j, q_j in [-127, 127].  The paper lists
-// quantized ES as future work (Appendix A.2): noise must respect the
-// quantization scale, updates must stay numerically stable, and
-// perturbations must remain replayable from a seed.  Here a perturbation or
-// update step d_j (in units of the row's quantum s) becomes the integer offset
+// Device code of the quantized paths: the table, loads, stores and scales
+// that int8 and E4M3 plans share, and the int8 rule -- ES on symmetric int8
+// codes with per-row binary32 scales, theta_j = s_r(j) q_j, q_j in
+// [-127, 127].  The paper lists quantized ES as future work (Appendix A.2):
+// noise must respect the quantization scale, updates must stay numerically
+// stable, and perturbations must remain replayable from a seed.  Here a
+// perturbation or update step d_j (in units of the row's quantum s) becomes
+// the integer offset
 //   k_j = floor(d_j + r_j 2^-16),   E[k_j] = d_j,
 // with a 16-bit draw r_j, and q_j <- clamp(q_j + k_j, -127, 127).
 //   * perturb / restore: d_j = sign sigma eps_j / s, eps_j the bf16 path's
@@ -33,7 +35,7 @@
 
 namespace esq {
 
-constexpr int kQGroup = 16;                     // int8 codes per lane-group
+constexpr int kQGroup = 16;                     // one-byte codes per lane-group
 
 // Quantized tensor table entry (a tensor, a contiguous shard of one or a
 // strided block of one).  Tiles are numbered as in the bf16 path: full tiles

@@ -1071,7 +1071,7 @@ UpdateKernel update_kernel(int threads, int groups, bool stochastic, bool rows,
                    : update_kernel_for<false>(threads, groups, stochastic, rows);
 }
 
-// ---- int8 path (device code of the passes; helpers in es_quant.hpp) ----
+// ---- quantized path: int8 and E4M3 codes (helpers in es_quant.hpp, es_fp8.hpp) ----
 
 // Kernel arguments of one quantized pass: the key of the update's rounding
 // draws, and for perturb / restore the single member inline (for a swap, m is
@@ -1172,9 +1172,9 @@ __device__ __forceinline__ void qmember_group(const uint32_t raw[4], uint32_t n,
     }
 }
 
-// One tile of an int8 pass: for each of the lane's 16-code groups in turn,
-// the step d in quanta (binary32) and the stochastically rounded, clamped
-// code.  e indexes the codes and scales at hand; n, the whole-tensor index
+// One tile of a quantized pass (int8 or E4M3 codes, kFmt): for each of the
+// lane's 16-code groups in turn, the step in scale units (binary32) and the
+// stochastically rounded, clamped code.  e indexes the codes and scales at hand; n, the whole-tensor index
 // of code e, selects the noise and the rounding draws.
 // kSwap: the member ps.m_from reverted and ps.m applied in registers, the
 // codes of the two separate passes.
@@ -1252,10 +1252,10 @@ __device__ __forceinline__ void qtile(const esq::QTileRef& r, const Member* __re
     }
 }
 
-// An int8 pass over the whole quantized parameter list: perturb / restore
-// (one inline member, draws from its own noise words) or the update (member
-// table and header written by es_prepare_kernel, draws of domain 1 under the
-// rounding seed).
+// A pass over the whole quantized parameter list: perturb / restore (one
+// inline member, draws from its own noise words), swap (two inline members)
+// or the update (member table and header written by es_prepare_kernel, draws
+// of domain 1 under the rounding seed).
 template <int kThreads, int kU, bool kTable, bool kNegate, int kFmt, bool kSwap>
 __global__ __launch_bounds__(kThreads) void es_qpass_kernel(const esq::DevQTensor* __restrict__ tab,
                                                             uint64_t n_full, uint64_t n_tail,
