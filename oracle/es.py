@@ -56,6 +56,7 @@ from .noise import normals, rounding_draws
 ES_UPDATE_DIV_SIGMA = 1
 ES_REWARDS_ARE_WEIGHTS = 2
 ES_UPDATE_STOCHASTIC_ROUND = 4
+ES_UPDATE_MASTER = 8
 
 
 def _f32(x):
@@ -185,6 +186,50 @@ def update(theta_bits, tensor_id, seeds, signs, rewards, alpha, sigma,
     if flags & ES_UPDATE_STOCHASTIC_ROUND:
         return f64_to_bf16_sr(x, rounding_draws(round_seed, tensor_id, el)), 0
     return f64_to_bf16_rne(x), 0
+
+
+def update_master(master, tensor_id, seeds, signs, rewards, alpha, sigma, flags=0,
+                  zscore_eps=1e-8, elems=None):
+    """The update into binary32 master copies (ES_UPDATE_MASTER, the
+    library's update-numerics variant of Section 3's update):
+
+        m' = binary32(m + sum_d w_d eps_d)     (the fp64 sum rounded once)
+        working copy = RNE_bf16(m')
+
+    with the z-score, coefficient and merged weights of update().  With
+    nothing to add (no nonzero merged weight, or a non-finite reward: status
+    1) m' = m, and the working copy is still RNE_bf16(m).
+    Returns (m' as float32, working-copy bf16 bits, status).
+    """
+    seeds = [int(s) for s in seeds]
+    signs = [int(s) for s in signs]
+    if len(seeds) == 0 or len(seeds) != len(signs) or len(seeds) != len(rewards):
+        raise ValueError("seeds, signs and rewards must have the same nonzero length")
+    if any(s not in (1, -1) for s in signs):
+        raise ValueError("signs must be +1 or -1")
+    m = np.asarray(master, dtype=np.float32).ravel().astype(np.float64)
+    if flags & ES_REWARDS_ARE_WEIGHTS:
+        z = np.asarray(rewards, dtype=np.float32).astype(np.float64)
+        status = 0 if np.all(np.isfinite(z)) else 1
+    else:
+        z, status = zscore(rewards, zscore_eps)
+    live = []
+    if not status:
+        c = update_coefficient(alpha, sigma, len(seeds), flags)
+        distinct, w = member_weights(seeds, signs, z, c)
+        live = [(sd, wd) for sd, wd in zip(distinct, w) if wd != 0.0]
+    out = m
+    if live:
+        el = np.arange(m.size, dtype=np.uint64) if elems is None else \
+            np.asarray(elems, dtype=np.uint64).ravel()
+        delta = np.zeros(el.size, dtype=np.float64)
+        for sd, wd in live:
+            delta += wd * normals(sd, tensor_id, el)
+        with np.errstate(over="ignore", invalid="ignore"):
+            out = m + delta
+    with np.errstate(over="ignore"):
+        m32 = out.astype(np.float32)
+    return m32, f64_to_bf16_rne(m32.astype(np.float64)), status
 
 
 def sigma_cosine(sigma0, sigma_T, t, T):

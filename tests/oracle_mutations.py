@@ -75,6 +75,9 @@ MUTS = [
  ("oracle/fp8.py", "delta = np.where(ok, delta / np.where(ok, s, 1.0), 0.0)", "delta = np.where(ok, delta * np.where(ok, s, 1.0), 0.0)"),
  ("oracle/fp8.py", "ok = np.isfinite(s) & (s >= 2.0 ** -126) & np.isfinite(v)\n    d = sign", "ok = np.isfinite(s) & (s > 0) & np.isfinite(v)\n    d = sign"),
  ("oracle/fp8.py", "return _pass(c, round_onto_grid(_f32(v - d), \"restore\", u), ok)", "return _pass(c, round_onto_grid(_f32(v + d), \"restore\", u), ok)"),
+ ("oracle/es.py", "        m32 = out.astype(np.float32)", "        m32 = bf16_to_f64(f64_to_bf16_rne(out)).astype(np.float32)"),
+ ("oracle/es.py", "            delta += wd * normals(sd, tensor_id, el)\n        with np.errstate(over=\"ignore\", invalid=\"ignore\"):\n            out = m + delta", "            delta += wd * normals(sd, tensor_id, el)\n        with np.errstate(over=\"ignore\", invalid=\"ignore\"):\n            out = m + delta.astype(np.float32)"),
+ ("oracle/es.py", "    return m32, f64_to_bf16_rne(m32.astype(np.float64)), status", "    return m32, f64_to_bf16_rne(m), status"),
 
 ]
 

@@ -315,3 +315,118 @@ def test_swap_walk_returns_home_where_no_binade_is_crossed():
     assert np.mean(back != theta) < 0.5 * np.mean(one_back != theta)
 
 
+
+
+# ------------------------------------------------------------ master update --
+
+def _binary32_of(fr):
+    """The binary32 value nearest the exact rational fr (ties to even), written
+    out from the format: 24-bit significands, exponents down to -126, then
+    the subnormal quantum 2^-149 (no overflow in these tests)."""
+    from fractions import Fraction
+    if fr == 0:
+        return 0.0
+    sign = -1 if fr < 0 else 1
+    a = abs(fr)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1                                   # now 2^e <= a < 2^(e+1)
+    quantum = Fraction(2) ** (max(e, -126) - 23)
+    q = a / quantum
+    n = q.numerator // q.denominator
+    rem = q - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sign * float(n * quantum)
+
+
+def test_master_update_rounds_the_exact_sum_once():
+    """m' is the exact m + sum_d w_d eps_d (with the oracle's weights and fp64
+    normals) rounded once to binary32 -- against a rounding written from the
+    format on exact rationals, for masters from 1e-30 to 10 and both signs."""
+    from fractions import Fraction
+    rng = np.random.default_rng(40)
+    n = 3000
+    m = (rng.standard_normal(n) * np.exp(rng.uniform(np.log(1e-30), np.log(10.0), n))).astype(
+        np.float32)
+    m[:4] = [0.0, -0.0, 1e-45, -3e-38]
+    seeds, signs = [5, 5, 6, 9], [1, -1, 1, 1]
+    r = np.array([0.2, 0.9, 0.4, 0.7], np.float32)
+    got, bits, st = oracle.update_master(m, 3, seeds, signs, r, 5e-4, 1e-3)
+    assert st == 0 and got.dtype == np.float32
+    z, _ = zscore(r)
+    distinct, w = member_weights(seeds, signs, z, update_coefficient(5e-4, 1e-3, 4))
+    el = np.arange(n, dtype=np.uint64)
+    eps = {sd: normals(sd, 3, el) for sd in distinct}
+    for j in range(n):
+        exact = Fraction(float(m[j])) + sum(Fraction(float(wd)) * Fraction(float(eps[sd][j]))
+                                            for sd, wd in zip(distinct, w))
+        assert float(got[j]) == _binary32_of(exact), j
+    np.testing.assert_array_equal(bits, f64_to_bf16_rne(got.astype(np.float64)))
+
+
+def test_master_update_agrees_with_the_bf16_update():
+    """From bf16-representable masters the working copy RNE_bf16(binary32(x))
+    equals update()'s RNE_bf16(x) except where the binary32 rounding lands on
+    a bf16 tie (double rounding): pins the master path's sum to the update's."""
+    theta = random_bf16_bits(1 << 16, 41)
+    seeds, signs = [1, 2, 2, 3], [1, 1, -1, 1]
+    r = np.array([0.3, 0.8, 0.1, 0.6], np.float32)
+    for flags, sigma in [(0, 1e-3), (ES_UPDATE_DIV_SIGMA, 2e-3)]:
+        want, st = update(theta, 7, seeds, signs, r, 5e-4, sigma, flags=flags)
+        _, got, st2 = oracle.update_master(bf16_to_f64(theta).astype(np.float32), 7, seeds,
+                                           signs, r, 5e-4, sigma, flags=flags)
+        assert st == st2 == 0
+        assert np.mean(got == want) > 0.9999
+        assert np.mean(got != theta) > 0.3
+
+
+def test_master_update_identities():
+    m = np.random.default_rng(42).standard_normal(5000).astype(np.float32) * np.float32(0.02)
+    seeds, signs = [1, 2], [1, 1]
+    for r, alpha, want_st in [([0.3, 0.9], 0.0, 0), ([0.5, 0.5], 5e-4, 0),
+                              ([0.5, float("nan")], 5e-4, 1)]:
+        got, bits, st = oracle.update_master(m, 1, seeds, signs, np.array(r, np.float32), alpha,
+                                             1e-3)
+        assert st == want_st
+        np.testing.assert_array_equal(got, m)
+        np.testing.assert_array_equal(bits, f64_to_bf16_rne(m.astype(np.float64)))
+    # an antithetic pair with equal rewards merges to weight 0
+    got, _, _ = oracle.update_master(m, 1, [4, 4], [1, -1], np.array([0.6, 0.6], np.float32),
+                                     5e-4, 1e-3)
+    np.testing.assert_array_equal(got, m)
+
+
+def test_master_keeps_what_bf16_rounding_drops():
+    """70 updates at the paper's G = 8, alpha = 2.5e-4 from N(0, 0.02): the
+    binary32 masters stay within the sum of each step's half-ulp of the exact
+    running sum of steps (one rounding per step), while bf16 storage rounded to nearest
+    keeps markedly less of the sum of steps where |theta| >= 0.04 (its
+    regression slope there, about 0.8, against 1 for the masters)."""
+    rng = np.random.default_rng(43)
+    n = 1 << 14
+    theta = random_bf16_bits(n, 44)
+    m = bf16_to_f64(theta).astype(np.float32)
+    exact = bf16_to_f64(theta)
+    cur = theta
+    bound = np.zeros(n)
+    for t in range(70):
+        seeds = [1000 * t + i for i in range(8)]
+        r = rng.random(8).astype(np.float32)
+        before = m.astype(np.float64)
+        m, _, _ = oracle.update_master(m, 2, seeds, [1] * 8, r, 2.5e-4, 1e-3)
+        z, _ = zscore(r)
+        d, w = member_weights(seeds, [1] * 8, z, update_coefficient(2.5e-4, 1e-3, 8))
+        exact = exact + sum(wd * normals(sd, 2, np.arange(n, dtype=np.uint64))
+                            for sd, wd in zip(d, w))
+        cur, _ = update(cur, 2, seeds, [1] * 8, r, 2.5e-4, 1e-3)
+        assert np.all(np.abs(m.astype(np.float64) - before) < 1e-2)
+        bound += np.spacing(np.abs(m)).astype(np.float64) / 2     # this step's rounding
+    assert np.all(np.abs(m.astype(np.float64) - exact) <= bound * (1 + 1e-9))
+    big = np.abs(bf16_to_f64(theta)) >= 0.04
+    steps = (exact - bf16_to_f64(theta))[big]
+    slope_bf16 = np.polyfit(steps, (bf16_to_f64(cur) - bf16_to_f64(theta))[big], 1)[0]
+    slope_master = np.polyfit(steps, (m.astype(np.float64) - bf16_to_f64(theta))[big], 1)[0]
+    print(f"slope where |theta| >= 0.04: masters {slope_master:.5f}, bf16 {slope_bf16:.3f}")
+    assert abs(slope_master - 1.0) < 1e-3
+    assert slope_bf16 < 0.9
