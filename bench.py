@@ -53,6 +53,9 @@ def parse():
                     help="the fp8 path: E4M3 codes with per-row scales (es_qplan_create_format)")
     ap.add_argument("--stochastic-round", action="store_true",
                     help="round the update stochastically (ES_UPDATE_STOCHASTIC_ROUND)")
+    ap.add_argument("--master", action="store_true",
+                    help="binary32 masters of every parameter (es_plan_set_master); the update "
+                         "goes into them and rewrites the bf16 values (ES_UPDATE_MASTER)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target CPU time of the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -545,6 +548,20 @@ def timed_region(torch, stream, steps, fn):
     return start.elapsed_time(end) / steps, wall
 
 
+def master_views(torch, flat, views):
+    """Binary32 masters of a flat bf16 parameter buffer's tensors: one float32
+    buffer holding the values (4 bytes per parameter: 91 GB for the 27B-shaped
+    set, which one MI355X's 288 GB holds beside the bf16 copy), viewed at the
+    same offsets (each view 16-byte aligned, as the bf16 views are)."""
+    mflat = flat.float()
+    base = flat.data_ptr()
+    out = []
+    for v in views:
+        off = (v.data_ptr() - base) // 2
+        out.append(mflat[off:off + v.numel()])
+    return mflat, out
+
+
 def main():
     args = parse()
     if args.summarize:
@@ -598,6 +615,12 @@ def main():
 
     log = EventLog(torch, stream)
     update_flags = esopt.ES_UPDATE_STOCHASTIC_ROUND if args.stochastic_round else 0
+    if args.master:
+        if args.stochastic_round:
+            raise SystemExit("--master rounds the bf16 copy to nearest-even: no --stochastic-round")
+        mflat, masters = master_views(torch, flat, views)
+        plan.set_master(masters)
+        update_flags = esopt.ES_UPDATE_MASTER
 
     def run_step(t, record, swap):
         """One generation's parameter work: every member applied and reverted
@@ -610,14 +633,19 @@ def main():
             for i in range(N - 1):
                 log.call("es_swap", record, plan.swap, seeds[i], signs[i], seeds[i + 1],
                          signs[i + 1], sigma)
+            if args.master:                 # the update rewrites the bf16 values
+                log.call("es_update", record, plan.update, seeds, signs, rewards_all[t],
+                         W.alpha, sigma=sigma, flags=update_flags)
+                return
             log.call("es_restore_update", record, plan.restore_update, seeds[-1], signs[-1],
                      sigma, seeds, signs, rewards_all[t], W.alpha, sigma=sigma,
                      flags=update_flags, round_seed=1000 + t)
             return
         else:
-            for sd, sg in zip(seeds, signs):
+            for i, (sd, sg) in enumerate(zip(seeds, signs)):
                 log.call("es_perturb", record, plan.perturb, sd, sg, sigma)
-                log.call("es_restore", record, plan.restore, sd, sg, sigma)
+                if not (args.master and i == N - 1):  # with masters: no last revert
+                    log.call("es_restore", record, plan.restore, sd, sg, sigma)
         log.call("es_update", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
                  sigma=sigma, flags=update_flags, round_seed=1000 + t)
 
@@ -628,7 +656,8 @@ def main():
     per = log.ms()
     t_pert = median_s(per["es_perturb"] + per["es_restore"])
     t_upd = median_s(per["es_update"])
-    value = (2 * N + 1) * P / (ms_step / 1e3)
+    passes = 2 * N if args.master else 2 * N + 1
+    value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
                             for t in range(args.warmup, total_steps)]))
@@ -645,7 +674,8 @@ def main():
         per_sw = log.ms()
         swap = {"ms_step": ms_swap, "wall": wall_swap, "t_swap": median_s(per_sw["es_swap"]),
                 "calls": len(per_sw["es_swap"]),
-                "t_restore_update": median_s(per_sw["es_restore_update"])}
+                "t_restore_update": (None if args.master
+                                     else median_s(per_sw["es_restore_update"]))}
 
     # the practical in-place streaming ceiling over the same memory: the same
     # tiles and launch, loads and stores only, not pipelined (es_stream_pass),
@@ -659,7 +689,8 @@ def main():
     ceiling_gbs = 4 * P / t_stream / 1e9
     flat_rates = flat_ceilings(esopt, stream)
     c_pert = _counters_for(args.counters_json, "es_perturb", W.name)
-    c_upd = _counters_for(args.counters_json, "es_update", W.name)
+    c_upd = _counters_for(args.counters_json,
+                          "es_update_master" if args.master else "es_update", W.name)
     c_swap = _counters_for(args.counters_json, "es_swap", W.name)
     perturb_gbs = 4 * P / t_pert / 1e9
     roofline = {"bound": "hbm", "achieved": round(perturb_gbs, 1), "peak": HBM_PEAK_GBS,
@@ -685,8 +716,9 @@ def main():
             r.update(achieved=round(ach, 2), frac=round(ach / VALU_PEAK_TINST, 4))
         return r
     default_pop = N == len(W.seeds) and n_members is None
+    upd_bytes = 10 * P if args.master else 4 * P    # masters: 4 read + 4 written, bf16 2 written
     update = {"ms": round(t_upd * 1e3, 3), "params_per_s": P / t_upd,
-              "GBps_algorithmic": round(4 * P / t_upd / 1e9, 1),
+              "GBps_algorithmic": round(upd_bytes / t_upd / 1e9, 1),
               "normals_per_s": n_live * P / t_upd, "distinct_seeds": n_distinct,
               "live_seeds": round(n_live, 3)}
     per_kernel = {
@@ -708,9 +740,15 @@ def main():
                    "param_bytes": 2 * P, "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
                    "member_moves": "es_perturb/es_restore",
-                   "update_rounding": "stochastic" if args.stochastic_round else "nearest-even",
-                   "counting": "value = (2N+1) P / step time: 2N perturb/restore passes "
-                               "and one fused N-member update pass per step"},
+                   "update_rounding": ("binary32 masters, bf16 copy nearest-even"
+                                       if args.master else
+                                       "stochastic" if args.stochastic_round else "nearest-even"),
+                   "counting": ("value = 2N P / step time: N perturb and N - 1 restore passes "
+                                "(the update rewrites the bf16 values, so the last member is not "
+                                "reverted) and one N-member update into binary32 masters"
+                                if args.master else
+                                "value = (2N+1) P / step time: 2N perturb/restore passes "
+                                "and one fused N-member update pass per step")},
         "roofline": roofline,
         "roofline_update": valu_roofline(c_upd, t_upd, "es_update_kernel (fused N-member update)",
                                          default_pop and not args.stochastic_round),
@@ -724,12 +762,15 @@ def main():
                                  "GBps_algorithmic": round(4 * P / t_sw / 1e9, 1),
                                  "normals_per_s": 2 * P / t_sw, "calls": swap["calls"]}
         out["ms_per_step_swap"] = round(swap["ms_step"], 3)
-        per_kernel["es_restore_update"] = {
-            "ms": round(swap["t_restore_update"] * 1e3, 3),
-            "ms_over_update": round(swap["t_restore_update"] / t_upd, 4)}
+        if swap["t_restore_update"] is not None:
+            per_kernel["es_restore_update"] = {
+                "ms": round(swap["t_restore_update"] * 1e3, 3),
+                "ms_over_update": round(swap["t_restore_update"] / t_upd, 4)}
         out["swap_walk"] = {
-            "member_moves": "es_perturb, N-1 fused es_swap, then the last revert and the update "
-                            "in one pass (es_restore_update)",
+            "member_moves": ("es_perturb, N-1 fused es_swap, then the update into the masters "
+                             "(no last revert)" if args.master else
+                             "es_perturb, N-1 fused es_swap, then the last revert and the update "
+                             "in one pass (es_restore_update)"),
             "ms_per_step": round(swap["ms_step"], 3),
             "speedup_vs_perturb_restore": round(ms_step / swap["ms_step"], 4),
             "wall_s_timed": round(swap["wall"], 3),
@@ -846,6 +887,14 @@ def run_profile_pass(args):
     log.add(f"es_restore_update (N={N}, nearest-even; the last member reverted in the pass)",
             "update", P, 4 * P, nd * P, plan.restore_update, seeds[-1], signs[-1], s0, seeds,
             signs, rewards, W.alpha, sigma=s0, repeat=R)
+    mflat, masters = master_views(torch, flat, views)
+    plan.set_master(masters)
+    log.add(f"es_update (N={N}, binary32 masters)", "update", P, 10 * P, nd * P, plan.update,
+            seeds, signs, rewards, W.alpha, sigma=s0, flags=esopt.ES_UPDATE_MASTER, repeat=R)
+    torch.cuda.synchronize()
+    plan.set_master(None)
+    del mflat, masters
+    torch.cuda.empty_cache()
     log.add("es_stream_pass (in-place copy over the plan's tiles)", "ceiling", P, 4 * P, 0,
             plan.stream_pass, repeat=R)
     out = torch.zeros(1, dtype=torch.int64, device="cuda")
@@ -1014,7 +1063,8 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
             "es_swap (two keys)": "es_swap", "es_qperturb": "es_qperturb",
             f"es_qupdate (N={lab['members']})": "es_qupdate", "es_f8perturb": "es_f8perturb",
             f"es_f8update (N={lab['members']})": "es_f8update", "es_qswap": "es_qswap",
-            "es_f8swap": "es_f8swap"}
+            "es_f8swap": "es_f8swap",
+            f"es_update (N={lab['members']}, binary32 masters)": "es_update_master"}
     for group, (stem, title) in groups.items():
         rows = [r for r in per["_rows"] if r["group"] == group]
         if not rows:

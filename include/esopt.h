@@ -78,6 +78,8 @@ extern "C" {
                                        instead of the paper's alpha / G */
 #define ES_REWARDS_ARE_WEIGHTS  2u  /* use rewards as zhat directly (no z-score) */
 #define ES_UPDATE_STOCHASTIC_ROUND 4u /* round the update stochastically (round_seed) */
+#define ES_UPDATE_MASTER        8u  /* update the plan's binary32 masters and rewrite
+                                       the bf16 values from them (es_plan_set_master) */
 
 typedef void* es_stream_t;          /* hipStream_t */
 
@@ -213,7 +215,7 @@ typedef struct es_update_opts {
                              ES_UPDATE_DIV_SIGMA (then finite and > 0) */
     float    zscore_eps;  /* epsilon of the z-score denominator, >= 0 (1e-8) */
     uint32_t flags;       /* ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
-                             ES_UPDATE_STOCHASTIC_ROUND */
+                             ES_UPDATE_STOCHASTIC_ROUND | ES_UPDATE_MASTER */
     uint64_t round_seed;  /* key of the stochastic-rounding draws; read only
                              with ES_UPDATE_STOCHASTIC_ROUND */
 } es_update_opts_t;
@@ -239,6 +241,13 @@ typedef struct es_update_opts {
  * half for odd j.  Overflow past the largest finite bf16 gives infinity; NaN
  * gives 0x7FC0.  A non-finite reward leaves theta unchanged
  * and sets the status word to 1.
+ * With ES_UPDATE_MASTER (a plan with masters, es_plan_set_master; not with
+ * ES_UPDATE_STOCHASTIC_ROUND): the sum is added to the binary32 master m_j
+ * instead, m_j <- m_j + sum (one binary32 rounding of the binary32 sum), and
+ * every bf16 value is rewritten as RNE_bf16(m_j) without being read -- also
+ * when the update adds nothing (then the masters are not written), so the
+ * bf16 values left by the generation's perturbations and reverts do not
+ * matter and the last member need not be reverted.
  *   seeds, signs : host arrays of n_members entries (signs +1 or -1)
  *   rewards_dev  : device array of n_members binary32 rewards
  *   n_members    : 1 .. ES_MAX_MEMBERS
@@ -269,6 +278,24 @@ int es_restore_update(es_plan_t* plan, uint64_t restore_seed, int32_t restore_si
                       const float* rewards_dev, uint32_t n_members,
                       const es_update_opts_t* opts, float* z_out_dev,
                       int32_t* status_out_dev, es_stream_t stream);
+
+/* Binary32 master copies of a plan's parameters (an update-numerics variant
+ * of Section 3's update, the library's: the update accumulates in binary32
+ * and the bf16 parameters the rollouts read are its nearest-even rounding, so
+ * updates far below a bf16 step are kept and no restore drift carries over
+ * from one generation to the next).  masters[i] is the binary32 copy of the
+ * plan's tensor (or block) i, in the same element order: numel (rows * cols)
+ * floats, 16-byte aligned, device memory of the plan's device, overlapping
+ * no other master and no bf16 tensor of the plan; the caller owns it and
+ * keeps it in place while attached.  Used by es_update / es_update_noalloc
+ * with ES_UPDATE_MASTER; the perturbation passes work on the bf16 values as
+ * before.  Allocates 8 bytes per tile of device memory (es_plan_device_bytes
+ * counts it); a second call replaces the masters, masters == NULL detaches
+ * them (synchronising the plan's device first).  Errors: INVALID_ARG for a
+ * count other than the plan's tensor count, a null master, one outside its
+ * device's memory, or overlaps; ALIGN for a master not 16-byte aligned;
+ * DEVICE, NOMEM, HIP as elsewhere. */
+int es_plan_set_master(es_plan_t* plan, void* const* masters, uint32_t n);
 
 /* es_update for callers that cannot allocate (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the same

@@ -60,6 +60,8 @@
 #include <mutex>
 #include <new>
 #include <string>
+#include <type_traits>
+#include <limits>
 #include <unordered_map>
 #include <vector>
 #include <algorithm>
@@ -236,6 +238,51 @@ __device__ __forceinline__ void store_group(uint16_t* __restrict__ p, uint64_t e
             if (e + 2 * k < limit) g[e + 2 * k] = static_cast<uint16_t>(out[k] & 0xFFFFu);
             if (e + 2 * k + 1 < limit) g[e + 2 * k + 1] = static_cast<uint16_t>(out[k] >> 16);
         }
+    }
+}
+
+// The binary32 master copies of a group's 8 elements (es_plan_set_master):
+// element e's master sits at mb + 4 e, mb being the tile's master base.  A
+// group that takes the 16-byte bf16 path has a 16-byte aligned master group
+// (the masters are 16-byte aligned and laid out as their bf16 tensors), so it
+// takes two 16-byte accesses; element-wise accesses below the bound otherwise.
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+template <bool kFast, bool kNT>
+__device__ __forceinline__ void load_master(uintptr_t mb, uint64_t e, uint64_t limit, float m[8],
+                                            bool vec = false) {
+    if (kFast || (vec && e + 8 <= limit)) {
+        const ES_GLOBAL f32x4_t* a = (const ES_GLOBAL f32x4_t*)(mb + 4 * e);
+        const f32x4_t v0 = kNT ? __builtin_nontemporal_load(a) : a[0];
+        const f32x4_t v1 = kNT ? __builtin_nontemporal_load(a + 1) : a[1];
+        m[0] = v0.x; m[1] = v0.y; m[2] = v0.z; m[3] = v0.w;
+        m[4] = v1.x; m[5] = v1.y; m[6] = v1.z; m[7] = v1.w;
+    } else {
+        const ES_GLOBAL float* g = (const ES_GLOBAL float*)mb;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) m[k] = (e + k < limit) ? g[e + k] : 0.0f;
+    }
+}
+
+template <bool kFast, bool kNT>
+__device__ __forceinline__ void store_master(uintptr_t mb, uint64_t e, uint64_t limit,
+                                             const float m[8], bool vec = false) {
+    if (kFast || (vec && e + 8 <= limit)) {
+        ES_GLOBAL f32x4_t* a = (ES_GLOBAL f32x4_t*)(mb + 4 * e);
+        const f32x4_t v0 = {m[0], m[1], m[2], m[3]};
+        const f32x4_t v1 = {m[4], m[5], m[6], m[7]};
+        if constexpr (kNT) {
+            __builtin_nontemporal_store(v0, a);
+            __builtin_nontemporal_store(v1, a + 1);
+        } else {
+            a[0] = v0;
+            a[1] = v1;
+        }
+    } else {
+        ES_GLOBAL float* g = (ES_GLOBAL float*)mb;
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (e + k < limit) g[e + k] = m[k];
     }
 }
 
@@ -765,26 +812,43 @@ __device__ __forceinline__ void restore_group(const uint32_t w[8], float coef_k,
 // kRestore: one member (rst) is reverted first, in registers, and the update
 // is added to the reverted values; with no live weight (add == false) the
 // reverted values are stored as they are, as es_update would then leave them.
-template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows, bool kRestore>
+// kMaster (ES_UPDATE_MASTER): the update is added to the binary32 masters at
+// mb + 4 e instead (one rounding to binary32), and the bf16 values are
+// rewritten as the masters rounded to nearest-even -- also with no live
+// weight, when the masters are not written -- without reading them.
+template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows, bool kRestore,
+          bool kMaster>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct, RoundKey rk, RestoreArg rst,
-                                            bool add) {
+                                            bool add, uintptr_t mb) {
+    constexpr int kIn = kMaster ? 8 : 4;                 // words of a group's input
     const uint32_t q_hi = tile_high_word<kRows>(r);
     const uint32_t g_hi = q_hi >> 1;                     // index >> 35
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
-    uint32_t next[4];
-    if constexpr (kFast) load_group<true, kNT>(r.data, e0, r.limit, next);
+    uint32_t next[kIn];
+    auto load_in = [&](auto fast, uint64_t e, uint32_t in[kIn]) {
+        constexpr bool kF = decltype(fast)::value;
+        if constexpr (kMaster) {
+            float m[8];
+            load_master<kF, kNT>(mb, e, r.limit, m, r.aligned16 != 0u);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) in[k] = __builtin_bit_cast(uint32_t, m[k]);
+        } else {
+            load_group<kF, kNT>(r.data, e, r.limit, in, r.aligned16 != 0u);
+        }
+    };
+    if constexpr (kFast) load_in(std::true_type{}, e0, next);
 #pragma unroll 1
     for (int u = 0; u < kU; ++u) {
         const uint64_t e = e0 + uint64_t(u) * kThreads * kGroupElems;
         if (!kFast && e >= r.limit) break;
-        uint32_t raw[4];
+        uint32_t raw[kIn];
         if constexpr (kFast) {
 #pragma unroll
-            for (int k = 0; k < 4; ++k) raw[k] = next[k];
-            if (u + 1 < kU) load_group<true, kNT>(r.data, e + uint64_t(kThreads) * kGroupElems, r.limit, next);
+            for (int k = 0; k < kIn; ++k) raw[k] = next[k];
+            if (u + 1 < kU) load_in(std::true_type{}, e + uint64_t(kThreads) * kGroupElems, next);
         } else {
-            load_group<false, kNT>(r.data, e, r.limit, raw, r.aligned16 != 0u);
+            load_in(std::false_type{}, e, raw);
         }
         const uint64_t n = noise_index<kRows>(r, e);
         const uint32_t q_lo = static_cast<uint32_t>(n >> 2);
@@ -808,7 +872,18 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
             group_axpy(w, m.w_k, acc);
         }
         uint32_t out[4];
-        if (kRestore && !add) {
+        if constexpr (kMaster) {
+            float m[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) m[k] = __builtin_bit_cast(float, raw[k]);
+            if (add) {
+#pragma unroll
+                for (int k = 0; k < 8; ++k) m[k] += acc[k];
+                store_master<kFast, kNT>(mb, e, r.limit, m, r.aligned16 != 0u);
+            }
+#pragma unroll
+            for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(m[2 * k], m[2 * k + 1]);
+        } else if (kRestore && !add) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) out[k] = raw[k];
         } else if constexpr (kSR) {
@@ -833,22 +908,32 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
 // written by es_prepare_kernel): full tiles, then tail tiles; with kRows the
 // tiles of strided blocks, through their row maps; with kRestore the member
 // rst reverted in the same pass.
-template <int kThreads, int kU, bool kNT, bool kSR, bool kRows, bool kRestore>
+template <int kThreads, int kU, bool kNT, bool kSR, bool kRows, bool kRestore, bool kMaster>
 __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              const DevRows* __restrict__ rows,
                                                              const Member* __restrict__ members,
                                                              const UpdateHeader* __restrict__ hdr,
-                                                             RoundKey rk, RestoreArg rst) {
+                                                             RoundKey rk, RestoreArg rst,
+                                                             const uint64_t* __restrict__ mdelta) {
     const bool add = hdr->n_live != 0u;
-    if (!kRestore && !add) return;          // nothing to add: theta is not written
+    if (!kRestore && !kMaster && !add) return;   // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
-    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x)
-        update_tile<kThreads, kU, true, kNT, kSR, kRows, kRestore>(
-            load_ref<kRows>(tiles, rows, tile), members, n_distinct, rk, rst, add);
-    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x)
-        update_tile<kThreads, kU, false, kNT, kSR, kRows, kRestore>(
-            load_ref<kRows>(tiles, rows, n_full + tile), members, n_distinct, rk, rst, add);
+    // a tile's master base: its bf16 base times two plus the tensor's delta
+    auto mbase = [&](const TileRef& r, uint64_t i) -> uintptr_t {
+        if constexpr (kMaster) return mdelta[i] + 2 * reinterpret_cast<uintptr_t>(r.data);
+        else return 0;
+    };
+    for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
+        const TileRef r = load_ref<kRows>(tiles, rows, tile);
+        update_tile<kThreads, kU, true, kNT, kSR, kRows, kRestore, kMaster>(
+            r, members, n_distinct, rk, rst, add, mbase(r, tile));
+    }
+    for (uint64_t tile = blockIdx.x; tile < n_tail; tile += gridDim.x) {
+        const TileRef r = load_ref<kRows>(tiles, rows, n_full + tile);
+        update_tile<kThreads, kU, false, kNT, kSR, kRows, kRestore, kMaster>(
+            r, members, n_distinct, rk, rst, add, mbase(r, n_full + tile));
+    }
 }
 
 // The scratch of es_update_noalloc: one update's staged member tables, merged
@@ -1001,7 +1086,7 @@ __global__ __launch_bounds__(kAuxBlock) void es_normals_kernel(uint32_t k0, uint
 
 using PerturbKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, Streams);
 using UpdateKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, const Member*,
-                              const UpdateHeader*, RoundKey, RestoreArg);
+                              const UpdateHeader*, RoundKey, RestoreArg, const uint64_t*);
 
 // Tile shapes instantiated: T lanes per workgroup x U groups per lane.
 #define ES_TILE_SHAPES(X) X(256, 4) X(256, 8) X(512, 4) X(512, 8) X(1024, 4) X(1024, 8)
@@ -1051,14 +1136,25 @@ PerturbKernel perturb_kernel(int streams, int threads, int groups, bool rows) {
 
 template <bool kRestore>
 UpdateKernel update_kernel_for(int threads, int groups, bool stochastic, bool rows) {
-#define ES_CASE(T, U)                                                                     \
-    if (threads == T && groups == U) {                                                    \
-        if (rows)                                                                         \
-            return stochastic ? es_update_kernel<T, U, true, true, true, kRestore>        \
-                              : es_update_kernel<T, U, true, false, true, kRestore>;      \
-        return stochastic ? es_update_kernel<T, U, true, true, false, kRestore>           \
-                          : es_update_kernel<T, U, true, false, false, kRestore>;         \
+#define ES_CASE(T, U)                                                                        \
+    if (threads == T && groups == U) {                                                       \
+        if (rows)                                                                            \
+            return stochastic ? es_update_kernel<T, U, true, true, true, kRestore, false>    \
+                              : es_update_kernel<T, U, true, false, true, kRestore, false>;  \
+        return stochastic ? es_update_kernel<T, U, true, true, false, kRestore, false>       \
+                          : es_update_kernel<T, U, true, false, false, kRestore, false>;     \
     }
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
+// The update into binary32 masters (nearest-even rounding of the bf16 copy).
+UpdateKernel update_master_kernel(int threads, int groups, bool rows) {
+#define ES_CASE(T, U)                                                                   \
+    if (threads == T && groups == U)                                                    \
+        return rows ? es_update_kernel<T, U, true, false, true, false, true>            \
+                    : es_update_kernel<T, U, true, false, false, false, true>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -1377,6 +1473,12 @@ struct es_plan {
                                     //   n_rfull + n_rtail of strided blocks
     DevRows* d_rows = nullptr;      // their row maps (same allocation, after the descriptors)
     uint8_t* d_scratch = nullptr;   // kScratchBytes
+    // each tensor's or block's bf16 data and element count, in plan order
+    std::vector<std::pair<uintptr_t, uint64_t>> owners;
+    // binary32 masters (es_plan_set_master): per tile, the delta D with
+    // master address = D + 2 * bf16 address (its tensor's master minus twice
+    // its bf16 data pointer, mod 2^64); null when none are attached
+    uint64_t* d_master = nullptr;
 };
 
 struct es_qplan {
@@ -1688,8 +1790,12 @@ int validate_update(const char* name, const uint64_t* seeds, const int32_t* sign
     if (n_members == 0 || n_members > ES_MAX_MEMBERS)
         return fail_in(ES_ERR_INVALID_ARG, name, "n_members out of range (1 .. 1024)");
     if ((opts->flags & ~(ES_UPDATE_DIV_SIGMA | ES_REWARDS_ARE_WEIGHTS |
-                         ES_UPDATE_STOCHASTIC_ROUND)) != 0)
+                         ES_UPDATE_STOCHASTIC_ROUND | ES_UPDATE_MASTER)) != 0)
         return fail_in(ES_ERR_INVALID_ARG, name, "unknown flags");
+    if ((opts->flags & ES_UPDATE_MASTER) && (opts->flags & ES_UPDATE_STOCHASTIC_ROUND))
+        return fail_in(ES_ERR_INVALID_ARG, name,
+                       "ES_UPDATE_MASTER rounds the bf16 copy to nearest-even: no "
+                       "ES_UPDATE_STOCHASTIC_ROUND with it");
     if (!std::isfinite(opts->alpha)) return fail_in(ES_ERR_INVALID_ARG, name, "alpha not finite");
     if ((opts->flags & ES_UPDATE_DIV_SIGMA) && !(std::isfinite(opts->sigma) && opts->sigma > 0.0f))
         return fail_in(ES_ERR_INVALID_ARG, name,
@@ -1818,25 +1924,40 @@ int update_impl(const char* name, es_plan_t* plan, uint8_t* d_scratch, const uin
                 const int32_t* signs, const float* rewards_dev, uint32_t n_members,
                 const es_update_opts_t* opts, float* z_out_dev, int32_t* status_out_dev,
                 hipStream_t s, const RestoreMember* restore = nullptr) {
+    if (opts->flags & ES_UPDATE_MASTER) {
+        if (restore != nullptr)
+            return fail_in(ES_ERR_INVALID_ARG, name,
+                           "ES_UPDATE_MASTER rewrites the bf16 values from the masters, so no "
+                           "member needs reverting first: use es_update");
+        if (plan->d_master == nullptr)
+            return fail_in(ES_ERR_INVALID_ARG, name,
+                           "ES_UPDATE_MASTER on a plan without masters (es_plan_set_master)");
+    }
     RestoreArg rst{0u, 0.0f};
     int rc = prepare_update(d_scratch, seeds, signs, rewards_dev, n_members, opts, z_out_dev,
                             status_out_dev, s, restore ? &restore->seed : nullptr, &rst.d);
     if (rc != ES_OK) return rc;
     if (restore) rst.coef_k = static_cast<float>(restore->coef * kSqrt2Ln2Double);
     const bool sr = (opts->flags & ES_UPDATE_STOCHASTIC_ROUND) != 0;
+    const bool master = (opts->flags & ES_UPDATE_MASTER) != 0;
     const RoundKey rk{static_cast<uint32_t>(opts->round_seed),
                       static_cast<uint32_t>(opts->round_seed >> 32)};
     Segment seg[2];
     const int n_seg = plan_segments(plan, seg);
     for (int k = 0; k < n_seg; ++k) {
         const Segment& g = seg[k];
+        const bool strided = g.rows != nullptr;
         const UpdateKernel kernel =
-            update_kernel(plan->threads, plan->groups, sr, g.rows != nullptr, restore != nullptr);
+            master ? update_master_kernel(plan->threads, plan->groups, strided)
+                   : update_kernel(plan->threads, plan->groups, sr, strided, restore != nullptr);
+        // the segment's masters: the delta table runs parallel to the tiles
+        const uint64_t* mdelta =
+            master ? plan->d_master + (strided ? plan->n_full + plan->n_tail : 0) : nullptr;
         hipLaunchKernelGGL(kernel, dim3(g.grid_update), dim3(plan->threads), 0, s, g.tiles,
                            g.n_full, g.n_tail, g.rows,
                            reinterpret_cast<const Member*>(d_scratch + kOffMembers),
                            reinterpret_cast<const UpdateHeader*>(d_scratch + kOffHeader), rk,
-                           rst);
+                           rst, mdelta);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return hip_fail(e, std::string(name) + ": es_update_kernel launch");
     }
@@ -2229,7 +2350,12 @@ int es_plan_create(const es_tensor_t* tensors, uint32_t n_tensors, es_plan_t** o
         tile_tensor(static_cast<uint16_t*>(tensors[i].data), tensors[i].numel,
                     8 * uint64_t(tensors[i].offset8), tensors[i].tensor_id, tile_elems, t.full,
                     t.tail);
-    return finish_plan("es_plan_create", device, n_tensors, numel, threads, groups, t, out);
+    rc = finish_plan("es_plan_create", device, n_tensors, numel, threads, groups, t, out);
+    if (rc == ES_OK)
+        for (uint32_t i = 0; i < n_tensors; ++i)
+            (*out)->owners.emplace_back(reinterpret_cast<uintptr_t>(tensors[i].data),
+                                        tensors[i].numel);
+    return rc;
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_plan_create: host allocation failed");
 }
@@ -2275,26 +2401,109 @@ int es_plan_create_blocks(const es_block_t* blocks, uint32_t n_blocks, es_plan_t
     if (rc != ES_OK) return rc;
     PlanTiles t;
     for (uint32_t i = 0; i < n_blocks; ++i) tile_block(blocks[i], tile_elems, t);
-    return finish_plan("es_plan_create_blocks", device, n_blocks, numel, threads, groups, t, out);
+    rc = finish_plan("es_plan_create_blocks", device, n_blocks, numel, threads, groups, t, out);
+    if (rc == ES_OK)
+        for (uint32_t i = 0; i < n_blocks; ++i)
+            (*out)->owners.emplace_back(reinterpret_cast<uintptr_t>(blocks[i].data),
+                                        blocks[i].rows * blocks[i].cols);
+    return rc;
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_plan_create_blocks: host allocation failed");
 }
 
 int es_plan_destroy(es_plan_t* plan) {
     if (plan == nullptr) return ES_OK;
-    const int rc = release_device_memory(plan->device, plan->d_tiles, plan->d_scratch,
-                                         "es_plan_destroy");
+    int rc = release_device_memory(plan->device, plan->d_tiles, plan->d_scratch,
+                                   "es_plan_destroy");
+    if (plan->d_master != nullptr) {
+        const int rc2 = release_device_memory(plan->device, plan->d_master, nullptr,
+                                              "es_plan_destroy");
+        if (rc == ES_OK) rc = rc2;
+    }
     delete plan;
     return rc;
+}
+
+int es_plan_set_master(es_plan_t* plan, void* const* masters, uint32_t n) try {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_plan_set_master: null plan");
+    if (masters == nullptr) {                         // detach
+        if (plan->d_master == nullptr) return ES_OK;
+        uint64_t* old = plan->d_master;
+        plan->d_master = nullptr;
+        return release_device_memory(plan->device, old, nullptr, "es_plan_set_master");
+    }
+    if (n != plan->owners.size())
+        return fail(ES_ERR_INVALID_ARG, "es_plan_set_master: " + std::to_string(n) +
+                                            " masters for a plan of " +
+                                            std::to_string(plan->owners.size()) + " tensors");
+    int rc = check_device(plan);
+    if (rc != ES_OK) return rc;
+    // validation: 16-byte aligned, inside one allocation of this device, and
+    // overlapping no other master and no bf16 tensor of the plan
+    std::vector<std::pair<uintptr_t, uintptr_t>> ranges;
+    for (uint32_t i = 0; i < n; ++i) {
+        const uint64_t numel = plan->owners[i].second;
+        if (numel == 0) continue;
+        const std::string where = "es_plan_set_master: master " + std::to_string(i);
+        const uintptr_t a = reinterpret_cast<uintptr_t>(masters[i]);
+        if (a == 0) return fail(ES_ERR_INVALID_ARG, where + ": null");
+        if (a % 16 != 0) return fail(ES_ERR_ALIGN, where + ": not 16-byte aligned");
+        rc = check_access(masters[i], 4 * numel, plan->device, where);
+        if (rc != ES_OK) return rc;
+        ranges.emplace_back(a, a + 4 * numel);
+        ranges.emplace_back(plan->owners[i].first, plan->owners[i].first + 2 * numel);
+    }
+    std::sort(ranges.begin(), ranges.end());
+    for (size_t i = 1; i < ranges.size(); ++i)
+        if (ranges[i].first < ranges[i - 1].second)
+            return fail(ES_ERR_INVALID_ARG,
+                        "es_plan_set_master: masters overlap each other or the bf16 tensors");
+    // each tile's owner: the tensor whose bf16 bytes hold the tile's first
+    // element (tensors do not overlap), found by bisection over their starts
+    const uint64_t n_tiles = plan->n_full + plan->n_tail + plan->n_rfull + plan->n_rtail;
+    std::vector<DevTile> tiles(n_tiles);
+    hipError_t e = hipSuccess;
+    if (n_tiles > 0)
+        e = hipMemcpy(tiles.data(), plan->d_tiles, sizeof(DevTile) * n_tiles,
+                      hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return hip_fail(e, "es_plan_set_master: tile table read-back");
+    std::vector<std::pair<uintptr_t, uint32_t>> starts;      // (bf16 start, owner)
+    for (uint32_t i = 0; i < n; ++i)
+        if (plan->owners[i].second > 0) starts.emplace_back(plan->owners[i].first, i);
+    std::sort(starts.begin(), starts.end());
+    std::vector<uint64_t> delta(std::max<uint64_t>(n_tiles, 1), 0);
+    for (uint64_t k = 0; k < n_tiles; ++k) {
+        const uintptr_t first = reinterpret_cast<uintptr_t>(tiles[k].data) + 2 * tiles[k].elem0;
+        auto it = std::upper_bound(starts.begin(), starts.end(),
+                                   std::make_pair(first, std::numeric_limits<uint32_t>::max()));
+        const uint32_t i = std::prev(it)->second;
+        delta[k] = reinterpret_cast<uintptr_t>(masters[i]) - 2 * plan->owners[i].first;
+    }
+    uint64_t* d = nullptr;
+    e = hipMalloc(reinterpret_cast<void**>(&d), sizeof(uint64_t) * delta.size());
+    if (e != hipSuccess) return fail(ES_ERR_NOMEM, std::string("hipMalloc: ") + hipGetErrorString(e));
+    e = hipMemcpy(d, delta.data(), sizeof(uint64_t) * delta.size(), hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(d);
+        return hip_fail(e, "es_plan_set_master: table upload");
+    }
+    uint64_t* old = plan->d_master;
+    plan->d_master = d;
+    if (old != nullptr) return release_device_memory(plan->device, old, nullptr,
+                                                     "es_plan_set_master");
+    return ES_OK;
+} catch (const std::bad_alloc&) {
+    return fail(ES_ERR_NOMEM, "es_plan_set_master: host allocation failed");
 }
 
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }
 
 uint64_t es_plan_device_bytes(const es_plan_t* plan) {
-    return plan ? sizeof(DevTile) * std::max<uint64_t>(plan->n_full + plan->n_tail +
-                                                           plan->n_rfull + plan->n_rtail, 1) +
-                      sizeof(DevRows) * (plan->n_rfull + plan->n_rtail) + kScratchBytes
-                : 0;
+    if (plan == nullptr) return 0;
+    const uint64_t tiles =
+        std::max<uint64_t>(plan->n_full + plan->n_tail + plan->n_rfull + plan->n_rtail, 1);
+    return sizeof(DevTile) * tiles + sizeof(DevRows) * (plan->n_rfull + plan->n_rtail) +
+           kScratchBytes + (plan->d_master != nullptr ? sizeof(uint64_t) * tiles : 0);
 }
 uint64_t es_plan_tiles(const es_plan_t* plan) {
     return plan ? plan->n_full + plan->n_tail + plan->n_rfull + plan->n_rtail : 0;
@@ -2528,6 +2737,8 @@ int es_qupdate(es_qplan_t* plan, const uint64_t* seeds, const int32_t* signs,
     if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_qupdate: null plan");
     int rc = validate_update("es_qupdate", seeds, signs, rewards_dev, n_members, opts);
     if (rc != ES_OK) return rc;
+    if (opts->flags & ES_UPDATE_MASTER)
+        return fail(ES_ERR_INVALID_ARG, "es_qupdate: quantized plans have no binary32 masters");
     rc = check_qdevice(plan);
     if (rc == ES_OK)
         rc = check_update_arrays("es_qupdate", plan->device, rewards_dev, n_members, z_out_dev,

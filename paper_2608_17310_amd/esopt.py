@@ -31,6 +31,7 @@ ES_MAX_MEMBERS = 1024
 ES_UPDATE_DIV_SIGMA = 1
 ES_REWARDS_ARE_WEIGHTS = 2
 ES_UPDATE_STOCHASTIC_ROUND = 4
+ES_UPDATE_MASTER = 8
 
 # Every symbol the header declares, with (restype, argtypes).
 _u32, _u64, _i32, _f32, _f64 = (ctypes.c_uint32, ctypes.c_uint64, ctypes.c_int32,
@@ -72,6 +73,7 @@ SIGNATURES = {
     "es_plan_create_blocks": (ctypes.c_int, [ctypes.POINTER(EsBlock), _u32,
                                              ctypes.POINTER(_vp)]),
     "es_plan_destroy": (ctypes.c_int, [_vp]),
+    "es_plan_set_master": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), _u32]),
     "es_plan_numel": (_u64, [_vp]),
     "es_plan_tiles": (_u64, [_vp]),
     "es_plan_device_bytes": (_u64, [_vp]),
@@ -344,6 +346,35 @@ class Plan:
             return load().es_restore_update(handle, rs, rsign, rsig, *rest)
         _call_update(fn, "es_restore_update", self.handle, seeds, signs, rewards, alpha, sigma,
                      zscore_eps, flags, z_out, status_out, stream, round_seed)
+
+    def set_master(self, masters):
+        """Attach binary32 master copies (es_plan_set_master): masters[i] a
+        contiguous float32 CUDA tensor with the element count of the plan's
+        tensor (or block) i, 16-byte aligned.  Updates with
+        flags=ES_UPDATE_MASTER then accumulate into them and rewrite the bf16
+        tensors as their nearest-even rounding.  None detaches them."""
+        if masters is None:
+            _check(load().es_plan_set_master(self.handle, None, 0), "es_plan_set_master")
+            self._masters = None
+            return
+        masters = list(masters)
+        if len(masters) != len(self._tensors):
+            raise ValueError(f"{len(masters)} masters for {len(self._tensors)} tensors")
+        arr = (_vp * len(masters))()
+        for i, (m, t) in enumerate(zip(masters, self._tensors)):
+            if m.dtype != torch.float32 or not m.is_cuda or not m.is_contiguous():
+                raise ValueError(f"master {i} must be a contiguous float32 CUDA tensor")
+            if m.numel() != t.numel():
+                raise ValueError(f"master {i} has {m.numel()} elements, its tensor {t.numel()}")
+            arr[i] = m.data_ptr() if m.numel() else None
+        with torch.cuda.device(self.device):
+            _check(load().es_plan_set_master(self.handle, arr, len(masters)),
+                   "es_plan_set_master")
+        self._masters = masters
+
+    @property
+    def has_master(self):
+        return getattr(self, "_masters", None) is not None
 
     def update_noalloc(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                        z_out=None, status_out=None, stream=None, round_seed=0):

@@ -12,7 +12,10 @@ pass (es_swap), and the last member's revert is made in the update's pass
 parameters instead of 2N, plus the update; the bits are those of the
 separate passes.  The same driver runs the quantized paths (esopt.QPlan, int8
 or E4M3 codes), whose swaps are fused too (es_qswap); their last member is
-reverted in a pass of its own.
+reverted in a pass of its own.  A bf16 plan with binary32 masters
+(Plan.set_master) updates the masters (ES_UPDATE_MASTER), which rewrites the
+bf16 values, so its last member is not reverted at all, and its replay needs
+only the updates.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
@@ -135,9 +138,13 @@ def run_generation(plan, seeds, signs, sigma, alpha, evaluate: Callable[[int], f
     if checksum and not hasattr(plan, "checksum"):
         raise ValueError("this plan has no checksum")
     rewards = []
-    fuse = _fuses_last_revert(plan, fused_swap)
+    master = getattr(plan, "has_master", False)
+    if master:
+        flags |= esopt.ES_UPDATE_MASTER
+    fuse = not master and _fuses_last_revert(plan, fused_swap)
+    # with masters the update rewrites the bf16 values: nothing to revert last
     _walk(plan, seeds, signs, sigma, fused_swap, lambda i: rewards.append(float(evaluate(i))),
-          stream, revert_last=not fuse)
+          stream, revert_last=not fuse and not master)
     rec = GenerationRecord(list(map(int, seeds)), list(map(int, signs)),
                            [float(torch.tensor(r, dtype=torch.float32)) for r in rewards],
                            float(sigma), float(alpha), int(flags), float(zscore_eps), fused_swap,
@@ -182,17 +189,24 @@ def replay(plan, records, with_perturbations=True, stream=None, verify=True):
     """Re-apply recorded generations.  With with_perturbations (default) the
     perturb / swap / restore passes are replayed too, which reproduces the
     live run bit for bit (their bf16 rounding residues included); without,
-    only the updates are applied.  With verify (default), every record that
-    carries a checksum is checked after its update (replays with
-    perturbations only: without them the bits differ by design), raising
-    ReplayMismatch at the first generation that differs."""
+    only the updates are applied.  Records of updates into masters
+    (ES_UPDATE_MASTER) replay their update alone in either case: it rewrites
+    the bf16 values from the masters, which the walk does not touch.  With
+    verify (default), every record that carries a checksum is checked after
+    its update (replays with perturbations, or of master records: otherwise
+    the bits differ by design), raising ReplayMismatch at the first
+    generation that differs."""
     for g, rec in enumerate(records):
-        fuse = with_perturbations and _fuses_last_revert(plan, rec.fused_swap)
-        if with_perturbations:
+        # an update into masters does not depend on the bf16 values it
+        # rewrites, so the walk is not replayed for it
+        master = bool(rec.flags & esopt.ES_UPDATE_MASTER)
+        walk = with_perturbations and not master
+        fuse = walk and _fuses_last_revert(plan, rec.fused_swap)
+        if walk:
             _walk(plan, rec.seeds, rec.signs, rec.sigma, rec.fused_swap, lambda i: None, stream,
                   revert_last=not fuse)
         apply_update(plan, rec, stream, revert_last=fuse)
-        if verify and with_perturbations and rec.checksum is not None:
+        if verify and (with_perturbations or master) and rec.checksum is not None:
             got = plan.checksum(stream=stream)
             if got != rec.checksum:
                 raise ReplayMismatch(f"generation {g}: checksum {got:#018x}, "

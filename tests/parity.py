@@ -169,3 +169,39 @@ def f8report(got, exp, x32, thr, tol, ok):
 def assert_f8parity(rep, what=""):
     assert rep["bad"] == 0, (what, rep)
     assert rep["exact"] >= 0.9999, (what, rep)
+
+
+# ----------------------------------------------------------- binary32 masters --
+# An update into binary32 masters (ES_UPDATE_MASTER) rounds once to binary32
+# on both sides, so its bar is the bound of their difference, derived from
+# the kernel's arithmetic: the normals' error (the bar above: 4e-6 + 2e-6 |eps|
+# per normal, times |w|), the binary32 products and accumulation over the
+# live members (at most N + 3 roundings of a partial sum bounded by
+# sum |w eps|), and the two final roundings (one ulp of the result).
+
+def master_tolerance(m_exp, live, tensor_id, elems):
+    """Per-element bound |got - exp| for an update into masters; live is the
+    oracle's [(seed, weight)] of nonzero merged weights."""
+    import oracle
+    wsum = np.zeros(elems.size)
+    weps = np.zeros(elems.size)
+    for sd, w in live:
+        e = np.abs(oracle.normals(sd, tensor_id, elems))
+        wsum += abs(w) * (4e-6 + 2e-6 * e)
+        weps += abs(w) * e
+    ulp = np.spacing(np.abs(np.asarray(m_exp, np.float32))).astype(np.float64)
+    return wsum + (len(live) + 3) * 2.0 ** -24 * weps + ulp
+
+
+def master_report(got, exp, tol):
+    got = np.asarray(got, np.float32).astype(np.float64)
+    exp = np.asarray(exp, np.float32).astype(np.float64)
+    err = np.abs(got - exp)
+    bad = ~(err <= tol)
+    return {"n": int(got.size), "exact": float(np.mean(got == exp)) if got.size else 1.0,
+            "max_err_over_tol": float(np.max(err / tol)) if got.size else 0.0,
+            "bad": int(bad.sum()), "first_bad": np.flatnonzero(bad)[:5].tolist()}
+
+
+def assert_master_parity(rep, what=""):
+    assert rep["bad"] == 0, (what, rep)

@@ -139,7 +139,9 @@ def test_call_validation_without_device(lib):
         for o in [esopt.EsUpdateOpts(float("inf"), 1e-3, 1e-8, 0),
                   esopt.EsUpdateOpts(5e-4, 0.0, 1e-8, esopt.ES_UPDATE_DIV_SIGMA),
                   esopt.EsUpdateOpts(5e-4, 1e-3, -1.0, 0),
-                  esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8)]:
+                  esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 16),             # unknown flag
+                  esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, esopt.ES_UPDATE_MASTER
+                                     | esopt.ES_UPDATE_STOCHASTIC_ROUND)]:
             assert U(fake, seeds, signs, fake, 2, ctypes.byref(o), None, None, None) == esopt.ES_ERR_INVALID_ARG
     for sign, sigma in ((0, 1e-3), (2, 1e-3), (1, float("nan")), (1, -1e-3)):
         assert lib.es_restore_update(fake, 1, sign, sigma, seeds, signs, fake, 2,
@@ -249,10 +251,14 @@ def test_quantized_plan_validation_without_gpu(lib):
     signs = (ctypes.c_int32 * 2)(1, 1)
     opts = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 0, 0)
     assert lib.es_qupdate(None, seeds, signs, fake, 2, ctypes.byref(opts), None, None, None) == E
-    bad = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 8, 0)
+    bad = esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, 16, 0)
+    assert lib.es_qupdate(fake, seeds, signs, fake, 2,
+                          ctypes.byref(esopt.EsUpdateOpts(5e-4, 1e-3, 1e-8, esopt.ES_UPDATE_MASTER,
+                                                          0)), None, None, None) == E
     assert lib.es_qupdate(fake, seeds, signs, fake, 2, ctypes.byref(bad), None, None, None) == E
     assert lib.es_qplan_destroy(None) == esopt.ES_OK
     assert lib.es_qplan_numel(None) == 0
+    assert lib.es_plan_set_master(None, None, 0) == E
 
 
 def test_quantized_shard_validation_without_gpu(lib):

@@ -5,7 +5,7 @@ two tensors) is -||B theta - y||^2 for a fixed random 4 x 65 536 matrix B,
 so, as in the paper's setting, a few directions of a large parameter space
 decide the reward.  Over 60 one-sided generations of 32 members the loss
 falls well below its start for bf16 (nearest-even and stochastically rounded
-updates), int8 and E4M3 codes; with the reward's sign flipped it rises (the
+updates, and updates into binary32 masters), int8 and E4M3 codes; with the reward's sign flipped it rises (the
 update climbs the reward, it does not merely move)."""
 import numpy as np
 import pytest
@@ -60,15 +60,18 @@ def _bf16():
     return esopt.Plan(ts), ts
 
 
-@pytest.mark.parametrize("flags", [0, esopt.ES_UPDATE_STOCHASTIC_ROUND],
-                         ids=["nearest-even", "stochastic"])
+@pytest.mark.parametrize("flags", [0, esopt.ES_UPDATE_STOCHASTIC_ROUND, "masters"],
+                         ids=["nearest-even", "stochastic", "binary32 masters"])
 def test_bf16_es_reduces_the_loss(flags):
     holder = {}
 
     def make():
         holder["plan"], holder["ts"] = _bf16()
+        if flags == "masters":       # the driver then updates the masters
+            holder["plan"].set_master([torch.zeros(P // 2, device="cuda") for _ in range(2)])
         return holder["plan"], holder["ts"]
-    start, end = _run(make, lambda: torch.cat([t.float() for t in holder["ts"]]), flags)
+    start, end = _run(make, lambda: torch.cat([t.float() for t in holder["ts"]]),
+                      0 if flags == "masters" else flags)
     assert end < 0.3 * start             # measured 0.13, as an fp64 simulation of the same run
 
 
