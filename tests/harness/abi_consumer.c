@@ -26,8 +26,8 @@ int main(void) {
            sizeof(es_update_opts_t), offsetof(es_update_opts_t, alpha),
            offsetof(es_update_opts_t, sigma), offsetof(es_update_opts_t, zscore_eps),
            offsetof(es_update_opts_t, flags), offsetof(es_update_opts_t, round_seed));
-    printf("flags %u %u %u max_members %u\n", ES_UPDATE_DIV_SIGMA, ES_REWARDS_ARE_WEIGHTS,
-           ES_UPDATE_STOCHASTIC_ROUND, ES_MAX_MEMBERS);
+    printf("flags %u %u %u %u max_members %u\n", ES_UPDATE_DIV_SIGMA, ES_REWARDS_ARE_WEIGHTS,
+           ES_UPDATE_STOCHASTIC_ROUND, ES_UPDATE_MASTER, ES_MAX_MEMBERS);
     printf("es_qblock_t %zu data %zu scales %zu rows %zu cols %zu row_len %zu row0 %zu "
            "col0 %zu row %zu tensor_id %zu\n",
            sizeof(es_qblock_t), offsetof(es_qblock_t, data), offsetof(es_qblock_t, scales),
@@ -39,6 +39,7 @@ int main(void) {
     printf("plan_create_null %d\n", es_plan_create(NULL, 1, &plan));
     printf("plan_create_blocks_null %d\n", es_plan_create_blocks(NULL, 1, &plan));
     printf("perturb_null %d\n", es_perturb(NULL, 1, 1, 1e-3f, NULL));
+    printf("set_master_null %d\n", es_plan_set_master(NULL, NULL, 0));
     es_qplan_t* qplan = NULL;
     printf("qplan_create_null %d\n", es_qplan_create(NULL, 1, &qplan));
     printf("qplan_create_shards_null %d\n",

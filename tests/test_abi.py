@@ -214,7 +214,9 @@ def test_plain_c_consumer_of_header(lib, tmp_path):
     assert rows["qplan_create_shards_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["qplan_create_blocks_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["flags"] == [str(esopt.ES_UPDATE_DIV_SIGMA), str(esopt.ES_REWARDS_ARE_WEIGHTS),
-                             str(esopt.ES_UPDATE_STOCHASTIC_ROUND), "max_members", "1024"]
+                             str(esopt.ES_UPDATE_STOCHASTIC_ROUND), str(esopt.ES_UPDATE_MASTER),
+                             "max_members", "1024"]
+    assert rows["set_master_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["plan_create_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert rows["perturb_null"] == [str(esopt.ES_ERR_INVALID_ARG)]
     assert float(rows["sigma_cosine"][0]) == lib.es_sigma_cosine(1e-3, 1e-4, 50, 100)
