@@ -43,7 +43,7 @@ from .noise import (key_words, counter_words, uniform_from_word, angle_from_word
                     box_muller, noise_words, normals, rounding_draws, spare_draws)
 from .bf16 import bf16_to_f64, f64_to_bf16_rne, f64_to_bf16_sr, bf16_ulp
 from .es import (perturb, restore, swap, zscore, update_coefficient, member_weights,
-                 update, update_master, sigma_cosine, ES_UPDATE_DIV_SIGMA,
+                 update, update_master, perturb_master, sigma_cosine, ES_UPDATE_DIV_SIGMA,
                  ES_REWARDS_ARE_WEIGHTS, ES_UPDATE_STOCHASTIC_ROUND, ES_UPDATE_MASTER)
 from .quant import (QMAX, row_scales, round_offset, round_offset9, offset_values, qperturb,
                     qrestore, update_values, qupdate)
@@ -58,7 +58,7 @@ __all__ = [
     "noise_words", "normals", "rounding_draws", "spare_draws",
     "bf16_to_f64", "f64_to_bf16_rne", "f64_to_bf16_sr", "bf16_ulp",
     "perturb", "restore", "swap", "zscore", "update_coefficient", "member_weights",
-    "update", "update_master", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
+    "update", "update_master", "perturb_master", "sigma_cosine", "ES_UPDATE_DIV_SIGMA", "ES_REWARDS_ARE_WEIGHTS",
     "ES_UPDATE_MASTER",
     "ES_UPDATE_STOCHASTIC_ROUND",
     "QMAX", "row_scales", "round_offset", "round_offset9", "offset_values", "qperturb", "qrestore", "update_values", "qupdate",

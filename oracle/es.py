@@ -232,6 +232,18 @@ def update_master(master, tensor_id, seeds, signs, rewards, alpha, sigma, flags=
     return m32, f64_to_bf16_rne(m32.astype(np.float64)), status
 
 
+def perturb_master(master, seed, tensor_id, sign, sigma, elems=None):
+    """A member applied from binary32 masters (es_perturb_master): the bf16
+    working copy RNE_bf16(m + sign sigma eps) of the masters m, rounded once
+    from fp64 (Section 3's theta + sigma eps_i with theta the masters).
+    sigma = 0 gives RNE_bf16(m)."""
+    m = np.asarray(master, dtype=np.float32).ravel().astype(np.float64)
+    el = np.arange(m.size, dtype=np.uint64) if elems is None else \
+        np.asarray(elems, dtype=np.uint64).ravel()
+    eps = normals(seed, tensor_id, el)
+    return f64_to_bf16_rne(m + sign * _f32(sigma) * eps)
+
+
 def sigma_cosine(sigma0, sigma_T, t, T):
     """sigma_t = sigma_T + (sigma_0 - sigma_T) (1 + cos(pi t / T)) / 2."""
     if T <= 0 or t < 0 or t > T:

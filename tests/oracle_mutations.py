@@ -78,6 +78,7 @@ MUTS = [
  ("oracle/es.py", "        m32 = out.astype(np.float32)", "        m32 = bf16_to_f64(f64_to_bf16_rne(out)).astype(np.float32)"),
  ("oracle/es.py", "            delta += wd * normals(sd, tensor_id, el)\n        with np.errstate(over=\"ignore\", invalid=\"ignore\"):\n            out = m + delta", "            delta += wd * normals(sd, tensor_id, el)\n        with np.errstate(over=\"ignore\", invalid=\"ignore\"):\n            out = m + delta.astype(np.float32)"),
  ("oracle/es.py", "    return m32, f64_to_bf16_rne(m32.astype(np.float64)), status", "    return m32, f64_to_bf16_rne(m), status"),
+ ("oracle/es.py", "    return f64_to_bf16_rne(m + sign * _f32(sigma) * eps)", "    return f64_to_bf16_rne(m + _f32(sigma) * eps)"),
 
 ]
 

@@ -430,3 +430,21 @@ def test_master_keeps_what_bf16_rounding_drops():
     print(f"slope where |theta| >= 0.04: masters {slope_master:.5f}, bf16 {slope_bf16:.3f}")
     assert abs(slope_master - 1.0) < 1e-3
     assert slope_bf16 < 0.9
+
+
+def test_perturb_from_masters_is_the_perturbation_of_the_masters():
+    """From bf16-representable masters, a member applied from the masters is
+    exactly perturb() of those values (the same single rounding of
+    theta + s sigma eps); sigma 0 gives the masters' rounding; and from
+    masters between bf16 values it does not round m to bf16 first."""
+    theta = random_bf16_bits(1 << 16, 45)
+    m = bf16_to_f64(theta).astype(np.float32)
+    for seed, sign, sigma in [(3, 1, 1e-3), (4, -1, 1.5e-3), ((1 << 63) + 9, 1, 1e-4)]:
+        np.testing.assert_array_equal(oracle.perturb_master(m, seed, 6, sign, sigma),
+                                      perturb(theta, seed, 6, sign, sigma))
+    m2 = (np.random.default_rng(46).standard_normal(1 << 16) * 0.02).astype(np.float32)
+    np.testing.assert_array_equal(oracle.perturb_master(m2, 1, 6, 1, 0.0),
+                                  f64_to_bf16_rne(m2.astype(np.float64)))
+    got = oracle.perturb_master(m2, 5, 6, 1, 1e-3)
+    twice = perturb(f64_to_bf16_rne(m2.astype(np.float64)), 5, 6, 1, 1e-3)
+    assert np.mean(got != twice) > 0.01          # rounding m first would differ
