@@ -641,11 +641,13 @@ def main():
                      sigma, seeds, signs, rewards_all[t], W.alpha, sigma=sigma,
                      flags=update_flags, round_seed=1000 + t)
             return
+        elif args.master:                   # every member applied from the masters
+            for sd, sg in zip(seeds, signs):
+                log.call("es_perturb_master", record, plan.perturb_master, sd, sg, sigma)
         else:
-            for i, (sd, sg) in enumerate(zip(seeds, signs)):
+            for sd, sg in zip(seeds, signs):
                 log.call("es_perturb", record, plan.perturb, sd, sg, sigma)
-                if not (args.master and i == N - 1):  # with masters: no last revert
-                    log.call("es_restore", record, plan.restore, sd, sg, sigma)
+                log.call("es_restore", record, plan.restore, sd, sg, sigma)
         log.call("es_update", record, plan.update, seeds, signs, rewards_all[t], W.alpha,
                  sigma=sigma, flags=update_flags, round_seed=1000 + t)
 
@@ -654,9 +656,17 @@ def main():
     ms_step, wall = timed_region(torch, stream, args.steps,
                                  lambda i: run_step(args.warmup + i, record=True, swap=False))
     per = log.ms()
+    if args.master:
+        # the perturb roofline stays es_perturb's, timed separately below
+        t_pmaster = median_s(per["es_perturb_master"])
+        for _ in range(3):
+            log.call("es_perturb", True, plan.perturb, 1, 1, W.sigma0)
+            log.call("es_restore", True, plan.restore, 1, 1, W.sigma0)
+        torch.cuda.synchronize()
+        per = log.ms()
     t_pert = median_s(per["es_perturb"] + per["es_restore"])
     t_upd = median_s(per["es_update"])
-    passes = 2 * N if args.master else 2 * N + 1
+    passes = N + 1 if args.master else 2 * N + 1
     value = passes * P / (ms_step / 1e3)
     n_distinct = len(dict.fromkeys(step_seeds(W, 0, n_members)))
     n_live = float(np.mean([live_seeds(step_seeds(W, t, n_members), signs, rewards_np[t])
@@ -728,6 +738,11 @@ def main():
         "es_update": update,
         "es_stream_pass": {"ms": round(t_stream * 1e3, 3), "GBps": round(ceiling_gbs, 1)},
     }
+    if args.master:
+        per_kernel["es_perturb_master"] = {
+            "ms": round(t_pmaster * 1e3, 3), "params_per_s": P / t_pmaster,
+            "GBps_algorithmic": round(6 * P / t_pmaster / 1e9, 1),
+            "frac_hbm_peak": round(6 * P / t_pmaster / 1e9 / HBM_PEAK_GBS, 4)}
     out = {
         "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
         "value": value,
@@ -739,14 +754,15 @@ def main():
         "config": {"workload": W.name, "params": P, "tensors": len(views), "members": N,
                    "param_bytes": 2 * P, "plan_device_bytes": plan.device_bytes,
                    "distinct_seeds": n_distinct, "sigma0": W.sigma0, "alpha": W.alpha,
-                   "member_moves": "es_perturb/es_restore",
                    "update_rounding": ("binary32 masters, bf16 copy nearest-even"
                                        if args.master else
                                        "stochastic" if args.stochastic_round else "nearest-even"),
-                   "counting": ("value = 2N P / step time: N perturb and N - 1 restore passes "
-                                "(the update rewrites the bf16 values, so the last member is not "
-                                "reverted) and one N-member update into binary32 masters"
-                                if args.master else
+                   "member_moves": ("es_perturb_master (each member applied from the "
+                                    "masters; no revert)" if args.master else
+                                    "es_perturb/es_restore"),
+                   "counting": ("value = (N+1) P / step time: N passes applying a member from "
+                                "the masters (no revert) and one N-member update into binary32 "
+                                "masters" if args.master else
                                 "value = (2N+1) P / step time: 2N perturb/restore passes "
                                 "and one fused N-member update pass per step")},
         "roofline": roofline,
@@ -891,6 +907,8 @@ def run_profile_pass(args):
     plan.set_master(masters)
     log.add(f"es_update (N={N}, binary32 masters)", "update", P, 10 * P, nd * P, plan.update,
             seeds, signs, rewards, W.alpha, sigma=s0, flags=esopt.ES_UPDATE_MASTER, repeat=R)
+    log.add("es_perturb_master (a member from binary32 masters)", "perturb", P, 6 * P, P,
+            plan.perturb_master, seeds[0], signs[0], s0, repeat=R)
     torch.cuda.synchronize()
     plan.set_master(None)
     del mflat, masters
@@ -1064,7 +1082,8 @@ def summarize(out_dir, profiles_dir=os.path.join(REPO, "profiles")):
             f"es_qupdate (N={lab['members']})": "es_qupdate", "es_f8perturb": "es_f8perturb",
             f"es_f8update (N={lab['members']})": "es_f8update", "es_qswap": "es_qswap",
             "es_f8swap": "es_f8swap",
-            f"es_update (N={lab['members']}, binary32 masters)": "es_update_master"}
+            f"es_update (N={lab['members']}, binary32 masters)": "es_update_master",
+            "es_perturb_master (a member from binary32 masters)": "es_perturb_master"}
     for group, (stem, title) in groups.items():
         rows = [r for r in per["_rows"] if r["group"] == group]
         if not rows:

@@ -297,6 +297,20 @@ int es_restore_update(es_plan_t* plan, uint64_t restore_seed, int32_t restore_si
  * DEVICE, NOMEM, HIP as elsewhere. */
 int es_plan_set_master(es_plan_t* plan, void* const* masters, uint32_t n);
 
+/* Apply one member from the masters: every bf16 value becomes
+ * RNE_bf16(m_j + sign sigma eps_j(seed)), m_j + sign sigma eps_j formed in
+ * binary32 with one rounding, read from the plan's masters (which stay
+ * unchanged) and written to the bf16 tensors without reading them (6 bytes
+ * per parameter).  In a generation over a plan with masters it replaces
+ * perturb, swap and restore: each candidate is applied afresh, so no revert
+ * is needed and the weights a candidate is evaluated at do not depend on the
+ * candidates before it (Section 3's theta + sigma eps_i, rounded once).
+ * sigma 0 writes RNE_bf16(m_j) (the bf16 copy refreshed from the masters).
+ * Uses the plan's scratch, as es_update.  Errors: INVALID_ARG (null plan, a
+ * plan without masters, sign, sigma), DEVICE, HIP. */
+int es_perturb_master(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma,
+                      es_stream_t stream);
+
 /* es_update for callers that cannot allocate (code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation): the same
  * arguments, checks, results and errors as es_update, bit for bit, but the

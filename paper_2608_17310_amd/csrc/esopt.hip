@@ -812,23 +812,26 @@ __device__ __forceinline__ void restore_group(const uint32_t w[8], float coef_k,
 // kRestore: one member (rst) is reverted first, in registers, and the update
 // is added to the reverted values; with no live weight (add == false) the
 // reverted values are stored as they are, as es_update would then leave them.
-// kMaster (ES_UPDATE_MASTER): the update is added to the binary32 masters at
-// mb + 4 e instead (one rounding to binary32), and the bf16 values are
-// rewritten as the masters rounded to nearest-even -- also with no live
+// kMaster == 1 (ES_UPDATE_MASTER): the update is added to the binary32
+// masters at mb + 4 e instead (one rounding to binary32), and the bf16 values
+// are rewritten as the masters rounded to nearest-even -- also with no live
 // weight, when the masters are not written -- without reading them.
+// kMaster == 2 (es_perturb_master): the members' terms are added to the
+// masters in registers, m + sum w eps with one rounding for one member (the
+// accumulation starts from m), and only the bf16 values are written.
 template <int kThreads, int kU, bool kFast, bool kNT, bool kSR, bool kRows, bool kRestore,
-          bool kMaster>
+          int kMaster>
 __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __restrict__ members,
                                             uint32_t n_distinct, RoundKey rk, RestoreArg rst,
                                             bool add, uintptr_t mb) {
-    constexpr int kIn = kMaster ? 8 : 4;                 // words of a group's input
+    constexpr int kIn = kMaster != 0 ? 8 : 4;            // words of a group's input
     const uint32_t q_hi = tile_high_word<kRows>(r);
     const uint32_t g_hi = q_hi >> 1;                     // index >> 35
     const uint64_t e0 = r.elem0 + uint64_t(threadIdx.x) * kGroupElems;
     uint32_t next[kIn];
     auto load_in = [&](auto fast, uint64_t e, uint32_t in[kIn]) {
         constexpr bool kF = decltype(fast)::value;
-        if constexpr (kMaster) {
+        if constexpr (kMaster != 0) {
             float m[8];
             load_master<kF, kNT>(mb, e, r.limit, m, r.aligned16 != 0u);
 #pragma unroll
@@ -854,7 +857,8 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
         const uint32_t q_lo = static_cast<uint32_t>(n >> 2);
         float acc[8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) acc[k] = 0.0f;
+        for (int k = 0; k < 8; ++k)
+            acc[k] = kMaster == 2 ? __builtin_bit_cast(float, raw[k]) : 0.0f;
         for (uint32_t d = 0; d < n_distinct; ++d) {
             const Member m = members[d];
             const bool live = !is_zero_weight(m.w_k);
@@ -872,7 +876,10 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
             group_axpy(w, m.w_k, acc);
         }
         uint32_t out[4];
-        if constexpr (kMaster) {
+        if constexpr (kMaster == 2) {
+#pragma unroll
+            for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(acc[2 * k], acc[2 * k + 1]);
+        } else if constexpr (kMaster == 1) {
             float m[8];
 #pragma unroll
             for (int k = 0; k < 8; ++k) m[k] = __builtin_bit_cast(float, raw[k]);
@@ -908,7 +915,7 @@ __device__ __forceinline__ void update_tile(const TileRef& r, const Member* __re
 // written by es_prepare_kernel): full tiles, then tail tiles; with kRows the
 // tiles of strided blocks, through their row maps; with kRestore the member
 // rst reverted in the same pass.
-template <int kThreads, int kU, bool kNT, bool kSR, bool kRows, bool kRestore, bool kMaster>
+template <int kThreads, int kU, bool kNT, bool kSR, bool kRows, bool kRestore, int kMaster>
 __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __restrict__ tiles,
                                                              uint64_t n_full, uint64_t n_tail,
                                                              const DevRows* __restrict__ rows,
@@ -917,11 +924,11 @@ __global__ __launch_bounds__(kThreads) void es_update_kernel(const DevTile* __re
                                                              RoundKey rk, RestoreArg rst,
                                                              const uint64_t* __restrict__ mdelta) {
     const bool add = hdr->n_live != 0u;
-    if (!kRestore && !kMaster && !add) return;   // nothing to add: theta is not written
+    if (!kRestore && kMaster == 0 && !add) return;   // nothing to add: theta is not written
     const uint32_t n_distinct = hdr->n_distinct;
     // a tile's master base: its bf16 base times two plus the tensor's delta
     auto mbase = [&](const TileRef& r, uint64_t i) -> uintptr_t {
-        if constexpr (kMaster) return mdelta[i] + 2 * reinterpret_cast<uintptr_t>(r.data);
+        if constexpr (kMaster != 0) return mdelta[i] + 2 * reinterpret_cast<uintptr_t>(r.data);
         else return 0;
     };
     for (uint64_t tile = blockIdx.x; tile < n_full; tile += gridDim.x) {
@@ -1139,25 +1146,32 @@ UpdateKernel update_kernel_for(int threads, int groups, bool stochastic, bool ro
 #define ES_CASE(T, U)                                                                        \
     if (threads == T && groups == U) {                                                       \
         if (rows)                                                                            \
-            return stochastic ? es_update_kernel<T, U, true, true, true, kRestore, false>    \
-                              : es_update_kernel<T, U, true, false, true, kRestore, false>;  \
-        return stochastic ? es_update_kernel<T, U, true, true, false, kRestore, false>       \
-                          : es_update_kernel<T, U, true, false, false, kRestore, false>;     \
+            return stochastic ? es_update_kernel<T, U, true, true, true, kRestore, 0>    \
+                              : es_update_kernel<T, U, true, false, true, kRestore, 0>;  \
+        return stochastic ? es_update_kernel<T, U, true, true, false, kRestore, 0>       \
+                          : es_update_kernel<T, U, true, false, false, kRestore, 0>;     \
     }
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
 }
 
-// The update into binary32 masters (nearest-even rounding of the bf16 copy).
-UpdateKernel update_master_kernel(int threads, int groups, bool rows) {
+// The update into binary32 masters (mode 1) and the application of members
+// from the masters (mode 2), both rewriting the bf16 values.
+template <int kMode>
+UpdateKernel master_kernel_for(int threads, int groups, bool rows) {
 #define ES_CASE(T, U)                                                                   \
     if (threads == T && groups == U)                                                    \
-        return rows ? es_update_kernel<T, U, true, false, true, false, true>            \
-                    : es_update_kernel<T, U, true, false, false, false, true>;
+        return rows ? es_update_kernel<T, U, true, false, true, false, kMode>           \
+                    : es_update_kernel<T, U, true, false, false, false, kMode>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
+}
+
+UpdateKernel update_master_kernel(int threads, int groups, bool rows, bool apply = false) {
+    return apply ? master_kernel_for<2>(threads, groups, rows)
+                 : master_kernel_for<1>(threads, groups, rows);
 }
 
 // restore: the update with one member reverted in the same pass.
@@ -1861,6 +1875,25 @@ void build_member_tables(const uint64_t* seeds, const int32_t* signs, uint32_t n
 // and its header in the scratch.  Allocates nothing.  With `find`, *found is
 // set to the distinct-table entry of seed *find before anything is launched
 // (or the call fails with INVALID_ARG when no member has that seed).
+// Host words into device scratch at dst_off, in launches of es_stage_kernel
+// carrying 1 KB of kernel arguments each (no staging buffer, no host
+// synchronisation).
+int stage_words(uint8_t* d_scratch, size_t dst_off, const void* src, size_t bytes,
+                hipStream_t s) {
+    const uint32_t* words = static_cast<const uint32_t*>(src);
+    const size_t n_words = bytes / 4;
+    for (size_t w0 = 0; w0 < n_words; w0 += kStageWords) {
+        StageChunk chunk;
+        const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
+        std::memcpy(chunk.words, words + w0, nw * 4);
+        hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s,
+                           reinterpret_cast<uint32_t*>(d_scratch + dst_off) + w0, nw, chunk);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
+    }
+    return ES_OK;
+}
+
 int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* signs,
                    const float* rewards_dev, uint32_t n_members, const es_update_opts_t* opts,
                    float* z_out_dev, int32_t* status_out_dev, hipStream_t s,
@@ -1877,20 +1910,8 @@ int prepare_update(uint8_t* d_scratch, const uint64_t* seeds, const int32_t* sig
         *found = d;
     }
 
-    // 1 KB of kernel arguments per staging launch
     auto stage = [&](size_t dst_off, const void* src, size_t bytes) -> int {
-        const uint32_t* words = static_cast<const uint32_t*>(src);
-        const size_t n_words = bytes / 4;
-        for (size_t w0 = 0; w0 < n_words; w0 += kStageWords) {
-            StageChunk chunk;
-            const uint32_t nw = static_cast<uint32_t>(std::min<size_t>(kStageWords, n_words - w0));
-            std::memcpy(chunk.words, words + w0, nw * 4);
-            hipLaunchKernelGGL(es_stage_kernel, dim3(1), dim3(kAuxBlock), 0, s,
-                               reinterpret_cast<uint32_t*>(d_scratch + dst_off) + w0, nw, chunk);
-            const hipError_t e = hipGetLastError();
-            if (e != hipSuccess) return hip_fail(e, "es_stage_kernel launch");
-        }
-        return ES_OK;
+        return stage_words(d_scratch, dst_off, src, bytes, s);
     };
     int rc = stage(kOffMembersIn, t.min, sizeof(MemberIn) * n_members);
     if (rc == ES_OK) rc = stage(kOffDistinctIn, t.din, sizeof(DistinctIn) * nd);
@@ -2494,6 +2515,45 @@ int es_plan_set_master(es_plan_t* plan, void* const* masters, uint32_t n) try {
     return ES_OK;
 } catch (const std::bad_alloc&) {
     return fail(ES_ERR_NOMEM, "es_plan_set_master: host allocation failed");
+}
+
+int es_perturb_master(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma,
+                      es_stream_t stream) {
+    if (plan == nullptr) return fail(ES_ERR_INVALID_ARG, "es_perturb_master: null plan");
+    if (sign != 1 && sign != -1)
+        return fail(ES_ERR_INVALID_ARG, "es_perturb_master: sign must be +1 or -1");
+    if (!std::isfinite(sigma) || sigma < 0.0f)
+        return fail(ES_ERR_INVALID_ARG, "es_perturb_master: sigma must be finite and >= 0");
+    if (plan->d_master == nullptr)
+        return fail(ES_ERR_INVALID_ARG, "es_perturb_master: the plan has no masters "
+                                        "(es_plan_set_master)");
+    int rc = check_device(plan);
+    if (rc != ES_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // a one-member table in the plan's scratch, as an update's
+    const double coef = sign > 0 ? double(sigma) : -double(sigma);
+    const Member m{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                   static_cast<float>(coef * kSqrt2Ln2Double), 0u};
+    const UpdateHeader h{1u, sigma != 0.0f ? 1u : 0u, 0, 0u};
+    rc = stage_words(plan->d_scratch, kOffMembers, &m, sizeof(m), s);
+    if (rc == ES_OK) rc = stage_words(plan->d_scratch, kOffHeader, &h, sizeof(h), s);
+    if (rc != ES_OK) return rc;
+    Segment seg[2];
+    const int n_seg = plan_segments(plan, seg);
+    for (int k = 0; k < n_seg; ++k) {
+        const Segment& g = seg[k];
+        const bool strided = g.rows != nullptr;
+        hipLaunchKernelGGL(update_master_kernel(plan->threads, plan->groups, strided, true),
+                           dim3(g.grid_update), dim3(plan->threads), 0, s, g.tiles, g.n_full,
+                           g.n_tail, g.rows,
+                           reinterpret_cast<const Member*>(plan->d_scratch + kOffMembers),
+                           reinterpret_cast<const UpdateHeader*>(plan->d_scratch + kOffHeader),
+                           RoundKey{0u, 0u}, RestoreArg{0u, 0.0f},
+                           plan->d_master + (strided ? plan->n_full + plan->n_tail : 0));
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return hip_fail(e, "es_perturb_master: es_update_kernel launch");
+    }
+    return ES_OK;
 }
 
 uint64_t es_plan_numel(const es_plan_t* plan) { return plan ? plan->numel : 0; }

@@ -74,6 +74,7 @@ SIGNATURES = {
                                              ctypes.POINTER(_vp)]),
     "es_plan_destroy": (ctypes.c_int, [_vp]),
     "es_plan_set_master": (ctypes.c_int, [_vp, ctypes.POINTER(_vp), _u32]),
+    "es_perturb_master": (ctypes.c_int, [_vp, _u64, _i32, _f32, _vp]),
     "es_plan_numel": (_u64, [_vp]),
     "es_plan_tiles": (_u64, [_vp]),
     "es_plan_device_bytes": (_u64, [_vp]),
@@ -375,6 +376,13 @@ class Plan:
     @property
     def has_master(self):
         return getattr(self, "_masters", None) is not None
+
+    def perturb_master(self, seed, sign, sigma, stream=None):
+        """bf16 values = RNE(master + sign sigma eps(seed)) (es_perturb_master):
+        a member applied from the masters, which stay unchanged; sigma 0
+        refreshes the bf16 values from the masters."""
+        _check(load().es_perturb_master(self.handle, _u64_arg(seed, "seed"), int(sign),
+                                        float(sigma), _stream(stream)), "es_perturb_master")
 
     def update_noalloc(self, seeds, signs, rewards, alpha, sigma=0.0, zscore_eps=1e-8, flags=0,
                        z_out=None, status_out=None, stream=None, round_seed=0):

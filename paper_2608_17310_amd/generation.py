@@ -13,9 +13,10 @@ parameters instead of 2N, plus the update; the bits are those of the
 separate passes.  The same driver runs the quantized paths (esopt.QPlan, int8
 or E4M3 codes), whose swaps are fused too (es_qswap); their last member is
 reverted in a pass of its own.  A bf16 plan with binary32 masters
-(Plan.set_master) updates the masters (ES_UPDATE_MASTER), which rewrites the
-bf16 values, so its last member is not reverted at all, and its replay needs
-only the updates.
+(Plan.set_master) applies each member from the masters (es_perturb_master:
+no revert, and each candidate's weights independent of the ones before it)
+and updates the masters (ES_UPDATE_MASTER), which rewrites the bf16 values;
+its replay needs only the updates.
 
 Only seeds, signs, rewards and scalars (and the stochastic-rounding seed) are
 recorded; because every kernel is deterministic, replaying the records from
@@ -98,7 +99,9 @@ def _fuses_last_revert(plan, fused_swap):
 
 def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream, revert_last=True):
     """Apply member 0, visit it, move to member 1, ... and revert the last
-    (unless revert_last is false: the update then reverts it).
+    (unless revert_last is false: the update then reverts it).  A plan with
+    masters applies every member from them (es_perturb_master) and reverts
+    nothing.
     When the passes run on a stream other than PyTorch's current one, each
     visit is ordered after its member's pass and the next pass after the
     visit's work on the current stream, so an evaluation that reads the
@@ -108,14 +111,22 @@ def _walk(plan, seeds, signs, sigma, fused_swap, visit, stream, revert_last=True
     s = _torch_stream(stream, plan.device)
     cur = torch.cuda.current_stream(plan.device)
     side = s.cuda_stream != cur.cuda_stream
-    plan.perturb(seeds[0], signs[0], sigma, stream=s)
+    # with masters every member is applied from them: nothing to revert
+    master = getattr(plan, "has_master", False)
+    if master:
+        plan.perturb_master(seeds[0], signs[0], sigma, stream=s)
+    else:
+        plan.perturb(seeds[0], signs[0], sigma, stream=s)
     for i in range(n):
         if side:
             cur.wait_stream(s)
         visit(i)
         if side:
             s.wait_stream(cur)
-        if i + 1 < n and fused_swap:
+        if master:
+            if i + 1 < n:
+                plan.perturb_master(seeds[i + 1], signs[i + 1], sigma, stream=s)
+        elif i + 1 < n and fused_swap:
             plan.swap(seeds[i], signs[i], seeds[i + 1], signs[i + 1], sigma, stream=s)
         elif i + 1 < n:
             plan.restore(seeds[i], signs[i], sigma, stream=s)

@@ -239,3 +239,100 @@ def test_generation_driver_and_replay_from_updates():
     for x, y in zip(vc, final_b):
         np.testing.assert_array_equal(to_host(x), y)
     pc.close()
+
+
+# ------------------------------------------------- members applied from masters --
+
+def test_perturb_master_matches_oracle_and_leaves_the_masters():
+    from parity import assert_parity, perturb_delta, report
+    plan, views, mdev, ms = _setup(80)
+    for seed, sign, sigma in [(11, 1, 1e-3), (12, -1, 1.5e-3), ((1 << 62) + 3, 1, 2e-3)]:
+        plan.perturb_master(seed, sign, sigma)
+        torch.cuda.synchronize()
+        for i, (tid, m0) in enumerate(zip(plan.tensor_ids, ms)):
+            el = np.arange(m0.size, dtype=np.uint64)
+            exp = oracle.perturb_master(m0, seed, tid, sign, sigma)
+            rep = report(to_host(views[i]), exp, _rne(m0), perturb_delta(seed, tid, sign, sigma, el))
+            assert_parity(rep, f"perturb_master tensor {i}")
+            np.testing.assert_array_equal(mdev[i].cpu().numpy(), m0)     # masters unchanged
+    plan.perturb_master(1, 1, 0.0)                                         # refresh
+    torch.cuda.synchronize()
+    for v, m0 in zip(views, ms):
+        np.testing.assert_array_equal(to_host(v), _rne(m0))
+    with pytest.raises(esopt.EsError):
+        plan.perturb_master(1, 0, 1e-3)
+    plan.set_master(None)
+    with pytest.raises(esopt.EsError):                                     # no masters
+        plan.perturb_master(1, 1, 1e-3)
+    plan.close()
+
+
+def test_a_candidate_does_not_depend_on_the_ones_before_it():
+    pa, va, _, _ = _setup(81, garbage=2)
+    pb, vb, _, _ = _setup(81, garbage=3)
+    for sd in (5, 6, 7):
+        pa.perturb_master(sd, 1, 1e-3)
+    pb.perturb_master(7, 1, 1e-3)
+    torch.cuda.synchronize()
+    for x, y in zip(va, vb):
+        np.testing.assert_array_equal(to_host(x), to_host(y))
+    pa.close()
+    pb.close()
+
+
+def test_perturb_master_on_blocks_and_shards():
+    rows, cols = 64, 1024
+    m0 = (np.random.default_rng(82).standard_normal((rows, cols)) * 0.02).astype(np.float32)
+    whole = torch.zeros(rows * cols, dtype=torch.bfloat16, device="cuda")
+    with esopt.Plan([whole], tensor_ids=[2]) as p:
+        p.set_master([torch.from_numpy(m0.reshape(-1).copy()).cuda()])
+        p.perturb_master(9, -1, 1e-3)
+        torch.cuda.synchronize()
+        ref = to_host(whole).reshape(rows, cols)
+    blk = torch.zeros(rows, 384, dtype=torch.bfloat16, device="cuda")
+    with esopt.Plan(blocks=[esopt.Block(blk, 2, cols, 0, 512)]) as p:
+        p.set_master([torch.from_numpy(np.ascontiguousarray(m0[:, 512:896])).cuda()])
+        p.perturb_master(9, -1, 1e-3)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_host(blk).reshape(rows, 384), ref[:, 512:896])
+    buf = torch.zeros(24 * cols + 3, dtype=torch.bfloat16, device="cuda")
+    sh = buf[3:]
+    with esopt.Plan([sh], tensor_ids=[2], offsets=[40 * cols]) as p:
+        p.set_master([torch.from_numpy(m0[40:].reshape(-1).copy()).cuda()])
+        p.perturb_master(9, -1, 1e-3)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_host(sh), ref[40:].reshape(-1))
+
+
+def test_driver_evaluates_each_candidate_at_its_masters_perturbation():
+    """run_generation over a plan with masters: while member i is visited the
+    bf16 values are exactly the oracle's perturb_master of the masters (on
+    sampled elements of every tensor), whatever came before it."""
+    plan, views, mdev, ms = _setup(83)
+    rng = np.random.default_rng(84)
+    picks = [np.unique(rng.integers(0, n, 300)) for n in SHAPES]
+    seeds, signs = [21, 21, 22, 23], [1, -1, 1, 1]
+    seen = []
+
+    from parity import assert_parity, perturb_delta, report
+    parts = ([], [], [], [])
+
+    def evaluate(i):
+        torch.cuda.synchronize()
+        for k, (tid, idx) in enumerate(zip(plan.tensor_ids, picks)):
+            el = idx.astype(np.uint64)
+            for lst, x in zip(parts, (to_host(views[k])[idx],
+                                      oracle.perturb_master(ms[k][idx], seeds[i], tid, signs[i],
+                                                            1e-3, elems=el),
+                                      _rne(ms[k][idx]),
+                                      perturb_delta(seeds[i], tid, signs[i], 1e-3, el))):
+                lst.append(x)
+        seen.append(i)
+        return float(i)
+
+    run_generation(plan, seeds, signs, 1e-3, 5e-4, evaluate)
+    assert seen == [0, 1, 2, 3]
+    rep = report(*[np.concatenate(x) for x in parts])
+    print("candidates seen by the evaluation:", rep)
+    assert_parity(rep, "candidates applied from the masters")
+    plan.close()
