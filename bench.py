@@ -806,9 +806,9 @@ def main():
 # trace and one run per counter set -- and --summarize matches the k-th
 # dispatch of a library kernel in each run's CSV to the k-th label.
 
-LIBRARY_KERNELS = ("es_perturb_kernel", "es_update_kernel", "es_stream_kernel",
-                   "es_calibrate_kernel", "es_qpass_kernel", "es_checksum_kernel",
-                   "es_qchecksum_kernel")
+LIBRARY_KERNELS = ("es_perturb_kernel", "es_update_kernel", "es_apply_master_kernel",
+                   "es_stream_kernel", "es_calibrate_kernel", "es_qpass_kernel",
+                   "es_checksum_kernel", "es_qchecksum_kernel")
 COUNTER_SETS = {
     "fetch": "FETCH_SIZE",
     "write": "WRITE_SIZE",

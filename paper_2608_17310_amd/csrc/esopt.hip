@@ -557,6 +557,128 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTile* __r
         perturb_tail<kThreads, kU, kM, kRows>(load_ref<kRows>(tiles, rows, n_full + tl), st);
 }
 
+// A member applied from binary32 masters (es_perturb_master) with sigma > 0:
+// bf16 values RNE(m + c eps) from the masters at mb + 4 e, the masters only
+// read -- the arithmetic of es_perturb on the masters' values.  The perturb
+// kernel's pipeline at half a tile per step: a half tile's masters (kU / 2
+// groups of 32 bytes per lane) take the registers a whole tile of bf16 takes
+// there, so two half-tile buffers alternate, the next half's loads issued
+// before the current half's arithmetic and each half's bf16 stores leaving
+// in one burst.
+template <int kThreads, int kH>
+__device__ __forceinline__ void master_half_load(const TileRef& r, uintptr_t mb, int h,
+                                                 float m[kH][8]) {
+#pragma unroll
+    for (int u = 0; u < kH; ++u) {
+        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
+        load_master<true, true>(mb, e, r.limit, m[u]);
+    }
+}
+
+template <int kThreads, int kH, bool kRows>
+__device__ __forceinline__ void master_half_apply(const TileRef& r, int h, float m[kH][8],
+                                                  const Streams& st) {
+    const uint32_t q_hi = tile_high_word<kRows>(r);
+    uint32_t out[kH][4];
+#pragma unroll
+    for (int u = 0; u < kH; ++u) {
+        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
+        uint32_t w[8];
+        group_words(static_cast<uint32_t>(noise_index<kRows>(r, e) >> 2), q_hi, r.tensor_id,
+                    st.k0[0], st.k1[0], w);
+        group_axpy(w, st.coef_k[0], m[u]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) out[u][k] = es::pack_bf16x2(m[u][2 * k], m[u][2 * k + 1]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < kH; ++u) {
+        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
+        store_group<true, true>(r.data, e, r.limit, out[u]);
+    }
+}
+
+// A tile's master base: its bf16 base times two plus the tensor's delta.
+__device__ __forceinline__ uintptr_t master_base(const uint64_t* __restrict__ mdelta,
+                                                 const TileRef& r, uint64_t i) {
+    return mdelta[i] + 2 * reinterpret_cast<uintptr_t>(r.data);
+}
+
+// Full tiles: buffer a holds a tile's first half, b its second.  Each turn
+// of the loop finishes the current tile's second half while the next tile's
+// first half loads, then loads that tile's second half under its first
+// half's arithmetic; the last tile's second half is done after the loop.
+// Every path into the loop's head then has the same memory operations
+// outstanding (the second half's loads, then the first half's stores), so
+// its first wait leaves the stores in flight; the next tile's descriptor is
+// read a turn ahead, as in the perturb kernel.  Tail tiles follow, group by
+// group with bounds-checked accesses.
+template <int kThreads, int kU, bool kRows>
+__global__ __launch_bounds__(kThreads) void es_apply_master_kernel(
+    const DevTile* __restrict__ tiles, uint64_t n_full, uint64_t n_tail,
+    const DevRows* __restrict__ rows, Streams st, const uint64_t* __restrict__ mdelta) {
+    static_assert(kU % 2 == 0, "a tile is taken in two halves");
+    constexpr int kH = kU / 2;
+    uint64_t tile = blockIdx.x;
+    if (tile < n_full) {
+        TileRef cur = load_ref<kRows>(tiles, rows, tile);
+        uintptr_t cur_mb = master_base(mdelta, cur, tile);
+        const uint64_t nxt_i = min(tile + gridDim.x, n_full - 1);
+        TileRef nxt = load_ref<kRows>(tiles, rows, nxt_i);
+        uintptr_t nxt_mb = master_base(mdelta, nxt, nxt_i);
+        float a[kH][8], b[kH][8];
+        master_half_load<kThreads, kH>(cur, cur_mb, 0, a);
+        master_half_load<kThreads, kH>(cur, cur_mb, 1, b);
+        __builtin_amdgcn_sched_barrier(0);
+        master_half_apply<kThreads, kH, kRows>(cur, 0, a, st);
+        while (tile + gridDim.x < n_full) {
+            tile += gridDim.x;
+            __builtin_amdgcn_sched_barrier(0);
+            master_half_load<kThreads, kH>(nxt, nxt_mb, 0, a);
+            __builtin_amdgcn_sched_barrier(0);
+            const uint64_t after_i = min(tile + gridDim.x, n_full - 1);
+            DevTile after = tiles[after_i];
+            DevRows after_rows{};
+            if constexpr (kRows) after_rows = rows[after_i];
+            uint64_t after_d = mdelta[after_i];
+            __builtin_amdgcn_sched_barrier(0);
+            master_half_apply<kThreads, kH, kRows>(cur, 1, b, st);
+            keep_in_sgprs(after);
+            if constexpr (kRows) keep_in_sgprs(after_rows);
+            asm volatile("" : "+s"(after_d));
+            cur = nxt;
+            cur_mb = nxt_mb;
+            if constexpr (kRows) nxt = tile_ref(after, after_rows);
+            else nxt = tile_ref(after);
+            nxt_mb = after_d + 2 * reinterpret_cast<uintptr_t>(nxt.data);
+            __builtin_amdgcn_sched_barrier(0);
+            master_half_load<kThreads, kH>(cur, cur_mb, 1, b);
+            __builtin_amdgcn_sched_barrier(0);
+            master_half_apply<kThreads, kH, kRows>(cur, 0, a, st);
+        }
+        master_half_apply<kThreads, kH, kRows>(cur, 1, b, st);
+    }
+    for (uint64_t tl = blockIdx.x; tl < n_tail; tl += gridDim.x) {
+        const TileRef r = load_ref<kRows>(tiles, rows, n_full + tl);
+        const uintptr_t mb = master_base(mdelta, r, n_full + tl);
+        const uint32_t q_hi = tile_high_word<kRows>(r);
+#pragma unroll 1
+        for (int u = 0; u < kU; ++u) {
+            const uint64_t e = r.elem0 + uint64_t(u * kThreads + threadIdx.x) * kGroupElems;
+            if (e >= r.limit) break;
+            float m[8];
+            load_master<false, true>(mb, e, r.limit, m, r.aligned16 != 0u);
+            uint32_t w[8], out[4];
+            group_words(static_cast<uint32_t>(noise_index<kRows>(r, e) >> 2), q_hi, r.tensor_id,
+                        st.k0[0], st.k1[0], w);
+            group_axpy(w, st.coef_k[0], m);
+#pragma unroll
+            for (int k = 0; k < 4; ++k) out[k] = es::pack_bf16x2(m[2 * k], m[2 * k + 1]);
+            store_group<false, true>(r.data, e, r.limit, out, r.aligned16 != 0u);
+        }
+    }
+}
+
 // The in-place streaming ceiling of a plan (es_stream_pass): every element
 // is read and written back as itself (XOR with `flip`, which the host passes
 // as 0, so the compiler keeps the stores), over the same tiles and 16-byte
@@ -1164,6 +1286,18 @@ UpdateKernel master_kernel_for(int threads, int groups, bool rows) {
     if (threads == T && groups == U)                                                    \
         return rows ? es_update_kernel<T, U, true, false, true, false, kMode>           \
                     : es_update_kernel<T, U, true, false, false, false, kMode>;
+    ES_TILE_SHAPES(ES_CASE)
+#undef ES_CASE
+    return nullptr;
+}
+
+using ApplyMasterKernel = void (*)(const DevTile*, uint64_t, uint64_t, const DevRows*, Streams,
+                                   const uint64_t*);
+
+ApplyMasterKernel apply_master_kernel(int threads, int groups, bool rows) {
+#define ES_CASE(T, U)                                                                   \
+    if (threads == T && groups == U)                                                    \
+        return rows ? es_apply_master_kernel<T, U, true> : es_apply_master_kernel<T, U, false>;
     ES_TILE_SHAPES(ES_CASE)
 #undef ES_CASE
     return nullptr;
@@ -2530,16 +2664,36 @@ int es_perturb_master(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma,
     int rc = check_device(plan);
     if (rc != ES_OK) return rc;
     hipStream_t s = static_cast<hipStream_t>(stream);
-    // a one-member table in the plan's scratch, as an update's
     const double coef = sign > 0 ? double(sigma) : -double(sigma);
+    Segment seg[2];
+    const int n_seg = plan_segments(plan, seg);
+    if (sigma != 0.0f) {
+        Streams st = {};
+        st.k0[0] = static_cast<uint32_t>(seed);
+        st.k1[0] = static_cast<uint32_t>(seed >> 32);
+        st.coef_k[0] = static_cast<float>(coef * kSqrt2Ln2Double);
+        for (int k = 0; k < n_seg; ++k) {
+            const Segment& g = seg[k];
+            const bool strided = g.rows != nullptr;
+            hipLaunchKernelGGL(apply_master_kernel(plan->threads, plan->groups, strided),
+                               dim3(g.grid_perturb), dim3(plan->threads), 0, s, g.tiles, g.n_full,
+                               g.n_tail, g.rows, st,
+                               plan->d_master + (strided ? plan->n_full + plan->n_tail : 0));
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess)
+                return hip_fail(e, "es_perturb_master: es_apply_master_kernel launch");
+        }
+        return ES_OK;
+    }
+    // sigma == 0 rewrites the bf16 values as the masters rounded to nearest
+    // even (-0 stays -0: no term is added): the update kernel's application
+    // of members with a one-member table of zero weight in the plan's scratch
     const Member m{static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
                    static_cast<float>(coef * kSqrt2Ln2Double), 0u};
-    const UpdateHeader h{1u, sigma != 0.0f ? 1u : 0u, 0, 0u};
+    const UpdateHeader h{1u, 0u, 0, 0u};
     rc = stage_words(plan->d_scratch, kOffMembers, &m, sizeof(m), s);
     if (rc == ES_OK) rc = stage_words(plan->d_scratch, kOffHeader, &h, sizeof(h), s);
     if (rc != ES_OK) return rc;
-    Segment seg[2];
-    const int n_seg = plan_segments(plan, seg);
     for (int k = 0; k < n_seg; ++k) {
         const Segment& g = seg[k];
         const bool strided = g.rows != nullptr;

@@ -267,6 +267,42 @@ def test_perturb_master_matches_oracle_and_leaves_the_masters():
     plan.close()
 
 
+def test_perturb_master_of_bf16_masters_is_es_perturb_bit_for_bit():
+    """Masters equal to bf16 values: a member applied from them is es_perturb
+    of those bf16 values, bit for bit (one FMA per element on the same
+    binary32 value, then nearest-even) -- over full and tail tiles, views at
+    odd offsets, a strided block and both signs."""
+    plan, views, mdev, ms = _setup(85)
+    bits = [_rne(m) for m in ms]
+    for d, b in zip(mdev, bits):                     # masters := their bf16 values
+        d.copy_(torch.from_numpy((b.astype(np.uint32) << 16).view(np.float32)).cuda())
+    twins = [torch.from_numpy(b.view(np.int16)).cuda().view(torch.bfloat16) for b in bits]
+    ref = esopt.Plan(twins, tensor_ids=plan.tensor_ids)
+    for seed, sign, sigma in [(31, 1, 1e-3), (32, -1, 3e-2), ((1 << 63) + 5, 1, 7e-4)]:
+        plan.perturb_master(seed, sign, sigma)
+        ref.perturb(seed, sign, sigma)
+        torch.cuda.synchronize()
+        for v, t in zip(views, twins):
+            np.testing.assert_array_equal(to_host(v), to_host(t))
+        for t, b in zip(twins, bits):                # the twins back at the masters' values
+            t.view(torch.int16).copy_(torch.from_numpy(b.view(np.int16)).cuda())
+    ref.close()
+    plan.close()
+    rows, cols = 40, 1000
+    b0 = _rne((np.random.default_rng(86).standard_normal((rows, 2 * cols)) * 0.02))
+    blk = torch.zeros(rows, cols, dtype=torch.bfloat16, device="cuda")
+    twin = torch.from_numpy(np.ascontiguousarray(b0[:, 600:600 + cols]).view(np.int16)).cuda()
+    twin = twin.view(torch.bfloat16)
+    m = (np.ascontiguousarray(b0[:, 600:600 + cols]).astype(np.uint32) << 16).view(np.float32)
+    with esopt.Plan(blocks=[esopt.Block(blk, 4, 2 * cols, 0, 600)]) as p, \
+            esopt.Plan(blocks=[esopt.Block(twin, 4, 2 * cols, 0, 600)]) as q:
+        p.set_master([torch.from_numpy(m.reshape(-1).copy()).cuda()])
+        p.perturb_master(77, -1, 2e-3)
+        q.perturb(77, -1, 2e-3)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(to_host(blk), to_host(twin))
+
+
 def test_a_candidate_does_not_depend_on_the_ones_before_it():
     pa, va, _, _ = _setup(81, garbage=2)
     pb, vb, _, _ = _setup(81, garbage=3)

@@ -159,7 +159,8 @@ def test_invalid_arguments_raise():
 def test_results_do_not_depend_on_launch_shape(shape, monkeypatch):
     """Noise is a function of (seed, tensor, element) only, so the tile shape
     and grid (environment overrides read at plan creation) change no bit of
-    perturb, swap, restore or update (both roundings, and into masters)."""
+    perturb, swap, restore, update (both roundings, and into masters) or a
+    member applied from the masters."""
     threads, groups, wg_p, wg_u = shape
     sizes = [300001, 1 << 16, 4097, 9]
     bits = [wl.random_bf16_bits(n, 90 + i) for i, n in enumerate(sizes)]
@@ -184,6 +185,9 @@ def test_results_do_not_depend_on_launch_shape(shape, monkeypatch):
         plan.update([6, 7], [1, -1], r[:2], 5e-4, flags=esopt.ES_UPDATE_MASTER)
         torch.cuda.synchronize()
         out.append([to_host(t) for t in ts] + [m.cpu().numpy() for m in masters])
+        plan.perturb_master(8, -1, 2e-3)                 # a member applied from them
+        torch.cuda.synchronize()
+        out.append([to_host(t) for t in ts])
         plan.close()
         return out
 
