@@ -561,41 +561,70 @@ __global__ __launch_bounds__(kThreads) void es_perturb_kernel(const DevTile* __r
 // bf16 values RNE(m + c eps) from the masters at mb + 4 e, the masters only
 // read -- the arithmetic of es_perturb on the masters' values.  The perturb
 // kernel's pipeline at half a tile per step: a half tile's masters (kU / 2
-// groups of 32 bytes per lane) take the registers a whole tile of bf16 takes
+// slabs of 32 bytes per lane) take the registers a whole tile of bf16 takes
 // there, so two half-tile buffers alternate, the next half's loads issued
 // before the current half's arithmetic and each half's bf16 stores leaving
 // in one burst.
+//
+// Within a slab (kThreads * 8 consecutive elements) lane t takes the quads
+// at elements 4 t and 4 (kThreads + t): each 16-byte master load then covers
+// 1 KB of consecutive masters per wave (one lane's 8 consecutive masters
+// would take two loads of 16 bytes at a 32-byte stride, and streamed lines
+// were fetched twice), and each 8-byte bf16 store 512 consecutive bytes.
+// A quad is one Philox block: its two Box-Muller pairs are its elements.
+template <int kThreads>
+__device__ __forceinline__ uint64_t slab_quad(const TileRef& r, int slab, int q) {
+    return r.elem0 + uint64_t(slab * kThreads) * kGroupElems +
+           4 * (uint64_t(q) * kThreads + threadIdx.x);
+}
+
 template <int kThreads, int kH>
 __device__ __forceinline__ void master_half_load(const TileRef& r, uintptr_t mb, int h,
                                                  float m[kH][8]) {
 #pragma unroll
-    for (int u = 0; u < kH; ++u) {
-        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
-        load_master<true, true>(mb, e, r.limit, m[u]);
-    }
+    for (int u = 0; u < kH; ++u)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const uint64_t e = slab_quad<kThreads>(r, h * kH + u, q);
+            const f32x4_t v = __builtin_nontemporal_load((const ES_GLOBAL f32x4_t*)(mb + 4 * e));
+            m[u][4 * q] = v.x; m[u][4 * q + 1] = v.y; m[u][4 * q + 2] = v.z; m[u][4 * q + 3] = v.w;
+        }
 }
 
 template <int kThreads, int kH, bool kRows>
 __device__ __forceinline__ void master_half_apply(const TileRef& r, int h, float m[kH][8],
                                                   const Streams& st) {
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
     const uint32_t q_hi = tile_high_word<kRows>(r);
     uint32_t out[kH][4];
 #pragma unroll
-    for (int u = 0; u < kH; ++u) {
-        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
-        uint32_t w[8];
-        group_words(static_cast<uint32_t>(noise_index<kRows>(r, e) >> 2), q_hi, r.tensor_id,
-                    st.k0[0], st.k1[0], w);
-        group_axpy(w, st.coef_k[0], m[u]);
+    for (int u = 0; u < kH; ++u)
 #pragma unroll
-        for (int k = 0; k < 4; ++k) out[u][k] = es::pack_bf16x2(m[u][2 * k], m[u][2 * k + 1]);
-    }
+        for (int q = 0; q < 2; ++q) {
+            const uint64_t e = slab_quad<kThreads>(r, h * kH + u, q);
+            const es::Words w = es::philox4x32_10(
+                static_cast<uint32_t>(noise_index<kRows>(r, e) >> 2), q_hi, r.tensor_id,
+                es::kDomainNoise, st.k0[0], st.k1[0]);
+            float* x = &m[u][4 * q];
+            float t, c, sn;
+            es::scaled_pair(w.w0, w.w1, st.coef_k[0], t, c, sn);
+            x[0] = __builtin_fmaf(t, c, x[0]);
+            x[1] = __builtin_fmaf(t, sn, x[1]);
+            es::scaled_pair(w.w2, w.w3, st.coef_k[0], t, c, sn);
+            x[2] = __builtin_fmaf(t, c, x[2]);
+            x[3] = __builtin_fmaf(t, sn, x[3]);
+            out[u][2 * q] = es::pack_bf16x2(x[0], x[1]);
+            out[u][2 * q + 1] = es::pack_bf16x2(x[2], x[3]);
+        }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int u = 0; u < kH; ++u) {
-        const uint64_t e = r.elem0 + uint64_t((h * kH + u) * kThreads + threadIdx.x) * kGroupElems;
-        store_group<true, true>(r.data, e, r.limit, out[u]);
-    }
+    for (int u = 0; u < kH; ++u)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+            const uint64_t e = slab_quad<kThreads>(r, h * kH + u, q);
+            const u32x2_t v = {out[u][2 * q], out[u][2 * q + 1]};
+            __builtin_nontemporal_store(v, (ES_GLOBAL u32x2_t*)(r.data + e));
+        }
 }
 
 // A tile's master base: its bf16 base times two plus the tensor's delta.
