@@ -308,7 +308,8 @@ int es_plan_set_master(es_plan_t* plan, void* const* masters, uint32_t n);
  * For bf16-representable masters the result is es_perturb's of those
  * values, bit for bit.  sigma 0 writes RNE_bf16(m_j) (the bf16 copy
  * refreshed from the masters; -0 stays -0) and uses the plan's scratch, as
- * es_update; sigma > 0 needs no scratch.  Errors: INVALID_ARG (null plan, a
+ * es_update; sigma > 0 uses no scratch (one kernel launch per part of the
+ * plan, which a HIP graph can capture).  Errors: INVALID_ARG (null plan, a
  * plan without masters, sign, sigma), DEVICE, HIP. */
 int es_perturb_master(es_plan_t* plan, uint64_t seed, int32_t sign, float sigma,
                       es_stream_t stream);

@@ -271,9 +271,15 @@ def test_perturb_master_of_bf16_masters_is_es_perturb_bit_for_bit():
     """Masters equal to bf16 values: a member applied from them is es_perturb
     of those bf16 values, bit for bit (one FMA per element on the same
     binary32 value, then nearest-even) -- over full and tail tiles, views at
-    odd offsets, a strided block and both signs."""
+    odd offsets, a strided block and both signs; zeros of both signs,
+    infinities, NaNs with payloads, subnormals and the largest finite values
+    among them, in the head, a full tile and the tail."""
     plan, views, mdev, ms = _setup(85)
     bits = [_rne(m) for m in ms]
+    special = [0x0000, 0x8000, 0x7F80, 0xFF80, 0x0001, 0x807F, 0x7FC1, 0xFF81, 0x7F81, 0x7F7F,
+               0xFF7F, 0x0080]
+    for at in (0, 100_000, bits[3].size - len(special)):
+        bits[3][at:at + len(special)] = special
     for d, b in zip(mdev, bits):                     # masters := their bf16 values
         d.copy_(torch.from_numpy((b.astype(np.uint32) << 16).view(np.float32)).cuda())
     twins = [torch.from_numpy(b.view(np.int16)).cuda().view(torch.bfloat16) for b in bits]
@@ -312,6 +318,31 @@ def test_a_candidate_does_not_depend_on_the_ones_before_it():
     torch.cuda.synchronize()
     for x, y in zip(va, vb):
         np.testing.assert_array_equal(to_host(x), to_host(y))
+    pa.close()
+    pb.close()
+
+
+def test_perturb_master_replays_from_a_hip_graph():
+    """With sigma > 0 a member applied from the masters uses no scratch, so a
+    captured walk of members replays: each replay, after eager passes that
+    leave other values behind, gives the eager result of its last member."""
+    pa, va, _, _ = _setup(87, garbage=4)
+    pb, vb, _, _ = _setup(87, garbage=5)
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        pa.perturb_master(41, 1, 1e-3)
+        pa.perturb_master(42, -1, 2e-3)
+    torch.cuda.synchronize()
+    pb.perturb_master(42, -1, 2e-3)
+    for k in range(3):
+        pa.perturb_master(100 + k, 1, 5e-3)          # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for x, y in zip(va, vb):
+            np.testing.assert_array_equal(to_host(x), to_host(y))
     pa.close()
     pb.close()
 
