@@ -4,13 +4,17 @@
  * swap each member for the next, then revert the last member inside the
  * update (Section 3; Appendix D.6 order), and checksum the result.
  *
- *   c_generation IN PERTURBED FINAL N0 N1
+ *   c_generation IN PERTURBED FINAL N0 N1 [MASTERS]
  *
  * IN holds N0 + N1 bf16 bit patterns (tensor 0, then tensor 1, little
  * endian); PERTURBED receives both tensors after the first member is
- * applied, FINAL after the update.  Prints the radius, the z-scores, the
- * status word and the plan checksum on stdout.  Exits non-zero, naming the
- * failing call, on any error. */
+ * applied, FINAL after the update.  With MASTERS the generation runs over
+ * binary32 masters instead, initialised to IN's values: each member is
+ * applied from them (es_perturb_master, no revert), the update goes into
+ * them (ES_UPDATE_MASTER), and MASTERS receives their N0 + N1 binary32 bit
+ * patterns.  Prints the radius, the z-scores, the status word and the plan
+ * checksum on stdout.  Exits non-zero, naming the failing call, on any
+ * error. */
 #include <hip/hip_runtime_api.h>
 #include <inttypes.h>
 #include <stdio.h>
@@ -52,10 +56,11 @@ static int save(const char* path, const uint16_t* d0, uint64_t n0, const uint16_
 }
 
 int main(int argc, char** argv) {
-    if (argc != 6) {
-        fprintf(stderr, "usage: %s IN PERTURBED FINAL N0 N1\n", argv[0]);
+    if (argc != 6 && argc != 7) {
+        fprintf(stderr, "usage: %s IN PERTURBED FINAL N0 N1 [MASTERS]\n", argv[0]);
         return 2;
     }
+    const int with_masters = argc == 7;
     const uint64_t n0 = strtoull(argv[4], NULL, 10), n1 = strtoull(argv[5], NULL, 10);
     const uint64_t n = n0 + n1;
     uint16_t* host = malloc(2 * n);
@@ -87,14 +92,42 @@ int main(int argc, char** argv) {
     hipStream_t s = NULL;
     if (check_hip(hipStreamCreate(&s), "hipStreamCreate")) return 1;
 
-    if (check_es(es_perturb(plan, seeds[0], signs[0], sigma, s), "es_perturb") ||
-        check_hip(hipStreamSynchronize(s), "hipStreamSynchronize") ||
+    /* binary32 masters of both tensors, one allocation each, set to IN's
+     * values (a bf16 pattern shifted up 16 bits is that value in binary32) */
+    float* m0 = NULL;
+    float* m1 = NULL;
+    uint32_t* mhost = NULL;
+    if (with_masters) {
+        mhost = malloc(4 * n);
+        if (mhost == NULL) return 1;
+        for (uint64_t j = 0; j < n; ++j) mhost[j] = (uint32_t)host[j] << 16;
+        void* masters[2];
+        if (check_hip(hipMalloc((void**)&m0, 4 * n0), "hipMalloc") ||
+            check_hip(hipMalloc((void**)&m1, 4 * n1), "hipMalloc") ||
+            check_hip(hipMemcpy(m0, mhost, 4 * n0, hipMemcpyHostToDevice), "hipMemcpy") ||
+            check_hip(hipMemcpy(m1, mhost + n0, 4 * n1, hipMemcpyHostToDevice), "hipMemcpy"))
+            return 1;
+        masters[0] = m0;
+        masters[1] = m1;
+        if (check_es(es_plan_set_master(plan, masters, 2), "es_plan_set_master")) return 1;
+    }
+
+    if (with_masters) {
+        if (check_es(es_perturb_master(plan, seeds[0], signs[0], sigma, s), "es_perturb_master"))
+            return 1;
+    } else if (check_es(es_perturb(plan, seeds[0], signs[0], sigma, s), "es_perturb")) {
+        return 1;
+    }
+    if (check_hip(hipStreamSynchronize(s), "hipStreamSynchronize") ||
         save(argv[2], d0, n0, d1, n1, host))
         return 1;
-    for (int i = 1; i < G; ++i)
-        if (check_es(es_swap(plan, seeds[i - 1], signs[i - 1], sigma, seeds[i], signs[i], sigma, s),
-                     "es_swap"))
-            return 1;
+    for (int i = 1; i < G; ++i) {
+        const int rc = with_masters
+                           ? es_perturb_master(plan, seeds[i], signs[i], sigma, s)
+                           : es_swap(plan, seeds[i - 1], signs[i - 1], sigma, seeds[i], signs[i],
+                                     sigma, s);
+        if (check_es(rc, with_masters ? "es_perturb_master" : "es_swap")) return 1;
+    }
 
     float* d_rewards = NULL;
     float* d_z = NULL;
@@ -107,10 +140,13 @@ int main(int argc, char** argv) {
         check_hip(hipMemcpy(d_rewards, rewards, sizeof rewards, hipMemcpyHostToDevice),
                   "hipMemcpy"))
         return 1;
-    es_update_opts_t opts = {5e-4f, sigma, 1e-8f, 0u, 0u};
-    if (check_es(es_restore_update(plan, seeds[G - 1], signs[G - 1], sigma, seeds, signs,
-                                   d_rewards, G, &opts, d_z, d_status, s),
-                 "es_restore_update") ||
+    es_update_opts_t opts = {5e-4f, sigma, 1e-8f, with_masters ? ES_UPDATE_MASTER : 0u, 0u};
+    /* with masters the update rewrites every bf16 value: no revert first */
+    const int rc = with_masters
+                       ? es_update(plan, seeds, signs, d_rewards, G, &opts, d_z, d_status, s)
+                       : es_restore_update(plan, seeds[G - 1], signs[G - 1], sigma, seeds, signs,
+                                           d_rewards, G, &opts, d_z, d_status, s);
+    if (check_es(rc, with_masters ? "es_update" : "es_restore_update") ||
         check_es(es_plan_checksum(plan, d_sum, s), "es_plan_checksum") ||
         check_hip(hipStreamSynchronize(s), "hipStreamSynchronize") ||
         save(argv[3], d0, n0, d1, n1, host))
@@ -129,7 +165,22 @@ int main(int argc, char** argv) {
     printf("status %d\n", (int)status);
     printf("checksum %" PRIu64 "\n", sum);
 
+    if (with_masters) {
+        FILE* mf = NULL;
+        if (check_hip(hipMemcpy(mhost, m0, 4 * n0, hipMemcpyDeviceToHost), "hipMemcpy") ||
+            check_hip(hipMemcpy(mhost + n0, m1, 4 * n1, hipMemcpyDeviceToHost), "hipMemcpy"))
+            return 1;
+        mf = fopen(argv[6], "wb");
+        if (mf == NULL || fwrite(mhost, 4, n, mf) != n || fclose(mf) != 0) {
+            fprintf(stderr, "cannot write %s\n", argv[6]);
+            return 1;
+        }
+    }
+
     if (check_es(es_plan_destroy(plan), "es_plan_destroy")) return 1;
+    hipFree(m0);
+    hipFree(m1);
+    free(mhost);
     hipFree(d_rewards);
     hipFree(d_z);
     hipFree(d_status);
