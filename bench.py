@@ -739,10 +739,13 @@ def main():
         "es_stream_pass": {"ms": round(t_stream * 1e3, 3), "GBps": round(ceiling_gbs, 1)},
     }
     if args.master:
+        c_pm = _counters_for(args.counters_json, "es_perturb_master", W.name)
         per_kernel["es_perturb_master"] = {
             "ms": round(t_pmaster * 1e3, 3), "params_per_s": P / t_pmaster,
             "GBps_algorithmic": round(6 * P / t_pmaster / 1e9, 1),
-            "frac_hbm_peak": round(6 * P / t_pmaster / 1e9 / HBM_PEAK_GBS, 4)}
+            "frac_hbm_peak": round(6 * P / t_pmaster / 1e9 / HBM_PEAK_GBS, 4),
+            "algorithmic_bytes_per_launch": 6 * P,
+            "traffic": c_pm["bytes_per_launch"] if c_pm else None}
     out = {
         "metric": "params/s and achieved HBM GB/s for es_perturb and fused es_update (N members)",
         "value": value,
