@@ -309,6 +309,46 @@ def test_perturb_master_of_bf16_masters_is_es_perturb_bit_for_bit():
         np.testing.assert_array_equal(to_host(blk), to_host(twin))
 
 
+def _bf16_twins(x0, make_plan, shape):
+    """A plan over bf16 values x0 with binary32 masters equal to them, and a
+    plan over a copy of x0: es_perturb_master on the first and es_perturb on
+    the second must agree bit for bit."""
+    a = torch.from_numpy(x0.view(np.int16).reshape(shape)).cuda().view(torch.bfloat16)
+    b = a.clone()
+    m = torch.from_numpy((x0.astype(np.uint32) << 16).view(np.float32).copy()).cuda()
+    pa, pb = make_plan(a), make_plan(b)
+    pa.set_master([m])
+    return pa, pb, a, b
+
+
+@pytest.mark.parametrize("kind", ["shard", "block"])
+def test_perturb_master_across_element_2_34_is_es_perturb_bit_for_bit(kind):
+    """Whole-tensor indices from below to above 2^34, where the counter's high
+    word changes (mid-tile for the block's rows): with bf16-representable
+    masters every value is es_perturb's, full tiles, tails and row maps."""
+    tid = 3
+    if kind == "shard":
+        a0, n = (1 << 34) - 200_000, 500_017
+        x0 = wl.random_bf16_bits(n, 88)
+        pa, pb, va, vb = _bf16_twins(
+            x0, lambda t: esopt.Plan([t], tensor_ids=[tid], offsets=[a0]), (n,))
+    else:
+        row_len, rows, cols = (1 << 20) + 4096, 256, 1024     # 512 KB: full tiles too
+        row0 = (1 << 34) // row_len - rows // 2
+        col0 = (1 << 34) - ((1 << 34) // row_len) * row_len - 512
+        x0 = wl.random_bf16_bits(rows * cols, 89)
+        pa, pb, va, vb = _bf16_twins(
+            x0, lambda t: esopt.Plan(blocks=[esopt.Block(t, tid, row_len, row0, col0)]),
+            (rows, cols))
+    pa.perturb_master(61, -1, 1.5e-3)
+    pb.perturb(61, -1, 1.5e-3)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_host(va), to_host(vb))
+    assert np.mean(to_host(va) != x0) > 0.9
+    pa.close()
+    pb.close()
+
+
 def test_a_candidate_does_not_depend_on_the_ones_before_it():
     pa, va, _, _ = _setup(81, garbage=2)
     pb, vb, _, _ = _setup(81, garbage=3)
