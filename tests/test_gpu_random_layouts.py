@@ -2,7 +2,9 @@
 (empty to a few hundred thousand elements) at random 2-byte offsets inside
 shared buffers, random tensor ids, random tile shapes (environment
 overrides); every element of every tensor is checked after perturb, swap,
-restore and both update roundings.  Seeded, so every case is reproducible."""
+restore and both update roundings, and, over binary32 masters, after
+members applied from them and the update into them.  Seeded, so every case
+is reproducible."""
 import numpy as np
 import pytest
 import torch
@@ -108,6 +110,108 @@ def test_random_layout(case, monkeypatch):
         rep = report(got, exp, base, delta)
         print("case", case, k, rep)
         assert_parity(rep, f"case {case} {k}")
+
+
+@pytest.mark.parametrize("case", range(4))
+def test_random_master_layout(case, monkeypatch):
+    """Binary32 masters (16-byte aligned, at random gaps in one float32
+    buffer) of a random bf16 layout: a member applied from them, the update
+    into them and a member applied from the updated masters, every element
+    against the oracle (the bf16 values at the parity bar, the masters within
+    the bound of the kernel's arithmetic, the bf16 copy after the update the
+    rounding of the GPU's masters), and no byte outside the tensors or the
+    masters written."""
+    from parity import assert_master_parity, master_report, master_tolerance
+    rng = np.random.default_rng(3000 + case)
+    threads, groups = SHAPES[rng.integers(len(SHAPES))]
+    monkeypatch.setenv("ESOPT_THREADS", str(threads))
+    monkeypatch.setenv("ESOPT_GROUPS", str(groups))
+    monkeypatch.setenv("ESOPT_PERTURB_WG_PER_CU", str(int(rng.integers(1, 4))))
+    monkeypatch.setenv("ESOPT_UPDATE_WG_PER_CU", str(int(rng.integers(1, 9))))
+    n_t = int(rng.integers(1, 17))
+    sizes = [int(x) for x in np.where(rng.random(n_t) < 0.15, rng.integers(0, 20, n_t),
+                                      rng.integers(1, 300_000, n_t))]
+    offsets = [int(x) for x in rng.integers(0, 9, n_t)]
+    ids = [int(x) for x in rng.choice(1 << 20, n_t, replace=False)]
+    print("case", case, "shape", threads, groups, "tensors", list(zip(sizes, offsets)))
+    starts, cur = [], 0
+    for n, off in zip(sizes, offsets):
+        cur = (cur + 7) // 8 * 8 + off
+        starts.append(cur)
+        cur += n
+    buf = torch.zeros(cur + 8, dtype=torch.bfloat16, device="cuda")
+    views = [buf[s:s + n] for s, n in zip(starts, sizes)]
+    mstarts, mcur = [], 0
+    for n in sizes:                                   # 16-byte aligned, random gaps
+        mcur = (mcur + 3) // 4 * 4 + 4 * int(rng.integers(0, 3))
+        mstarts.append(mcur)
+        mcur += n
+    m0 = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in sizes]
+    mflat = np.full(mcur + 4, 7.0, np.float32)        # sentinel outside the masters
+    for s, m in zip(mstarts, m0):
+        mflat[s:s + m.size] = m
+    mbuf = torch.from_numpy(mflat).cuda()
+    mviews = [mbuf[s:s + n] for s, n in zip(mstarts, sizes)]
+    plan = esopt.Plan(views, tensor_ids=ids)
+    plan.set_master(mviews)
+    seeds = [int(x) for x in rng.integers(0, 1 << 62, 4)]
+    signs = [1, -1, 1, 1]
+    r = rng.random(4).astype(np.float32)
+    sigma, alpha = 1e-3, 5e-4
+
+    def snap():
+        torch.cuda.synchronize()
+        return [to_host(v) for v in views], [m.cpu().numpy() for m in mviews]
+    plan.perturb_master(seeds[0], 1, sigma)
+    x1, _ = snap()
+    plan.update(seeds, signs, torch.from_numpy(r).cuda(), alpha, flags=esopt.ES_UPDATE_MASTER)
+    x2, m2 = snap()
+    plan.perturb_master(seeds[1], -1, 2 * sigma)
+    x3, m3 = snap()
+    plan.close()
+    full = mbuf.cpu().numpy()
+    mask = np.ones(full.size, bool)
+    for s, n in zip(mstarts, sizes):
+        mask[s:s + n] = False
+    assert np.all(full[mask] == 7.0)
+    fb = to_host(buf)
+    bmask = np.ones(fb.size, bool)
+    for s, n in zip(starts, sizes):
+        bmask[s:s + n] = False
+    assert np.all(fb[bmask] == 0)
+
+    z, _ = oracle.zscore(r)
+    c = oracle.update_coefficient(alpha, sigma, len(seeds), 0)
+    d, w = oracle.member_weights(seeds, signs, z, c)
+    live = [(sd, wd) for sd, wd in zip(d, w) if wd != 0.0]
+
+    def rne(m):
+        return oracle.f64_to_bf16_rne(np.asarray(m, np.float32).astype(np.float64))
+    pooled = {k: ([], [], [], []) for k in ("apply", "apply after update")}
+    mrep = ([], [], [])
+    for i, (tid, n) in enumerate(zip(ids, sizes)):
+        if n == 0:
+            continue
+        el = np.arange(n, dtype=np.uint64)
+        for k, got, mm, sd, sg, sg_sigma in (("apply", x1[i], m0[i], seeds[0], 1, sigma),
+                                             ("apply after update", x3[i], m2[i], seeds[1], -1,
+                                              2 * sigma)):
+            for acc, part in zip(pooled[k], (got, oracle.perturb_master(mm, sd, tid, sg, sg_sigma),
+                                             rne(mm), perturb_delta(sd, tid, sg, sg_sigma, el))):
+                acc.append(part)
+        exp, _, st = oracle.update_master(m0[i], tid, seeds, signs, r, alpha, sigma)
+        assert st == 0
+        for acc, part in zip(mrep, (m2[i], exp, master_tolerance(exp, live, tid, el))):
+            acc.append(part)
+        np.testing.assert_array_equal(x2[i], rne(m2[i]))          # the copy: the masters' rounding
+        np.testing.assert_array_equal(m3[i], m2[i])               # applying leaves the masters
+    for k, parts in pooled.items():
+        rep = report(*(np.concatenate(a) for a in parts))
+        print("case", case, k, rep)
+        assert_parity(rep, f"case {case} {k}")
+    rep = master_report(*(np.concatenate(a) for a in mrep))
+    print("case", case, "masters", rep)
+    assert_master_parity(rep, f"case {case} masters")
 
 
 @pytest.mark.parametrize("case", range(4))
