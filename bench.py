@@ -568,7 +568,7 @@ def main():
         summarize(args.summarize)
         return
     if args.summarize_trace:
-        summarize_bench_trace(args.summarize_trace, workload=args.workload)
+        summarize_bench_trace(args.summarize_trace, workload=args.workload, master=args.master)
         return
     if args.gpus != 1:
         print(json.dumps({"error": "the ES parameter path runs on one GPU; --gpus above 1 is "
@@ -1255,23 +1255,27 @@ BENCH_TRACE_COMMAND = ("rocprofv3 --kernel-trace --stats -f csv -d <out> -o benc
 
 
 def summarize_bench_trace(trace_dir, profiles_dir=os.path.join(REPO, "profiles"),
-                          workload="dense-27b"):
+                          workload="dense-27b", master=False):
     """profiles/bench_kernel_stats_<workload>.md: the --stats table of a
     kernel trace of the default bench command (every kernel the timed step,
-    the swap walk and the ceiling passes launch)."""
+    the swap walk and the ceiling passes launch); with master, of the
+    command with --master (..._<workload>-master.md)."""
     stats = _read_csv(trace_dir, "kernel_stats.csv")
-    lines = [f"# Kernel statistics of the benchmark command on {workload}", "",
+    cmd = BENCH_TRACE_COMMAND + (" --master" if master else "")
+    what = "the benchmark command" + (" with binary32 masters" if master else "")
+    lines = [f"# Kernel statistics of {what} on {workload}", "",
              "Command (from the repository root on an MI355X machine, after "
              "`cd /tmp && export TMPDIR=/tmp`; `<out>` is an output directory; then "
-             "`python3 bench.py --summarize-trace <out>`):", "",
-             f"* `{BENCH_TRACE_COMMAND}`", "", f"Kernel-sources hash: `{_kernel_source_hash()}`",
+             f"`python3 bench.py --summarize-trace <out>{' --master' if master else ''}`):", "",
+             f"* `{cmd}`", "", f"Kernel-sources hash: `{_kernel_source_hash()}`",
              "", "| kernel | calls | average ns | min ns | max ns | share of GPU time |",
              "|---|---|---|---|---|---|"]
     for r in stats:
         name = _short_name(r["Name"])
         lines.append(f"| `{name}` | {r['Calls']} | {float(r['AverageNs']):.0f} | {r['MinNs']} | "
                      f"{r['MaxNs']} | {float(r['Percentage']):.2f} % |")
-    path = os.path.join(profiles_dir, f"bench_kernel_stats_{workload}.md")
+    path = os.path.join(profiles_dir,
+                        f"bench_kernel_stats_{workload}{'-master' if master else ''}.md")
     with open(path, "w") as fh:
         fh.write("\n".join(lines) + "\n")
     print(path)
